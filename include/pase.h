@@ -1,0 +1,215 @@
+/*
+ * pase.h - C ABI of the MI355X (gfx950) implementation of PaSE's strategy
+ * search (V. Elango, "PaSE: Parallelization Strategies for Efficient DNN
+ * Training", IPDPS 2021).
+ *
+ * The library finds a parallelization strategy phi (one configuration per
+ * vertex of a computation graph) minimising the cost function F of eq. (1),
+ * using the vertex ordering GenerateSeq (Fig. 3) and the dynamic program
+ * FindBestStrategy (Fig. 4, recurrence (4)).  The DP tables are filled on the
+ * GPU by hand-written HIP kernels; the ordering and the per-vertex plans are
+ * computed on the host.
+ *
+ * Conventions for every function below:
+ *  - Return value: PASE_OK (0) or one of the pase_status error codes.  On an
+ *    error, caller-owned outputs are left untouched, the handle stays valid
+ *    and pase_last_error() describes the problem.
+ *  - Pointers named host_* or documented as "host" are host memory; every
+ *    array argument is owned by the caller and only read (inputs) or written
+ *    (outputs) during the call.  Inputs are copied at pase_graph_create().
+ *  - Device memory: the library owns what it allocates (hipMalloc, kept on the
+ *    handle and reused across calls) unless the caller lends a device buffer
+ *    with pase_set_workspace().
+ *  - A handle may be used by one thread at a time.
+ *  - Vertex ids are positions in the vertex array passed at creation; edge ids
+ *    likewise.  Vertex ids break ties in the vertex ordering (see
+ *    pase_enumerate_configs), so they are part of the problem statement.
+ */
+#ifndef PASE_H
+#define PASE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PASE_MAX_DIMS 8   /* loop dims per vertex (iteration-space rank) */
+#define PASE_MAX_DEP 8    /* largest dependent set |D(i)| the kernels accept */
+
+typedef enum {
+    PASE_OK = 0,
+    PASE_ERR_INVALID_ARGUMENT = 1, /* null pointer, ndims not in [1,8], size 0, bad id,
+                                      self-loop, tensor-dim map out of range, elems 0,
+                                      p not a power of two, array of the wrong length */
+    PASE_ERR_NOT_CONNECTED = 2,    /* the graph is not weakly connected (Sec. II) */
+    PASE_ERR_BAD_STATE = 3,        /* call order violated (e.g. search before enumeration,
+                                      table query without PASE_OPT_KEEP_TABLES) */
+    PASE_ERR_OVERFLOW = 4,         /* a cost, or the worst-case total cost shifted by the
+                                      argmin bits, does not fit in 64 bits */
+    PASE_ERR_TOO_LARGE = 5,        /* a DP table, |D(i)|, the number of table lookups or
+                                      the device memory need exceeds a limit; detected on the
+                                      host before any device work */
+    PASE_ERR_OUT_OF_MEMORY = 6,    /* a device allocation failed, or a lent workspace is
+                                      too small */
+    PASE_ERR_HIP = 7,              /* a HIP runtime call failed */
+    PASE_ERR_INTERNAL = 8          /* a device-side consistency check failed */
+} pase_status;
+
+/* One vertex = one layer and its iteration space (Sec. II).  size[k] is the
+ * extent of loop dim k.  reduce_mask bit k marks loop dim k as contracted
+ * (splitting it requires a partial-sum reduction).  flops_per_point is the
+ * work of one iteration point (2 for a GEMM, 2*kh*kw for a convolution). */
+typedef struct {
+    uint32_t ndims;
+    uint64_t size[PASE_MAX_DIMS];
+    uint32_t reduce_mask;
+    uint64_t flops_per_point;
+} pase_vertex_desc;
+
+/* One edge = a tensor flowing from src to dst (Sec. II).  Tensor dim k is
+ * indexed by loop dim src_dim[k] of src and dst_dim[k] of dst (-1: that
+ * endpoint does not split tensor dim k).  elems = tensor element count.
+ * Parallel edges are allowed; self-loops are not. */
+typedef struct {
+    uint32_t src, dst, rank;
+    int32_t src_dim[PASE_MAX_DIMS];
+    int32_t dst_dim[PASE_MAX_DIMS];
+    uint64_t elems;
+} pase_edge_desc;
+
+/* comm_weight: r, the FLOP-to-byte ratio of eq. (1) (0 selects the default 8).
+ * seq_rule: 0 = GenerateSeq where a vertex's d-set never contains itself
+ * (default); 1 = the update of Fig. 3 as printed, where an unsequenced vertex
+ * may count itself in |v.d|.  Both yield the same minimum cost (Theorem 1) but
+ * may order the vertices differently. */
+typedef struct {
+    uint64_t comm_weight;
+    uint32_t seq_rule;
+} pase_cost_params;
+
+typedef struct pase_graph_s *pase_graph_t;
+
+typedef enum {
+    PASE_OPT_KEEP_TABLES = 1,   /* 1: keep every DP cost table until the next search so that
+                                   pase_table_entry / pase_table_fingerprint can read it */
+    PASE_OPT_MEMORY_BUDGET = 2, /* bytes of device memory a search may use (default 64 GiB) */
+    PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
+    PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
+    PASE_OPT_PROFILE = 5        /* 1: time every fill launch with HIP events (pase_stats) */
+} pase_option;
+
+/* Search statistics of the last pase_find_best_strategy call. */
+typedef struct {
+    uint64_t cells;            /* DP cell updates: sum over vertices of K_i * |table i| */
+    uint64_t table_entries;    /* sum of |table i| */
+    uint64_t workspace_bytes;  /* device bytes the search used */
+    uint32_t max_dep;          /* max |D(i)| */
+    uint32_t key_type;         /* 0 = fp64 exact-integer keys, 1 = uint64 keys */
+    uint32_t launches;         /* kernels launched by the search */
+    uint32_t rows_vertices;    /* vertices filled by the row/column-chunk kernel */
+    uint64_t rows_cells;       /* cells filled by that kernel */
+    double host_plan_ms;       /* pase_enumerate_configs: ordering + plans (host) */
+    double wall_ms;            /* pase_find_best_strategy, host wall clock */
+    double fill_ms;            /* PASE_OPT_PROFILE: sum of fill-kernel event times */
+    double rows_fill_ms;       /* PASE_OPT_PROFILE: same, row/column-chunk kernel only */
+    uint32_t rows_launches;    /* PASE_OPT_PROFILE: launches of that kernel */
+} pase_run_stats;
+
+/* Copy a computation graph G=(V,E) (Sec. II) into a new handle.
+ * v: host array of nv vertices; e: host array of ne edges; params: NULL for
+ * defaults.  Errors: INVALID_ARGUMENT, NOT_CONNECTED. */
+pase_status pase_graph_create(const pase_vertex_desc *v, uint32_t nv, const pase_edge_desc *e,
+                              uint32_t ne, const pase_cost_params *params, pase_graph_t *out);
+
+/* Release the handle and every device buffer it owns.  NULL is ignored. */
+void pase_graph_destroy(pase_graph_t g);
+
+/* Text of the last error on this handle ("" if none).  Valid until the next call. */
+const char *pase_last_error(pase_graph_t g);
+
+/* Enumerate the configuration set C(v) of every vertex for p modeled devices
+ * (Sec. II: tuples of split factors with product <= p; here the power-of-two
+ * split factors, so p must be 2^L with L <= 16), ordered lexicographically by
+ * the exponent tuple with loop dim 0 slowest.  Then order the vertices with
+ * GenerateSeq (Fig. 3; ties of |u.d| go to the lowest vertex id), derive the
+ * dependent sets D(i), connected sets X(i) and connected subsets S(i)
+ * (Sec. III-B) and the device memory plan.  Host only; resets any earlier
+ * search state and cost override.
+ * Errors: INVALID_ARGUMENT (p), OVERFLOW (a layer cost exceeds 64 bits),
+ * TOO_LARGE (|D(i)| > PASE_MAX_DEP, a table over 2^31 entries, K_v > 65535). */
+pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p);
+
+/* K_v = |C(v)|.  Needs pase_enumerate_configs. */
+pase_status pase_num_configs(pase_graph_t g, uint32_t v, uint32_t *k);
+
+/* Split factors of configuration idx of vertex v into host array splits[ndims]. */
+pase_status pase_config_splits(pase_graph_t g, uint32_t v, uint32_t idx, uint32_t *splits);
+
+/* The GenerateSeq order: order[i] = vertex id at position i (host array of nv). */
+pase_status pase_get_sequence(pase_graph_t g, uint32_t *order);
+
+/* D(v) of vertex id v (Sec. III-B), ascending vertex ids, into host out[cap];
+ * *n receives |D(v)| (TOO_LARGE if cap < |D(v)|). */
+pase_status pase_get_dependent_set(pase_graph_t g, uint32_t v, uint32_t *out, uint32_t cap,
+                                   uint32_t *n);
+
+/* Set one pase_option. */
+pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t value);
+
+/* Replace the cost model by caller-given costs (testing hook; needs
+ * pase_enumerate_configs).  layer: host array, the K_v layer costs of every
+ * vertex concatenated in vertex order.  edge: host array, for every edge the
+ * row-major K_src x K_dst matrix of r*t_x, concatenated in edge order (may be
+ * NULL when ne = 0).  Cleared by the next pase_enumerate_configs. */
+pase_status pase_override_costs(pase_graph_t g, const uint64_t *layer, const uint64_t *edge);
+
+/* Device bytes pase_find_best_strategy needs (after pase_enumerate_configs). */
+pase_status pase_workspace_size(pase_graph_t g, uint64_t *bytes);
+
+/* Lend a device buffer of `bytes` bytes (256-byte aligned) for the next
+ * searches instead of library allocations; NULL returns to library-owned
+ * memory.  The caller keeps ownership and must keep it alive while the handle
+ * uses it. */
+pase_status pase_set_workspace(pase_graph_t g, void *device_ptr, uint64_t bytes);
+
+/* Run FindBestStrategy (Fig. 4) on the GPU: cost tables, per-vertex DP table
+ * fill in sequence order, and back-substitution from the last vertex.
+ * stream: a hipStream_t (NULL = the null stream) on the current device; all
+ * device work is enqueued on it and the call returns after it is finished.
+ * min_cost: host, receives R(|V|, {}) = min over phi of F(G, phi) (Theorem 1).
+ * config_idx: host array of nv, receives the chosen configuration index per
+ * vertex id.  Among equal-cost configurations a table entry keeps the lowest
+ * index (the strict "<" of Fig. 4 with ascending indices).
+ * Errors: BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMORY, HIP, INTERNAL. */
+pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_cost,
+                                    uint32_t *config_idx);
+
+/* Read entry T_v[dep_cfg] of the DP table of vertex v and its argmin after a
+ * search with PASE_OPT_KEEP_TABLES=1.  dep_cfg: host array of |D(v)|
+ * configuration indices, one per member of D(v) in ascending vertex id. */
+pase_status pase_table_entry(pase_graph_t g, uint32_t v, const uint32_t *dep_cfg, uint64_t *cost,
+                             uint32_t *argmin);
+
+/* Order-independent fingerprints of the DP table of vertex v (needs
+ * PASE_OPT_KEEP_TABLES=1): with phi the canonical index (D(v) ascending,
+ * first digit slowest) and mix the SplitMix64 output function,
+ *   fp_cost = sum_phi mix(mix(phi) ^ T[phi]),  fp_arg = sum_phi mix(mix(phi) ^ A[phi])
+ * (sums mod 2^64). */
+pase_status pase_table_fingerprint(pase_graph_t g, uint32_t v, uint64_t *fp_cost, uint64_t *fp_arg);
+
+/* Device-computed layer costs t_l(v, c) of the last search, host out[K_v]. */
+pase_status pase_layer_costs(pase_graph_t g, uint32_t v, uint64_t *out);
+
+/* Device-computed r*t_x(e, c_src, c_dst) of edge e, host out[K_src*K_dst]
+ * row-major (evaluated on the GPU from the configurations). */
+pase_status pase_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out);
+
+/* Statistics of the last search. */
+pase_status pase_stats(pase_graph_t g, pase_run_stats *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PASE_H */

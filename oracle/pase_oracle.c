@@ -1,0 +1,637 @@
+/*
+ * Plain CPU oracle for PaSE's strategy search (Elango, "PaSE: Parallelization
+ * Strategies for Efficient DNN Training", IPDPS 2021).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this file's library.  It shares no
+ * code with the HIP library and is deliberately slow and literal:
+ *
+ *   - configurations: Sec. II, C(v) = {c : prod c_k <= p}, restricted to powers
+ *     of two, enumerated in lexicographic order of the exponent tuple
+ *     (first loop dim slowest);
+ *   - cost function F: eq. (1), with the integer layer / transfer cost model
+ *     documented at layer_cost() and transfer_cost();
+ *   - vertex ordering: GenerateSeq, Fig. 3 (argmin of |u.d|, ties to the
+ *     lowest vertex id);
+ *   - dynamic program: recurrence (4) evaluated as in FindBestStrategy, Fig. 4,
+ *     with the node function of eq. (3), the connected set X(i) and connected
+ *     subsets S(i) of Sec. III-B, the strict "<" update over configurations in
+ *     ascending index order, and back-substitution from the last vertex;
+ *   - every addition is overflow-checked in uint64.
+ *
+ * Tables are stored in canonical order: the dependent set D(i) sorted by
+ * vertex id, first digit slowest.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <stdio.h>
+#include <time.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define MAXD 8
+
+typedef struct {
+    /* graph */
+    int nv, ne;
+    int ndims[4096];
+    uint64_t *size;          /* nv*MAXD */
+    uint32_t *reduce_mask;   /* nv */
+    uint64_t *fpp;           /* nv flops per iteration point */
+    int *src, *dst, *rank;   /* ne */
+    int *src_dim, *dst_dim;  /* ne*MAXD */
+    uint64_t *elems;         /* ne */
+    uint64_t r;              /* FLOP-to-byte ratio weighting communication */
+    /* configurations */
+    int p, log2p;
+    int *K;                  /* configs per vertex */
+    uint8_t **ex;            /* ex[v][c*ndims+k] = exponent of the split of dim k */
+    /* cost tables */
+    uint64_t **Lc;           /* Lc[v][c]       = t_l(v, c)            */
+    uint64_t **Rx;           /* Rx[e][cu*Kv+cv] = r * t_x(e, cu, cv)  */
+    /* undirected neighbourhoods, deduplicated: nbr[v][0..deg[v]) */
+    int **nbr, *deg;
+    /* ordering */
+    int *seq, *pos;          /* seq[i] = vertex at position i, pos[v] = its position */
+    int **D, *nD;            /* D[i] = dependent set of position i, sorted by vertex id */
+    /* DP tables by position */
+    uint64_t *N;             /* entries of table i */
+    uint64_t **T;            /* cost tables */
+    uint16_t **A;            /* argmin tables (config index of seq[i]) */
+    uint64_t min_cost;
+    int *strategy;           /* config index per vertex id */
+    int solved;
+    uint64_t cells, cells_done;
+    double seconds;
+    int overflow;
+    char err[256];
+} oracle_t;
+
+static int fail(oracle_t *o, const char *msg) {
+    snprintf(o->err, sizeof o->err, "%s", msg);
+    return 1;
+}
+
+const char *oracle_error(oracle_t *o) { return o->err; }
+
+static int add_ok(uint64_t a, uint64_t b, uint64_t *out) { return !__builtin_add_overflow(a, b, out); }
+static int mul_ok(uint64_t a, uint64_t b, uint64_t *out) { return !__builtin_mul_overflow(a, b, out); }
+
+static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
+
+/* ------------------------------------------------------------------ graph */
+
+oracle_t *oracle_new(int nv, const int *ndims, const uint64_t *sizes, const uint32_t *reduce_mask,
+                     const uint64_t *fpp, int ne, const int *src, const int *dst, const int *rank,
+                     const int *src_dim, const int *dst_dim, const uint64_t *elems, uint64_t r) {
+    if (nv < 1 || nv > 4096 || ne < 0) return NULL;
+    oracle_t *o = calloc(1, sizeof *o);
+    o->nv = nv; o->ne = ne; o->r = r;
+    o->size = calloc((size_t)nv * MAXD, sizeof(uint64_t));
+    o->reduce_mask = calloc(nv, sizeof(uint32_t));
+    o->fpp = calloc(nv, sizeof(uint64_t));
+    for (int v = 0; v < nv; v++) {
+        o->ndims[v] = ndims[v];
+        for (int k = 0; k < ndims[v]; k++) o->size[v * MAXD + k] = sizes[v * MAXD + k];
+        o->reduce_mask[v] = reduce_mask[v];
+        o->fpp[v] = fpp[v];
+    }
+    o->src = calloc(ne + 1, sizeof(int)); o->dst = calloc(ne + 1, sizeof(int));
+    o->rank = calloc(ne + 1, sizeof(int));
+    o->src_dim = calloc((size_t)(ne + 1) * MAXD, sizeof(int));
+    o->dst_dim = calloc((size_t)(ne + 1) * MAXD, sizeof(int));
+    o->elems = calloc(ne + 1, sizeof(uint64_t));
+    for (int e = 0; e < ne; e++) {
+        o->src[e] = src[e]; o->dst[e] = dst[e]; o->rank[e] = rank[e]; o->elems[e] = elems[e];
+        for (int k = 0; k < rank[e]; k++) {
+            o->src_dim[e * MAXD + k] = src_dim[e * MAXD + k];
+            o->dst_dim[e * MAXD + k] = dst_dim[e * MAXD + k];
+        }
+    }
+    /* N(v) = {u : (u,v) in E or (v,u) in E}, as a set (Sec. III notation) */
+    o->deg = calloc(nv, sizeof(int));
+    o->nbr = calloc(nv, sizeof(int *));
+    char *adj = calloc((size_t)nv * nv, 1);
+    for (int e = 0; e < ne; e++) {
+        adj[(size_t)src[e] * nv + dst[e]] = 1;
+        adj[(size_t)dst[e] * nv + src[e]] = 1;
+    }
+    for (int v = 0; v < nv; v++) {
+        o->nbr[v] = calloc(nv, sizeof(int));
+        for (int u = 0; u < nv; u++)
+            if (adj[(size_t)v * nv + u]) o->nbr[v][o->deg[v]++] = u;
+    }
+    free(adj);
+    return o;
+}
+
+static void free_tables(oracle_t *o) {
+    if (o->T) {
+        for (int i = 0; i < o->nv; i++) { free(o->T[i]); free(o->A[i]); free(o->D[i]); }
+        free(o->T); free(o->A); free(o->D); free(o->nD); free(o->N);
+        free(o->seq); free(o->pos); free(o->strategy);
+        o->T = NULL;
+    }
+}
+
+static void free_configs(oracle_t *o) {
+    if (o->K) {
+        for (int v = 0; v < o->nv; v++) { free(o->ex[v]); free(o->Lc[v]); }
+        for (int e = 0; e < o->ne; e++) free(o->Rx[e]);
+        free(o->ex); free(o->Lc); free(o->Rx); free(o->K);
+        o->K = NULL;
+    }
+}
+
+void oracle_free(oracle_t *o) {
+    if (!o) return;
+    free_tables(o);
+    free_configs(o);
+    for (int v = 0; v < o->nv; v++) free(o->nbr[v]);
+    free(o->nbr); free(o->deg);
+    free(o->size); free(o->reduce_mask); free(o->fpp);
+    free(o->src); free(o->dst); free(o->rank); free(o->src_dim); free(o->dst_dim); free(o->elems);
+    free(o);
+}
+
+/* --------------------------------------------------------- configurations */
+
+/* Append every exponent tuple with sum <= budget, dims k..d-1 free, in
+ * lexicographic order (dim 0 slowest). */
+static void enum_rec(int d, int k, int budget, uint8_t *cur, uint8_t *out, int *count) {
+    if (k == d) {
+        memcpy(out + (size_t)(*count) * d, cur, d);
+        (*count)++;
+        return;
+    }
+    for (int e = 0; e <= budget; e++) {
+        cur[k] = (uint8_t)e;
+        enum_rec(d, k + 1, budget - e, cur, out, count);
+    }
+}
+
+static uint64_t binom(int n, int k) {
+    uint64_t r = 1;
+    for (int i = 1; i <= k; i++) r = r * (uint64_t)(n - k + i) / (uint64_t)i;
+    return r;
+}
+
+/* Layer cost t_l(v, c): compute time plus r times the intra-layer
+ * communication (eq. 1 and the text after it).  Integer model:
+ *   compute = ceil(fpp * prod(n_k) / P),  P = prod(s_k)
+ *   comm    = (prod_{k in reduce} s_k - 1) * ceil(prod_{k not in reduce} n_k
+ *                                                 / prod_{k not in reduce} s_k)
+ *   t_l     = compute + r * comm
+ * (comm is the partial-sum reduction a split contraction dim requires.) */
+static int layer_cost(oracle_t *o, int v, const uint8_t *e, uint64_t *out) {
+    uint64_t flops = o->fpp[v], P = 1, red_split = 1, keep_n = 1, keep_split = 1;
+    for (int k = 0; k < o->ndims[v]; k++) {
+        uint64_t n = o->size[v * MAXD + k], s = (uint64_t)1 << e[k];
+        if (!mul_ok(flops, n, &flops)) return 0;
+        P *= s;
+        if (o->reduce_mask[v] >> k & 1u) {
+            red_split *= s;
+        } else {
+            if (!mul_ok(keep_n, n, &keep_n)) return 0;
+            keep_split *= s;
+        }
+    }
+    uint64_t compute = ceil_div(flops, P);
+    uint64_t comm, comm_r, total;
+    if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;
+    if (!mul_ok(o->r, comm, &comm_r)) return 0;
+    if (!add_ok(compute, comm_r, &total)) return 0;
+    *out = total;
+    return 1;
+}
+
+/* r * t_x(u, v): zero when both endpoints split every dim of the tensor the
+ * same way, otherwise the tensor is re-distributed: ceil(elems / max(P_u, P_v))
+ * words per device, weighted by r.  Symmetric in (u, v) as the paper requires. */
+static int transfer_cost(oracle_t *o, int e, const uint8_t *eu, const uint8_t *ev, uint64_t *out) {
+    int u = o->src[e], v = o->dst[e];
+    int match = 1;
+    for (int k = 0; k < o->rank[e]; k++) {
+        int a = o->src_dim[e * MAXD + k], b = o->dst_dim[e * MAXD + k];
+        uint64_t su = a >= 0 ? (uint64_t)1 << eu[a] : 1;
+        uint64_t sv = b >= 0 ? (uint64_t)1 << ev[b] : 1;
+        if (su != sv) match = 0;
+    }
+    if (match) { *out = 0; return 1; }
+    uint64_t Pu = 1, Pv = 1;
+    for (int k = 0; k < o->ndims[u]; k++) Pu *= (uint64_t)1 << eu[k];
+    for (int k = 0; k < o->ndims[v]; k++) Pv *= (uint64_t)1 << ev[k];
+    uint64_t words = ceil_div(o->elems[e], Pu > Pv ? Pu : Pv);
+    return mul_ok(o->r, words, out);
+}
+
+/* Enumerate C(v) for every v and fill the cost tables. p must be 2^L. */
+int oracle_configs(oracle_t *o, int p) {
+    free_tables(o);
+    free_configs(o);
+    o->solved = 0;
+    if (p < 1 || (p & (p - 1))) return fail(o, "p must be a power of two");
+    int L = 0;
+    while ((1 << L) < p) L++;
+    o->p = p; o->log2p = L;
+    o->K = calloc(o->nv, sizeof(int));
+    o->ex = calloc(o->nv, sizeof(uint8_t *));
+    o->Lc = calloc(o->nv, sizeof(uint64_t *));
+    o->Rx = calloc(o->ne + 1, sizeof(uint64_t *));
+    for (int v = 0; v < o->nv; v++) {
+        int d = o->ndims[v];
+        uint64_t cnt = binom(L + d, d);
+        if (cnt > 65535) return fail(o, "too many configurations for a uint16 argmin");
+        o->ex[v] = calloc(cnt * d, 1);
+        uint8_t cur[MAXD];
+        int count = 0;
+        enum_rec(d, 0, L, cur, o->ex[v], &count);
+        o->K[v] = count;
+        o->Lc[v] = calloc(count, sizeof(uint64_t));
+        for (int c = 0; c < count; c++)
+            if (!layer_cost(o, v, o->ex[v] + (size_t)c * d, &o->Lc[v][c]))
+                return fail(o, "layer cost overflows uint64");
+    }
+    for (int e = 0; e < o->ne; e++) {
+        int u = o->src[e], v = o->dst[e];
+        o->Rx[e] = calloc((size_t)o->K[u] * o->K[v], sizeof(uint64_t));
+        for (int cu = 0; cu < o->K[u]; cu++)
+            for (int cv = 0; cv < o->K[v]; cv++)
+                if (!transfer_cost(o, e, o->ex[u] + (size_t)cu * o->ndims[u],
+                                   o->ex[v] + (size_t)cv * o->ndims[v],
+                                   &o->Rx[e][(size_t)cu * o->K[v] + cv]))
+                    return fail(o, "transfer cost overflows uint64");
+    }
+    return 0;
+}
+
+/* Replace the cost tables by caller-given ones (tests with random costs).
+ * layer: concatenation of K_v values per vertex; edge: concatenation of the
+ * row-major K_src x K_dst matrices per edge. */
+int oracle_set_costs(oracle_t *o, const uint64_t *layer, const uint64_t *edge) {
+    if (!o->K) return fail(o, "configs not enumerated");
+    free_tables(o);
+    o->solved = 0;
+    size_t off = 0;
+    for (int v = 0; v < o->nv; v++)
+        for (int c = 0; c < o->K[v]; c++) o->Lc[v][c] = layer[off++];
+    off = 0;
+    for (int e = 0; e < o->ne; e++) {
+        size_t n = (size_t)o->K[o->src[e]] * o->K[o->dst[e]];
+        for (size_t k = 0; k < n; k++) o->Rx[e][k] = edge[off++];
+    }
+    return 0;
+}
+
+/* --------------------------------------------------------- ordering */
+
+static int cmp_int(const void *a, const void *b) { return *(const int *)a - *(const int *)b; }
+
+/* GenerateSeq (Fig. 3).  rule 0: the d-set of v never contains v itself,
+ * v.d <- (v.d U v_i.d) - {v_i, v}.  rule 1: the update exactly as printed,
+ * v.d <- v.d U v_i.d - {v_i}, so v may count itself while unsequenced; the
+ * recorded dependent set drops v_i.  Either way D(i) is v_i.d at selection. */
+static void generate_seq(oracle_t *o, int rule) {
+    int n = o->nv;
+    char *d = calloc((size_t)n * n, 1);   /* d[v*n+u] = u in v.d */
+    char *in_U = calloc(n, 1);
+    for (int v = 0; v < n; v++) {
+        in_U[v] = 1;
+        for (int k = 0; k < o->deg[v]; k++) d[(size_t)v * n + o->nbr[v][k]] = 1;
+    }
+    for (int i = 0; i < n; i++) {
+        int best = -1, best_sz = 0;
+        for (int u = 0; u < n; u++) {
+            if (!in_U[u]) continue;
+            int sz = 0;
+            for (int w = 0; w < n; w++) sz += d[(size_t)u * n + w];
+            if (best < 0 || sz < best_sz) { best = u; best_sz = sz; }
+        }
+        int vi = best;
+        o->seq[i] = vi;
+        o->pos[vi] = i;
+        in_U[vi] = 0;
+        o->nD[i] = 0;
+        for (int w = 0; w < n; w++)
+            if (d[(size_t)vi * n + w] && w != vi) o->D[i][o->nD[i]++] = w;
+        for (int v = 0; v < n; v++) {
+            if (!d[(size_t)vi * n + v] || v == vi) continue;
+            for (int w = 0; w < n; w++) d[(size_t)v * n + w] |= d[(size_t)vi * n + w];
+            d[(size_t)v * n + vi] = 0;
+            if (rule == 0) d[(size_t)v * n + v] = 0;
+        }
+    }
+    free(d);
+    free(in_U);
+}
+
+/* Vertices reachable from `start` through vertices whose position is <= lim
+ * (the paper's DFS(G, U, v) with U = V_{<=lim}). mark[] receives `tag`. */
+static void dfs(oracle_t *o, int start, int lim, int *mark, int tag, int *stack) {
+    int top = 0;
+    stack[top++] = start;
+    mark[start] = tag;
+    while (top) {
+        int v = stack[--top];
+        for (int k = 0; k < o->deg[v]; k++) {
+            int u = o->nbr[v][k];
+            if (o->pos[u] <= lim && mark[u] != tag) {
+                mark[u] = tag;
+                stack[top++] = u;
+            }
+        }
+    }
+}
+
+/* Dependent sets from their definition, D(i) = N(X(i)) intersected with
+ * V_{>i} (Sec. III-B), for a caller-given order. */
+static void dependent_sets_by_definition(oracle_t *o) {
+    int n = o->nv;
+    int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
+    char *inD = calloc(n, 1);
+    for (int i = 0; i < n; i++) {
+        for (int v = 0; v < n; v++) mark[v] = -1;
+        dfs(o, o->seq[i], i, mark, 1, stack);
+        memset(inD, 0, n);
+        for (int v = 0; v < n; v++)
+            if (mark[v] == 1)
+                for (int k = 0; k < o->deg[v]; k++)
+                    if (o->pos[o->nbr[v][k]] > i) inD[o->nbr[v][k]] = 1;
+        o->nD[i] = 0;
+        for (int v = 0; v < n; v++) if (inD[v]) o->D[i][o->nD[i]++] = v;
+    }
+    free(mark); free(stack); free(inD);
+}
+
+/* --------------------------------------------------------- dynamic program */
+
+typedef struct {          /* one lookup T_j[phi''] in recurrence (4) */
+    int j;                /* position of the component's last vertex */
+} term_t;
+
+/* Canonical index of phi restricted to D(j), read from a full assignment. */
+static uint64_t table_index(oracle_t *o, int j, const int *cfg_of) {
+    uint64_t idx = 0;
+    for (int k = 0; k < o->nD[j]; k++) idx = idx * (uint64_t)o->K[o->D[j][k]] + (uint64_t)cfg_of[o->D[j][k]];
+    return idx;
+}
+
+/* Node function H_V(i, phi') of eq. (3): layer cost of v_i plus r*t_x for
+ * every edge joining v_i and a vertex later in the sequence (each edge of a
+ * multigraph counted, as in the sum over E of eq. 1). */
+static int node_cost(oracle_t *o, int i, const int *later_edges, int nlater, const int *cfg_of,
+                     uint64_t *out) {
+    int vi = o->seq[i];
+    uint64_t cost = o->Lc[vi][cfg_of[vi]];
+    for (int k = 0; k < nlater; k++) {
+        int e = later_edges[k], u = o->src[e], v = o->dst[e];
+        uint64_t x = o->Rx[e][(size_t)cfg_of[u] * o->K[v] + cfg_of[v]];
+        if (!add_ok(cost, x, &cost)) return 0;
+    }
+    *out = cost;
+    return 1;
+}
+
+/* FindBestStrategy (Fig. 4).  order: NULL -> GenerateSeq with `rule`, else the
+ * given sequence of vertex ids (dependent sets then come from their
+ * definition).  max_cells > 0 stops after the first vertex that reaches that
+ * many cell evaluations (a timing sample; the result is then partial).
+ * nthreads > 0 runs the loop over phi on that many OpenMP threads; the loop
+ * over configurations stays sequential, so the tie-break is unchanged. */
+int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, int nthreads) {
+    if (!o->K) return fail(o, "configs not enumerated");
+    free_tables(o);
+    int n = o->nv;
+    o->seq = calloc(n, sizeof(int)); o->pos = calloc(n, sizeof(int));
+    o->D = calloc(n, sizeof(int *)); o->nD = calloc(n, sizeof(int));
+    for (int i = 0; i < n; i++) o->D[i] = calloc(n, sizeof(int));
+    o->N = calloc(n, sizeof(uint64_t));
+    o->T = calloc(n, sizeof(uint64_t *)); o->A = calloc(n, sizeof(uint16_t *));
+    o->strategy = calloc(n, sizeof(int));
+    o->solved = 0; o->overflow = 0; o->cells_done = 0;
+
+    /* weak connectivity (the paper's computation graphs are weakly connected) */
+    {
+        int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
+        for (int v = 0; v < n; v++) { mark[v] = 0; o->pos[v] = 0; }
+        dfs(o, 0, 0, mark, 1, stack);
+        int ok = 1;
+        for (int v = 0; v < n; v++) ok &= mark[v] == 1;
+        free(mark); free(stack);
+        if (!ok) return fail(o, "graph is not weakly connected");
+    }
+
+    if (order) {
+        char *seen = calloc(n, 1);
+        for (int i = 0; i < n; i++) {
+            if (order[i] < 0 || order[i] >= n || seen[order[i]]) { free(seen); return fail(o, "bad order"); }
+            seen[order[i]] = 1;
+            o->seq[i] = order[i];
+            o->pos[order[i]] = i;
+        }
+        free(seen);
+        dependent_sets_by_definition(o);
+    } else {
+        generate_seq(o, rule);
+    }
+    for (int i = 0; i < n; i++) qsort(o->D[i], o->nD[i], sizeof(int), cmp_int);
+
+    o->cells = 0;
+    for (int i = 0; i < n; i++) {
+        uint64_t N = 1;
+        for (int k = 0; k < o->nD[i]; k++)
+            if (!mul_ok(N, (uint64_t)o->K[o->D[i][k]], &N)) return fail(o, "table too large");
+        o->N[i] = N;
+        o->cells += N * (uint64_t)o->K[o->seq[i]];
+    }
+
+    int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
+    int *comp = calloc(n, sizeof(int));
+    term_t *terms = calloc(n, sizeof(term_t));
+    int *later = calloc(o->ne + 1, sizeof(int));
+    struct timespec t0, t1;
+    clock_gettime(CLOCK_MONOTONIC, &t0);
+    int stopped = 0;
+
+    for (int i = 0; i < n && !stopped; i++) {
+        int vi = o->seq[i];
+        /* X(i) = DFS(G, V_{<=i}, v_i) */
+        for (int v = 0; v < n; v++) { mark[v] = 0; comp[v] = 0; }
+        dfs(o, vi, i, mark, 1, stack);
+        /* S(i): components of X(i) - {v_i} inside V_{<i}; each is represented
+         * by j = the largest position among its vertices */
+        int nterms = 0;
+        for (int v = 0; v < n; v++) {
+            if (mark[v] != 1 || v == vi || comp[v]) continue;
+            int tag = nterms + 2;
+            int *m2 = comp;
+            /* DFS(G, V_{<i}, v) */
+            int top = 0;
+            stack[top++] = v; m2[v] = tag;
+            int jmax = o->pos[v];
+            while (top) {
+                int x = stack[--top];
+                if (o->pos[x] > jmax) jmax = o->pos[x];
+                for (int k = 0; k < o->deg[x]; k++) {
+                    int u = o->nbr[x][k];
+                    if (o->pos[u] < i && m2[u] != tag) { m2[u] = tag; stack[top++] = u; }
+                }
+            }
+            terms[nterms++].j = jmax;
+        }
+
+        /* edges joining v_i and a vertex later in the sequence */
+        int nlater = 0;
+        for (int e = 0; e < o->ne; e++) {
+            int other = o->src[e] == vi ? o->dst[e] : (o->dst[e] == vi ? o->src[e] : -1);
+            if (other >= 0 && o->pos[other] > i) later[nlater++] = e;
+        }
+
+        uint64_t N = o->N[i];
+        int Ki = o->K[vi];
+        o->T[i] = malloc(N * sizeof(uint64_t));
+        o->A[i] = malloc(N * sizeof(uint16_t));
+        int nd = o->nD[i];
+        const int *Di = o->D[i];
+        int ovf = 0;
+
+#ifdef _OPENMP
+        int nt = nthreads > 0 ? nthreads : 1;
+#pragma omp parallel num_threads(nt) reduction(| : ovf)
+#endif
+        {
+            int *cfg_of = malloc(n * sizeof(int));
+            for (int v = 0; v < n; v++) cfg_of[v] = -1;
+#ifdef _OPENMP
+#pragma omp for schedule(static)
+#endif
+            for (int64_t phi = 0; phi < (int64_t)N; phi++) {
+                /* decode phi in canonical mixed radix (first digit slowest) */
+                uint64_t rem = (uint64_t)phi;
+                for (int k = nd - 1; k >= 0; k--) {
+                    uint64_t Kw = (uint64_t)o->K[Di[k]];
+                    cfg_of[Di[k]] = (int)(rem % Kw);
+                    rem /= Kw;
+                }
+                uint64_t mincost = UINT64_MAX;   /* the paper's top element */
+                int arg = 0;
+                for (int c = 0; c < Ki; c++) {
+                    cfg_of[vi] = c;                     /* phi' = phi U {(v_i, C)} */
+                    uint64_t cost;
+                    if (!node_cost(o, i, later, nlater, cfg_of, &cost)) { ovf = 1; break; }
+                    for (int t = 0; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */
+                        int j = terms[t].j;
+                        if (!add_ok(cost, o->T[j][table_index(o, j, cfg_of)], &cost)) { ovf = 1; break; }
+                    }
+                    if (cost < mincost) { mincost = cost; arg = c; }
+                }
+                o->T[i][phi] = mincost;
+                o->A[i][phi] = (uint16_t)arg;
+            }
+            free(cfg_of);
+        }
+        if (ovf) { o->overflow = 1; stopped = 1; break; }
+        o->cells_done += N * (uint64_t)Ki;
+        if (max_cells && o->cells_done >= max_cells && i + 1 < n) stopped = 2;
+    }
+    clock_gettime(CLOCK_MONOTONIC, &t1);
+    o->seconds = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
+    free(mark); free(stack); free(comp); free(terms); free(later);
+    if (o->overflow) return fail(o, "cost overflows uint64");
+    if (stopped == 2) return 2;  /* partial run: timing sample only */
+
+    /* R_V(|V|, empty) and back-substitution from the last vertex */
+    o->min_cost = o->T[n - 1][0];
+    int *cfg_of = calloc(n, sizeof(int));
+    for (int i = n - 1; i >= 0; i--) {
+        uint64_t idx = table_index(o, i, cfg_of);
+        cfg_of[o->seq[i]] = o->A[i][idx];
+    }
+    for (int v = 0; v < n; v++) o->strategy[v] = cfg_of[v];
+    free(cfg_of);
+    o->solved = 1;
+    return 0;
+}
+
+/* --------------------------------------------------------- getters */
+
+int oracle_num_configs(oracle_t *o, int v) { return o->K ? o->K[v] : -1; }
+int oracle_config_exponents(oracle_t *o, int v, int c, uint8_t *out) {
+    if (!o->K || c < 0 || c >= o->K[v]) return 1;
+    memcpy(out, o->ex[v] + (size_t)c * o->ndims[v], o->ndims[v]);
+    return 0;
+}
+int oracle_layer_costs(oracle_t *o, int v, uint64_t *out) {
+    if (!o->K) return 1;
+    memcpy(out, o->Lc[v], o->K[v] * sizeof(uint64_t));
+    return 0;
+}
+int oracle_edge_costs(oracle_t *o, int e, uint64_t *out) {
+    if (!o->K) return 1;
+    memcpy(out, o->Rx[e], (size_t)o->K[o->src[e]] * o->K[o->dst[e]] * sizeof(uint64_t));
+    return 0;
+}
+int oracle_sequence(oracle_t *o, int *out) {
+    if (!o->seq) return 1;
+    memcpy(out, o->seq, o->nv * sizeof(int));
+    return 0;
+}
+/* dependent set of the vertex at position i (sorted by vertex id) */
+int oracle_dependent_set(oracle_t *o, int i, int *out) {
+    if (!o->D) return -1;
+    memcpy(out, o->D[i], o->nD[i] * sizeof(int));
+    return o->nD[i];
+}
+uint64_t oracle_table_size(oracle_t *o, int i) { return o->N ? o->N[i] : 0; }
+int oracle_table(oracle_t *o, int i, uint64_t *T, uint16_t *A) {
+    if (!o->T || !o->T[i]) return 1;
+    if (T) memcpy(T, o->T[i], o->N[i] * sizeof(uint64_t));
+    if (A) memcpy(A, o->A[i], o->N[i] * sizeof(uint16_t));
+    return 0;
+}
+int oracle_entry(oracle_t *o, int i, uint64_t idx, uint64_t *T, uint32_t *A) {
+    if (!o->T || !o->T[i] || idx >= o->N[i]) return 1;
+    *T = o->T[i][idx];
+    *A = o->A[i][idx];
+    return 0;
+}
+int oracle_result(oracle_t *o, uint64_t *min_cost, int *strategy) {
+    if (!o->solved) return 1;
+    *min_cost = o->min_cost;
+    memcpy(strategy, o->strategy, o->nv * sizeof(int));
+    return 0;
+}
+uint64_t oracle_cells(oracle_t *o) { return o->cells; }
+uint64_t oracle_cells_done(oracle_t *o) { return o->cells_done; }
+double oracle_seconds(oracle_t *o) { return o->seconds; }
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* SplitMix64 output function (Steele, Lea, Flood, OOPSLA 2014). */
+static uint64_t splitmix64_mix(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+/* Order-independent fingerprints of table i over canonical indices:
+ *   fpT = sum_phi mix(mix(phi) ^ T[phi]),  fpA = sum_phi mix(mix(phi) ^ A[phi])
+ * (sums mod 2^64). */
+int oracle_fingerprint(oracle_t *o, int i, uint64_t *fpT, uint64_t *fpA) {
+    if (!o->T || !o->T[i]) return 1;
+    uint64_t st = 0, sa = 0;
+    for (uint64_t phi = 0; phi < o->N[i]; phi++) {
+        uint64_t h = splitmix64_mix(phi);
+        st += splitmix64_mix(h ^ o->T[i][phi]);
+        sa += splitmix64_mix(h ^ (uint64_t)o->A[i][phi]);
+    }
+    *fpT = st; *fpA = sa;
+    return 0;
+}

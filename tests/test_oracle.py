@@ -1,0 +1,467 @@
+"""Pins of the CPU oracle (no GPU).
+
+The oracle is the reference every GPU result is compared with, so it is first
+checked against things it does not compute itself: hand-derived values of the
+integer cost model, closed forms (binomial configuration counts, the FC-chain
+optimum), exhaustive search over all strategies (Theorem 1), exhaustive search
+of every DP table entry, the Viterbi recursion on path graphs, the definition
+of the dependent set (Theorem 2), and order independence of the minimum.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+import pins
+from workloads import chain_graph, fc_chain, random_costs, random_graph, workload
+
+pytestmark = pytest.mark.usefixtures("oracle_lib")
+
+
+def _solve(g, p=None, rule=0, costs=None, order=None, lib=None):
+    from oracle.oracle import Oracle
+    o = Oracle(g, lib)
+    K = o.configs(p or g["p"])
+    if costs is not None:
+        o.set_costs(*costs)
+    o.solve(rule=rule, order=order)
+    return o, K
+
+
+def _tables(o, g):
+    L = [o.layer_costs(v) for v in range(len(g["vertices"]))]
+    R = [o.edge_costs(e) for e in range(len(g["edges"]))]
+    src = [e["src"] for e in g["edges"]]
+    dst = [e["dst"] for e in g["edges"]]
+    return L, R, src, dst
+
+
+# ------------------------------------------------------------------ configurations
+@pytest.mark.parametrize("d", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("p", [1, 2, 4, 8, 16, 64])
+def test_config_count_and_order(d, p):
+    """|C(v)| = C(L+d, d) for power-of-two splits with product <= p = 2^L
+    (stars and bars); order is lexicographic in the exponent tuple, dim 0
+    slowest; every tuple has product <= p and all are distinct."""
+    from oracle.oracle import Oracle
+    g = {"name": "one", "p": p, "comm_weight": 8,
+         "vertices": [{"name": "v", "dims": [7] * d, "dim_names": ["x"] * d, "reduce": [],
+                       "flops_per_point": 1}], "edges": []}
+    o = Oracle(g)
+    K = o.configs(p)
+    L = int(math.log2(p))
+    assert int(K[0]) == math.comb(L + d, d)
+    ex = [tuple(int(x) for x in row) for row in o.exponents(0)]
+    assert ex == sorted(ex)
+    assert len(set(ex)) == len(ex)
+    assert all(sum(t) <= L for t in ex)
+    # every admissible tuple is present
+    assert set(ex) == {t for t in itertools.product(range(L + 1), repeat=d) if sum(t) <= L}
+
+
+def test_workload_config_counts():
+    """10 (W0, p=4, 3 dims), 56 (W1, p=8, 5 dims), 126/70/35 (W2, p=16),
+    56 (W3, p=32, 3 dims), 462/210/84 (W4, p=64)."""
+    from oracle.oracle import Oracle
+    expect = {"w0_fc_chain": {10}, "w1_residual_cnn": {56}, "w2_inception": {126, 70, 35},
+              "w3_lstm_grid": {56}, "w4_transformer": {462, 210, 84}}
+    for name, ks in expect.items():
+        g = workload(name)
+        o = Oracle(g)
+        assert set(int(k) for k in o.configs(g["p"])) == ks
+
+
+def test_p_must_be_power_of_two():
+    from oracle.oracle import Oracle, OracleError
+    o = Oracle(fc_chain())
+    with pytest.raises(OracleError):
+        o.configs(6)
+
+
+# ------------------------------------------------------------------ cost model (hand values)
+def test_layer_cost_fc_hand_values():
+    """FC (64, 256, 256), contraction over `in`, r = 8, p = 4.
+    (4,1,1): 2*64*256*256/4 = 2 097 152 FLOPs, no partial sums.
+    (1,1,4): same compute + 8 * (4-1) * 64*256 = 2 097 152 + 393 216.
+    (1,1,1): 8 388 608.  (2,2,1): 2 097 152.  (1,2,2): 2 097 152 + 8*(2-1)*64*128."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain())
+    o.configs(4)
+    ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
+    L = o.layer_costs(0)
+    want = {(2, 0, 0): 2_097_152, (0, 0, 2): 2_490_368, (0, 0, 0): 8_388_608,
+            (1, 1, 0): 2_097_152, (0, 1, 1): 2_097_152 + 8 * 64 * 128}
+    for t, v in want.items():
+        assert int(L[ex.index(t)]) == v, t
+    assert ex.index((2, 0, 0)) == 9
+
+
+def test_layer_cost_ragged_hand_values():
+    """dims (3, 5), contraction over dim 1, 3 FLOPs per point (45 total), r = 8, p = 4:
+    (2,2): ceil(45/4)=12 + 8*(2-1)*ceil(3/2)=16 -> 28;  (1,4): 12 + 8*3*3 = 84;
+    (4,1): 12;  (1,1): 45;  (2,1): ceil(45/2)=23;  (1,2): 23 + 8*1*3 = 47."""
+    from oracle.oracle import Oracle
+    g = {"name": "r", "p": 4, "comm_weight": 8,
+         "vertices": [{"name": "v", "dims": [3, 5], "dim_names": ["a", "b"], "reduce": [1],
+                       "flops_per_point": 3}], "edges": []}
+    o = Oracle(g)
+    o.configs(4)
+    ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
+    L = o.layer_costs(0)
+    want = {(1, 1): 28, (0, 2): 84, (2, 0): 12, (0, 0): 45, (1, 0): 23, (0, 1): 47}
+    for t, v in want.items():
+        assert int(L[ex.index(t)]) == v, t
+
+
+def test_transfer_cost_hand_values():
+    """Edge fc0 -> fc1 carries (b, feat) from (b, out) of fc0 to (b, in) of fc1.
+    Equal splits on both tensor dims -> 0; otherwise 8 * ceil(16384 / max(P_u, P_v))."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain())
+    o.configs(4)
+    ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
+    R = o.edge_costs(0)
+    i = ex.index
+    assert int(R[i((2, 0, 0)), i((2, 0, 0))]) == 0
+    assert int(R[i((2, 0, 0)), i((0, 0, 2))]) == 8 * 4096
+    assert int(R[i((0, 0, 0)), i((0, 0, 0))]) == 0
+    assert int(R[i((1, 1, 0)), i((1, 0, 1))]) == 0          # b:2=2, feat: out 2 = in 2
+    assert int(R[i((1, 1, 0)), i((1, 1, 0))]) == 8 * 4096   # feat: out 2 vs in 1
+    assert int(R[i((0, 0, 0)), i((1, 0, 0))]) == 8 * 8192   # max(P) = 2
+    # the unsplit `out` dim of fc1 plays no role: (2,1,1) vs (2,2,1) on fc1 side
+    assert int(R[i((1, 0, 0)), i((1, 1, 0))]) == 0
+
+
+def test_transfer_cost_unsplit_tensor_dim():
+    """A tensor dim mapped to -1 on one side counts as split factor 1 there."""
+    from oracle.oracle import Oracle
+    g = {"name": "u", "p": 4, "comm_weight": 2,
+         "vertices": [{"name": "a", "dims": [8, 8], "dim_names": ["x", "y"], "reduce": [],
+                       "flops_per_point": 1},
+                      {"name": "b", "dims": [8], "dim_names": ["x"], "reduce": [],
+                       "flops_per_point": 1}],
+         "edges": [{"src": 0, "dst": 1, "src_dim": [0, 1], "dst_dim": [0, -1], "elems": 10}]}
+    o = Oracle(g)
+    o.configs(4)
+    exa = [tuple(int(x) for x in r) for r in o.exponents(0)]
+    exb = [tuple(int(x) for x in r) for r in o.exponents(1)]
+    R = o.edge_costs(0)
+    assert int(R[exa.index((1, 0)), exb.index((1,))]) == 0
+    assert int(R[exa.index((1, 1)), exb.index((1,))]) == 2 * math.ceil(10 / 4)
+    assert int(R[exa.index((0, 0)), exb.index((2,))]) == 2 * math.ceil(10 / 4)
+
+
+def test_cost_overflow_is_reported():
+    from oracle.oracle import Oracle, OracleError
+    g = {"name": "big", "p": 2, "comm_weight": 8,
+         "vertices": [{"name": "v", "dims": [2**40, 2**30], "dim_names": ["a", "b"], "reduce": [],
+                       "flops_per_point": 1}], "edges": []}
+    o = Oracle(g)
+    with pytest.raises(OracleError):
+        o.configs(2)
+
+
+# ------------------------------------------------------------------ GenerateSeq
+def test_generate_seq_fc_chain_both_rules():
+    """Hand trace of Fig. 3 on the path 0-1-2-3: excluding self gives [0,1,2,3];
+    the printed update (v may count itself) gives [0,3,1,2]."""
+    g = fc_chain()
+    o, _ = _solve(g, rule=0)
+    assert o.sequence() == [0, 1, 2, 3]
+    assert [o.dependent_set(i) for i in range(4)] == [[1], [2], [3], []]
+    o, _ = _solve(g, rule=1)
+    assert o.sequence() == [0, 3, 1, 2]
+    assert [o.dependent_set(i) for i in range(4)] == [[1], [2], [2], []]
+
+
+@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("rule", [0, 1])
+def test_theorem2_dependent_sets(seed, rule):
+    """Theorem 2: the d-set GenerateSeq records equals N(X(i)) after position i."""
+    g = random_graph(seed, n=5 + seed % 7, extra_edges=seed % 5, p=2)
+    o, _ = _solve(g, rule=rule)
+    seq = o.sequence()
+    nb = pins.neighbours(len(g["vertices"]), [e["src"] for e in g["edges"]],
+                         [e["dst"] for e in g["edges"]])
+    assert sorted(seq) == list(range(len(seq)))
+    for i in range(len(seq)):
+        assert o.dependent_set(i) == pins.dependent_set(nb, seq, i)
+    assert o.dependent_set(len(seq) - 1) == []
+
+
+def test_workload_dependent_set_histograms():
+    """Structure of the large workloads under the default rule."""
+    from oracle.oracle import Oracle
+    for name, hist in [("w1_residual_cnn", {0: 1, 1: 8, 2: 7}),
+                       ("w4_transformer", {0: 1, 1: 17, 2: 102, 3: 16})]:
+        g = workload(name)
+        o = Oracle(g)
+        o.configs(g["p"])
+        o.solve(max_cells=1)
+        h = {}
+        for i in range(len(g["vertices"])):
+            k = len(o.dependent_set(i))
+            h[k] = h.get(k, 0) + 1
+        assert h == hist
+
+
+# ------------------------------------------------------------------ dynamic program
+def test_fc_chain_closed_form():
+    """W0: every 4-way config costs 2 097 152; zero communication needs s_in = 1,
+    zero redistribution needs equal batch splits and s_out = 1 upstream, so the
+    unique optimum is (4,1,1) everywhere: 4 * 2 097 152 = 8 388 608."""
+    o, _ = _solve(fc_chain())
+    assert o.result() == (8_388_608, [9, 9, 9, 9])
+    assert o.cells() == 310
+
+
+def _check_against_brute_force(g, costs=None, rule=0):
+    o, K = _solve(g, costs=costs, rule=rule)
+    L, R, src, dst = _tables(o, g)
+    mc, strat = o.result()
+    bf_min, optimal = pins.brute_force(L, R, src, dst)
+    assert mc == bf_min                                   # Theorem 1
+    assert pins.total_cost(strat, L, R, src, dst) == mc   # recovered strategy costs the minimum
+    assert bool(optimal[tuple(strat)])
+    return o, K, L, R, src, dst
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_theorem1_model_costs(seed):
+    g = random_graph(seed, n=3 + seed % 4, p=4 if seed % 2 else 2, max_dims=2,
+                     extra_edges=seed % 3)
+    _check_against_brute_force(g)
+
+
+@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("rule", [0, 1])
+def test_every_table_entry_random_ties(seed, rule):
+    """Random integer costs in [0, 4) make ties dense; every entry of every
+    table and its argmin (lowest configuration index among the optimal ones)
+    must equal an exhaustive search conditioned on D(i)."""
+    g = random_graph(seed + 100, n=3 + seed % 4, p=4, max_dims=2, extra_edges=1 + seed % 3)
+    from oracle.oracle import Oracle
+    o0 = Oracle(g)
+    K = o0.configs(4)
+    costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    o, K, L, R, src, dst = _check_against_brute_force(g, costs=costs, rule=rule)
+    seq = o.sequence()
+    for i in range(len(seq)):
+        D, T, A = pins.conditioned_table(L, R, src, dst, seq, i, [int(k) for k in K])
+        assert o.dependent_set(i) == D
+        To, Ao = o.table(i)
+        assert To.tolist() == T, (i, seq)
+        assert Ao.tolist() == A, (i, seq)
+        assert o.fingerprint(i) == pins.fingerprint(T, A)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_viterbi_on_chains(seed):
+    """On a path graph the sequence is the path and the DP is the Viterbi
+    recursion: equal minimum and equal (lowest-index) strategy."""
+    g = chain_graph(seed, n=4 + seed % 5, p=8, max_dims=3)
+    from oracle.oracle import Oracle
+    o0 = Oracle(g)
+    K = o0.configs(8)
+    for costs in (None, random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=3)):
+        o, _ = _solve(g, costs=costs)
+        assert o.sequence() == list(range(len(g["vertices"])))
+        L, R, src, dst = _tables(o, g)
+        forward = [e["src"] < e["dst"] for e in g["edges"]]
+        mc, strat = o.result()
+        vmin, _ = pins.viterbi_chain(L, R, forward)
+        tmin, tstrat = pins.viterbi_table_strategy(L, R, forward)
+        assert mc == vmin == tmin
+        assert strat == tstrat
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_order_independence(seed):
+    """Theorem 1 holds for any order: GenerateSeq (both rules), breadth-first
+    and random orders give the same minimum, and each recovered strategy costs it."""
+    g = random_graph(seed + 7, n=6, p=4, max_dims=2, extra_edges=3)
+    from oracle.oracle import Oracle
+    mins = set()
+    nv = len(g["vertices"])
+    nb = pins.neighbours(nv, [e["src"] for e in g["edges"]], [e["dst"] for e in g["edges"]])
+    bfs = [0]
+    for v in bfs:
+        for u in sorted(nb[v]):
+            if u not in bfs:
+                bfs.append(u)
+    rng = np.random.default_rng(seed)
+    orders = [None, None, bfs, rng.permutation(nv).tolist(), rng.permutation(nv).tolist()]
+    for k, order in enumerate(orders):
+        o = Oracle(g)
+        o.configs(4)
+        o.solve(rule=1 if k == 1 else 0, order=order)
+        L, R, src, dst = _tables(o, g)
+        mc, strat = o.result()
+        assert pins.total_cost(strat, L, R, src, dst) == mc
+        if order is not None:
+            seq = o.sequence()
+            for i in range(nv):
+                assert o.dependent_set(i) == pins.dependent_set(nb, seq, i)
+        mins.add(mc)
+    assert len(mins) == 1
+
+
+def _fig2_graph():
+    """A graph built to satisfy the facts stated for the toy example (the
+    figure itself is not available): with the identity order v1..v9,
+    X(5) = {v1,v2,v3,v5}, S(5) = {{v1,v2},{v3}}, D(5) = {v8}, and the
+    breadth-first dependent set of position 5 is {v7,v8,v9}."""
+    edges = [(1, 2), (2, 5), (3, 5), (3, 8), (5, 8), (4, 7), (4, 9), (6, 7), (6, 9), (8, 9)]
+    vs = [{"name": f"v{k}", "dims": [4, 3], "dim_names": ["a", "b"], "reduce": [1],
+           "flops_per_point": k} for k in range(1, 10)]
+    es = [{"src": a - 1, "dst": b - 1, "src_dim": [0], "dst_dim": [0], "elems": 6 * a + b}
+          for a, b in edges]
+    return {"name": "fig2", "p": 2, "comm_weight": 8, "vertices": vs, "edges": es}
+
+
+def test_fig2_facts():
+    g = _fig2_graph()
+    order = list(range(9))
+    src = [e["src"] for e in g["edges"]]
+    dst = [e["dst"] for e in g["edges"]]
+    nb = pins.neighbours(9, src, dst)
+    i5 = 4  # position of v5 (0-based)
+    assert pins.connected_set(nb, order, i5) == {0, 1, 2, 4}
+    assert pins.connected_subsets(nb, order, i5) == [[0, 1], [2]]
+    assert pins.dependent_set(nb, order, i5) == [7]
+    assert pins.bfs_dependent_set(nb, order, i5) == [6, 7, 8]
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    K = o.configs(2)
+    costs = random_costs(5, K, [(K[a], K[b]) for a, b in zip(src, dst)], hi=5)
+    o.set_costs(*costs)
+    o.solve(order=order)
+    assert o.dependent_set(i5) == [7]
+    L, R = costs
+    D, T, A = pins.conditioned_table(L, R, src, dst, order, i5, [int(k) for k in K])
+    To, Ao = o.table(i5)
+    assert To.tolist() == T and Ao.tolist() == A
+    mc, strat = o.result()
+    assert mc == pins.brute_force(L, R, src, dst)[0]
+
+
+def test_multi_edges_counted_per_edge():
+    """Parallel edges each contribute their transfer cost (sum over E in eq. 1)."""
+    g = random_graph(3, n=4, p=2, max_dims=2, extra_edges=4, multi_edges=True)
+    pairs = [frozenset((e["src"], e["dst"])) for e in g["edges"]]
+    assert len(pairs) != len(set(pairs))
+    _check_against_brute_force(g)
+
+
+def test_disconnected_graph_rejected():
+    from oracle.oracle import Oracle, OracleError
+    g = random_graph(1, n=3, p=2)
+    g["vertices"].append({"name": "lonely", "dims": [2], "dim_names": ["a"], "reduce": [],
+                          "flops_per_point": 1})
+    o = Oracle(g)
+    o.configs(2)
+    with pytest.raises(OracleError):
+        o.solve()
+
+
+# ------------------------------------------------------------------ planted mistakes
+MUTANTS = {
+    "tie_break_last": ("if (cost < mincost) { mincost = cost; arg = c; }",
+                       "if (cost <= mincost) { mincost = cost; arg = c; }"),
+    "transposed_edge": ("uint64_t x = o->Rx[e][(size_t)cfg_of[u] * o->K[v] + cfg_of[v]];",
+                        "uint64_t x = o->Rx[e][(size_t)cfg_of[v] * o->K[u] + cfg_of[u]];"),
+    "dropped_lookup": ("for (int t = 0; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */",
+                       "for (int t = 1; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */"),
+    "earlier_edges": ("if (other >= 0 && o->pos[other] > i) later[nlater++] = e;",
+                      "if (other >= 0 && o->pos[other] < i) later[nlater++] = e;"),
+    "seq_tie_highest": ("if (best < 0 || sz < best_sz) { best = u; best_sz = sz; }",
+                        "if (best < 0 || sz <= best_sz) { best = u; best_sz = sz; }"),
+    "comm_off_by_one": ("if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;",
+                        "if (!mul_ok(red_split, ceil_div(keep_n, keep_split), &comm)) return 0;"),
+    "floor_not_ceil": ("static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }",
+                       "static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b; }"),
+    "no_match_check": ("if (su != sv) match = 0;", "if (su != sv) match = 1;"),
+}
+
+
+def _pin_suite(lib):
+    """A compact run of the pins above against an oracle library; returns the
+    list of pins that failed."""
+    failed = []
+    from oracle.oracle import Oracle, OracleError
+
+    def guard(name, fn):
+        try:
+            if not fn():
+                failed.append(name)
+        except (AssertionError, OracleError, ValueError, IndexError):
+            failed.append(name)
+
+    def w0():
+        o, _ = _solve(fc_chain(), lib=lib)
+        return o.result() == (8_388_608, [9, 9, 9, 9]) and o.sequence() == [0, 1, 2, 3]
+
+    def hand_costs():
+        o = Oracle({"name": "r", "p": 4, "comm_weight": 8,
+                    "vertices": [{"name": "v", "dims": [3, 5], "dim_names": ["a", "b"],
+                                  "reduce": [1], "flops_per_point": 3}], "edges": []}, lib)
+        o.configs(4)
+        ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
+        L = o.layer_costs(0)
+        return int(L[ex.index((1, 1))]) == 28 and int(L[ex.index((0, 2))]) == 84
+
+    def edge_costs():
+        o = Oracle(fc_chain(), lib)
+        o.configs(4)
+        ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
+        R = o.edge_costs(0)
+        return (int(R[ex.index((2, 0, 0)), ex.index((0, 0, 2))]) == 8 * 4096
+                and int(R[ex.index((1, 1, 0)), ex.index((1, 0, 1))]) == 0)
+
+    def tables():
+        for seed in range(6):
+            g = random_graph(seed + 100, n=3 + seed % 4, p=4, max_dims=2, extra_edges=1 + seed % 3)
+            o0 = Oracle(g, lib)
+            K = o0.configs(4)
+            costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+            o, K = _solve(g, costs=costs, lib=lib)
+            L, R, src, dst = _tables(o, g)
+            seq = o.sequence()
+            nb = pins.neighbours(len(seq), src, dst)
+            for i in range(len(seq)):
+                if o.dependent_set(i) != pins.dependent_set(nb, seq, i):
+                    return False
+                D, T, A = pins.conditioned_table(L, R, src, dst, seq, i, [int(k) for k in K])
+                To, Ao = o.table(i)
+                if To.tolist() != T or Ao.tolist() != A:
+                    return False
+            mc, strat = o.result()
+            if mc != pins.brute_force(L, R, src, dst)[0]:
+                return False
+        return True
+
+    guard("w0", w0)
+    guard("hand_costs", hand_costs)
+    guard("edge_costs", edge_costs)
+    guard("tables", tables)
+    return failed
+
+
+def test_pins_pass_on_the_oracle():
+    from oracle import oracle
+    assert _pin_suite(oracle._LIB) == []
+
+
+@pytest.mark.parametrize("mutant", sorted(MUTANTS))
+def test_pins_catch_planted_mistakes(mutant, tmp_path):
+    """Each plausible mistake planted in a copy of the oracle source makes at
+    least one pin fail (the mistake is planted on the CPU, never on a GPU)."""
+    from oracle import oracle
+    old, new = MUTANTS[mutant]
+    src = open(oracle._SRC).read()
+    assert src.count(old) == 1, mutant
+    path = tmp_path / f"mut_{mutant}.c"
+    path.write_text(src.replace(old, new))
+    lib = oracle.build(force=True, src=str(path), out=str(tmp_path / f"lib_{mutant}.so"))
+    assert _pin_suite(lib) != [], mutant
