@@ -1,0 +1,144 @@
+"""Benchmark of the PaSE strategy search on one MI355X.
+
+One step = the whole search for one graph: pase_enumerate_configs(p) (config
+enumeration, GenerateSeq, plans) + pase_find_best_strategy (cost tables,
+per-vertex DP fill, back-substitution).  Default workload: the Transformer
+encoder-decoder graph at p = 64 modeled devices (6.99e10 DP cell updates).
+
+Prints one JSON line: DP cell-updates/s of whole steps (`value`), the step
+wall time, the roofline of the dominant kernel (the row/column-chunk fill,
+fp64 add + min per cell, timed with HIP events on the search stream), the
+parity of the result with the CPU oracle's stored answer, and the oracle's
+own speed on a bounded prefix of the same vertex sequence.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DP cell-updates/sec and FindBestStrategy wall time (Transformer, p=64)"
+# fp64 VALU: 256 CUs x 64 lanes x 2.4 GHz, one add or one min per lane-cycle
+FP64_OPS_PEAK_T = 256 * 64 * 2.4e9 / 1e12
+OPS_PER_CELL = 2          # one add and one min (the min-plus multiply-accumulate)
+
+
+def cpu_threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp and omp.isdigit():
+        n = min(n, int(omp))
+    return max(1, n)
+
+
+def oracle_baseline(g, p, max_cells):
+    from oracle.oracle import Oracle
+    threads = cpu_threads()
+    o = Oracle(g)
+    o.configs(p)
+    o.solve(max_cells=max_cells, threads=threads)
+    done = o.cells_done()
+    n_done = 0
+    cum = 0
+    seq = o.sequence()
+    for i in range(len(seq)):
+        cum += o.table_size(i) * int(o.K[seq[i]])
+        n_done += 1
+        if cum >= done:
+            break
+    return {"value": done / o.seconds(), "unit": "cell-updates/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n_done} of {len(seq)} vertices of the same GenerateSeq order "
+                      f"({done:.3e} of {o.cells():.3e} cells, {o.seconds():.1f} s, "
+                      f"OpenMP over table entries)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="w4_transformer")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-cells", type=float, default=4e9, help="oracle sample size (cells)")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the strategy search runs on a single device "
+              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2407_04001_amd import OPT_PROFILE, Graph
+    from workloads import workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    g = workload(args.workload, args.seed)
+    p = g["p"]
+    pg = Graph(g)
+    pg.enumerate_configs(p)
+    pg.set_option(OPT_PROFILE, 1)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pg.enumerate_configs(p)
+        return pg.find_best_strategy(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    walls, rows_ms, rows_launches, fill_ms = [], 0.0, 0, 0.0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        mc, strat = step()
+        st = pg.stats()
+        walls.append(st["wall_ms"])
+        rows_ms += st["rows_fill_ms"]
+        fill_ms += st["fill_ms"]
+        rows_launches += st["rows_launches"]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    cells = st["cells"]
+    value = cells * args.steps / elapsed
+    achieved = OPS_PER_CELL * st["rows_cells"] * args.steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
+
+    parity = None
+    gold_path = os.path.join(ROOT, "tests", "golden", f"{args.workload}_seed{args.seed}.json")
+    if os.path.exists(gold_path):
+        with open(gold_path) as f:
+            gold = json.load(f)
+        parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "cell-updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
+        "config": {"workload": g["name"], "p": p, "vertices": len(g["vertices"]),
+                   "edges": len(g["edges"]), "cells": cells, "seed": args.seed},
+        "find_best_strategy_ms": sum(walls) / len(walls),
+        "fill_ms_per_step": fill_ms / args.steps,
+        "fill_cells_per_s": cells / (fill_ms / args.steps / 1e3) if fill_ms else None,
+        "min_cost": mc, "parity_with_oracle": parity,
+        "roofline": {"bound": "alu", "kernel": "k_fill_rows",
+                     "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
+                     "frac": achieved / FP64_OPS_PEAK_T, "traffic": None,
+                     "launches_per_step": rows_launches // args.steps,
+                     "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
+                     "cells_per_step": st["rows_cells"]},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = oracle_baseline(g, p, int(args.cpu_cells))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,1036 @@
+// Device runtime and HIP kernels of libpase (gfx950).
+//
+// FindBestStrategy (Fig. 4) runs as: one cost-table kernel for all layer
+// costs; then, for each position i of the GenerateSeq order, a prep kernel
+// that folds every term of recurrence (4) depending on at most (c, one digit)
+// -- or, for the row kernel, on (c, outer digits, column digit) -- into
+// key-space blocks, and one fill kernel that evaluates
+//     T_i[phi] = min_c  sum of terms(phi, c)      (and the minimising c)
+// for every phi; finally one back-substitution kernel.
+//
+// Keys.  A key is cost * 2^b + c with b = ceil(log2 K_i): the minimum key
+// gives the minimum cost and, among equal costs, the lowest configuration
+// index -- exactly the strict "<" update of Fig. 4 over ascending indices.
+// When the host proves every key is below 2^53 (sum of the maximal layer and
+// transfer costs, shifted by b), keys are doubles: every add of two keys is
+// then exact integer arithmetic and min-plus costs one v_add_f64 and one
+// v_min_f64 per cell.  Otherwise keys are uint64.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <type_traits>
+#include <cstring>
+#include <vector>
+
+#include "internal.h"
+
+using namespace pase;
+
+// ------------------------------------------------------------------ key arithmetic
+template <typename KeyT> struct KeyOps;
+
+template <> struct KeyOps<double> {
+    using Val = double;   // table value type
+    static constexpr double sentinel() { return 1152921504606846976.0; }  // 2^60 > any key
+    __device__ static double from_u64(uint64_t x) { return (double)x; }
+    __device__ static uint64_t val_to_u64(double x) { return (uint64_t)x; }
+    __device__ static double add(double a, double b) { return a + b; }
+    __device__ static double min(double a, double b) { return __builtin_fmin(a, b); }
+    // key = cost * 2^bits + c  ->  (cost * 2^out_shift, c)
+    __device__ static void split(double key, uint32_t bits, uint32_t out_shift, double &val, uint32_t &c) {
+        double s = __builtin_ldexp(1.0, (int)bits);
+        double v = __builtin_trunc(key * __builtin_ldexp(1.0, -(int)bits));
+        val = v * __builtin_ldexp(1.0, (int)out_shift);
+        c = (uint32_t)__builtin_fma(-v, s, key);
+    }
+};
+
+template <> struct KeyOps<uint64_t> {
+    using Val = uint64_t;
+    static constexpr uint64_t sentinel() { return ~0ull; }
+    __device__ static uint64_t from_u64(uint64_t x) { return x; }
+    __device__ static uint64_t val_to_u64(uint64_t x) { return x; }
+    __device__ static uint64_t add(uint64_t a, uint64_t b) { return a + b; }
+    __device__ static uint64_t min(uint64_t a, uint64_t b) { return a < b ? a : b; }
+    __device__ static void split(uint64_t key, uint32_t bits, uint32_t out_shift, uint64_t &val, uint32_t &c) {
+        val = (key >> bits) << out_shift;
+        c = (uint32_t)(key & ((1ull << bits) - 1));
+    }
+};
+
+
+// Buffer resource word 3 (data format 32-bit, raw addressing) for gfx9-family
+// buffer instructions.
+constexpr int kBufferWord3 = 0x00020000;
+
+// ------------------------------------------------------------------ cost model (device)
+// Layer cost t_l(v, c) = ceil(F / P) + r * (2^e_red - 1) * ceil(keep / 2^(E - e_red)),
+// with P = 2^E the device count of the configuration and e_red the exponent
+// sum over contracted dims.  Power-of-two divisions are shifts; the host has
+// bounded every operand so nothing overflows.
+__device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
+    uint32_t E = 0, ered = 0;
+    for (uint32_t k = 0; k < dv.ndims; k++) {
+        E += ex[k];
+        if ((dv.reduce_mask >> k) & 1u) ered += ex[k];
+    }
+    uint64_t compute = (dv.flops + ((1ull << E) - 1)) >> E;
+    uint32_t ek = E - ered;
+    uint64_t part = (dv.keep_n + ((1ull << ek) - 1)) >> ek;
+    return compute + r * (((1ull << ered) - 1) * part);
+}
+
+// r * t_x: 0 when every tensor dim is split equally at both ends, else the
+// tensor re-distributed over max(P_u, P_v) devices.
+__device__ __forceinline__ uint64_t edge_cost(const DevEdge &de, const uint8_t *exu, uint32_t du,
+                                              const uint8_t *exv, uint32_t dv, uint64_t r) {
+    bool match = true;
+    for (uint32_t k = 0; k < de.rank; k++) {
+        uint32_t a = de.sdim[k] >= 0 ? exu[de.sdim[k]] : 0;
+        uint32_t b = de.ddim[k] >= 0 ? exv[de.ddim[k]] : 0;
+        match &= a == b;
+    }
+    if (match) return 0;
+    uint32_t Eu = 0, Ev = 0;
+    for (uint32_t k = 0; k < du; k++) Eu += exu[k];
+    for (uint32_t k = 0; k < dv; k++) Ev += exv[k];
+    uint32_t s = Eu > Ev ? Eu : Ev;
+    return r * ((de.elems + ((1ull << s) - 1)) >> s);
+}
+
+__global__ void k_layer_costs(const DevVertex *__restrict__ V, uint32_t nv, const uint8_t *__restrict__ ex,
+                              uint64_t *__restrict__ L, uint64_t total, uint64_t r) {
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        uint32_t lo = 0, hi = nv;   // last vertex with L_off <= t
+        while (hi - lo > 1) {
+            uint32_t mid = (lo + hi) / 2;
+            if (V[mid].L_off <= t) lo = mid; else hi = mid;
+        }
+        const DevVertex dv = V[lo];
+        uint64_t c = t - dv.L_off;
+        L[t] = layer_cost(dv, ex + dv.ex_off + c * dv.ndims, r);
+    }
+}
+
+__global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t e,
+                             const uint8_t *__restrict__ ex, uint64_t *__restrict__ out, uint64_t r) {
+    const DevEdge de = E[e];
+    const DevVertex u = V[de.src], v = V[de.dst];
+    uint64_t total = (uint64_t)u.K * v.K;
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        uint64_t cu = t / v.K, cv = t % v.K;
+        out[t] = edge_cost(de, ex + u.ex_off + cu * u.ndims, u.ndims, ex + v.ex_off + cv * v.ndims,
+                           v.ndims, r);
+    }
+}
+
+// ------------------------------------------------------------------ prep: key-space blocks
+template <typename KeyT>
+__global__ void k_prep(PrepArgs a, const DevVertex *__restrict__ V, const DevEdge *__restrict__ E,
+                       const uint8_t *__restrict__ ex, const uint64_t *__restrict__ L,
+                       const Contrib *__restrict__ cb, KeyT *__restrict__ blocks, uint64_t r) {
+    using Val = typename KeyOps<KeyT>::Val;
+    const DevVertex me = V[a.vi];
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < a.total;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        uint32_t b = 0;
+        uint64_t e = t;
+        while (e >= a.blk[b].elems) { e -= a.blk[b].elems; b++; }
+        const Block &bk = a.blk[b];
+        uint32_t q = (uint32_t)(e % bk.ld);
+        uint64_t rest = e / bk.ld;
+        uint32_t c = (uint32_t)(rest % a.K);
+        rest /= a.K;
+        KeyT *out = blocks + bk.out_off + e;
+        if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; continue; }
+        uint32_t dv[kMaxDep];
+        for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
+        for (int k = (int)bk.npre - 1; k >= 0; k--) {
+            dv[bk.pre[k]] = (uint32_t)(rest % bk.prerad[k]);
+            rest /= bk.prerad[k];
+        }
+        if (bk.post >= 0) dv[bk.post] = q;
+        // plain costs (layer, transfer) are summed in `sum` and shifted into key
+        // space at the end; DP tables are stored in this vertex's key space already
+        uint64_t sum = 0, keysum = 0, low = 0;
+        const uint8_t *exme = ex + me.ex_off + (uint64_t)c * me.ndims;
+        for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
+            const Contrib &ct = cb[k];
+            if (ct.kind == kContribLayer) {
+                sum += L[me.L_off + c];
+                low = c;
+            } else if (ct.kind == kContribEdge) {
+                const DevEdge de = E[ct.edge];
+                uint32_t x = dv[ct.dig];
+                uint32_t other = ct.vi_is_src ? de.dst : de.src;
+                const DevVertex ov = V[other];
+                const uint8_t *exo = ex + ov.ex_off + (uint64_t)x * ov.ndims;
+                sum += ct.vi_is_src ? edge_cost(de, exme, me.ndims, exo, ov.ndims, r)
+                                    : edge_cost(de, exo, ov.ndims, exme, me.ndims, r);
+            } else {
+                uint64_t idx = (uint64_t)c * ct.sc;
+                for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
+                if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
+                else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
+            }
+        }
+        *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
+    }
+}
+
+// ------------------------------------------------------------------ fill: row kernel
+// Output T_i is laid out [z][o][r]: column digit z slowest, then the outer
+// digits o (those sharing a lookup with z), then the row digits r.  A wave
+// owns 64 consecutive rows of one (o, column chunk, c range); lane = row.
+// For each c the lane forms its row operand a = sum of its row terms, and the
+// wave reads the TZ column operands B[o][c][z0..z0+TZ) through the scalar
+// unit (they are wave-uniform), so each cell is one add and one min.
+template <typename KeyT, int TZ, int NA>
+__global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    const uint32_t lane = threadIdx.x & 63;
+    // the wave index is uniform across the wave: say so, so that everything
+    // derived from it (tile, c range, column addresses) lives in SGPRs
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // blocks are dealt round-robin to the 8 XCDs: give every XCD a contiguous
+    // range of tiles so that waves sharing a column slice share an L2
+    const uint32_t nb = a.nblocks_launched, b = blockIdx.x;
+    const uint64_t logical = (uint64_t)(b % 8) * (nb / 8) + b / 8;
+    const uint64_t tile = logical * 4 + wave;
+    if (tile >= a.total_tiles) return;
+    const uint32_t rowtile = (uint32_t)(tile % a.tiles_per_o);
+    uint64_t t2 = tile / a.tiles_per_o;
+    const uint32_t o = (uint32_t)(t2 % a.MO);
+    t2 /= a.MO;
+    const uint32_t chunk = (uint32_t)(t2 % a.nchunks);
+    const uint32_t split = (uint32_t)(t2 / a.nchunks);
+    const uint32_t r = rowtile * 64 + lane;
+    const bool valid = r < a.MR;
+    const uint32_t rr = valid ? r : a.MR - 1;
+
+    uint32_t dO[kMaxDep], dR[kMaxDep];
+    {
+        uint32_t x = o;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.nO) { dO[k] = x % a.radO[k]; x /= a.radO[k]; } else dO[k] = 0;
+        x = rr;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
+    }
+    constexpr int NT = NA < 0 ? kMaxATerms : NA;
+    const int na = NA < 0 ? (int)a.na : NA;
+    // row terms are read with buffer loads: per-lane byte offset in a VGPR,
+    // the c-dependent part as a scalar offset, no per-c address arithmetic
+    uint32_t offb[NT > 0 ? NT : 1];
+    __amdgpu_buffer_rsrc_t rsrc[NT > 0 ? NT : 1];
+#pragma unroll
+    for (int t = 0; t < NT; t++) {
+        uint32_t off = 0;
+        if (t < na) {
+            for (int k = 0; k < kMaxDep; k++) off += dO[k] * a.a[t].sdO[k] + dR[k] * a.a[t].sdR[k];
+            rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.a[t].ptr), (short)0,
+                                                        (int)a.a[t].bytes, kBufferWord3);
+        } else {
+            rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(nullptr, (short)0, 0, kBufferWord3);
+        }
+        offb[t] = off * (uint32_t)sizeof(Val);
+    }
+    const uint32_t c0 = split * a.cper;
+    const uint32_t c1 = min(a.K, c0 + a.cper);
+    const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * a.ldz + (uint64_t)chunk * TZ;
+
+    KeyT acc[TZ];
+#pragma unroll
+    for (int t = 0; t < TZ; t++) acc[t] = Ops::sentinel();
+
+    for (uint32_t c = c0; c < c1; c++) {
+        KeyT av = (KeyT)0;
+#pragma unroll
+        for (int t = 0; t < NT; t++) {
+            if (t < na) {
+                const uint64_t raw = __builtin_bit_cast(
+                    uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc[t], (int)offb[t],
+                                                                  (int)(c * a.a[t].sc * sizeof(Val)), 0));
+                const KeyT x = __builtin_bit_cast(KeyT, raw);
+                av = t == 0 ? x : Ops::add(av, x);
+            }
+        }
+        const __attribute__((address_space(4))) KeyT *brow =
+            (const __attribute__((address_space(4))) KeyT *)(uintptr_t)(B + (uint64_t)c * a.ldz);
+#pragma unroll
+        for (int t = 0; t < TZ; t++) acc[t] = Ops::min(acc[t], Ops::add(av, brow[t]));
+    }
+
+    if (!valid) return;
+    const uint64_t plane = (uint64_t)a.MO * a.MR;
+    const uint64_t base_idx = (uint64_t)o * a.MR + r;
+    const uint32_t zbase = chunk * TZ;
+#pragma unroll
+    for (int t = 0; t < TZ; t++) {
+        const uint32_t z = zbase + t;
+        if (z < a.Kz) {
+            const uint64_t idx = (uint64_t)z * plane + base_idx;
+            if (a.nsplit > 1) {
+                ((KeyT *)a.partial)[(uint64_t)split * a.N + idx] = acc[t];
+            } else {
+                Val v;
+                uint32_t cc;
+                Ops::split(acc[t], a.bits, a.out_shift, v, cc);
+                ((Val *)a.T)[idx] = v;
+                a.A[idx] = (uint16_t)cc;
+            }
+        }
+    }
+}
+
+template <typename KeyT>
+__global__ void k_reduce_splits(ReduceArgs a) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < a.N;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        KeyT best = ((const KeyT *)a.partial)[t];
+        for (uint32_t s = 1; s < a.nsplit; s++) best = Ops::min(best, ((const KeyT *)a.partial)[s * a.N + t]);
+        Val v;
+        uint32_t cc;
+        Ops::split(best, a.bits, a.out_shift, v, cc);
+        ((Val *)a.T)[t] = v;
+        a.A[t] = (uint16_t)cc;
+    }
+}
+
+// ------------------------------------------------------------------ fill: generic kernel
+// One thread per entry phi (any |D(i)| <= PASE_MAX_DEP, any term shapes):
+// key(c) = sum over terms, minimum over c in ascending order.
+template <typename KeyT>
+__global__ __launch_bounds__(256) void k_fill_generic(GenericArgs a) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    for (uint64_t phi = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; phi < a.N;
+         phi += (uint64_t)gridDim.x * blockDim.x) {
+        uint32_t d[kMaxDep];
+        uint64_t x = phi;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.m) { d[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else d[k] = 0;
+        uint64_t off[kMaxGTerms];
+#pragma unroll
+        for (int t = 0; t < kMaxGTerms; t++) {
+            uint64_t o = 0;
+            if (t < (int)a.nt)
+                for (int k = 0; k < kMaxDep; k++) o += (uint64_t)d[k] * a.t[t].sd[k];
+            off[t] = o;
+        }
+        KeyT best = Ops::sentinel();
+        for (uint32_t c = 0; c < a.K; c++) {
+            KeyT key = ((const KeyT *)a.t[0].ptr)[(uint64_t)c * a.t[0].sc + off[0]];
+#pragma unroll
+            for (int t = 1; t < kMaxGTerms; t++)
+                if (t < (int)a.nt)
+                    key = Ops::add(key, ((const KeyT *)a.t[t].ptr)[(uint64_t)c * a.t[t].sc + off[t]]);
+            best = Ops::min(best, key);
+        }
+        Val v;
+        uint32_t cc;
+        Ops::split(best, a.bits, a.out_shift, v, cc);
+        ((Val *)a.T)[phi] = v;
+        a.A[phi] = (uint16_t)cc;
+    }
+}
+
+// ------------------------------------------------------------------ back-substitution
+// From the last position down: the configuration of v_i is A_i at the
+// already-chosen configurations of D(i) (every member of D(i) is later in the
+// sequence).  Single thread; n dependent reads.
+template <typename KeyT>
+__global__ void k_backtrack(const BacktrackDesc *__restrict__ bt, uint32_t n, const void *Tlast,
+                            uint32_t *__restrict__ cfg, SearchOut *out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    uint32_t status = 0;
+    for (int i = (int)n - 1; i >= 0; i--) {
+        const BacktrackDesc d = bt[i];
+        uint64_t idx = 0;
+        for (uint32_t k = 0; k < d.m; k++) idx += (uint64_t)cfg[d.dig[k]] * d.stride[k];
+        cfg[d.vi] = d.A[idx];
+    }
+    out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
+    out->status = status;
+}
+
+// ------------------------------------------------------------------ fingerprints (tests)
+struct FingerArgs {
+    const void *T;
+    const uint16_t *A;
+    uint64_t N;
+    uint32_t m, out_shift;
+    uint32_t rad[kMaxDep];
+    uint64_t cstride[kMaxDep];
+    unsigned long long *out;
+};
+
+__device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+template <typename KeyT>
+__global__ void k_fingerprint(FingerArgs a) {
+    using Val = typename KeyOps<KeyT>::Val;
+    uint64_t st = 0, sa = 0;
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < a.N;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        uint64_t x = t, canon = 0;
+        for (int k = (int)a.m - 1; k >= 0; k--) {
+            canon += (x % a.rad[k]) * a.cstride[k];
+            x /= a.rad[k];
+        }
+        uint64_t h = splitmix64_mix(canon);
+        st += splitmix64_mix(h ^ (KeyOps<KeyT>::val_to_u64(((const Val *)a.T)[t]) >> a.out_shift));
+        sa += splitmix64_mix(h ^ (uint64_t)a.A[t]);
+    }
+    __shared__ uint64_t red[2][256];
+    red[0][threadIdx.x] = st;
+    red[1][threadIdx.x] = sa;
+    __syncthreads();
+    for (uint32_t s = blockDim.x / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) {
+            red[0][threadIdx.x] += red[0][threadIdx.x + s];
+            red[1][threadIdx.x] += red[1][threadIdx.x + s];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        atomicAdd(a.out, (unsigned long long)red[0][0]);
+        atomicAdd(a.out + 1, (unsigned long long)red[1][0]);
+    }
+}
+
+// ------------------------------------------------------------------ runtime
+namespace pase {
+
+struct DeviceState {
+    void *ws = nullptr;
+    uint64_t ws_bytes = 0;
+    bool owned = false;
+    void *lent = nullptr;
+    uint64_t lent_bytes = 0;
+    void *pinned = nullptr;
+    uint64_t pinned_bytes = 0;
+    std::vector<hipEvent_t> ev;
+    hipStream_t last_stream = nullptr;
+};
+
+#define HIPCHK(x)                                                                              \
+    do {                                                                                       \
+        hipError_t e_ = (x);                                                                   \
+        if (e_ != hipSuccess)                                                                  \
+            return fail(g, PASE_ERR_HIP, std::string(#x) + ": " + hipGetErrorString(e_));      \
+    } while (0)
+
+void device_release(pase_graph_t g) {
+    DeviceState *d = g->dev;
+    if (!d) return;
+    if (d->owned && d->ws) (void)hipFree(d->ws);
+    if (d->pinned) (void)hipHostFree(d->pinned);
+    for (auto e : d->ev) (void)hipEventDestroy(e);
+    delete d;
+    g->dev = nullptr;
+}
+
+static DeviceState *state(pase_graph_t g) {
+    if (!g->dev) g->dev = new DeviceState();
+    return g->dev;
+}
+
+pase_status device_set_workspace(pase_graph_t g, void *ptr, uint64_t bytes) {
+    DeviceState *d = state(g);
+    d->lent = ptr;
+    d->lent_bytes = ptr ? bytes : 0;
+    g->searched = false;
+    return PASE_OK;
+}
+
+static pase_status ensure_memory(pase_graph_t g, char **ws) {
+    DeviceState *d = state(g);
+    const uint64_t need = g->plan.total;
+    if (d->lent) {
+        if (d->lent_bytes < need)
+            return fail(g, PASE_ERR_OUT_OF_MEMORY, "lent workspace smaller than pase_workspace_size");
+        *ws = (char *)d->lent;
+    } else {
+        if (!d->owned || d->ws_bytes < need) {
+            if (d->owned && d->ws) HIPCHK(hipFree(d->ws));
+            d->ws = nullptr;
+            d->owned = false;
+            if (hipMalloc(&d->ws, need) != hipSuccess) {
+                (void)hipGetLastError();
+                d->ws = nullptr;
+                return fail(g, PASE_ERR_OUT_OF_MEMORY, "device allocation of the workspace failed");
+            }
+            d->owned = true;
+            d->ws_bytes = need;
+        }
+        *ws = (char *)d->ws;
+    }
+    const uint64_t pin_need = g->plan.off_cfg;
+    if (d->pinned_bytes < pin_need || !d->pinned) {
+        if (d->pinned) HIPCHK(hipHostFree(d->pinned));
+        d->pinned = nullptr;
+        HIPCHK(hipHostMalloc(&d->pinned, std::max<uint64_t>(pin_need, 4096)));
+        d->pinned_bytes = std::max<uint64_t>(pin_need, 4096);
+    }
+    return PASE_OK;
+}
+
+// One vertex's launch description, resolved against the workspace base.
+template <typename KeyT>
+struct Launch {
+    PrepArgs prep;
+    bool rows = false;
+    RowsArgs ra;
+    GenericArgs ga;
+    ReduceArgs red;
+};
+
+static uint32_t plan_digit(const VPlan &vp, int vertex) {
+    for (size_t k = 0; k < vp.layout.size(); k++)
+        if (vp.layout[k] == vertex) return (uint32_t)k;
+    return ~0u;
+}
+
+// Strides with which consumer position i reads table T_j: (stride of v_i, per plan digit).
+static void lookup_strides(const Plan &P, int i, int j, uint32_t &sc, uint32_t sd[kMaxDep]) {
+    const VPlan &vi = P.v[i], &vj = P.v[j];
+    sc = 0;
+    for (int k = 0; k < kMaxDep; k++) sd[k] = 0;
+    for (size_t k = 0; k < vj.layout.size(); k++) {
+        int u = vj.layout[k];
+        if (u == vi.vi) sc = (uint32_t)vj.stride[k];
+        else sd[plan_digit(vi, u)] = (uint32_t)vj.stride[k];
+    }
+}
+
+// Largest element index a strided read can reach: (K-1)*sc + sum (radix-1)*stride.
+static uint64_t max_index(uint32_t K, uint32_t sc, const uint32_t *sd, const uint32_t *rad, int m) {
+    uint64_t x = (uint64_t)(K - 1) * sc;
+    for (int k = 0; k < m; k++) x += (uint64_t)(rad[k] - 1) * sd[k];
+    return x;
+}
+
+template <typename KeyT>
+static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &out,
+                                   std::vector<Contrib> &contrib) {
+    const Plan &P = g->plan;
+    const int n = (int)P.v.size();
+    out.assign(n, Launch<KeyT>());
+    contrib.clear();
+    KeyT *blocks = (KeyT *)(ws + P.off_block);
+    const uint64_t *ovedge = (const uint64_t *)(ws + P.off_ovedge);
+    for (int i = 0; i < n; i++) {
+        const VPlan &vp = P.v[i];
+        Launch<KeyT> &L = out[i];
+        std::memset(&L.prep, 0, sizeof L.prep);
+        L.prep.vi = (uint32_t)vp.vi;
+        L.prep.K = vp.K;
+        L.prep.bits = vp.bits;
+        uint32_t rad[kMaxDep];
+        for (size_t k = 0; k < vp.layout.size(); k++) rad[k] = g->K[vp.layout[k]];
+        const int m = (int)vp.layout.size();
+        bool bounds_ok = true;
+        auto other_of = [&](int e) {
+            return (int)g->E[e].src == vp.vi ? (int)g->E[e].dst : (int)g->E[e].src;
+        };
+        auto edge_contrib = [&](int e, uint32_t dig) {
+            Contrib c;
+            std::memset(&c, 0, sizeof c);
+            bool is_src = (int)g->E[e].src == vp.vi;
+            if (g->overridden) {
+                c.kind = kContribTable;
+                c.raw_u64 = 1;
+                c.ptr = ovedge + g->ov_edge_off[e];
+                uint32_t Kd = g->K[g->E[e].dst];
+                if (is_src) { c.sc = Kd; c.sd[dig] = 1; }
+                else { c.sc = 1; c.sd[dig] = Kd; }
+                if (max_index(vp.K, c.sc, c.sd, rad, m) >= (uint64_t)g->K[g->E[e].src] * Kd)
+                    bounds_ok = false;
+            } else {
+                c.kind = kContribEdge;
+                c.edge = (uint32_t)e;
+                c.dig = dig;
+                c.vi_is_src = is_src;
+            }
+            contrib.push_back(c);
+        };
+        auto table_contrib = [&](const TermRef &t) {
+            Contrib c;
+            std::memset(&c, 0, sizeof c);
+            c.kind = kContribTable;
+            c.ptr = ws + P.off_T + P.v[t.j].T_off;
+            lookup_strides(P, i, t.j, c.sc, c.sd);
+            // the prep block only feeds digits of the lookup, so every index stays inside T_j
+            if (max_index(vp.K, c.sc, c.sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
+            contrib.push_back(c);
+        };
+        auto layer_contrib = [&]() {
+            Contrib c;
+            std::memset(&c, 0, sizeof c);
+            c.kind = kContribLayer;
+            contrib.push_back(c);
+        };
+        uint64_t boff = 0;
+        auto add_block = [&](const std::vector<int> &pre, int post, uint32_t ld, uint32_t cb) -> int {
+            Block &bk = L.prep.blk[L.prep.nblocks];
+            std::memset(&bk, 0, sizeof bk);
+            bk.npre = (uint32_t)pre.size();
+            uint64_t el = 1;
+            for (size_t k = 0; k < pre.size(); k++) {
+                bk.pre[k] = plan_digit(vp, pre[k]);
+                bk.prerad[k] = g->K[pre[k]];
+                el *= g->K[pre[k]];
+            }
+            bk.post = post >= 0 ? (int32_t)plan_digit(vp, post) : -1;
+            bk.postrad = post >= 0 ? g->K[post] : 1;
+            bk.ld = ld;
+            bk.elems = el * vp.K * ld;
+            bk.out_off = boff;
+            boff += (bk.elems + 31) / 32 * 32;
+            bk.c_begin = cb;
+            bk.c_end = (uint32_t)contrib.size();
+            L.prep.total += bk.elems;
+            return (int)L.prep.nblocks++;
+        };
+        if (vp.kernel == kRows) {
+            // column block B over (O..., c, z): everything not touching a row digit
+            std::vector<int> OZ = vp.O;
+            OZ.push_back(vp.z);
+            auto in_oz = [&](int u) { return std::find(OZ.begin(), OZ.end(), u) != OZ.end(); };
+            uint32_t cb = (uint32_t)contrib.size();
+            layer_contrib();
+            for (int e : vp.edges)
+                if (in_oz(other_of(e))) edge_contrib(e, plan_digit(vp, other_of(e)));
+            for (const auto &t : vp.terms) {
+                bool all = true;
+                for (int u : t.dig) all &= in_oz(u);
+                if (all) table_contrib(t);
+            }
+            add_block(vp.O, vp.z, vp.ldz, cb);
+            RowsArgs &ra = L.ra;
+            std::memset(&ra, 0, sizeof ra);
+            ra.B = blocks + L.prep.blk[0].out_off;
+            // one-digit row blocks E_w, w in R
+            for (size_t rk = 0; rk < vp.R.size(); rk++) {
+                int w = vp.R[rk];
+                cb = (uint32_t)contrib.size();
+                for (int e : vp.edges)
+                    if (other_of(e) == w) edge_contrib(e, plan_digit(vp, w));
+                for (const auto &t : vp.terms)
+                    if (t.dig.size() == 1 && t.dig[0] == w) table_contrib(t);
+                if (contrib.size() == cb) continue;
+                int b = add_block({}, w, g->K[w], cb);
+                ATerm &at = ra.a[ra.na++];
+                at.ptr = blocks + L.prep.blk[b].out_off;
+                at.sc = g->K[w];
+                at.bytes = (uint32_t)(L.prep.blk[b].elems * sizeof(KeyT));
+                at.sdR[rk] = 1;
+            }
+            // lookups touching a row digit with two or more digits: read in the kernel
+            for (const auto &t : vp.terms) {
+                if (t.dig.size() < 2) continue;
+                bool touches = false;
+                for (int u : t.dig) touches |= std::count(vp.R.begin(), vp.R.end(), u) > 0;
+                if (!touches) continue;
+                if (ra.na >= (uint32_t)kMaxATerms) return fail(g, PASE_ERR_INTERNAL, "row terms");
+                ATerm &at = ra.a[ra.na++];
+                uint32_t sc, sd[kMaxDep];
+                lookup_strides(P, i, t.j, sc, sd);
+                if (max_index(vp.K, sc, sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
+                at.ptr = ws + P.off_T + P.v[t.j].T_off;
+                at.sc = sc;
+                at.bytes = (uint32_t)(P.v[t.j].N * 8);
+                // plan digits: 0 = z, 1..|O| = O, then R
+                for (size_t k = 0; k < vp.O.size(); k++) at.sdO[k] = sd[1 + k];
+                for (size_t k = 0; k < vp.R.size(); k++) at.sdR[k] = sd[1 + vp.O.size() + k];
+            }
+            ra.ldz = vp.ldz;
+            ra.Kz = g->K[vp.z];
+            ra.K = vp.K;
+            ra.bits = vp.bits;
+            ra.MO = (uint32_t)vp.MO;
+            ra.MR = (uint32_t)vp.MR;
+            ra.tiles_per_o = (uint32_t)((vp.MR + 63) / 64);
+            ra.nchunks = vp.nchunks;
+            ra.nsplit = vp.nsplit;
+            ra.cper = vp.cper;
+            ra.nO = (uint32_t)vp.O.size();
+            ra.nR = (uint32_t)vp.R.size();
+            for (size_t k = 0; k < vp.O.size(); k++) ra.radO[k] = g->K[vp.O[k]];
+            for (size_t k = 0; k < vp.R.size(); k++) ra.radR[k] = g->K[vp.R[k]];
+            ra.T = ws + P.off_T + vp.T_off;
+            ra.A = (uint16_t *)(ws + P.off_A + vp.A_off);
+            ra.partial = ws + P.off_partial;
+            ra.N = vp.N;
+            ra.out_shift = vp.out_shift;
+            ra.total_tiles = (uint64_t)vp.nsplit * vp.nchunks * vp.MO * ra.tiles_per_o;
+            uint64_t nbk = (ra.total_tiles + 3) / 4;
+            nbk = (nbk + 7) / 8 * 8;
+            if (nbk > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "grid too large");
+            ra.nblocks_launched = (uint32_t)nbk;
+            L.rows = true;
+            if (vp.nsplit > 1) {
+                L.red.partial = ra.partial;
+                L.red.T = ra.T;
+                L.red.A = ra.A;
+                L.red.N = vp.N;
+                L.red.nsplit = vp.nsplit;
+                L.red.bits = vp.bits;
+                L.red.out_shift = vp.out_shift;
+            }
+        } else {
+            GenericArgs &ga = L.ga;
+            std::memset(&ga, 0, sizeof ga);
+            uint32_t cb = (uint32_t)contrib.size();
+            layer_contrib();
+            for (const auto &t : vp.terms)
+                if (t.dig.empty()) table_contrib(t);
+            int b0 = add_block({}, -1, 1, cb);
+            GTerm &g0 = ga.t[ga.nt++];
+            g0.ptr = blocks + L.prep.blk[b0].out_off;
+            g0.sc = 1;
+            for (int w : vp.D) {
+                cb = (uint32_t)contrib.size();
+                for (int e : vp.edges)
+                    if (other_of(e) == w) edge_contrib(e, plan_digit(vp, w));
+                for (const auto &t : vp.terms)
+                    if (t.dig.size() == 1 && t.dig[0] == w) table_contrib(t);
+                if (contrib.size() == cb) continue;
+                int b = add_block({}, w, g->K[w], cb);
+                GTerm &gt = ga.t[ga.nt++];
+                gt.ptr = blocks + L.prep.blk[b].out_off;
+                gt.sc = g->K[w];
+                gt.sd[plan_digit(vp, w)] = 1;
+            }
+            for (const auto &t : vp.terms) {
+                if (t.dig.size() < 2) continue;
+                if (ga.nt >= (uint32_t)kMaxGTerms)
+                    return fail(g, PASE_ERR_TOO_LARGE, "too many table lookups for one vertex");
+                GTerm &gt = ga.t[ga.nt++];
+                gt.ptr = ws + P.off_T + P.v[t.j].T_off;
+                lookup_strides(P, i, t.j, gt.sc, gt.sd);
+                if (max_index(vp.K, gt.sc, gt.sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
+            }
+            ga.m = (uint32_t)vp.layout.size();
+            ga.K = vp.K;
+            ga.bits = vp.bits;
+            for (size_t k = 0; k < vp.layout.size(); k++) ga.rad[k] = g->K[vp.layout[k]];
+            ga.T = ws + P.off_T + vp.T_off;
+            ga.A = (uint16_t *)(ws + P.off_A + vp.A_off);
+            ga.N = vp.N;
+            ga.out_shift = vp.out_shift;
+        }
+        if (boff > vp.block_elems) return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
+        if (!bounds_ok) return fail(g, PASE_ERR_INTERNAL, "a table lookup would leave its table");
+        if (vp.nsplit > 1 && (uint64_t)vp.nsplit * vp.N * sizeof(KeyT) > P.partial_bytes)
+            return fail(g, PASE_ERR_INTERNAL, "split scratch overflow");
+    }
+    if (contrib.size() > P.contrib_count) return fail(g, PASE_ERR_INTERNAL, "contribution overflow");
+    return PASE_OK;
+}
+
+template <typename KeyT, int TZ>
+static void launch_rows_tz(const RowsArgs &ra, hipStream_t s) {
+    dim3 grid(ra.nblocks_launched), block(256);
+    if constexpr (std::is_same<KeyT, double>::value) {
+        switch (ra.na) {
+        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 0>), grid, block, 0, s, ra); break;
+        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 1>), grid, block, 0, s, ra); break;
+        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 2>), grid, block, 0, s, ra); break;
+        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 3>), grid, block, 0, s, ra); break;
+        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 4>), grid, block, 0, s, ra); break;
+        }
+    } else {
+        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, -1>), grid, block, 0, s, ra);
+    }
+}
+
+template <typename KeyT>
+static bool launch_rows(const RowsArgs &ra, uint32_t TZ, hipStream_t s) {
+    switch (TZ) {
+    case 8: launch_rows_tz<KeyT, 8>(ra, s); return true;
+    case 12: launch_rows_tz<KeyT, 12>(ra, s); return true;
+    case 16: launch_rows_tz<KeyT, 16>(ra, s); return true;
+    case 20: launch_rows_tz<KeyT, 20>(ra, s); return true;
+    case 21: launch_rows_tz<KeyT, 21>(ra, s); return true;
+    case 24: launch_rows_tz<KeyT, 24>(ra, s); return true;
+    case 28: launch_rows_tz<KeyT, 28>(ra, s); return true;
+    case 30: launch_rows_tz<KeyT, 30>(ra, s); return true;
+    case 32: launch_rows_tz<KeyT, 32>(ra, s); return true;
+    default: return false;
+    }
+}
+
+static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) {
+    uint64_t b = (n + block - 1) / block;
+    return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, cap));
+}
+
+template <typename KeyT>
+static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t *min_cost, uint32_t *cfg) {
+    DeviceState *d = g->dev;
+    const Plan &P = g->plan;
+    const int n = (int)P.v.size();
+    const size_t nv = g->V.size(), ne = g->E.size();
+
+    std::vector<Launch<KeyT>> launches;
+    std::vector<Contrib> contrib;
+    pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
+    if (st != PASE_OK) return st;
+
+    // ---- constant region image (one host-to-device copy)
+    char *img = (char *)d->pinned;
+    std::memset(img, 0, P.off_cfg);
+    uint64_t off = 0;
+    std::vector<DevVertex> dvs(nv);
+    uint64_t loff = 0;
+    for (size_t v = 0; v < nv; v++) {
+        std::memcpy(img + P.off_ex + off, g->ex[v].data(), g->ex[v].size());
+        DevVertex &x = dvs[v];
+        x.ex_off = off;
+        x.L_off = loff;
+        x.flops = g->flops[v];
+        x.keep_n = g->keep_n[v];
+        x.K = g->K[v];
+        x.ndims = g->V[v].ndims;
+        x.reduce_mask = g->V[v].reduce_mask;
+        off += g->ex[v].size();
+        loff += g->K[v];
+    }
+    std::memcpy(img + P.off_vert, dvs.data(), nv * sizeof(DevVertex));
+    std::vector<DevEdge> des(ne);
+    for (size_t e = 0; e < ne; e++) {
+        DevEdge &x = des[e];
+        std::memset(&x, 0, sizeof x);
+        x.src = g->E[e].src;
+        x.dst = g->E[e].dst;
+        x.rank = g->E[e].rank;
+        for (uint32_t k = 0; k < kMaxDims; k++) {
+            x.sdim[k] = (int8_t)(k < x.rank ? g->E[e].src_dim[k] : -1);
+            x.ddim[k] = (int8_t)(k < x.rank ? g->E[e].dst_dim[k] : -1);
+        }
+        x.elems = g->E[e].elems;
+    }
+    if (ne) std::memcpy(img + P.off_edge, des.data(), ne * sizeof(DevEdge));
+    if (g->overridden) {
+        std::memcpy(img + P.off_L, g->ov_layer.data(), g->ov_layer.size() * 8);
+        if (!g->ov_edge.empty()) std::memcpy(img + P.off_ovedge, g->ov_edge.data(), g->ov_edge.size() * 8);
+    }
+    std::memcpy(img + P.off_contrib, contrib.data(), contrib.size() * sizeof(Contrib));
+    std::vector<BacktrackDesc> bt(n);
+    for (int i = 0; i < n; i++) {
+        const VPlan &vp = P.v[i];
+        BacktrackDesc &b = bt[i];
+        std::memset(&b, 0, sizeof b);
+        b.A = (const uint16_t *)(ws + P.off_A + vp.A_off);
+        b.vi = (uint32_t)vp.vi;
+        b.m = (uint32_t)vp.layout.size();
+        for (size_t k = 0; k < vp.layout.size(); k++) {
+            b.dig[k] = (uint32_t)vp.layout[k];
+            b.stride[k] = vp.stride[k];
+        }
+    }
+    std::memcpy(img + P.off_bt, bt.data(), n * sizeof(BacktrackDesc));
+    HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
+
+    const DevVertex *dV = (const DevVertex *)(ws + P.off_vert);
+    const DevEdge *dE = (const DevEdge *)(ws + P.off_edge);
+    const uint8_t *dex = (const uint8_t *)(ws + P.off_ex);
+    uint64_t *dL = (uint64_t *)(ws + P.off_L);
+    const Contrib *dC = (const Contrib *)(ws + P.off_contrib);
+    KeyT *dB = (KeyT *)(ws + P.off_block);
+    uint32_t launches_n = 0;
+    if (!g->overridden) {
+        hipLaunchKernelGGL(k_layer_costs, dim3(grid_for(loff)), dim3(256), 0, s, dV, (uint32_t)nv, dex, dL,
+                           loff, g->r);
+        launches_n++;
+    }
+    // per-vertex contribution ranges were recorded relative to the global list
+    if (g->profile && d->ev.size() < 2 * (size_t)n) {
+        for (size_t k = d->ev.size(); k < 2 * (size_t)n; k++) {
+            hipEvent_t e;
+            HIPCHK(hipEventCreate(&e));
+            d->ev.push_back(e);
+        }
+    }
+    for (int i = 0; i < n; i++) {
+        Launch<KeyT> &L = launches[i];
+        const VPlan &vp = P.v[i];
+        hipLaunchKernelGGL((k_prep<KeyT>), dim3(grid_for(L.prep.total)), dim3(256), 0, s, L.prep, dV, dE, dex,
+                           (const uint64_t *)dL, dC, dB, g->r);
+        launches_n++;
+        // with profiling, events bracket exactly the fill kernel of this vertex
+        if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i], s));
+        if (L.rows) {
+            if (!launch_rows<KeyT>(L.ra, vp.TZ, s)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+        } else {
+            hipLaunchKernelGGL((k_fill_generic<KeyT>), dim3(grid_for(vp.N, 256, 65535)), dim3(256), 0, s, L.ga);
+        }
+        launches_n++;
+        if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i + 1], s));
+        if (L.rows && vp.nsplit > 1) {
+            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(grid_for(vp.N)), dim3(256), 0, s, L.red);
+            launches_n++;
+        }
+    }
+    uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
+    SearchOut *dout = (SearchOut *)(ws + P.off_out);
+    hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
+                       (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+    launches_n++;
+    HIPCHK(hipGetLastError());
+    char *host_out = img;   // reuse the staging buffer after the upload has been consumed
+    HIPCHK(hipStreamSynchronize(s));
+    HIPCHK(hipMemcpyAsync(host_out, dout, sizeof(SearchOut), hipMemcpyDeviceToHost, s));
+    HIPCHK(hipMemcpyAsync(host_out + sizeof(SearchOut), dcfg, nv * 4, hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    SearchOut so;
+    std::memcpy(&so, host_out, sizeof so);
+    if (so.status) return fail(g, PASE_ERR_INTERNAL, "device consistency check failed");
+    *min_cost = so.min_cost;
+    std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
+
+    g->stats.launches = launches_n;
+    g->stats.fill_ms = g->stats.rows_fill_ms = 0;
+    g->stats.rows_launches = 0;
+    if (g->profile) {
+        for (int i = 0; i < n; i++) {
+            float ms = 0;
+            HIPCHK(hipEventElapsedTime(&ms, d->ev[2 * i], d->ev[2 * i + 1]));
+            g->stats.fill_ms += ms;
+            if (launches[i].rows) { g->stats.rows_fill_ms += ms; g->stats.rows_launches++; }
+        }
+    }
+    return PASE_OK;
+}
+
+pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
+    auto t0 = std::chrono::steady_clock::now();
+    pase_status st;
+    uint32_t kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    char *ws = nullptr;
+    st = ensure_memory(g, &ws);
+    if (st != PASE_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    g->searched = false;
+    uint64_t mc = 0;
+    std::vector<uint32_t> out(g->V.size());
+    st = kt == 0 ? run_search<double>(g, s, ws, &mc, out.data()) : run_search<uint64_t>(g, s, ws, &mc, out.data());
+    if (st != PASE_OK) return st;
+    *min_cost = mc;
+    std::memcpy(cfg, out.data(), out.size() * 4);
+    g->key_type = kt;
+    g->searched = true;
+    g->dev->last_stream = s;
+    const Plan &P = g->plan;
+    g->stats.cells = P.cells;
+    g->stats.table_entries = P.entries;
+    g->stats.workspace_bytes = P.total;
+    g->stats.max_dep = P.max_dep;
+    g->stats.key_type = kt;
+    g->stats.rows_vertices = P.rows_vertices;
+    g->stats.rows_cells = P.rows_cells;
+    g->stats.wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return PASE_OK;
+}
+
+static char *workspace(pase_graph_t g) {
+    DeviceState *d = g->dev;
+    return d->lent ? (char *)d->lent : (char *)d->ws;
+}
+
+pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *cost, uint32_t *arg) {
+    const Plan &P = g->plan;
+    char *ws = workspace(g);
+    const VPlan &vp = P.v[pos];
+    uint64_t raw = 0;
+    uint16_t a = 0;
+    HIPCHK(hipMemcpy(&raw, ws + P.off_T + vp.T_off + idx * 8, 8, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(&a, ws + P.off_A + vp.A_off + idx * 2, 2, hipMemcpyDeviceToHost));
+    // tables are stored in their reader's key space (x 2^out_shift)
+    if (g->key_type == 0) {
+        double dv;
+        std::memcpy(&dv, &raw, 8);
+        *cost = ((uint64_t)dv) >> vp.out_shift;
+    } else {
+        *cost = raw >> vp.out_shift;
+    }
+    *arg = a;
+    return PASE_OK;
+}
+
+pase_status device_fingerprint(pase_graph_t g, int pos, uint64_t *fpT, uint64_t *fpA) {
+    const Plan &P = g->plan;
+    char *ws = workspace(g);
+    const VPlan &vp = P.v[pos];
+    FingerArgs fa;
+    std::memset(&fa, 0, sizeof fa);
+    fa.T = ws + P.off_T + vp.T_off;
+    fa.A = (const uint16_t *)(ws + P.off_A + vp.A_off);
+    fa.N = vp.N;
+    fa.m = (uint32_t)vp.layout.size();
+    fa.out_shift = vp.out_shift;
+    // canonical order: D ascending, first digit slowest
+    std::vector<uint64_t> cst(vp.D.size(), 1);
+    for (int k = (int)vp.D.size() - 2; k >= 0; k--) cst[k] = cst[k + 1] * g->K[vp.D[k + 1]];
+    for (size_t k = 0; k < vp.layout.size(); k++) {
+        fa.rad[k] = g->K[vp.layout[k]];
+        size_t at = std::lower_bound(vp.D.begin(), vp.D.end(), vp.layout[k]) - vp.D.begin();
+        fa.cstride[k] = cst[at];
+    }
+    unsigned long long *dout = nullptr;
+    HIPCHK(hipMalloc(&dout, 16));
+    HIPCHK(hipMemset(dout, 0, 16));
+    fa.out = dout;
+    uint32_t grid = grid_for(vp.N, 256, 1024);
+    if (g->key_type == 0) hipLaunchKernelGGL(k_fingerprint<double>, dim3(grid), dim3(256), 0, 0, fa);
+    else hipLaunchKernelGGL(k_fingerprint<uint64_t>, dim3(grid), dim3(256), 0, 0, fa);
+    unsigned long long h[2];
+    hipError_t e = hipMemcpy(h, dout, 16, hipMemcpyDeviceToHost);
+    (void)hipFree(dout);
+    HIPCHK(e);
+    *fpT = h[0];
+    *fpA = h[1];
+    return PASE_OK;
+}
+
+pase_status device_layer_costs(pase_graph_t g, uint32_t v, uint64_t *out) {
+    const Plan &P = g->plan;
+    char *ws = workspace(g);
+    uint64_t loff = 0;
+    for (uint32_t u = 0; u < v; u++) loff += g->K[u];
+    HIPCHK(hipMemcpy(out, ws + P.off_L + loff * 8, (size_t)g->K[v] * 8, hipMemcpyDeviceToHost));
+    return PASE_OK;
+}
+
+pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
+    const Plan &P = g->plan;
+    char *ws = workspace(g);
+    uint64_t n = (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+    if (g->overridden) {
+        HIPCHK(hipMemcpy(out, ws + P.off_ovedge + g->ov_edge_off[e] * 8, n * 8, hipMemcpyDeviceToHost));
+        return PASE_OK;
+    }
+    uint64_t *tmp = nullptr;
+    HIPCHK(hipMalloc(&tmp, n * 8));
+    hipLaunchKernelGGL(k_edge_costs, dim3(grid_for(n)), dim3(256), 0, 0, (const DevVertex *)(ws + P.off_vert),
+                       (const DevEdge *)(ws + P.off_edge), e, (const uint8_t *)(ws + P.off_ex), tmp, g->r);
+    hipError_t err = hipMemcpy(out, tmp, n * 8, hipMemcpyDeviceToHost);
+    (void)hipFree(tmp);
+    HIPCHK(err);
+    return PASE_OK;
+}
+
+}  // namespace pase

@@ -1,0 +1,681 @@
+// Host side of libpase: graph validation, configuration enumeration, the
+// GenerateSeq vertex order (Fig. 3), connected sets / dependent sets /
+// connected subsets (Sec. III-B), per-vertex DP plans and the device memory
+// layout.  No HIP calls here: everything is pure host computation so it can be
+// exercised without a GPU.
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+
+#include "internal.h"
+
+using namespace pase;
+
+namespace pase {
+
+pase_status fail(pase_graph_t g, pase_status st, const std::string &msg) {
+    if (g) g->err = msg;
+    return st;
+}
+
+static bool mul_ok(uint64_t a, uint64_t b, uint64_t *out) { return !__builtin_mul_overflow(a, b, out); }
+static bool add_ok(uint64_t a, uint64_t b, uint64_t *out) { return !__builtin_add_overflow(a, b, out); }
+static uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+static uint32_t bits_for(uint32_t K) {
+    uint32_t b = 0;
+    while ((1u << b) < K) b++;
+    return b;
+}
+
+// Key type: fp64 when every key (cost * 2^bits + c) of every vertex stays
+// below 2^53 so that double arithmetic on them is exact integer arithmetic;
+// otherwise uint64 when it stays below 2^64; otherwise overflow.
+uint32_t choose_key_type(pase_graph_t g, pase_status *st) {
+    *st = PASE_OK;
+    uint64_t bound = 0;
+    size_t nv = g->V.size(), ne = g->E.size();
+    for (size_t v = 0; v < nv; v++) {
+        uint64_t m = g->maxL[v];
+        if (g->overridden) {
+            m = 0;
+            for (uint32_t c = 0; c < g->K[v]; c++) m = std::max(m, g->ov_layer[g->ov_layer_off[v] + c]);
+        }
+        if (!add_ok(bound, m, &bound)) { *st = PASE_ERR_OVERFLOW; return 0; }
+    }
+    for (size_t e = 0; e < ne; e++) {
+        uint64_t m = g->maxR[e];
+        if (g->overridden) {
+            m = 0;
+            uint64_t n = (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+            for (uint64_t k = 0; k < n; k++) m = std::max(m, g->ov_edge[g->ov_edge_off[e] + k]);
+        }
+        if (!add_ok(bound, m, &bound)) { *st = PASE_ERR_OVERFLOW; return 0; }
+    }
+    uint32_t bmax = 0;
+    for (uint32_t k : g->K) bmax = std::max(bmax, bits_for(k));
+    // largest key: bound * 2^bmax + (2^bmax - 1) < (bound + 1) * 2^bmax
+    unsigned __int128 top = ((unsigned __int128)bound + 1) << bmax;
+    if (g->key_mode == 0 && top <= ((unsigned __int128)1 << 53)) return 0;
+    if (top <= ((unsigned __int128)1 << 64)) return 1;
+    *st = PASE_ERR_OVERFLOW;
+    return 0;
+}
+
+}  // namespace pase
+
+// ------------------------------------------------------------------ create / destroy
+extern "C" pase_status pase_graph_create(const pase_vertex_desc *v, uint32_t nv,
+                                         const pase_edge_desc *e, uint32_t ne,
+                                         const pase_cost_params *params, pase_graph_t *out) {
+    if (!v || !out || nv == 0 || (ne > 0 && !e)) return PASE_ERR_INVALID_ARGUMENT;
+    if (nv > (1u << 20) || ne > (1u << 24)) return PASE_ERR_INVALID_ARGUMENT;
+    for (uint32_t i = 0; i < nv; i++) {
+        if (v[i].ndims < 1 || v[i].ndims > kMaxDims) return PASE_ERR_INVALID_ARGUMENT;
+        for (uint32_t k = 0; k < v[i].ndims; k++)
+            if (v[i].size[k] == 0) return PASE_ERR_INVALID_ARGUMENT;
+        if (v[i].reduce_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
+    }
+    for (uint32_t k = 0; k < ne; k++) {
+        const pase_edge_desc &d = e[k];
+        if (d.src >= nv || d.dst >= nv || d.src == d.dst) return PASE_ERR_INVALID_ARGUMENT;
+        if (d.rank > kMaxDims || d.elems == 0) return PASE_ERR_INVALID_ARGUMENT;
+        for (uint32_t t = 0; t < d.rank; t++) {
+            if (d.src_dim[t] < -1 || d.src_dim[t] >= (int32_t)v[d.src].ndims)
+                return PASE_ERR_INVALID_ARGUMENT;
+            if (d.dst_dim[t] < -1 || d.dst_dim[t] >= (int32_t)v[d.dst].ndims)
+                return PASE_ERR_INVALID_ARGUMENT;
+        }
+    }
+    auto *g = new pase_graph_s();
+    g->V.assign(v, v + nv);
+    if (ne) g->E.assign(e, e + ne);
+    if (params) {
+        g->r = params->comm_weight ? params->comm_weight : 8;
+        if (params->seq_rule > 1) { delete g; return PASE_ERR_INVALID_ARGUMENT; }
+        g->seq_rule = params->seq_rule;
+    }
+    g->nbr.assign(nv, {});
+    for (const auto &d : g->E) {
+        g->nbr[d.src].push_back((int)d.dst);
+        g->nbr[d.dst].push_back((int)d.src);
+    }
+    for (auto &l : g->nbr) {
+        std::sort(l.begin(), l.end());
+        l.erase(std::unique(l.begin(), l.end()), l.end());
+    }
+    // weak connectivity (computation graphs are weakly connected, Sec. II)
+    std::vector<char> seen(nv, 0);
+    std::vector<int> stack{0};
+    seen[0] = 1;
+    size_t count = 1;
+    while (!stack.empty()) {
+        int x = stack.back();
+        stack.pop_back();
+        for (int y : g->nbr[x])
+            if (!seen[y]) { seen[y] = 1; count++; stack.push_back(y); }
+    }
+    if (count != nv) { delete g; return PASE_ERR_NOT_CONNECTED; }
+    *out = g;
+    return PASE_OK;
+}
+
+extern "C" void pase_graph_destroy(pase_graph_t g) {
+    if (!g) return;
+    device_release(g);
+    delete g;
+}
+
+extern "C" const char *pase_last_error(pase_graph_t g) { return g ? g->err.c_str() : ""; }
+
+// ------------------------------------------------------------------ planning
+namespace {
+
+// GenerateSeq (Fig. 3): repeatedly sequence the unsequenced vertex with the
+// smallest d-set (ties: lowest vertex id); every member of its d-set absorbs
+// it.  rule 0 keeps a vertex out of its own d-set; rule 1 applies the printed
+// update literally.  The d-set at selection (minus the vertex) is D(i)
+// (Theorem 2).  Bitsets, one per vertex.
+void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector<int>> &Dpos) {
+    const size_t n = g->V.size(), W = (n + 63) / 64;
+    std::vector<uint64_t> d(n * W, 0);
+    auto has = [&](size_t v, size_t u) { return (d[v * W + u / 64] >> (u % 64)) & 1ull; };
+    for (size_t v = 0; v < n; v++)
+        for (int u : g->nbr[v]) d[v * W + u / 64] |= 1ull << (u % 64);
+    std::vector<char> done(n, 0);
+    seq.clear();
+    Dpos.assign(n, {});
+    for (size_t i = 0; i < n; i++) {
+        size_t best = n;
+        int best_sz = 0;
+        for (size_t u = 0; u < n; u++) {
+            if (done[u]) continue;
+            int sz = 0;
+            for (size_t w = 0; w < W; w++) sz += __builtin_popcountll(d[u * W + w]);
+            if (best == n || sz < best_sz) { best = u; best_sz = sz; }
+        }
+        const size_t vi = best;
+        done[vi] = 1;
+        seq.push_back((int)vi);
+        for (size_t u = 0; u < n; u++)
+            if (u != vi && has(vi, u)) Dpos[i].push_back((int)u);
+        for (int v : Dpos[i]) {
+            for (size_t w = 0; w < W; w++) d[(size_t)v * W + w] |= d[vi * W + w];
+            d[(size_t)v * W + vi / 64] &= ~(1ull << (vi % 64));
+            if (g->seq_rule == 0) d[(size_t)v * W + v / 64] &= ~(1ull << (v % 64));
+        }
+    }
+}
+
+const uint32_t kTZ[] = {8, 12, 16, 20, 21, 24, 28, 30, 32};
+
+struct RowsChoice {
+    bool ok = false;
+    double cost = 0;
+    int z = -1;
+    std::vector<int> O, R;
+    uint32_t TZ = 0;
+    uint64_t MO = 1, MR = 1;
+};
+
+}  // namespace
+
+static pase_status build_plan(pase_graph_t g) {
+    const int n = (int)g->V.size();
+    Plan &P = g->plan;
+    P = Plan();
+    std::vector<std::vector<int>> Dpos;
+    generate_seq(g, P.seq, Dpos);
+    P.pos.assign(n, 0);
+    for (int i = 0; i < n; i++) P.pos[P.seq[i]] = i;
+    P.v.assign(n, VPlan());
+
+    std::vector<int> mark(n, -1), comp(n, -1), stack;
+    for (int i = 0; i < n; i++) {
+        VPlan &vp = P.v[i];
+        vp.vi = P.seq[i];
+        vp.K = g->K[vp.vi];
+        vp.bits = bits_for(vp.K);
+        vp.D = Dpos[i];
+        std::sort(vp.D.begin(), vp.D.end());
+        if (vp.D.size() > (size_t)kMaxDep)
+            return fail(g, PASE_ERR_TOO_LARGE, "dependent set larger than PASE_MAX_DEP");
+        P.max_dep = std::max<uint32_t>(P.max_dep, (uint32_t)vp.D.size());
+        vp.N = 1;
+        for (int w : vp.D)
+            if (!mul_ok(vp.N, g->K[w], &vp.N) || vp.N > kMaxTableEntries)
+                return fail(g, PASE_ERR_TOO_LARGE, "a DP table exceeds 2^31 entries");
+        // X(i): reachable from v_i through positions <= i
+        stack.assign(1, vp.vi);
+        mark[vp.vi] = i;
+        std::vector<int> X{vp.vi};
+        while (!stack.empty()) {
+            int x = stack.back();
+            stack.pop_back();
+            for (int y : g->nbr[x])
+                if (P.pos[y] <= i && mark[y] != i) { mark[y] = i; X.push_back(y); stack.push_back(y); }
+        }
+        // S(i): components of X(i) - {v_i} inside positions < i, each represented by
+        // its last position j; every one is a neighbour component of v_i
+        for (int s : g->nbr[vp.vi]) {
+            if (P.pos[s] >= i || comp[s] == i) continue;
+            int jmax = P.pos[s];
+            stack.assign(1, s);
+            comp[s] = i;
+            while (!stack.empty()) {
+                int x = stack.back();
+                stack.pop_back();
+                jmax = std::max(jmax, P.pos[x]);
+                for (int y : g->nbr[x])
+                    if (P.pos[y] < i && comp[y] != i) { comp[y] = i; stack.push_back(y); }
+            }
+            TermRef t;
+            t.j = jmax;
+            bool has_vi = false;
+            for (int u : P.v[jmax].D) {
+                if (u == vp.vi) { has_vi = true; continue; }
+                if (!std::binary_search(vp.D.begin(), vp.D.end(), u))
+                    return fail(g, PASE_ERR_INTERNAL, "D(j) not within D(i) + v_i");
+                t.dig.push_back(u);
+            }
+            if (!has_vi) return fail(g, PASE_ERR_INTERNAL, "v_i missing from D(j)");
+            if (P.v[jmax].consumer != -1) return fail(g, PASE_ERR_INTERNAL, "table read twice");
+            P.v[jmax].consumer = i;
+            vp.terms.push_back(t);
+        }
+        for (size_t k = 0; k < g->E.size(); k++) {
+            const auto &d = g->E[k];
+            int other = (int)d.src == vp.vi ? (int)d.dst : ((int)d.dst == vp.vi ? (int)d.src : -1);
+            if (other >= 0 && P.pos[other] > i) vp.edges.push_back((int)k);
+        }
+        P.cells += vp.N * vp.K;
+        P.entries += vp.N;
+    }
+    for (int i = 0; i + 1 < n; i++) {
+        if (P.v[i].consumer < 0) return fail(g, PASE_ERR_INTERNAL, "table never read");
+        P.v[i].out_shift = P.v[P.v[i].consumer].bits;
+    }
+
+    // ---- kernel choice and T_i layout
+    for (int i = 0; i < n; i++) {
+        VPlan &vp = P.v[i];
+        RowsChoice best;
+        if (g->kernel_mode == 0 && vp.D.size() >= 2) {
+            for (int z : vp.D) {
+                RowsChoice rc;
+                rc.z = z;
+                std::vector<int> O;
+                for (const auto &t : vp.terms)
+                    if (t.dig.size() >= 2 && std::count(t.dig.begin(), t.dig.end(), z))
+                        for (int u : t.dig)
+                            if (u != z) O.push_back(u);
+                std::sort(O.begin(), O.end());
+                O.erase(std::unique(O.begin(), O.end()), O.end());
+                for (int u : vp.D)
+                    if (u != z && !std::binary_search(O.begin(), O.end(), u)) rc.R.push_back(u);
+                rc.O = O;
+                for (int u : rc.O) rc.MO *= g->K[u];
+                for (int u : rc.R) rc.MR *= g->K[u];
+                if (rc.MR < 16) continue;
+                uint32_t na = 0;
+                for (int u : rc.R) {
+                    bool used = false;
+                    for (int e : vp.edges) {
+                        int other = (int)g->E[e].src == vp.vi ? (int)g->E[e].dst : (int)g->E[e].src;
+                        used |= other == u;
+                    }
+                    for (const auto &t : vp.terms) used |= t.dig.size() == 1 && t.dig[0] == u;
+                    na += used;
+                }
+                bool small = true;   // row terms are read with 32-bit buffer offsets
+                for (const auto &t : vp.terms) {
+                    if (t.dig.size() < 2) continue;
+                    bool touches = false;
+                    for (int u : t.dig) touches |= std::binary_search(rc.R.begin(), rc.R.end(), u);
+                    na += touches;
+                    if (touches && P.v[t.j].N * 8 >= (1ull << 31)) small = false;
+                }
+                if (na > (uint32_t)kMaxATerms || !small) continue;
+                const uint32_t Kz = g->K[z];
+                for (uint32_t tz : kTZ) {
+                    uint64_t nch = (Kz + tz - 1) / tz;
+                    if (rc.MO * vp.K * nch * tz > kMaxTableEntries) continue;
+                    double lanes = (double)rc.MO * (double)((rc.MR + 63) / 64 * 64);
+                    double cost = lanes * (double)nch * (2.0 * tz + na + 1) * vp.K;
+                    if (!rc.ok || cost < rc.cost) { rc.ok = true; rc.cost = cost; rc.TZ = tz; }
+                }
+                if (rc.ok && (!best.ok || rc.cost < best.cost)) best = rc;
+            }
+        }
+        if (best.ok) {
+            vp.kernel = kRows;
+            vp.z = best.z;
+            vp.O = best.O;
+            vp.R = best.R;
+            vp.MO = best.MO;
+            vp.MR = best.MR;
+            vp.TZ = best.TZ;
+            vp.nchunks = (g->K[vp.z] + vp.TZ - 1) / vp.TZ;
+            vp.ldz = vp.nchunks * vp.TZ;
+            vp.layout.clear();
+            vp.layout.push_back(vp.z);
+            vp.layout.insert(vp.layout.end(), vp.O.begin(), vp.O.end());
+            vp.layout.insert(vp.layout.end(), vp.R.begin(), vp.R.end());
+            uint64_t tiles_per_o = (vp.MR + 63) / 64;
+            uint64_t waves = vp.MO * tiles_per_o * vp.nchunks;
+            uint64_t want = (4096 + waves - 1) / waves;
+            uint64_t maxs = std::max<uint64_t>(1, vp.K / 16);
+            uint64_t ns = std::min(want, maxs);
+            vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
+            vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
+            P.rows_vertices++;
+            P.rows_cells += vp.N * vp.K;
+        } else {
+            vp.kernel = kGeneric;
+            vp.layout = vp.D;
+            vp.nsplit = 1;
+            vp.cper = vp.K;
+        }
+        vp.stride.assign(vp.layout.size(), 1);
+        for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
+            vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
+    }
+    return PASE_OK;
+}
+
+// Device memory layout: constant region (configurations, vertex/edge
+// descriptors, layer costs, caller-given edge matrices, prep contributions,
+// back-substitution descriptors), outputs, the table arenas and scratch.
+// Cost tables T_i live from their fill to their single reader (or to the end
+// when tables are kept or i is last) and share memory by interval packing;
+// argmin tables A_i all live until back-substitution.
+static pase_status layout_memory(pase_graph_t g) {
+    Plan &P = g->plan;
+    const int n = (int)P.v.size();
+    const uint64_t A = 256;
+    uint64_t off = 0;
+    P.off_ex = off;
+    for (size_t v = 0; v < g->V.size(); v++) off += (uint64_t)g->K[v] * g->V[v].ndims;
+    off = align_up(off, A);
+    P.off_vert = off;
+    off = align_up(off + g->V.size() * sizeof(DevVertex), A);
+    P.off_edge = off;
+    off = align_up(off + std::max<size_t>(1, g->E.size()) * sizeof(DevEdge), A);
+    P.off_L = off;
+    uint64_t sumK = 0;
+    for (uint32_t k : g->K) sumK += k;
+    off = align_up(off + sumK * 8, A);
+    P.off_ovedge = off;
+    if (g->overridden) off = align_up(off + g->ov_edge.size() * 8, A);
+    // contributions: count per vertex (layer + edges + lookups is an upper bound)
+    uint64_t ncontrib = 0;
+    for (const auto &vp : P.v) ncontrib += 1 + vp.edges.size() + vp.terms.size();
+    P.contrib_count = ncontrib;
+    P.off_contrib = off;
+    off = align_up(off + ncontrib * sizeof(Contrib), A);
+    P.off_bt = off;
+    off = align_up(off + n * sizeof(BacktrackDesc), A);
+    P.off_cfg = off;
+    off = align_up(off + g->V.size() * 4, A);
+    P.off_out = off;
+    off = align_up(off + sizeof(SearchOut), A);
+
+    // T arena: interval packing
+    struct Iv { int i, s, e; uint64_t size; };
+    std::vector<Iv> iv;
+    for (int i = 0; i < n; i++) {
+        int end = (g->keep_tables || i == n - 1) ? n : P.v[i].consumer;
+        iv.push_back({i, i, end, align_up(P.v[i].N * 8, A)});
+    }
+    std::vector<int> order(n);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return iv[a].size > iv[b].size; });
+    std::vector<int> placed;
+    uint64_t tbytes = 0;
+    for (int k : order) {
+        std::vector<std::pair<uint64_t, uint64_t>> busy;
+        for (int q : placed)
+            if (iv[q].s <= iv[k].e && iv[k].s <= iv[q].e)
+                busy.push_back({P.v[iv[q].i].T_off, P.v[iv[q].i].T_off + iv[q].size});
+        std::sort(busy.begin(), busy.end());
+        uint64_t cand = 0;
+        for (const auto &b : busy) {
+            if (cand + iv[k].size <= b.first) break;
+            cand = std::max(cand, b.second);
+        }
+        P.v[iv[k].i].T_off = cand;
+        tbytes = std::max(tbytes, cand + iv[k].size);
+        placed.push_back(k);
+    }
+    P.T_bytes = tbytes;
+    P.off_T = off;
+    off = align_up(off + tbytes, A);
+    uint64_t abytes = 0;
+    for (auto &vp : P.v) { vp.A_off = abytes; abytes += align_up(vp.N * 2, A); }
+    P.A_bytes = abytes;
+    P.off_A = off;
+    off = align_up(off + abytes, A);
+    // block scratch
+    uint64_t bmax = 0, pmax = 0;
+    for (auto &vp : P.v) {
+        uint64_t e = 0;
+        if (vp.kernel == kRows) {
+            e += align_up(vp.MO * vp.K * vp.ldz, 32);
+            for (int u : vp.R) e += align_up((uint64_t)vp.K * g->K[u], 32);
+            if (vp.nsplit > 1) pmax = std::max(pmax, (uint64_t)vp.nsplit * vp.N * 8);
+        } else {
+            e += align_up(vp.K, 32);
+            for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
+        }
+        vp.block_elems = e;
+        bmax = std::max(bmax, e);
+    }
+    P.block_bytes = bmax * 8;
+    P.off_block = off;
+    off = align_up(off + P.block_bytes, A);
+    P.partial_bytes = pmax;
+    P.off_partial = off;
+    off = align_up(off + pmax, A);
+    P.total = off;
+    if (P.total > g->mem_budget)
+        return fail(g, PASE_ERR_TOO_LARGE, "device memory need exceeds the memory budget");
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
+    if (!g) return PASE_ERR_INVALID_ARGUMENT;
+    if (p == 0 || (p & (p - 1)) || p > (1u << 16))
+        return fail(g, PASE_ERR_INVALID_ARGUMENT, "p must be a power of two <= 65536");
+    g->enumerated = g->planned = g->searched = g->overridden = false;
+    g->ov_layer.clear(); g->ov_edge.clear();
+    uint32_t L = 0;
+    while ((1u << L) < p) L++;
+    g->p = p;
+    g->log2p = L;
+    const size_t nv = g->V.size();
+    g->K.assign(nv, 0);
+    g->ex.assign(nv, {});
+    g->flops.assign(nv, 0);
+    g->keep_n.assign(nv, 0);
+    g->maxL.assign(nv, 0);
+    for (size_t v = 0; v < nv; v++) {
+        const uint32_t d = g->V[v].ndims;
+        // exponent tuples with sum <= L in lexicographic order (dim 0 slowest),
+        // produced by the lexicographic successor: bump the last dim that still
+        // has room and clear the dims after it
+        std::vector<uint8_t> cur(d, 0), rows;
+        for (;;) {
+            rows.insert(rows.end(), cur.begin(), cur.end());
+            uint32_t sum = 0;
+            for (uint8_t x : cur) sum += x;
+            int k = (int)d - 1;
+            if (sum < L) {
+                cur[k]++;
+                continue;
+            }
+            // sum == L: find the last k > 0... increment dim k-1 and zero dims >= k
+            while (k >= 0 && cur[k] == 0) k--;
+            if (k <= 0) break;
+            cur[k] = 0;
+            cur[k - 1]++;
+        }
+        uint64_t K = rows.size() / d;
+        if (K > 65535) return fail(g, PASE_ERR_TOO_LARGE, "more than 65535 configurations");
+        g->K[v] = (uint32_t)K;
+        g->ex[v] = std::move(rows);
+        uint64_t fl = g->V[v].flops_per_point, keep = 1;
+        for (uint32_t k = 0; k < d; k++) {
+            if (!mul_ok(fl, g->V[v].size[k], &fl))
+                return fail(g, PASE_ERR_OVERFLOW, "layer FLOPs exceed 64 bits");
+            if (!((g->V[v].reduce_mask >> k) & 1u) && !mul_ok(keep, g->V[v].size[k], &keep))
+                return fail(g, PASE_ERR_OVERFLOW, "layer size exceeds 64 bits");
+        }
+        if (fl >> 62 || keep >> 62) return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 2^62");
+        g->flops[v] = fl;
+        g->keep_n[v] = keep;
+        // t_l <= flops + r * (p - 1) * keep
+        uint64_t comm, m;
+        if (!mul_ok(g->r, (uint64_t)(p - 1), &comm) || !mul_ok(comm, keep, &comm) || !add_ok(fl, comm, &m))
+            return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 64 bits");
+        g->maxL[v] = m;
+    }
+    g->maxR.assign(g->E.size(), 0);
+    for (size_t e = 0; e < g->E.size(); e++) {
+        if (g->E[e].elems >> 62 || !mul_ok(g->r, g->E[e].elems, &g->maxR[e]))
+            return fail(g, PASE_ERR_OVERFLOW, "transfer cost exceeds 64 bits");
+    }
+    g->enumerated = true;
+    pase_status st = build_plan(g);
+    if (st != PASE_OK) { g->enumerated = false; return st; }
+    st = layout_memory(g);
+    if (st != PASE_OK) { g->enumerated = false; return st; }
+    g->planned = true;
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_num_configs(pase_graph_t g, uint32_t v, uint32_t *k) {
+    if (!g || !k) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->enumerated) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    *k = g->K[v];
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_config_splits(pase_graph_t g, uint32_t v, uint32_t idx, uint32_t *splits) {
+    if (!g || !splits) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->enumerated) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    if (v >= g->V.size() || idx >= g->K[v]) return fail(g, PASE_ERR_INVALID_ARGUMENT, "bad id");
+    const uint32_t d = g->V[v].ndims;
+    for (uint32_t k = 0; k < d; k++) splits[k] = 1u << g->ex[v][(size_t)idx * d + k];
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_get_sequence(pase_graph_t g, uint32_t *order) {
+    if (!g || !order) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    for (size_t i = 0; i < g->plan.seq.size(); i++) order[i] = (uint32_t)g->plan.seq[i];
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_get_dependent_set(pase_graph_t g, uint32_t v, uint32_t *out, uint32_t cap,
+                                              uint32_t *n) {
+    if (!g || !n || (cap && !out)) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    const auto &D = g->plan.v[g->plan.pos[v]].D;
+    if (D.size() > cap) return fail(g, PASE_ERR_TOO_LARGE, "output array too small");
+    for (size_t k = 0; k < D.size(); k++) out[k] = (uint32_t)D[k];
+    *n = (uint32_t)D.size();
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t value) {
+    if (!g) return PASE_ERR_INVALID_ARGUMENT;
+    switch (opt) {
+    case PASE_OPT_KEEP_TABLES: g->keep_tables = value != 0; break;
+    case PASE_OPT_MEMORY_BUDGET: g->mem_budget = value; break;
+    case PASE_OPT_KERNEL:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "kernel mode 0 or 1");
+        g->kernel_mode = (int)value;
+        break;
+    case PASE_OPT_KEY_TYPE:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "key type 0 or 1");
+        g->key_mode = (int)value;
+        break;
+    case PASE_OPT_PROFILE: g->profile = value != 0; break;
+    default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
+    }
+    // options that change the plan need a fresh enumeration
+    if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET) &&
+        g->enumerated) {
+        g->searched = false;
+        pase_status st = build_plan(g);
+        if (st == PASE_OK) st = layout_memory(g);
+        g->planned = st == PASE_OK;
+        if (st != PASE_OK) return st;
+    }
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_override_costs(pase_graph_t g, const uint64_t *layer, const uint64_t *edge) {
+    if (!g || !layer || (!edge && !g->E.empty())) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    const size_t nv = g->V.size(), ne = g->E.size();
+    g->ov_layer_off.assign(nv, 0);
+    uint64_t tot = 0;
+    for (size_t v = 0; v < nv; v++) { g->ov_layer_off[v] = tot; tot += g->K[v]; }
+    g->ov_layer.assign(layer, layer + tot);
+    g->ov_edge_off.assign(ne, 0);
+    tot = 0;
+    for (size_t e = 0; e < ne; e++) {
+        g->ov_edge_off[e] = tot;
+        tot += (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+    }
+    g->ov_edge.assign(edge ? edge : layer, edge ? edge + tot : layer);
+    g->overridden = true;
+    g->searched = false;
+    return layout_memory(g);
+}
+
+extern "C" pase_status pase_workspace_size(pase_graph_t g, uint64_t *bytes) {
+    if (!g || !bytes) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    *bytes = g->plan.total;
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_set_workspace(pase_graph_t g, void *device_ptr, uint64_t bytes) {
+    if (!g) return PASE_ERR_INVALID_ARGUMENT;
+    if (device_ptr && ((uintptr_t)device_ptr % 256))
+        return fail(g, PASE_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+    return device_set_workspace(g, device_ptr, bytes);
+}
+
+extern "C" pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_cost,
+                                               uint32_t *config_idx) {
+    if (!g || !min_cost || !config_idx) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    return device_search(g, stream, min_cost, config_idx);
+}
+
+static pase_status find_entry(pase_graph_t g, uint32_t v, const uint32_t *dep_cfg, int *pos,
+                              uint64_t *idx) {
+    if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    const VPlan &vp = g->plan.v[g->plan.pos[v]];
+    uint64_t x = 0;
+    for (size_t k = 0; k < vp.layout.size(); k++) {
+        size_t at = std::lower_bound(vp.D.begin(), vp.D.end(), vp.layout[k]) - vp.D.begin();
+        uint32_t c = dep_cfg[at];
+        if (c >= g->K[vp.layout[k]]) return fail(g, PASE_ERR_INVALID_ARGUMENT, "config out of range");
+        x += c * vp.stride[k];
+    }
+    *pos = g->plan.pos[v];
+    *idx = x;
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_table_entry(pase_graph_t g, uint32_t v, const uint32_t *dep_cfg,
+                                        uint64_t *cost, uint32_t *argmin) {
+    if (!g || !cost || !argmin) return PASE_ERR_INVALID_ARGUMENT;
+    if (v < g->V.size() && g->planned && !g->plan.v[g->plan.pos[v]].D.empty() && !dep_cfg)
+        return PASE_ERR_INVALID_ARGUMENT;
+    int pos;
+    uint64_t idx;
+    pase_status st = find_entry(g, v, dep_cfg, &pos, &idx);
+    if (st != PASE_OK) return st;
+    if (!g->keep_tables && pos != (int)g->plan.v.size() - 1)
+        return fail(g, PASE_ERR_BAD_STATE, "tables are not kept (PASE_OPT_KEEP_TABLES)");
+    return device_table_entry(g, pos, idx, cost, argmin);
+}
+
+extern "C" pase_status pase_table_fingerprint(pase_graph_t g, uint32_t v, uint64_t *fp_cost,
+                                              uint64_t *fp_arg) {
+    if (!g || !fp_cost || !fp_arg) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    int pos = g->plan.pos[v];
+    if (!g->keep_tables && pos != (int)g->plan.v.size() - 1)
+        return fail(g, PASE_ERR_BAD_STATE, "tables are not kept (PASE_OPT_KEEP_TABLES)");
+    return device_fingerprint(g, pos, fp_cost, fp_arg);
+}
+
+extern "C" pase_status pase_layer_costs(pase_graph_t g, uint32_t v, uint64_t *out) {
+    if (!g || !out) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    return device_layer_costs(g, v, out);
+}
+
+extern "C" pase_status pase_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
+    if (!g || !out) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
+    if (e >= g->E.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "edge id out of range");
+    return device_edge_costs(g, e, out);
+}
+
+extern "C" pase_status pase_stats(pase_graph_t g, pase_run_stats *out) {
+    if (!g || !out) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
+    *out = g->stats;
+    return PASE_OK;
+}

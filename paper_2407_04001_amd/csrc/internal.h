@@ -1,0 +1,235 @@
+// Internal data structures of libpase (host planning + device descriptors).
+//
+// Vocabulary (Sec. III-B of the paper): the vertices are visited in the order
+// of GenerateSeq; position i holds vertex v_i with dependent set D(i).  The DP
+// table of position i, T_i, has one entry per assignment phi of D(i); the
+// entry is min over the configurations c of v_i of
+//     layer cost + transfer costs to later neighbours + sum_j T_j[phi' | D(j)]
+// (recurrence (4)).  Here the terms of that sum are grouped by the digits of
+// phi they depend on, and the "digits" of a table are the members of its
+// dependent set in the table's own memory order.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "pase.h"
+
+namespace pase {
+
+constexpr int kMaxDims = PASE_MAX_DIMS;
+constexpr int kMaxDep = PASE_MAX_DEP;
+constexpr int kMaxATerms = 4;      // per-lane row terms of the row kernel
+constexpr int kMaxGTerms = 24;     // terms of the generic kernel
+constexpr int kMaxContrib = 64;    // contributions to one precomputed block
+constexpr int kMaxBlocks = kMaxDep + 1;
+constexpr uint64_t kMaxTableEntries = (1ull << 31) - 1;
+
+// ------------------------------------------------------------------ device descriptors
+struct DevVertex {            // configuration data of one vertex (uploaded once per search)
+    uint64_t ex_off;          // byte offset of its exponent rows (K x ndims uint8)
+    uint64_t L_off;           // element offset of its layer-cost vector
+    uint64_t flops;           // flops_per_point * prod(size)
+    uint64_t keep_n;          // prod of the sizes of the non-contracted dims
+    uint32_t K, ndims, reduce_mask, pad;
+};
+
+struct DevEdge {
+    uint32_t src, dst, rank, pad;
+    int8_t sdim[kMaxDims], ddim[kMaxDims];
+    uint64_t elems;
+};
+
+// One contribution to a precomputed block element (see Prep below).
+enum ContribKind : uint32_t { kContribLayer = 0, kContribEdge = 1, kContribTable = 2 };
+struct Contrib {
+    uint32_t kind;
+    uint32_t edge;            // kContribEdge: edge id
+    uint32_t dig;             // kContribEdge: plan digit of the other endpoint
+    uint32_t vi_is_src;       // kContribEdge: v_i is the edge's source
+    const void *ptr;          // kContribTable: value table (key type's value form, or uint64 for
+                              // caller-given edge matrices)
+    uint32_t sc;              // kContribTable: element stride of v_i's configuration
+    uint32_t raw_u64;         // kContribTable: 1 = plain uint64 costs (caller-given edge
+                              // matrices), 0 = a DP table already in this vertex's key space
+    uint32_t sd[kMaxDep];     // kContribTable: element stride per plan digit (0 = unused)
+};
+
+// A precomputed block: a key-space array over (pre digits, c, post digit)
+// laid out [pre...][c][ld].  Each element is the sum of its contributions,
+// multiplied by 2^bits (the low bits of a key hold the configuration index).
+struct Block {
+    uint64_t out_off;         // element offset in the block scratch
+    uint64_t elems;           // prod(pre radices) * K * ld
+    uint32_t npre;
+    uint32_t pre[kMaxDep];    // plan digits, slowest first
+    uint32_t prerad[kMaxDep];
+    int32_t post;             // plan digit, -1 = none
+    uint32_t postrad;         // its radix (columns actually filled)
+    uint32_t ld;              // row pitch (>= postrad, padded columns hold 0)
+    uint32_t c_begin, c_end;  // contribution range
+};
+
+struct PrepArgs {
+    uint32_t vi, K, bits, nblocks;
+    uint64_t total;           // sum of block elements
+    Block blk[kMaxBlocks];
+};
+
+struct ATerm {                // per-lane row term of the row kernel (key space)
+    const void *ptr;
+    uint32_t sc;              // stride of c
+    uint32_t bytes;           // size of the array (buffer-load range, < 2^31)
+    uint32_t sdO[kMaxDep];    // strides per outer digit
+    uint32_t sdR[kMaxDep];    // strides per row digit
+};
+
+struct RowsArgs {
+    const void *B;            // [o][c][ldz] key space: layer cost, c, outer and column terms
+    uint32_t ldz, Kz, K, bits;
+    uint32_t MO, MR, tiles_per_o, nchunks;
+    uint32_t nsplit, cper;
+    uint32_t nO, nR;
+    uint32_t radO[kMaxDep], radR[kMaxDep];
+    uint32_t na;
+    ATerm a[kMaxATerms];
+    void *T;                  // output values, index z*(MO*MR) + o*MR + r
+    uint16_t *A;              // output argmins
+    void *partial;            // nsplit > 1: keys [split][N]
+    uint64_t N;
+    uint64_t total_tiles;
+    uint32_t nblocks_launched;
+    uint32_t out_shift;       // bits of the table's reader: values are stored x 2^out_shift
+};
+
+struct GTerm {                // term of the generic kernel (key space)
+    const void *ptr;
+    uint32_t sc, pad;
+    uint32_t sd[kMaxDep];
+};
+
+struct GenericArgs {
+    uint32_t m, K, bits, nt;
+    uint32_t rad[kMaxDep];    // radices of the plan digits (= T_i layout), slowest first
+    GTerm t[kMaxGTerms];
+    void *T;
+    uint16_t *A;
+    uint64_t N;
+    uint32_t out_shift, pad;
+};
+
+struct ReduceArgs {
+    const void *partial;
+    void *T;
+    uint16_t *A;
+    uint64_t N;
+    uint32_t nsplit, bits, out_shift, pad;
+};
+
+struct BacktrackDesc {        // per position, for the back-substitution kernel
+    const uint16_t *A;
+    uint32_t vi, m;
+    uint32_t dig[kMaxDep];    // vertex ids of the layout digits
+    uint64_t stride[kMaxDep];
+};
+
+struct SearchOut {            // written by the back-substitution kernel
+    uint64_t min_cost;
+    uint32_t status;
+    uint32_t pad;
+};
+
+// ------------------------------------------------------------------ host plan
+struct TermRef {
+    int j;                    // position of the producer (last vertex of the component)
+    std::vector<int> dig;     // D(j) - {v_i}: vertex ids
+};
+
+enum KernelKind { kGeneric = 0, kRows = 1 };
+
+struct VPlan {
+    int vi = -1;
+    uint32_t K = 0, bits = 0;
+    std::vector<int> D;             // D(i), ascending vertex id
+    std::vector<int> layout;        // plan digits = T_i memory order, slowest first (vertex ids)
+    std::vector<uint64_t> stride;   // element stride of each layout digit in T_i
+    uint64_t N = 1;
+    std::vector<int> edges;         // edges joining v_i and a later vertex
+    std::vector<TermRef> terms;     // one lookup per connected subset in S(i)
+    int consumer = -1;              // position whose lookups read T_i
+    uint32_t out_shift = 0;         // T_i is stored x 2^(bits of its reader): in the reader's key space
+    KernelKind kernel = kGeneric;
+    // row kernel shape
+    int z = -1;                     // column digit (vertex id)
+    std::vector<int> O, R;          // outer / row digits (vertex ids), slowest first
+    uint32_t TZ = 0, ldz = 0, nchunks = 0, nsplit = 1, cper = 0;
+    uint64_t MO = 1, MR = 1;
+    // memory
+    uint64_t T_off = 0, A_off = 0;  // bytes into the table arenas
+    uint64_t block_elems = 0;       // block scratch this vertex needs
+};
+
+struct Plan {
+    std::vector<int> seq, pos;
+    std::vector<VPlan> v;           // by position
+    uint64_t cells = 0, entries = 0, rows_cells = 0;
+    uint32_t max_dep = 0, rows_vertices = 0;
+    // workspace layout, byte offsets from the workspace base
+    uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_ovedge = 0, off_contrib = 0,
+             off_bt = 0, off_cfg = 0, off_out = 0, off_T = 0, off_A = 0, off_block = 0,
+             off_partial = 0, total = 0;
+    uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
+};
+
+struct DeviceState;   // defined by the device runtime
+
+}  // namespace pase
+
+struct pase_graph_s {
+    std::vector<pase_vertex_desc> V;
+    std::vector<pase_edge_desc> E;
+    uint64_t r = 8;
+    uint32_t seq_rule = 0;
+    std::vector<std::vector<int>> nbr;     // undirected, deduplicated, ascending
+    std::string err;
+    // options
+    bool keep_tables = false, profile = false;
+    uint64_t mem_budget = 64ull << 30;
+    int kernel_mode = 0, key_mode = 0;
+    // configurations
+    bool enumerated = false;
+    uint32_t p = 0, log2p = 0;
+    std::vector<uint32_t> K;
+    std::vector<std::vector<uint8_t>> ex;  // [v][c*ndims + k]
+    std::vector<uint64_t> flops, keep_n;
+    std::vector<uint64_t> maxL;            // upper bound of the layer cost per vertex
+    std::vector<uint64_t> maxR;            // upper bound of the transfer cost per edge
+    // caller-given costs
+    bool overridden = false;
+    std::vector<uint64_t> ov_layer, ov_edge, ov_layer_off, ov_edge_off;
+    // plan
+    pase::Plan plan;
+    bool planned = false;
+    // last search
+    bool searched = false;
+    uint32_t key_type = 0;
+    pase_run_stats stats{};
+    // device runtime
+    pase::DeviceState *dev = nullptr;
+};
+
+namespace pase {
+// host.cpp
+pase_status fail(pase_graph_t g, pase_status st, const std::string &msg);
+uint32_t choose_key_type(pase_graph_t g, pase_status *st);
+// device.hip
+void device_release(pase_graph_t g);
+pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);
+pase_status device_set_workspace(pase_graph_t g, void *ptr, uint64_t bytes);
+pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *cost,
+                               uint32_t *arg);
+pase_status device_fingerprint(pase_graph_t g, int pos, uint64_t *fpT, uint64_t *fpA);
+pase_status device_layer_costs(pase_graph_t g, uint32_t v, uint64_t *out);
+pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out);
+}  // namespace pase

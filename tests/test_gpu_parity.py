@@ -1,0 +1,248 @@
+"""GPU parity: the HIP search against the CPU oracle, bit for bit.
+
+Costs are integers and ties break to the lowest configuration index, so every
+compared quantity must be identical: minimum cost, strategy, vertex order,
+dependent sets, every table entry (small graphs, element by element), table
+fingerprints and sampled entries (full-size workloads, against the oracle's
+committed golden files), and the device cost tables.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from workloads import chain_graph, random_costs, random_graph, workload
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2407_04001_amd import pase
+    pase.load()
+    return pase
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def _oracle(g, p=None, costs=None, rule=0):
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    o.configs(p or g["p"])
+    if costs is not None:
+        o.set_costs(*costs)
+    o.solve(rule=rule, threads=os.cpu_count() or 1)
+    return o
+
+
+def _compare_all_entries(pg, o, g, max_entries=2048):
+    """Every entry of every table element by element (tables up to
+    `max_entries` entries; larger ones on a seeded sample of that many), plus
+    the fingerprints of every table."""
+    K = pg.K
+    rng = np.random.default_rng(7)
+    for i, v in enumerate(o.sequence()):
+        D = o.dependent_set(i)
+        assert pg.dependent_set(v) == D
+        T, A = o.table(i)
+        idxs = range(len(T)) if len(T) <= max_entries else rng.integers(0, len(T), max_entries)
+        for idx in idxs:
+            idx = int(idx)
+            cfg, x = [], idx
+            for w in reversed(D):
+                cfg.append(x % K[w])
+                x //= K[w]
+            cfg.reverse()
+            got = pg.table_entry(v, cfg)
+            assert got == (int(T[idx]), int(A[idx])), (v, cfg)
+        assert pg.fingerprint(v) == o.fingerprint(i)
+
+
+def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0):
+    pg = P.Graph(g, seq_rule=rule)
+    pg.enumerate_configs(p or g["p"])
+    pg.set_option(P.OPT_KEEP_TABLES, int(keep))
+    pg.set_option(P.OPT_KERNEL, kernel)
+    pg.set_option(P.OPT_KEY_TYPE, key)
+    if costs is not None:
+        pg.override_costs(*costs)
+    mc, strat = pg.find_best_strategy()
+    return pg, mc, strat
+
+
+# ------------------------------------------------------------------ small graphs, every entry
+@pytest.mark.parametrize("kernel,key", [(0, 0), (1, 0), (0, 1), (1, 1)])
+def test_fc_chain_closed_form(P, kernel, key):
+    say(f"fc_chain kernel={kernel} key={key}")
+    g = workload("w0_fc_chain")
+    pg, mc, strat = _run(P, g, kernel=kernel, key=key)
+    assert (mc, strat) == (8_388_608, [9, 9, 9, 9])
+    _compare_all_entries(pg, _oracle(g), g)
+
+
+@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("key", [0, 1])
+def test_random_graphs_random_costs(P, seed, key):
+    """Dense ties (costs in [0,4)) exercise the lowest-index tie-break."""
+    g = random_graph(seed + 200, n=4 + seed % 6, p=8, max_dims=3, extra_edges=1 + seed % 4)
+    say(f"random graph seed={seed + 200} key={key}")
+    o0 = _oracle(g)
+    K = [int(k) for k in o0.K]
+    costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    o = _oracle(g, costs=costs)
+    pg, mc, strat = _run(P, g, key=key, costs=costs)
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_graphs_model_costs(P, seed):
+    g = random_graph(seed + 300, n=5 + seed % 5, p=16, max_dims=3, extra_edges=seed % 5,
+                     max_size=512)
+    say(f"random graph model costs seed={seed + 300}")
+    o = _oracle(g)
+    pg, mc, strat = _run(P, g)
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g)
+    for v in range(len(g["vertices"])):
+        assert np.array_equal(pg.layer_costs(v), o.layer_costs(v))
+    for e in range(len(g["edges"])):
+        assert np.array_equal(pg.edge_costs(e), o.edge_costs(e))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_chains(P, seed):
+    g = chain_graph(seed, n=6 + seed, p=32, max_dims=3)
+    say(f"chain seed={seed}")
+    o = _oracle(g)
+    pg, mc, strat = _run(P, g)
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g)
+
+
+def test_edge_cases(P):
+    # one vertex, no edges: the minimum layer cost
+    g = {"name": "one", "p": 8, "comm_weight": 8, "edges": [],
+         "vertices": [{"name": "v", "dims": [5, 7, 3], "dim_names": list("abc"), "reduce": [1],
+                       "flops_per_point": 3}]}
+    say("edge case: single vertex")
+    o = _oracle(g)
+    pg, mc, strat = _run(P, g)
+    assert (mc, strat) == o.result()
+    # p = 1: a single configuration everywhere
+    g = random_graph(11, n=6, p=1, extra_edges=3)
+    say("edge case: p=1")
+    o = _oracle(g, p=1)
+    pg, mc, strat = _run(P, g, p=1)
+    assert (mc, strat) == o.result() and set(strat) == {0}
+    # parallel edges and the printed GenerateSeq rule
+    g = random_graph(3, n=5, p=4, extra_edges=6, multi_edges=True)
+    for rule in (0, 1):
+        say(f"edge case: multigraph rule={rule}")
+        o = _oracle(g, rule=rule)
+        pg, mc, strat = _run(P, g, rule=rule)
+        assert pg.sequence() == o.sequence()
+        assert (mc, strat) == o.result()
+        _compare_all_entries(pg, o, g)
+
+
+def test_repeat_and_reenumerate(P):
+    g = workload("w1_residual_cnn")
+    say("repeat + re-enumerate")
+    pg = P.Graph(g)
+    results = []
+    for p in (8, 4, 8):
+        pg.enumerate_configs(p)
+        results.append(pg.find_best_strategy())
+        results.append(pg.find_best_strategy())
+        assert results[-1] == results[-2]
+    assert results[0] == results[4]
+    assert results[2] == _oracle(g, p=4).result()
+
+
+def test_library_owned_workspace(P):
+    g = workload("w1_residual_cnn", 1)
+    say("library-owned workspace")
+    pg = P.Graph(g)
+    pg.enumerate_configs(g["p"])
+    mc, strat = pg.find_best_strategy(torch_workspace=False)
+    assert (mc, strat) == _oracle(g).result()
+
+
+# ------------------------------------------------------------------ full-size workloads
+def _golden(name, seed):
+    with open(os.path.join(GOLDEN, f"{name}_seed{seed}.json")) as f:
+        return json.load(f)
+
+
+def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True):
+    gold = _golden(name, seed)
+    g = workload(name, seed)
+    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep}")
+    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key)
+    st = pg.stats()
+    say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
+        f"rows_vertices {st['rows_vertices']}")
+    assert pg.K == gold["num_configs"]
+    assert pg.sequence() == gold["sequence"]
+    assert st["cells"] == gold["cells"]
+    assert mc == int(gold["min_cost"])
+    assert strat == gold["strategy"]
+    if not keep:
+        return
+    K = gold["num_configs"]
+    for tb in gold["tables"]:
+        v = tb["vertex"]
+        assert pg.dependent_set(v) == tb["dep"]
+        assert pg.fingerprint(v) == (int(tb["fp_cost"]), int(tb["fp_arg"])), v
+        if samples:
+            for idx, t, a in tb["samples"]:
+                cfg, x = [], idx
+                for w in reversed(tb["dep"]):
+                    cfg.append(x % K[w])
+                    x //= K[w]
+                cfg.reverse()
+                assert pg.table_entry(v, cfg) == (int(t), a), (v, idx)
+
+
+@pytest.mark.parametrize("name,seed", [("w0_fc_chain", 0), ("w1_residual_cnn", 0),
+                                       ("w1_residual_cnn", 1), ("w1_residual_cnn", 2),
+                                       ("w2_inception", 0), ("w2_inception", 1),
+                                       ("w2_inception", 2), ("w3_lstm_grid", 0)])
+def test_workloads_against_golden(P, name, seed):
+    _check_golden(P, name, seed)
+
+
+@pytest.mark.parametrize("name", ["w2_inception", "w3_lstm_grid"])
+def test_generic_and_u64_paths_against_golden(P, name):
+    _check_golden(P, name, 0, kernel=1)
+    _check_golden(P, name, 0, key=1)
+
+
+def test_transformer_p64_against_golden(P):
+    """The measured workload at full size, in the configuration the benchmark
+    times (default kernels and memory plan), then with every table kept and
+    fingerprinted."""
+    _check_golden(P, "w4_transformer", 0, keep=False)
+    _check_golden(P, "w4_transformer", 0, keep=True)
+
+
+def test_cost_tables_against_oracle(P):
+    for name in ("w0_fc_chain", "w1_residual_cnn", "w2_inception"):
+        g = workload(name)
+        say(f"cost tables {name}")
+        from oracle.oracle import Oracle
+        o = Oracle(g)
+        o.configs(g["p"])
+        pg, _, _ = _run(P, g, keep=False)
+        for v in range(len(g["vertices"])):
+            assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
+        for e in range(len(g["edges"])):
+            assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e

@@ -1,0 +1,162 @@
+"""Host-side tests of libpase (no GPU): the library loads and exports the C ABI,
+input validation and error paths, configuration enumeration, GenerateSeq and
+the dependent sets (checked against the oracle and against their definition)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import pins
+from workloads import fc_chain, random_graph, transformer, workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def pase():
+    from paper_2407_04001_amd import pase as P
+    P.load()
+    return P
+
+
+def test_exports_every_declared_symbol(pase):
+    header = open(os.path.join(ROOT, "include", "pase.h")).read()
+    declared = set(re.findall(r"\b(pase_[a-z_]+)\s*\(", header))
+    assert declared, "no declarations found"
+    lib = pase.load()
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared == set(pase.EXPORTS)
+
+
+def _status(fn):
+    from paper_2407_04001_amd.pase import PaseError
+    try:
+        fn()
+    except PaseError as e:
+        return e.status
+    return 0
+
+
+def test_create_validation(pase):
+    g = fc_chain()
+    P = pase
+    bad = []
+    v = [dict(x) for x in g["vertices"]]
+    e = [dict(x) for x in g["edges"]]
+    bad.append((v, [dict(e[0], dst=e[0]["src"])]))                       # self-loop
+    bad.append(([dict(v[0], dims=[])] + v[1:], e))                        # ndims 0
+    bad.append(([dict(v[0], dims=[0, 1, 1])] + v[1:], e))                 # size 0
+    bad.append((v, [dict(e[0], src_dim=[0, 5])] + e[1:]))                 # map out of range
+    bad.append((v, [dict(e[0], elems=0)] + e[1:]))                        # elems 0
+    bad.append((v, [dict(e[0], dst=17)] + e[1:]))                         # id out of range
+    bad.append(([dict(v[0], reduce=[3])] + v[1:], e))                     # reduce dim out of range
+    for vv, ee in bad:
+        assert _status(lambda: P.pase_graph_create(vv, ee)) == P.INVALID_ARGUMENT
+    # disconnected: drop the middle edge of the chain
+    assert _status(lambda: P.pase_graph_create(v, [e[0], e[2]])) == P.NOT_CONNECTED
+    assert _status(lambda: P.pase_graph_create(v, e, seq_rule=2)) == P.INVALID_ARGUMENT
+
+
+def test_call_order_and_p(pase):
+    P = pase
+    g = P.Graph(fc_chain())
+    assert _status(lambda: g.sequence()) == P.BAD_STATE
+    assert _status(lambda: P.pase_num_configs(g.h, 0)) == P.BAD_STATE
+    assert _status(lambda: P.pase_stats(g.h)) == P.BAD_STATE
+    for p in (0, 3, 6, 1 << 17):
+        assert _status(lambda: g.enumerate_configs(p)) == P.INVALID_ARGUMENT
+    g.enumerate_configs(4)
+    assert _status(lambda: g.table_entry(0, [0])) == P.BAD_STATE       # no search yet
+
+
+def test_overflow_and_too_large(pase):
+    P = pase
+    big = {"vertices": [{"dims": [2**40, 2**30], "reduce": [], "flops_per_point": 1}], "edges": []}
+    g = P.Graph(big)
+    assert _status(lambda: g.enumerate_configs(2)) == P.OVERFLOW
+    # a 6-clique at p=64: the first dependent set has 5 members of 84 configs -> table > 2^31
+    vs = [{"dims": [8, 8, 8], "reduce": [], "flops_per_point": 1} for _ in range(6)]
+    es = [{"src": a, "dst": b, "src_dim": [0], "dst_dim": [0], "elems": 8}
+          for a in range(6) for b in range(a + 1, 6)]
+    g = P.Graph({"vertices": vs, "edges": es})
+    assert _status(lambda: g.enumerate_configs(64)) == P.TOO_LARGE
+    # the memory budget is enforced before any device work
+    g = P.Graph(transformer())
+    g.enumerate_configs(64)
+    assert _status(lambda: g.set_option(P.OPT_MEMORY_BUDGET, 1 << 20)) == P.TOO_LARGE
+
+
+def test_lent_workspace_too_small(pase):
+    P = pase
+    g = P.Graph(fc_chain())
+    g.enumerate_configs(4)
+    assert g.workspace_size() > 0
+    P.pase_set_workspace(g.h, 4096 * 256, 256)
+    assert _status(lambda: P.pase_find_best_strategy(g.h, 4)) == P.OUT_OF_MEMORY
+    assert _status(lambda: P.pase_set_workspace(g.h, 4096 * 256 + 8, 1 << 20)) == P.INVALID_ARGUMENT
+
+
+def test_configs_match_oracle(pase):
+    from oracle.oracle import Oracle
+    for name in ("w0_fc_chain", "w1_residual_cnn", "w4_transformer"):
+        g = workload(name)
+        pg = pase.Graph(g)
+        K = pg.enumerate_configs(g["p"])
+        o = Oracle(g)
+        assert list(o.configs(g["p"])) == K
+        for v in (0, len(K) - 1):
+            ex = o.exponents(v)
+            for c in range(K[v]):
+                assert pg.config_splits(v, c) == [1 << int(x) for x in ex[c]]
+    g = fc_chain()
+    pg = pase.Graph(g)
+    pg.enumerate_configs(4)
+    assert pg.config_splits(0, 9) == [4, 1, 1]
+
+
+@pytest.mark.parametrize("seed", range(20))
+@pytest.mark.parametrize("rule", [0, 1])
+def test_sequence_and_dependent_sets(pase, seed, rule):
+    from oracle.oracle import Oracle
+    g = random_graph(seed, n=4 + seed % 9, extra_edges=seed % 6, p=4)
+    pg = pase.Graph(g, seq_rule=rule)
+    pg.enumerate_configs(4)
+    o = Oracle(g)
+    o.configs(4)
+    o.solve(rule=rule, max_cells=1)
+    seq = pg.sequence()
+    assert seq == o.sequence()
+    nb = pins.neighbours(len(seq), [e["src"] for e in g["edges"]], [e["dst"] for e in g["edges"]])
+    for i, v in enumerate(seq):
+        D = pg.dependent_set(v)
+        assert D == o.dependent_set(i) == pins.dependent_set(nb, seq, i)
+
+
+def test_workload_sequences_match_oracle(pase):
+    from oracle.oracle import Oracle
+    for name in ("w2_inception", "w3_lstm_grid", "w4_transformer"):
+        g = workload(name)
+        pg = pase.Graph(g)
+        pg.enumerate_configs(g["p"])
+        o = Oracle(g)
+        o.configs(g["p"])
+        o.solve(max_cells=1)
+        assert pg.sequence() == o.sequence()
+        for i, v in enumerate(o.sequence()):
+            assert pg.dependent_set(v) == o.dependent_set(i)
+
+
+def test_options_validate(pase):
+    P = pase
+    g = P.Graph(fc_chain())
+    g.enumerate_configs(4)
+    assert _status(lambda: g.set_option(P.OPT_KERNEL, 2)) == P.INVALID_ARGUMENT
+    assert _status(lambda: g.set_option(P.OPT_KEY_TYPE, 7)) == P.INVALID_ARGUMENT
+    assert _status(lambda: g.set_option(99, 1)) == P.INVALID_ARGUMENT
+    g.set_option(P.OPT_KEEP_TABLES, 1)
+    g.set_option(P.OPT_KERNEL, 1)
+    assert g.sequence() == [0, 1, 2, 3]
+    costs = [np.zeros(10, np.uint64)] * 4
+    assert _status(lambda: P.pase_override_costs(g.h, costs, [np.zeros((10, 10), np.uint64)] * 3)) == 0
