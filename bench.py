@@ -58,6 +58,38 @@ def oracle_baseline(g, p, max_cells):
                       f"OpenMP over table entries)"}
 
 
+def copy_calibration(mib):
+    """A plain device-to-device copy of known size: under rocprofv3 --pmc its
+    FETCH_SIZE / WRITE_SIZE readings give the scale of those counters."""
+    import torch
+    n = mib * 1024 * 1024
+    a = torch.ones(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "copies": 3}), flush=True)
+
+
+def traffic_from_profile():
+    """HBM bytes per launch of the row kernel from the committed counter
+    summary, if it was taken on the current kernel source; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_fill_rows_hbm_traffic.json")
+    src = os.path.join(ROOT, "paper_2407_04001_amd", "csrc", "device.hip")
+    try:
+        with open(path) as f:
+            prof = json.load(f)
+        with open(src, "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    if prof.get("device_hip_sha256") != digest:
+        return None
+    return prof.get("bytes_per_launch")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -65,9 +97,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="w4_transformer")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-cells", type=float, default=4e9, help="oracle sample size (cells)")
+    ap.add_argument("--cpu-cells", type=float, default=3e10, help="oracle sample size (cells)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the strategy search runs on a single device "
               "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
@@ -130,7 +167,7 @@ def main():
         "min_cost": mc, "parity_with_oracle": parity,
         "roofline": {"bound": "alu", "kernel": "k_fill_rows",
                      "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
-                     "frac": achieved / FP64_OPS_PEAK_T, "traffic": None,
+                     "frac": achieved / FP64_OPS_PEAK_T, "traffic": traffic_from_profile(),
                      "launches_per_step": rows_launches // args.steps,
                      "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
                      "cells_per_step": st["rows_cells"]},

@@ -208,6 +208,21 @@ pase_status pase_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out);
 /* Statistics of the last search. */
 pase_status pase_stats(pase_graph_t g, pase_run_stats *out);
 
+/* Plan of one vertex (after pase_enumerate_configs) and, after a search with
+ * PASE_OPT_PROFILE=1, its fill time. */
+typedef struct {
+    uint32_t position;   /* index in the GenerateSeq order */
+    uint32_t kernel;     /* 0 = generic fill, 1 = row/column-chunk fill */
+    uint32_t num_configs, dep_count;
+    uint64_t entries;    /* |table| = product of K over D(v) */
+    uint64_t cells;      /* K_v * entries */
+    int32_t column;      /* row kernel: column digit (vertex id), else -1 */
+    uint32_t outer, rows, tile_cols, splits, row_terms, lookups;
+    double fill_ms;      /* PASE_OPT_PROFILE: event time of this vertex's fill kernel */
+} pase_vertex_info;
+
+pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -81,104 +81,138 @@ __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_
     return compute + r * (((1ull << ered) - 1) * part);
 }
 
-// r * t_x: 0 when every tensor dim is split equally at both ends, else the
-// tensor re-distributed over max(P_u, P_v) devices.
-__device__ __forceinline__ uint64_t edge_cost(const DevEdge &de, const uint8_t *exu, uint32_t du,
-                                              const uint8_t *exv, uint32_t dv, uint64_t r) {
-    bool match = true;
-    for (uint32_t k = 0; k < de.rank; k++) {
-        uint32_t a = de.sdim[k] >= 0 ? exu[de.sdim[k]] : 0;
-        uint32_t b = de.ddim[k] >= 0 ? exv[de.ddim[k]] : 0;
-        match &= a == b;
-    }
-    if (match) return 0;
-    uint32_t Eu = 0, Ev = 0;
-    for (uint32_t k = 0; k < du; k++) Eu += exu[k];
-    for (uint32_t k = 0; k < dv; k++) Ev += exv[k];
-    uint32_t s = Eu > Ev ? Eu : Ev;
-    return r * ((de.elems + ((1ull << s) - 1)) >> s);
+// Split signature of one endpoint configuration of an edge: the split
+// exponent of every tensor dim (0 for an unsplit dim), 5 bits each.  Two
+// endpoints redistribute nothing exactly when their signatures are equal.
+__device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t rank, const uint8_t *ex) {
+    uint64_t sig = 0;
+    for (uint32_t k = 0; k < rank; k++) sig |= (uint64_t)(dims[k] >= 0 ? ex[dims[k]] : 0) << (5 * k);
+    return sig;
 }
 
-__global__ void k_layer_costs(const DevVertex *__restrict__ V, uint32_t nv, const uint8_t *__restrict__ ex,
-                              uint64_t *__restrict__ L, uint64_t total, uint64_t r) {
-    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
+// Cost tables of the search: layer cost and device count exponent of every
+// (vertex, configuration), and the split signatures of every (edge endpoint,
+// configuration); r * t_x(e, cu, cv) is then read off two signatures and two
+// exponents (edge_cost_sig).
+__global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, const DevEdge *__restrict__ E,
+                              uint32_t ne, const uint8_t *__restrict__ ex, uint64_t *__restrict__ L,
+                              uint8_t *__restrict__ lsum, uint64_t *__restrict__ sig, uint64_t nL,
+                              uint64_t nS, uint64_t r) {
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < nL + nS;
          t += (uint64_t)gridDim.x * blockDim.x) {
-        uint32_t lo = 0, hi = nv;   // last vertex with L_off <= t
-        while (hi - lo > 1) {
-            uint32_t mid = (lo + hi) / 2;
-            if (V[mid].L_off <= t) lo = mid; else hi = mid;
+        if (t < nL) {
+            uint32_t lo = 0, hi = nv;   // last vertex with L_off <= t
+            while (hi - lo > 1) {
+                uint32_t mid = (lo + hi) / 2;
+                if (V[mid].L_off <= t) lo = mid; else hi = mid;
+            }
+            const DevVertex dv = V[lo];
+            const uint8_t *e = ex + dv.ex_off + (t - dv.L_off) * dv.ndims;
+            L[t] = layer_cost(dv, e, r);
+            uint32_t E0 = 0;
+            for (uint32_t k = 0; k < dv.ndims; k++) E0 += e[k];
+            lsum[t] = (uint8_t)E0;
+        } else {
+            uint64_t u = t - nL;
+            uint32_t lo = 0, hi = ne;   // last edge with sig_off <= u
+            while (hi - lo > 1) {
+                uint32_t mid = (lo + hi) / 2;
+                if (E[mid].sig_off <= u) lo = mid; else hi = mid;
+            }
+            const DevEdge de = E[lo];
+            uint64_t c = u - de.sig_off;
+            const DevVertex vs = V[de.src];
+            if (c < vs.K) {
+                sig[u] = split_signature(de.sdim, de.rank, ex + vs.ex_off + c * vs.ndims);
+            } else {
+                const DevVertex vd = V[de.dst];
+                c -= vs.K;
+                sig[u] = split_signature(de.ddim, de.rank, ex + vd.ex_off + c * vd.ndims);
+            }
         }
-        const DevVertex dv = V[lo];
-        uint64_t c = t - dv.L_off;
-        L[t] = layer_cost(dv, ex + dv.ex_off + c * dv.ndims, r);
     }
+}
+
+__device__ __forceinline__ uint64_t edge_cost_sig(uint64_t sig_a, uint64_t sig_b, uint32_t la, uint32_t lb,
+                                                  uint64_t elems, uint64_t r) {
+    if (sig_a == sig_b) return 0;
+    uint32_t s = la > lb ? la : lb;
+    return r * ((elems + ((1ull << s) - 1)) >> s);
 }
 
 __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t e,
-                             const uint8_t *__restrict__ ex, uint64_t *__restrict__ out, uint64_t r) {
+                             const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
+                             uint64_t *__restrict__ out, uint64_t r) {
     const DevEdge de = E[e];
     const DevVertex u = V[de.src], v = V[de.dst];
     uint64_t total = (uint64_t)u.K * v.K;
     for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
          t += (uint64_t)gridDim.x * blockDim.x) {
         uint64_t cu = t / v.K, cv = t % v.K;
-        out[t] = edge_cost(de, ex + u.ex_off + cu * u.ndims, u.ndims, ex + v.ex_off + cv * v.ndims,
-                           v.ndims, r);
+        out[t] = edge_cost_sig(sig[de.sig_off + cu], sig[de.sig_off + u.K + cv], lsum[u.L_off + cu],
+                               lsum[v.L_off + cv], de.elems, r);
     }
 }
 
 // ------------------------------------------------------------------ prep: key-space blocks
+// One workgroup handles kPrepThreads consecutive (c, column) elements of one
+// outer index of one block, so the block, its contributions and the outer
+// digits are uniform across the workgroup (scalar loads); lanes differ only in
+// (c, column).
 template <typename KeyT>
-__global__ void k_prep(PrepArgs a, const DevVertex *__restrict__ V, const DevEdge *__restrict__ E,
-                       const uint8_t *__restrict__ ex, const uint64_t *__restrict__ L,
-                       const Contrib *__restrict__ cb, KeyT *__restrict__ blocks, uint64_t r) {
+__global__ __launch_bounds__(kPrepThreads) void k_prep(PrepArgs a, const DevVertex *__restrict__ V,
+                                                     const DevEdge *__restrict__ E,
+                                                     const uint64_t *__restrict__ L,
+                                                     const uint8_t *__restrict__ lsum,
+                                                     const uint64_t *__restrict__ sig,
+                                                     const Contrib *__restrict__ cb,
+                                                     KeyT *__restrict__ blocks, uint64_t r) {
     using Val = typename KeyOps<KeyT>::Val;
-    const DevVertex me = V[a.vi];
-    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < a.total;
-         t += (uint64_t)gridDim.x * blockDim.x) {
-        uint32_t b = 0;
-        uint64_t e = t;
-        while (e >= a.blk[b].elems) { e -= a.blk[b].elems; b++; }
-        const Block &bk = a.blk[b];
-        uint32_t q = (uint32_t)(e % bk.ld);
-        uint64_t rest = e / bk.ld;
-        uint32_t c = (uint32_t)(rest % a.K);
-        rest /= a.K;
-        KeyT *out = blocks + bk.out_off + e;
-        if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; continue; }
-        uint32_t dv[kMaxDep];
-        for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
-        for (int k = (int)bk.npre - 1; k >= 0; k--) {
-            dv[bk.pre[k]] = (uint32_t)(rest % bk.prerad[k]);
-            rest /= bk.prerad[k];
-        }
-        if (bk.post >= 0) dv[bk.post] = q;
-        // plain costs (layer, transfer) are summed in `sum` and shifted into key
-        // space at the end; DP tables are stored in this vertex's key space already
-        uint64_t sum = 0, keysum = 0, low = 0;
-        const uint8_t *exme = ex + me.ex_off + (uint64_t)c * me.ndims;
-        for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
-            const Contrib &ct = cb[k];
-            if (ct.kind == kContribLayer) {
-                sum += L[me.L_off + c];
-                low = c;
-            } else if (ct.kind == kContribEdge) {
-                const DevEdge de = E[ct.edge];
-                uint32_t x = dv[ct.dig];
-                uint32_t other = ct.vi_is_src ? de.dst : de.src;
-                const DevVertex ov = V[other];
-                const uint8_t *exo = ex + ov.ex_off + (uint64_t)x * ov.ndims;
-                sum += ct.vi_is_src ? edge_cost(de, exme, me.ndims, exo, ov.ndims, r)
-                                    : edge_cost(de, exo, ov.ndims, exme, me.ndims, r);
-            } else {
-                uint64_t idx = (uint64_t)c * ct.sc;
-                for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
-                if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
-                else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
-            }
-        }
-        *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
+    const uint32_t wg = blockIdx.x;
+    uint32_t b = 0;
+    while (b + 1 < a.nblocks && wg >= a.blk[b + 1].wg_begin) b++;
+    b = __builtin_amdgcn_readfirstlane(b);
+    const Block &bk = a.blk[b];
+    const uint32_t rel = wg - bk.wg_begin;
+    const uint32_t row = rel / bk.chunks, chunk = rel % bk.chunks;
+    const uint32_t per_row = a.K * bk.ld;
+    const uint32_t e = chunk * kPrepThreads + threadIdx.x;
+    if (e >= per_row) return;
+    const uint32_t c = e / bk.ld, q = e % bk.ld;
+    KeyT *out = blocks + bk.out_off + (uint64_t)row * per_row + e;
+    if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; return; }
+    uint32_t dv[kMaxDep];
+    for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
+    uint32_t x = row;
+    for (int k = (int)bk.npre - 1; k >= 0; k--) {
+        dv[bk.pre[k]] = x % bk.prerad[k];
+        x /= bk.prerad[k];
     }
+    if (bk.post >= 0) dv[bk.post] = q;
+    const DevVertex me = V[a.vi];
+    // plain costs (layer, transfer) are summed in `sum` and shifted into key
+    // space at the end; DP tables are stored in this vertex's key space already
+    uint64_t sum = 0, keysum = 0, low = 0;
+    for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
+        const Contrib ct = cb[k];
+        if (ct.kind == kContribLayer) {
+            sum += L[me.L_off + c];
+            low = c;
+        } else if (ct.kind == kContribEdge) {
+            const DevEdge de = E[ct.edge];
+            const uint32_t xo = dv[ct.dig];
+            const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
+            const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
+            const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
+            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r);
+        } else {
+            uint64_t idx = (uint64_t)c * ct.sc;
+            for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
+            if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
+            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
+        }
+    }
+    *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
 }
 
 // ------------------------------------------------------------------ fill: row kernel
@@ -202,12 +236,14 @@ __global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
     const uint64_t logical = (uint64_t)(b % 8) * (nb / 8) + b / 8;
     const uint64_t tile = logical * 4 + wave;
     if (tile >= a.total_tiles) return;
+    // tile order (fastest first): row tile, column chunk, outer index, c split --
+    // all chunks of one outer index run close together and share its slices
     const uint32_t rowtile = (uint32_t)(tile % a.tiles_per_o);
     uint64_t t2 = tile / a.tiles_per_o;
-    const uint32_t o = (uint32_t)(t2 % a.MO);
-    t2 /= a.MO;
     const uint32_t chunk = (uint32_t)(t2 % a.nchunks);
-    const uint32_t split = (uint32_t)(t2 / a.nchunks);
+    t2 /= a.nchunks;
+    const uint32_t o = (uint32_t)(t2 % a.MO);
+    const uint32_t split = (uint32_t)(t2 / a.MO);
     const uint32_t r = rowtile * 64 + lane;
     const bool valid = r < a.MR;
     const uint32_t rr = valid ? r : a.MR - 1;
@@ -304,40 +340,77 @@ __global__ void k_reduce_splits(ReduceArgs a) {
 }
 
 // ------------------------------------------------------------------ fill: generic kernel
-// One thread per entry phi (any |D(i)| <= PASE_MAX_DEP, any term shapes):
-// key(c) = sum over terms, minimum over c in ascending order.
+// Any |D(i)| <= PASE_MAX_DEP and any term shapes.  A group of 2^group_log2
+// lanes owns one entry phi: lane l evaluates c = l, l + G, ... (key = sum of
+// the terms), the group then takes the minimum key with cross-lane swaps.
+// Keys are distinct for distinct c, so the minimum -- and with it the lowest
+// optimal c -- does not depend on the evaluation order.
 template <typename KeyT>
+__device__ __forceinline__ KeyT shfl_xor_key(KeyT v, int mask) {
+    uint64_t u = __builtin_bit_cast(uint64_t, v);
+    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)u, mask, 64);
+    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), mask, 64);
+    return __builtin_bit_cast(KeyT, ((uint64_t)hi << 32) | lo);
+}
+
+template <typename KeyT, int NT>
 __global__ __launch_bounds__(256) void k_fill_generic(GenericArgs a) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
-    for (uint64_t phi = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; phi < a.N;
-         phi += (uint64_t)gridDim.x * blockDim.x) {
+    const uint32_t G = 1u << a.group_log2;
+    const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
+    constexpr int MT = NT < 0 ? kMaxGTerms : NT;
+    const int nt = NT < 0 ? (int)a.nt : NT;
+    for (uint64_t tid = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x;
+         tid < ((nthreads + 255) / 256) * 256; tid += (uint64_t)gridDim.x * blockDim.x) {
+        const bool live = tid < nthreads;
+        const uint64_t phi = live ? tid >> a.group_log2 : a.N - 1;
+        const uint32_t lane = (uint32_t)(tid & (G - 1));
         uint32_t d[kMaxDep];
         uint64_t x = phi;
         for (int k = kMaxDep - 1; k >= 0; k--)
             if (k < (int)a.m) { d[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else d[k] = 0;
-        uint64_t off[kMaxGTerms];
+        const KeyT *base[MT];
+        uint32_t sc[MT];
 #pragma unroll
-        for (int t = 0; t < kMaxGTerms; t++) {
+        for (int t = 0; t < MT; t++) {
             uint64_t o = 0;
-            if (t < (int)a.nt)
+            if (t < nt)
                 for (int k = 0; k < kMaxDep; k++) o += (uint64_t)d[k] * a.t[t].sd[k];
-            off[t] = o;
+            base[t] = (const KeyT *)a.t[t < nt ? t : 0].ptr + (t < nt ? o : 0);
+            sc[t] = t < nt ? a.t[t].sc : 0;
         }
-        KeyT best = Ops::sentinel();
-        for (uint32_t c = 0; c < a.K; c++) {
-            KeyT key = ((const KeyT *)a.t[0].ptr)[(uint64_t)c * a.t[0].sc + off[0]];
+        KeyT best0 = Ops::sentinel(), best1 = Ops::sentinel();
+        uint32_t c = lane;
+        // two independent chains keep two loads of every term in flight
+        for (; c + G < a.K; c += 2 * G) {
+            KeyT k0 = base[0][(uint64_t)c * sc[0]];
+            KeyT k1 = base[0][(uint64_t)(c + G) * sc[0]];
 #pragma unroll
-            for (int t = 1; t < kMaxGTerms; t++)
-                if (t < (int)a.nt)
-                    key = Ops::add(key, ((const KeyT *)a.t[t].ptr)[(uint64_t)c * a.t[t].sc + off[t]]);
-            best = Ops::min(best, key);
+            for (int t = 1; t < MT; t++)
+                if (t < nt) {
+                    k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
+                    k1 = Ops::add(k1, base[t][(uint64_t)(c + G) * sc[t]]);
+                }
+            best0 = Ops::min(best0, k0);
+            best1 = Ops::min(best1, k1);
         }
-        Val v;
-        uint32_t cc;
-        Ops::split(best, a.bits, a.out_shift, v, cc);
-        ((Val *)a.T)[phi] = v;
-        a.A[phi] = (uint16_t)cc;
+        if (c < a.K) {
+            KeyT k0 = base[0][(uint64_t)c * sc[0]];
+#pragma unroll
+            for (int t = 1; t < MT; t++)
+                if (t < nt) k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
+            best0 = Ops::min(best0, k0);
+        }
+        KeyT best = Ops::min(best0, best1);
+        for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
+        if (live && lane == 0) {
+            Val v;
+            uint32_t cc;
+            Ops::split(best, a.bits, a.out_shift, v, cc);
+            ((Val *)a.T)[phi] = v;
+            a.A[phi] = (uint16_t)cc;
+        }
     }
 }
 
@@ -600,6 +673,10 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             boff += (bk.elems + 31) / 32 * 32;
             bk.c_begin = cb;
             bk.c_end = (uint32_t)contrib.size();
+            bk.rows = (uint32_t)el;
+            bk.chunks = (uint32_t)(((uint64_t)vp.K * ld + kPrepThreads - 1) / kPrepThreads);
+            bk.wg_begin = L.prep.nwg;
+            L.prep.nwg += bk.rows * bk.chunks;
             L.prep.total += bk.elems;
             return (int)L.prep.nblocks++;
         };
@@ -725,6 +802,10 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             ga.m = (uint32_t)vp.layout.size();
             ga.K = vp.K;
             ga.bits = vp.bits;
+            // lanes per entry: enough threads to fill the GPU, at most one wave, at most K
+            ga.group_log2 = 0;
+            while (ga.group_log2 < 6 && (vp.N << ga.group_log2) < 65536 && (2u << ga.group_log2) <= vp.K)
+                ga.group_log2++;
             for (size_t k = 0; k < vp.layout.size(); k++) ga.rad[k] = g->K[vp.layout[k]];
             ga.T = ws + P.off_T + vp.T_off;
             ga.A = (uint16_t *)(ws + P.off_A + vp.A_off);
@@ -772,6 +853,21 @@ static bool launch_rows(const RowsArgs &ra, uint32_t TZ, hipStream_t s) {
     }
 }
 
+template <typename KeyT>
+static void launch_generic(const GenericArgs &ga, hipStream_t s) {
+    uint64_t threads = (uint64_t)ga.N << ga.group_log2;
+    dim3 grid((uint32_t)std::min<uint64_t>((threads + 255) / 256, 65535)), block(256);
+    switch (ga.nt) {
+    case 1: hipLaunchKernelGGL((k_fill_generic<KeyT, 1>), grid, block, 0, s, ga); break;
+    case 2: hipLaunchKernelGGL((k_fill_generic<KeyT, 2>), grid, block, 0, s, ga); break;
+    case 3: hipLaunchKernelGGL((k_fill_generic<KeyT, 3>), grid, block, 0, s, ga); break;
+    case 4: hipLaunchKernelGGL((k_fill_generic<KeyT, 4>), grid, block, 0, s, ga); break;
+    case 5: hipLaunchKernelGGL((k_fill_generic<KeyT, 5>), grid, block, 0, s, ga); break;
+    case 6: hipLaunchKernelGGL((k_fill_generic<KeyT, 6>), grid, block, 0, s, ga); break;
+    default: hipLaunchKernelGGL((k_fill_generic<KeyT, -1>), grid, block, 0, s, ga); break;
+    }
+}
+
 static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) {
     uint64_t b = (n + block - 1) / block;
     return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, cap));
@@ -780,7 +876,7 @@ static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) 
 template <typename KeyT>
 static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t *min_cost, uint32_t *cfg) {
     DeviceState *d = g->dev;
-    const Plan &P = g->plan;
+    Plan &P = g->plan;
     const int n = (int)P.v.size();
     const size_t nv = g->V.size(), ne = g->E.size();
 
@@ -810,6 +906,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     }
     std::memcpy(img + P.off_vert, dvs.data(), nv * sizeof(DevVertex));
     std::vector<DevEdge> des(ne);
+    uint64_t sig_off = 0;
     for (size_t e = 0; e < ne; e++) {
         DevEdge &x = des[e];
         std::memset(&x, 0, sizeof x);
@@ -821,6 +918,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             x.ddim[k] = (int8_t)(k < x.rank ? g->E[e].dst_dim[k] : -1);
         }
         x.elems = g->E[e].elems;
+        x.sig_off = sig_off;
+        sig_off += (uint64_t)g->K[x.src] + g->K[x.dst];
     }
     if (ne) std::memcpy(img + P.off_edge, des.data(), ne * sizeof(DevEdge));
     if (g->overridden) {
@@ -848,12 +947,14 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     const DevEdge *dE = (const DevEdge *)(ws + P.off_edge);
     const uint8_t *dex = (const uint8_t *)(ws + P.off_ex);
     uint64_t *dL = (uint64_t *)(ws + P.off_L);
+    uint8_t *dls = (uint8_t *)(ws + P.off_lsum);
+    uint64_t *dsig = (uint64_t *)(ws + P.off_sig);
     const Contrib *dC = (const Contrib *)(ws + P.off_contrib);
     KeyT *dB = (KeyT *)(ws + P.off_block);
     uint32_t launches_n = 0;
     if (!g->overridden) {
-        hipLaunchKernelGGL(k_layer_costs, dim3(grid_for(loff)), dim3(256), 0, s, dV, (uint32_t)nv, dex, dL,
-                           loff, g->r);
+        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
+                           dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
         launches_n++;
     }
     // per-vertex contribution ranges were recorded relative to the global list
@@ -867,15 +968,15 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     for (int i = 0; i < n; i++) {
         Launch<KeyT> &L = launches[i];
         const VPlan &vp = P.v[i];
-        hipLaunchKernelGGL((k_prep<KeyT>), dim3(grid_for(L.prep.total)), dim3(256), 0, s, L.prep, dV, dE, dex,
-                           (const uint64_t *)dL, dC, dB, g->r);
+        hipLaunchKernelGGL((k_prep<KeyT>), dim3(L.prep.nwg), dim3(kPrepThreads), 0, s, L.prep, dV, dE,
+                           (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, dB, g->r);
         launches_n++;
         // with profiling, events bracket exactly the fill kernel of this vertex
         if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i], s));
         if (L.rows) {
             if (!launch_rows<KeyT>(L.ra, vp.TZ, s)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
         } else {
-            hipLaunchKernelGGL((k_fill_generic<KeyT>), dim3(grid_for(vp.N, 256, 65535)), dim3(256), 0, s, L.ga);
+            launch_generic<KeyT>(L.ga, s);
         }
         launches_n++;
         if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i + 1], s));
@@ -909,6 +1010,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             float ms = 0;
             HIPCHK(hipEventElapsedTime(&ms, d->ev[2 * i], d->ev[2 * i + 1]));
             g->stats.fill_ms += ms;
+            g->plan.v[i].fill_ms = ms;
             if (launches[i].rows) { g->stats.rows_fill_ms += ms; g->stats.rows_launches++; }
         }
     }
@@ -1026,7 +1128,8 @@ pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
     uint64_t *tmp = nullptr;
     HIPCHK(hipMalloc(&tmp, n * 8));
     hipLaunchKernelGGL(k_edge_costs, dim3(grid_for(n)), dim3(256), 0, 0, (const DevVertex *)(ws + P.off_vert),
-                       (const DevEdge *)(ws + P.off_edge), e, (const uint8_t *)(ws + P.off_ex), tmp, g->r);
+                       (const DevEdge *)(ws + P.off_edge), e, (const uint8_t *)(ws + P.off_lsum),
+                       (const uint64_t *)(ws + P.off_sig), tmp, g->r);
     hipError_t err = hipMemcpy(out, tmp, n * 8, hipMemcpyDeviceToHost);
     (void)hipFree(tmp);
     HIPCHK(err);

@@ -173,7 +173,7 @@ struct RowsChoice {
     double cost = 0;
     int z = -1;
     std::vector<int> O, R;
-    uint32_t TZ = 0;
+    uint32_t TZ = 0, na = 0;
     uint64_t MO = 1, MR = 1;
 };
 
@@ -295,6 +295,7 @@ static pase_status build_plan(pase_graph_t g) {
                     if (touches && P.v[t.j].N * 8 >= (1ull << 31)) small = false;
                 }
                 if (na > (uint32_t)kMaxATerms || !small) continue;
+                rc.na = na;
                 const uint32_t Kz = g->K[z];
                 for (uint32_t tz : kTZ) {
                     uint64_t nch = (Kz + tz - 1) / tz;
@@ -314,6 +315,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.MO = best.MO;
             vp.MR = best.MR;
             vp.TZ = best.TZ;
+            vp.na = best.na;
             vp.nchunks = (g->K[vp.z] + vp.TZ - 1) / vp.TZ;
             vp.ldz = vp.nchunks * vp.TZ;
             vp.layout.clear();
@@ -332,6 +334,21 @@ static pase_status build_plan(pase_graph_t g) {
         } else {
             vp.kernel = kGeneric;
             vp.layout = vp.D;
+            // threads walk the table in layout order: follow the memory order of the
+            // largest lookup that spans several digits so that its reads coalesce
+            int big = -1;
+            for (size_t t = 0; t < vp.terms.size(); t++)
+                if (vp.terms[t].dig.size() >= 2 && (big < 0 || P.v[vp.terms[t].j].N > P.v[vp.terms[big].j].N))
+                    big = (int)t;
+            if (big >= 0) {
+                const VPlan &pj = P.v[vp.terms[big].j];
+                std::vector<int> order;
+                for (int u : pj.layout)
+                    if (u != vp.vi) order.push_back(u);   // slowest first in T_j
+                for (int u : vp.D)
+                    if (std::find(order.begin(), order.end(), u) == order.end()) order.insert(order.begin(), u);
+                vp.layout = order;
+            }
             vp.nsplit = 1;
             vp.cper = vp.K;
         }
@@ -364,6 +381,12 @@ static pase_status layout_memory(pase_graph_t g) {
     uint64_t sumK = 0;
     for (uint32_t k : g->K) sumK += k;
     off = align_up(off + sumK * 8, A);
+    P.off_lsum = off;
+    off = align_up(off + sumK, A);
+    P.sig_count = 0;
+    for (const auto &d : g->E) P.sig_count += (uint64_t)g->K[d.src] + g->K[d.dst];
+    P.off_sig = off;
+    off = align_up(off + P.sig_count * 8, A);
     P.off_ovedge = off;
     if (g->overridden) off = align_up(off + g->ov_edge.size() * 8, A);
     // contributions: count per vertex (layer + edges + lookups is an upper bound)
@@ -677,5 +700,30 @@ extern "C" pase_status pase_stats(pase_graph_t g, pase_run_stats *out) {
     if (!g || !out) return PASE_ERR_INVALID_ARGUMENT;
     if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");
     *out = g->stats;
+    return PASE_OK;
+}
+
+extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out) {
+    if (!g || !out) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    if (v >= g->V.size()) return fail(g, PASE_ERR_INVALID_ARGUMENT, "vertex id out of range");
+    const VPlan &vp = g->plan.v[g->plan.pos[v]];
+    pase_vertex_info x;
+    std::memset(&x, 0, sizeof x);
+    x.position = (uint32_t)g->plan.pos[v];
+    x.kernel = vp.kernel == kRows ? 1 : 0;
+    x.num_configs = vp.K;
+    x.dep_count = (uint32_t)vp.D.size();
+    x.entries = vp.N;
+    x.cells = vp.N * vp.K;
+    x.column = vp.kernel == kRows ? vp.z : -1;
+    x.outer = (uint32_t)vp.MO;
+    x.rows = (uint32_t)vp.MR;
+    x.tile_cols = vp.TZ;
+    x.splits = vp.nsplit;
+    x.row_terms = vp.na;
+    x.lookups = (uint32_t)vp.terms.size();
+    x.fill_ms = vp.fill_ms;
+    *out = x;
     return PASE_OK;
 }

@@ -39,6 +39,7 @@ struct DevEdge {
     uint32_t src, dst, rank, pad;
     int8_t sdim[kMaxDims], ddim[kMaxDims];
     uint64_t elems;
+    uint64_t sig_off;         // element offset of its split signatures: K_src, then K_dst
 };
 
 // One contribution to a precomputed block element (see Prep below).
@@ -69,11 +70,17 @@ struct Block {
     uint32_t postrad;         // its radix (columns actually filled)
     uint32_t ld;              // row pitch (>= postrad, padded columns hold 0)
     uint32_t c_begin, c_end;  // contribution range
+    uint32_t rows;            // prod(pre radices)
+    uint32_t chunks;          // workgroups per row: ceil(K * ld / kPrepThreads)
+    uint32_t wg_begin;        // first workgroup of this block
 };
+
+constexpr uint32_t kPrepThreads = 256;
 
 struct PrepArgs {
     uint32_t vi, K, bits, nblocks;
     uint64_t total;           // sum of block elements
+    uint32_t nwg, pad;        // workgroups of the launch
     Block blk[kMaxBlocks];
 };
 
@@ -111,6 +118,8 @@ struct GTerm {                // term of the generic kernel (key space)
 
 struct GenericArgs {
     uint32_t m, K, bits, nt;
+    uint32_t group_log2;      // lanes per entry = 2^group_log2 (c is strided over them)
+    uint32_t pad2;
     uint32_t rad[kMaxDep];    // radices of the plan digits (= T_i layout), slowest first
     GTerm t[kMaxGTerms];
     void *T;
@@ -165,6 +174,8 @@ struct VPlan {
     std::vector<int> O, R;          // outer / row digits (vertex ids), slowest first
     uint32_t TZ = 0, ldz = 0, nchunks = 0, nsplit = 1, cper = 0;
     uint64_t MO = 1, MR = 1;
+    uint32_t na = 0;                // row kernel: per-lane row terms
+    double fill_ms = 0;             // last profiled fill time
     // memory
     uint64_t T_off = 0, A_off = 0;  // bytes into the table arenas
     uint64_t block_elems = 0;       // block scratch this vertex needs
@@ -176,10 +187,12 @@ struct Plan {
     uint64_t cells = 0, entries = 0, rows_cells = 0;
     uint32_t max_dep = 0, rows_vertices = 0;
     // workspace layout, byte offsets from the workspace base
-    uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_ovedge = 0, off_contrib = 0,
+    uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_lsum = 0, off_sig = 0,
+             off_ovedge = 0, off_contrib = 0,
              off_bt = 0, off_cfg = 0, off_out = 0, off_T = 0, off_A = 0, off_block = 0,
              off_partial = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
+    uint64_t sig_count = 0;         // split signatures of all edge endpoints
 };
 
 struct DeviceState;   // defined by the device runtime

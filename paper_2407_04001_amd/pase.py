@@ -48,11 +48,22 @@ class RunStats(C.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+class VertexInfo(C.Structure):
+    _fields_ = [("position", C.c_uint32), ("kernel", C.c_uint32), ("num_configs", C.c_uint32),
+                ("dep_count", C.c_uint32), ("entries", C.c_uint64), ("cells", C.c_uint64),
+                ("column", C.c_int32), ("outer", C.c_uint32), ("rows", C.c_uint32),
+                ("tile_cols", C.c_uint32), ("splits", C.c_uint32), ("row_terms", C.c_uint32),
+                ("lookups", C.c_uint32), ("fill_ms", C.c_double)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
 EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_enumerate_configs",
            "pase_num_configs", "pase_config_splits", "pase_get_sequence", "pase_get_dependent_set",
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
-           "pase_layer_costs", "pase_edge_costs", "pase_stats"]
+           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get"]
 
 _lib = None
 
@@ -87,6 +98,7 @@ def load(path: str = LIB_PATH):
         "pase_layer_costs": (st, [P, U32, P]),
         "pase_edge_costs": (st, [P, U32, P]),
         "pase_stats": (st, [P, P]),
+        "pase_vertex_info_get": (st, [P, U32, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -232,6 +244,12 @@ def pase_stats(h) -> dict:
     return s.as_dict()
 
 
+def pase_vertex_info_get(h, v: int) -> dict:
+    x = VertexInfo()
+    _check(h, load().pase_vertex_info_get(h, int(v), C.byref(x)))
+    return x.as_dict()
+
+
 # ------------------------------------------------------------------ convenience wrapper
 class Graph:
     """A computation graph handle.  ``graph`` is a dict in the layout of
@@ -312,3 +330,6 @@ class Graph:
 
     def stats(self) -> dict:
         return pase_stats(self.h)
+
+    def vertex_info(self, v: int) -> dict:
+        return pase_vertex_info_get(self.h, v)
