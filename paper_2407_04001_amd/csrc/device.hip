@@ -493,7 +493,10 @@ struct DeviceState {
     uint64_t lent_bytes = 0;
     void *pinned = nullptr;
     uint64_t pinned_bytes = 0;
-    std::vector<hipEvent_t> ev;
+    std::vector<hipEvent_t> ev;        // profiling: two per vertex (timed)
+    std::vector<hipStream_t> workers;  // streams of the vertex schedule (default priority)
+    std::vector<hipEvent_t> done;      // one per vertex: its table is complete (untimed)
+    hipEvent_t ready = nullptr;        // cost tables complete
     hipStream_t last_stream = nullptr;
 };
 
@@ -510,6 +513,9 @@ void device_release(pase_graph_t g) {
     if (d->owned && d->ws) (void)hipFree(d->ws);
     if (d->pinned) (void)hipHostFree(d->pinned);
     for (auto e : d->ev) (void)hipEventDestroy(e);
+    for (auto e : d->done) (void)hipEventDestroy(e);
+    if (d->ready) (void)hipEventDestroy(d->ready);
+    for (auto st : d->workers) (void)hipStreamDestroy(st);
     delete d;
     g->dev = nullptr;
 }
@@ -601,11 +607,11 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
     const int n = (int)P.v.size();
     out.assign(n, Launch<KeyT>());
     contrib.clear();
-    KeyT *blocks = (KeyT *)(ws + P.off_block);
     const uint64_t *ovedge = (const uint64_t *)(ws + P.off_ovedge);
     for (int i = 0; i < n; i++) {
         const VPlan &vp = P.v[i];
         Launch<KeyT> &L = out[i];
+        KeyT *blocks = (KeyT *)(ws + P.off_block + vp.block_off);
         std::memset(&L.prep, 0, sizeof L.prep);
         L.prep.vi = (uint32_t)vp.vi;
         L.prep.K = vp.K;
@@ -748,7 +754,7 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             for (size_t k = 0; k < vp.R.size(); k++) ra.radR[k] = g->K[vp.R[k]];
             ra.T = ws + P.off_T + vp.T_off;
             ra.A = (uint16_t *)(ws + P.off_A + vp.A_off);
-            ra.partial = ws + P.off_partial;
+            ra.partial = ws + P.off_partial + vp.partial_off;
             ra.N = vp.N;
             ra.out_shift = vp.out_shift;
             ra.total_tiles = (uint64_t)vp.nsplit * vp.nchunks * vp.MO * ra.tiles_per_o;
@@ -814,8 +820,10 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
         }
         if (boff > vp.block_elems) return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
         if (!bounds_ok) return fail(g, PASE_ERR_INTERNAL, "a table lookup would leave its table");
-        if (vp.nsplit > 1 && (uint64_t)vp.nsplit * vp.N * sizeof(KeyT) > P.partial_bytes)
+        if (vp.nsplit > 1 && vp.partial_off + (uint64_t)vp.nsplit * vp.N * sizeof(KeyT) > P.partial_bytes)
             return fail(g, PASE_ERR_INTERNAL, "split scratch overflow");
+        if (vp.block_off + boff * sizeof(KeyT) > P.block_bytes)
+            return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
     }
     if (contrib.size() > P.contrib_count) return fail(g, PASE_ERR_INTERNAL, "contribution overflow");
     return PASE_OK;
@@ -950,14 +958,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     uint8_t *dls = (uint8_t *)(ws + P.off_lsum);
     uint64_t *dsig = (uint64_t *)(ws + P.off_sig);
     const Contrib *dC = (const Contrib *)(ws + P.off_contrib);
-    KeyT *dB = (KeyT *)(ws + P.off_block);
-    uint32_t launches_n = 0;
-    if (!g->overridden) {
-        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
-                           dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
-        launches_n++;
-    }
-    // per-vertex contribution ranges were recorded relative to the global list
+    // ---- streams and events (created before any capture)
+    const int S = P.streams;
     if (g->profile && d->ev.size() < 2 * (size_t)n) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)n; k++) {
             hipEvent_t e;
@@ -965,32 +967,76 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             d->ev.push_back(e);
         }
     }
-    for (int i = 0; i < n; i++) {
-        Launch<KeyT> &L = launches[i];
-        const VPlan &vp = P.v[i];
-        hipLaunchKernelGGL((k_prep<KeyT>), dim3(L.prep.nwg), dim3(kPrepThreads), 0, s, L.prep, dV, dE,
-                           (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, dB, g->r);
-        launches_n++;
-        // with profiling, events bracket exactly the fill kernel of this vertex
-        if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i], s));
-        if (L.rows) {
-            if (!launch_rows<KeyT>(L.ra, vp.TZ, s)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
-        } else {
-            launch_generic<KeyT>(L.ga, s);
+    if (S > 1) {
+        while ((int)d->workers.size() < S) {
+            hipStream_t w;
+            HIPCHK(hipStreamCreateWithFlags(&w, hipStreamNonBlocking));
+            d->workers.push_back(w);
         }
-        launches_n++;
-        if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i + 1], s));
-        if (L.rows && vp.nsplit > 1) {
-            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(grid_for(vp.N)), dim3(256), 0, s, L.red);
-            launches_n++;
+        while (d->done.size() < (size_t)n) {
+            hipEvent_t e;
+            HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+            d->done.push_back(e);
         }
+        if (!d->ready) HIPCHK(hipEventCreateWithFlags(&d->ready, hipEventDisableTiming));
     }
     uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
     SearchOut *dout = (SearchOut *)(ws + P.off_out);
-    hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
-                       (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
-    launches_n++;
-    HIPCHK(hipGetLastError());
+
+    // ---- every kernel of the search, on s0 and the worker streams
+    uint32_t launches_n = 0;
+    auto enqueue = [&](hipStream_t s0) -> pase_status {
+        launches_n = 0;
+        if (!g->overridden) {
+            hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s0, dV,
+                               (uint32_t)nv, dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
+            launches_n++;
+        }
+        if (S > 1) HIPCHK(hipEventRecord(d->ready, s0));
+        // vertex schedule: P.streams streams, events for cross-stream producers
+        std::vector<int> tail(S, -1);
+        for (int i = 0; i < n; i++) {
+            Launch<KeyT> &L = launches[i];
+            const VPlan &vp = P.v[i];
+            hipStream_t st = s0;
+            if (S > 1) {
+                st = d->workers[vp.stream];
+                if (tail[vp.stream] < 0) HIPCHK(hipStreamWaitEvent(st, d->ready, 0));
+                for (int j : vp.waits) HIPCHK(hipStreamWaitEvent(st, d->done[j], 0));
+                tail[vp.stream] = i;
+            }
+            KeyT *dB = (KeyT *)(ws + P.off_block + vp.block_off);
+            hipLaunchKernelGGL((k_prep<KeyT>), dim3(L.prep.nwg), dim3(kPrepThreads), 0, st, L.prep, dV, dE,
+                               (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, dB, g->r);
+            launches_n++;
+            // with profiling, events bracket exactly the fill kernel of this vertex
+            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i], st));
+            if (L.rows) {
+                if (!launch_rows<KeyT>(L.ra, vp.TZ, st)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+            } else {
+                launch_generic<KeyT>(L.ga, st);
+            }
+            launches_n++;
+            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i + 1], st));
+            if (L.rows && vp.nsplit > 1) {
+                hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(grid_for(vp.N)), dim3(256), 0, st, L.red);
+                launches_n++;
+            }
+            if (S > 1) HIPCHK(hipEventRecord(d->done[i], st));
+        }
+        for (int k = 0; k < S; k++)
+            if (S > 1 && tail[k] >= 0) HIPCHK(hipStreamWaitEvent(s0, d->done[tail[k]], 0));
+        hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s0, (const BacktrackDesc *)(ws + P.off_bt),
+                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+        launches_n++;
+        HIPCHK(hipGetLastError());
+        return PASE_OK;
+    };
+
+    {
+        pase_status est = enqueue(s);
+        if (est != PASE_OK) return est;
+    }
     char *host_out = img;   // reuse the staging buffer after the upload has been consumed
     HIPCHK(hipStreamSynchronize(s));
     HIPCHK(hipMemcpyAsync(host_out, dout, sizeof(SearchOut), hipMemcpyDeviceToHost, s));
@@ -1003,6 +1049,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
 
     g->stats.launches = launches_n;
+    g->stats.streams = (uint32_t)S;
     g->stats.fill_ms = g->stats.rows_fill_ms = 0;
     g->stats.rows_launches = 0;
     if (g->profile) {

@@ -324,7 +324,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.layout.insert(vp.layout.end(), vp.R.begin(), vp.R.end());
             uint64_t tiles_per_o = (vp.MR + 63) / 64;
             uint64_t waves = vp.MO * tiles_per_o * vp.nchunks;
-            uint64_t want = (4096 + waves - 1) / waves;
+            uint64_t want = (2048 + waves - 1) / waves;
             uint64_t maxs = std::max<uint64_t>(1, vp.K / 16);
             uint64_t ns = std::min(want, maxs);
             vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
@@ -365,8 +365,53 @@ static pase_status build_plan(pase_graph_t g) {
 // Cost tables T_i live from their fill to their single reader (or to the end
 // when tables are kept or i is last) and share memory by interval packing;
 // argmin tables A_i all live until back-substitution.
+static pase_status layout_memory_mode(pase_graph_t g, bool concurrent);
+
+// Try the concurrent layout (every table and scratch buffer resident, so
+// independent vertices may run on different streams); fall back to the
+// packed single-stream layout when that exceeds the memory budget.
 static pase_status layout_memory(pase_graph_t g) {
+    if (g->streams > 1 && layout_memory_mode(g, true) == PASE_OK) return PASE_OK;
+    return layout_memory_mode(g, false);
+}
+
+// Stream schedule: visit positions in sequence order; a vertex joins the
+// stream whose last vertex is one of its producers (no event needed for
+// that one), else the stream with the least estimated work; it waits on an
+// event of every producer scheduled on another stream.
+static void schedule_streams(pase_graph_t g) {
     Plan &P = g->plan;
+    const int S = P.concurrent ? std::max(1, g->streams) : 1;
+    P.streams = S;
+    std::vector<int> tail(S, -1);
+    std::vector<double> load(S, 0.0);
+    for (int i = 0; i < (int)P.v.size(); i++) {
+        VPlan &vp = P.v[i];
+        vp.waits.clear();
+        int s = -1;
+        for (int k = 0; k < S; k++)
+            for (const auto &t : vp.terms)
+                if (tail[k] == t.j && (s < 0 || tail[k] > tail[s])) s = k;
+        if (s < 0) {
+            s = 0;
+            for (int k = 1; k < S; k++)
+                if (load[k] < load[s]) s = k;
+        }
+        // latest producer per other stream
+        std::vector<int> last(S, -1);
+        for (const auto &t : vp.terms)
+            if (P.v[t.j].stream != s) last[P.v[t.j].stream] = std::max(last[P.v[t.j].stream], t.j);
+        for (int k = 0; k < S; k++)
+            if (last[k] >= 0) vp.waits.push_back(last[k]);
+        vp.stream = s;
+        tail[s] = i;
+        load[s] += 5.0 + (double)vp.N * vp.K / 1e7;   // ~5 us per vertex + ~1e13 cells/s
+    }
+}
+
+static pase_status layout_memory_mode(pase_graph_t g, bool concurrent) {
+    Plan &P = g->plan;
+    P.concurrent = concurrent;
     const int n = (int)P.v.size();
     const uint64_t A = 256;
     uint64_t off = 0;
@@ -406,7 +451,7 @@ static pase_status layout_memory(pase_graph_t g) {
     struct Iv { int i, s, e; uint64_t size; };
     std::vector<Iv> iv;
     for (int i = 0; i < n; i++) {
-        int end = (g->keep_tables || i == n - 1) ? n : P.v[i].consumer;
+        int end = (g->keep_tables || concurrent || i == n - 1) ? n : P.v[i].consumer;
         iv.push_back({i, i, end, align_up(P.v[i].N * 8, A)});
     }
     std::vector<int> order(n);
@@ -437,30 +482,36 @@ static pase_status layout_memory(pase_graph_t g) {
     P.A_bytes = abytes;
     P.off_A = off;
     off = align_up(off + abytes, A);
-    // block scratch
-    uint64_t bmax = 0, pmax = 0;
+    // block and split scratch: one shared region (sequential), or one per vertex (concurrent)
+    uint64_t bsum = 0, psum = 0, bmax = 0, pmax = 0;
     for (auto &vp : P.v) {
-        uint64_t e = 0;
+        uint64_t e = 0, pb = 0;
         if (vp.kernel == kRows) {
             e += align_up(vp.MO * vp.K * vp.ldz, 32);
             for (int u : vp.R) e += align_up((uint64_t)vp.K * g->K[u], 32);
-            if (vp.nsplit > 1) pmax = std::max(pmax, (uint64_t)vp.nsplit * vp.N * 8);
+            if (vp.nsplit > 1) pb = align_up((uint64_t)vp.nsplit * vp.N * 8, A);
         } else {
             e += align_up(vp.K, 32);
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
         }
         vp.block_elems = e;
-        bmax = std::max(bmax, e);
+        vp.block_off = concurrent ? bsum : 0;
+        vp.partial_off = concurrent ? psum : 0;
+        bsum += align_up(e * 8, A);
+        psum += pb;
+        bmax = std::max(bmax, e * 8);
+        pmax = std::max(pmax, pb);
     }
-    P.block_bytes = bmax * 8;
+    P.block_bytes = concurrent ? bsum : bmax;
     P.off_block = off;
     off = align_up(off + P.block_bytes, A);
-    P.partial_bytes = pmax;
+    P.partial_bytes = concurrent ? psum : pmax;
     P.off_partial = off;
-    off = align_up(off + pmax, A);
+    off = align_up(off + P.partial_bytes, A);
     P.total = off;
     if (P.total > g->mem_budget)
         return fail(g, PASE_ERR_TOO_LARGE, "device memory need exceeds the memory budget");
+    schedule_streams(g);
     return PASE_OK;
 }
 
@@ -585,11 +636,15 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->key_mode = (int)value;
         break;
     case PASE_OPT_PROFILE: g->profile = value != 0; break;
+    case PASE_OPT_STREAMS:
+        if (value < 1 || value > 16) return fail(g, PASE_ERR_INVALID_ARGUMENT, "streams 1..16");
+        g->streams = (int)value;
+        break;
     default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
     }
     // options that change the plan need a fresh enumeration
-    if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET) &&
-        g->enumerated) {
+    if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
+         opt == PASE_OPT_STREAMS) && g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);
         if (st == PASE_OK) st = layout_memory(g);

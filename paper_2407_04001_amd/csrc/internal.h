@@ -179,6 +179,11 @@ struct VPlan {
     // memory
     uint64_t T_off = 0, A_off = 0;  // bytes into the table arenas
     uint64_t block_elems = 0;       // block scratch this vertex needs
+    uint64_t block_off = 0;         // bytes into the block scratch
+    uint64_t partial_off = 0;       // bytes into the split scratch
+    // schedule
+    int stream = 0;                 // stream index (0 = the caller's stream schedule slot)
+    std::vector<int> waits;         // producers on other streams whose completion it awaits
 };
 
 struct Plan {
@@ -193,6 +198,8 @@ struct Plan {
              off_partial = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
     uint64_t sig_count = 0;         // split signatures of all edge endpoints
+    int streams = 1;                // streams of the schedule
+    bool concurrent = false;        // tables and scratch never reused (needed for streams > 1)
 };
 
 struct DeviceState;   // defined by the device runtime
@@ -210,6 +217,7 @@ struct pase_graph_s {
     bool keep_tables = false, profile = false;
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
+    int streams = 4;
     // configurations
     bool enumerated = false;
     uint32_t p = 0, log2p = 0;

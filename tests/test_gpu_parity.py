@@ -65,12 +65,13 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
         assert pg.fingerprint(v) == o.fingerprint(i)
 
 
-def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0):
+def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, streams=4):
     pg = P.Graph(g, seq_rule=rule)
     pg.enumerate_configs(p or g["p"])
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
     pg.set_option(P.OPT_KEY_TYPE, key)
+    pg.set_option(P.OPT_STREAMS, streams)
     if costs is not None:
         pg.override_costs(*costs)
     mc, strat = pg.find_best_strategy()
@@ -174,6 +175,7 @@ def test_library_owned_workspace(P):
     pg.enumerate_configs(g["p"])
     mc, strat = pg.find_best_strategy(torch_workspace=False)
     assert (mc, strat) == _oracle(g).result()
+    assert pg.stats()["streams"] == 4
 
 
 # ------------------------------------------------------------------ full-size workloads
@@ -182,14 +184,14 @@ def _golden(name, seed):
         return json.load(f)
 
 
-def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True):
+def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, streams=4):
     gold = _golden(name, seed)
     g = workload(name, seed)
-    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep}")
-    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key)
+    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} streams={streams}")
+    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, streams=streams)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
-        f"rows_vertices {st['rows_vertices']}")
+        f"rows_vertices {st['rows_vertices']} streams {st['streams']}")
     assert pg.K == gold["num_configs"]
     assert pg.sequence() == gold["sequence"]
     assert st["cells"] == gold["cells"]
@@ -224,6 +226,41 @@ def test_workloads_against_golden(P, name, seed):
 def test_generic_and_u64_paths_against_golden(P, name):
     _check_golden(P, name, 0, kernel=1)
     _check_golden(P, name, 0, key=1)
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
+def test_single_stream_against_golden(P, name):
+    """The strictly sequential schedule (packed table arena) gives the same answer."""
+    _check_golden(P, name, 0, keep=False, streams=1)
+
+
+@pytest.mark.skip(reason="captured HIP-graph replay of the search was removed: its first GPU run "
+                         "ended in a host segmentation fault inside pase_find_best_strategy (W2, first "
+                         "capture) whose cause was not found; the search now uses direct launches")
+@pytest.mark.parametrize("name", ["w2_inception", "w4_transformer"])
+def test_graph_replays_match_direct_launches(P, name):
+    """The captured HIP graph is replayed several times, with unrelated eager
+    GPU work and synchronisations in between; every replay must equal the
+    result of direct launches (and the oracle's)."""
+    import torch
+    gold = _golden(name, 0)
+    g = workload(name)
+    say(f"graph replays {name}")
+    _, mc0, st0 = _run(P, g, keep=False)
+    assert (mc0, st0) == (int(gold["min_cost"]), gold["strategy"])
+    pg = P.Graph(g)
+    for rep in range(4):
+        pg.enumerate_configs(g["p"])
+        mc, st = pg.find_best_strategy()
+        x = torch.randn(512, 512, device="cuda")
+        (x @ x).sum().item()
+        torch.cuda.synchronize()
+        assert (mc, st) == (mc0, st0), rep
+    # a different plan (other p) forces a new capture; going back replays again
+    pg.enumerate_configs(g["p"] // 2)
+    pg.find_best_strategy()
+    pg.enumerate_configs(g["p"])
+    assert pg.find_best_strategy() == (mc0, st0)
 
 
 def test_transformer_p64_against_golden(P):
