@@ -97,11 +97,10 @@ typedef enum {
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
     PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats) */
-    PASE_OPT_STREAMS = 6        /* HIP streams the per-vertex work is spread over, following the
-                                   dependencies between DP tables (default 4; 1 = strictly in
-                                   sequence order).  More than 1 needs every table and scratch
-                                   buffer resident at once; if that exceeds the memory budget the
-                                   search runs on one stream. */
+    PASE_OPT_SCHEDULE = 6       /* 0 (default): vertices of one dependency level (whose tables
+                                   do not read each other) share their kernel launches and run
+                                   concurrently; 1: one vertex at a time in sequence order.  Memory
+                                   is packed by table lifetimes in either case. */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */
@@ -119,7 +118,7 @@ typedef struct {
     double fill_ms;            /* PASE_OPT_PROFILE: sum of fill-kernel event times */
     double rows_fill_ms;       /* PASE_OPT_PROFILE: same, row/column-chunk kernel only */
     uint32_t rows_launches;    /* PASE_OPT_PROFILE: launches of that kernel */
-    uint32_t streams;          /* streams the search used */
+    uint32_t slots;            /* launch slots: dependency levels, or vertices when sequential */
 } pase_run_stats;
 
 /* Copy a computation graph G=(V,E) (Sec. II) into a new handle.

@@ -155,20 +155,35 @@ __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__r
 }
 
 // ------------------------------------------------------------------ prep: key-space blocks
+// Batched launches: the workgroups of one launch are the concatenation of the
+// workgroups of its vertices; find the vertex of this workgroup (uniform).
+__device__ __forceinline__ uint32_t batch_find(const BatchEntry *__restrict__ be, uint32_t nbe, uint32_t wg) {
+    uint32_t lo = 0, hi = nbe;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (be[mid].first <= wg) lo = mid; else hi = mid;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
 // One workgroup handles kPrepThreads consecutive (c, column) elements of one
 // outer index of one block, so the block, its contributions and the outer
 // digits are uniform across the workgroup (scalar loads); lanes differ only in
 // (c, column).
 template <typename KeyT>
-__global__ __launch_bounds__(kPrepThreads) void k_prep(PrepArgs a, const DevVertex *__restrict__ V,
+__global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restrict__ descs,
+                                                     const BatchEntry *__restrict__ be, uint32_t nbe,
+                                                     const DevVertex *__restrict__ V,
                                                      const DevEdge *__restrict__ E,
                                                      const uint64_t *__restrict__ L,
                                                      const uint8_t *__restrict__ lsum,
                                                      const uint64_t *__restrict__ sig,
-                                                     const Contrib *__restrict__ cb,
-                                                     KeyT *__restrict__ blocks, uint64_t r) {
+                                                     const Contrib *__restrict__ cb, uint64_t r) {
     using Val = typename KeyOps<KeyT>::Val;
-    const uint32_t wg = blockIdx.x;
+    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    const PrepArgs &a = descs[be[kb].pos];
+    KeyT *__restrict__ blocks = (KeyT *)a.blocks;
+    const uint32_t wg = blockIdx.x - be[kb].first;
     uint32_t b = 0;
     while (b + 1 < a.nblocks && wg >= a.blk[b + 1].wg_begin) b++;
     b = __builtin_amdgcn_readfirstlane(b);
@@ -223,16 +238,21 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(PrepArgs a, const DevVert
 // wave reads the TZ column operands B[o][c][z0..z0+TZ) through the scalar
 // unit (they are wave-uniform), so each cell is one add and one min.
 template <typename KeyT, int TZ, int NA>
-__global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
+__global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ descs,
+                                                  const BatchEntry *__restrict__ be, uint32_t nbe) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
+    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    const RowsArgs &a = descs[be[kb].pos];
     const uint32_t lane = threadIdx.x & 63;
     // the wave index is uniform across the wave: say so, so that everything
     // derived from it (tile, c range, column addresses) lives in SGPRs
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     // blocks are dealt round-robin to the 8 XCDs: give every XCD a contiguous
     // range of tiles so that waves sharing a column slice share an L2
-    const uint32_t nb = a.nblocks_launched, b = blockIdx.x;
+    // (every vertex's block count and first block are multiples of 8, so the
+    // XCD of a block is its local index mod 8)
+    const uint32_t nb = a.nblocks_launched, b = blockIdx.x - be[kb].first;
     const uint64_t logical = (uint64_t)(b % 8) * (nb / 8) + b / 8;
     const uint64_t tile = logical * 4 + wave;
     if (tile >= a.total_tiles) return;
@@ -277,7 +297,11 @@ __global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
     }
     const uint32_t c0 = split * a.cper;
     const uint32_t c1 = min(a.K, c0 + a.cper);
-    const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * a.ldz + (uint64_t)chunk * TZ;
+    const uint32_t ldz = a.ldz;
+    uint32_t tsc[NT > 0 ? NT : 1];
+#pragma unroll
+    for (int t = 0; t < NT; t++) tsc[t] = t < na ? a.a[t].sc * (uint32_t)sizeof(Val) : 0;
+    const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * ldz + (uint64_t)chunk * TZ;
 
     KeyT acc[TZ];
 #pragma unroll
@@ -289,14 +313,13 @@ __global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
         for (int t = 0; t < NT; t++) {
             if (t < na) {
                 const uint64_t raw = __builtin_bit_cast(
-                    uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc[t], (int)offb[t],
-                                                                  (int)(c * a.a[t].sc * sizeof(Val)), 0));
+                    uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc[t], (int)offb[t], (int)(c * tsc[t]), 0));
                 const KeyT x = __builtin_bit_cast(KeyT, raw);
                 av = t == 0 ? x : Ops::add(av, x);
             }
         }
         const __attribute__((address_space(4))) KeyT *brow =
-            (const __attribute__((address_space(4))) KeyT *)(uintptr_t)(B + (uint64_t)c * a.ldz);
+            (const __attribute__((address_space(4))) KeyT *)(uintptr_t)(B + (uint64_t)c * ldz);
 #pragma unroll
         for (int t = 0; t < TZ; t++) acc[t] = Ops::min(acc[t], Ops::add(av, brow[t]));
     }
@@ -324,11 +347,14 @@ __global__ __launch_bounds__(256) void k_fill_rows(RowsArgs a) {
 }
 
 template <typename KeyT>
-__global__ void k_reduce_splits(ReduceArgs a) {
+__global__ __launch_bounds__(256) void k_reduce_splits(const ReduceArgs *__restrict__ descs,
+                                                      const BatchEntry *__restrict__ be, uint32_t nbe) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
-    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < a.N;
-         t += (uint64_t)gridDim.x * blockDim.x) {
+    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    const ReduceArgs &a = descs[be[kb].pos];
+    const uint32_t lb = blockIdx.x - be[kb].first;
+    for (uint64_t t = lb * (uint64_t)blockDim.x + threadIdx.x; t < a.N; t += (uint64_t)a.nblk * blockDim.x) {
         KeyT best = ((const KeyT *)a.partial)[t];
         for (uint32_t s = 1; s < a.nsplit; s++) best = Ops::min(best, ((const KeyT *)a.partial)[s * a.N + t]);
         Val v;
@@ -354,15 +380,19 @@ __device__ __forceinline__ KeyT shfl_xor_key(KeyT v, int mask) {
 }
 
 template <typename KeyT, int NT>
-__global__ __launch_bounds__(256) void k_fill_generic(GenericArgs a) {
+__global__ __launch_bounds__(256) void k_fill_generic(const GenericArgs *__restrict__ descs,
+                                                     const BatchEntry *__restrict__ be, uint32_t nbe) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
+    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    const GenericArgs &a = descs[be[kb].pos];
+    const uint32_t lb = blockIdx.x - be[kb].first;
     const uint32_t G = 1u << a.group_log2;
     const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
     constexpr int MT = NT < 0 ? kMaxGTerms : NT;
     const int nt = NT < 0 ? (int)a.nt : NT;
-    for (uint64_t tid = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x;
-         tid < ((nthreads + 255) / 256) * 256; tid += (uint64_t)gridDim.x * blockDim.x) {
+    for (uint64_t tid = lb * (uint64_t)blockDim.x + threadIdx.x; tid < ((nthreads + 255) / 256) * 256;
+         tid += (uint64_t)a.nblk * blockDim.x) {
         const bool live = tid < nthreads;
         const uint64_t phi = live ? tid >> a.group_log2 : a.N - 1;
         const uint32_t lane = (uint32_t)(tid & (G - 1));
@@ -493,10 +523,7 @@ struct DeviceState {
     uint64_t lent_bytes = 0;
     void *pinned = nullptr;
     uint64_t pinned_bytes = 0;
-    std::vector<hipEvent_t> ev;        // profiling: two per vertex (timed)
-    std::vector<hipStream_t> workers;  // streams of the vertex schedule (default priority)
-    std::vector<hipEvent_t> done;      // one per vertex: its table is complete (untimed)
-    hipEvent_t ready = nullptr;        // cost tables complete
+    std::vector<hipEvent_t> ev;        // profiling: two per fill launch (timed)
     hipStream_t last_stream = nullptr;
 };
 
@@ -513,9 +540,6 @@ void device_release(pase_graph_t g) {
     if (d->owned && d->ws) (void)hipFree(d->ws);
     if (d->pinned) (void)hipHostFree(d->pinned);
     for (auto e : d->ev) (void)hipEventDestroy(e);
-    for (auto e : d->done) (void)hipEventDestroy(e);
-    if (d->ready) (void)hipEventDestroy(d->ready);
-    for (auto st : d->workers) (void)hipStreamDestroy(st);
     delete d;
     g->dev = nullptr;
 }
@@ -563,6 +587,11 @@ static pase_status ensure_memory(pase_graph_t g, char **ws) {
         d->pinned_bytes = std::max<uint64_t>(pin_need, 4096);
     }
     return PASE_OK;
+}
+
+static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) {
+    uint64_t b = (n + block - 1) / block;
+    return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, cap));
 }
 
 // One vertex's launch description, resolved against the workspace base.
@@ -613,6 +642,7 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
         Launch<KeyT> &L = out[i];
         KeyT *blocks = (KeyT *)(ws + P.off_block + vp.block_off);
         std::memset(&L.prep, 0, sizeof L.prep);
+        L.prep.blocks = blocks;
         L.prep.vi = (uint32_t)vp.vi;
         L.prep.K = vp.K;
         L.prep.bits = vp.bits;
@@ -764,6 +794,7 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             ra.nblocks_launched = (uint32_t)nbk;
             L.rows = true;
             if (vp.nsplit > 1) {
+                L.red.nblk = grid_for(vp.N);
                 L.red.partial = ra.partial;
                 L.red.T = ra.T;
                 L.red.A = ra.A;
@@ -817,6 +848,7 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             ga.A = (uint16_t *)(ws + P.off_A + vp.A_off);
             ga.N = vp.N;
             ga.out_shift = vp.out_shift;
+            ga.nblk = (uint32_t)std::min<uint64_t>(((vp.N << ga.group_log2) + 255) / 256, 65535);
         }
         if (boff > vp.block_elems) return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
         if (!bounds_ok) return fail(g, PASE_ERR_INTERNAL, "a table lookup would leave its table");
@@ -829,57 +861,63 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
     return PASE_OK;
 }
 
+// A batched launch: vertices (sequence positions) sharing one kernel variant
+// within one launch slot, with their first workgroups.
+struct Batch {
+    enum Kind { kPrep, kRows, kGeneric, kReduce } kind;
+    uint32_t variant;      // rows: TZ * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime count)
+    uint32_t entry0;       // first BatchEntry of this batch
+    uint32_t nentries;
+    uint32_t blocks;       // workgroups of the launch
+};
+
 template <typename KeyT, int TZ>
-static void launch_rows_tz(const RowsArgs &ra, hipStream_t s) {
-    dim3 grid(ra.nblocks_launched), block(256);
+static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+    dim3 grid(b.blocks), block(256);
+    const uint32_t na = b.variant % 8;
     if constexpr (std::is_same<KeyT, double>::value) {
-        switch (ra.na) {
-        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 0>), grid, block, 0, s, ra); break;
-        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 1>), grid, block, 0, s, ra); break;
-        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 2>), grid, block, 0, s, ra); break;
-        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 3>), grid, block, 0, s, ra); break;
-        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 4>), grid, block, 0, s, ra); break;
+        switch (na) {
+        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 0>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 1>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 2>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 3>), grid, block, 0, s, descs, be, b.nentries); break;
+        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 4>), grid, block, 0, s, descs, be, b.nentries); break;
         }
     } else {
-        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, -1>), grid, block, 0, s, ra);
+        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, -1>), grid, block, 0, s, descs, be, b.nentries);
     }
 }
 
 template <typename KeyT>
-static bool launch_rows(const RowsArgs &ra, uint32_t TZ, hipStream_t s) {
-    switch (TZ) {
-    case 8: launch_rows_tz<KeyT, 8>(ra, s); return true;
-    case 12: launch_rows_tz<KeyT, 12>(ra, s); return true;
-    case 16: launch_rows_tz<KeyT, 16>(ra, s); return true;
-    case 20: launch_rows_tz<KeyT, 20>(ra, s); return true;
-    case 21: launch_rows_tz<KeyT, 21>(ra, s); return true;
-    case 24: launch_rows_tz<KeyT, 24>(ra, s); return true;
-    case 28: launch_rows_tz<KeyT, 28>(ra, s); return true;
-    case 30: launch_rows_tz<KeyT, 30>(ra, s); return true;
-    case 32: launch_rows_tz<KeyT, 32>(ra, s); return true;
+static bool launch_rows(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+    switch (b.variant / 8) {
+    case 8: launch_rows_tz<KeyT, 8>(descs, be, b, s); return true;
+    case 12: launch_rows_tz<KeyT, 12>(descs, be, b, s); return true;
+    case 16: launch_rows_tz<KeyT, 16>(descs, be, b, s); return true;
+    case 20: launch_rows_tz<KeyT, 20>(descs, be, b, s); return true;
+    case 21: launch_rows_tz<KeyT, 21>(descs, be, b, s); return true;
+    case 24: launch_rows_tz<KeyT, 24>(descs, be, b, s); return true;
+    case 28: launch_rows_tz<KeyT, 28>(descs, be, b, s); return true;
+    case 30: launch_rows_tz<KeyT, 30>(descs, be, b, s); return true;
+    case 32: launch_rows_tz<KeyT, 32>(descs, be, b, s); return true;
     default: return false;
     }
 }
 
 template <typename KeyT>
-static void launch_generic(const GenericArgs &ga, hipStream_t s) {
-    uint64_t threads = (uint64_t)ga.N << ga.group_log2;
-    dim3 grid((uint32_t)std::min<uint64_t>((threads + 255) / 256, 65535)), block(256);
-    switch (ga.nt) {
-    case 1: hipLaunchKernelGGL((k_fill_generic<KeyT, 1>), grid, block, 0, s, ga); break;
-    case 2: hipLaunchKernelGGL((k_fill_generic<KeyT, 2>), grid, block, 0, s, ga); break;
-    case 3: hipLaunchKernelGGL((k_fill_generic<KeyT, 3>), grid, block, 0, s, ga); break;
-    case 4: hipLaunchKernelGGL((k_fill_generic<KeyT, 4>), grid, block, 0, s, ga); break;
-    case 5: hipLaunchKernelGGL((k_fill_generic<KeyT, 5>), grid, block, 0, s, ga); break;
-    case 6: hipLaunchKernelGGL((k_fill_generic<KeyT, 6>), grid, block, 0, s, ga); break;
-    default: hipLaunchKernelGGL((k_fill_generic<KeyT, -1>), grid, block, 0, s, ga); break;
+static void launch_generic(const GenericArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+    dim3 grid(b.blocks), block(256);
+    switch (b.variant) {
+    case 1: hipLaunchKernelGGL((k_fill_generic<KeyT, 1>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 2: hipLaunchKernelGGL((k_fill_generic<KeyT, 2>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 3: hipLaunchKernelGGL((k_fill_generic<KeyT, 3>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 4: hipLaunchKernelGGL((k_fill_generic<KeyT, 4>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 5: hipLaunchKernelGGL((k_fill_generic<KeyT, 5>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 6: hipLaunchKernelGGL((k_fill_generic<KeyT, 6>), grid, block, 0, s, descs, be, b.nentries); break;
+    default: hipLaunchKernelGGL((k_fill_generic<KeyT, -1>), grid, block, 0, s, descs, be, b.nentries); break;
     }
 }
 
-static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) {
-    uint64_t b = (n + block - 1) / block;
-    return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, cap));
-}
 
 template <typename KeyT>
 static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t *min_cost, uint32_t *cfg) {
@@ -949,6 +987,77 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
     }
     std::memcpy(img + P.off_bt, bt.data(), n * sizeof(BacktrackDesc));
+
+    // ---- batches: per launch slot, one prep launch, one fill launch per kernel
+    // variant and one split-reduction launch
+    PrepArgs *hp = (PrepArgs *)(img + P.off_desc);
+    RowsArgs *hr = (RowsArgs *)(hp + n);
+    GenericArgs *hg = (GenericArgs *)(hr + n);
+    ReduceArgs *hd = (ReduceArgs *)(hg + n);
+    for (int i = 0; i < n; i++) {
+        hp[i] = launches[i].prep;
+        hr[i] = launches[i].ra;
+        hg[i] = launches[i].ga;
+        hd[i] = launches[i].red;
+    }
+    BatchEntry *hbe = (BatchEntry *)(img + P.off_batch);
+    std::vector<Batch> batches;
+    uint32_t nbe = 0;
+    std::vector<std::vector<int>> slot_members(P.nslots);
+    for (int i = 0; i < n; i++) slot_members[P.v[i].slot].push_back(i);
+    auto add_batch = [&](Batch::Kind kind, uint32_t variant, const std::vector<int> &members,
+                         uint32_t (*nblk)(const Launch<KeyT> &)) {
+        if (members.empty()) return;
+        Batch b{kind, variant, nbe, 0, 0};
+        for (int i : members) {
+            hbe[nbe].pos = (uint32_t)i;
+            hbe[nbe].first = b.blocks;
+            b.blocks += nblk(launches[i]);
+            nbe++;
+            b.nentries++;
+        }
+        batches.push_back(b);
+    };
+    for (int sl = 0; sl < P.nslots; sl++) {
+        const auto &mem = slot_members[sl];
+        add_batch(Batch::kPrep, 0, mem, [](const Launch<KeyT> &L) { return L.prep.nwg; });
+        std::vector<std::pair<uint32_t, int>> rows, gens, reds;
+        for (int i : mem) {
+            const Launch<KeyT> &L = launches[i];
+            if (L.rows) {
+                uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
+                rows.push_back({P.v[i].TZ * 8 + na, i});
+                if (P.v[i].nsplit > 1) reds.push_back({0, i});
+            } else {
+                gens.push_back({L.ga.nt <= 6 ? L.ga.nt : 0, i});
+            }
+        }
+        std::stable_sort(rows.begin(), rows.end(),
+                         [](const std::pair<uint32_t, int> &a, const std::pair<uint32_t, int> &b) { return a.first < b.first; });
+        std::stable_sort(gens.begin(), gens.end(),
+                         [](const std::pair<uint32_t, int> &a, const std::pair<uint32_t, int> &b) { return a.first < b.first; });
+        for (size_t k = 0; k < rows.size();) {
+            std::vector<int> grp;
+            size_t k2 = k;
+            for (; k2 < rows.size() && rows[k2].first == rows[k].first; k2++) grp.push_back(rows[k2].second);
+            add_batch(Batch::kRows, rows[k].first, grp, [](const Launch<KeyT> &L) { return L.ra.nblocks_launched; });
+            k = k2;
+        }
+        for (size_t k = 0; k < gens.size();) {
+            std::vector<int> grp;
+            size_t k2 = k;
+            for (; k2 < gens.size() && gens[k2].first == gens[k].first; k2++) grp.push_back(gens[k2].second);
+            add_batch(Batch::kGeneric, gens[k].first, grp, [](const Launch<KeyT> &L) { return L.ga.nblk; });
+            k = k2;
+        }
+        std::vector<int> rgrp;
+        for (auto &x : reds) rgrp.push_back(x.second);
+        add_batch(Batch::kReduce, 0, rgrp, [](const Launch<KeyT> &L) { return L.red.nblk; });
+    }
+    if (nbe > 3 * (uint64_t)n) return fail(g, PASE_ERR_INTERNAL, "batch table overflow");
+    for (const Batch &b : batches)
+        if (b.blocks == 0 || b.blocks > 0x7fffffffu) return fail(g, PASE_ERR_TOO_LARGE, "launch grid size");
+
     HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
 
     const DevVertex *dV = (const DevVertex *)(ws + P.off_vert);
@@ -958,85 +1067,61 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     uint8_t *dls = (uint8_t *)(ws + P.off_lsum);
     uint64_t *dsig = (uint64_t *)(ws + P.off_sig);
     const Contrib *dC = (const Contrib *)(ws + P.off_contrib);
-    // ---- streams and events (created before any capture)
-    const int S = P.streams;
-    if (g->profile && d->ev.size() < 2 * (size_t)n) {
-        for (size_t k = d->ev.size(); k < 2 * (size_t)n; k++) {
+    const PrepArgs *dp = (const PrepArgs *)(ws + P.off_desc);
+    const RowsArgs *dr = (const RowsArgs *)(dp + n);
+    const GenericArgs *dg = (const GenericArgs *)(dr + n);
+    const ReduceArgs *dd = (const ReduceArgs *)(dg + n);
+    const BatchEntry *dbe = (const BatchEntry *)(ws + P.off_batch);
+    uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
+    SearchOut *dout = (SearchOut *)(ws + P.off_out);
+
+    uint32_t nfill = 0;
+    for (const Batch &b : batches) nfill += b.kind == Batch::kRows || b.kind == Batch::kGeneric;
+    if (g->profile && d->ev.size() < 2 * (size_t)nfill) {
+        for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
             hipEvent_t e;
             HIPCHK(hipEventCreate(&e));
             d->ev.push_back(e);
         }
     }
-    if (S > 1) {
-        while ((int)d->workers.size() < S) {
-            hipStream_t w;
-            HIPCHK(hipStreamCreateWithFlags(&w, hipStreamNonBlocking));
-            d->workers.push_back(w);
-        }
-        while (d->done.size() < (size_t)n) {
-            hipEvent_t e;
-            HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-            d->done.push_back(e);
-        }
-        if (!d->ready) HIPCHK(hipEventCreateWithFlags(&d->ready, hipEventDisableTiming));
-    }
-    uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
-    SearchOut *dout = (SearchOut *)(ws + P.off_out);
-
-    // ---- every kernel of the search, on s0 and the worker streams
     uint32_t launches_n = 0;
-    auto enqueue = [&](hipStream_t s0) -> pase_status {
-        launches_n = 0;
-        if (!g->overridden) {
-            hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s0, dV,
-                               (uint32_t)nv, dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
-            launches_n++;
-        }
-        if (S > 1) HIPCHK(hipEventRecord(d->ready, s0));
-        // vertex schedule: P.streams streams, events for cross-stream producers
-        std::vector<int> tail(S, -1);
-        for (int i = 0; i < n; i++) {
-            Launch<KeyT> &L = launches[i];
-            const VPlan &vp = P.v[i];
-            hipStream_t st = s0;
-            if (S > 1) {
-                st = d->workers[vp.stream];
-                if (tail[vp.stream] < 0) HIPCHK(hipStreamWaitEvent(st, d->ready, 0));
-                for (int j : vp.waits) HIPCHK(hipStreamWaitEvent(st, d->done[j], 0));
-                tail[vp.stream] = i;
-            }
-            KeyT *dB = (KeyT *)(ws + P.off_block + vp.block_off);
-            hipLaunchKernelGGL((k_prep<KeyT>), dim3(L.prep.nwg), dim3(kPrepThreads), 0, st, L.prep, dV, dE,
-                               (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, dB, g->r);
-            launches_n++;
-            // with profiling, events bracket exactly the fill kernel of this vertex
-            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i], st));
-            if (L.rows) {
-                if (!launch_rows<KeyT>(L.ra, vp.TZ, st)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
-            } else {
-                launch_generic<KeyT>(L.ga, st);
-            }
-            launches_n++;
-            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * i + 1], st));
-            if (L.rows && vp.nsplit > 1) {
-                hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(grid_for(vp.N)), dim3(256), 0, st, L.red);
-                launches_n++;
-            }
-            if (S > 1) HIPCHK(hipEventRecord(d->done[i], st));
-        }
-        for (int k = 0; k < S; k++)
-            if (S > 1 && tail[k] >= 0) HIPCHK(hipStreamWaitEvent(s0, d->done[tail[k]], 0));
-        hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s0, (const BacktrackDesc *)(ws + P.off_bt),
-                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+    if (!g->overridden) {
+        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
+                           dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
         launches_n++;
-        HIPCHK(hipGetLastError());
-        return PASE_OK;
-    };
-
-    {
-        pase_status est = enqueue(s);
-        if (est != PASE_OK) return est;
     }
+    std::vector<int> fill_of(n, -1);   // fill batch of each vertex (profiling)
+    uint32_t fb = 0;
+    for (const Batch &b : batches) {
+        const BatchEntry *e = dbe + b.entry0;
+        switch (b.kind) {
+        case Batch::kPrep:
+            hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, s, dp, e, b.nentries, dV, dE,
+                               (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r);
+            break;
+        case Batch::kRows:
+        case Batch::kGeneric:
+            // with profiling, events bracket exactly this fill launch
+            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * fb], s));
+            if (b.kind == Batch::kRows) {
+                if (!launch_rows<KeyT>(dr, e, b, s)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+            } else {
+                launch_generic<KeyT>(dg, e, b, s);
+            }
+            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * fb + 1], s));
+            for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
+            fb++;
+            break;
+        case Batch::kReduce:
+            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, s, dd, e, b.nentries);
+            break;
+        }
+        launches_n++;
+    }
+    hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
+                       (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+    launches_n++;
+    HIPCHK(hipGetLastError());
     char *host_out = img;   // reuse the staging buffer after the upload has been consumed
     HIPCHK(hipStreamSynchronize(s));
     HIPCHK(hipMemcpyAsync(host_out, dout, sizeof(SearchOut), hipMemcpyDeviceToHost, s));
@@ -1049,17 +1134,20 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
 
     g->stats.launches = launches_n;
-    g->stats.streams = (uint32_t)S;
+    g->stats.slots = (uint32_t)P.nslots;
     g->stats.fill_ms = g->stats.rows_fill_ms = 0;
     g->stats.rows_launches = 0;
     if (g->profile) {
-        for (int i = 0; i < n; i++) {
-            float ms = 0;
-            HIPCHK(hipEventElapsedTime(&ms, d->ev[2 * i], d->ev[2 * i + 1]));
-            g->stats.fill_ms += ms;
-            g->plan.v[i].fill_ms = ms;
-            if (launches[i].rows) { g->stats.rows_fill_ms += ms; g->stats.rows_launches++; }
+        std::vector<float> ms(fb, 0.f);
+        uint32_t k = 0;
+        for (const Batch &b : batches) {
+            if (b.kind != Batch::kRows && b.kind != Batch::kGeneric) continue;
+            HIPCHK(hipEventElapsedTime(&ms[k], d->ev[2 * k], d->ev[2 * k + 1]));
+            g->stats.fill_ms += ms[k];
+            if (b.kind == Batch::kRows) { g->stats.rows_fill_ms += ms[k]; g->stats.rows_launches++; }
+            k++;
         }
+        for (int i = 0; i < n; i++) P.v[i].fill_ms = fill_of[i] >= 0 ? ms[fill_of[i]] : 0.0;
     }
     return PASE_OK;
 }

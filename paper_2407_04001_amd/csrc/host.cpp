@@ -254,6 +254,11 @@ static pase_status build_plan(pase_graph_t g) {
         if (P.v[i].consumer < 0) return fail(g, PASE_ERR_INTERNAL, "table never read");
         P.v[i].out_shift = P.v[P.v[i].consumer].bits;
     }
+    // dependency level: vertices of one level read no table of each other
+    for (int i = 0; i < n; i++) {
+        P.v[i].level = 0;
+        for (const auto &t : P.v[i].terms) P.v[i].level = std::max(P.v[i].level, P.v[t.j].level + 1);
+    }
 
     // ---- kernel choice and T_i layout
     for (int i = 0; i < n; i++) {
@@ -365,53 +370,22 @@ static pase_status build_plan(pase_graph_t g) {
 // Cost tables T_i live from their fill to their single reader (or to the end
 // when tables are kept or i is last) and share memory by interval packing;
 // argmin tables A_i all live until back-substitution.
-static pase_status layout_memory_mode(pase_graph_t g, bool concurrent);
+static pase_status layout_memory_mode(pase_graph_t g, bool by_level);
 
-// Try the concurrent layout (every table and scratch buffer resident, so
-// independent vertices may run on different streams); fall back to the
-// packed single-stream layout when that exceeds the memory budget.
+// Level schedule when its memory fits the budget, else one vertex at a time.
 static pase_status layout_memory(pase_graph_t g) {
-    if (g->streams > 1 && layout_memory_mode(g, true) == PASE_OK) return PASE_OK;
+    if (g->schedule == 0 && layout_memory_mode(g, true) == PASE_OK) return PASE_OK;
     return layout_memory_mode(g, false);
 }
 
-// Stream schedule: visit positions in sequence order; a vertex joins the
-// stream whose last vertex is one of its producers (no event needed for
-// that one), else the stream with the least estimated work; it waits on an
-// event of every producer scheduled on another stream.
-static void schedule_streams(pase_graph_t g) {
+static pase_status layout_memory_mode(pase_graph_t g, bool by_level) {
     Plan &P = g->plan;
-    const int S = P.concurrent ? std::max(1, g->streams) : 1;
-    P.streams = S;
-    std::vector<int> tail(S, -1);
-    std::vector<double> load(S, 0.0);
-    for (int i = 0; i < (int)P.v.size(); i++) {
-        VPlan &vp = P.v[i];
-        vp.waits.clear();
-        int s = -1;
-        for (int k = 0; k < S; k++)
-            for (const auto &t : vp.terms)
-                if (tail[k] == t.j && (s < 0 || tail[k] > tail[s])) s = k;
-        if (s < 0) {
-            s = 0;
-            for (int k = 1; k < S; k++)
-                if (load[k] < load[s]) s = k;
-        }
-        // latest producer per other stream
-        std::vector<int> last(S, -1);
-        for (const auto &t : vp.terms)
-            if (P.v[t.j].stream != s) last[P.v[t.j].stream] = std::max(last[P.v[t.j].stream], t.j);
-        for (int k = 0; k < S; k++)
-            if (last[k] >= 0) vp.waits.push_back(last[k]);
-        vp.stream = s;
-        tail[s] = i;
-        load[s] += 5.0 + (double)vp.N * vp.K / 1e7;   // ~5 us per vertex + ~1e13 cells/s
+    P.by_level = by_level;
+    P.nslots = 0;
+    for (auto &vp : P.v) {
+        vp.slot = by_level ? vp.level : (int)(&vp - &P.v[0]);
+        P.nslots = std::max(P.nslots, vp.slot + 1);
     }
-}
-
-static pase_status layout_memory_mode(pase_graph_t g, bool concurrent) {
-    Plan &P = g->plan;
-    P.concurrent = concurrent;
     const int n = (int)P.v.size();
     const uint64_t A = 256;
     uint64_t off = 0;
@@ -442,17 +416,22 @@ static pase_status layout_memory_mode(pase_graph_t g, bool concurrent) {
     off = align_up(off + ncontrib * sizeof(Contrib), A);
     P.off_bt = off;
     off = align_up(off + n * sizeof(BacktrackDesc), A);
+    P.off_desc = off;
+    off = align_up(off + n * (sizeof(PrepArgs) + sizeof(RowsArgs) + sizeof(GenericArgs) + sizeof(ReduceArgs)), A);
+    P.off_batch = off;
+    off = align_up(off + 3 * (uint64_t)n * sizeof(BatchEntry), A);
     P.off_cfg = off;
     off = align_up(off + g->V.size() * 4, A);
     P.off_out = off;
     off = align_up(off + sizeof(SearchOut), A);
 
-    // T arena: interval packing
+    // T arena: interval packing over launch slots -- a table is written in the
+    // slot of its vertex and last read in the slot of its reader
     struct Iv { int i, s, e; uint64_t size; };
     std::vector<Iv> iv;
     for (int i = 0; i < n; i++) {
-        int end = (g->keep_tables || concurrent || i == n - 1) ? n : P.v[i].consumer;
-        iv.push_back({i, i, end, align_up(P.v[i].N * 8, A)});
+        int end = (g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
+        iv.push_back({i, P.v[i].slot, end, align_up(P.v[i].N * 8, A)});
     }
     std::vector<int> order(n);
     std::iota(order.begin(), order.end(), 0);
@@ -482,8 +461,9 @@ static pase_status layout_memory_mode(pase_graph_t g, bool concurrent) {
     P.A_bytes = abytes;
     P.off_A = off;
     off = align_up(off + abytes, A);
-    // block and split scratch: one shared region (sequential), or one per vertex (concurrent)
-    uint64_t bsum = 0, psum = 0, bmax = 0, pmax = 0;
+    // block and split scratch: vertices of one slot get disjoint pieces; slots reuse it
+    std::vector<uint64_t> bsum(P.nslots, 0), psum(P.nslots, 0);
+    uint64_t bmax = 0, pmax = 0;
     for (auto &vp : P.v) {
         uint64_t e = 0, pb = 0;
         if (vp.kernel == kRows) {
@@ -495,23 +475,22 @@ static pase_status layout_memory_mode(pase_graph_t g, bool concurrent) {
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
         }
         vp.block_elems = e;
-        vp.block_off = concurrent ? bsum : 0;
-        vp.partial_off = concurrent ? psum : 0;
-        bsum += align_up(e * 8, A);
-        psum += pb;
-        bmax = std::max(bmax, e * 8);
-        pmax = std::max(pmax, pb);
+        vp.block_off = bsum[vp.slot];
+        vp.partial_off = psum[vp.slot];
+        bsum[vp.slot] += align_up(e * 8, A);
+        psum[vp.slot] += pb;
+        bmax = std::max(bmax, bsum[vp.slot]);
+        pmax = std::max(pmax, psum[vp.slot]);
     }
-    P.block_bytes = concurrent ? bsum : bmax;
+    P.block_bytes = bmax;
     P.off_block = off;
     off = align_up(off + P.block_bytes, A);
-    P.partial_bytes = concurrent ? psum : pmax;
+    P.partial_bytes = pmax;
     P.off_partial = off;
     off = align_up(off + P.partial_bytes, A);
     P.total = off;
     if (P.total > g->mem_budget)
         return fail(g, PASE_ERR_TOO_LARGE, "device memory need exceeds the memory budget");
-    schedule_streams(g);
     return PASE_OK;
 }
 
@@ -636,15 +615,15 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->key_mode = (int)value;
         break;
     case PASE_OPT_PROFILE: g->profile = value != 0; break;
-    case PASE_OPT_STREAMS:
-        if (value < 1 || value > 16) return fail(g, PASE_ERR_INVALID_ARGUMENT, "streams 1..16");
-        g->streams = (int)value;
+    case PASE_OPT_SCHEDULE:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0 or 1");
+        g->schedule = (int)value;
         break;
     default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
     }
     // options that change the plan need a fresh enumeration
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
-         opt == PASE_OPT_STREAMS) && g->enumerated) {
+         opt == PASE_OPT_SCHEDULE) && g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);
         if (st == PASE_OK) st = layout_memory(g);

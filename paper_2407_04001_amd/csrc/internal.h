@@ -80,8 +80,17 @@ constexpr uint32_t kPrepThreads = 256;
 struct PrepArgs {
     uint32_t vi, K, bits, nblocks;
     uint64_t total;           // sum of block elements
-    uint32_t nwg, pad;        // workgroups of the launch
+    uint32_t nwg, pad;        // workgroups of this vertex
+    void *blocks;             // this vertex's block scratch
     Block blk[kMaxBlocks];
+};
+
+// One vertex of a batched launch: its descriptor index (sequence position)
+// and its first workgroup.  The workgroups of a launch are the concatenation
+// of the workgroups of its vertices.
+struct BatchEntry {
+    uint32_t pos;
+    uint32_t first;
 };
 
 struct ATerm {                // per-lane row term of the row kernel (key space)
@@ -125,7 +134,7 @@ struct GenericArgs {
     void *T;
     uint16_t *A;
     uint64_t N;
-    uint32_t out_shift, pad;
+    uint32_t out_shift, nblk;  // nblk: workgroups of this vertex
 };
 
 struct ReduceArgs {
@@ -133,7 +142,7 @@ struct ReduceArgs {
     void *T;
     uint16_t *A;
     uint64_t N;
-    uint32_t nsplit, bits, out_shift, pad;
+    uint32_t nsplit, bits, out_shift, nblk;
 };
 
 struct BacktrackDesc {        // per position, for the back-substitution kernel
@@ -182,8 +191,8 @@ struct VPlan {
     uint64_t block_off = 0;         // bytes into the block scratch
     uint64_t partial_off = 0;       // bytes into the split scratch
     // schedule
-    int stream = 0;                 // stream index (0 = the caller's stream schedule slot)
-    std::vector<int> waits;         // producers on other streams whose completion it awaits
+    int level = 0;                  // dependency level: 1 + max level of the tables it reads
+    int slot = 0;                   // launch slot: its level (level schedule) or its position
 };
 
 struct Plan {
@@ -198,8 +207,9 @@ struct Plan {
              off_partial = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
     uint64_t sig_count = 0;         // split signatures of all edge endpoints
-    int streams = 1;                // streams of the schedule
-    bool concurrent = false;        // tables and scratch never reused (needed for streams > 1)
+    int nslots = 0;                 // launch slots (levels, or positions when sequential)
+    bool by_level = false;          // the vertices of one dependency level share launches
+    uint64_t off_desc = 0, off_batch = 0;   // per-vertex launch descriptors, batch tables
 };
 
 struct DeviceState;   // defined by the device runtime
@@ -217,7 +227,7 @@ struct pase_graph_s {
     bool keep_tables = false, profile = false;
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
-    int streams = 4;
+    int schedule = 0;               // 0 = by dependency level, 1 = strictly in sequence
     // configurations
     bool enumerated = false;
     uint32_t p = 0, log2p = 0;

@@ -19,7 +19,7 @@ MAX_DIMS = 8
 OK, INVALID_ARGUMENT, NOT_CONNECTED, BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMORY, HIP, INTERNAL = range(9)
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STATE", 4: "OVERFLOW",
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
-OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_STREAMS = range(1, 7)
+OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE = range(1, 7)
 
 
 class VertexDesc(C.Structure):
@@ -42,7 +42,7 @@ class RunStats(C.Structure):
                 ("max_dep", C.c_uint32), ("key_type", C.c_uint32), ("launches", C.c_uint32),
                 ("rows_vertices", C.c_uint32), ("rows_cells", C.c_uint64), ("host_plan_ms", C.c_double),
                 ("wall_ms", C.c_double), ("fill_ms", C.c_double), ("rows_fill_ms", C.c_double),
-                ("rows_launches", C.c_uint32), ("streams", C.c_uint32)]
+                ("rows_launches", C.c_uint32), ("slots", C.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
