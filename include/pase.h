@@ -97,10 +97,19 @@ typedef enum {
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
     PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats) */
-    PASE_OPT_SCHEDULE = 6       /* 0 (default): vertices of one dependency level (whose tables
+    PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
                                    do not read each other) share their kernel launches and run
                                    concurrently; 1: one vertex at a time in sequence order.  Memory
                                    is packed by table lifetimes in either case. */
+    PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
+                                   vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
+                                   that kernel runs (a tuning and test knob) */
+    PASE_OPT_TILE_ROWS = 8,     /* same kernel: table rows per lane, 0 = chosen (default), 1 or 2 */
+    PASE_OPT_TILE_PARTS = 9,    /* same kernel: waves sharing one tile's c range, 0 = chosen
+                                   (default), 1, 2 or 4 */
+    PASE_OPT_C_SPLITS = 10      /* same kernel: workgroups sharing one tile's c range (partial
+                                   keys reduced by a second launch), 0 = chosen (default), else
+                                   min(value, K_v) for every vertex */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */
@@ -221,8 +230,11 @@ typedef struct {
     uint32_t num_configs, dep_count;
     uint64_t entries;    /* |table| = product of K over D(v) */
     uint64_t cells;      /* K_v * entries */
-    int32_t column;      /* row kernel: column digit (vertex id), else -1 */
-    uint32_t outer, rows, tile_cols, splits, row_terms, lookups;
+    int32_t column;      /* row kernel: column digit (vertex id), -1 for none or the generic kernel */
+    uint32_t outer, rows, tile_cols;
+    uint32_t tile_rows;  /* rows per lane (1 or 2) */
+    uint32_t splits, row_terms, lookups;
+    uint32_t parts;      /* row kernel: waves sharing one tile's c range (1, 2 or 4) */
     double fill_ms;      /* PASE_OPT_PROFILE: event time of this vertex's fill kernel */
 } pase_vertex_info;
 

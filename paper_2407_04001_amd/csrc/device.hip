@@ -230,32 +230,54 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restric
     *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
 }
 
+// Waits for every outstanding scalar-memory and LDS read (s_waitcnt
+// lgkmcnt(0), other counters left alone).  Scalar loads return out of order,
+// so a wait for one of them is always a wait for all of them: the pipelined
+// loops wait for the operands of c *before* they request those of c + 1,
+// otherwise the wait the compiler places before the first use of c's
+// operands would also wait for the prefetch.
+__device__ __forceinline__ void wait_lgkm_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
 // ------------------------------------------------------------------ fill: row kernel
 // Output T_i is laid out [z][o][r]: column digit z slowest, then the outer
-// digits o (those sharing a lookup with z), then the row digits r.  A wave
-// owns 64 consecutive rows of one (o, column chunk, c range); lane = row.
-// For each c the lane forms its row operand a = sum of its row terms, and the
-// wave reads the TZ column operands B[o][c][z0..z0+TZ) through the scalar
-// unit (they are wave-uniform), so each cell is one add and one min.
-template <typename KeyT, int TZ, int NA>
+// digits o (those sharing a lookup with z), then the row digits r.  A tile is
+// TM x 64 consecutive rows of one (o, column chunk, c range); lane l holds
+// rows l, l + 64, ...  For each c every row forms its operand a = sum of its
+// row terms, and the wave reads the TZ column operands B[o][c][z0..z0+TZ)
+// through the scalar unit (they are wave-uniform), so each cell is one add
+// (SGPR operand) and one min; one scalar round trip per c feeds TM x 64 x TZ
+// cells.  The four waves of a workgroup take the same tile and a quarter of
+// its c range each, and combine their minima through LDS at the end: a wave
+// then does a quarter of a tile's work, so a launch has four times as many,
+// shorter, work items and its last partial round of waves costs little.
+constexpr int kMergeVals = 16;   // values per lane moved through LDS per merge pass
+
+template <typename KeyT, int TZ, int TM, int NA>
 __global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ descs,
                                                   const BatchEntry *__restrict__ be, uint32_t nbe) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
+    __shared__ KeyT xch[2][kMergeVals][64];
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
     const RowsArgs &a = descs[be[kb].pos];
     const uint32_t lane = threadIdx.x & 63;
     // the wave index is uniform across the wave: say so, so that everything
-    // derived from it (tile, c range, column addresses) lives in SGPRs
+    // derived from it (c range, column addresses) lives in SGPRs
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     // blocks are dealt round-robin to the 8 XCDs: give every XCD a contiguous
-    // range of tiles so that waves sharing a column slice share an L2
-    // (every vertex's block count and first block are multiples of 8, so the
-    // XCD of a block is its local index mod 8)
+    // range of tiles so that tiles sharing a column slice share an L2 (every
+    // vertex's block count and first block are multiples of 8, so the XCD of
+    // a block is its local index mod 8)
     const uint32_t nb = a.nblocks_launched, b = blockIdx.x - be[kb].first;
-    const uint64_t logical = (uint64_t)(b % 8) * (nb / 8) + b / 8;
-    const uint64_t tile = logical * 4 + wave;
-    if (tile >= a.total_tiles) return;
+    const uint64_t wg = (uint64_t)(b % 8) * (nb / 8) + b / 8;
+    // a workgroup takes 4 / P tiles, P = a.parts waves per tile, each wave a
+    // P-th of the tile's c range
+    const uint32_t P = a.parts, tpw = 4 / P;
+    if (wg * tpw >= a.total_tiles) return;   // the whole workgroup leaves together
+    const uint32_t part = wave % P, tin = wave / P;
+    const bool has_tile = wg * tpw + tin < a.total_tiles;
+    // (a wave without a tile computes nothing but still takes part in the merge)
+    const uint64_t tile = min(wg * tpw + tin, a.total_tiles - 1);
     // tile order (fastest first): row tile, column chunk, outer index, c split --
     // all chunks of one outer index run close together and share its slices
     const uint32_t rowtile = (uint32_t)(tile % a.tiles_per_o);
@@ -264,83 +286,180 @@ __global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ 
     t2 /= a.nchunks;
     const uint32_t o = (uint32_t)(t2 % a.MO);
     const uint32_t split = (uint32_t)(t2 / a.MO);
-    const uint32_t r = rowtile * 64 + lane;
-    const bool valid = r < a.MR;
-    const uint32_t rr = valid ? r : a.MR - 1;
 
-    uint32_t dO[kMaxDep], dR[kMaxDep];
+    constexpr int NT = NA < 0 ? kMaxATerms : NA;
+    constexpr int NTA = NT > 0 ? NT : 1;
+    const int na = NA < 0 ? (int)a.na : NA;
+    uint32_t dO[kMaxDep];
     {
         uint32_t x = o;
         for (int k = kMaxDep - 1; k >= 0; k--)
             if (k < (int)a.nO) { dO[k] = x % a.radO[k]; x /= a.radO[k]; } else dO[k] = 0;
-        x = rr;
-        for (int k = kMaxDep - 1; k >= 0; k--)
-            if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
     }
-    constexpr int NT = NA < 0 ? kMaxATerms : NA;
-    const int na = NA < 0 ? (int)a.na : NA;
     // row terms are read with buffer loads: per-lane byte offset in a VGPR,
     // the c-dependent part as a scalar offset, no per-c address arithmetic
-    uint32_t offb[NT > 0 ? NT : 1];
-    __amdgpu_buffer_rsrc_t rsrc[NT > 0 ? NT : 1];
+    __amdgpu_buffer_rsrc_t rsrc[NTA];
+    uint32_t tsc[NTA];
 #pragma unroll
-    for (int t = 0; t < NT; t++) {
-        uint32_t off = 0;
-        if (t < na) {
-            for (int k = 0; k < kMaxDep; k++) off += dO[k] * a.a[t].sdO[k] + dR[k] * a.a[t].sdR[k];
-            rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.a[t].ptr), (short)0,
-                                                        (int)a.a[t].bytes, kBufferWord3);
-        } else {
-            rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(nullptr, (short)0, 0, kBufferWord3);
-        }
-        offb[t] = off * (uint32_t)sizeof(Val);
+    for (int t = 0; t < NTA; t++) {
+        rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(t < na ? const_cast<void *>(a.a[t].ptr) : nullptr, (short)0,
+                                                    t < na ? (int)a.a[t].bytes : 0, kBufferWord3);
+        tsc[t] = t < na ? a.a[t].sc * (uint32_t)sizeof(Val) : 0;
     }
-    const uint32_t c0 = split * a.cper;
-    const uint32_t c1 = min(a.K, c0 + a.cper);
-    const uint32_t ldz = a.ldz;
-    uint32_t tsc[NT > 0 ? NT : 1];
+    uint32_t r[TM], offb[TM][NTA];
+    bool valid[TM];
 #pragma unroll
-    for (int t = 0; t < NT; t++) tsc[t] = t < na ? a.a[t].sc * (uint32_t)sizeof(Val) : 0;
+    for (int m = 0; m < TM; m++) {
+        r[m] = (rowtile * TM + m) * 64 + lane;
+        valid[m] = r[m] < a.MR;
+        uint32_t x = valid[m] ? r[m] : a.MR - 1, dR[kMaxDep];
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
+#pragma unroll
+        for (int t = 0; t < NTA; t++) {
+            uint32_t off = 0;
+            if (t < na)
+                for (int k = 0; k < kMaxDep; k++) off += dO[k] * a.a[t].sdO[k] + dR[k] * a.a[t].sdR[k];
+            offb[m][t] = off * (uint32_t)sizeof(Val);
+        }
+    }
+    // this wave's part [c0, c1) of the tile's c range (possibly empty)
+    const uint32_t cs = split * a.cper, ce_ = has_tile ? min(a.K, cs + a.cper) : cs;
+    const uint32_t q = (ce_ - cs + P - 1) / P;
+    const uint32_t c0 = min(ce_, cs + part * q), c1 = min(ce_, c0 + q);
+    const uint32_t ldz = a.ldz;
     const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * ldz + (uint64_t)chunk * TZ;
 
-    KeyT acc[TZ];
+    KeyT acc[TM][TZ];
 #pragma unroll
-    for (int t = 0; t < TZ; t++) acc[t] = Ops::sentinel();
+    for (int m = 0; m < TM; m++)
+#pragma unroll
+        for (int t = 0; t < TZ; t++) acc[m][t] = Ops::sentinel();
 
-    for (uint32_t c = c0; c < c1; c++) {
-        KeyT av = (KeyT)0;
+    // Software pipeline over two register sets of U values of c each: the
+    // row terms and column chunks of the next U values are requested while
+    // the cells of the current ones are computed from the other set, so load
+    // latency overlaps VALU work.  Narrow tiles have little work per c and
+    // keep U = 4 values in flight per set.  Loads past c1 repeat column
+    // c1 - 1 (in bounds, unused) so that every load is unconditional and the
+    // register sets never need copying.
+    constexpr int U = TZ <= 2 ? 4 : 1;
+    using SKey = const __attribute__((address_space(4))) KeyT;
+    uint64_t xe[U][TM][NTA], xo[U][TM][NTA];
+    KeyT ce[U][TZ], co[U][TZ];
+    auto load = [&](uint64_t (&xs)[U][TM][NTA], KeyT (&bs)[U][TZ], uint32_t cc) {
 #pragma unroll
-        for (int t = 0; t < NT; t++) {
-            if (t < na) {
-                const uint64_t raw = __builtin_bit_cast(
-                    uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc[t], (int)offb[t], (int)(c * tsc[t]), 0));
-                const KeyT x = __builtin_bit_cast(KeyT, raw);
-                av = t == 0 ? x : Ops::add(av, x);
-            }
+        for (int u = 0; u < U; u++) {
+            const uint32_t cu = min(cc + u, c1 - 1);
+#pragma unroll
+            for (int m = 0; m < TM; m++)
+#pragma unroll
+                for (int t = 0; t < NTA; t++)
+                    if (t < na)
+                        xs[u][m][t] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(
+                                                                       rsrc[t], (int)offb[m][t], (int)(cu * tsc[t]), 0));
+            SKey *brow = (SKey *)(uintptr_t)(B + (uint64_t)cu * ldz);
+#pragma unroll
+            for (int t = 0; t < TZ; t++) bs[u][t] = brow[t];
         }
-        const __attribute__((address_space(4))) KeyT *brow =
-            (const __attribute__((address_space(4))) KeyT *)(uintptr_t)(B + (uint64_t)c * ldz);
+    };
+    auto cells = [&](const uint64_t (&xs)[U][TM][NTA], const KeyT (&bs)[U][TZ], uint32_t n) {
 #pragma unroll
-        for (int t = 0; t < TZ; t++) acc[t] = Ops::min(acc[t], Ops::add(av, brow[t]));
+        for (int u = 0; u < U; u++) {
+            if (u > 0 && (uint32_t)u >= n) break;
+            KeyT av[TM];
+#pragma unroll
+            for (int m = 0; m < TM; m++) {
+                av[m] = (KeyT)0;
+#pragma unroll
+                for (int t = 0; t < NTA; t++)
+                    if (t < na) {
+                        const KeyT v = __builtin_bit_cast(KeyT, xs[u][m][t]);
+                        av[m] = t == 0 ? v : Ops::add(av[m], v);
+                    }
+            }
+#pragma unroll
+            for (int t = 0; t < TZ; t++)
+#pragma unroll
+                for (int m = 0; m < TM; m++) acc[m][t] = Ops::min(acc[m][t], Ops::add(av[m], bs[u][t]));
+        }
+    };
+    if (c0 < c1) {
+        load(xe, ce, c0);
+        uint32_t c = c0;
+        for (; c + U < c1; c += 2 * U) {
+            // up to 16 columns both sets fit in SGPRs at once: the barriers
+            // keep the scheduler from sinking the loads of the next set below
+            // the cells of the current one, and the explicit wait for the
+            // current operands comes before those loads are issued
+            if constexpr (TZ <= 16) {
+                wait_lgkm_all();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            load(xo, co, c + U);
+            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
+            cells(xe, ce, U);
+            if constexpr (TZ <= 16) {
+                wait_lgkm_all();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            load(xe, ce, c + 2 * U);
+            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
+            cells(xo, co, min((uint32_t)U, c1 - (c + U)));
+        }
+        if (c < c1) cells(xe, ce, min((uint32_t)U, c1 - c));
     }
 
-    if (!valid) return;
+    // combine the parts of a tile through LDS, halving the number of holders
+    // per stage (P = 4: parts 2, 3 -> 0, 1, then 1 -> 0; P = 2: 1 -> 0),
+    // kMergeVals values per lane and pass; P is uniform across the workgroup,
+    // so every wave meets the same barriers
+    constexpr int V = TM * TZ;
+    for (uint32_t d = P / 2; d >= 1; d /= 2) {
+#pragma unroll
+        for (int p0 = 0; p0 < V; p0 += kMergeVals) {
+            constexpr int W = kMergeVals;
+            __syncthreads();
+            if (part >= d && part < 2 * d) {
+                const uint32_t slot = tin * d + (part - d);
+#pragma unroll
+                for (int j = 0; j < W; j++)
+                    if (p0 + j < V) xch[slot][j][lane] = acc[(p0 + j) / TZ][(p0 + j) % TZ];
+            }
+            __syncthreads();
+            if (part < d) {
+                const uint32_t slot = tin * d + part;
+#pragma unroll
+                for (int j = 0; j < W; j++)
+                    if (p0 + j < V) {
+                        KeyT &x = acc[(p0 + j) / TZ][(p0 + j) % TZ];
+                        x = Ops::min(x, xch[slot][j][lane]);
+                    }
+            }
+        }
+    }
+    if (part != 0 || !has_tile) return;
+
     const uint64_t plane = (uint64_t)a.MO * a.MR;
-    const uint64_t base_idx = (uint64_t)o * a.MR + r;
     const uint32_t zbase = chunk * TZ;
 #pragma unroll
-    for (int t = 0; t < TZ; t++) {
-        const uint32_t z = zbase + t;
-        if (z < a.Kz) {
-            const uint64_t idx = (uint64_t)z * plane + base_idx;
-            if (a.nsplit > 1) {
-                ((KeyT *)a.partial)[(uint64_t)split * a.N + idx] = acc[t];
-            } else {
-                Val v;
-                uint32_t cc;
-                Ops::split(acc[t], a.bits, a.out_shift, v, cc);
-                ((Val *)a.T)[idx] = v;
-                a.A[idx] = (uint16_t)cc;
+    for (int m = 0; m < TM; m++) {
+        if (!valid[m]) continue;
+        const uint64_t base_idx = (uint64_t)o * a.MR + r[m];
+#pragma unroll
+        for (int t = 0; t < TZ; t++) {
+            const uint32_t z = zbase + t;
+            if (z < a.Kz) {
+                const uint64_t idx = (uint64_t)z * plane + base_idx;
+                if (a.nsplit > 1) {
+                    ((KeyT *)a.partial)[(uint64_t)split * a.N + idx] = acc[m][t];
+                } else {
+                    Val v;
+                    uint32_t cc;
+                    Ops::split(acc[m][t], a.bits, a.out_shift, v, cc);
+                    ((Val *)a.T)[idx] = v;
+                    a.A[idx] = (uint16_t)cc;
+                }
             }
         }
     }
@@ -764,17 +883,18 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
                 at.ptr = ws + P.off_T + P.v[t.j].T_off;
                 at.sc = sc;
                 at.bytes = (uint32_t)(P.v[t.j].N * 8);
-                // plan digits: 0 = z, 1..|O| = O, then R
-                for (size_t k = 0; k < vp.O.size(); k++) at.sdO[k] = sd[1 + k];
-                for (size_t k = 0; k < vp.R.size(); k++) at.sdR[k] = sd[1 + vp.O.size() + k];
+                // plan digits: z (if there is a column digit), then O, then R
+                const size_t zoff = vp.z >= 0 ? 1 : 0;
+                for (size_t k = 0; k < vp.O.size(); k++) at.sdO[k] = sd[zoff + k];
+                for (size_t k = 0; k < vp.R.size(); k++) at.sdR[k] = sd[zoff + vp.O.size() + k];
             }
             ra.ldz = vp.ldz;
-            ra.Kz = g->K[vp.z];
+            ra.Kz = vp.z >= 0 ? g->K[vp.z] : 1;
             ra.K = vp.K;
             ra.bits = vp.bits;
             ra.MO = (uint32_t)vp.MO;
             ra.MR = (uint32_t)vp.MR;
-            ra.tiles_per_o = (uint32_t)((vp.MR + 63) / 64);
+            ra.tiles_per_o = (uint32_t)((vp.MR + 64 * vp.TM - 1) / (64 * vp.TM));
             ra.nchunks = vp.nchunks;
             ra.nsplit = vp.nsplit;
             ra.cper = vp.cper;
@@ -787,8 +907,10 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             ra.partial = ws + P.off_partial + vp.partial_off;
             ra.N = vp.N;
             ra.out_shift = vp.out_shift;
+            // a workgroup takes 4 / parts tiles
+            ra.parts = vp.parts;
             ra.total_tiles = (uint64_t)vp.nsplit * vp.nchunks * vp.MO * ra.tiles_per_o;
-            uint64_t nbk = (ra.total_tiles + 3) / 4;
+            uint64_t nbk = (ra.total_tiles + 4 / vp.parts - 1) / (4 / vp.parts);
             nbk = (nbk + 7) / 8 * 8;
             if (nbk > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "grid too large");
             ra.nblocks_launched = (uint32_t)nbk;
@@ -865,41 +987,47 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
 // within one launch slot, with their first workgroups.
 struct Batch {
     enum Kind { kPrep, kRows, kGeneric, kReduce } kind;
-    uint32_t variant;      // rows: TZ * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime count)
+    uint32_t variant;      // rows: (TZ * 4 + TM) * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime)
     uint32_t entry0;       // first BatchEntry of this batch
     uint32_t nentries;
     uint32_t blocks;       // workgroups of the launch
 };
 
-template <typename KeyT, int TZ>
+template <typename KeyT, int TZ, int TM>
 static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
     dim3 grid(b.blocks), block(256);
     const uint32_t na = b.variant % 8;
     if constexpr (std::is_same<KeyT, double>::value) {
         switch (na) {
-        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 0>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 1>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 2>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 3>), grid, block, 0, s, descs, be, b.nentries); break;
-        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, 4>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 0>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 1>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 2>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 3>), grid, block, 0, s, descs, be, b.nentries); break;
+        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 4>), grid, block, 0, s, descs, be, b.nentries); break;
         }
     } else {
-        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, -1>), grid, block, 0, s, descs, be, b.nentries);
+        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, -1>), grid, block, 0, s, descs, be, b.nentries);
     }
 }
 
+// variant = (TZ * 4 + TM) * 8 + NA
 template <typename KeyT>
 static bool launch_rows(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
     switch (b.variant / 8) {
-    case 8: launch_rows_tz<KeyT, 8>(descs, be, b, s); return true;
-    case 12: launch_rows_tz<KeyT, 12>(descs, be, b, s); return true;
-    case 16: launch_rows_tz<KeyT, 16>(descs, be, b, s); return true;
-    case 20: launch_rows_tz<KeyT, 20>(descs, be, b, s); return true;
-    case 21: launch_rows_tz<KeyT, 21>(descs, be, b, s); return true;
-    case 24: launch_rows_tz<KeyT, 24>(descs, be, b, s); return true;
-    case 28: launch_rows_tz<KeyT, 28>(descs, be, b, s); return true;
-    case 30: launch_rows_tz<KeyT, 30>(descs, be, b, s); return true;
-    case 32: launch_rows_tz<KeyT, 32>(descs, be, b, s); return true;
+    case 1 * 4 + 1: launch_rows_tz<KeyT, 1, 1>(descs, be, b, s); return true;
+    case 1 * 4 + 2: launch_rows_tz<KeyT, 1, 2>(descs, be, b, s); return true;
+    case 8 * 4 + 1: launch_rows_tz<KeyT, 8, 1>(descs, be, b, s); return true;
+    case 8 * 4 + 2: launch_rows_tz<KeyT, 8, 2>(descs, be, b, s); return true;
+    case 12 * 4 + 1: launch_rows_tz<KeyT, 12, 1>(descs, be, b, s); return true;
+    case 12 * 4 + 2: launch_rows_tz<KeyT, 12, 2>(descs, be, b, s); return true;
+    case 14 * 4 + 1: launch_rows_tz<KeyT, 14, 1>(descs, be, b, s); return true;
+    case 14 * 4 + 2: launch_rows_tz<KeyT, 14, 2>(descs, be, b, s); return true;
+    case 16 * 4 + 1: launch_rows_tz<KeyT, 16, 1>(descs, be, b, s); return true;
+    case 16 * 4 + 2: launch_rows_tz<KeyT, 16, 2>(descs, be, b, s); return true;
+    case 24 * 4 + 1: launch_rows_tz<KeyT, 24, 1>(descs, be, b, s); return true;
+    case 24 * 4 + 2: launch_rows_tz<KeyT, 24, 2>(descs, be, b, s); return true;
+    case 28 * 4 + 1: launch_rows_tz<KeyT, 28, 1>(descs, be, b, s); return true;
+    case 28 * 4 + 2: launch_rows_tz<KeyT, 28, 2>(descs, be, b, s); return true;
     default: return false;
     }
 }
@@ -1026,7 +1154,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             const Launch<KeyT> &L = launches[i];
             if (L.rows) {
                 uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
-                rows.push_back({P.v[i].TZ * 8 + na, i});
+                rows.push_back({(P.v[i].TZ * 4 + P.v[i].TM) * 8 + na, i});
                 if (P.v[i].nsplit > 1) reds.push_back({0, i});
             } else {
                 gens.push_back({L.ga.nt <= 6 ? L.ga.nt : 0, i});

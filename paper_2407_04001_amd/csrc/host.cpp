@@ -166,14 +166,16 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
     }
 }
 
-const uint32_t kTZ[] = {8, 12, 16, 20, 21, 24, 28, 30, 32};
+// column chunk widths of the row kernel (keys per lane and c, read as one
+// scalar round trip of up to two s_load_dwordx16 plus a smaller load)
+const uint32_t kTZ[] = {8, 12, 14, 16, 24, 28};
 
 struct RowsChoice {
     bool ok = false;
     double cost = 0;
     int z = -1;
     std::vector<int> O, R;
-    uint32_t TZ = 0, na = 0;
+    uint32_t TZ = 0, TM = 1, na = 0;
     uint64_t MO = 1, MR = 1;
 };
 
@@ -264,13 +266,21 @@ static pase_status build_plan(pase_graph_t g) {
     for (int i = 0; i < n; i++) {
         VPlan &vp = P.v[i];
         RowsChoice best;
-        if (g->kernel_mode == 0 && vp.D.size() >= 2) {
-            for (int z : vp.D) {
+        // candidates: every digit of D(i) as the column digit z, and -- only
+        // when none of those fits -- no column at all (z = -1: every digit is
+        // a row digit, each lane streams its own entry's terms over c; for a
+        // lookup that covers all of D(i) this reads T_j once, coalesced)
+        std::vector<int> zs;
+        if (g->kernel_mode == 0 && vp.D.size() >= 2) zs = vp.D;
+        if (g->kernel_mode == 0 && !vp.D.empty()) zs.push_back(-1);
+        for (int z : zs) {
+            if (z < 0 && best.ok) break;
+            {
                 RowsChoice rc;
                 rc.z = z;
                 std::vector<int> O;
                 for (const auto &t : vp.terms)
-                    if (t.dig.size() >= 2 && std::count(t.dig.begin(), t.dig.end(), z))
+                    if (z >= 0 && t.dig.size() >= 2 && std::count(t.dig.begin(), t.dig.end(), z))
                         for (int u : t.dig)
                             if (u != z) O.push_back(u);
                 std::sort(O.begin(), O.end());
@@ -280,7 +290,7 @@ static pase_status build_plan(pase_graph_t g) {
                 rc.O = O;
                 for (int u : rc.O) rc.MO *= g->K[u];
                 for (int u : rc.R) rc.MR *= g->K[u];
-                if (rc.MR < 16) continue;
+                if (rc.MR < (z < 0 ? 256u : 16u)) continue;
                 uint32_t na = 0;
                 for (int u : rc.R) {
                     bool used = false;
@@ -301,13 +311,25 @@ static pase_status build_plan(pase_graph_t g) {
                 }
                 if (na > (uint32_t)kMaxATerms || !small) continue;
                 rc.na = na;
-                const uint32_t Kz = g->K[z];
-                for (uint32_t tz : kTZ) {
+                const uint32_t Kz = z >= 0 ? g->K[z] : 1;
+                static const uint32_t kNoColumn[] = {1};
+                for (uint32_t tz : z >= 0 ? std::vector<uint32_t>(std::begin(kTZ), std::end(kTZ))
+                                          : std::vector<uint32_t>(std::begin(kNoColumn), std::end(kNoColumn))) {
+                    if (z >= 0 && g->tile_cols && tz != g->tile_cols) continue;
                     uint64_t nch = (Kz + tz - 1) / tz;
                     if (rc.MO * vp.K * nch * tz > kMaxTableEntries) continue;
-                    double lanes = (double)rc.MO * (double)((rc.MR + 63) / 64 * 64);
-                    double cost = lanes * (double)nch * (2.0 * tz + na + 1) * vp.K;
-                    if (!rc.ok || cost < rc.cost) { rc.ok = true; rc.cost = cost; rc.TZ = tz; }
+                    for (uint32_t tm = 1; tm <= 2; tm++) {
+                        if (g->tile_rows && tm != g->tile_rows) continue;
+                        if (z < 0 && tm == 2 && !g->tile_rows) continue;   // latency-bound: more waves
+                        // VALU instructions per wave and c: two per cell plus the
+                        // row-term adds; chunks wider than 16 keys do not fit in
+                        // SGPRs twice, lose the scalar-load overlap and are
+                        // charged a few slots of waiting per c
+                        double rows = (double)rc.MO * (double)((rc.MR + 64 * tm - 1) / (64 * tm) * 64 * tm);
+                        double valu = 2.0 * tz * tm + tm * (na > 0 ? na - 1 : 0) + (tz > 16 ? 6.0 : 1.0);
+                        double cost = rows / tm * (double)nch * vp.K * valu;
+                        if (!rc.ok || cost < rc.cost) { rc.ok = true; rc.cost = cost; rc.TZ = tz; rc.TM = tm; }
+                    }
                 }
                 if (rc.ok && (!best.ok || rc.cost < best.cost)) best = rc;
             }
@@ -320,18 +342,35 @@ static pase_status build_plan(pase_graph_t g) {
             vp.MO = best.MO;
             vp.MR = best.MR;
             vp.TZ = best.TZ;
+            vp.TM = best.TM;
             vp.na = best.na;
-            vp.nchunks = (g->K[vp.z] + vp.TZ - 1) / vp.TZ;
+            vp.nchunks = ((vp.z >= 0 ? g->K[vp.z] : 1) + vp.TZ - 1) / vp.TZ;
             vp.ldz = vp.nchunks * vp.TZ;
             vp.layout.clear();
-            vp.layout.push_back(vp.z);
+            if (vp.z >= 0) vp.layout.push_back(vp.z);
             vp.layout.insert(vp.layout.end(), vp.O.begin(), vp.O.end());
             vp.layout.insert(vp.layout.end(), vp.R.begin(), vp.R.end());
-            uint64_t tiles_per_o = (vp.MR + 63) / 64;
-            uint64_t waves = vp.MO * tiles_per_o * vp.nchunks;
-            uint64_t want = (2048 + waves - 1) / waves;
-            uint64_t maxs = std::max<uint64_t>(1, vp.K / 16);
-            uint64_t ns = std::min(want, maxs);
+            uint64_t tiles_per_o = (vp.MR + 64 * vp.TM - 1) / (64 * vp.TM);
+            uint64_t tiles = vp.MO * tiles_per_o * vp.nchunks;
+            // c parts per tile (waves of a workgroup sharing a tile): enough
+            // waves for two full rounds of the chip (256 CUs x 32), but at
+            // least 32 values of c per wave
+            vp.parts = 1;
+            while (vp.parts < 4 && tiles * vp.parts < 16384 && vp.K / (2 * vp.parts) >= 32) vp.parts *= 2;
+            if (g->tile_parts) vp.parts = g->tile_parts;
+            // c split across workgroups (partial keys + a reduction launch):
+            // only when there are fewer waves than SIMDs and one wave's share
+            // of c would run long (> ~10 us; a lone wave issues at about half
+            // rate, and column-less tiles wait on memory, ~150 ns per c); at
+            // least 32 values of c per wave
+            uint64_t ns = 1;
+            const double c_ns = vp.TZ <= 2 ? 150.0 : (2.0 * vp.TZ * vp.TM + vp.na + 2) * 8 / 2.4;
+            const double wave_us = (double)vp.K / vp.parts * c_ns / 1000.0;
+            if (tiles * vp.parts < 1024 && wave_us > 10.0) {
+                uint64_t want = (2048 + tiles * vp.parts - 1) / (tiles * vp.parts);
+                ns = std::min<uint64_t>(want, std::max<uint64_t>(1, vp.K / (32 * vp.parts)));
+            }
+            if (g->c_splits) ns = std::min<uint64_t>(g->c_splits, vp.K);
             vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
             vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
             P.rows_vertices++;
@@ -619,11 +658,31 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0 or 1");
         g->schedule = (int)value;
         break;
+    case PASE_OPT_TILE_COLS:
+        if (value != 0 && std::find(std::begin(kTZ), std::end(kTZ), value) == std::end(kTZ))
+            return fail(g, PASE_ERR_INVALID_ARGUMENT, "tile columns 0, 8, 12, 14, 16, 24 or 28");
+        g->tile_cols = (uint32_t)value;
+        break;
+    case PASE_OPT_TILE_ROWS:
+        if (value > 2) return fail(g, PASE_ERR_INVALID_ARGUMENT, "tile rows 0, 1 or 2");
+        g->tile_rows = (uint32_t)value;
+        break;
+    case PASE_OPT_TILE_PARTS:
+        if (value != 0 && value != 1 && value != 2 && value != 4)
+            return fail(g, PASE_ERR_INVALID_ARGUMENT, "tile parts 0, 1, 2 or 4");
+        g->tile_parts = (uint32_t)value;
+        break;
+    case PASE_OPT_C_SPLITS:
+        if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "c splits 0..65535");
+        g->c_splits = (uint32_t)value;
+        break;
     default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
     }
     // options that change the plan need a fresh enumeration
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
-         opt == PASE_OPT_SCHEDULE) && g->enumerated) {
+         opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
+         opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS) &&
+        g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);
         if (st == PASE_OK) st = layout_memory(g);
@@ -754,6 +813,8 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     x.outer = (uint32_t)vp.MO;
     x.rows = (uint32_t)vp.MR;
     x.tile_cols = vp.TZ;
+    x.tile_rows = vp.TM;
+    x.parts = vp.kernel == kRows ? vp.parts : 0;
     x.splits = vp.nsplit;
     x.row_terms = vp.na;
     x.lookups = (uint32_t)vp.terms.size();

@@ -114,8 +114,9 @@ struct RowsArgs {
     uint16_t *A;              // output argmins
     void *partial;            // nsplit > 1: keys [split][N]
     uint64_t N;
-    uint64_t total_tiles;
+    uint64_t total_tiles;     // tiles (a workgroup takes 4 / parts of them)
     uint32_t nblocks_launched;
+    uint32_t parts;           // waves sharing one tile's c range: 1, 2 or 4
     uint32_t out_shift;       // bits of the table's reader: values are stored x 2^out_shift
 };
 
@@ -181,7 +182,7 @@ struct VPlan {
     // row kernel shape
     int z = -1;                     // column digit (vertex id)
     std::vector<int> O, R;          // outer / row digits (vertex ids), slowest first
-    uint32_t TZ = 0, ldz = 0, nchunks = 0, nsplit = 1, cper = 0;
+    uint32_t TZ = 0, TM = 1, ldz = 0, nchunks = 0, nsplit = 1, cper = 0, parts = 1;
     uint64_t MO = 1, MR = 1;
     uint32_t na = 0;                // row kernel: per-lane row terms
     double fill_ms = 0;             // last profiled fill time
@@ -227,6 +228,7 @@ struct pase_graph_s {
     bool keep_tables = false, profile = false;
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
+    uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
     int schedule = 0;               // 0 = by dependency level, 1 = strictly in sequence
     // configurations
     bool enumerated = false;

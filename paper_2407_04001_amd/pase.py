@@ -19,7 +19,8 @@ MAX_DIMS = 8
 OK, INVALID_ARGUMENT, NOT_CONNECTED, BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMORY, HIP, INTERNAL = range(9)
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STATE", 4: "OVERFLOW",
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
-OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE = range(1, 7)
+(OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
+ OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS) = range(1, 11)
 
 
 class VertexDesc(C.Structure):
@@ -52,8 +53,9 @@ class VertexInfo(C.Structure):
     _fields_ = [("position", C.c_uint32), ("kernel", C.c_uint32), ("num_configs", C.c_uint32),
                 ("dep_count", C.c_uint32), ("entries", C.c_uint64), ("cells", C.c_uint64),
                 ("column", C.c_int32), ("outer", C.c_uint32), ("rows", C.c_uint32),
-                ("tile_cols", C.c_uint32), ("splits", C.c_uint32), ("row_terms", C.c_uint32),
-                ("lookups", C.c_uint32), ("fill_ms", C.c_double)]
+                ("tile_cols", C.c_uint32), ("tile_rows", C.c_uint32), ("splits", C.c_uint32),
+                ("row_terms", C.c_uint32), ("lookups", C.c_uint32), ("parts", C.c_uint32),
+                ("fill_ms", C.c_double)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

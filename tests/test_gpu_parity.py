@@ -65,13 +65,18 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
         assert pg.fingerprint(v) == o.fingerprint(i)
 
 
-def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0):
+def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
+         parts=0, splits=0):
     pg = P.Graph(g, seq_rule=rule)
     pg.enumerate_configs(p or g["p"])
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
     pg.set_option(P.OPT_KEY_TYPE, key)
     pg.set_option(P.OPT_SCHEDULE, schedule)
+    pg.set_option(P.OPT_TILE_COLS, tile[0])
+    pg.set_option(P.OPT_TILE_ROWS, tile[1])
+    pg.set_option(P.OPT_TILE_PARTS, parts)
+    pg.set_option(P.OPT_C_SPLITS, splits)
     if costs is not None:
         pg.override_costs(*costs)
     mc, strat = pg.find_best_strategy()
@@ -116,6 +121,65 @@ def test_random_graphs_model_costs(P, seed):
         assert np.array_equal(pg.layer_costs(v), o.layer_costs(v))
     for e in range(len(g["edges"])):
         assert np.array_equal(pg.edge_costs(e), o.edge_costs(e))
+
+
+# every form of the row kernel: columns x rows per lane, fp64 and uint64 keys
+TILES = [(8, 1), (8, 2), (12, 1), (12, 2), (14, 1), (14, 2), (16, 1), (16, 2), (24, 1), (24, 2),
+         (28, 1), (28, 2)]
+
+
+# (seed, n, extra edges, max dims): together these give row-kernel vertices
+# with 1, 2, 3 and 4 row terms, with and without a column digit
+TILE_GRAPHS = [(600, 8, 6, 3), (600, 10, 10, 2), (600, 9, 8, 3), (601, 8, 6, 3), (601, 9, 8, 3),
+               (661, 10, 10, 2)]
+
+
+@pytest.mark.parametrize("tile", TILES, ids=[f"{a}x{b}" for a, b in TILES])
+def test_forced_row_tiles(P, tile):
+    """Each tile form on graphs whose vertices take the row kernel with one to
+    four row terms, split and unsplit c ranges, and on ties (random costs)."""
+    used = 0
+    for seed, n, extra, dims in TILE_GRAPHS:
+        g = random_graph(seed, n=n, p=16, max_dims=dims, extra_edges=extra, max_size=256)
+        o = _oracle(g)
+        for key in (0, 1):
+            say(f"tile {tile} random graph seed={seed} n={n} key={key}")
+            pg, mc, strat = _run(P, g, key=key, tile=tile)
+            assert (mc, strat) == o.result()
+            _compare_all_entries(pg, o, g, max_entries=256)
+            used += pg.stats()["rows_vertices"]
+        K = [int(k) for k in o.K]
+        costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+        ot = _oracle(g, costs=costs)
+        say(f"tile {tile} random graph seed={seed} n={n} tied costs")
+        pg, mc, strat = _run(P, g, costs=costs, tile=tile)
+        assert (mc, strat) == ot.result()
+        _compare_all_entries(pg, ot, g, max_entries=256)
+    assert used > 0
+
+
+@pytest.mark.parametrize("parts,splits", [(1, 2), (2, 1), (2, 3), (4, 1), (4, 5), (4, 64)],
+                         ids=["p1s2", "p2s1", "p2s3", "p4s1", "p4s5", "p4s64"])
+def test_forced_parts_and_splits(P, parts, splits):
+    """c ranges shared by the waves of a workgroup (merged through LDS) and by
+    workgroups (partial keys and a reduction launch), including empty parts
+    (more parts or splits than values of c)."""
+    for tile in [(16, 1), (14, 2), (28, 1)]:
+        for seed, n, extra, dims in TILE_GRAPHS:
+            g = random_graph(seed, n=n, p=16, max_dims=dims, extra_edges=extra, max_size=256)
+            o = _oracle(g)
+            for key in (0, 1):
+                say(f"parts {parts} splits {splits} tile {tile} graph seed={seed} n={n} key={key}")
+                pg, mc, strat = _run(P, g, key=key, tile=tile, parts=parts, splits=splits)
+                assert (mc, strat) == o.result()
+                _compare_all_entries(pg, o, g, max_entries=128)
+
+
+@pytest.mark.parametrize("tile", [(8, 1), (16, 1), (16, 2), (28, 1), (28, 2)],
+                         ids=["8x1", "16x1", "16x2", "28x1", "28x2"])
+def test_forced_row_tiles_against_golden(P, tile):
+    for name in ("w2_inception", "w4_transformer"):
+        _check_golden(P, name, 0, tile=tile)
 
 
 @pytest.mark.parametrize("seed", range(4))
@@ -184,11 +248,11 @@ def _golden(name, seed):
         return json.load(f)
 
 
-def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0):
+def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0)):
     gold = _golden(name, seed)
     g = workload(name, seed)
-    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule}")
-    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, schedule=schedule)
+    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile}")
+    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']}")
