@@ -4,6 +4,7 @@
 // layout.  No HIP calls here: everything is pure host computation so it can be
 // exercised without a GPU.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <numeric>
 
@@ -175,9 +176,76 @@ struct RowsChoice {
     double cost = 0;
     int z = -1;
     std::vector<int> O, R;
-    uint32_t TZ = 0, TM = 1, na = 0;
+    uint32_t TZ = 0, TM = 1, na = 0, parts = 1, nsplit = 1;
     uint64_t MO = 1, MR = 1;
 };
+
+// Estimated fill time (us) of one row-kernel vertex for a tile shape, with the
+// best number of c parts per tile (waves of a workgroup) and c splits (across
+// workgroups) -- or the forced ones.  The time is the larger of the throughput
+// bound (the busiest SIMD's waves, each issuing a VALU op every 4 cycles) and
+// the latency bound of a single wave: per value of c at least one memory round
+// trip for the operands prefetched one c ahead (~450 cycles; column-less tiles
+// keep 8 values of c in flight, ~360 cycles per c), or its own VALU work at
+// about one op per 8 cycles; column-less tiles also stream their row terms at
+// ~5 TB/s.  A c split adds a reduction launch (~10 us with its gap) and the
+// partial keys' traffic; the column block is built at ~115 G elements/s.
+struct TileTime {
+    double us;
+    uint32_t parts, nsplit;
+};
+
+TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t na, uint32_t tz, uint32_t tm,
+                   uint32_t force_parts, uint32_t force_splits) {
+    const double clk = 2400.0;   // cycles per us
+    const uint64_t nch = (Kz + tz - 1) / tz;
+    const uint64_t tiles = MO * ((MR + 64 * tm - 1) / (64 * tm)) * nch;
+    const uint64_t N = MO * MR * (uint64_t)Kz;
+    const double prep_us = (double)MO * K * nch * tz / 1.15e5;
+    TileTime best{1e300, 1, 1};
+    for (uint32_t P = 1; P <= 4; P *= 2) {
+        if (force_parts && P != force_parts) continue;
+        for (uint32_t S = 1; S <= 64; S *= 2) {
+            if (force_splits && S != 1) break;
+            const uint32_t Sx = force_splits ? std::min(force_splits, K) : S;
+            if (!force_splits && S > 1 && K < 8 * P * S) break;
+            const double cw = std::ceil(std::ceil((double)K / Sx) / P);
+            double wave_cyc, lat_cyc, bw_us = 0;
+            if (tz >= 8) {
+                // VALU slots per c: two per cell, the row-term adds, and (measured)
+                // a few for wide chunks (> 16 keys: no scalar-load overlap) and
+                // for two rows per lane (more VGPRs, fewer waves).  Every row-term
+                // load is a wave-wide vector load that keeps the CU's texture
+                // address unit ~16 cycles busy; shared by four SIMDs, that costs
+                // ~15 VALU slots per load per wave when all SIMDs are busy; the
+                // two overlap imperfectly (fitted: the smaller adds a quarter).
+                const double valu = 2.0 * tz * tm + tm * (na > 0 ? na - 1.0 : 0.0) + 1.0 + (tz > 16 ? 2.0 : 0.0) +
+                                    (tm == 2 ? 2.0 : 0.0);
+                const double ta = 14.7 * na * tm;
+                double per_c = std::max(valu, ta) + 0.25 * std::min(valu, ta);
+                // a column block larger than the L2s is read from HBM: a scalar
+                // round trip then takes ~2000 cycles, ~60 slots per wave with
+                // eight waves per SIMD -- hidden behind one c of work when the
+                // loads of c + 1 are in flight (up to 16 keys), exposed when not
+                if ((double)MO * K * nch * tz * 8 > 16e6) per_c = tz > 16 ? per_c + 62.0 : std::max(per_c, 62.0);
+                const double tail = tz * tm * (P > 1 ? 8.0 : 6.0);
+                wave_cyc = 4.0 * (cw * per_c + tail);
+                lat_cyc = cw * std::max(8.0 * per_c, 450.0) + 8.0 * tail;
+            } else {
+                wave_cyc = 4.0 * cw * (2.0 * tm + tm * (na > 0 ? na - 1.0 : 0.0) + 1.0);
+                lat_cyc = 360.0 * cw;
+                bw_us = (double)N * K * na * 8 / 5e6;
+            }
+            // the busiest SIMD: the average share plus, on average, half a wave
+            const double W = (double)tiles * P * Sx;
+            const double t_tp = (W / 1024.0 + 0.5) * wave_cyc / clk;
+            double us = std::max(std::max(t_tp, lat_cyc / clk), bw_us) + prep_us;
+            if (Sx > 1) us += 10.0 + (double)N * Sx * 16 / 5e6;
+            if (us < best.us) best = {us, P, Sx};
+        }
+    }
+    return best;
+}
 
 }  // namespace
 
@@ -191,7 +259,14 @@ static pase_status build_plan(pase_graph_t g) {
     for (int i = 0; i < n; i++) P.pos[P.seq[i]] = i;
     P.v.assign(n, VPlan());
 
-    std::vector<int> mark(n, -1), comp(n, -1), stack;
+    // components of the graph induced on positions < i, grown one position at
+    // a time (union-find over vertex ids); each set remembers its last position
+    std::vector<int> uf(n), last(n, -1), seen(n, -1);
+    std::iota(uf.begin(), uf.end(), 0);
+    auto find = [&](int x) {
+        while (uf[x] != x) x = uf[x] = uf[uf[x]];
+        return x;
+    };
     for (int i = 0; i < n; i++) {
         VPlan &vp = P.v[i];
         vp.vi = P.seq[i];
@@ -206,30 +281,14 @@ static pase_status build_plan(pase_graph_t g) {
         for (int w : vp.D)
             if (!mul_ok(vp.N, g->K[w], &vp.N) || vp.N > kMaxTableEntries)
                 return fail(g, PASE_ERR_TOO_LARGE, "a DP table exceeds 2^31 entries");
-        // X(i): reachable from v_i through positions <= i
-        stack.assign(1, vp.vi);
-        mark[vp.vi] = i;
-        std::vector<int> X{vp.vi};
-        while (!stack.empty()) {
-            int x = stack.back();
-            stack.pop_back();
-            for (int y : g->nbr[x])
-                if (P.pos[y] <= i && mark[y] != i) { mark[y] = i; X.push_back(y); stack.push_back(y); }
-        }
-        // S(i): components of X(i) - {v_i} inside positions < i, each represented by
-        // its last position j; every one is a neighbour component of v_i
+        // S(i): the components of V<i that v_i touches, each represented by its
+        // last position j (X(i) - {v_i} is their union)
         for (int s : g->nbr[vp.vi]) {
-            if (P.pos[s] >= i || comp[s] == i) continue;
-            int jmax = P.pos[s];
-            stack.assign(1, s);
-            comp[s] = i;
-            while (!stack.empty()) {
-                int x = stack.back();
-                stack.pop_back();
-                jmax = std::max(jmax, P.pos[x]);
-                for (int y : g->nbr[x])
-                    if (P.pos[y] < i && comp[y] != i) { comp[y] = i; stack.push_back(y); }
-            }
+            if (P.pos[s] >= i) continue;
+            const int rt = find(s);
+            if (seen[rt] == i) continue;
+            seen[rt] = i;
+            const int jmax = last[rt];
             TermRef t;
             t.j = jmax;
             bool has_vi = false;
@@ -244,6 +303,14 @@ static pase_status build_plan(pase_graph_t g) {
             P.v[jmax].consumer = i;
             vp.terms.push_back(t);
         }
+        // v_i joins the components it touches and is their last position
+        last[vp.vi] = i;
+        for (int s : g->nbr[vp.vi])
+            if (P.pos[s] < i) {
+                const int a = find(s), b = find(vp.vi);
+                if (a != b) uf[a] = b;
+            }
+        last[find(vp.vi)] = i;
         for (size_t k = 0; k < g->E.size(); k++) {
             const auto &d = g->E[k];
             int other = (int)d.src == vp.vi ? (int)d.dst : ((int)d.dst == vp.vi ? (int)d.src : -1);
@@ -320,15 +387,17 @@ static pase_status build_plan(pase_graph_t g) {
                     if (rc.MO * vp.K * nch * tz > kMaxTableEntries) continue;
                     for (uint32_t tm = 1; tm <= 2; tm++) {
                         if (g->tile_rows && tm != g->tile_rows) continue;
-                        if (z < 0 && tm == 2 && !g->tile_rows) continue;   // latency-bound: more waves
-                        // VALU instructions per wave and c: two per cell plus the
-                        // row-term adds; chunks wider than 16 keys do not fit in
-                        // SGPRs twice, lose the scalar-load overlap and are
-                        // charged a few slots of waiting per c
-                        double rows = (double)rc.MO * (double)((rc.MR + 64 * tm - 1) / (64 * tm) * 64 * tm);
-                        double valu = 2.0 * tz * tm + tm * (na > 0 ? na - 1 : 0) + (tz > 16 ? 6.0 : 1.0);
-                        double cost = rows / tm * (double)nch * vp.K * valu;
-                        if (!rc.ok || cost < rc.cost) { rc.ok = true; rc.cost = cost; rc.TZ = tz; rc.TM = tm; }
+                        // more than 32 accumulators per lane cost waves (VGPRs)
+                        if (!g->tile_rows && !g->tile_cols && tz * tm > 32) continue;
+                        const TileTime tt = tile_time(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts, g->c_splits);
+                        if (!rc.ok || tt.us < rc.cost) {
+                            rc.ok = true;
+                            rc.cost = tt.us;
+                            rc.TZ = tz;
+                            rc.TM = tm;
+                            rc.parts = tt.parts;
+                            rc.nsplit = tt.nsplit;
+                        }
                     }
                 }
                 if (rc.ok && (!best.ok || rc.cost < best.cost)) best = rc;
@@ -350,27 +419,8 @@ static pase_status build_plan(pase_graph_t g) {
             if (vp.z >= 0) vp.layout.push_back(vp.z);
             vp.layout.insert(vp.layout.end(), vp.O.begin(), vp.O.end());
             vp.layout.insert(vp.layout.end(), vp.R.begin(), vp.R.end());
-            uint64_t tiles_per_o = (vp.MR + 64 * vp.TM - 1) / (64 * vp.TM);
-            uint64_t tiles = vp.MO * tiles_per_o * vp.nchunks;
-            // c parts per tile (waves of a workgroup sharing a tile): enough
-            // waves for two full rounds of the chip (256 CUs x 32), but at
-            // least 32 values of c per wave
-            vp.parts = 1;
-            while (vp.parts < 4 && tiles * vp.parts < 16384 && vp.K / (2 * vp.parts) >= 32) vp.parts *= 2;
-            if (g->tile_parts) vp.parts = g->tile_parts;
-            // c split across workgroups (partial keys + a reduction launch):
-            // only when there are fewer waves than SIMDs and one wave's share
-            // of c would run long (> ~10 us; a lone wave issues at about half
-            // rate, and column-less tiles wait on memory, ~150 ns per c); at
-            // least 32 values of c per wave
-            uint64_t ns = 1;
-            const double c_ns = vp.TZ <= 2 ? 150.0 : (2.0 * vp.TZ * vp.TM + vp.na + 2) * 8 / 2.4;
-            const double wave_us = (double)vp.K / vp.parts * c_ns / 1000.0;
-            if (tiles * vp.parts < 1024 && wave_us > 10.0) {
-                uint64_t want = (2048 + tiles * vp.parts - 1) / (tiles * vp.parts);
-                ns = std::min<uint64_t>(want, std::max<uint64_t>(1, vp.K / (32 * vp.parts)));
-            }
-            if (g->c_splits) ns = std::min<uint64_t>(g->c_splits, vp.K);
+            vp.parts = best.parts;
+            const uint64_t ns = best.nsplit;
             vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
             vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
             P.rows_vertices++;
@@ -549,31 +599,36 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->flops.assign(nv, 0);
     g->keep_n.assign(nv, 0);
     g->maxL.assign(nv, 0);
+    // the configurations of a vertex depend only on its dimension count
+    std::vector<std::vector<uint8_t>> by_dims(kMaxDims + 1);
     for (size_t v = 0; v < nv; v++) {
         const uint32_t d = g->V[v].ndims;
-        // exponent tuples with sum <= L in lexicographic order (dim 0 slowest),
-        // produced by the lexicographic successor: bump the last dim that still
-        // has room and clear the dims after it
-        std::vector<uint8_t> cur(d, 0), rows;
-        for (;;) {
-            rows.insert(rows.end(), cur.begin(), cur.end());
-            uint32_t sum = 0;
-            for (uint8_t x : cur) sum += x;
-            int k = (int)d - 1;
-            if (sum < L) {
-                cur[k]++;
-                continue;
+        std::vector<uint8_t> &rows = by_dims[d];
+        if (rows.empty()) {
+            // exponent tuples with sum <= L in lexicographic order (dim 0 slowest),
+            // produced by the lexicographic successor: bump the last dim that still
+            // has room and clear the dims after it
+            std::vector<uint8_t> cur(d, 0);
+            for (;;) {
+                rows.insert(rows.end(), cur.begin(), cur.end());
+                uint32_t sum = 0;
+                for (uint8_t x : cur) sum += x;
+                int k = (int)d - 1;
+                if (sum < L) {
+                    cur[k]++;
+                    continue;
+                }
+                // sum == L: find the last k > 0... increment dim k-1 and zero dims >= k
+                while (k >= 0 && cur[k] == 0) k--;
+                if (k <= 0) break;
+                cur[k] = 0;
+                cur[k - 1]++;
             }
-            // sum == L: find the last k > 0... increment dim k-1 and zero dims >= k
-            while (k >= 0 && cur[k] == 0) k--;
-            if (k <= 0) break;
-            cur[k] = 0;
-            cur[k - 1]++;
         }
         uint64_t K = rows.size() / d;
         if (K > 65535) return fail(g, PASE_ERR_TOO_LARGE, "more than 65535 configurations");
         g->K[v] = (uint32_t)K;
-        g->ex[v] = std::move(rows);
+        g->ex[v] = rows;
         uint64_t fl = g->V[v].flops_per_point, keep = 1;
         for (uint32_t k = 0; k < d; k++) {
             if (!mul_ok(fl, g->V[v].size[k], &fl))

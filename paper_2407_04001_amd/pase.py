@@ -264,7 +264,7 @@ class Graph:
         self.h = pase_graph_create(graph["vertices"], graph["edges"], graph.get("comm_weight", 8),
                                    seq_rule)
         self._ws = None
-        self.K = None
+        self._K = None
 
     def close(self):
         if getattr(self, "h", None):
@@ -276,9 +276,16 @@ class Graph:
         self.close()
 
     def enumerate_configs(self, p: int):
+        """Enumerate configurations and plan the search for p devices; the
+        per-vertex configuration counts are read lazily through `K`."""
         pase_enumerate_configs(self.h, p)
-        self.K = [pase_num_configs(self.h, v) for v in range(self.nv)]
-        return self.K
+        self._K = None
+
+    @property
+    def K(self):
+        if self._K is None:
+            self._K = [pase_num_configs(self.h, v) for v in range(self.nv)]
+        return self._K
 
     def set_option(self, opt: int, value: int):
         pase_set_option(self.h, opt, value)
