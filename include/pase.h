@@ -128,6 +128,11 @@ typedef struct {
     double rows_fill_ms;       /* PASE_OPT_PROFILE: same, row/column-chunk kernel only */
     uint32_t rows_launches;    /* PASE_OPT_PROFILE: launches of that kernel */
     uint32_t slots;            /* launch slots: dependency levels, or vertices when sequential */
+    uint64_t stream_cells;     /* cells of the row kernel's column-less (streaming) form, a part
+                                  of rows_cells */
+    double stream_fill_ms;     /* PASE_OPT_PROFILE: event time of those launches, a part of
+                                  rows_fill_ms */
+    uint32_t stream_launches;  /* PASE_OPT_PROFILE: their launches, a part of rows_launches */
 } pase_run_stats;
 
 /* Copy a computation graph G=(V,E) (Sec. II) into a new handle.

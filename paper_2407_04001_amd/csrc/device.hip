@@ -16,6 +16,7 @@
 // then exact integer arithmetic and min-plus costs one v_add_f64 and one
 // v_min_f64 per cell.  Otherwise keys are uint64.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <algorithm>
 #include <chrono>
@@ -994,55 +995,58 @@ struct Batch {
 };
 
 template <typename KeyT, int TZ, int TM>
-static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s, hipEvent_t e0,
+                           hipEvent_t e1) {
     dim3 grid(b.blocks), block(256);
     const uint32_t na = b.variant % 8;
     if constexpr (std::is_same<KeyT, double>::value) {
         switch (na) {
-        case 0: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 0>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 1: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 1>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 2: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 2>), grid, block, 0, s, descs, be, b.nentries); break;
-        case 3: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 3>), grid, block, 0, s, descs, be, b.nentries); break;
-        default: hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 4>), grid, block, 0, s, descs, be, b.nentries); break;
+        case 0: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 0>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+        case 1: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+        case 2: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 2>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+        case 3: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 3>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+        default: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 4>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
         }
     } else {
-        hipLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, -1>), grid, block, 0, s, descs, be, b.nentries);
+        hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, -1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries);
     }
 }
 
 // variant = (TZ * 4 + TM) * 8 + NA
 template <typename KeyT>
-static bool launch_rows(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+static bool launch_rows(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s, hipEvent_t e0,
+                        hipEvent_t e1) {
     switch (b.variant / 8) {
-    case 1 * 4 + 1: launch_rows_tz<KeyT, 1, 1>(descs, be, b, s); return true;
-    case 1 * 4 + 2: launch_rows_tz<KeyT, 1, 2>(descs, be, b, s); return true;
-    case 8 * 4 + 1: launch_rows_tz<KeyT, 8, 1>(descs, be, b, s); return true;
-    case 8 * 4 + 2: launch_rows_tz<KeyT, 8, 2>(descs, be, b, s); return true;
-    case 12 * 4 + 1: launch_rows_tz<KeyT, 12, 1>(descs, be, b, s); return true;
-    case 12 * 4 + 2: launch_rows_tz<KeyT, 12, 2>(descs, be, b, s); return true;
-    case 14 * 4 + 1: launch_rows_tz<KeyT, 14, 1>(descs, be, b, s); return true;
-    case 14 * 4 + 2: launch_rows_tz<KeyT, 14, 2>(descs, be, b, s); return true;
-    case 16 * 4 + 1: launch_rows_tz<KeyT, 16, 1>(descs, be, b, s); return true;
-    case 16 * 4 + 2: launch_rows_tz<KeyT, 16, 2>(descs, be, b, s); return true;
-    case 24 * 4 + 1: launch_rows_tz<KeyT, 24, 1>(descs, be, b, s); return true;
-    case 24 * 4 + 2: launch_rows_tz<KeyT, 24, 2>(descs, be, b, s); return true;
-    case 28 * 4 + 1: launch_rows_tz<KeyT, 28, 1>(descs, be, b, s); return true;
-    case 28 * 4 + 2: launch_rows_tz<KeyT, 28, 2>(descs, be, b, s); return true;
+    case 1 * 4 + 1: launch_rows_tz<KeyT, 1, 1>(descs, be, b, s, e0, e1); return true;
+    case 1 * 4 + 2: launch_rows_tz<KeyT, 1, 2>(descs, be, b, s, e0, e1); return true;
+    case 8 * 4 + 1: launch_rows_tz<KeyT, 8, 1>(descs, be, b, s, e0, e1); return true;
+    case 8 * 4 + 2: launch_rows_tz<KeyT, 8, 2>(descs, be, b, s, e0, e1); return true;
+    case 12 * 4 + 1: launch_rows_tz<KeyT, 12, 1>(descs, be, b, s, e0, e1); return true;
+    case 12 * 4 + 2: launch_rows_tz<KeyT, 12, 2>(descs, be, b, s, e0, e1); return true;
+    case 14 * 4 + 1: launch_rows_tz<KeyT, 14, 1>(descs, be, b, s, e0, e1); return true;
+    case 14 * 4 + 2: launch_rows_tz<KeyT, 14, 2>(descs, be, b, s, e0, e1); return true;
+    case 16 * 4 + 1: launch_rows_tz<KeyT, 16, 1>(descs, be, b, s, e0, e1); return true;
+    case 16 * 4 + 2: launch_rows_tz<KeyT, 16, 2>(descs, be, b, s, e0, e1); return true;
+    case 24 * 4 + 1: launch_rows_tz<KeyT, 24, 1>(descs, be, b, s, e0, e1); return true;
+    case 24 * 4 + 2: launch_rows_tz<KeyT, 24, 2>(descs, be, b, s, e0, e1); return true;
+    case 28 * 4 + 1: launch_rows_tz<KeyT, 28, 1>(descs, be, b, s, e0, e1); return true;
+    case 28 * 4 + 2: launch_rows_tz<KeyT, 28, 2>(descs, be, b, s, e0, e1); return true;
     default: return false;
     }
 }
 
 template <typename KeyT>
-static void launch_generic(const GenericArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s) {
+static void launch_generic(const GenericArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s,
+                           hipEvent_t e0, hipEvent_t e1) {
     dim3 grid(b.blocks), block(256);
     switch (b.variant) {
-    case 1: hipLaunchKernelGGL((k_fill_generic<KeyT, 1>), grid, block, 0, s, descs, be, b.nentries); break;
-    case 2: hipLaunchKernelGGL((k_fill_generic<KeyT, 2>), grid, block, 0, s, descs, be, b.nentries); break;
-    case 3: hipLaunchKernelGGL((k_fill_generic<KeyT, 3>), grid, block, 0, s, descs, be, b.nentries); break;
-    case 4: hipLaunchKernelGGL((k_fill_generic<KeyT, 4>), grid, block, 0, s, descs, be, b.nentries); break;
-    case 5: hipLaunchKernelGGL((k_fill_generic<KeyT, 5>), grid, block, 0, s, descs, be, b.nentries); break;
-    case 6: hipLaunchKernelGGL((k_fill_generic<KeyT, 6>), grid, block, 0, s, descs, be, b.nentries); break;
-    default: hipLaunchKernelGGL((k_fill_generic<KeyT, -1>), grid, block, 0, s, descs, be, b.nentries); break;
+    case 1: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    case 2: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 2>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    case 3: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 3>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    case 4: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 4>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    case 5: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 5>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    case 6: hipExtLaunchKernelGGL((k_fill_generic<KeyT, 6>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+    default: hipExtLaunchKernelGGL((k_fill_generic<KeyT, -1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
     }
 }
 
@@ -1229,14 +1233,16 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             break;
         case Batch::kRows:
         case Batch::kGeneric:
-            // with profiling, events bracket exactly this fill launch
-            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * fb], s));
+        {
+            // with profiling, the launch itself records its start and end
+            // (events attached to the dispatch, no extra packets in the stream)
+            hipEvent_t e0 = g->profile ? d->ev[2 * fb] : nullptr, e1 = g->profile ? d->ev[2 * fb + 1] : nullptr;
             if (b.kind == Batch::kRows) {
-                if (!launch_rows<KeyT>(dr, e, b, s)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+                if (!launch_rows<KeyT>(dr, e, b, s, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
             } else {
-                launch_generic<KeyT>(dg, e, b, s);
+                launch_generic<KeyT>(dg, e, b, s, e0, e1);
             }
-            if (g->profile) HIPCHK(hipEventRecord(d->ev[2 * fb + 1], s));
+        }
             for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
             fb++;
             break;
@@ -1263,8 +1269,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
-    g->stats.fill_ms = g->stats.rows_fill_ms = 0;
-    g->stats.rows_launches = 0;
+    g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
+    g->stats.rows_launches = g->stats.stream_launches = 0;
     if (g->profile) {
         std::vector<float> ms(fb, 0.f);
         uint32_t k = 0;
@@ -1272,7 +1278,14 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             if (b.kind != Batch::kRows && b.kind != Batch::kGeneric) continue;
             HIPCHK(hipEventElapsedTime(&ms[k], d->ev[2 * k], d->ev[2 * k + 1]));
             g->stats.fill_ms += ms[k];
-            if (b.kind == Batch::kRows) { g->stats.rows_fill_ms += ms[k]; g->stats.rows_launches++; }
+            if (b.kind == Batch::kRows) {
+                g->stats.rows_fill_ms += ms[k];
+                g->stats.rows_launches++;
+                if (b.variant / 32 == 1) {   // one column per lane: the column-less form
+                    g->stats.stream_fill_ms += ms[k];
+                    g->stats.stream_launches++;
+                }
+            }
             k++;
         }
         for (int i = 0; i < n; i++) P.v[i].fill_ms = fill_of[i] >= 0 ? ms[fill_of[i]] : 0.0;
@@ -1307,6 +1320,7 @@ pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint
     g->stats.key_type = kt;
     g->stats.rows_vertices = P.rows_vertices;
     g->stats.rows_cells = P.rows_cells;
+    g->stats.stream_cells = P.stream_cells;
     g->stats.wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
     return PASE_OK;
 }

@@ -425,6 +425,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
             P.rows_vertices++;
             P.rows_cells += vp.N * vp.K;
+            if (vp.z < 0) P.stream_cells += vp.N * vp.K;
         } else {
             vp.kernel = kGeneric;
             vp.layout = vp.D;

@@ -199,7 +199,7 @@ struct VPlan {
 struct Plan {
     std::vector<int> seq, pos;
     std::vector<VPlan> v;           // by position
-    uint64_t cells = 0, entries = 0, rows_cells = 0;
+    uint64_t cells = 0, entries = 0, rows_cells = 0, stream_cells = 0;
     uint32_t max_dep = 0, rows_vertices = 0;
     // workspace layout, byte offsets from the workspace base
     uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_lsum = 0, off_sig = 0,

@@ -43,7 +43,8 @@ class RunStats(C.Structure):
                 ("max_dep", C.c_uint32), ("key_type", C.c_uint32), ("launches", C.c_uint32),
                 ("rows_vertices", C.c_uint32), ("rows_cells", C.c_uint64), ("host_plan_ms", C.c_double),
                 ("wall_ms", C.c_double), ("fill_ms", C.c_double), ("rows_fill_ms", C.c_double),
-                ("rows_launches", C.c_uint32), ("slots", C.c_uint32)]
+                ("rows_launches", C.c_uint32), ("slots", C.c_uint32), ("stream_cells", C.c_uint64),
+                ("stream_fill_ms", C.c_double), ("stream_launches", C.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
