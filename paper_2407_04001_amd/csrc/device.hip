@@ -583,6 +583,36 @@ __global__ void k_backtrack(const BacktrackDesc *__restrict__ bt, uint32_t n, co
     out->status = status;
 }
 
+// Back-substitution by backward levels: one thread per position; the
+// configurations of one level depend only on those of lower levels, so a level
+// costs one dependent argmin read instead of one per vertex.  Configurations
+// live in LDS until the end.
+template <typename KeyT>
+__global__ __launch_bounds__(kMaxBacktrackThreads) void k_backtrack_levels(const BacktrackDesc *__restrict__ bt,
+                                                                          uint32_t n, uint32_t nlev,
+                                                                          const void *Tlast,
+                                                                          uint32_t *__restrict__ cfg,
+                                                                          SearchOut *out) {
+    __shared__ uint32_t scfg[kMaxBacktrackThreads];
+    const uint32_t t = threadIdx.x;
+    const bool mine = t < n;
+    BacktrackDesc d;
+    if (mine) d = bt[t];
+    for (uint32_t lev = 0; lev < nlev; lev++) {
+        if (mine && d.level == lev) {
+            uint64_t idx = 0;
+            for (uint32_t k = 0; k < d.m; k++) idx += (uint64_t)scfg[d.dig[k]] * d.stride[k];
+            scfg[d.vi] = d.A[idx];
+        }
+        __syncthreads();
+    }
+    if (mine) cfg[t] = scfg[t];
+    if (t == 0) {
+        out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
+        out->status = 0;
+    }
+}
+
 // ------------------------------------------------------------------ fingerprints (tests)
 struct FingerArgs {
     const void *T;
@@ -1106,7 +1136,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     }
     std::memcpy(img + P.off_contrib, contrib.data(), contrib.size() * sizeof(Contrib));
     std::vector<BacktrackDesc> bt(n);
-    for (int i = 0; i < n; i++) {
+    uint32_t nlev = 0;
+    for (int i = n - 1; i >= 0; i--) {
         const VPlan &vp = P.v[i];
         BacktrackDesc &b = bt[i];
         std::memset(&b, 0, sizeof b);
@@ -1117,6 +1148,9 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             b.dig[k] = (uint32_t)vp.layout[k];
             b.stride[k] = vp.stride[k];
         }
+        // the configuration of v_i needs those of D(i), all later in the order
+        for (int u : vp.D) b.level = std::max(b.level, bt[P.pos[u]].level + 1);
+        nlev = std::max(nlev, b.level + 1);
     }
     std::memcpy(img + P.off_bt, bt.data(), n * sizeof(BacktrackDesc));
 
@@ -1252,8 +1286,13 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
         launches_n++;
     }
-    hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
-                       (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+    if ((uint32_t)n <= kMaxBacktrackThreads)
+        hipLaunchKernelGGL((k_backtrack_levels<KeyT>), dim3(1), dim3((n + 63) / 64 * 64), 0, s,
+                           (const BacktrackDesc *)(ws + P.off_bt), (uint32_t)n, nlev,
+                           (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+    else
+        hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
+                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
     launches_n++;
     HIPCHK(hipGetLastError());
     char *host_out = img;   // reuse the staging buffer after the upload has been consumed

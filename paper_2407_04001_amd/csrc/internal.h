@@ -149,9 +149,12 @@ struct ReduceArgs {
 struct BacktrackDesc {        // per position, for the back-substitution kernel
     const uint16_t *A;
     uint32_t vi, m;
+    uint32_t level, pad;      // backward level: 1 + max level over D(i) (0 when D(i) is empty)
     uint32_t dig[kMaxDep];    // vertex ids of the layout digits
     uint64_t stride[kMaxDep];
 };
+
+constexpr uint32_t kMaxBacktrackThreads = 1024;   // one thread per position
 
 struct SearchOut {            // written by the back-substitution kernel
     uint64_t min_cost;

@@ -192,6 +192,17 @@ def test_chains(P, seed):
     _compare_all_entries(pg, o, g)
 
 
+def test_long_chain_back_substitution(P):
+    """More positions than the level-parallel back-substitution's one
+    workgroup takes (1024): the search falls back to the sequential walk."""
+    for n in (1024, 1100):
+        g = chain_graph(5, n=n, p=4, max_dims=2)
+        say(f"long chain n={n}")
+        o = _oracle(g)
+        pg, mc, strat = _run(P, g, keep=False)
+        assert (mc, strat) == o.result()
+
+
 def test_edge_cases(P):
     # one vertex, no edges: the minimum layer cost
     g = {"name": "one", "p": 8, "comm_weight": 8, "edges": [],
