@@ -97,19 +97,25 @@ typedef enum {
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
     PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats) */
-    PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
-                                   do not read each other) share their kernel launches and run
-                                   concurrently; 1: one vertex at a time in sequence order.  Memory
-                                   is packed by table lifetimes in either case. */
+    PASE_OPT_SCHEDULE = 6,      /* 0 (default): dataflow -- one persistent launch runs the prep,
+                                   fill and reduction work of every vertex as soon as the tables
+                                   it reads are complete (device-side dependency counters); needs
+                                   every table resident at once, else falls back to 2.
+                                   1: one vertex at a time in sequence order.  2: vertices of one
+                                   dependency level (whose tables do not read each other) share
+                                   their kernel launches.  1 and 2 pack table memory by lifetimes. */
     PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
                                    vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
                                    that kernel runs (a tuning and test knob) */
     PASE_OPT_TILE_ROWS = 8,     /* same kernel: table rows per lane, 0 = chosen (default), 1 or 2 */
     PASE_OPT_TILE_PARTS = 9,    /* same kernel: waves sharing one tile's c range, 0 = chosen
                                    (default), 1, 2 or 4 */
-    PASE_OPT_C_SPLITS = 10      /* same kernel: workgroups sharing one tile's c range (partial
+    PASE_OPT_C_SPLITS = 10,     /* same kernel: workgroups sharing one tile's c range (partial
                                    keys reduced by a second launch), 0 = chosen (default), else
                                    min(value, K_v) for every vertex */
+    PASE_OPT_LATENCY_WORKERS = 11 /* dataflow schedule: workgroups that serve the latency queue
+                                   (the chains of small vertices) before the bulk queue; 0 =
+                                   chosen (default: one in 16), else clamped to [1, grid - 1] */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */
@@ -133,6 +139,12 @@ typedef struct {
     double stream_fill_ms;     /* PASE_OPT_PROFILE: event time of those launches, a part of
                                   rows_fill_ms */
     uint32_t stream_launches;  /* PASE_OPT_PROFILE: their launches, a part of rows_launches */
+    uint32_t schedule;         /* schedule the search ran with: 0 = dataflow (one launch runs every
+                                  prep, fill and reduction; rows_fill_ms is its duration), 1 = one
+                                  vertex at a time, 2 = by dependency level */
+    uint32_t flow_grid;        /* dataflow: workgroups of the launch */
+    uint32_t flow_lat_workers; /* dataflow: of them, latency workers */
+    uint64_t flow_items;       /* dataflow: work items (prep, fill and reduction workgroups) */
 } pase_run_stats;
 
 /* Copy a computation graph G=(V,E) (Sec. II) into a new handle.
@@ -241,9 +253,22 @@ typedef struct {
     uint32_t splits, row_terms, lookups;
     uint32_t parts;      /* row kernel: waves sharing one tile's c range (1, 2 or 4) */
     double fill_ms;      /* PASE_OPT_PROFILE: event time of this vertex's fill kernel */
+    uint32_t level;      /* dependency level: 1 + the largest level of the tables it reads */
+    uint32_t lane;       /* lane schedule: the stream it runs on (0 = the caller's, 1, 2) */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);
+
+/* Test hook (host only, no device work): build the dataflow schedule of the
+ * current plan (PASE_OPT_SCHEDULE 0, after pase_enumerate_configs) and run a
+ * randomized simulation of its worker protocol with `workers` workgroups, the
+ * first `lat_workers` of them serving the latency queue first.  *items: the
+ * number of work items.  Errors: INVALID_ARGUMENT (workers < 2, lat_workers
+ * not in [1, workers)), BAD_STATE (no plan, or the plan fell back to another
+ * schedule), INTERNAL (the simulated workers deadlock, an item would start
+ * before its dependencies are met, or items are left undone). */
+pase_status pase_flow_check(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
+                            uint64_t *items);
 
 #ifdef __cplusplus
 }

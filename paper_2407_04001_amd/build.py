@@ -1,4 +1,6 @@
-"""Build libpase.so (host planner + gfx950 kernels) in-tree with hipcc."""
+"""Build libpase.so (host planner + gfx950 kernels) in-tree with hipcc.
+
+The sources are compiled to objects in parallel, then linked."""
 from __future__ import annotations
 
 import os
@@ -18,18 +20,31 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
 
 
 def sources():
-    return [os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "device.hip")]
+    return [os.path.join(CSRC, f) for f in ("host.cpp", "device.hip", "flow.hip")]
 
 
 def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    objs, procs = [], []
+    for src in sources():
+        obj = out + "." + os.path.splitext(os.path.basename(src))[0] + ".o"
+        cmd = [hipcc, *HIP_FLAGS, *inc, "-c", src, "-o", obj, *extra]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((subprocess.Popen(cmd), cmd))
+        objs.append(obj)
+    failed = [cmd for p, cmd in procs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = out + ".tmp"
-    cmd = [hipcc, *HIP_FLAGS, "-shared", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           *sources(), "-o", tmp, *extra]
+    cmd = [hipcc, *HIP_FLAGS, "-shared", *objs, "-o", tmp, *extra]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
+    for obj in objs:
+        os.remove(obj)
     return out
 
 

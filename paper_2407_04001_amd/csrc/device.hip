@@ -22,74 +22,13 @@
 #include <chrono>
 #include <type_traits>
 #include <cstring>
+#include <numeric>
 #include <vector>
 
 #include "internal.h"
+#include "kernels.h"
 
 using namespace pase;
-
-// ------------------------------------------------------------------ key arithmetic
-template <typename KeyT> struct KeyOps;
-
-template <> struct KeyOps<double> {
-    using Val = double;   // table value type
-    static constexpr double sentinel() { return 1152921504606846976.0; }  // 2^60 > any key
-    __device__ static double from_u64(uint64_t x) { return (double)x; }
-    __device__ static uint64_t val_to_u64(double x) { return (uint64_t)x; }
-    __device__ static double add(double a, double b) { return a + b; }
-    __device__ static double min(double a, double b) { return __builtin_fmin(a, b); }
-    // key = cost * 2^bits + c  ->  (cost * 2^out_shift, c)
-    __device__ static void split(double key, uint32_t bits, uint32_t out_shift, double &val, uint32_t &c) {
-        double s = __builtin_ldexp(1.0, (int)bits);
-        double v = __builtin_trunc(key * __builtin_ldexp(1.0, -(int)bits));
-        val = v * __builtin_ldexp(1.0, (int)out_shift);
-        c = (uint32_t)__builtin_fma(-v, s, key);
-    }
-};
-
-template <> struct KeyOps<uint64_t> {
-    using Val = uint64_t;
-    static constexpr uint64_t sentinel() { return ~0ull; }
-    __device__ static uint64_t from_u64(uint64_t x) { return x; }
-    __device__ static uint64_t val_to_u64(uint64_t x) { return x; }
-    __device__ static uint64_t add(uint64_t a, uint64_t b) { return a + b; }
-    __device__ static uint64_t min(uint64_t a, uint64_t b) { return a < b ? a : b; }
-    __device__ static void split(uint64_t key, uint32_t bits, uint32_t out_shift, uint64_t &val, uint32_t &c) {
-        val = (key >> bits) << out_shift;
-        c = (uint32_t)(key & ((1ull << bits) - 1));
-    }
-};
-
-
-// Buffer resource word 3 (data format 32-bit, raw addressing) for gfx9-family
-// buffer instructions.
-constexpr int kBufferWord3 = 0x00020000;
-
-// ------------------------------------------------------------------ cost model (device)
-// Layer cost t_l(v, c) = ceil(F / P) + r * (2^e_red - 1) * ceil(keep / 2^(E - e_red)),
-// with P = 2^E the device count of the configuration and e_red the exponent
-// sum over contracted dims.  Power-of-two divisions are shifts; the host has
-// bounded every operand so nothing overflows.
-__device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
-    uint32_t E = 0, ered = 0;
-    for (uint32_t k = 0; k < dv.ndims; k++) {
-        E += ex[k];
-        if ((dv.reduce_mask >> k) & 1u) ered += ex[k];
-    }
-    uint64_t compute = (dv.flops + ((1ull << E) - 1)) >> E;
-    uint32_t ek = E - ered;
-    uint64_t part = (dv.keep_n + ((1ull << ek) - 1)) >> ek;
-    return compute + r * (((1ull << ered) - 1) * part);
-}
-
-// Split signature of one endpoint configuration of an edge: the split
-// exponent of every tensor dim (0 for an unsplit dim), 5 bits each.  Two
-// endpoints redistribute nothing exactly when their signatures are equal.
-__device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t rank, const uint8_t *ex) {
-    uint64_t sig = 0;
-    for (uint32_t k = 0; k < rank; k++) sig |= (uint64_t)(dims[k] >= 0 ? ex[dims[k]] : 0) << (5 * k);
-    return sig;
-}
 
 // Cost tables of the search: layer cost and device count exponent of every
 // (vertex, configuration), and the split signatures of every (edge endpoint,
@@ -134,13 +73,6 @@ __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, cons
     }
 }
 
-__device__ __forceinline__ uint64_t edge_cost_sig(uint64_t sig_a, uint64_t sig_b, uint32_t la, uint32_t lb,
-                                                  uint64_t elems, uint64_t r) {
-    if (sig_a == sig_b) return 0;
-    uint32_t s = la > lb ? la : lb;
-    return r * ((elems + ((1ull << s) - 1)) >> s);
-}
-
 __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t e,
                              const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
                              uint64_t *__restrict__ out, uint64_t r) {
@@ -155,22 +87,6 @@ __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__r
     }
 }
 
-// ------------------------------------------------------------------ prep: key-space blocks
-// Batched launches: the workgroups of one launch are the concatenation of the
-// workgroups of its vertices; find the vertex of this workgroup (uniform).
-__device__ __forceinline__ uint32_t batch_find(const BatchEntry *__restrict__ be, uint32_t nbe, uint32_t wg) {
-    uint32_t lo = 0, hi = nbe;
-    while (hi - lo > 1) {
-        uint32_t mid = (lo + hi) >> 1;
-        if (be[mid].first <= wg) lo = mid; else hi = mid;
-    }
-    return __builtin_amdgcn_readfirstlane(lo);
-}
-
-// One workgroup handles kPrepThreads consecutive (c, column) elements of one
-// outer index of one block, so the block, its contributions and the outer
-// digits are uniform across the workgroup (scalar loads); lanes differ only in
-// (c, column).
 template <typename KeyT>
 __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restrict__ descs,
                                                      const BatchEntry *__restrict__ be, uint32_t nbe,
@@ -180,388 +96,30 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restric
                                                      const uint8_t *__restrict__ lsum,
                                                      const uint64_t *__restrict__ sig,
                                                      const Contrib *__restrict__ cb, uint64_t r) {
-    using Val = typename KeyOps<KeyT>::Val;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
-    const PrepArgs &a = descs[be[kb].pos];
-    KeyT *__restrict__ blocks = (KeyT *)a.blocks;
-    const uint32_t wg = blockIdx.x - be[kb].first;
-    uint32_t b = 0;
-    while (b + 1 < a.nblocks && wg >= a.blk[b + 1].wg_begin) b++;
-    b = __builtin_amdgcn_readfirstlane(b);
-    const Block &bk = a.blk[b];
-    const uint32_t rel = wg - bk.wg_begin;
-    const uint32_t row = rel / bk.chunks, chunk = rel % bk.chunks;
-    const uint32_t per_row = a.K * bk.ld;
-    const uint32_t e = chunk * kPrepThreads + threadIdx.x;
-    if (e >= per_row) return;
-    const uint32_t c = e / bk.ld, q = e % bk.ld;
-    KeyT *out = blocks + bk.out_off + (uint64_t)row * per_row + e;
-    if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; return; }
-    uint32_t dv[kMaxDep];
-    for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
-    uint32_t x = row;
-    for (int k = (int)bk.npre - 1; k >= 0; k--) {
-        dv[bk.pre[k]] = x % bk.prerad[k];
-        x /= bk.prerad[k];
-    }
-    if (bk.post >= 0) dv[bk.post] = q;
-    const DevVertex me = V[a.vi];
-    // plain costs (layer, transfer) are summed in `sum` and shifted into key
-    // space at the end; DP tables are stored in this vertex's key space already
-    uint64_t sum = 0, keysum = 0, low = 0;
-    for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
-        const Contrib ct = cb[k];
-        if (ct.kind == kContribLayer) {
-            sum += L[me.L_off + c];
-            low = c;
-        } else if (ct.kind == kContribEdge) {
-            const DevEdge de = E[ct.edge];
-            const uint32_t xo = dv[ct.dig];
-            const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
-            const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
-            const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
-            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r);
-        } else {
-            uint64_t idx = (uint64_t)c * ct.sc;
-            for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
-            if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
-            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
-        }
-    }
-    *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
+    prep_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r);
 }
-
-// Waits for every outstanding scalar-memory and LDS read (s_waitcnt
-// lgkmcnt(0), other counters left alone).  Scalar loads return out of order,
-// so a wait for one of them is always a wait for all of them: the pipelined
-// loops wait for the operands of c *before* they request those of c + 1,
-// otherwise the wait the compiler places before the first use of c's
-// operands would also wait for the prefetch.
-__device__ __forceinline__ void wait_lgkm_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }
-
-// ------------------------------------------------------------------ fill: row kernel
-// Output T_i is laid out [z][o][r]: column digit z slowest, then the outer
-// digits o (those sharing a lookup with z), then the row digits r.  A tile is
-// TM x 64 consecutive rows of one (o, column chunk, c range); lane l holds
-// rows l, l + 64, ...  For each c every row forms its operand a = sum of its
-// row terms, and the wave reads the TZ column operands B[o][c][z0..z0+TZ)
-// through the scalar unit (they are wave-uniform), so each cell is one add
-// (SGPR operand) and one min; one scalar round trip per c feeds TM x 64 x TZ
-// cells.  The four waves of a workgroup take the same tile and a quarter of
-// its c range each, and combine their minima through LDS at the end: a wave
-// then does a quarter of a tile's work, so a launch has four times as many,
-// shorter, work items and its last partial round of waves costs little.
-constexpr int kMergeVals = 16;   // values per lane moved through LDS per merge pass
 
 template <typename KeyT, int TZ, int TM, int NA>
 __global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ descs,
                                                   const BatchEntry *__restrict__ be, uint32_t nbe) {
-    using Ops = KeyOps<KeyT>;
-    using Val = typename Ops::Val;
-    __shared__ KeyT xch[2][kMergeVals][64];
+    __shared__ MergeBuf<KeyT> xch;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
-    const RowsArgs &a = descs[be[kb].pos];
-    const uint32_t lane = threadIdx.x & 63;
-    // the wave index is uniform across the wave: say so, so that everything
-    // derived from it (c range, column addresses) lives in SGPRs
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    // blocks are dealt round-robin to the 8 XCDs: give every XCD a contiguous
-    // range of tiles so that tiles sharing a column slice share an L2 (every
-    // vertex's block count and first block are multiples of 8, so the XCD of
-    // a block is its local index mod 8)
-    const uint32_t nb = a.nblocks_launched, b = blockIdx.x - be[kb].first;
-    const uint64_t wg = (uint64_t)(b % 8) * (nb / 8) + b / 8;
-    // a workgroup takes 4 / P tiles, P = a.parts waves per tile, each wave a
-    // P-th of the tile's c range
-    const uint32_t P = a.parts, tpw = 4 / P;
-    if (wg * tpw >= a.total_tiles) return;   // the whole workgroup leaves together
-    const uint32_t part = wave % P, tin = wave / P;
-    const bool has_tile = wg * tpw + tin < a.total_tiles;
-    // (a wave without a tile computes nothing but still takes part in the merge)
-    const uint64_t tile = min(wg * tpw + tin, a.total_tiles - 1);
-    // tile order (fastest first): row tile, column chunk, outer index, c split --
-    // all chunks of one outer index run close together and share its slices
-    const uint32_t rowtile = (uint32_t)(tile % a.tiles_per_o);
-    uint64_t t2 = tile / a.tiles_per_o;
-    const uint32_t chunk = (uint32_t)(t2 % a.nchunks);
-    t2 /= a.nchunks;
-    const uint32_t o = (uint32_t)(t2 % a.MO);
-    const uint32_t split = (uint32_t)(t2 / a.MO);
-
-    constexpr int NT = NA < 0 ? kMaxATerms : NA;
-    constexpr int NTA = NT > 0 ? NT : 1;
-    const int na = NA < 0 ? (int)a.na : NA;
-    uint32_t dO[kMaxDep];
-    {
-        uint32_t x = o;
-        for (int k = kMaxDep - 1; k >= 0; k--)
-            if (k < (int)a.nO) { dO[k] = x % a.radO[k]; x /= a.radO[k]; } else dO[k] = 0;
-    }
-    // row terms are read with buffer loads: per-lane byte offset in a VGPR,
-    // the c-dependent part as a scalar offset, no per-c address arithmetic
-    __amdgpu_buffer_rsrc_t rsrc[NTA];
-    uint32_t tsc[NTA];
-#pragma unroll
-    for (int t = 0; t < NTA; t++) {
-        rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(t < na ? const_cast<void *>(a.a[t].ptr) : nullptr, (short)0,
-                                                    t < na ? (int)a.a[t].bytes : 0, kBufferWord3);
-        tsc[t] = t < na ? a.a[t].sc * (uint32_t)sizeof(Val) : 0;
-    }
-    uint32_t r[TM], offb[TM][NTA];
-    bool valid[TM];
-#pragma unroll
-    for (int m = 0; m < TM; m++) {
-        r[m] = (rowtile * TM + m) * 64 + lane;
-        valid[m] = r[m] < a.MR;
-        uint32_t x = valid[m] ? r[m] : a.MR - 1, dR[kMaxDep];
-        for (int k = kMaxDep - 1; k >= 0; k--)
-            if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
-#pragma unroll
-        for (int t = 0; t < NTA; t++) {
-            uint32_t off = 0;
-            if (t < na)
-                for (int k = 0; k < kMaxDep; k++) off += dO[k] * a.a[t].sdO[k] + dR[k] * a.a[t].sdR[k];
-            offb[m][t] = off * (uint32_t)sizeof(Val);
-        }
-    }
-    // this wave's part [c0, c1) of the tile's c range (possibly empty)
-    const uint32_t cs = split * a.cper, ce_ = has_tile ? min(a.K, cs + a.cper) : cs;
-    const uint32_t q = (ce_ - cs + P - 1) / P;
-    const uint32_t c0 = min(ce_, cs + part * q), c1 = min(ce_, c0 + q);
-    const uint32_t ldz = a.ldz;
-    const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * ldz + (uint64_t)chunk * TZ;
-
-    KeyT acc[TM][TZ];
-#pragma unroll
-    for (int m = 0; m < TM; m++)
-#pragma unroll
-        for (int t = 0; t < TZ; t++) acc[m][t] = Ops::sentinel();
-
-    // Software pipeline over two register sets of U values of c each: the
-    // row terms and column chunks of the next U values are requested while
-    // the cells of the current ones are computed from the other set, so load
-    // latency overlaps VALU work.  Narrow tiles have little work per c and
-    // keep U = 4 values in flight per set.  Loads past c1 repeat column
-    // c1 - 1 (in bounds, unused) so that every load is unconditional and the
-    // register sets never need copying.
-    constexpr int U = TZ <= 2 ? 4 : 1;
-    using SKey = const __attribute__((address_space(4))) KeyT;
-    uint64_t xe[U][TM][NTA], xo[U][TM][NTA];
-    KeyT ce[U][TZ], co[U][TZ];
-    auto load = [&](uint64_t (&xs)[U][TM][NTA], KeyT (&bs)[U][TZ], uint32_t cc) {
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            const uint32_t cu = min(cc + u, c1 - 1);
-#pragma unroll
-            for (int m = 0; m < TM; m++)
-#pragma unroll
-                for (int t = 0; t < NTA; t++)
-                    if (t < na)
-                        xs[u][m][t] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(
-                                                                       rsrc[t], (int)offb[m][t], (int)(cu * tsc[t]), 0));
-            SKey *brow = (SKey *)(uintptr_t)(B + (uint64_t)cu * ldz);
-#pragma unroll
-            for (int t = 0; t < TZ; t++) bs[u][t] = brow[t];
-        }
-    };
-    auto cells = [&](const uint64_t (&xs)[U][TM][NTA], const KeyT (&bs)[U][TZ], uint32_t n) {
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            if (u > 0 && (uint32_t)u >= n) break;
-            KeyT av[TM];
-#pragma unroll
-            for (int m = 0; m < TM; m++) {
-                av[m] = (KeyT)0;
-#pragma unroll
-                for (int t = 0; t < NTA; t++)
-                    if (t < na) {
-                        const KeyT v = __builtin_bit_cast(KeyT, xs[u][m][t]);
-                        av[m] = t == 0 ? v : Ops::add(av[m], v);
-                    }
-            }
-#pragma unroll
-            for (int t = 0; t < TZ; t++)
-#pragma unroll
-                for (int m = 0; m < TM; m++) acc[m][t] = Ops::min(acc[m][t], Ops::add(av[m], bs[u][t]));
-        }
-    };
-    if (c0 < c1) {
-        load(xe, ce, c0);
-        uint32_t c = c0;
-        for (; c + U < c1; c += 2 * U) {
-            // up to 16 columns both sets fit in SGPRs at once: the barriers
-            // keep the scheduler from sinking the loads of the next set below
-            // the cells of the current one, and the explicit wait for the
-            // current operands comes before those loads are issued
-            if constexpr (TZ <= 16) {
-                wait_lgkm_all();
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            load(xo, co, c + U);
-            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
-            cells(xe, ce, U);
-            if constexpr (TZ <= 16) {
-                wait_lgkm_all();
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            load(xe, ce, c + 2 * U);
-            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
-            cells(xo, co, min((uint32_t)U, c1 - (c + U)));
-        }
-        if (c < c1) cells(xe, ce, min((uint32_t)U, c1 - c));
-    }
-
-    // combine the parts of a tile through LDS, halving the number of holders
-    // per stage (P = 4: parts 2, 3 -> 0, 1, then 1 -> 0; P = 2: 1 -> 0),
-    // kMergeVals values per lane and pass; P is uniform across the workgroup,
-    // so every wave meets the same barriers
-    constexpr int V = TM * TZ;
-    for (uint32_t d = P / 2; d >= 1; d /= 2) {
-#pragma unroll
-        for (int p0 = 0; p0 < V; p0 += kMergeVals) {
-            constexpr int W = kMergeVals;
-            __syncthreads();
-            if (part >= d && part < 2 * d) {
-                const uint32_t slot = tin * d + (part - d);
-#pragma unroll
-                for (int j = 0; j < W; j++)
-                    if (p0 + j < V) xch[slot][j][lane] = acc[(p0 + j) / TZ][(p0 + j) % TZ];
-            }
-            __syncthreads();
-            if (part < d) {
-                const uint32_t slot = tin * d + part;
-#pragma unroll
-                for (int j = 0; j < W; j++)
-                    if (p0 + j < V) {
-                        KeyT &x = acc[(p0 + j) / TZ][(p0 + j) % TZ];
-                        x = Ops::min(x, xch[slot][j][lane]);
-                    }
-            }
-        }
-    }
-    if (part != 0 || !has_tile) return;
-
-    const uint64_t plane = (uint64_t)a.MO * a.MR;
-    const uint32_t zbase = chunk * TZ;
-#pragma unroll
-    for (int m = 0; m < TM; m++) {
-        if (!valid[m]) continue;
-        const uint64_t base_idx = (uint64_t)o * a.MR + r[m];
-#pragma unroll
-        for (int t = 0; t < TZ; t++) {
-            const uint32_t z = zbase + t;
-            if (z < a.Kz) {
-                const uint64_t idx = (uint64_t)z * plane + base_idx;
-                if (a.nsplit > 1) {
-                    ((KeyT *)a.partial)[(uint64_t)split * a.N + idx] = acc[m][t];
-                } else {
-                    Val v;
-                    uint32_t cc;
-                    Ops::split(acc[m][t], a.bits, a.out_shift, v, cc);
-                    ((Val *)a.T)[idx] = v;
-                    a.A[idx] = (uint16_t)cc;
-                }
-            }
-        }
-    }
+    rows_item<KeyT, TZ, TM, NA>(descs[be[kb].pos], blockIdx.x - be[kb].first, xch);
 }
 
 template <typename KeyT>
 __global__ __launch_bounds__(256) void k_reduce_splits(const ReduceArgs *__restrict__ descs,
                                                       const BatchEntry *__restrict__ be, uint32_t nbe) {
-    using Ops = KeyOps<KeyT>;
-    using Val = typename Ops::Val;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
-    const ReduceArgs &a = descs[be[kb].pos];
-    const uint32_t lb = blockIdx.x - be[kb].first;
-    for (uint64_t t = lb * (uint64_t)blockDim.x + threadIdx.x; t < a.N; t += (uint64_t)a.nblk * blockDim.x) {
-        KeyT best = ((const KeyT *)a.partial)[t];
-        for (uint32_t s = 1; s < a.nsplit; s++) best = Ops::min(best, ((const KeyT *)a.partial)[s * a.N + t]);
-        Val v;
-        uint32_t cc;
-        Ops::split(best, a.bits, a.out_shift, v, cc);
-        ((Val *)a.T)[t] = v;
-        a.A[t] = (uint16_t)cc;
-    }
-}
-
-// ------------------------------------------------------------------ fill: generic kernel
-// Any |D(i)| <= PASE_MAX_DEP and any term shapes.  A group of 2^group_log2
-// lanes owns one entry phi: lane l evaluates c = l, l + G, ... (key = sum of
-// the terms), the group then takes the minimum key with cross-lane swaps.
-// Keys are distinct for distinct c, so the minimum -- and with it the lowest
-// optimal c -- does not depend on the evaluation order.
-template <typename KeyT>
-__device__ __forceinline__ KeyT shfl_xor_key(KeyT v, int mask) {
-    uint64_t u = __builtin_bit_cast(uint64_t, v);
-    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)u, mask, 64);
-    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), mask, 64);
-    return __builtin_bit_cast(KeyT, ((uint64_t)hi << 32) | lo);
+    reduce_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first);
 }
 
 template <typename KeyT, int NT>
 __global__ __launch_bounds__(256) void k_fill_generic(const GenericArgs *__restrict__ descs,
                                                      const BatchEntry *__restrict__ be, uint32_t nbe) {
-    using Ops = KeyOps<KeyT>;
-    using Val = typename Ops::Val;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
-    const GenericArgs &a = descs[be[kb].pos];
-    const uint32_t lb = blockIdx.x - be[kb].first;
-    const uint32_t G = 1u << a.group_log2;
-    const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
-    constexpr int MT = NT < 0 ? kMaxGTerms : NT;
-    const int nt = NT < 0 ? (int)a.nt : NT;
-    for (uint64_t tid = lb * (uint64_t)blockDim.x + threadIdx.x; tid < ((nthreads + 255) / 256) * 256;
-         tid += (uint64_t)a.nblk * blockDim.x) {
-        const bool live = tid < nthreads;
-        const uint64_t phi = live ? tid >> a.group_log2 : a.N - 1;
-        const uint32_t lane = (uint32_t)(tid & (G - 1));
-        uint32_t d[kMaxDep];
-        uint64_t x = phi;
-        for (int k = kMaxDep - 1; k >= 0; k--)
-            if (k < (int)a.m) { d[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else d[k] = 0;
-        const KeyT *base[MT];
-        uint32_t sc[MT];
-#pragma unroll
-        for (int t = 0; t < MT; t++) {
-            uint64_t o = 0;
-            if (t < nt)
-                for (int k = 0; k < kMaxDep; k++) o += (uint64_t)d[k] * a.t[t].sd[k];
-            base[t] = (const KeyT *)a.t[t < nt ? t : 0].ptr + (t < nt ? o : 0);
-            sc[t] = t < nt ? a.t[t].sc : 0;
-        }
-        KeyT best0 = Ops::sentinel(), best1 = Ops::sentinel();
-        uint32_t c = lane;
-        // two independent chains keep two loads of every term in flight
-        for (; c + G < a.K; c += 2 * G) {
-            KeyT k0 = base[0][(uint64_t)c * sc[0]];
-            KeyT k1 = base[0][(uint64_t)(c + G) * sc[0]];
-#pragma unroll
-            for (int t = 1; t < MT; t++)
-                if (t < nt) {
-                    k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
-                    k1 = Ops::add(k1, base[t][(uint64_t)(c + G) * sc[t]]);
-                }
-            best0 = Ops::min(best0, k0);
-            best1 = Ops::min(best1, k1);
-        }
-        if (c < a.K) {
-            KeyT k0 = base[0][(uint64_t)c * sc[0]];
-#pragma unroll
-            for (int t = 1; t < MT; t++)
-                if (t < nt) k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
-            best0 = Ops::min(best0, k0);
-        }
-        KeyT best = Ops::min(best0, best1);
-        for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
-        if (live && lane == 0) {
-            Val v;
-            uint32_t cc;
-            Ops::split(best, a.bits, a.out_shift, v, cc);
-            ((Val *)a.T)[phi] = v;
-            a.A[phi] = (uint16_t)cc;
-        }
-    }
+    generic_item<KeyT, NT>(descs[be[kb].pos], blockIdx.x - be[kb].first);
 }
 
 // ------------------------------------------------------------------ back-substitution
@@ -570,17 +128,20 @@ __global__ __launch_bounds__(256) void k_fill_generic(const GenericArgs *__restr
 // sequence).  Single thread; n dependent reads.
 template <typename KeyT>
 __global__ void k_backtrack(const BacktrackDesc *__restrict__ bt, uint32_t n, const void *Tlast,
-                            uint32_t *__restrict__ cfg, SearchOut *out) {
+                            uint32_t *__restrict__ cfg, SearchOut *out, const uint32_t *flow_error) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     uint32_t status = 0;
     for (int i = (int)n - 1; i >= 0; i--) {
         const BacktrackDesc d = bt[i];
         uint64_t idx = 0;
         for (uint32_t k = 0; k < d.m; k++) idx += (uint64_t)cfg[d.dig[k]] * d.stride[k];
-        cfg[d.vi] = d.A[idx];
+        uint32_t c = d.A[idx];
+        // every index above is in range as long as each stored argmin is
+        if (c >= d.K) { status |= 4u; c = 0; }
+        cfg[d.vi] = c;
     }
     out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
-    out->status = status;
+    out->status = status | (flow_error ? *flow_error : 0u);
 }
 
 // Back-substitution by backward levels: one thread per position; the
@@ -592,24 +153,31 @@ __global__ __launch_bounds__(kMaxBacktrackThreads) void k_backtrack_levels(const
                                                                           uint32_t n, uint32_t nlev,
                                                                           const void *Tlast,
                                                                           uint32_t *__restrict__ cfg,
-                                                                          SearchOut *out) {
+                                                                          SearchOut *out,
+                                                                          const uint32_t *flow_error) {
     __shared__ uint32_t scfg[kMaxBacktrackThreads];
+    __shared__ uint32_t sbad;
     const uint32_t t = threadIdx.x;
     const bool mine = t < n;
+    if (t == 0) sbad = 0;
     BacktrackDesc d;
     if (mine) d = bt[t];
+    __syncthreads();
     for (uint32_t lev = 0; lev < nlev; lev++) {
         if (mine && d.level == lev) {
             uint64_t idx = 0;
             for (uint32_t k = 0; k < d.m; k++) idx += (uint64_t)scfg[d.dig[k]] * d.stride[k];
-            scfg[d.vi] = d.A[idx];
+            uint32_t c = d.A[idx];
+            // every index above is in range as long as each stored argmin is
+            if (c >= d.K) { atomicOr(&sbad, 4u); c = 0; }
+            scfg[d.vi] = c;
         }
         __syncthreads();
     }
     if (mine) cfg[t] = scfg[t];
     if (t == 0) {
         out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
-        out->status = 0;
+        out->status = sbad | (flow_error ? *flow_error : 0u);
     }
 }
 
@@ -665,6 +233,8 @@ __global__ void k_fingerprint(FingerArgs a) {
 // ------------------------------------------------------------------ runtime
 namespace pase {
 
+constexpr int kLanes = 3;   // streams of the lane schedule
+
 struct DeviceState {
     void *ws = nullptr;
     uint64_t ws_bytes = 0;
@@ -675,6 +245,10 @@ struct DeviceState {
     uint64_t pinned_bytes = 0;
     std::vector<hipEvent_t> ev;        // profiling: two per fill launch (timed)
     hipStream_t last_stream = nullptr;
+    int flow_grid[2] = {0, 0};         // resident workgroups of the dataflow kernel, per key type
+    int wall_khz = 0;                  // device wall clock (wall_clock64) rate
+    hipStream_t side[kLanes - 1] = {}; // lane schedule: the streams of lanes 1.. (default priority)
+    std::vector<hipEvent_t> lane_ev;   // lane schedule: joins (no timing)
 };
 
 #define HIPCHK(x)                                                                              \
@@ -690,6 +264,9 @@ void device_release(pase_graph_t g) {
     if (d->owned && d->ws) (void)hipFree(d->ws);
     if (d->pinned) (void)hipHostFree(d->pinned);
     for (auto e : d->ev) (void)hipEventDestroy(e);
+    for (auto e : d->lane_ev) (void)hipEventDestroy(e);
+    for (auto st : d->side)
+        if (st) (void)hipStreamDestroy(st);
     delete d;
     g->dev = nullptr;
 }
@@ -1014,10 +591,224 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
     return PASE_OK;
 }
 
+// ------------------------------------------------------------------ dataflow segments
+// Vertices whose planned fill takes at least this long (us, whole GPU) go to
+// the bulk queue; the rest -- the long chains of small dependent vertices --
+// to the latency queue.
+constexpr double kBulkUs = 25.0;
+
+struct FlowPlan {
+    std::vector<Seg> seg[2];
+    std::vector<SegDep> deps;
+    uint32_t nitems[2] = {0, 0};
+};
+
+// Segments (prep, fill, split reduction of every position) in one global
+// order: by the start time of their vertex in a simulation of the schedule
+// (latency vertices start when their producers end; bulk vertices also wait
+// for the previous bulk vertex), then position, then phase.  Every vertex
+// starts strictly after its producers end, so the order is topological.
+template <typename KeyT>
+static pase_status build_flow(pase_graph_t g, const std::vector<Launch<KeyT>> &launches, FlowPlan &fp) {
+    const Plan &P = g->plan;
+    const int n = (int)P.v.size();
+    std::vector<uint32_t> np(n), nf(n), nr(n);
+    std::vector<char> bulk(n);
+    for (int i = 0; i < n; i++) {
+        const Launch<KeyT> &L = launches[i];
+        np[i] = L.prep.nwg;
+        nf[i] = L.rows ? L.ra.nblocks_launched : L.ga.nblk;
+        nr[i] = (L.rows && P.v[i].nsplit > 1) ? L.red.nblk : 0;
+        bulk[i] = P.v[i].est_us >= kBulkUs;
+        if (np[i] == 0 || nf[i] == 0) return fail(g, PASE_ERR_INTERNAL, "empty segment");
+    }
+    const double delta = 2.0;
+    std::vector<int> order(n);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return P.v[a].level < P.v[b].level; });
+    std::vector<double> esi(n, 0.0), efi(n, 0.0);
+    for (int i : order) {
+        for (const auto &t : P.v[i].terms) esi[i] = std::max(esi[i], efi[t.j]);
+        efi[i] = esi[i] + P.v[i].est_us + delta;
+    }
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return esi[a] < esi[b]; });
+    std::vector<double> start(n, 0.0), fin(n, 0.0);
+    double bulk_free = 0;
+    for (int i : order) {
+        double r = 0;
+        for (const auto &t : P.v[i].terms) r = std::max(r, fin[t.j]);
+        start[i] = bulk[i] ? std::max(r, bulk_free) : r;
+        fin[i] = start[i] + P.v[i].est_us + delta;
+        if (bulk[i]) bulk_free = start[i] + P.v[i].est_us;
+    }
+    struct Item { double key; int pos, phase; };
+    std::vector<Item> items;
+    for (int i = 0; i < n; i++) {
+        items.push_back({start[i], i, 0});
+        items.push_back({start[i], i, 1});
+        if (nr[i]) items.push_back({start[i], i, 2});
+    }
+    std::sort(items.begin(), items.end(), [](const Item &a, const Item &b) {
+        if (a.key != b.key) return a.key < b.key;
+        if (a.pos != b.pos) return a.pos < b.pos;
+        return a.phase < b.phase;
+    });
+    // check the order before anything runs: a vertex's segments come after
+    // all segments of every producer it reads, and in phase order
+    std::vector<int> last_idx(n, -1), first_idx(n, -1);
+    for (size_t k = 0; k < items.size(); k++) {
+        const int i = items[k].pos;
+        if (first_idx[i] < 0) first_idx[i] = (int)k;
+        if (last_idx[i] >= 0 && items[last_idx[i]].phase >= items[k].phase)
+            return fail(g, PASE_ERR_INTERNAL, "dataflow order: phases out of order");
+        last_idx[i] = (int)k;
+    }
+    for (int i = 0; i < n; i++)
+        for (const auto &t : P.v[i].terms)
+            if (last_idx[t.j] >= first_idx[i]) return fail(g, PASE_ERR_INTERNAL, "dataflow order not topological");
+    fp = FlowPlan();
+    for (const Item &it : items) {
+        const int i = it.pos;
+        const int q = bulk[i] ? kBulkQ : kLatQ;
+        Seg sg;
+        std::memset(&sg, 0, sizeof sg);
+        sg.first = fp.nitems[q];
+        sg.pos = (uint32_t)i;
+        sg.dep_begin = (uint32_t)fp.deps.size();
+        if (it.phase == 0) {
+            sg.kind = kSegPrep;
+            sg.count = np[i];
+            for (const auto &t : P.v[i].terms) fp.deps.push_back({(uint32_t)t.j, np[t.j] + nf[t.j] + nr[t.j]});
+        } else if (it.phase == 1) {
+            const Launch<KeyT> &L = launches[i];
+            if (L.rows) {
+                sg.kind = kSegRows;
+                const uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
+                sg.variant = (P.v[i].TZ * 4 + P.v[i].TM) * 8 + na;
+            } else {
+                sg.kind = kSegGeneric;
+                sg.variant = L.ga.nt <= 6 ? L.ga.nt : 0;
+            }
+            sg.count = nf[i];
+            fp.deps.push_back({(uint32_t)i, np[i]});
+        } else {
+            sg.kind = kSegReduce;
+            sg.count = nr[i];
+            fp.deps.push_back({(uint32_t)i, np[i] + nf[i]});
+        }
+        sg.dep_end = (uint32_t)fp.deps.size();
+        if ((uint64_t)fp.nitems[q] + sg.count > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "dataflow items");
+        fp.nitems[q] += sg.count;
+        fp.seg[q].push_back(sg);
+    }
+    return PASE_OK;
+}
+
+// Randomized simulation of the k_flow worker protocol on the host: `workers`
+// workgroups, the first `lat_workers` of them latency workers, take tickets
+// exactly as the kernel does, wait until the dependencies of their item are
+// met, run it for a random time and count it as done.  Fails if the workers
+// can no longer make progress (deadlock), if an item would start before its
+// dependencies are met, or if a counter does not end at its vertex's item
+// count.
+static pase_status flow_simulate(pase_graph_t g, const FlowPlan &fp, uint32_t workers, uint32_t lat_workers,
+                                 uint64_t seed) {
+    const int n = (int)g->plan.v.size();
+    std::vector<uint32_t> done(n, 0), total(n, 0);
+    for (int q = 0; q < 2; q++)
+        for (const Seg &sg : fp.seg[q]) total[sg.pos] += sg.count;
+    auto seg_of = [&](int q, uint32_t t) -> const Seg & {
+        size_t lo = 0, hi = fp.seg[q].size();
+        while (hi - lo > 1) {
+            const size_t mid = (lo + hi) / 2;
+            if (fp.seg[q][mid].first <= t) lo = mid; else hi = mid;
+        }
+        return fp.seg[q][lo];
+    };
+    auto met = [&](const Seg &sg) {
+        for (uint32_t k = sg.dep_begin; k < sg.dep_end; k++)
+            if (done[fp.deps[k].counter] < fp.deps[k].target) return false;
+        return true;
+    };
+    for (const SegDep &d : fp.deps)
+        if (d.counter >= (uint32_t)n || d.target > total[d.counter])
+            return fail(g, PASE_ERR_INTERNAL, "dataflow dependency can never be met");
+    enum { kIdle, kWaiting, kRunning, kExited };
+    struct W { bool lat; int state; int q; uint32_t t; double until; };
+    std::vector<W> w(workers);
+    for (uint32_t k = 0; k < workers; k++) w[k] = {k < lat_workers, kIdle, -1, 0, 0.0};
+    uint64_t head[2] = {0, 0};
+    uint64_t rs = seed * 0x9E3779B97F4A7C15ull + 1;
+    auto rnd = [&]() {   // xorshift64*
+        rs ^= rs >> 12; rs ^= rs << 25; rs ^= rs >> 27;
+        return rs * 0x2545F4914F6CDD1Dull;
+    };
+    std::vector<uint32_t> idx(workers);
+    std::iota(idx.begin(), idx.end(), 0u);
+    double now = 0;
+    for (;;) {
+        for (uint32_t k = workers; k > 1; k--) std::swap(idx[k - 1], idx[rnd() % k]);
+        for (uint32_t k : idx) {
+            W &x = w[k];
+            if (x.state != kIdle) continue;
+            int q = -1;
+            uint64_t t = 0;
+            if (x.lat) {
+                t = head[kLatQ]++;
+                if (t < fp.nitems[kLatQ]) q = kLatQ; else x.lat = false;
+            }
+            if (q < 0 && head[kLatQ] < fp.nitems[kLatQ] && met(seg_of(kLatQ, (uint32_t)head[kLatQ]))) {
+                t = head[kLatQ]++;
+                q = kLatQ;
+            }
+            if (q < 0) {
+                t = head[kBulkQ]++;
+                if (t < fp.nitems[kBulkQ]) {
+                    q = kBulkQ;
+                } else {
+                    t = head[kLatQ]++;
+                    if (t < fp.nitems[kLatQ]) q = kLatQ;
+                }
+            }
+            if (q < 0) { x.state = kExited; continue; }
+            x.q = q;
+            x.t = (uint32_t)t;
+            x.state = kWaiting;
+        }
+        bool any_running = false, any_waiting = false;
+        for (W &x : w) {
+            if (x.state == kWaiting && met(seg_of(x.q, x.t))) {
+                x.state = kRunning;
+                x.until = now + 1.0 + (double)(rnd() % 1000) / 100.0;
+            }
+            any_running |= x.state == kRunning;
+            any_waiting |= x.state == kWaiting;
+        }
+        if (!any_running) {
+            if (any_waiting) return fail(g, PASE_ERR_INTERNAL, "dataflow schedule deadlocks");
+            break;
+        }
+        double next = 1e300;
+        for (const W &x : w)
+            if (x.state == kRunning) next = std::min(next, x.until);
+        now = next;
+        for (W &x : w)
+            if (x.state == kRunning && x.until <= now) {
+                done[seg_of(x.q, x.t).pos]++;
+                x.state = kIdle;
+            }
+    }
+    for (int i = 0; i < n; i++)
+        if (done[i] != total[i]) return fail(g, PASE_ERR_INTERNAL, "dataflow items left undone");
+    return PASE_OK;
+}
+
 // A batched launch: vertices (sequence positions) sharing one kernel variant
 // within one launch slot, with their first workgroups.
 struct Batch {
     enum Kind { kPrep, kRows, kGeneric, kReduce } kind;
+    int lane;              // two-lane schedule: the stream it runs on
+    int group;             // launch group (a slot, or a (level, lane) pair) it belongs to
     uint32_t variant;      // rows: (TZ * 4 + TM) * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime)
     uint32_t entry0;       // first BatchEntry of this batch
     uint32_t nentries;
@@ -1092,6 +883,15 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     std::vector<Contrib> contrib;
     pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
     if (st != PASE_OK) return st;
+    // the dataflow launch needs the resident layout and a kernel variant it
+    // carries for every row fill; otherwise the level schedule runs (the
+    // resident layout serves it as well)
+    bool use_flow = P.resident && g->schedule == kSchedFlow;
+    const bool use_lanes = P.resident && g->schedule == kSchedLanes;
+    for (int i = 0; i < n && use_flow; i++)
+        if (launches[i].rows)
+            use_flow = flow_rows_ok(!std::is_same<KeyT, double>::value, P.v[i].TZ, P.v[i].TM,
+                                    std::min<uint32_t>(launches[i].ra.na, std::is_same<KeyT, double>::value ? 4 : 7));
 
     // ---- constant region image (one host-to-device copy)
     char *img = (char *)d->pinned;
@@ -1143,6 +943,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         std::memset(&b, 0, sizeof b);
         b.A = (const uint16_t *)(ws + P.off_A + vp.A_off);
         b.vi = (uint32_t)vp.vi;
+        b.K = vp.K;
         b.m = (uint32_t)vp.layout.size();
         for (size_t k = 0; k < vp.layout.size(); k++) {
             b.dig[k] = (uint32_t)vp.layout[k];
@@ -1169,12 +970,22 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     BatchEntry *hbe = (BatchEntry *)(img + P.off_batch);
     std::vector<Batch> batches;
     uint32_t nbe = 0;
-    std::vector<std::vector<int>> slot_members(P.nslots);
-    for (int i = 0; i < n; i++) slot_members[P.v[i].slot].push_back(i);
+    // launch groups in enqueue order: the slots (levels, or positions); with
+    // lanes, each level's vertices of lane 0, then lane 1, then lane 2
+    std::vector<std::vector<int>> groups;
+    std::vector<int> group_lane;
+    const int nl = use_lanes ? kLanes : 1;
+    if (!use_flow) {
+        groups.assign((size_t)P.nslots * nl, {});
+        group_lane.assign(groups.size(), 0);
+        for (int i = 0; i < n; i++) groups[(size_t)P.v[i].slot * nl + (use_lanes ? P.v[i].lane : 0)].push_back(i);
+        for (size_t k = 0; k < groups.size(); k++) group_lane[k] = (int)(k % nl);
+    }
+    int cur_lane = 0, cur_group = 0;
     auto add_batch = [&](Batch::Kind kind, uint32_t variant, const std::vector<int> &members,
                          uint32_t (*nblk)(const Launch<KeyT> &)) {
         if (members.empty()) return;
-        Batch b{kind, variant, nbe, 0, 0};
+        Batch b{kind, cur_lane, cur_group, variant, nbe, 0, 0};
         for (int i : members) {
             hbe[nbe].pos = (uint32_t)i;
             hbe[nbe].first = b.blocks;
@@ -1184,8 +995,10 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
         batches.push_back(b);
     };
-    for (int sl = 0; sl < P.nslots; sl++) {
-        const auto &mem = slot_members[sl];
+    for (size_t sl = 0; sl < groups.size(); sl++) {
+        const auto &mem = groups[sl];
+        cur_lane = group_lane[sl];
+        cur_group = (int)sl;
         add_batch(Batch::kPrep, 0, mem, [](const Launch<KeyT> &L) { return L.prep.nwg; });
         std::vector<std::pair<uint32_t, int>> rows, gens, reds;
         for (int i : mem) {
@@ -1224,6 +1037,34 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     for (const Batch &b : batches)
         if (b.blocks == 0 || b.blocks > 0x7fffffffu) return fail(g, PASE_ERR_TOO_LARGE, "launch grid size");
 
+    // ---- dataflow tables: control block and done counters (zeroed), then the
+    // segments of both queues and their dependencies
+    FlowPlan fp;
+    FlowArgs fa;
+    std::memset(&fa, 0, sizeof fa);
+    if (use_flow) {
+        st = build_flow<KeyT>(g, launches, fp);
+        if (st != PASE_OK) return st;
+        const uint64_t ctl_bytes = sizeof(FlowCtl) + (4ull * n + 15) / 16 * 16;
+        const uint64_t need = ctl_bytes + (fp.seg[0].size() + fp.seg[1].size()) * sizeof(Seg) +
+                              fp.deps.size() * sizeof(SegDep);
+        if (need > P.flow_bytes) return fail(g, PASE_ERR_INTERNAL, "dataflow table overflow");
+        char *fimg = img + P.off_flow;
+        std::memset(fimg, 0, ctl_bytes);
+        uint64_t o = ctl_bytes;
+        for (int q = 0; q < 2; q++) {
+            if (!fp.seg[q].empty()) std::memcpy(fimg + o, fp.seg[q].data(), fp.seg[q].size() * sizeof(Seg));
+            fa.seg[q] = (const Seg *)(ws + P.off_flow + o);
+            fa.nseg[q] = (uint32_t)fp.seg[q].size();
+            fa.nitems[q] = fp.nitems[q];
+            o += fp.seg[q].size() * sizeof(Seg);
+        }
+        if (!fp.deps.empty()) std::memcpy(fimg + o, fp.deps.data(), fp.deps.size() * sizeof(SegDep));
+        fa.deps = (const SegDep *)(ws + P.off_flow + o);
+        fa.ctl = (FlowCtl *)(ws + P.off_flow);
+        fa.done = (uint32_t *)(ws + P.off_flow + sizeof(FlowCtl));
+    }
+
     HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
 
     const DevVertex *dV = (const DevVertex *)(ws + P.off_vert);
@@ -1241,7 +1082,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
     SearchOut *dout = (SearchOut *)(ws + P.off_out);
 
-    uint32_t nfill = 0;
+    uint32_t nfill = use_flow ? 1 : 0;
     for (const Batch &b : batches) nfill += b.kind == Batch::kRows || b.kind == Batch::kGeneric;
     if (g->profile && d->ev.size() < 2 * (size_t)nfill) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
@@ -1258,11 +1099,94 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     }
     std::vector<int> fill_of(n, -1);   // fill batch of each vertex (profiling)
     uint32_t fb = 0;
+    if (use_flow) {
+        // every resident workgroup is a worker; at least one per queue
+        int &grid = d->flow_grid[std::is_same<KeyT, double>::value ? 0 : 1];
+        if (grid == 0) {
+            int dev = 0, cus = 0, per_cu = 0;
+            HIPCHK(hipGetDevice(&dev));
+            HIPCHK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+            HIPCHK(hipDeviceGetAttribute(&d->wall_khz, hipDeviceAttributeWallClockRate, dev));
+            HIPCHK(flow_occupancy<KeyT>(&per_cu));
+            grid = std::max(2, cus * std::max(1, per_cu));
+        }
+        const uint64_t items = (uint64_t)fp.nitems[0] + fp.nitems[1];
+        const uint32_t G = (uint32_t)std::max<uint64_t>(2, std::min<uint64_t>((uint64_t)grid, items));
+        const uint32_t lw = g->lat_workers ? g->lat_workers : G / 16;
+        fa.lat_workers = std::max(1u, std::min(G - 1, lw));
+        fa.prep = dp;
+        fa.rows = dr;
+        fa.gen = dg;
+        fa.red = dd;
+        fa.V = dV;
+        fa.E = dE;
+        fa.L = dL;
+        fa.lsum = dls;
+        fa.sig = dsig;
+        fa.cb = dC;
+        fa.r = g->r;
+        // a dependency wait gives up after 10 s plus 100x the planned search time
+        double est = 0;
+        for (int i = 0; i < n; i++) est += P.v[i].est_us;
+        const double hz = 1e3 * (d->wall_khz > 0 ? d->wall_khz : 100000);
+        fa.timeout_ticks = (uint64_t)(hz * (10.0 + 100.0 * est * 1e-6));
+        hipEvent_t e0 = g->profile ? d->ev[0] : nullptr, e1 = g->profile ? d->ev[1] : nullptr;
+        HIPCHK(flow_launch<KeyT>(fa, G, s, e0, e1));
+        g->stats.flow_grid = G;
+        g->stats.flow_lat_workers = fa.lat_workers;
+        g->stats.flow_items = items;
+        for (int i = 0; i < n; i++) fill_of[i] = 0;
+        fb = 1;
+        launches_n++;
+    }
+    // lanes: every lane starts after the upload and the cost tables; a group
+    // (level, lane) waits, per other lane, for the latest level of that lane
+    // whose tables it reads (always a lower level: the event is recorded
+    // already); the caller's stream joins every lane at the end
+    hipStream_t lane_stream[kLanes] = {s, s, s};
+    // event of (lane l, level L): lane_ev[1 + L * kLanes + l]; lane_ev[0]: start
+    auto lev = [&](int l, int L) { return d->lane_ev[1 + (size_t)L * kLanes + l]; };
+    std::vector<std::vector<int>> waited(kLanes, std::vector<int>(kLanes, -1));
+    if (use_lanes) {
+        for (int l = 1; l < kLanes; l++) {
+            if (!d->side[l - 1]) HIPCHK(hipStreamCreateWithFlags(&d->side[l - 1], hipStreamNonBlocking));
+            lane_stream[l] = d->side[l - 1];
+        }
+        const size_t nev = 1 + (size_t)(P.nslots + 1) * kLanes;
+        while (d->lane_ev.size() < nev) {
+            hipEvent_t e;
+            HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+            d->lane_ev.push_back(e);
+        }
+        HIPCHK(hipEventRecord(d->lane_ev[0], s));
+        for (int l = 1; l < kLanes; l++) HIPCHK(hipStreamWaitEvent(lane_stream[l], d->lane_ev[0], 0));
+    }
+    int prev_group = -1;
     for (const Batch &b : batches) {
         const BatchEntry *e = dbe + b.entry0;
+        hipStream_t bs = s;
+        if (use_lanes) {
+            if (b.group != prev_group) {
+                if (prev_group >= 0)
+                    HIPCHK(hipEventRecord(lev(group_lane[prev_group], prev_group / nl), lane_stream[group_lane[prev_group]]));
+                std::vector<int> need(kLanes, -1);
+                for (int i : groups[b.group])
+                    for (const auto &t : P.v[i].terms)
+                        if (P.v[t.j].lane != b.lane) need[P.v[t.j].lane] = std::max(need[P.v[t.j].lane], P.v[t.j].slot);
+                for (int l = 0; l < kLanes; l++)
+                    if (need[l] > waited[b.lane][l]) {
+                        if (need[l] >= b.group / nl)   // a table is read at a later level only
+                            return fail(g, PASE_ERR_INTERNAL, "lane wait on a level not enqueued yet");
+                        HIPCHK(hipStreamWaitEvent(lane_stream[b.lane], lev(l, need[l]), 0));
+                        waited[b.lane][l] = need[l];
+                    }
+                prev_group = b.group;
+            }
+            bs = lane_stream[b.lane];
+        }
         switch (b.kind) {
         case Batch::kPrep:
-            hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, s, dp, e, b.nentries, dV, dE,
+            hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, bs, dp, e, b.nentries, dV, dE,
                                (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r);
             break;
         case Batch::kRows:
@@ -1272,45 +1196,64 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             // (events attached to the dispatch, no extra packets in the stream)
             hipEvent_t e0 = g->profile ? d->ev[2 * fb] : nullptr, e1 = g->profile ? d->ev[2 * fb + 1] : nullptr;
             if (b.kind == Batch::kRows) {
-                if (!launch_rows<KeyT>(dr, e, b, s, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+                if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
             } else {
-                launch_generic<KeyT>(dg, e, b, s, e0, e1);
+                launch_generic<KeyT>(dg, e, b, bs, e0, e1);
             }
         }
             for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
             fb++;
             break;
         case Batch::kReduce:
-            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, s, dd, e, b.nentries);
+            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, bs, dd, e, b.nentries);
             break;
         }
         launches_n++;
     }
+    if (use_lanes) {
+        // join: the caller's stream waits for the last work of every other lane
+        for (int l = 1; l < kLanes; l++) {
+            HIPCHK(hipEventRecord(lev(l, P.nslots), lane_stream[l]));
+            HIPCHK(hipStreamWaitEvent(s, lev(l, P.nslots), 0));
+        }
+    }
+    const uint32_t *flow_err = use_flow ? &fa.ctl->error : nullptr;
     if ((uint32_t)n <= kMaxBacktrackThreads)
         hipLaunchKernelGGL((k_backtrack_levels<KeyT>), dim3(1), dim3((n + 63) / 64 * 64), 0, s,
                            (const BacktrackDesc *)(ws + P.off_bt), (uint32_t)n, nlev,
-                           (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+                           (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout, flow_err);
     else
         hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
-                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
+                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout, flow_err);
     launches_n++;
     HIPCHK(hipGetLastError());
-    char *host_out = img;   // reuse the staging buffer after the upload has been consumed
-    HIPCHK(hipStreamSynchronize(s));
+    // the staging buffer is reused for the results: the stream runs the
+    // upload before these copies
+    char *host_out = img;
     HIPCHK(hipMemcpyAsync(host_out, dout, sizeof(SearchOut), hipMemcpyDeviceToHost, s));
     HIPCHK(hipMemcpyAsync(host_out + sizeof(SearchOut), dcfg, nv * 4, hipMemcpyDeviceToHost, s));
     HIPCHK(hipStreamSynchronize(s));
     SearchOut so;
     std::memcpy(&so, host_out, sizeof so);
-    if (so.status) return fail(g, PASE_ERR_INTERNAL, "device consistency check failed");
+    if (so.status & 1u) return fail(g, PASE_ERR_INTERNAL, "a dependency wait of the dataflow launch timed out");
+    if (so.status & 2u) return fail(g, PASE_ERR_INTERNAL, "the dataflow launch met an item it cannot run");
+    if (so.status) return fail(g, PASE_ERR_INTERNAL, "back-substitution read an argmin out of range");
     *min_cost = so.min_cost;
     std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
+    if (!use_flow) g->stats.flow_grid = g->stats.flow_lat_workers = 0, g->stats.flow_items = 0;
+    g->stats.schedule = use_flow ? 3u : use_lanes ? 0u : (P.by_level ? 2u : 1u);
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;
-    if (g->profile) {
+    if (g->profile && use_flow) {
+        float ms = 0.f;
+        HIPCHK(hipEventElapsedTime(&ms, d->ev[0], d->ev[1]));
+        g->stats.fill_ms = g->stats.rows_fill_ms = ms;
+        g->stats.rows_launches = 1;
+        for (int i = 0; i < n; i++) P.v[i].fill_ms = 0.0;
+    } else if (g->profile) {
         std::vector<float> ms(fb, 0.f);
         uint32_t k = 0;
         for (const Batch &b : batches) {
@@ -1453,3 +1396,34 @@ pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
 }
 
 }  // namespace pase
+
+template <typename KeyT>
+static pase_status flow_check_t(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
+                                uint64_t *items) {
+    // descriptors hold device addresses only: any base will do, nothing is read through it
+    char *fake_ws = (char *)(uintptr_t)(1ull << 40);
+    std::vector<Launch<KeyT>> launches;
+    std::vector<Contrib> contrib;
+    pase_status st = build_launches<KeyT>(g, fake_ws, launches, contrib);
+    if (st != PASE_OK) return st;
+    FlowPlan fp;
+    st = build_flow<KeyT>(g, launches, fp);
+    if (st != PASE_OK) return st;
+    *items = (uint64_t)fp.nitems[0] + fp.nitems[1];
+    return flow_simulate(g, fp, workers, lat_workers, seed);
+}
+
+extern "C" pase_status pase_flow_check(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
+                                       uint64_t *items) {
+    if (!g || !items || workers < 2 || lat_workers < 1 || lat_workers >= workers)
+        return g ? fail(g, PASE_ERR_INVALID_ARGUMENT, "need items, workers >= 2, 1 <= lat_workers < workers")
+                 : PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "call pase_enumerate_configs first");
+    if (!g->plan.resident || g->schedule != kSchedFlow)
+        return fail(g, PASE_ERR_BAD_STATE, "the plan does not use the dataflow schedule");
+    pase_status st;
+    const uint32_t kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    return kt == 0 ? flow_check_t<double>(g, workers, lat_workers, seed, items)
+                   : flow_check_t<uint64_t>(g, workers, lat_workers, seed, items);
+}

@@ -249,6 +249,54 @@ TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t n
 
 }  // namespace
 
+// Lane schedule.  The tables form an in-tree: every table but the last has
+// exactly one reader, a later position.  The tree is cut into chains: each
+// vertex continues the chain of its reader when it is the reader's longest
+// producer path (planned fill time plus a launch latency per vertex), and
+// heads a chain of its own otherwise.  The chain through the root runs on
+// lane 0 (the caller's stream), the longest other chain on lane 1, every
+// other chain with substantial work on lane 2, and small chains on the lane
+// of the vertex that reads them.  Lanes are streams: the long chains of small
+// vertices then no longer queue behind large vertices they do not depend on.
+static void assign_lanes(Plan &P) {
+    const int n = (int)P.v.size();
+    constexpr double kLaunchUs = 10.0, kLongUs = 200.0, kWorkUs = 50.0;
+    std::vector<double> top(n, 0.0);   // largest time of a producer path ending at i
+    for (int i = 0; i < n; i++) {
+        double m = 0;
+        for (const auto &t : P.v[i].terms) m = std::max(m, top[t.j]);
+        top[i] = m + P.v[i].est_us + kLaunchUs;
+    }
+    std::vector<int> chain(n, -1), head;
+    std::vector<double> work;
+    for (int x = n - 1; x >= 0; x--) {
+        if (chain[x] < 0) {
+            chain[x] = (int)head.size();
+            head.push_back(x);
+            work.push_back(0.0);
+        }
+        work[chain[x]] += P.v[x].est_us;
+        int best = -1;
+        for (const auto &t : P.v[x].terms)
+            if (best < 0 || top[t.j] > top[best]) best = t.j;
+        if (best >= 0) chain[best] = chain[x];
+    }
+    // chains are numbered by decreasing head position, so the chain of a
+    // head's reader always has its lane already
+    const int nc = (int)head.size();
+    std::vector<int> lane(nc, -1);
+    int second = -1;
+    for (int c = 1; c < nc; c++)
+        if (top[head[c]] >= kLongUs && (second < 0 || top[head[c]] > top[head[second]])) second = c;
+    for (int c = 0; c < nc; c++) {
+        if (c == 0) lane[c] = 0;
+        else if (c == second) lane[c] = 1;
+        else if (work[c] >= kWorkUs) lane[c] = 2;
+        else lane[c] = lane[chain[P.v[head[c]].consumer]];
+    }
+    for (int i = 0; i < n; i++) P.v[i].lane = lane[chain[i]];
+}
+
 static pase_status build_plan(pase_graph_t g) {
     const int n = (int)g->V.size();
     Plan &P = g->plan;
@@ -389,6 +437,10 @@ static pase_status build_plan(pase_graph_t g) {
                         if (g->tile_rows && tm != g->tile_rows) continue;
                         // more than 32 accumulators per lane cost waves (VGPRs)
                         if (!g->tile_rows && !g->tile_cols && tz * tm > 32) continue;
+                        // the dataflow kernel carries the variants of modest register need
+                        if (g->schedule == kSchedFlow && !g->tile_rows && !g->tile_cols &&
+                            !flow_rows_ok(false, tz, tm, std::min<uint32_t>(na, 4)))
+                            continue;
                         const TileTime tt = tile_time(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts, g->c_splits);
                         if (!rc.ok || tt.us < rc.cost) {
                             rc.ok = true;
@@ -420,6 +472,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.layout.insert(vp.layout.end(), vp.O.begin(), vp.O.end());
             vp.layout.insert(vp.layout.end(), vp.R.begin(), vp.R.end());
             vp.parts = best.parts;
+            vp.est_us = best.cost;
             const uint64_t ns = best.nsplit;
             vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
             vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
@@ -428,6 +481,8 @@ static pase_status build_plan(pase_graph_t g) {
             if (vp.z < 0) P.stream_cells += vp.N * vp.K;
         } else {
             vp.kernel = kGeneric;
+            // gather-bound: ~1e11 cell updates/s, plus a launch's worth of latency
+            vp.est_us = 5.0 + (double)vp.N * vp.K / 1e5;
             vp.layout = vp.D;
             // threads walk the table in layout order: follow the memory order of the
             // largest lookup that spans several digits so that its reads coalesce
@@ -451,6 +506,7 @@ static pase_status build_plan(pase_graph_t g) {
         for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
             vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
     }
+    assign_lanes(P);
     return PASE_OK;
 }
 
@@ -460,17 +516,28 @@ static pase_status build_plan(pase_graph_t g) {
 // Cost tables T_i live from their fill to their single reader (or to the end
 // when tables are kept or i is last) and share memory by interval packing;
 // argmin tables A_i all live until back-substitution.
-static pase_status layout_memory_mode(pase_graph_t g, bool by_level);
+enum LayoutMode { kLayoutResident = 0, kLayoutSeq = 1, kLayoutLevel = 2 };
+static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode);
 
-// Level schedule when its memory fits the budget, else one vertex at a time.
+// The two-lane and dataflow schedules run vertices concurrently and need
+// every table and scratch buffer resident at once; when that exceeds the
+// budget, or for the level schedule, tables share memory by lifetimes over
+// levels; when even that does not fit, one vertex at a time.
 static pase_status layout_memory(pase_graph_t g) {
-    if (g->schedule == 0 && layout_memory_mode(g, true) == PASE_OK) return PASE_OK;
-    return layout_memory_mode(g, false);
+    if ((g->schedule == kSchedLanes || g->schedule == kSchedFlow) &&
+        layout_memory_mode(g, kLayoutResident) == PASE_OK)
+        return PASE_OK;
+    if (g->schedule != kSchedSeq && layout_memory_mode(g, kLayoutLevel) == PASE_OK) return PASE_OK;
+    return layout_memory_mode(g, kLayoutSeq);
 }
 
-static pase_status layout_memory_mode(pase_graph_t g, bool by_level) {
+static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     Plan &P = g->plan;
+    // resident: vertices may run in any order the dependencies allow, so
+    // every vertex has scratch of its own and no table memory is reused
+    const bool flow = mode == kLayoutResident, by_level = mode != kLayoutSeq;
     P.by_level = by_level;
+    P.resident = flow;
     P.nslots = 0;
     for (auto &vp : P.v) {
         vp.slot = by_level ? vp.level : (int)(&vp - &P.v[0]);
@@ -510,6 +577,16 @@ static pase_status layout_memory_mode(pase_graph_t g, bool by_level) {
     off = align_up(off + n * (sizeof(PrepArgs) + sizeof(RowsArgs) + sizeof(GenericArgs) + sizeof(ReduceArgs)), A);
     P.off_batch = off;
     off = align_up(off + 3 * (uint64_t)n * sizeof(BatchEntry), A);
+    // dataflow tables: control block, done counters, segments (prep, fill,
+    // reduce per vertex, two queues) and their dependencies
+    P.off_flow = off;
+    P.flow_bytes = 0;
+    if (flow) {
+        uint64_t ndeps = 0;
+        for (const auto &vp : P.v) ndeps += vp.terms.size() + 2;
+        P.flow_bytes = sizeof(FlowCtl) + align_up(4ull * n, 16) + 3ull * n * sizeof(Seg) + ndeps * sizeof(SegDep);
+        off = align_up(off + P.flow_bytes, A);
+    }
     P.off_cfg = off;
     off = align_up(off + g->V.size() * 4, A);
     P.off_out = off;
@@ -520,7 +597,7 @@ static pase_status layout_memory_mode(pase_graph_t g, bool by_level) {
     struct Iv { int i, s, e; uint64_t size; };
     std::vector<Iv> iv;
     for (int i = 0; i < n; i++) {
-        int end = (g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
+        int end = (flow || g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
         iv.push_back({i, P.v[i].slot, end, align_up(P.v[i].N * 8, A)});
     }
     std::vector<int> order(n);
@@ -565,12 +642,14 @@ static pase_status layout_memory_mode(pase_graph_t g, bool by_level) {
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
         }
         vp.block_elems = e;
-        vp.block_off = bsum[vp.slot];
-        vp.partial_off = psum[vp.slot];
-        bsum[vp.slot] += align_up(e * 8, A);
-        psum[vp.slot] += pb;
-        bmax = std::max(bmax, bsum[vp.slot]);
-        pmax = std::max(pmax, psum[vp.slot]);
+        // (the dataflow schedule keeps every vertex's scratch: one slot for all)
+        const int sl = flow ? 0 : vp.slot;
+        vp.block_off = bsum[sl];
+        vp.partial_off = psum[sl];
+        bsum[sl] += align_up(e * 8, A);
+        psum[sl] += pb;
+        bmax = std::max(bmax, bsum[sl]);
+        pmax = std::max(pmax, psum[sl]);
     }
     P.block_bytes = bmax;
     P.off_block = off;
@@ -711,7 +790,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         break;
     case PASE_OPT_PROFILE: g->profile = value != 0; break;
     case PASE_OPT_SCHEDULE:
-        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0 or 1");
+        if (value > 3) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 2 or 3");
         g->schedule = (int)value;
         break;
     case PASE_OPT_TILE_COLS:
@@ -727,6 +806,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value != 0 && value != 1 && value != 2 && value != 4)
             return fail(g, PASE_ERR_INVALID_ARGUMENT, "tile parts 0, 1, 2 or 4");
         g->tile_parts = (uint32_t)value;
+        break;
+    case PASE_OPT_LATENCY_WORKERS:
+        if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "latency workers <= 65535");
+        g->lat_workers = (uint32_t)value;
         break;
     case PASE_OPT_C_SPLITS:
         if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "c splits 0..65535");
@@ -875,6 +958,8 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     x.row_terms = vp.na;
     x.lookups = (uint32_t)vp.terms.size();
     x.fill_ms = vp.fill_ms;
+    x.level = (uint32_t)vp.level;
+    x.lane = (uint32_t)vp.lane;
     *out = x;
     return PASE_OK;
 }

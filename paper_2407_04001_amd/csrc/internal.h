@@ -149,7 +149,8 @@ struct ReduceArgs {
 struct BacktrackDesc {        // per position, for the back-substitution kernel
     const uint16_t *A;
     uint32_t vi, m;
-    uint32_t level, pad;      // backward level: 1 + max level over D(i) (0 when D(i) is empty)
+    uint32_t level;           // backward level: 1 + max level over D(i) (0 when D(i) is empty)
+    uint32_t K;               // configurations of v_i: a stored argmin must be below it
     uint32_t dig[kMaxDep];    // vertex ids of the layout digits
     uint64_t stride[kMaxDep];
 };
@@ -158,7 +159,56 @@ constexpr uint32_t kMaxBacktrackThreads = 1024;   // one thread per position
 
 struct SearchOut {            // written by the back-substitution kernel
     uint64_t min_cost;
-    uint32_t status;
+    uint32_t status;          // 0 = ok; bits: 1, 2 = dataflow error word, 4 = an argmin out of range
+    uint32_t pad;
+};
+
+// ------------------------------------------------------------------ dataflow schedule
+// One persistent launch runs every prep, fill and split-reduction workgroup of
+// a search ("items").  Items are grouped in segments (one segment = the
+// workgroups one of those launches would have had) and handed out by two
+// ticket queues: the latency queue (vertices on the dependency chains, small)
+// and the bulk queue (large vertices).  Both queues hand out their items in
+// one global order that is a topological order of the item dependencies, so
+// the smallest unfinished item can always run.  Position i counts its
+// finished items in done[i]; a segment waits until the counters it depends
+// on reach their targets.
+enum SegKind : uint32_t { kSegPrep = 0, kSegRows = 1, kSegGeneric = 2, kSegReduce = 3 };
+
+struct Seg {
+    uint32_t first;           // first ticket of the segment in its queue
+    uint32_t count;           // items
+    uint32_t kind;            // SegKind
+    uint32_t variant;         // rows: (TZ * 4 + TM) * 8 + NA; generic: NT (0 = runtime count)
+    uint32_t pos;             // sequence position (descriptor index and done counter)
+    uint32_t dep_begin, dep_end;   // range in the dependency array
+    uint32_t pad;
+};
+
+struct SegDep {
+    uint32_t counter;         // position whose done counter is waited for
+    uint32_t target;          // value it must reach
+};
+
+constexpr int kLatQ = 0, kBulkQ = 1;
+
+// PASE_OPT_SCHEDULE values
+enum SchedKind { kSchedLanes = 0, kSchedSeq = 1, kSchedLevel = 2, kSchedFlow = 3 };
+
+// Row-fill variants (columns per lane TZ, rows per lane TM, row terms NA) the
+// dataflow kernel carries: those that need at most ~96 VGPRs, so that the one
+// kernel keeps the occupancy (5 waves per SIMD) of the per-vertex launches of
+// the hot variants.  A plan using another variant runs the level schedule.
+constexpr bool flow_rows_ok(bool u64_keys, uint32_t TZ, uint32_t TM, uint32_t NA) {
+    if (u64_keys) return TM == 1 ? (TZ >= 8 && TZ <= 24) : TZ == 8;
+    if (TM == 1) return true;
+    if (TZ == 1) return NA <= 2;
+    return TZ <= 12 || (TZ <= 16 && NA <= 2);
+}
+
+struct FlowCtl {              // zeroed by the per-search upload
+    uint32_t head[2];         // next ticket of each queue
+    uint32_t error;           // 1: a dependency wait gave up (the result is invalid)
     uint32_t pad;
 };
 
@@ -189,6 +239,7 @@ struct VPlan {
     uint64_t MO = 1, MR = 1;
     uint32_t na = 0;                // row kernel: per-lane row terms
     double fill_ms = 0;             // last profiled fill time
+    double est_us = 0;              // planned fill time (tile model), for the schedule
     // memory
     uint64_t T_off = 0, A_off = 0;  // bytes into the table arenas
     uint64_t block_elems = 0;       // block scratch this vertex needs
@@ -197,6 +248,7 @@ struct VPlan {
     // schedule
     int level = 0;                  // dependency level: 1 + max level of the tables it reads
     int slot = 0;                   // launch slot: its level (level schedule) or its position
+    int lane = 0;                   // lane schedule: stream 0 (the caller's), 1 or 2 (see assign_lanes)
 };
 
 struct Plan {
@@ -213,6 +265,9 @@ struct Plan {
     uint64_t sig_count = 0;         // split signatures of all edge endpoints
     int nslots = 0;                 // launch slots (levels, or positions when sequential)
     bool by_level = false;          // the vertices of one dependency level share launches
+    bool resident = false;          // every table and scratch buffer resident at once (no reuse)
+    uint64_t off_flow = 0;          // dataflow tables: control block, done counters, segments, deps
+    uint64_t flow_bytes = 0;
     uint64_t off_desc = 0, off_batch = 0;   // per-vertex launch descriptors, batch tables
 };
 
@@ -232,7 +287,8 @@ struct pase_graph_s {
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
     uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
-    int schedule = 0;               // 0 = by dependency level, 1 = strictly in sequence
+    uint32_t lat_workers = 0;       // dataflow latency workers, 0 = chosen
+    int schedule = 0;               // pase_option PASE_OPT_SCHEDULE (SchedKind)
     // configurations
     bool enumerated = false;
     uint32_t p = 0, log2p = 0;

@@ -1,0 +1,546 @@
+// Device code shared by the kernels of libpase (gfx950): key arithmetic, the
+// device cost model, and the work of one workgroup of each kernel ("items"),
+// which the per-vertex launches and the one-launch dataflow schedule both run.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <type_traits>
+
+#include "internal.h"
+
+namespace pase {
+
+// ------------------------------------------------------------------ key arithmetic
+template <typename KeyT> struct KeyOps;
+
+template <> struct KeyOps<double> {
+    using Val = double;   // table value type
+    static constexpr double sentinel() { return 1152921504606846976.0; }  // 2^60 > any key
+    __device__ static double from_u64(uint64_t x) { return (double)x; }
+    __device__ static uint64_t val_to_u64(double x) { return (uint64_t)x; }
+    __device__ static double add(double a, double b) { return a + b; }
+    __device__ static double min(double a, double b) { return __builtin_fmin(a, b); }
+    // key = cost * 2^bits + c  ->  (cost * 2^out_shift, c)
+    __device__ static void split(double key, uint32_t bits, uint32_t out_shift, double &val, uint32_t &c) {
+        double s = __builtin_ldexp(1.0, (int)bits);
+        double v = __builtin_trunc(key * __builtin_ldexp(1.0, -(int)bits));
+        val = v * __builtin_ldexp(1.0, (int)out_shift);
+        c = (uint32_t)__builtin_fma(-v, s, key);
+    }
+};
+
+template <> struct KeyOps<uint64_t> {
+    using Val = uint64_t;
+    static constexpr uint64_t sentinel() { return ~0ull; }
+    __device__ static uint64_t from_u64(uint64_t x) { return x; }
+    __device__ static uint64_t val_to_u64(uint64_t x) { return x; }
+    __device__ static uint64_t add(uint64_t a, uint64_t b) { return a + b; }
+    __device__ static uint64_t min(uint64_t a, uint64_t b) { return a < b ? a : b; }
+    __device__ static void split(uint64_t key, uint32_t bits, uint32_t out_shift, uint64_t &val, uint32_t &c) {
+        val = (key >> bits) << out_shift;
+        c = (uint32_t)(key & ((1ull << bits) - 1));
+    }
+};
+
+
+// Buffer resource word 3 (data format 32-bit, raw addressing) for gfx9-family
+// buffer instructions.
+constexpr int kBufferWord3 = 0x00020000;
+
+// ------------------------------------------------------------------ cost model (device)
+// Layer cost t_l(v, c) = ceil(F / P) + r * (2^e_red - 1) * ceil(keep / 2^(E - e_red)),
+// with P = 2^E the device count of the configuration and e_red the exponent
+// sum over contracted dims.  Power-of-two divisions are shifts; the host has
+// bounded every operand so nothing overflows.
+__device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
+    uint32_t E = 0, ered = 0;
+    for (uint32_t k = 0; k < dv.ndims; k++) {
+        E += ex[k];
+        if ((dv.reduce_mask >> k) & 1u) ered += ex[k];
+    }
+    uint64_t compute = (dv.flops + ((1ull << E) - 1)) >> E;
+    uint32_t ek = E - ered;
+    uint64_t part = (dv.keep_n + ((1ull << ek) - 1)) >> ek;
+    return compute + r * (((1ull << ered) - 1) * part);
+}
+
+// Split signature of one endpoint configuration of an edge: the split
+// exponent of every tensor dim (0 for an unsplit dim), 5 bits each.  Two
+// endpoints redistribute nothing exactly when their signatures are equal.
+__device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t rank, const uint8_t *ex) {
+    uint64_t sig = 0;
+    for (uint32_t k = 0; k < rank; k++) sig |= (uint64_t)(dims[k] >= 0 ? ex[dims[k]] : 0) << (5 * k);
+    return sig;
+}
+
+__device__ __forceinline__ uint64_t edge_cost_sig(uint64_t sig_a, uint64_t sig_b, uint32_t la, uint32_t lb,
+                                                  uint64_t elems, uint64_t r) {
+    if (sig_a == sig_b) return 0;
+    uint32_t s = la > lb ? la : lb;
+    return r * ((elems + ((1ull << s) - 1)) >> s);
+}
+
+// ------------------------------------------------------------------ prep: key-space blocks
+// Batched launches: the workgroups of one launch are the concatenation of the
+// workgroups of its vertices; find the vertex of this workgroup (uniform).
+__device__ __forceinline__ uint32_t batch_find(const BatchEntry *__restrict__ be, uint32_t nbe, uint32_t wg) {
+    uint32_t lo = 0, hi = nbe;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (be[mid].first <= wg) lo = mid; else hi = mid;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
+// One workgroup handles kPrepThreads consecutive (c, column) elements of one
+// outer index of one block, so the block, its contributions and the outer
+// digits are uniform across the workgroup (scalar loads); lanes differ only in
+// (c, column).
+template <typename KeyT>
+__device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const DevVertex *__restrict__ V,
+                                          const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
+                                          const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
+                                          const Contrib *__restrict__ cb, uint64_t r) {
+    using Val = typename KeyOps<KeyT>::Val;
+    KeyT *__restrict__ blocks = (KeyT *)a.blocks;
+    uint32_t b = 0;
+    while (b + 1 < a.nblocks && wg >= a.blk[b + 1].wg_begin) b++;
+    b = __builtin_amdgcn_readfirstlane(b);
+    const Block &bk = a.blk[b];
+    const uint32_t rel = wg - bk.wg_begin;
+    const uint32_t row = rel / bk.chunks, chunk = rel % bk.chunks;
+    const uint32_t per_row = a.K * bk.ld;
+    const uint32_t e = chunk * kPrepThreads + threadIdx.x;
+    if (e >= per_row) return;
+    const uint32_t c = e / bk.ld, q = e % bk.ld;
+    KeyT *out = blocks + bk.out_off + (uint64_t)row * per_row + e;
+    if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; return; }
+    uint32_t dv[kMaxDep];
+    for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
+    uint32_t x = row;
+    for (int k = (int)bk.npre - 1; k >= 0; k--) {
+        dv[bk.pre[k]] = x % bk.prerad[k];
+        x /= bk.prerad[k];
+    }
+    if (bk.post >= 0) dv[bk.post] = q;
+    const DevVertex me = V[a.vi];
+    // plain costs (layer, transfer) are summed in `sum` and shifted into key
+    // space at the end; DP tables are stored in this vertex's key space already
+    uint64_t sum = 0, keysum = 0, low = 0;
+    for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
+        const Contrib ct = cb[k];
+        if (ct.kind == kContribLayer) {
+            sum += L[me.L_off + c];
+            low = c;
+        } else if (ct.kind == kContribEdge) {
+            const DevEdge de = E[ct.edge];
+            const uint32_t xo = dv[ct.dig];
+            const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
+            const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
+            const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
+            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r);
+        } else {
+            uint64_t idx = (uint64_t)c * ct.sc;
+            for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
+            if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
+            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
+        }
+    }
+    *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
+}
+
+// Waits for every outstanding scalar-memory and LDS read (s_waitcnt
+// lgkmcnt(0), other counters left alone).  Scalar loads return out of order,
+// so a wait for one of them is always a wait for all of them: the pipelined
+// loops wait for the operands of c *before* they request those of c + 1,
+// otherwise the wait the compiler places before the first use of c's
+// operands would also wait for the prefetch.
+__device__ __forceinline__ void wait_lgkm_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// ------------------------------------------------------------------ fill: row kernel
+// Output T_i is laid out [z][o][r]: column digit z slowest, then the outer
+// digits o (those sharing a lookup with z), then the row digits r.  A tile is
+// TM x 64 consecutive rows of one (o, column chunk, c range); lane l holds
+// rows l, l + 64, ...  For each c every row forms its operand a = sum of its
+// row terms, and the wave reads the TZ column operands B[o][c][z0..z0+TZ)
+// through the scalar unit (they are wave-uniform), so each cell is one add
+// (SGPR operand) and one min; one scalar round trip per c feeds TM x 64 x TZ
+// cells.  The four waves of a workgroup take the same tile and a quarter of
+// its c range each, and combine their minima through LDS at the end: a wave
+// then does a quarter of a tile's work, so a launch has four times as many,
+// shorter, work items and its last partial round of waves costs little.
+constexpr int kMergeVals = 16;   // values per lane moved through LDS per merge pass
+
+template <typename KeyT>
+using MergeBuf = KeyT[2][kMergeVals][64];
+
+// Workgroup b of one vertex's row fill; xch: the workgroup's LDS merge buffer.
+template <typename KeyT, int TZ, int TM, int NA>
+__device__ __forceinline__ void rows_item(const RowsArgs &a, uint32_t b, MergeBuf<KeyT> &xch) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    const uint32_t lane = threadIdx.x & 63;
+    // the wave index is uniform across the wave: say so, so that everything
+    // derived from it (c range, column addresses) lives in SGPRs
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // blocks are dealt round-robin to the 8 XCDs: give every XCD a contiguous
+    // range of tiles so that tiles sharing a column slice share an L2 (every
+    // vertex's block count and first block are multiples of 8, so the XCD of
+    // a block is its local index mod 8)
+    const uint32_t nb = a.nblocks_launched;
+    const uint64_t wg = (uint64_t)(b % 8) * (nb / 8) + b / 8;
+    // a workgroup takes 4 / P tiles, P = a.parts waves per tile, each wave a
+    // P-th of the tile's c range
+    const uint32_t P = a.parts, tpw = 4 / P;
+    if (wg * tpw >= a.total_tiles) return;   // the whole workgroup leaves together
+    const uint32_t part = wave % P, tin = wave / P;
+    const bool has_tile = wg * tpw + tin < a.total_tiles;
+    // (a wave without a tile computes nothing but still takes part in the merge)
+    const uint64_t tile = min(wg * tpw + tin, a.total_tiles - 1);
+    // tile order (fastest first): row tile, column chunk, outer index, c split --
+    // all chunks of one outer index run close together and share its slices
+    const uint32_t rowtile = (uint32_t)(tile % a.tiles_per_o);
+    uint64_t t2 = tile / a.tiles_per_o;
+    const uint32_t chunk = (uint32_t)(t2 % a.nchunks);
+    t2 /= a.nchunks;
+    const uint32_t o = (uint32_t)(t2 % a.MO);
+    const uint32_t split = (uint32_t)(t2 / a.MO);
+
+    constexpr int NT = NA < 0 ? kMaxATerms : NA;
+    constexpr int NTA = NT > 0 ? NT : 1;
+    const int na = NA < 0 ? (int)a.na : NA;
+    uint32_t dO[kMaxDep];
+    {
+        uint32_t x = o;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.nO) { dO[k] = x % a.radO[k]; x /= a.radO[k]; } else dO[k] = 0;
+    }
+    // row terms are read with buffer loads: per-lane byte offset in a VGPR,
+    // the c-dependent part as a scalar offset, no per-c address arithmetic
+    __amdgpu_buffer_rsrc_t rsrc[NTA];
+    uint32_t tsc[NTA];
+#pragma unroll
+    for (int t = 0; t < NTA; t++) {
+        rsrc[t] = __builtin_amdgcn_make_buffer_rsrc(t < na ? const_cast<void *>(a.a[t].ptr) : nullptr, (short)0,
+                                                    t < na ? (int)a.a[t].bytes : 0, kBufferWord3);
+        tsc[t] = t < na ? a.a[t].sc * (uint32_t)sizeof(Val) : 0;
+    }
+    uint32_t r[TM], offb[TM][NTA];
+    bool valid[TM];
+#pragma unroll
+    for (int m = 0; m < TM; m++) {
+        r[m] = (rowtile * TM + m) * 64 + lane;
+        valid[m] = r[m] < a.MR;
+        uint32_t x = valid[m] ? r[m] : a.MR - 1, dR[kMaxDep];
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
+#pragma unroll
+        for (int t = 0; t < NTA; t++) {
+            uint32_t off = 0;
+            if (t < na)
+                for (int k = 0; k < kMaxDep; k++) off += dO[k] * a.a[t].sdO[k] + dR[k] * a.a[t].sdR[k];
+            offb[m][t] = off * (uint32_t)sizeof(Val);
+        }
+    }
+    // this wave's part [c0, c1) of the tile's c range (possibly empty)
+    const uint32_t cs = split * a.cper, ce_ = has_tile ? min(a.K, cs + a.cper) : cs;
+    const uint32_t q = (ce_ - cs + P - 1) / P;
+    const uint32_t c0 = min(ce_, cs + part * q), c1 = min(ce_, c0 + q);
+    const uint32_t ldz = a.ldz;
+    const KeyT *B = (const KeyT *)a.B + (uint64_t)o * a.K * ldz + (uint64_t)chunk * TZ;
+
+    KeyT acc[TM][TZ];
+#pragma unroll
+    for (int m = 0; m < TM; m++)
+#pragma unroll
+        for (int t = 0; t < TZ; t++) acc[m][t] = Ops::sentinel();
+
+    // Software pipeline over two register sets of U values of c each: the
+    // row terms and column chunks of the next U values are requested while
+    // the cells of the current ones are computed from the other set, so load
+    // latency overlaps VALU work.  Narrow tiles have little work per c and
+    // keep U = 4 values in flight per set.  Loads past c1 repeat column
+    // c1 - 1 (in bounds, unused) so that every load is unconditional and the
+    // register sets never need copying.
+    constexpr int U = TZ <= 2 ? 4 : 1;
+    using SKey = const __attribute__((address_space(4))) KeyT;
+    uint64_t xe[U][TM][NTA], xo[U][TM][NTA];
+    KeyT ce[U][TZ], co[U][TZ];
+    auto load = [&](uint64_t (&xs)[U][TM][NTA], KeyT (&bs)[U][TZ], uint32_t cc) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const uint32_t cu = min(cc + u, c1 - 1);
+#pragma unroll
+            for (int m = 0; m < TM; m++)
+#pragma unroll
+                for (int t = 0; t < NTA; t++)
+                    if (t < na)
+                        xs[u][m][t] = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(
+                                                                       rsrc[t], (int)offb[m][t], (int)(cu * tsc[t]), 0));
+            SKey *brow = (SKey *)(uintptr_t)(B + (uint64_t)cu * ldz);
+#pragma unroll
+            for (int t = 0; t < TZ; t++) bs[u][t] = brow[t];
+        }
+    };
+    auto cells = [&](const uint64_t (&xs)[U][TM][NTA], const KeyT (&bs)[U][TZ], uint32_t n) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (u > 0 && (uint32_t)u >= n) break;
+            KeyT av[TM];
+#pragma unroll
+            for (int m = 0; m < TM; m++) {
+                av[m] = (KeyT)0;
+#pragma unroll
+                for (int t = 0; t < NTA; t++)
+                    if (t < na) {
+                        const KeyT v = __builtin_bit_cast(KeyT, xs[u][m][t]);
+                        av[m] = t == 0 ? v : Ops::add(av[m], v);
+                    }
+            }
+#pragma unroll
+            for (int t = 0; t < TZ; t++)
+#pragma unroll
+                for (int m = 0; m < TM; m++) acc[m][t] = Ops::min(acc[m][t], Ops::add(av[m], bs[u][t]));
+        }
+    };
+    if (c0 < c1) {
+        load(xe, ce, c0);
+        uint32_t c = c0;
+        for (; c + U < c1; c += 2 * U) {
+            // up to 16 columns both sets fit in SGPRs at once: the barriers
+            // keep the scheduler from sinking the loads of the next set below
+            // the cells of the current one, and the explicit wait for the
+            // current operands comes before those loads are issued
+            if constexpr (TZ <= 16) {
+                wait_lgkm_all();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            load(xo, co, c + U);
+            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
+            cells(xe, ce, U);
+            if constexpr (TZ <= 16) {
+                wait_lgkm_all();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            load(xe, ce, c + 2 * U);
+            if constexpr (TZ <= 16) __builtin_amdgcn_sched_barrier(0);
+            cells(xo, co, min((uint32_t)U, c1 - (c + U)));
+        }
+        if (c < c1) cells(xe, ce, min((uint32_t)U, c1 - c));
+    }
+
+    // combine the parts of a tile through LDS, halving the number of holders
+    // per stage (P = 4: parts 2, 3 -> 0, 1, then 1 -> 0; P = 2: 1 -> 0),
+    // kMergeVals values per lane and pass; P is uniform across the workgroup,
+    // so every wave meets the same barriers
+    constexpr int V = TM * TZ;
+    for (uint32_t d = P / 2; d >= 1; d /= 2) {
+#pragma unroll
+        for (int p0 = 0; p0 < V; p0 += kMergeVals) {
+            constexpr int W = kMergeVals;
+            __syncthreads();
+            if (part >= d && part < 2 * d) {
+                const uint32_t slot = tin * d + (part - d);
+#pragma unroll
+                for (int j = 0; j < W; j++)
+                    if (p0 + j < V) xch[slot][j][lane] = acc[(p0 + j) / TZ][(p0 + j) % TZ];
+            }
+            __syncthreads();
+            if (part < d) {
+                const uint32_t slot = tin * d + part;
+#pragma unroll
+                for (int j = 0; j < W; j++)
+                    if (p0 + j < V) {
+                        KeyT &x = acc[(p0 + j) / TZ][(p0 + j) % TZ];
+                        x = Ops::min(x, xch[slot][j][lane]);
+                    }
+            }
+        }
+    }
+    if (part != 0 || !has_tile) return;
+
+    const uint64_t plane = (uint64_t)a.MO * a.MR;
+    const uint32_t zbase = chunk * TZ;
+#pragma unroll
+    for (int m = 0; m < TM; m++) {
+        if (!valid[m]) continue;
+        const uint64_t base_idx = (uint64_t)o * a.MR + r[m];
+#pragma unroll
+        for (int t = 0; t < TZ; t++) {
+            const uint32_t z = zbase + t;
+            if (z < a.Kz) {
+                const uint64_t idx = (uint64_t)z * plane + base_idx;
+                if (a.nsplit > 1) {
+                    ((KeyT *)a.partial)[(uint64_t)split * a.N + idx] = acc[m][t];
+                } else {
+                    Val v;
+                    uint32_t cc;
+                    Ops::split(acc[m][t], a.bits, a.out_shift, v, cc);
+                    ((Val *)a.T)[idx] = v;
+                    a.A[idx] = (uint16_t)cc;
+                }
+            }
+        }
+    }
+}
+
+template <typename KeyT>
+__device__ __forceinline__ void reduce_item(const ReduceArgs &a, uint32_t lb) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    for (uint64_t t = lb * (uint64_t)blockDim.x + threadIdx.x; t < a.N; t += (uint64_t)a.nblk * blockDim.x) {
+        KeyT best = ((const KeyT *)a.partial)[t];
+        for (uint32_t s = 1; s < a.nsplit; s++) best = Ops::min(best, ((const KeyT *)a.partial)[s * a.N + t]);
+        Val v;
+        uint32_t cc;
+        Ops::split(best, a.bits, a.out_shift, v, cc);
+        ((Val *)a.T)[t] = v;
+        a.A[t] = (uint16_t)cc;
+    }
+}
+
+// ------------------------------------------------------------------ fill: generic kernel
+// Any |D(i)| <= PASE_MAX_DEP and any term shapes.  A group of 2^group_log2
+// lanes owns one entry phi: lane l evaluates c = l, l + G, ... (key = sum of
+// the terms), the group then takes the minimum key with cross-lane swaps.
+// Keys are distinct for distinct c, so the minimum -- and with it the lowest
+// optimal c -- does not depend on the evaluation order.
+template <typename KeyT>
+__device__ __forceinline__ KeyT shfl_xor_key(KeyT v, int mask) {
+    uint64_t u = __builtin_bit_cast(uint64_t, v);
+    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)u, mask, 64);
+    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), mask, 64);
+    return __builtin_bit_cast(KeyT, ((uint64_t)hi << 32) | lo);
+}
+
+template <typename KeyT, int NT>
+__device__ __forceinline__ void generic_item(const GenericArgs &a, uint32_t lb) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    const uint32_t G = 1u << a.group_log2;
+    const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
+    constexpr int MT = NT < 0 ? kMaxGTerms : NT;
+    const int nt = NT < 0 ? (int)a.nt : NT;
+    for (uint64_t tid = lb * (uint64_t)blockDim.x + threadIdx.x; tid < ((nthreads + 255) / 256) * 256;
+         tid += (uint64_t)a.nblk * blockDim.x) {
+        const bool live = tid < nthreads;
+        const uint64_t phi = live ? tid >> a.group_log2 : a.N - 1;
+        const uint32_t lane = (uint32_t)(tid & (G - 1));
+        uint32_t d[kMaxDep];
+        uint64_t x = phi;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.m) { d[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else d[k] = 0;
+        const KeyT *base[MT];
+        uint32_t sc[MT];
+#pragma unroll
+        for (int t = 0; t < MT; t++) {
+            uint64_t o = 0;
+            if (t < nt)
+                for (int k = 0; k < kMaxDep; k++) o += (uint64_t)d[k] * a.t[t].sd[k];
+            base[t] = (const KeyT *)a.t[t < nt ? t : 0].ptr + (t < nt ? o : 0);
+            sc[t] = t < nt ? a.t[t].sc : 0;
+        }
+        KeyT best0 = Ops::sentinel(), best1 = Ops::sentinel();
+        uint32_t c = lane;
+        // two independent chains keep two loads of every term in flight
+        for (; c + G < a.K; c += 2 * G) {
+            KeyT k0 = base[0][(uint64_t)c * sc[0]];
+            KeyT k1 = base[0][(uint64_t)(c + G) * sc[0]];
+#pragma unroll
+            for (int t = 1; t < MT; t++)
+                if (t < nt) {
+                    k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
+                    k1 = Ops::add(k1, base[t][(uint64_t)(c + G) * sc[t]]);
+                }
+            best0 = Ops::min(best0, k0);
+            best1 = Ops::min(best1, k1);
+        }
+        if (c < a.K) {
+            KeyT k0 = base[0][(uint64_t)c * sc[0]];
+#pragma unroll
+            for (int t = 1; t < MT; t++)
+                if (t < nt) k0 = Ops::add(k0, base[t][(uint64_t)c * sc[t]]);
+            best0 = Ops::min(best0, k0);
+        }
+        KeyT best = Ops::min(best0, best1);
+        for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
+        if (live && lane == 0) {
+            Val v;
+            uint32_t cc;
+            Ops::split(best, a.bits, a.out_shift, v, cc);
+            ((Val *)a.T)[phi] = v;
+            a.A[phi] = (uint16_t)cc;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ dataflow launch
+// One persistent launch runs the prep, fill and split-reduction workgroups of
+// every vertex (the "items" of the segments built on the host).  Thread 0 of
+// a workgroup takes a ticket, the workgroup waits until the item's
+// dependencies (done counters of earlier positions) are met, runs the item
+// exactly as the corresponding kernel's workgroup would, publishes its stores
+// at device scope and counts the item as done.
+//
+// Taking a ticket: a latency worker (workgroup index < lat_workers) takes the
+// next latency-queue item; any other workgroup takes the latency queue's head
+// item when its dependencies are already met (so idle throughput can serve a
+// wide latency-bound vertex), else the next bulk item.  A drained queue sends
+// its workers to the other one; the launch ends when both are drained.
+// Both queues hand out items in one global topological order and each has a
+// worker of its own, so the smallest unfinished item can always run.  A wait
+// that exceeds timeout_ticks (100 MHz real-time clock) sets the error word and
+// every later wait returns at once: the launch still drains, and the host
+// reports the search as failed.
+struct FlowArgs {
+    const Seg *seg[2];
+    uint32_t nseg[2];
+    uint32_t nitems[2];
+    const SegDep *deps;
+    FlowCtl *ctl;
+    uint32_t *done;
+    const PrepArgs *prep;
+    const RowsArgs *rows;
+    const GenericArgs *gen;
+    const ReduceArgs *red;
+    const DevVertex *V;
+    const DevEdge *E;
+    const uint64_t *L;
+    const uint8_t *lsum;
+    const uint64_t *sig;
+    const Contrib *cb;
+    uint64_t r;
+    uint64_t timeout_ticks;
+    uint32_t lat_workers;
+};
+
+__device__ __forceinline__ uint32_t load_counter(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint32_t seg_find(const Seg *seg, uint32_t nseg, uint32_t t) {
+    uint32_t lo = 0, hi = nseg;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (seg[mid].first <= t) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ bool deps_met(const FlowArgs &f, const Seg &sg) {
+    for (uint32_t k = sg.dep_begin; k < sg.dep_end; k++)
+        if (load_counter(&f.done[f.deps[k].counter]) < f.deps[k].target) return false;
+    return true;
+}
+
+
+// Dataflow launch of the search (flow.hip): resident workgroups per compute
+// unit, and the launch itself.
+template <typename KeyT>
+hipError_t flow_occupancy(int *per_cu);
+template <typename KeyT>
+hipError_t flow_launch(const FlowArgs &f, uint32_t grid, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+
+}  // namespace pase

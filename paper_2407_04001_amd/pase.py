@@ -20,7 +20,7 @@ OK, INVALID_ARGUMENT, NOT_CONNECTED, BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMO
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STATE", 4: "OVERFLOW",
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
 (OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
- OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS) = range(1, 11)
+ OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS, OPT_LATENCY_WORKERS) = range(1, 12)
 
 
 class VertexDesc(C.Structure):
@@ -44,7 +44,8 @@ class RunStats(C.Structure):
                 ("rows_vertices", C.c_uint32), ("rows_cells", C.c_uint64), ("host_plan_ms", C.c_double),
                 ("wall_ms", C.c_double), ("fill_ms", C.c_double), ("rows_fill_ms", C.c_double),
                 ("rows_launches", C.c_uint32), ("slots", C.c_uint32), ("stream_cells", C.c_uint64),
-                ("stream_fill_ms", C.c_double), ("stream_launches", C.c_uint32)]
+                ("stream_fill_ms", C.c_double), ("stream_launches", C.c_uint32), ("schedule", C.c_uint32),
+                ("flow_grid", C.c_uint32), ("flow_lat_workers", C.c_uint32), ("flow_items", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -56,7 +57,7 @@ class VertexInfo(C.Structure):
                 ("column", C.c_int32), ("outer", C.c_uint32), ("rows", C.c_uint32),
                 ("tile_cols", C.c_uint32), ("tile_rows", C.c_uint32), ("splits", C.c_uint32),
                 ("row_terms", C.c_uint32), ("lookups", C.c_uint32), ("parts", C.c_uint32),
-                ("fill_ms", C.c_double)]
+                ("fill_ms", C.c_double), ("level", C.c_uint32), ("lane", C.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -66,7 +67,7 @@ EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_e
            "pase_num_configs", "pase_config_splits", "pase_get_sequence", "pase_get_dependent_set",
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
-           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get"]
+           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get", "pase_flow_check"]
 
 _lib = None
 
@@ -102,6 +103,7 @@ def load(path: str = LIB_PATH):
         "pase_edge_costs": (st, [P, U32, P]),
         "pase_stats": (st, [P, P]),
         "pase_vertex_info_get": (st, [P, U32, P]),
+        "pase_flow_check": (st, [P, U32, U32, U64, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -253,6 +255,12 @@ def pase_vertex_info_get(h, v: int) -> dict:
     return x.as_dict()
 
 
+def pase_flow_check(h, workers: int, lat_workers: int, seed: int = 0) -> int:
+    items = C.c_uint64()
+    _check(h, load().pase_flow_check(h, int(workers), int(lat_workers), int(seed), C.byref(items)))
+    return items.value
+
+
 # ------------------------------------------------------------------ convenience wrapper
 class Graph:
     """A computation graph handle.  ``graph`` is a dict in the layout of
@@ -343,3 +351,6 @@ class Graph:
 
     def vertex_info(self, v: int) -> dict:
         return pase_vertex_info_get(self.h, v)
+
+    def flow_check(self, workers: int, lat_workers: int, seed: int = 0) -> int:
+        return pase_flow_check(self.h, workers, lat_workers, seed)

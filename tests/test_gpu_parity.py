@@ -66,9 +66,10 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0):
+         parts=0, splits=0, lat_workers=0):
     pg = P.Graph(g, seq_rule=rule)
     pg.enumerate_configs(p or g["p"])
+    pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
     pg.set_option(P.OPT_KEY_TYPE, key)
@@ -259,14 +260,18 @@ def _golden(name, seed):
         return json.load(f)
 
 
-def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0)):
+def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
+                  lat_workers=0):
     gold = _golden(name, seed)
     g = workload(name, seed)
-    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile}")
-    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile)
+    say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
+        f"lat_workers={lat_workers}")
+    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
+                         lat_workers=lat_workers)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
-        f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']}")
+        f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
+        f"schedule {st['schedule']}")
     assert pg.K == gold["num_configs"]
     assert pg.sequence() == gold["sequence"]
     assert st["cells"] == gold["cells"]
@@ -307,6 +312,33 @@ def test_generic_and_u64_paths_against_golden(P, name):
 def test_sequential_schedule_against_golden(P, name):
     """One vertex per launch slot, in sequence order, gives the same answer."""
     _check_golden(P, name, 0, keep=False, schedule=1)
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
+def test_level_schedule_against_golden(P, name):
+    """The vertices of one dependency level share launches, memory packed by
+    table lifetimes: the same answer as the dataflow launch."""
+    _check_golden(P, name, 0, keep=False, schedule=2)
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
+@pytest.mark.parametrize("lat_workers", [0, 1, 65535])
+def test_dataflow_schedule_against_golden(P, name, lat_workers):
+    """The one-launch dataflow schedule with the default worker split, with
+    one latency worker, and with every workgroup but one serving the latency
+    queue first."""
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=3, lat_workers=lat_workers)
+
+
+def test_workloads_run_the_lane_schedule(P):
+    """The default schedule runs the lanes (the workloads fit the resident
+    layout) and puts chains of the Transformer off the caller's stream."""
+    for name in ("w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"):
+        g = workload(name)
+        pg, _, _ = _run(P, g, keep=False)
+        assert pg.stats()["schedule"] == 0, name
+    lanes = [pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))]
+    assert 0 < sum(1 for x in lanes if x) < len(lanes)
 
 
 @pytest.mark.skip(reason="captured HIP-graph replay of the search was removed: its first GPU run "
