@@ -97,13 +97,19 @@ typedef enum {
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
     PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats) */
-    PASE_OPT_SCHEDULE = 6,      /* 0 (default): dataflow -- one persistent launch runs the prep,
-                                   fill and reduction work of every vertex as soon as the tables
-                                   it reads are complete (device-side dependency counters); needs
-                                   every table resident at once, else falls back to 2.
-                                   1: one vertex at a time in sequence order.  2: vertices of one
-                                   dependency level (whose tables do not read each other) share
-                                   their kernel launches.  1 and 2 pack table memory by lifetimes. */
+    PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
+                                   do not read each other) share their kernel launches, one
+                                   stream, table memory packed by lifetimes.  1: one vertex at a
+                                   time in sequence order (same packing).  2: lanes -- the
+                                   tables' reader tree cut into chains that run on three streams
+                                   (the latency-bound chain at the highest wave priority), level
+                                   batches within each, events where a table is read across
+                                   lanes.  3: dataflow -- one persistent launch runs every prep,
+                                   fill and reduction workgroup as soon as the tables it reads
+                                   are complete (device-side dependency counters, two ticket
+                                   queues).  2 and 3 keep every table resident and fall back to 0
+                                   over the memory budget; 3 also when a vertex needs a fill
+                                   variant the persistent kernel does not carry. */
     PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
                                    vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
                                    that kernel runs (a tuning and test knob) */
@@ -139,9 +145,8 @@ typedef struct {
     double stream_fill_ms;     /* PASE_OPT_PROFILE: event time of those launches, a part of
                                   rows_fill_ms */
     uint32_t stream_launches;  /* PASE_OPT_PROFILE: their launches, a part of rows_launches */
-    uint32_t schedule;         /* schedule the search ran with: 0 = dataflow (one launch runs every
-                                  prep, fill and reduction; rows_fill_ms is its duration), 1 = one
-                                  vertex at a time, 2 = by dependency level */
+    uint32_t schedule;         /* schedule the search ran with (PASE_OPT_SCHEDULE values); with 3
+                                  rows_fill_ms is the duration of the one dataflow launch */
     uint32_t flow_grid;        /* dataflow: workgroups of the launch */
     uint32_t flow_lat_workers; /* dataflow: of them, latency workers */
     uint64_t flow_items;       /* dataflow: work items (prep, fill and reduction workgroups) */
@@ -254,7 +259,8 @@ typedef struct {
     uint32_t parts;      /* row kernel: waves sharing one tile's c range (1, 2 or 4) */
     double fill_ms;      /* PASE_OPT_PROFILE: event time of this vertex's fill kernel */
     uint32_t level;      /* dependency level: 1 + the largest level of the tables it reads */
-    uint32_t lane;       /* lane schedule: the stream it runs on (0 = the caller's, 1, 2) */
+    uint32_t lane;       /* lane schedule: the stream it runs on: 0 = the caller's, 1 = the latency-bound
+                            chain's (highest wave priority), 2 = the other chains' */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

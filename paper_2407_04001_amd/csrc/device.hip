@@ -97,6 +97,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restric
                                                      const uint64_t *__restrict__ sig,
                                                      const Contrib *__restrict__ cb, uint64_t r) {
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    set_priority(be[kb]);
     prep_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r);
 }
 
@@ -105,6 +106,7 @@ __global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ 
                                                   const BatchEntry *__restrict__ be, uint32_t nbe) {
     __shared__ MergeBuf<KeyT> xch;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    set_priority(be[kb]);
     rows_item<KeyT, TZ, TM, NA>(descs[be[kb].pos], blockIdx.x - be[kb].first, xch);
 }
 
@@ -112,6 +114,7 @@ template <typename KeyT>
 __global__ __launch_bounds__(256) void k_reduce_splits(const ReduceArgs *__restrict__ descs,
                                                       const BatchEntry *__restrict__ be, uint32_t nbe) {
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    set_priority(be[kb]);
     reduce_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first);
 }
 
@@ -119,6 +122,7 @@ template <typename KeyT, int NT>
 __global__ __launch_bounds__(256) void k_fill_generic(const GenericArgs *__restrict__ descs,
                                                      const BatchEntry *__restrict__ be, uint32_t nbe) {
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    set_priority(be[kb]);
     generic_item<KeyT, NT>(descs[be[kb].pos], blockIdx.x - be[kb].first);
 }
 
@@ -989,6 +993,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         for (int i : members) {
             hbe[nbe].pos = (uint32_t)i;
             hbe[nbe].first = b.blocks;
+            hbe[nbe].prio = use_lanes && P.v[i].lane == 1 ? 1u : 0u;
+            hbe[nbe].pad = 0;
             b.blocks += nblk(launches[i]);
             nbe++;
             b.nentries++;
@@ -1244,7 +1250,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
     if (!use_flow) g->stats.flow_grid = g->stats.flow_lat_workers = 0, g->stats.flow_items = 0;
-    g->stats.schedule = use_flow ? 3u : use_lanes ? 0u : (P.by_level ? 2u : 1u);
+    g->stats.schedule = use_flow ? 3u : use_lanes ? 2u : (P.by_level ? 0u : 1u);
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;
     if (g->profile && use_flow) {

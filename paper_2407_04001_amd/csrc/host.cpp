@@ -254,10 +254,12 @@ TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t n
 // vertex continues the chain of its reader when it is the reader's longest
 // producer path (planned fill time plus a launch latency per vertex), and
 // heads a chain of its own otherwise.  The chain through the root runs on
-// lane 0 (the caller's stream), the longest other chain on lane 1, every
-// other chain with substantial work on lane 2, and small chains on the lane
-// of the vertex that reads them.  Lanes are streams: the long chains of small
-// vertices then no longer queue behind large vertices they do not depend on.
+// lane 0 (the caller's stream); the longest other chain -- in a Transformer
+// graph, the encoder: a long run of small dependent vertices -- on lane 1,
+// whose waves issue at the highest priority; every other chain with
+// substantial work on lane 2; a chain with little work follows the lane of
+// the vertex that reads it.  Lanes are streams: the latency-bound chain then
+// no longer queues behind large vertices it does not depend on.
 static void assign_lanes(Plan &P) {
     const int n = (int)P.v.size();
     constexpr double kLaunchUs = 10.0, kLongUs = 200.0, kWorkUs = 50.0;
@@ -284,16 +286,12 @@ static void assign_lanes(Plan &P) {
     // chains are numbered by decreasing head position, so the chain of a
     // head's reader always has its lane already
     const int nc = (int)head.size();
-    std::vector<int> lane(nc, -1);
+    std::vector<int> lane(nc, 0);
     int second = -1;
     for (int c = 1; c < nc; c++)
         if (top[head[c]] >= kLongUs && (second < 0 || top[head[c]] > top[head[second]])) second = c;
-    for (int c = 0; c < nc; c++) {
-        if (c == 0) lane[c] = 0;
-        else if (c == second) lane[c] = 1;
-        else if (work[c] >= kWorkUs) lane[c] = 2;
-        else lane[c] = lane[chain[P.v[head[c]].consumer]];
-    }
+    for (int c = 1; c < nc; c++)
+        lane[c] = c == second ? 1 : work[c] >= kWorkUs ? 2 : lane[chain[P.v[head[c]].consumer]];
     for (int i = 0; i < n; i++) P.v[i].lane = lane[chain[i]];
 }
 

@@ -91,6 +91,8 @@ struct PrepArgs {
 struct BatchEntry {
     uint32_t pos;
     uint32_t first;
+    uint32_t prio;            // 1: the latency lane's work -- its waves issue before others
+    uint32_t pad;
 };
 
 struct ATerm {                // per-lane row term of the row kernel (key space)
@@ -193,7 +195,7 @@ struct SegDep {
 constexpr int kLatQ = 0, kBulkQ = 1;
 
 // PASE_OPT_SCHEDULE values
-enum SchedKind { kSchedLanes = 0, kSchedSeq = 1, kSchedLevel = 2, kSchedFlow = 3 };
+enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedLanes = 2, kSchedFlow = 3 };
 
 // Row-fill variants (columns per lane TZ, rows per lane TM, row terms NA) the
 // dataflow kernel carries: those that need at most ~96 VGPRs, so that the one
@@ -248,7 +250,7 @@ struct VPlan {
     // schedule
     int level = 0;                  // dependency level: 1 + max level of the tables it reads
     int slot = 0;                   // launch slot: its level (level schedule) or its position
-    int lane = 0;                   // lane schedule: stream 0 (the caller's), 1 or 2 (see assign_lanes)
+    int lane = 0;                   // lane schedule: 0 = the caller's stream, 1 = the latency chain's, 2 = other
 };
 
 struct Plan {

@@ -94,6 +94,13 @@ __device__ __forceinline__ uint32_t batch_find(const BatchEntry *__restrict__ be
     return __builtin_amdgcn_readfirstlane(lo);
 }
 
+// Work of the latency lane (the chain of small dependent vertices of the lane
+// schedule) runs its waves at the highest issue priority: on a SIMD shared
+// with the long fills of another stream they then issue first.
+__device__ __forceinline__ void set_priority(const BatchEntry &e) {
+    if (e.prio) __builtin_amdgcn_s_setprio(3);
+}
+
 // One workgroup handles kPrepThreads consecutive (c, column) elements of one
 // outer index of one block, so the block, its contributions and the outer
 // digits are uniform across the workgroup (scalar loads); lanes differ only in

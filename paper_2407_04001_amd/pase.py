@@ -282,7 +282,10 @@ class Graph:
             self._ws = None
 
     def __del__(self):
-        self.close()
+        try:
+            self.close()
+        except (TypeError, AttributeError):   # interpreter shutdown: module globals are gone
+            pass
 
     def enumerate_configs(self, p: int):
         """Enumerate configurations and plan the search for p devices; the

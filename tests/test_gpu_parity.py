@@ -315,10 +315,11 @@ def test_sequential_schedule_against_golden(P, name):
 
 
 @pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
-def test_level_schedule_against_golden(P, name):
-    """The vertices of one dependency level share launches, memory packed by
-    table lifetimes: the same answer as the dataflow launch."""
+def test_lane_schedule_against_golden(P, name):
+    """Chains of the tables' reader tree on three streams, every table
+    resident: the same answer as the level schedule."""
     _check_golden(P, name, 0, keep=False, schedule=2)
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=2)
 
 
 @pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
@@ -330,13 +331,15 @@ def test_dataflow_schedule_against_golden(P, name, lat_workers):
     _check_golden(P, name, 0, keep=True, samples=False, schedule=3, lat_workers=lat_workers)
 
 
-def test_workloads_run_the_lane_schedule(P):
-    """The default schedule runs the lanes (the workloads fit the resident
-    layout) and puts chains of the Transformer off the caller's stream."""
+def test_workloads_run_the_requested_schedule(P):
+    """The workloads fit the resident layout: the lane and dataflow schedules
+    run as requested, and the lanes put chains of the Transformer off the
+    caller's stream."""
     for name in ("w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"):
         g = workload(name)
-        pg, _, _ = _run(P, g, keep=False)
-        assert pg.stats()["schedule"] == 0, name
+        for sched in (0, 1, 2, 3):
+            pg, _, _ = _run(P, g, keep=False, schedule=sched)
+            assert pg.stats()["schedule"] == sched, (name, sched)
     lanes = [pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))]
     assert 0 < sum(1 for x in lanes if x) < len(lanes)
 
