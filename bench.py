@@ -74,20 +74,91 @@ def copy_calibration(mib):
 
 def traffic_from_profile():
     """HBM bytes per launch of the row kernel from the committed counter
-    summary, if it was taken on the current kernel source; else None."""
-    import hashlib
+    summary, if it was taken on the current kernel sources; else None."""
+    from paper_2407_04001_amd.profiling import kernel_source_digest
     path = os.path.join(ROOT, "profiles", "k_fill_rows_hbm_traffic.json")
-    src = os.path.join(ROOT, "paper_2407_04001_amd", "csrc", "device.hip")
     try:
         with open(path) as f:
             prof = json.load(f)
-        with open(src, "rb") as f:
-            digest = hashlib.sha256(f.read()).hexdigest()
+        digest = kernel_source_digest(ROOT)
     except OSError:
         return None
-    if prof.get("device_hip_sha256") != digest:
+    if prof.get("kernel_sources_sha256") != digest:
         return None
     return prof.get("bytes_per_launch")
+
+
+WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
+
+
+def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu):
+    """Time `steps` whole searches of one workload; returns the report dict
+    (the oracle timed on the same graph: the whole search when it has at most
+    `cpu_cells` cells, else a prefix of the vertex order)."""
+    import torch
+    from paper_2407_04001_amd import OPT_PROFILE, Graph
+    from workloads import workload
+
+    g = workload(name, seed)
+    p = g["p"]
+    pg = Graph(g)
+    pg.enumerate_configs(p)
+    pg.set_option(OPT_PROFILE, 1)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pg.enumerate_configs(p)
+        return pg.find_best_strategy(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    walls, rows_ms, rows_launches, fill_ms = [], 0.0, 0, 0.0
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        mc, strat = step()
+        st = pg.stats()
+        walls.append(st["wall_ms"])
+        # the dominant kernel: the row kernel with a column chunk per lane (its
+        # column-less, memory-streaming form is reported apart)
+        rows_ms += st["rows_fill_ms"] - st["stream_fill_ms"]
+        fill_ms += st["fill_ms"]
+        rows_launches += st["rows_launches"] - st["stream_launches"]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    cells = st["cells"]
+    col_cells = st["rows_cells"] - st["stream_cells"]
+    achieved = OPS_PER_CELL * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
+    parity = None
+    gold_path = os.path.join(ROOT, "tests", "golden", f"{name}_seed{seed}.json")
+    if os.path.exists(gold_path):
+        with open(gold_path) as f:
+            gold = json.load(f)
+        parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
+    out = {
+        "metric": METRIC, "value": cells * steps / elapsed, "unit": "cell-updates/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup,
+        "ms_per_step": elapsed * 1e3 / steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
+        "config": {"workload": g["name"], "p": p, "vertices": len(g["vertices"]),
+                   "edges": len(g["edges"]), "cells": cells, "seed": seed},
+        "find_best_strategy_ms": sum(walls) / len(walls),
+        "fill_ms_per_step": fill_ms / steps,
+        "fill_cells_per_s": cells / (fill_ms / steps / 1e3) if fill_ms else None,
+        "min_cost": mc, "parity_with_oracle": parity,
+        "roofline": {"bound": "alu", "kernel": "k_fill_rows",
+                     "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
+                     "frac": achieved / FP64_OPS_PEAK_T,
+                     "traffic": traffic_from_profile() if name == "w4_transformer" else None,
+                     "launches_per_step": rows_launches // steps,
+                     "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
+                     "cells_per_step": col_cells},
+    }
+    if not no_cpu:
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells))
+    return out
 
 
 def main():
@@ -101,6 +172,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (HBM counter calibration)")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="one JSON line per synthetic workload (W0..W4) instead of the W4 line")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -111,73 +184,12 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2407_04001_amd import OPT_PROFILE, Graph
-    from workloads import workload
-
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    g = workload(args.workload, args.seed)
-    p = g["p"]
-    pg = Graph(g)
-    pg.enumerate_configs(p)
-    pg.set_option(OPT_PROFILE, 1)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        pg.enumerate_configs(p)
-        return pg.find_best_strategy(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    walls, rows_ms, rows_launches, fill_ms = [], 0.0, 0, 0.0
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        mc, strat = step()
-        st = pg.stats()
-        walls.append(st["wall_ms"])
-        # the dominant kernel: the row kernel with a column chunk per lane (its
-        # column-less, memory-streaming form is reported apart)
-        rows_ms += st["rows_fill_ms"] - st["stream_fill_ms"]
-        fill_ms += st["fill_ms"]
-        rows_launches += st["rows_launches"] - st["stream_launches"]
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-
-    cells = st["cells"]
-    value = cells * args.steps / elapsed
-    col_cells = st["rows_cells"] - st["stream_cells"]
-    achieved = OPS_PER_CELL * col_cells * args.steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
-
-    parity = None
-    gold_path = os.path.join(ROOT, "tests", "golden", f"{args.workload}_seed{args.seed}.json")
-    if os.path.exists(gold_path):
-        with open(gold_path) as f:
-            gold = json.load(f)
-        parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
-
-    out = {
-        "metric": METRIC, "value": value, "unit": "cell-updates/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": elapsed * 1e3 / args.steps,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
-        "config": {"workload": g["name"], "p": p, "vertices": len(g["vertices"]),
-                   "edges": len(g["edges"]), "cells": cells, "seed": args.seed},
-        "find_best_strategy_ms": sum(walls) / len(walls),
-        "fill_ms_per_step": fill_ms / args.steps,
-        "fill_cells_per_s": cells / (fill_ms / args.steps / 1e3) if fill_ms else None,
-        "min_cost": mc, "parity_with_oracle": parity,
-        "roofline": {"bound": "alu", "kernel": "k_fill_rows",
-                     "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
-                     "frac": achieved / FP64_OPS_PEAK_T, "traffic": traffic_from_profile(),
-                     "launches_per_step": rows_launches // args.steps,
-                     "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
-                     "cells_per_step": col_cells},
-    }
-    if not args.no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(args.cpu_cells))
-    print(json.dumps(out), flush=True)
+    names = WORKLOADS if args.all_workloads else [args.workload]
+    for name in names:
+        out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu)
+        print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

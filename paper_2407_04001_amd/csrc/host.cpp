@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstring>
 #include <numeric>
+#include <unordered_map>
 
 #include "internal.h"
 
@@ -142,18 +143,21 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
     auto has = [&](size_t v, size_t u) { return (d[v * W + u / 64] >> (u % 64)) & 1ull; };
     for (size_t v = 0; v < n; v++)
         for (int u : g->nbr[v]) d[v * W + u / 64] |= 1ull << (u % 64);
+    // |u.d| is kept per vertex and recounted only when u.d changes
+    auto count = [&](size_t u) {
+        int sz = 0;
+        for (size_t w = 0; w < W; w++) sz += __builtin_popcountll(d[u * W + w]);
+        return sz;
+    };
+    std::vector<int> size(n);
+    for (size_t u = 0; u < n; u++) size[u] = count(u);
     std::vector<char> done(n, 0);
     seq.clear();
     Dpos.assign(n, {});
     for (size_t i = 0; i < n; i++) {
         size_t best = n;
-        int best_sz = 0;
-        for (size_t u = 0; u < n; u++) {
-            if (done[u]) continue;
-            int sz = 0;
-            for (size_t w = 0; w < W; w++) sz += __builtin_popcountll(d[u * W + w]);
-            if (best == n || sz < best_sz) { best = u; best_sz = sz; }
-        }
+        for (size_t u = 0; u < n; u++)
+            if (!done[u] && (best == n || size[u] < size[best])) best = u;
         const size_t vi = best;
         done[vi] = 1;
         seq.push_back((int)vi);
@@ -163,6 +167,7 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
             for (size_t w = 0; w < W; w++) d[(size_t)v * W + w] |= d[vi * W + w];
             d[(size_t)v * W + vi / 64] &= ~(1ull << (vi % 64));
             if (g->seq_rule == 0) d[(size_t)v * W + v / 64] &= ~(1ull << (v % 64));
+            size[v] = count((size_t)v);
         }
     }
 }
@@ -247,6 +252,35 @@ TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t n
     return best;
 }
 
+// Vertices of one graph often share a shape (the layers of a stack): the tile
+// model is evaluated once per distinct argument tuple.
+TileTime tile_time_cached(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t na, uint32_t tz, uint32_t tm,
+                          uint32_t force_parts, uint32_t force_splits) {
+    struct Key {
+        uint64_t MO, MR;
+        uint32_t Kz, K, na, tz, tm, parts, splits;
+        bool operator==(const Key &o) const {
+            return MO == o.MO && MR == o.MR && Kz == o.Kz && K == o.K && na == o.na && tz == o.tz && tm == o.tm &&
+                   parts == o.parts && splits == o.splits;
+        }
+    };
+    struct Hash {
+        size_t operator()(const Key &k) const {
+            uint64_t h = k.MO * 0x9E3779B97F4A7C15ull ^ (k.MR + 0x632BE59BD9B4E019ull);
+            for (uint32_t x : {k.Kz, k.K, k.na, k.tz, k.tm, k.parts, k.splits}) h = (h ^ x) * 0x100000001B3ull;
+            return (size_t)h;
+        }
+    };
+    thread_local std::unordered_map<Key, TileTime, Hash> memo;
+    const Key key{MO, MR, Kz, K, na, tz, tm, force_parts, force_splits};
+    auto it = memo.find(key);
+    if (it != memo.end()) return it->second;
+    if (memo.size() > 65536) memo.clear();
+    const TileTime t = tile_time(MO, MR, Kz, K, na, tz, tm, force_parts, force_splits);
+    memo.emplace(key, t);
+    return t;
+}
+
 }  // namespace
 
 // Lane schedule.  The tables form an in-tree: every table but the last has
@@ -305,6 +339,12 @@ static pase_status build_plan(pase_graph_t g) {
     for (int i = 0; i < n; i++) P.pos[P.seq[i]] = i;
     P.v.assign(n, VPlan());
 
+    // edges of each vertex, in edge order
+    std::vector<std::vector<int>> incident(n);
+    for (size_t k = 0; k < g->E.size(); k++) {
+        incident[g->E[k].src].push_back((int)k);
+        incident[g->E[k].dst].push_back((int)k);
+    }
     // components of the graph induced on positions < i, grown one position at
     // a time (union-find over vertex ids); each set remembers its last position
     std::vector<int> uf(n), last(n, -1), seen(n, -1);
@@ -357,10 +397,10 @@ static pase_status build_plan(pase_graph_t g) {
                 if (a != b) uf[a] = b;
             }
         last[find(vp.vi)] = i;
-        for (size_t k = 0; k < g->E.size(); k++) {
+        for (int k : incident[vp.vi]) {
             const auto &d = g->E[k];
-            int other = (int)d.src == vp.vi ? (int)d.dst : ((int)d.dst == vp.vi ? (int)d.src : -1);
-            if (other >= 0 && P.pos[other] > i) vp.edges.push_back((int)k);
+            const int other = (int)d.src == vp.vi ? (int)d.dst : (int)d.src;
+            if (P.pos[other] > i) vp.edges.push_back(k);
         }
         P.cells += vp.N * vp.K;
         P.entries += vp.N;
@@ -439,7 +479,8 @@ static pase_status build_plan(pase_graph_t g) {
                         if (g->schedule == kSchedFlow && !g->tile_rows && !g->tile_cols &&
                             !flow_rows_ok(false, tz, tm, std::min<uint32_t>(na, 4)))
                             continue;
-                        const TileTime tt = tile_time(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts, g->c_splits);
+                        const TileTime tt = tile_time_cached(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts,
+                                                             g->c_splits);
                         if (!rc.ok || tt.us < rc.cost) {
                             rc.ok = true;
                             rc.cost = tt.us;

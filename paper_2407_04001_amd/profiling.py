@@ -151,7 +151,7 @@ def report(trace_dir, fetch_dir, write_dir, cfetch_dir, cwrite_dir, valu_dir, wo
     L.append(f"# Kernel profile: {workload} strategy search on one MI355X\n")
     L.append(f"{cells:.3e} DP cell updates per search. Summary written by "
              "`python -m paper_2407_04001_amd.profiling report` from the rocprofv3 output of the commands below "
-             f"(kernel source sha256 `{src_hash[:16]}…`).\n")
+             f"(kernel sources sha256 `{src_hash[:16]}…`).\n")
     L.append("## Kernel time (rocprofv3 kernel trace)\n")
     L.append("Command (from the repository root, after `cd /tmp && export TMPDIR=/tmp`):\n")
     L.append(f"    {commands['trace']}\n")
@@ -202,7 +202,7 @@ def report(trace_dir, fetch_dir, write_dir, cfetch_dir, cwrite_dir, valu_dir, wo
         L.append(f"| all column-form launches of one search | | {tot_act * 4 / (1024 * tot_gui):.2f} | {tot_add:.3e} | "
                  f"{tot_valu:.3e} | {tot_valu / tot_add:.2f} |")
     L.append("")
-    rec = {"kernel": "k_fill_rows (column form, TZ > 1)", "workload": workload, "device_hip_sha256": src_hash,
+    rec = {"kernel": "k_fill_rows (column form, TZ > 1)", "workload": workload, "kernel_sources_sha256": src_hash,
            "bytes_per_launch": (f_col + w_col) / n_col, "fetch_bytes_per_search": f_col,
            "write_bytes_per_search": w_col, "launches_per_search": n_col,
            "copy_calibration": {"FETCH_SIZE": kf, "WRITE_SIZE": kw},
@@ -210,12 +210,24 @@ def report(trace_dir, fetch_dir, write_dir, cfetch_dir, cwrite_dir, valu_dir, wo
     return "\n".join(L) + "\n", rec
 
 
+KERNEL_SOURCES = ("device.hip", "kernels.h", "internal.h", "flow.hip")
+
+
+def kernel_source_digest(root: str) -> str:
+    """sha256 over the device-code sources, in a fixed order: a counter
+    record is valid for the kernels only while this digest matches."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(root, "paper_2407_04001_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def write_report(prof_dir: str, root: str, workload: str, cells: float, commands: dict):
     """Write profiles/k_fill_rows_<workload>.md and the traffic record from the
     six rocprofv3 output directories under prof_dir (kt, fetch, write,
     cfetch, cwrite, valu)."""
-    src = os.path.join(root, "paper_2407_04001_amd", "csrc", "device.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    digest = kernel_source_digest(root)
     sub = {k: os.path.join(prof_dir, k) for k in ("kt", "fetch", "write", "cfetch", "cwrite", "valu")}
     md, rec = report(sub["kt"], sub["fetch"], sub["write"], sub["cfetch"], sub["cwrite"], sub["valu"],
                      workload, cells, digest, commands)
