@@ -44,10 +44,11 @@ def _load(path: str | None = None):
     L.oracle_error.restype = C.c_char_p
     L.oracle_error.argtypes = [P]
     L.oracle_configs.argtypes = [P, I]
+    L.oracle_configs_all.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
     L.oracle_num_configs.argtypes = [P, I]
-    L.oracle_config_exponents.argtypes = [P, I, I, P]
+    L.oracle_config_splits.argtypes = [P, I, I, P]
     L.oracle_layer_costs.argtypes = [P, I, P]
     L.oracle_edge_costs.argtypes = [P, I, P]
     L.oracle_sequence.argtypes = [P, P]
@@ -123,19 +124,30 @@ class Oracle:
         return rc
 
     # -- configurations and costs
-    def configs(self, p: int):
-        self._check(self._L.oracle_configs(self._h, int(p)))
+    def configs(self, p: int, all_integers: bool = False):
+        """C(v) for p devices: power-of-two splits (p = 2^L), or with
+        all_integers every tuple of positive integers with product <= p."""
+        fn = self._L.oracle_configs_all if all_integers else self._L.oracle_configs
+        self._check(fn(self._h, int(p)))
         self.p = p
         self.K = np.array([self._L.oracle_num_configs(self._h, v) for v in range(self.nv)])
         return self.K
 
-    def exponents(self, v: int) -> np.ndarray:
-        out = np.zeros((int(self.K[v]), int(self.ndims[v])), dtype=np.uint8)
-        buf = np.zeros(MAXD, dtype=np.uint8)
+    def splits(self, v: int) -> np.ndarray:
+        """Split factors of every configuration of v, in index order."""
+        out = np.zeros((int(self.K[v]), int(self.ndims[v])), dtype=np.uint32)
+        buf = np.zeros(MAXD, dtype=np.uint32)
         for c in range(int(self.K[v])):
-            self._check(self._L.oracle_config_exponents(self._h, v, c, _ptr(buf)))
+            self._check(self._L.oracle_config_splits(self._h, v, c, _ptr(buf)))
             out[c] = buf[:self.ndims[v]]
         return out
+
+    def exponents(self, v: int) -> np.ndarray:
+        """log2 of the split factors (power-of-two configurations)."""
+        sp = self.splits(v)
+        ex = np.log2(sp).astype(np.uint8)
+        assert np.array_equal(np.left_shift(1, ex.astype(np.uint32)), sp), "not powers of two"
+        return ex
 
     def layer_costs(self, v: int) -> np.ndarray:
         out = np.zeros(int(self.K[v]), dtype=np.uint64)

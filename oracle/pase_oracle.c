@@ -6,9 +6,10 @@
  * benchmark's CPU-baseline leg may load this file's library.  It shares no
  * code with the HIP library and is deliberately slow and literal:
  *
- *   - configurations: Sec. II, C(v) = {c : prod c_k <= p}, restricted to powers
- *     of two, enumerated in lexicographic order of the exponent tuple
- *     (first loop dim slowest);
+ *   - configurations: Sec. II, C(v) = {c : prod c_k <= p}, either every tuple
+ *     of positive integers (oracle_configs_all) or only powers of two
+ *     (oracle_configs, p = 2^L), enumerated in lexicographic order of the
+ *     split tuple (first loop dim slowest);
  *   - cost function F: eq. (1), with the integer layer / transfer cost model
  *     documented at layer_cost() and transfer_cost();
  *   - vertex ordering: GenerateSeq, Fig. 3 (argmin of |u.d|, ties to the
@@ -45,9 +46,9 @@ typedef struct {
     uint64_t *elems;         /* ne */
     uint64_t r;              /* FLOP-to-byte ratio weighting communication */
     /* configurations */
-    int p, log2p;
+    int p;
     int *K;                  /* configs per vertex */
-    uint8_t **ex;            /* ex[v][c*ndims+k] = exponent of the split of dim k */
+    uint32_t **sp;           /* sp[v][c*ndims+k] = split factor of dim k */
     /* cost tables */
     uint64_t **Lc;           /* Lc[v][c]       = t_l(v, c)            */
     uint64_t **Rx;           /* Rx[e][cu*Kv+cv] = r * t_x(e, cu, cv)  */
@@ -138,9 +139,9 @@ static void free_tables(oracle_t *o) {
 
 static void free_configs(oracle_t *o) {
     if (o->K) {
-        for (int v = 0; v < o->nv; v++) { free(o->ex[v]); free(o->Lc[v]); }
+        for (int v = 0; v < o->nv; v++) { free(o->sp[v]); free(o->Lc[v]); }
         for (int e = 0; e < o->ne; e++) free(o->Rx[e]);
-        free(o->ex); free(o->Lc); free(o->Rx); free(o->K);
+        free(o->sp); free(o->Lc); free(o->Rx); free(o->K);
         o->K = NULL;
     }
 }
@@ -158,24 +159,22 @@ void oracle_free(oracle_t *o) {
 
 /* --------------------------------------------------------- configurations */
 
-/* Append every exponent tuple with sum <= budget, dims k..d-1 free, in
- * lexicographic order (dim 0 slowest). */
-static void enum_rec(int d, int k, int budget, uint8_t *cur, uint8_t *out, int *count) {
+/* Append every split tuple of dims k..d-1 in lexicographic order (dim 0
+ * slowest): with `pow2`, the powers of two with product <= budget, else every
+ * positive integer tuple with product <= budget (out = NULL: count only).
+ * Returns 0 when more than `cap` tuples would be produced. */
+static int enum_rec(int d, int k, uint64_t budget, int pow2, uint32_t *cur, uint32_t *out, int *count, int cap) {
     if (k == d) {
-        memcpy(out + (size_t)(*count) * d, cur, d);
+        if (*count >= cap) return 0;
+        if (out) memcpy(out + (size_t)(*count) * d, cur, d * sizeof(uint32_t));
         (*count)++;
-        return;
+        return 1;
     }
-    for (int e = 0; e <= budget; e++) {
-        cur[k] = (uint8_t)e;
-        enum_rec(d, k + 1, budget - e, cur, out, count);
+    for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {
+        cur[k] = (uint32_t)s;
+        if (!enum_rec(d, k + 1, budget / s, pow2, cur, out, count, cap)) return 0;
     }
-}
-
-static uint64_t binom(int n, int k) {
-    uint64_t r = 1;
-    for (int i = 1; i <= k; i++) r = r * (uint64_t)(n - k + i) / (uint64_t)i;
-    return r;
+    return 1;
 }
 
 /* Layer cost t_l(v, c): compute time plus r times the intra-layer
@@ -185,17 +184,17 @@ static uint64_t binom(int n, int k) {
  *                                                 / prod_{k not in reduce} s_k)
  *   t_l     = compute + r * comm
  * (comm is the partial-sum reduction a split contraction dim requires.) */
-static int layer_cost(oracle_t *o, int v, const uint8_t *e, uint64_t *out) {
+static int layer_cost(oracle_t *o, int v, const uint32_t *s, uint64_t *out) {
     uint64_t flops = o->fpp[v], P = 1, red_split = 1, keep_n = 1, keep_split = 1;
     for (int k = 0; k < o->ndims[v]; k++) {
-        uint64_t n = o->size[v * MAXD + k], s = (uint64_t)1 << e[k];
+        uint64_t n = o->size[v * MAXD + k];
         if (!mul_ok(flops, n, &flops)) return 0;
-        P *= s;
+        P *= s[k];
         if (o->reduce_mask[v] >> k & 1u) {
-            red_split *= s;
+            red_split *= s[k];
         } else {
             if (!mul_ok(keep_n, n, &keep_n)) return 0;
-            keep_split *= s;
+            keep_split *= s[k];
         }
     }
     uint64_t compute = ceil_div(flops, P);
@@ -210,48 +209,49 @@ static int layer_cost(oracle_t *o, int v, const uint8_t *e, uint64_t *out) {
 /* r * t_x(u, v): zero when both endpoints split every dim of the tensor the
  * same way, otherwise the tensor is re-distributed: ceil(elems / max(P_u, P_v))
  * words per device, weighted by r.  Symmetric in (u, v) as the paper requires. */
-static int transfer_cost(oracle_t *o, int e, const uint8_t *eu, const uint8_t *ev, uint64_t *out) {
+static int transfer_cost(oracle_t *o, int e, const uint32_t *su_, const uint32_t *sv_, uint64_t *out) {
     int u = o->src[e], v = o->dst[e];
     int match = 1;
     for (int k = 0; k < o->rank[e]; k++) {
         int a = o->src_dim[e * MAXD + k], b = o->dst_dim[e * MAXD + k];
-        uint64_t su = a >= 0 ? (uint64_t)1 << eu[a] : 1;
-        uint64_t sv = b >= 0 ? (uint64_t)1 << ev[b] : 1;
+        uint64_t su = a >= 0 ? su_[a] : 1;
+        uint64_t sv = b >= 0 ? sv_[b] : 1;
         if (su != sv) match = 0;
     }
     if (match) { *out = 0; return 1; }
     uint64_t Pu = 1, Pv = 1;
-    for (int k = 0; k < o->ndims[u]; k++) Pu *= (uint64_t)1 << eu[k];
-    for (int k = 0; k < o->ndims[v]; k++) Pv *= (uint64_t)1 << ev[k];
+    for (int k = 0; k < o->ndims[u]; k++) Pu *= su_[k];
+    for (int k = 0; k < o->ndims[v]; k++) Pv *= sv_[k];
     uint64_t words = ceil_div(o->elems[e], Pu > Pv ? Pu : Pv);
     return mul_ok(o->r, words, out);
 }
 
-/* Enumerate C(v) for every v and fill the cost tables. p must be 2^L. */
-int oracle_configs(oracle_t *o, int p) {
+/* Enumerate C(v) for every v and fill the cost tables. */
+static int configs(oracle_t *o, int p, int pow2) {
     free_tables(o);
     free_configs(o);
     o->solved = 0;
-    if (p < 1 || (p & (p - 1))) return fail(o, "p must be a power of two");
-    int L = 0;
-    while ((1 << L) < p) L++;
-    o->p = p; o->log2p = L;
+    if (p < 1) return fail(o, "p must be positive");
+    if (pow2 && (p & (p - 1))) return fail(o, "p must be a power of two");
+    o->p = p;
     o->K = calloc(o->nv, sizeof(int));
-    o->ex = calloc(o->nv, sizeof(uint8_t *));
+    o->sp = calloc(o->nv, sizeof(uint32_t *));
     o->Lc = calloc(o->nv, sizeof(uint64_t *));
     o->Rx = calloc(o->ne + 1, sizeof(uint64_t *));
+    const int cap = 65535;   /* argmins are uint16 */
     for (int v = 0; v < o->nv; v++) {
         int d = o->ndims[v];
-        uint64_t cnt = binom(L + d, d);
-        if (cnt > 65535) return fail(o, "too many configurations for a uint16 argmin");
-        o->ex[v] = calloc(cnt * d, 1);
-        uint8_t cur[MAXD];
+        uint32_t cur[MAXD];
         int count = 0;
-        enum_rec(d, 0, L, cur, o->ex[v], &count);
+        if (!enum_rec(d, 0, (uint64_t)p, pow2, cur, NULL, &count, cap))
+            return fail(o, "too many configurations for a uint16 argmin");
+        o->sp[v] = calloc((size_t)count * d, sizeof(uint32_t));
+        count = 0;
+        enum_rec(d, 0, (uint64_t)p, pow2, cur, o->sp[v], &count, cap);
         o->K[v] = count;
         o->Lc[v] = calloc(count, sizeof(uint64_t));
         for (int c = 0; c < count; c++)
-            if (!layer_cost(o, v, o->ex[v] + (size_t)c * d, &o->Lc[v][c]))
+            if (!layer_cost(o, v, o->sp[v] + (size_t)c * d, &o->Lc[v][c]))
                 return fail(o, "layer cost overflows uint64");
     }
     for (int e = 0; e < o->ne; e++) {
@@ -259,13 +259,19 @@ int oracle_configs(oracle_t *o, int p) {
         o->Rx[e] = calloc((size_t)o->K[u] * o->K[v], sizeof(uint64_t));
         for (int cu = 0; cu < o->K[u]; cu++)
             for (int cv = 0; cv < o->K[v]; cv++)
-                if (!transfer_cost(o, e, o->ex[u] + (size_t)cu * o->ndims[u],
-                                   o->ex[v] + (size_t)cv * o->ndims[v],
+                if (!transfer_cost(o, e, o->sp[u] + (size_t)cu * o->ndims[u],
+                                   o->sp[v] + (size_t)cv * o->ndims[v],
                                    &o->Rx[e][(size_t)cu * o->K[v] + cv]))
                     return fail(o, "transfer cost overflows uint64");
     }
     return 0;
 }
+
+/* Power-of-two splits only, p = 2^L. */
+int oracle_configs(oracle_t *o, int p) { return configs(o, p, 1); }
+
+/* Every tuple of positive integers with product <= p (Sec. II's C(v)). */
+int oracle_configs_all(oracle_t *o, int p) { return configs(o, p, 0); }
 
 /* Replace the cost tables by caller-given ones (tests with random costs).
  * layer: concatenation of K_v values per vertex; edge: concatenation of the
@@ -558,9 +564,9 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
 /* --------------------------------------------------------- getters */
 
 int oracle_num_configs(oracle_t *o, int v) { return o->K ? o->K[v] : -1; }
-int oracle_config_exponents(oracle_t *o, int v, int c, uint8_t *out) {
+int oracle_config_splits(oracle_t *o, int v, int c, uint32_t *out) {
     if (!o->K || c < 0 || c >= o->K[v]) return 1;
-    memcpy(out, o->ex[v] + (size_t)c * o->ndims[v], o->ndims[v]);
+    memcpy(out, o->sp[v] + (size_t)c * o->ndims[v], o->ndims[v] * sizeof(uint32_t));
     return 0;
 }
 int oracle_layer_costs(oracle_t *o, int v, uint64_t *out) {

@@ -79,6 +79,155 @@ def test_p_must_be_power_of_two():
         o.configs(6)
 
 
+
+# ------------------------------------------------------------------ all-integer configurations
+def _one_vertex(d, p, size=7):
+    return {"name": "one", "p": p, "comm_weight": 8,
+            "vertices": [{"name": "v", "dims": [size] * d, "dim_names": ["x"] * d, "reduce": [],
+                          "flops_per_point": 1}], "edges": []}
+
+
+def _divisor_power_count(p, d):
+    """Number of d-tuples of positive integers with product <= p, by the
+    recurrence N_d(p) = sum_{s=1..p} N_{d-1}(floor(p/s)), N_0 = 1 (the first
+    factor s leaves floor(p/s) for the product of the others)."""
+    if d == 0:
+        return 1
+    return sum(_divisor_power_count(p // s, d - 1) for s in range(1, p + 1))
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+@pytest.mark.parametrize("p", [1, 2, 3, 5, 6, 12])
+def test_all_integer_config_count_and_order(d, p):
+    """C(v) with every positive-integer split: exactly the tuples with product
+    <= p (exhaustive over [1, p]^d), each once, lexicographic with dim 0
+    slowest; the count agrees with the divisor-sum recurrence (p = 12, d = 2:
+    sum of the divisor counts of 1..12 = 35)."""
+    from oracle.oracle import Oracle
+    o = Oracle(_one_vertex(d, p))
+    K = o.configs(p, all_integers=True)
+    sp = [tuple(int(x) for x in row) for row in o.splits(0)]
+    brute = [t for t in itertools.product(range(1, p + 1), repeat=d) if math.prod(t) <= p]
+    assert sp == brute
+    assert int(K[0]) == len(brute) == _divisor_power_count(p, d)
+    if (p, d) == (12, 2):
+        assert int(K[0]) == 35
+
+
+def test_all_integer_contains_the_power_of_two_set():
+    """At p = 2^L the power-of-two configurations are the all-integer ones whose
+    factors are all powers of two, in the same relative order, with the same
+    layer costs."""
+    from oracle.oracle import Oracle
+    g = fc_chain(p=8)
+    a, b = Oracle(g), Oracle(g)
+    a.configs(8)
+    b.configs(8, all_integers=True)
+    sa = [tuple(int(x) for x in r) for r in a.splits(0)]
+    sb = [tuple(int(x) for x in r) for r in b.splits(0)]
+    pw = [t for t in sb if all(x & (x - 1) == 0 for x in t)]
+    assert sa == pw
+    La, Lb = a.layer_costs(0), b.layer_costs(0)
+    for i, t in enumerate(sa):
+        assert int(La[i]) == int(Lb[sb.index(t)])
+
+
+def test_all_integer_p_limits():
+    """p = 1 leaves the single unsplit configuration; p < 1 is rejected; a
+    configuration count above the uint16 argmin range is rejected."""
+    from oracle.oracle import Oracle, OracleError
+    o = Oracle(_one_vertex(3, 1))
+    assert o.configs(1, all_integers=True).tolist() == [1]
+    assert o.splits(0).tolist() == [[1, 1, 1]]
+    with pytest.raises(OracleError):
+        o.configs(0, all_integers=True)
+    with pytest.raises(OracleError):
+        Oracle(_one_vertex(4, 1)).configs(1000, all_integers=True)   # N_4(1000) > 65535
+
+
+def test_layer_cost_non_power_of_two_hand_values():
+    """FC (64, 256, 256) = 8 388 608 FLOPs, contraction over `in`, r = 8, p = 6:
+    (3,1,1): ceil(8388608/3) = 2 796 203;  (1,1,3): 2 796 203 + 8*2*16384 = 3 058 347;
+    (2,3,1): ceil(8388608/6) = 1 398 102;  (1,2,3): 1 398 102 + 8*2*8192 = 1 529 174;
+    (1,5,1): ceil(8388608/5) = 1 677 722.
+    Ragged dims (3, 5), contraction over dim 1, 45 FLOPs, p = 6:
+    (3,2): 8 + 8*1*1 = 16;  (1,5): 9 + 8*4*3 = 105;  (5,1): 9;  (2,3): 8 + 8*2*2 = 40."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain(p=6))
+    o.configs(6, all_integers=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    L = o.layer_costs(0)
+    want = {(3, 1, 1): 2_796_203, (1, 1, 3): 3_058_347, (2, 3, 1): 1_398_102,
+            (1, 2, 3): 1_529_174, (1, 5, 1): 1_677_722}
+    for t, v in want.items():
+        assert int(L[sp.index(t)]) == v, t
+    g = {"name": "r", "p": 6, "comm_weight": 8,
+         "vertices": [{"name": "v", "dims": [3, 5], "dim_names": ["a", "b"], "reduce": [1],
+                       "flops_per_point": 3}], "edges": []}
+    o = Oracle(g)
+    o.configs(6, all_integers=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    L = o.layer_costs(0)
+    for t, v in {(3, 2): 16, (1, 5): 105, (5, 1): 9, (2, 3): 40}.items():
+        assert int(L[sp.index(t)]) == v, t
+
+
+def test_transfer_cost_non_power_of_two_hand_values():
+    """Edge fc0 -> fc1 of the FC chain, (b, feat) = 64 x 256 = 16 384 words, r = 8, p = 6:
+    (3,1,1) vs (1,1,3): b 3 != 1 -> 8 * ceil(16384/3) = 43 696;
+    (1,1,1) vs (5,1,1): 8 * ceil(16384/5) = 26 216;
+    (2,3,1) vs (2,1,3): b 2 = 2 and feat out 3 = in 3 -> 0."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain(p=6))
+    o.configs(6, all_integers=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    R = o.edge_costs(0)
+    i = sp.index
+    assert int(R[i((3, 1, 1)), i((1, 1, 3))]) == 43_696
+    assert int(R[i((1, 1, 1)), i((5, 1, 1))]) == 26_216
+    assert int(R[i((2, 3, 1)), i((2, 1, 3))]) == 0
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_theorem1_all_integer_configs(seed):
+    """Theorem 1 with every positive-integer split (p = 3, 5, 6)."""
+    p = (3, 5, 6)[seed % 3]
+    g = random_graph(seed + 40, n=3 + seed % 3, p=p, max_dims=2, extra_edges=seed % 3)
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    K = o.configs(p, all_integers=True)
+    o.solve()
+    L, R, src, dst = _tables(o, g)
+    mc, strat = o.result()
+    bf_min, optimal = pins.brute_force(L, R, src, dst)
+    assert mc == bf_min
+    assert pins.total_cost(strat, L, R, src, dst) == mc and bool(optimal[tuple(strat)])
+    seq = o.sequence()
+    for i in range(len(seq)):
+        D, T, A = pins.conditioned_table(L, R, src, dst, seq, i, [int(k) for k in K])
+        To, Ao = o.table(i)
+        assert To.tolist() == T and Ao.tolist() == A, (i, seq)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_viterbi_all_integer_configs(seed):
+    """Path graphs with every positive-integer split at p = 6 or 12: the DP is
+    the Viterbi recursion (same minimum, same lowest-index strategy)."""
+    p = 6 if seed % 2 else 12
+    g = chain_graph(seed + 30, n=4 + seed, p=p, max_dims=2)
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    o.configs(p, all_integers=True)
+    o.solve()
+    assert o.sequence() == list(range(len(g["vertices"])))
+    L, R, src, dst = _tables(o, g)
+    forward = [e["src"] < e["dst"] for e in g["edges"]]
+    mc, strat = o.result()
+    vmin, _ = pins.viterbi_chain(L, R, forward)
+    tmin, tstrat = pins.viterbi_table_strategy(L, R, forward)
+    assert mc == vmin == tmin
+    assert strat == tstrat
+
 # ------------------------------------------------------------------ cost model (hand values)
 def test_layer_cost_fc_hand_values():
     """FC (64, 256, 256), contraction over `in`, r = 8, p = 4.
@@ -382,6 +531,10 @@ MUTANTS = {
     "floor_not_ceil": ("static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }",
                        "static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b; }"),
     "no_match_check": ("if (su != sv) match = 0;", "if (su != sv) match = 1;"),
+    "budget_difference": ("if (!enum_rec(d, k + 1, budget / s, pow2, cur, out, count, cap)) return 0;",
+                          "if (!enum_rec(d, k + 1, budget - s + 1, pow2, cur, out, count, cap)) return 0;"),
+    "pow2_only": ("for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {",
+                  "for (uint64_t s = 1; s <= budget; s = 2 * s) {"),
 }
 
 
@@ -441,7 +594,21 @@ def _pin_suite(lib):
                 return False
         return True
 
+    def all_integers():
+        o = Oracle({"name": "one", "p": 12, "comm_weight": 8,
+                    "vertices": [{"name": "v", "dims": [7, 7], "dim_names": ["x", "y"],
+                                  "reduce": [], "flops_per_point": 1}], "edges": []}, lib)
+        o.configs(12, all_integers=True)
+        sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+        o = Oracle(fc_chain(p=6), lib)
+        o.configs(6, all_integers=True)
+        sf = [tuple(int(x) for x in r) for r in o.splits(0)]
+        return (sp == [t for t in itertools.product(range(1, 13), repeat=2) if t[0] * t[1] <= 12]
+                and int(o.layer_costs(0)[sf.index((1, 2, 3))]) == 1_529_174
+                and int(o.edge_costs(0)[sf.index((3, 1, 1)), sf.index((1, 1, 3))]) == 43_696)
+
     guard("w0", w0)
+    guard("all_integers", all_integers)
     guard("hand_costs", hand_costs)
     guard("edge_costs", edge_costs)
     guard("tables", tables)
