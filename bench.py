@@ -37,11 +37,11 @@ def cpu_threads():
     return max(1, n)
 
 
-def oracle_baseline(g, p, max_cells):
+def oracle_baseline(g, p, max_cells, all_integers=False):
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
-    o.configs(p)
+    o.configs(p, all_integers=all_integers)
     o.solve(max_cells=max_cells, threads=threads)
     done = o.cells_done()
     n_done = 0
@@ -91,18 +91,19 @@ def traffic_from_profile():
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
-def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu):
-    """Time `steps` whole searches of one workload; returns the report dict
-    (the oracle timed on the same graph: the whole search when it has at most
-    `cpu_cells` cells, else a prefix of the vertex order)."""
+def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False):
+    """Time `steps` whole searches of one workload (at its own power-of-two p,
+    or at `p` with every integer split when `all_integers`); returns the report
+    dict (the oracle timed on the same graph: the whole search when it has at
+    most `cpu_cells` cells, else a prefix of the vertex order)."""
     import torch
     from paper_2407_04001_amd import OPT_PROFILE, Graph
     from workloads import workload
 
     g = workload(name, seed)
-    p = g["p"]
+    p = p or g["p"]
     pg = Graph(g)
-    pg.enumerate_configs(p)
+    pg.enumerate_configs(p, all_integers=all_integers)
     pg.set_option(OPT_PROFILE, 1)
     stream = torch.cuda.current_stream()
 
@@ -131,20 +132,27 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu):
     col_cells = st["rows_cells"] - st["stream_cells"]
     achieved = OPS_PER_CELL * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
     parity = None
-    gold_path = os.path.join(ROOT, "tests", "golden", f"{name}_seed{seed}.json")
-    if os.path.exists(gold_path):
+    gold_name = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
+    gold_path = os.path.join(ROOT, "tests", "golden", gold_name)
+    if os.path.exists(gold_path) and (all_integers or p == g["p"]):
         with open(gold_path) as f:
             gold = json.load(f)
         parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
-    metric = METRIC if name == "w4_transformer" else f"DP cell-updates/sec and FindBestStrategy wall time ({g['name']})"
+    headline = name == "w4_transformer" and p == g["p"] and not all_integers
+    wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
+    if all_integers:
+        wl += ", every integer split"
+    metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
     out = {
         "metric": metric, "value": cells * steps / elapsed, "unit": "cell-updates/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup,
         "ms_per_step": elapsed * 1e3 / steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
-        "config": {"workload": g["name"], "p": p, "vertices": len(g["vertices"]),
-                   "edges": len(g["edges"]), "cells": cells, "seed": seed},
+        "config": {"workload": g["name"], "p": p,
+                   "config_set": "every integer split" if all_integers else "powers of two",
+                   "vertices": len(g["vertices"]), "edges": len(g["edges"]), "cells": cells,
+                   "seed": seed},
         "find_best_strategy_ms": sum(walls) / len(walls),
         "fill_ms_per_step": fill_ms / steps,
         "fill_cells_per_s": cells / (fill_ms / steps / 1e3) if fill_ms else None,
@@ -152,13 +160,13 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu):
         "roofline": {"bound": "alu", "kernel": "k_fill_rows",
                      "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
                      "frac": achieved / FP64_OPS_PEAK_T,
-                     "traffic": traffic_from_profile() if name == "w4_transformer" else None,
+                     "traffic": traffic_from_profile() if headline else None,
                      "launches_per_step": rows_launches // steps,
                      "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
                      "cells_per_step": col_cells},
     }
     if not no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells))
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers)
     return out
 
 
@@ -175,6 +183,9 @@ def main():
                     help="only run a plain device copy of MIB MiB (HBM counter calibration)")
     ap.add_argument("--all-workloads", action="store_true",
                     help="one JSON line per synthetic workload (W0..W4) instead of the W4 line")
+    ap.add_argument("--p", type=int, default=0, help="modeled devices (default: the workload's own)")
+    ap.add_argument("--all-integers", action="store_true",
+                    help="every integer split factor (Sec. II's full C(v)) instead of powers of two")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -189,7 +200,8 @@ def main():
     torch.cuda.set_device(0)
     names = WORKLOADS if args.all_workloads else [args.workload]
     for name in names:
-        out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu)
+        out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
+                           args.p or None, args.all_integers)
         print(json.dumps(out), flush=True)
 
 

@@ -119,9 +119,13 @@ typedef enum {
     PASE_OPT_C_SPLITS = 10,     /* same kernel: workgroups sharing one tile's c range (partial
                                    keys reduced by a second launch), 0 = chosen (default), else
                                    min(value, K_v) for every vertex */
-    PASE_OPT_LATENCY_WORKERS = 11 /* dataflow schedule: workgroups that serve the latency queue
+    PASE_OPT_LATENCY_WORKERS = 11, /* dataflow schedule: workgroups that serve the latency queue
                                    (the chains of small vertices) before the bulk queue; 0 =
                                    chosen (default: one in 16), else clamped to [1, grid - 1] */
+    PASE_OPT_CONFIG_SET = 12    /* configuration set of the next pase_enumerate_configs: 0
+                                   (default) power-of-two split factors, p = 2^L <= 65536; 1
+                                   every tuple of positive integer factors (Sec. II's C(v)),
+                                   1 <= p <= 255 */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */
@@ -165,9 +169,11 @@ void pase_graph_destroy(pase_graph_t g);
 const char *pase_last_error(pase_graph_t g);
 
 /* Enumerate the configuration set C(v) of every vertex for p modeled devices
- * (Sec. II: tuples of split factors with product <= p; here the power-of-two
- * split factors, so p must be 2^L with L <= 16), ordered lexicographically by
- * the exponent tuple with loop dim 0 slowest.  Then order the vertices with
+ * (Sec. II: tuples of split factors with product <= p): by default the
+ * power-of-two factors, p = 2^L with L <= 16; with PASE_OPT_CONFIG_SET = 1
+ * every positive integer factor, 1 <= p <= 255.  Configurations are ordered
+ * lexicographically by the split tuple with loop dim 0 slowest (for powers of
+ * two the same order as the exponent tuple).  Then order the vertices with
  * GenerateSeq (Fig. 3; ties of |u.d| go to the lowest vertex id), derive the
  * dependent sets D(i), connected sets X(i) and connected subsets S(i)
  * (Sec. III-B) and the device memory plan.  Host only; resets any earlier

@@ -30,10 +30,10 @@
 
 using namespace pase;
 
-// Cost tables of the search: layer cost and device count exponent of every
-// (vertex, configuration), and the split signatures of every (edge endpoint,
-// configuration); r * t_x(e, cu, cv) is then read off two signatures and two
-// exponents (edge_cost_sig).
+// Cost tables of the search: layer cost and device byte (device count or its
+// log2) of every (vertex, configuration), and the split signatures of every
+// (edge endpoint, configuration); r * t_x(e, cu, cv) is then read off two
+// signatures and two device bytes (edge_cost_sig).
 __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, const DevEdge *__restrict__ E,
                               uint32_t ne, const uint8_t *__restrict__ ex, uint64_t *__restrict__ L,
                               uint8_t *__restrict__ lsum, uint64_t *__restrict__ sig, uint64_t nL,
@@ -49,9 +49,7 @@ __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, cons
             const DevVertex dv = V[lo];
             const uint8_t *e = ex + dv.ex_off + (t - dv.L_off) * dv.ndims;
             L[t] = layer_cost(dv, e, r);
-            uint32_t E0 = 0;
-            for (uint32_t k = 0; k < dv.ndims; k++) E0 += e[k];
-            lsum[t] = (uint8_t)E0;
+            lsum[t] = (uint8_t)device_byte(dv, e);
         } else {
             uint64_t u = t - nL;
             uint32_t lo = 0, hi = ne;   // last edge with sig_off <= u
@@ -63,11 +61,11 @@ __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, cons
             uint64_t c = u - de.sig_off;
             const DevVertex vs = V[de.src];
             if (c < vs.K) {
-                sig[u] = split_signature(de.sdim, de.rank, ex + vs.ex_off + c * vs.ndims);
+                sig[u] = split_signature(de.sdim, de.rank, ex + vs.ex_off + c * vs.ndims, de.factors);
             } else {
                 const DevVertex vd = V[de.dst];
                 c -= vs.K;
-                sig[u] = split_signature(de.ddim, de.rank, ex + vd.ex_off + c * vd.ndims);
+                sig[u] = split_signature(de.ddim, de.rank, ex + vd.ex_off + c * vd.ndims, de.factors);
             }
         }
     }
@@ -83,7 +81,7 @@ __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__r
          t += (uint64_t)gridDim.x * blockDim.x) {
         uint64_t cu = t / v.K, cv = t % v.K;
         out[t] = edge_cost_sig(sig[de.sig_off + cu], sig[de.sig_off + u.K + cv], lsum[u.L_off + cu],
-                               lsum[v.L_off + cv], de.elems, r);
+                               lsum[v.L_off + cv], de.elems, r, de.factors);
     }
 }
 
@@ -913,6 +911,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         x.K = g->K[v];
         x.ndims = g->V[v].ndims;
         x.reduce_mask = g->V[v].reduce_mask;
+        x.factors = g->factors ? 1 : 0;
         off += g->ex[v].size();
         loff += g->K[v];
     }
@@ -925,6 +924,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         x.src = g->E[e].src;
         x.dst = g->E[e].dst;
         x.rank = g->E[e].rank;
+        x.factors = g->factors ? 1 : 0;
         for (uint32_t k = 0; k < kMaxDims; k++) {
             x.sdim[k] = (int8_t)(k < x.rank ? g->E[e].src_dim[k] : -1);
             x.ddim[k] = (int8_t)(k < x.rank ? g->E[e].dst_dim[k] : -1);

@@ -704,14 +704,15 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
 
 extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     if (!g) return PASE_ERR_INVALID_ARGUMENT;
-    if (p == 0 || (p & (p - 1)) || p > (1u << 16))
+    const bool factors = g->config_set == 1;
+    if (factors && (p == 0 || p > 255))
+        return fail(g, PASE_ERR_INVALID_ARGUMENT, "p must be in 1..255 with every integer split");
+    if (!factors && (p == 0 || (p & (p - 1)) || p > (1u << 16)))
         return fail(g, PASE_ERR_INVALID_ARGUMENT, "p must be a power of two <= 65536");
     g->enumerated = g->planned = g->searched = g->overridden = false;
     g->ov_layer.clear(); g->ov_edge.clear();
-    uint32_t L = 0;
-    while ((1u << L) < p) L++;
     g->p = p;
-    g->log2p = L;
+    g->factors = factors;
     const size_t nv = g->V.size();
     g->K.assign(nv, 0);
     g->ex.assign(nv, {});
@@ -724,24 +725,30 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
         const uint32_t d = g->V[v].ndims;
         std::vector<uint8_t> &rows = by_dims[d];
         if (rows.empty()) {
-            // exponent tuples with sum <= L in lexicographic order (dim 0 slowest),
-            // produced by the lexicographic successor: bump the last dim that still
-            // has room and clear the dims after it
-            std::vector<uint8_t> cur(d, 0);
+            // split tuples with product <= p in lexicographic order (dim 0
+            // slowest), by the lexicographic successor: step the last dim whose
+            // next factor (x2, or +1 with every integer) still fits beside the
+            // dims before it, and reset the dims after it to 1
+            std::vector<uint32_t> cur(d, 1);
+            uint64_t cnt = 0;
             for (;;) {
-                rows.insert(rows.end(), cur.begin(), cur.end());
-                uint32_t sum = 0;
-                for (uint8_t x : cur) sum += x;
-                int k = (int)d - 1;
-                if (sum < L) {
-                    cur[k]++;
-                    continue;
+                if (++cnt > 65535) return fail(g, PASE_ERR_TOO_LARGE, "more than 65535 configurations");
+                for (uint32_t x : cur) {
+                    uint32_t code = x;
+                    if (!factors) for (code = 0; (1u << code) < x; code++) {}
+                    rows.push_back((uint8_t)code);
                 }
-                // sum == L: find the last k > 0... increment dim k-1 and zero dims >= k
-                while (k >= 0 && cur[k] == 0) k--;
-                if (k <= 0) break;
-                cur[k] = 0;
-                cur[k - 1]++;
+                uint64_t prefix[kMaxDims + 1];
+                prefix[0] = 1;
+                for (uint32_t k = 0; k < d; k++) prefix[k + 1] = prefix[k] * cur[k];
+                int k = (int)d - 1;
+                for (; k >= 0; k--) {
+                    const uint64_t next = factors ? cur[k] + 1ull : 2ull * cur[k];
+                    if (prefix[k] * next <= p) break;
+                }
+                if (k < 0) break;
+                cur[k] = factors ? cur[k] + 1 : 2 * cur[k];
+                for (uint32_t j = k + 1; j < d; j++) cur[j] = 1;
             }
         }
         uint64_t K = rows.size() / d;
@@ -791,7 +798,10 @@ extern "C" pase_status pase_config_splits(pase_graph_t g, uint32_t v, uint32_t i
     if (!g->enumerated) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
     if (v >= g->V.size() || idx >= g->K[v]) return fail(g, PASE_ERR_INVALID_ARGUMENT, "bad id");
     const uint32_t d = g->V[v].ndims;
-    for (uint32_t k = 0; k < d; k++) splits[k] = 1u << g->ex[v][(size_t)idx * d + k];
+    for (uint32_t k = 0; k < d; k++) {
+        const uint32_t x = g->ex[v][(size_t)idx * d + k];
+        splits[k] = g->factors ? x : 1u << x;
+    }
     return PASE_OK;
 }
 
@@ -849,6 +859,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     case PASE_OPT_LATENCY_WORKERS:
         if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "latency workers <= 65535");
         g->lat_workers = (uint32_t)value;
+        break;
+    case PASE_OPT_CONFIG_SET:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "config set 0 or 1");
+        g->config_set = (uint32_t)value;
         break;
     case PASE_OPT_C_SPLITS:
         if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "c splits 0..65535");

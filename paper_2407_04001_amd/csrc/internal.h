@@ -28,15 +28,19 @@ constexpr uint64_t kMaxTableEntries = (1ull << 31) - 1;
 
 // ------------------------------------------------------------------ device descriptors
 struct DevVertex {            // configuration data of one vertex (uploaded once per search)
-    uint64_t ex_off;          // byte offset of its exponent rows (K x ndims uint8)
+    uint64_t ex_off;          // byte offset of its split rows (K x ndims uint8)
     uint64_t L_off;           // element offset of its layer-cost vector
     uint64_t flops;           // flops_per_point * prod(size)
     uint64_t keep_n;          // prod of the sizes of the non-contracted dims
-    uint32_t K, ndims, reduce_mask, pad;
+    uint32_t K, ndims, reduce_mask;
+    uint32_t factors;         // 0: split rows hold log2 of power-of-two factors and the
+                              // per-configuration device byte its exponent sum; 1: both
+                              // hold the factors / device count themselves (p <= 255)
 };
 
 struct DevEdge {
-    uint32_t src, dst, rank, pad;
+    uint32_t src, dst, rank;
+    uint32_t factors;         // as DevVertex::factors
     int8_t sdim[kMaxDims], ddim[kMaxDims];
     uint64_t elems;
     uint64_t sig_off;         // element offset of its split signatures: K_src, then K_dst
@@ -293,9 +297,12 @@ struct pase_graph_s {
     int schedule = 0;               // pase_option PASE_OPT_SCHEDULE (SchedKind)
     // configurations
     bool enumerated = false;
-    uint32_t p = 0, log2p = 0;
+    uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
+    uint32_t p = 0;
+    bool factors = false;           // the enumerated set: split rows hold factors, not exponents
     std::vector<uint32_t> K;
-    std::vector<std::vector<uint8_t>> ex;  // [v][c*ndims + k]
+    std::vector<std::vector<uint8_t>> ex;  // [v][c*ndims + k]: log2 of the split factor, or the
+                                           // factor itself when `factors`
     std::vector<uint64_t> flops, keep_n;
     std::vector<uint64_t> maxL;            // upper bound of the layer cost per vertex
     std::vector<uint64_t> maxR;            // upper bound of the transfer cost per edge

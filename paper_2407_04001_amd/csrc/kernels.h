@@ -50,11 +50,23 @@ template <> struct KeyOps<uint64_t> {
 constexpr int kBufferWord3 = 0x00020000;
 
 // ------------------------------------------------------------------ cost model (device)
-// Layer cost t_l(v, c) = ceil(F / P) + r * (2^e_red - 1) * ceil(keep / 2^(E - e_red)),
-// with P = 2^E the device count of the configuration and e_red the exponent
-// sum over contracted dims.  Power-of-two divisions are shifts; the host has
-// bounded every operand so nothing overflows.
+// Layer cost t_l(v, c) = ceil(F / P) + r * (P_red - 1) * ceil(keep / (P / P_red)),
+// with P the device count of the configuration and P_red the product of the
+// split factors of the contracted dims.  With power-of-two factors (split rows
+// hold exponents) the divisions are shifts; otherwise (rows hold the factors,
+// P <= 255) they are integer divisions.  The host has bounded every operand so
+// nothing overflows.
+__device__ __forceinline__ uint64_t ceil_div_u64(uint64_t a, uint32_t b) { return (a + (b - 1)) / b; }
+
 __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
+    if (dv.factors) {
+        uint32_t P = 1, red = 1;
+        for (uint32_t k = 0; k < dv.ndims; k++) {
+            P *= ex[k];
+            if ((dv.reduce_mask >> k) & 1u) red *= ex[k];
+        }
+        return ceil_div_u64(dv.flops, P) + r * ((uint64_t)(red - 1) * ceil_div_u64(dv.keep_n, P / red));
+    }
     uint32_t E = 0, ered = 0;
     for (uint32_t k = 0; k < dv.ndims; k++) {
         E += ex[k];
@@ -66,19 +78,32 @@ __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_
     return compute + r * (((1ull << ered) - 1) * part);
 }
 
-// Split signature of one endpoint configuration of an edge: the split
-// exponent of every tensor dim (0 for an unsplit dim), 5 bits each.  Two
-// endpoints redistribute nothing exactly when their signatures are equal.
-__device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t rank, const uint8_t *ex) {
+// Device byte of one configuration: the exponent sum log2(P) of power-of-two
+// rows, else the device count P itself.
+__device__ __forceinline__ uint32_t device_byte(const DevVertex &dv, const uint8_t *ex) {
+    uint32_t x = dv.factors ? 1 : 0;
+    for (uint32_t k = 0; k < dv.ndims; k++) x = dv.factors ? x * ex[k] : x + ex[k];
+    return x;
+}
+
+// Split signature of one endpoint configuration of an edge: the split of every
+// tensor dim (an unsplit dim counts as factor 1), one field per dim -- 5-bit
+// exponents, or 8-bit factors.  Two endpoints redistribute nothing exactly when
+// their signatures are equal.
+__device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t rank, const uint8_t *ex,
+                                                   uint32_t factors) {
+    const uint32_t w = factors ? 8 : 5, one = factors ? 1 : 0;
     uint64_t sig = 0;
-    for (uint32_t k = 0; k < rank; k++) sig |= (uint64_t)(dims[k] >= 0 ? ex[dims[k]] : 0) << (5 * k);
+    for (uint32_t k = 0; k < rank; k++) sig |= (uint64_t)(dims[k] >= 0 ? ex[dims[k]] : one) << (w * k);
     return sig;
 }
 
+// r * t_x from the two signatures and device bytes of the endpoints.
 __device__ __forceinline__ uint64_t edge_cost_sig(uint64_t sig_a, uint64_t sig_b, uint32_t la, uint32_t lb,
-                                                  uint64_t elems, uint64_t r) {
+                                                  uint64_t elems, uint64_t r, uint32_t factors) {
     if (sig_a == sig_b) return 0;
     uint32_t s = la > lb ? la : lb;
+    if (factors) return r * ceil_div_u64(elems, s);
     return r * ((elems + ((1ull << s) - 1)) >> s);
 }
 
@@ -147,7 +172,7 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
             const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
             const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
             const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
-            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r);
+            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r, de.factors);
         } else {
             uint64_t idx = (uint64_t)c * ct.sc;
             for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];

@@ -20,7 +20,8 @@ OK, INVALID_ARGUMENT, NOT_CONNECTED, BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMO
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STATE", 4: "OVERFLOW",
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
 (OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
- OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS, OPT_LATENCY_WORKERS) = range(1, 12)
+ OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS, OPT_LATENCY_WORKERS,
+ OPT_CONFIG_SET) = range(1, 13)
 
 
 class VertexDesc(C.Structure):
@@ -287,9 +288,13 @@ class Graph:
         except (TypeError, AttributeError):   # interpreter shutdown: module globals are gone
             pass
 
-    def enumerate_configs(self, p: int):
+    def enumerate_configs(self, p: int, all_integers: bool | None = None):
         """Enumerate configurations and plan the search for p devices; the
-        per-vertex configuration counts are read lazily through `K`."""
+        per-vertex configuration counts are read lazily through `K`.
+        all_integers (when given) sets OPT_CONFIG_SET first: every positive
+        integer split instead of the power-of-two ones."""
+        if all_integers is not None:
+            pase_set_option(self.h, OPT_CONFIG_SET, 1 if all_integers else 0)
         pase_enumerate_configs(self.h, p)
         self._K = None
 

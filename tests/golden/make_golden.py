@@ -7,7 +7,7 @@ strategy, the cell count, per-vertex fingerprints of the cost and argmin
 tables (canonical order, SplitMix64-based, see ``pase.h``) and a seeded sample
 of table entries.
 
-    python tests/golden/make_golden.py [--only NAME] [--threads N]
+    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only]
 """
 from __future__ import annotations
 
@@ -26,16 +26,27 @@ sys.path.insert(0, ROOT)
 from oracle.oracle import Oracle, build  # noqa: E402
 from workloads import workload  # noqa: E402
 
-INSTANCES = [("w0_fc_chain", 0), ("w1_residual_cnn", 0), ("w1_residual_cnn", 1),
-             ("w1_residual_cnn", 2), ("w2_inception", 0), ("w2_inception", 1),
-             ("w2_inception", 2), ("w3_lstm_grid", 0), ("w4_transformer", 0)]
+# (workload, seed, p, every integer split): p None = the workload's own
+# power-of-two p; the every-integer instances enumerate Sec. II's full C(v)
+INSTANCES = [("w0_fc_chain", 0, None, False), ("w1_residual_cnn", 0, None, False),
+             ("w1_residual_cnn", 1, None, False), ("w1_residual_cnn", 2, None, False),
+             ("w2_inception", 0, None, False), ("w2_inception", 1, None, False),
+             ("w2_inception", 2, None, False), ("w3_lstm_grid", 0, None, False),
+             ("w4_transformer", 0, None, False),
+             ("w0_fc_chain", 0, 12, True), ("w2_inception", 0, 12, True),
+             ("w4_transformer", 0, 12, True)]
+
+
+def file_name(name: str, seed: int, p=None, all_integers: bool = False) -> str:
+    return f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
 SAMPLES_PER_TABLE = 24
 
 
-def golden(name: str, seed: int, threads: int) -> dict:
+def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False) -> dict:
     g = workload(name, seed)
+    p = p or g["p"]
     o = Oracle(g)
-    K = o.configs(g["p"])
+    K = o.configs(p, all_integers=all_integers)
     t0 = time.time()
     o.solve(rule=0, threads=threads)
     wall = time.time() - t0
@@ -53,7 +64,8 @@ def golden(name: str, seed: int, threads: int) -> dict:
             samples.append([k, str(t), a])
         tables.append({"vertex": seq[i], "dep": o.dependent_set(i), "entries": n,
                        "fp_cost": str(fpT), "fp_arg": str(fpA), "samples": samples})
-    return {"workload": name, "seed": seed, "p": g["p"], "num_configs": [int(k) for k in K],
+    return {"workload": name, "seed": seed, "p": p, "all_integers": all_integers,
+            "num_configs": [int(k) for k in K],
             "sequence": seq, "min_cost": str(mc), "strategy": strat, "cells": o.cells(),
             "tables": tables, "oracle_seconds": round(wall, 3)}
 
@@ -62,14 +74,18 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--only", default=None)
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 1)
+    ap.add_argument("--all-integers-only", action="store_true",
+                    help="only the instances with every integer split")
     args = ap.parse_args()
     build(force=False)
-    for name, seed in INSTANCES:
+    for name, seed, p, all_integers in INSTANCES:
         if args.only and args.only != name:
             continue
+        if args.all_integers_only and not all_integers:
+            continue
         t = time.time()
-        out = golden(name, seed, args.threads)
-        path = os.path.join(HERE, f"{name}_seed{seed}.json")
+        out = golden(name, seed, args.threads, p, all_integers)
+        path = os.path.join(HERE, file_name(name, seed, p, all_integers))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))
         print(f"{name} seed {seed}: min_cost {out['min_cost']} cells {out['cells']:.3e} "

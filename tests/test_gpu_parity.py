@@ -32,10 +32,10 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _oracle(g, p=None, costs=None, rule=0):
+def _oracle(g, p=None, costs=None, rule=0, all_integers=False):
     from oracle.oracle import Oracle
     o = Oracle(g)
-    o.configs(p or g["p"])
+    o.configs(p or g["p"], all_integers=all_integers)
     if costs is not None:
         o.set_costs(*costs)
     o.solve(rule=rule, threads=os.cpu_count() or 1)
@@ -66,9 +66,9 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0):
+         parts=0, splits=0, lat_workers=0, all_integers=False):
     pg = P.Graph(g, seq_rule=rule)
-    pg.enumerate_configs(p or g["p"])
+    pg.enumerate_configs(p or g["p"], all_integers=all_integers)
     pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
@@ -255,19 +255,20 @@ def test_library_owned_workspace(P):
 
 
 # ------------------------------------------------------------------ full-size workloads
-def _golden(name, seed):
-    with open(os.path.join(GOLDEN, f"{name}_seed{seed}.json")) as f:
+def _golden(name, seed, p=None, all_integers=False):
+    fn = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
+    with open(os.path.join(GOLDEN, fn)) as f:
         return json.load(f)
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0):
-    gold = _golden(name, seed)
+                  lat_workers=0, p=None, all_integers=False):
+    gold = _golden(name, seed, p, all_integers)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers}")
-    pg, mc, strat = _run(P, g, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers)
+        f"lat_workers={lat_workers} p={p} all_integers={all_integers}")
+    pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
+                         lat_workers=lat_workers, all_integers=all_integers)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -393,3 +394,98 @@ def test_cost_tables_against_oracle(P):
             assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
         for e in range(len(g["edges"])):
             assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e
+
+
+# ------------------------------------------------------------------ every integer split
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("key", [0, 1])
+def test_all_integer_random_graphs(P, seed, key):
+    """Sec. II's full configuration set (factors 3, 5, 6, 7 ... ): the result,
+    every table entry and the device cost tables equal the oracle's."""
+    p = (3, 5, 6, 7, 12, 12, 24, 10)[seed]
+    g = random_graph(seed + 700, n=4 + seed % 5, p=p, max_dims=3, extra_edges=1 + seed % 4,
+                     max_size=300)
+    say(f"every-integer random graph seed={seed + 700} p={p} key={key}")
+    o = _oracle(g, p=p, all_integers=True)
+    pg, mc, strat = _run(P, g, p=p, key=key, all_integers=True)
+    assert pg.K == [int(k) for k in o.K]
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=1024)
+    for v in range(len(g["vertices"])):
+        assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
+    for e in range(len(g["edges"])):
+        assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_all_integer_tied_costs_and_kernels(P, seed):
+    """Dense ties with every integer split, on the row kernel at two tile
+    forms and on the generic kernel."""
+    g = random_graph(seed + 720, n=5 + seed, p=12, max_dims=3, extra_edges=2 + seed)
+    o0 = _oracle(g, p=12, all_integers=True)
+    K = [int(k) for k in o0.K]
+    costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    o = _oracle(g, p=12, costs=costs, all_integers=True)
+    for kernel, tile in ((0, (0, 0)), (0, (8, 2)), (0, (28, 1)), (1, (0, 0))):
+        say(f"every-integer tied costs seed={seed + 720} kernel={kernel} tile={tile}")
+        pg, mc, strat = _run(P, g, p=12, costs=costs, kernel=kernel, tile=tile, all_integers=True)
+        assert (mc, strat) == o.result()
+        _compare_all_entries(pg, o, g, max_entries=512)
+
+
+def test_all_integer_edge_cases(P):
+    """p = 1 (one configuration), a prime p, and the largest p (255) with
+    one- and two-dim vertices."""
+    for p, seed, dims in ((1, 730, 3), (7, 731, 3), (255, 732, 1), (255, 733, 2)):
+        g = random_graph(seed, n=4, p=p, max_dims=dims, extra_edges=1, max_size=1000)
+        say(f"every-integer edge case p={p} seed={seed} dims<={dims}")
+        o = _oracle(g, p=p, all_integers=True)
+        pg, mc, strat = _run(P, g, p=p, all_integers=True)
+        assert (mc, strat) == o.result()
+        if p == 1:
+            assert set(strat) == {0}
+        for e in range(len(g["edges"])):
+            assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e
+
+
+@pytest.mark.parametrize("name", ["w0_fc_chain", "w2_inception"])
+def test_all_integer_workloads_against_golden(P, name):
+    """Full-size workloads at p = 12 with every integer split, against the
+    oracle's stored results: default plan, generic kernel, uint64 keys, and
+    the sequential, lane and dataflow schedules."""
+    _check_golden(P, name, 0, p=12, all_integers=True)
+    if name == "w2_inception":
+        _check_golden(P, name, 0, p=12, all_integers=True, kernel=1)
+        _check_golden(P, name, 0, p=12, all_integers=True, key=1)
+        for sched in (1, 2, 3):
+            _check_golden(P, name, 0, p=12, all_integers=True, keep=False, schedule=sched)
+
+
+def test_all_integer_transformer_p12_against_golden(P):
+    _check_golden(P, "w4_transformer", 0, p=12, all_integers=True, keep=False)
+    _check_golden(P, "w4_transformer", 0, p=12, all_integers=True, keep=True)
+
+
+def test_all_integer_transformer_p24_properties(P):
+    """Beyond the oracle's reach in a test (7.2e11 cells): the returned
+    strategy costs the returned minimum under the oracle's cost tables, the
+    level and sequential schedules and both key types agree, and the minimum
+    is at most the p = 12 optimum (every p = 12 configuration is a p = 24 one)."""
+    from oracle.oracle import Oracle
+    g = workload("w4_transformer", 0)
+    say("every-integer transformer p=24 level schedule")
+    pg, mc, strat = _run(P, g, p=24, keep=False, all_integers=True)
+    say(f"   cells {pg.stats()['cells']:.3e} wall {pg.stats()['wall_ms']:.1f} ms")
+    say("every-integer transformer p=24 sequential schedule, uint64 keys")
+    _, mc1, strat1 = _run(P, g, p=24, keep=False, schedule=1, key=1, all_integers=True)
+    assert (mc1, strat1) == (mc, strat)
+    assert mc <= int(_golden("w4_transformer", 0, 12, True)["min_cost"])
+    o = Oracle(g)
+    o.configs(24, all_integers=True)
+    L = [o.layer_costs(v) for v in range(len(g["vertices"]))]
+    src = [e["src"] for e in g["edges"]]
+    dst = [e["dst"] for e in g["edges"]]
+    tot = sum(int(L[v][c]) for v, c in enumerate(strat))
+    for e in range(len(src)):
+        tot += int(o.edge_costs(e)[strat[src[e]], strat[dst[e]]])
+    assert tot == mc

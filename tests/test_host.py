@@ -117,6 +117,53 @@ def test_configs_match_oracle(pase):
     assert pg.config_splits(0, 9) == [4, 1, 1]
 
 
+@pytest.mark.parametrize("p", [1, 2, 3, 5, 6, 7, 12, 16, 24, 255])
+def test_all_integer_configs_match_oracle(pase, p):
+    """PASE_OPT_CONFIG_SET = 1: the library's configurations (count, order and
+    split factors) are the oracle's every-integer set, for 1 to 8 loop dims."""
+    from oracle.oracle import Oracle
+    vs = [{"name": f"v{d}", "dims": [5] * d, "dim_names": ["x"] * d, "reduce": [],
+           "flops_per_point": 1} for d in range(1, 9)]
+    es = [{"src": d, "dst": d + 1, "src_dim": [0], "dst_dim": [0], "elems": 5} for d in range(7)]
+    g = {"name": "dims", "p": p, "comm_weight": 8, "vertices": vs, "edges": es}
+    o = Oracle(g)
+    try:
+        Ko = [int(k) for k in o.configs(p, all_integers=True)]
+    except Exception:
+        Ko = None
+    pg = pase.Graph(g)
+    if Ko is None:   # more than 65535 configurations for some vertex
+        assert _status(lambda: pg.enumerate_configs(p, all_integers=True)) == pase.TOO_LARGE
+        return
+    pg.enumerate_configs(p, all_integers=True)
+    assert pg.K == Ko
+    for v in range(len(vs)):
+        sp = o.splits(v)
+        for c in range(Ko[v]) if Ko[v] < 2000 else range(0, Ko[v], 7):
+            assert pg.config_splits(v, c) == [int(x) for x in sp[c]]
+
+
+def test_config_set_option(pase):
+    """The option takes effect at the next enumeration; p outside the set's
+    range is rejected; switching back restores the power-of-two set."""
+    P = pase
+    g = fc_chain()
+    pg = P.Graph(g)
+    pg.enumerate_configs(4)
+    assert pg.K[0] == 10
+    pg.enumerate_configs(4, all_integers=True)
+    assert pg.K[0] == 13          # 10 + (3,1,1), (1,3,1), (1,1,3)
+    assert pg.config_splits(0, 12) == [4, 1, 1]
+    assert _status(lambda: pg.enumerate_configs(256)) == P.INVALID_ARGUMENT
+    assert _status(lambda: pg.enumerate_configs(0)) == P.INVALID_ARGUMENT
+    pg.enumerate_configs(6)
+    assert pg.K[0] == 25          # N_3(6) = N_2(6) + N_2(3) + N_2(2) + 3 N_2(1) = 14 + 5 + 3 + 3
+    pg.enumerate_configs(4, all_integers=False)
+    assert pg.K[0] == 10
+    assert _status(lambda: pg.enumerate_configs(6)) == P.INVALID_ARGUMENT
+    assert _status(lambda: P.pase_set_option(pg.h, P.OPT_CONFIG_SET, 2)) == P.INVALID_ARGUMENT
+
+
 @pytest.mark.parametrize("seed", range(20))
 @pytest.mark.parametrize("rule", [0, 1])
 def test_sequence_and_dependent_sets(pase, seed, rule):
