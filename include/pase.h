@@ -267,6 +267,9 @@ typedef struct {
     uint32_t level;      /* dependency level: 1 + the largest level of the tables it reads */
     uint32_t lane;       /* lane schedule: the stream it runs on: 0 = the caller's, 1 = the latency-bound
                             chain's (highest wave priority), 2 = the other chains' */
+    uint64_t key_bound;  /* upper bound of every summed cost before the min over c (keys stay
+                            below (key_bound + 1) * 2^ceil(log2 K_v)); ~0 if it exceeds 64 bits */
+    uint64_t table_bound; /* upper bound of every entry of its DP table; ~0 likewise */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

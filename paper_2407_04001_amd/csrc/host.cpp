@@ -29,34 +29,71 @@ static uint32_t bits_for(uint32_t K) {
     return b;
 }
 
-// Key type: fp64 when every key (cost * 2^bits + c) of every vertex stays
-// below 2^53 so that double arithmetic on them is exact integer arithmetic;
-// otherwise uint64 when it stays below 2^64; otherwise overflow.
+// Upper bounds of the DP quantities at every sequence position i, used to
+// size the keys.  Q_i(phi, c) -- the layer cost of v_i at c, plus r * t_x of
+// every edge joining v_i and a later vertex, plus the table lookup of every
+// connected subset -- is at most maxL(v_i) + sum maxR + sum Tmax_j.  The table
+// entry T_i(phi) = min_c Q_i(phi, c) is at most Q_i(phi, c0) for any single c0:
+// with model costs c0 is the unsplit configuration (cost F) or the one that
+// splits a non-contracted dim p ways (cost ceil(F / p), no partial sums); with
+// caller-given costs it is the cheapest layer configuration.  These bounds
+// follow the recurrence instead of summing every cost of the graph, so deep
+// graphs keep exact fp64 keys.  false: a bound exceeds 64 bits.
+bool cost_bounds(pase_graph_t g, std::vector<uint64_t> *qmax, std::vector<uint64_t> *tmax) {
+    const Plan &P = g->plan;
+    const size_t n = P.v.size();
+    qmax->assign(n, 0);
+    tmax->assign(n, 0);
+    for (size_t i = 0; i < n; i++) {
+        const VPlan &vp = P.v[i];
+        const int v = vp.vi;
+        uint64_t hi = g->maxL[v], lo;
+        if (g->overridden) {
+            hi = 0;
+            lo = ~0ull;
+            for (uint32_t c = 0; c < g->K[v]; c++) {
+                hi = std::max(hi, g->ov_layer[g->ov_layer_off[v] + c]);
+                lo = std::min(lo, g->ov_layer[g->ov_layer_off[v] + c]);
+            }
+        } else {
+            const pase_vertex_desc &d = g->V[v];
+            const uint64_t F = g->flops[v];
+            const bool keep_dim = (d.reduce_mask & ((1u << d.ndims) - 1)) != ((1u << d.ndims) - 1);
+            // all dims contracted: keep_n = 1 and r * (p - 1) <= maxL - F
+            const uint64_t one = (F + g->p - 1) / g->p + (keep_dim ? 0 : g->r * (uint64_t)(g->p - 1));
+            lo = std::min(F, one);
+        }
+        uint64_t rest = 0;
+        for (int e : vp.edges) {
+            uint64_t m = g->maxR[e];
+            if (g->overridden) {
+                m = 0;
+                const uint64_t cnt = (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+                for (uint64_t k = 0; k < cnt; k++) m = std::max(m, g->ov_edge[g->ov_edge_off[e] + k]);
+            }
+            if (!add_ok(rest, m, &rest)) return false;
+        }
+        for (const TermRef &t : vp.terms)
+            if (!add_ok(rest, (*tmax)[t.j], &rest)) return false;
+        if (!add_ok(hi, rest, &(*qmax)[i]) || !add_ok(lo, rest, &(*tmax)[i])) return false;
+    }
+    return true;
+}
+
+// Key type: fp64 when every key (cost * 2^bits + c) of every position stays
+// within 2^53 so that double arithmetic on them is exact integer arithmetic;
+// otherwise uint64 when it stays within 2^64; otherwise overflow.  A stored
+// table entry T_j (in its reader's key space) is at most the reader's bound.
 uint32_t choose_key_type(pase_graph_t g, pase_status *st) {
     *st = PASE_OK;
-    uint64_t bound = 0;
-    size_t nv = g->V.size(), ne = g->E.size();
-    for (size_t v = 0; v < nv; v++) {
-        uint64_t m = g->maxL[v];
-        if (g->overridden) {
-            m = 0;
-            for (uint32_t c = 0; c < g->K[v]; c++) m = std::max(m, g->ov_layer[g->ov_layer_off[v] + c]);
-        }
-        if (!add_ok(bound, m, &bound)) { *st = PASE_ERR_OVERFLOW; return 0; }
+    std::vector<uint64_t> qmax, tmax;
+    if (!cost_bounds(g, &qmax, &tmax)) { *st = PASE_ERR_OVERFLOW; return 0; }
+    unsigned __int128 top = 0;
+    for (size_t i = 0; i < qmax.size(); i++) {
+        // largest key: qmax * 2^bits + (2^bits - 1) < (qmax + 1) * 2^bits
+        const unsigned __int128 t = ((unsigned __int128)qmax[i] + 1) << g->plan.v[i].bits;
+        top = std::max(top, t);
     }
-    for (size_t e = 0; e < ne; e++) {
-        uint64_t m = g->maxR[e];
-        if (g->overridden) {
-            m = 0;
-            uint64_t n = (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
-            for (uint64_t k = 0; k < n; k++) m = std::max(m, g->ov_edge[g->ov_edge_off[e] + k]);
-        }
-        if (!add_ok(bound, m, &bound)) { *st = PASE_ERR_OVERFLOW; return 0; }
-    }
-    uint32_t bmax = 0;
-    for (uint32_t k : g->K) bmax = std::max(bmax, bits_for(k));
-    // largest key: bound * 2^bmax + (2^bmax - 1) < (bound + 1) * 2^bmax
-    unsigned __int128 top = ((unsigned __int128)bound + 1) << bmax;
     if (g->key_mode == 0 && top <= ((unsigned __int128)1 << 53)) return 0;
     if (top <= ((unsigned __int128)1 << 64)) return 1;
     *st = PASE_ERR_OVERFLOW;
@@ -1013,6 +1050,13 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     x.fill_ms = vp.fill_ms;
     x.level = (uint32_t)vp.level;
     x.lane = (uint32_t)vp.lane;
+    std::vector<uint64_t> qmax, tmax;
+    if (cost_bounds(g, &qmax, &tmax)) {
+        x.key_bound = qmax[x.position];
+        x.table_bound = tmax[x.position];
+    } else {
+        x.key_bound = x.table_bound = ~0ull;
+    }
     *out = x;
     return PASE_OK;
 }

@@ -206,6 +206,38 @@ def conditioned_table(L, R, src, dst, seq, i, Ks, limit: int = 2_000_000):
     return D, T, A
 
 
+def conditioned_qmax(L, R, src, dst, seq, i, Ks, limit: int = 2_000_000) -> int:
+    """The largest value the DP minimises over at position i: max over
+    assignments phi of D(i) and configurations c of seq[i] of the min over
+    the rest of X(i) of the same sum as in conditioned_table (exhaustive)."""
+    nv = len(L)
+    nb = neighbours(nv, src, dst)
+    pos = {v: k for k, v in enumerate(seq)}
+    X = sorted(connected_set(nb, seq, i))
+    D = dependent_set(nb, seq, i)
+    vi = seq[i]
+    later_edges = [e for e in range(len(src))
+                   if (src[e] in X and pos[dst[e]] > pos[src[e]])
+                   or (dst[e] in X and pos[src[e]] > pos[dst[e]])]
+    space = 1
+    for v in X + D:
+        space *= Ks[v]
+    if space > limit:
+        raise ValueError("conditioned search too large")
+    best = {}
+    for phi in itertools.product(*[range(Ks[w]) for w in D]):
+        cfg = dict(zip(D, phi))
+        for xs in itertools.product(*[range(Ks[v]) for v in X]):
+            cfg.update(zip(X, xs))
+            cost = sum(int(L[v][cfg[v]]) for v in X)
+            for e in later_edges:
+                cost += int(R[e][cfg[src[e]], cfg[dst[e]]])
+            key = (phi, cfg[vi])
+            if key not in best or cost < best[key]:
+                best[key] = cost
+    return max(best.values())
+
+
 def splitmix64_mix(z: int) -> int:
     """SplitMix64 output function (Steele, Lea and Flood, 2014)."""
     m = (1 << 64) - 1

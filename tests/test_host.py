@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import pins
-from workloads import fc_chain, random_graph, transformer, workload
+from workloads import fc_chain, random_costs, random_graph, transformer, workload
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -162,6 +162,54 @@ def test_config_set_option(pase):
     assert pg.K[0] == 10
     assert _status(lambda: pg.enumerate_configs(6)) == P.INVALID_ARGUMENT
     assert _status(lambda: P.pase_set_option(pg.h, P.OPT_CONFIG_SET, 2)) == P.INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_key_bounds_hold(pase, seed):
+    """The per-position bounds that size the keys hold on the oracle's tables:
+    key_bound >= the largest value minimised over at that position (exhaustive
+    search) and table_bound >= every table entry; model costs with both
+    configuration sets, and caller-given costs."""
+    from oracle.oracle import Oracle
+    all_int = seed % 3 == 1
+    p = (4, 6, 8)[seed % 3]
+    g = random_graph(seed + 900, n=3 + seed % 4, p=p, max_dims=2, extra_edges=seed % 3, max_size=200)
+    o = Oracle(g)
+    K = [int(k) for k in o.configs(p, all_integers=all_int)]
+    costs = None
+    if seed % 3 == 2:
+        costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=1000)
+        o.set_costs(*costs)
+    o.solve()
+    pg = pase.Graph(g)
+    pg.enumerate_configs(p, all_integers=all_int)
+    if costs is not None:
+        pg.override_costs(*costs)
+    L = [o.layer_costs(v) for v in range(len(K))]
+    R = [o.edge_costs(e) for e in range(len(g["edges"]))]
+    src = [e["src"] for e in g["edges"]]
+    dst = [e["dst"] for e in g["edges"]]
+    seq = o.sequence()
+    for i, v in enumerate(seq):
+        info = pg.vertex_info(v)
+        T, _ = o.table(i)
+        assert info["table_bound"] >= int(max(T)), (i, v)
+        assert info["key_bound"] >= pins.conditioned_qmax(L, R, src, dst, seq, i, K), (i, v)
+
+
+@pytest.mark.parametrize("name,p,all_int", [("w4_transformer", 64, False),
+                                            ("w4_transformer", 24, True),
+                                            ("w3_lstm_grid", 32, False)])
+def test_workload_keys_fit_fp64(pase, name, p, all_int):
+    """The recurrence bounds keep exact fp64 keys ((key_bound + 1) * 2^bits
+    <= 2^53) on the full-size workloads, including the Transformer at p = 24
+    with every integer split (7.2e11 cells)."""
+    pg = pase.Graph(workload(name))
+    pg.enumerate_configs(p, all_integers=all_int)
+    for v in range(len(pg.K)):
+        info = pg.vertex_info(v)
+        bits = max(0, (pg.K[v] - 1).bit_length())
+        assert (info["key_bound"] + 1) << bits <= 1 << 53, v
 
 
 @pytest.mark.parametrize("seed", range(20))
