@@ -47,6 +47,7 @@ def _load(path: str | None = None):
     L.oracle_configs_all.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
+    L.oracle_solve_bf.argtypes = [P, U64, I]
     L.oracle_num_configs.argtypes = [P, I]
     L.oracle_config_splits.argtypes = [P, I, I, P]
     L.oracle_layer_costs.argtypes = [P, I, P]
@@ -178,6 +179,11 @@ class Oracle:
             ordp = _ptr(ord_arr)
         rc = self._L.oracle_solve(self._h, int(rule), ordp, int(max_cells), int(threads))
         return self._check(rc)
+
+    def solve_bf(self, max_cells: int = 0, threads: int = 1) -> int:
+        """The breadth-first recurrence (eq. 2): breadth-first order from
+        vertex 0, tables B over D_B(i); read back with the same getters."""
+        return self._check(self._L.oracle_solve_bf(self._h, int(max_cells), int(threads)))
 
     def sequence(self) -> list:
         out = np.zeros(self.nv, dtype=np.int32)

@@ -400,6 +400,35 @@ static int node_cost(oracle_t *o, int i, const int *later_edges, int nlater, con
     return 1;
 }
 
+/* Entries of every table (product of K over D(i)) and the cell count; 0 when
+ * a table would exceed 2^34 entries (the oracle keeps every table in memory). */
+static int table_sizes(oracle_t *o) {
+    o->cells = 0;
+    for (int i = 0; i < o->nv; i++) {
+        uint64_t N = 1;
+        for (int k = 0; k < o->nD[i]; k++)
+            if (!mul_ok(N, (uint64_t)o->K[o->D[i][k]], &N) || N > ((uint64_t)1 << 34)) return 0;
+        o->N[i] = N;
+        o->cells += N * (uint64_t)o->K[o->seq[i]];
+    }
+    return 1;
+}
+
+/* Back-substitution from the last position: c_i = A_i[phi restricted to
+ * D(i)], every vertex of D(i) being later in the sequence. */
+static void back_substitute(oracle_t *o) {
+    int n = o->nv;
+    o->min_cost = o->T[n - 1][0];
+    int *cfg_of = calloc(n, sizeof(int));
+    for (int i = n - 1; i >= 0; i--) {
+        uint64_t idx = table_index(o, i, cfg_of);
+        cfg_of[o->seq[i]] = o->A[i][idx];
+    }
+    for (int v = 0; v < n; v++) o->strategy[v] = cfg_of[v];
+    free(cfg_of);
+    o->solved = 1;
+}
+
 /* FindBestStrategy (Fig. 4).  order: NULL -> GenerateSeq with `rule`, else the
  * given sequence of vertex ids (dependent sets then come from their
  * definition).  max_cells > 0 stops after the first vertex that reaches that
@@ -444,14 +473,7 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
     }
     for (int i = 0; i < n; i++) qsort(o->D[i], o->nD[i], sizeof(int), cmp_int);
 
-    o->cells = 0;
-    for (int i = 0; i < n; i++) {
-        uint64_t N = 1;
-        for (int k = 0; k < o->nD[i]; k++)
-            if (!mul_ok(N, (uint64_t)o->K[o->D[i][k]], &N)) return fail(o, "table too large");
-        o->N[i] = N;
-        o->cells += N * (uint64_t)o->K[o->seq[i]];
-    }
+    if (!table_sizes(o)) return fail(o, "table too large");
 
     int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
     int *comp = calloc(n, sizeof(int));
@@ -549,15 +571,123 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
     if (stopped == 2) return 2;  /* partial run: timing sample only */
 
     /* R_V(|V|, empty) and back-substitution from the last vertex */
-    o->min_cost = o->T[n - 1][0];
-    int *cfg_of = calloc(n, sizeof(int));
-    for (int i = n - 1; i >= 0; i--) {
-        uint64_t idx = table_index(o, i, cfg_of);
-        cfg_of[o->seq[i]] = o->A[i][idx];
+    back_substitute(o);
+    return 0;
+}
+
+/* The breadth-first recurrence, eq. (2) of Sec. III-A, written as printed:
+ * the sequence is a breadth-first traversal from vertex 0 (neighbours taken
+ * in ascending id order), D_B(i) = N(V_{<=i}) intersected with V_{>i}, and
+ *   B(i, phi) = min over C of  H(i, phi') + B(i-1, phi'|D_B(i-1)),
+ *   phi' = phi U {(v_i, C)},  B(before the first position) = 0,
+ * with H the node function of eq. (3).  Ties keep the lowest C.  The tables
+ * are stored like those of oracle_solve (canonical order over D_B(i)), so the
+ * same getters read them; B(|V|, empty) is the minimum and back-substitution
+ * recovers the strategy.  max_cells / nthreads as in oracle_solve. */
+int oracle_solve_bf(oracle_t *o, uint64_t max_cells, int nthreads) {
+    if (!o->K) return fail(o, "configs not enumerated");
+    free_tables(o);
+    int n = o->nv;
+    o->seq = calloc(n, sizeof(int)); o->pos = calloc(n, sizeof(int));
+    o->D = calloc(n, sizeof(int *)); o->nD = calloc(n, sizeof(int));
+    for (int i = 0; i < n; i++) o->D[i] = calloc(n, sizeof(int));
+    o->N = calloc(n, sizeof(uint64_t));
+    o->T = calloc(n, sizeof(uint64_t *)); o->A = calloc(n, sizeof(uint16_t *));
+    o->strategy = calloc(n, sizeof(int));
+    o->solved = 0; o->overflow = 0; o->cells_done = 0;
+
+    /* breadth-first traversal from vertex 0 (nbr[] lists are ascending) */
+    char *visited = calloc(n, 1);
+    int head = 0, tail = 0;
+    o->seq[tail++] = 0;
+    visited[0] = 1;
+    while (head < tail) {
+        int v = o->seq[head++];
+        for (int k = 0; k < o->deg[v]; k++) {
+            int u = o->nbr[v][k];
+            if (!visited[u]) { visited[u] = 1; o->seq[tail++] = u; }
+        }
     }
-    for (int v = 0; v < n; v++) o->strategy[v] = cfg_of[v];
-    free(cfg_of);
-    o->solved = 1;
+    free(visited);
+    if (tail != n) return fail(o, "graph is not weakly connected");
+    for (int i = 0; i < n; i++) o->pos[o->seq[i]] = i;
+
+    /* D_B(i) = N(V_{<=i}) intersected with V_{>i}, ascending vertex ids */
+    for (int i = 0; i < n; i++) {
+        o->nD[i] = 0;
+        for (int w = 0; w < n; w++) {
+            if (o->pos[w] <= i) continue;
+            int adjacent = 0;
+            for (int k = 0; k < o->deg[w] && !adjacent; k++) adjacent = o->pos[o->nbr[w][k]] <= i;
+            if (adjacent) o->D[i][o->nD[i]++] = w;
+        }
+    }
+    if (!table_sizes(o)) return fail(o, "table too large");
+
+    int *later = calloc(o->ne + 1, sizeof(int));
+    struct timespec t0, t1;
+    clock_gettime(CLOCK_MONOTONIC, &t0);
+    int stopped = 0;
+    for (int i = 0; i < n && !stopped; i++) {
+        int vi = o->seq[i];
+        /* H(i, .) charges the edges joining v_i and a later vertex */
+        int nlater = 0;
+        for (int e = 0; e < o->ne; e++) {
+            int a = o->src[e], b = o->dst[e];
+            if ((a == vi && o->pos[b] > i) || (b == vi && o->pos[a] > i)) later[nlater++] = e;
+        }
+        uint64_t N = o->N[i];
+        int Ki = o->K[vi];
+        o->T[i] = malloc(N * sizeof(uint64_t));
+        o->A[i] = malloc(N * sizeof(uint16_t));
+        int nd = o->nD[i];
+        const int *Di = o->D[i];
+        int ovf = 0;
+#ifdef _OPENMP
+        int nt = nthreads > 0 ? nthreads : 1;
+#pragma omp parallel num_threads(nt) reduction(| : ovf)
+#endif
+        {
+            int *cfg_of = malloc(n * sizeof(int));
+            for (int v = 0; v < n; v++) cfg_of[v] = -1;
+#ifdef _OPENMP
+#pragma omp for schedule(static)
+#endif
+            for (int64_t phi = 0; phi < (int64_t)N; phi++) {
+                uint64_t rem = (uint64_t)phi;
+                for (int k = nd - 1; k >= 0; k--) {
+                    uint64_t Kw = (uint64_t)o->K[Di[k]];
+                    cfg_of[Di[k]] = (int)(rem % Kw);
+                    rem /= Kw;
+                }
+                uint64_t best = UINT64_MAX;
+                int arg = 0;
+                for (int c = 0; c < Ki; c++) {
+                    cfg_of[vi] = c;
+                    uint64_t cost;
+                    if (!node_cost(o, i, later, nlater, cfg_of, &cost)) { ovf = 1; break; }
+                    /* + B(i-1, phi'|D_B(i-1)); D_B(i-1) lies within D_B(i) + {v_i} */
+                    if (i > 0 && !add_ok(cost, o->T[i - 1][table_index(o, i - 1, cfg_of)], &cost)) {
+                        ovf = 1;
+                        break;
+                    }
+                    if (cost < best) { best = cost; arg = c; }
+                }
+                o->T[i][phi] = best;
+                o->A[i][phi] = (uint16_t)arg;
+            }
+            free(cfg_of);
+        }
+        if (ovf) { o->overflow = 1; stopped = 1; break; }
+        o->cells_done += N * (uint64_t)Ki;
+        if (max_cells && o->cells_done >= max_cells && i + 1 < n) stopped = 2;
+    }
+    clock_gettime(CLOCK_MONOTONIC, &t1);
+    o->seconds = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
+    free(later);
+    if (o->overflow) return fail(o, "cost overflows uint64");
+    if (stopped == 2) return 2;
+    back_substitute(o);
     return 0;
 }
 

@@ -514,6 +514,115 @@ def test_disconnected_graph_rejected():
         o.solve()
 
 
+
+# ------------------------------------------------------------------ breadth-first recurrence (eq. 2)
+def _bfs_order(g):
+    """Breadth-first traversal from vertex 0, neighbours in ascending id
+    (collections.deque; independent of the oracle's traversal)."""
+    from collections import deque
+    nb = pins.neighbours(len(g["vertices"]), [e["src"] for e in g["edges"]], [e["dst"] for e in g["edges"]])
+    order, seen, q = [], {0}, deque([0])
+    while q:
+        v = q.popleft()
+        order.append(v)
+        for u in sorted(nb[v]):
+            if u not in seen:
+                seen.add(u)
+                q.append(u)
+    return order, nb
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_bf_recurrence_against_brute_force(seed):
+    """Eq. (2): the order is a breadth-first traversal, D_B(i) = N(V<=i) after
+    i, B(|V|, empty) is the minimum over all strategies, and every entry of
+    every table B_i (with its lowest-index argmin) equals the exhaustive
+    conditioned search; model costs and dense random ties; both configuration
+    sets."""
+    from oracle.oracle import Oracle
+    all_int = seed % 4 == 3
+    p = 6 if all_int else 4
+    g = random_graph(seed + 500, n=3 + seed % 5, p=p, max_dims=2, extra_edges=seed % 4)
+    o = Oracle(g)
+    K = [int(k) for k in o.configs(p, all_integers=all_int)]
+    if seed % 2:
+        o.set_costs(*random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4))
+    o.solve_bf()
+    L, R, src, dst = _tables(o, g)
+    order, nb = _bfs_order(g)
+    assert o.sequence() == order
+    mc, strat = o.result()
+    bf_min, optimal = pins.brute_force(L, R, src, dst)
+    assert mc == bf_min and pins.total_cost(strat, L, R, src, dst) == mc and bool(optimal[tuple(strat)])
+    for i in range(len(order)):
+        assert o.dependent_set(i) == pins.bfs_dependent_set(nb, order, i)
+        D, T, A = pins.conditioned_table(L, R, src, dst, order, i, K)
+        assert D == o.dependent_set(i)
+        To, Ao = o.table(i)
+        assert To.tolist() == T and Ao.tolist() == A, i
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_bf_recurrence_is_recurrence4_on_a_bf_order(seed):
+    """On a breadth-first order V<=i is connected, so X(i) = V<=i, D(i) = D_B(i)
+    and S(i) = {V<=i-1}: recurrence (4) over that order gives the same tables,
+    entry by entry, as the chain recurrence (2)."""
+    from oracle.oracle import Oracle
+    g = random_graph(seed + 520, n=6 + seed % 4, p=8, max_dims=3, extra_edges=2 + seed % 3)
+    a, b = Oracle(g), Oracle(g)
+    a.configs(8)
+    b.configs(8)
+    a.solve_bf()
+    order, _ = _bfs_order(g)
+    b.solve(order=order)
+    assert a.sequence() == b.sequence() == order
+    assert a.result() == b.result()
+    for i in range(len(order)):
+        assert a.dependent_set(i) == b.dependent_set(i)
+        Ta, Aa = a.table(i)
+        Tb, Ab = b.table(i)
+        assert np.array_equal(Ta, Tb) and np.array_equal(Aa, Ab)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_bf_recurrence_viterbi_on_chains(seed):
+    """A path numbered from one end: the breadth-first order is the path and
+    eq. (2) is the Viterbi recursion."""
+    from oracle.oracle import Oracle
+    g = chain_graph(seed + 40, n=5 + seed, p=8, max_dims=3)
+    o = Oracle(g)
+    o.configs(8)
+    o.solve_bf()
+    assert o.sequence() == list(range(len(g["vertices"])))
+    L, R, src, dst = _tables(o, g)
+    forward = [e["src"] < e["dst"] for e in g["edges"]]
+    mc, strat = o.result()
+    vmin, _ = pins.viterbi_chain(L, R, forward)
+    tmin, tstrat = pins.viterbi_table_strategy(L, R, forward)
+    assert mc == vmin == tmin and strat == tstrat
+
+
+def test_bf_dependent_sets_blow_up_on_dense_graphs():
+    """The contrast of Table I: on the Inception-style and Transformer graphs
+    the breadth-first dependent sets reach 8 and 19 vertices (tables past
+    2^34 entries, refused), while GenerateSeq keeps them at 2 and 3; on the
+    FC chain both orders give the same 310 cells."""
+    from oracle.oracle import Oracle, OracleError
+    for name, want, ours in (("w2_inception", 8, 2), ("w4_transformer", 19, 3)):
+        g = workload(name)
+        order, nb = _bfs_order(g)
+        assert max(len(pins.bfs_dependent_set(nb, order, i)) for i in range(len(order))) == want
+        o = Oracle(g)
+        o.configs(g["p"])
+        with pytest.raises(OracleError):
+            o.solve_bf()
+        o.solve(max_cells=1)
+        assert max(len(o.dependent_set(i)) for i in range(len(order))) == ours
+    o = Oracle(fc_chain())
+    o.configs(4)
+    o.solve_bf()
+    assert o.result() == (8_388_608, [9, 9, 9, 9]) and o.cells() == 310
+
 # ------------------------------------------------------------------ planted mistakes
 MUTANTS = {
     "tie_break_last": ("if (cost < mincost) { mincost = cost; arg = c; }",
@@ -533,6 +642,12 @@ MUTANTS = {
     "no_match_check": ("if (su != sv) match = 0;", "if (su != sv) match = 1;"),
     "budget_difference": ("if (!enum_rec(d, k + 1, budget / s, pow2, cur, out, count, cap)) return 0;",
                           "if (!enum_rec(d, k + 1, budget - s + 1, pow2, cur, out, count, cap)) return 0;"),
+    "bf_no_chain_term": ("if (i > 0 && !add_ok(cost, o->T[i - 1][table_index(o, i - 1, cfg_of)], &cost)) {",
+                         "if (i > 1 && !add_ok(cost, o->T[i - 1][table_index(o, i - 1, cfg_of)], &cost)) {"),
+    "bf_dependent_inclusive": ("for (int k = 0; k < o->deg[w] && !adjacent; k++) adjacent = o->pos[o->nbr[w][k]] <= i;",
+                               "for (int k = 0; k < o->deg[w] && !adjacent; k++) adjacent = o->pos[o->nbr[w][k]] < i;"),
+    "bf_earlier_edges": ("if ((a == vi && o->pos[b] > i) || (b == vi && o->pos[a] > i)) later[nlater++] = e;",
+                         "if ((a == vi && o->pos[b] < i) || (b == vi && o->pos[a] < i)) later[nlater++] = e;"),
     "pow2_only": ("for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {",
                   "for (uint64_t s = 1; s <= budget; s = 2 * s) {"),
 }
@@ -607,7 +722,26 @@ def _pin_suite(lib):
                 and int(o.layer_costs(0)[sf.index((1, 2, 3))]) == 1_529_174
                 and int(o.edge_costs(0)[sf.index((3, 1, 1)), sf.index((1, 1, 3))]) == 43_696)
 
+    def bf():
+        for seed in range(4):
+            g = random_graph(seed + 500, n=4 + seed, p=4, max_dims=2, extra_edges=1 + seed % 3)
+            o = Oracle(g, lib)
+            K = [int(k) for k in o.configs(4)]
+            o.set_costs(*random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4))
+            o.solve_bf()
+            L, R, src, dst = _tables(o, g)
+            order = o.sequence()
+            for i in range(len(order)):
+                D, T, A = pins.conditioned_table(L, R, src, dst, order, i, K)
+                To, Ao = o.table(i)
+                if o.dependent_set(i) != D or To.tolist() != T or Ao.tolist() != A:
+                    return False
+            if o.result()[0] != pins.brute_force(L, R, src, dst)[0]:
+                return False
+        return True
+
     guard("w0", w0)
+    guard("bf", bf)
     guard("all_integers", all_integers)
     guard("hand_costs", hand_costs)
     guard("edge_costs", edge_costs)
