@@ -37,12 +37,15 @@ def cpu_threads():
     return max(1, n)
 
 
-def oracle_baseline(g, p, max_cells, all_integers=False):
+def oracle_baseline(g, p, max_cells, all_integers=False, bf=False):
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
     o.configs(p, all_integers=all_integers)
-    o.solve(max_cells=max_cells, threads=threads)
+    if bf:
+        o.solve_bf(max_cells=max_cells, threads=threads)
+    else:
+        o.solve(max_cells=max_cells, threads=threads)
     done = o.cells_done()
     n_done = 0
     cum = 0
@@ -91,19 +94,38 @@ def traffic_from_profile():
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
-def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False):
+def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
-    or at `p` with every integer split when `all_integers`); returns the report
+    or at `p` with every integer split when `all_integers`; over the
+    breadth-first order, i.e. recurrence (2), when `bf`); returns the report
     dict (the oracle timed on the same graph: the whole search when it has at
-    most `cpu_cells` cells, else a prefix of the vertex order)."""
+    most `cpu_cells` cells, else a prefix of the vertex order).  A search the
+    library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import OPT_PROFILE, Graph
+    from paper_2407_04001_amd import OPT_ORDER, OPT_PROFILE, Graph, PaseError
     from workloads import workload
 
     g = workload(name, seed)
     p = p or g["p"]
     pg = Graph(g)
-    pg.enumerate_configs(p, all_integers=all_integers)
+    pg.set_option(OPT_ORDER, int(bf))
+    wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
+    if all_integers:
+        wl += ", every integer split"
+    if bf:
+        wl += ", breadth-first order (eq. 2)"
+    headline = name == "w4_transformer" and p == g["p"] and not all_integers and not bf
+    metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
+    config = {"workload": g["name"], "p": p,
+              "config_set": "every integer split" if all_integers else "powers of two",
+              "order": "breadth-first" if bf else "GenerateSeq",
+              "vertices": len(g["vertices"]), "edges": len(g["edges"]), "seed": seed}
+    try:
+        pg.enumerate_configs(p, all_integers=all_integers)
+    except PaseError as e:
+        return {"metric": metric, "value": None, "unit": "cell-updates/s", "n_gpus": 1, "steps": 0,
+                "warmup": 0, "higher_is_better": True, "data": "synthetic", "config": config,
+                "refused": str(e)}
     pg.set_option(OPT_PROFILE, 1)
     stream = torch.cuda.current_stream()
 
@@ -132,27 +154,24 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     col_cells = st["rows_cells"] - st["stream_cells"]
     achieved = OPS_PER_CELL * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
     parity = None
-    gold_name = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
-    gold_path = os.path.join(ROOT, "tests", "golden", gold_name)
-    if os.path.exists(gold_path) and (all_integers or p == g["p"]):
+    if bf:
+        gold_name = f"{name}_seed{seed}_p{p}_bf.json"
+    elif all_integers:
+        gold_name = f"{name}_seed{seed}_p{p}_all.json"
+    else:
+        gold_name = f"{name}_seed{seed}.json" if p == g["p"] else None
+    gold_path = os.path.join(ROOT, "tests", "golden", gold_name) if gold_name else None
+    if gold_path and os.path.exists(gold_path):
         with open(gold_path) as f:
             gold = json.load(f)
         parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
-    headline = name == "w4_transformer" and p == g["p"] and not all_integers
-    wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
-    if all_integers:
-        wl += ", every integer split"
-    metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
     out = {
         "metric": metric, "value": cells * steps / elapsed, "unit": "cell-updates/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup,
         "ms_per_step": elapsed * 1e3 / steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
-        "config": {"workload": g["name"], "p": p,
-                   "config_set": "every integer split" if all_integers else "powers of two",
-                   "vertices": len(g["vertices"]), "edges": len(g["edges"]), "cells": cells,
-                   "seed": seed},
+        "config": dict(config, cells=cells),
         "find_best_strategy_ms": sum(walls) / len(walls),
         "fill_ms_per_step": fill_ms / steps,
         "fill_cells_per_s": cells / (fill_ms / steps / 1e3) if fill_ms else None,
@@ -166,7 +185,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
                      "cells_per_step": col_cells},
     }
     if not no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers)
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf)
     return out
 
 
@@ -186,6 +205,8 @@ def main():
     ap.add_argument("--p", type=int, default=0, help="modeled devices (default: the workload's own)")
     ap.add_argument("--all-integers", action="store_true",
                     help="every integer split factor (Sec. II's full C(v)) instead of powers of two")
+    ap.add_argument("--order", choices=("genseq", "bf"), default="genseq",
+                    help="vertex order: GenerateSeq (default) or breadth-first (recurrence 2)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -201,7 +222,7 @@ def main():
     names = WORKLOADS if args.all_workloads else [args.workload]
     for name in names:
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
-                           args.p or None, args.all_integers)
+                           args.p or None, args.all_integers, args.order == "bf")
         print(json.dumps(out), flush=True)
 
 

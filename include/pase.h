@@ -122,10 +122,18 @@ typedef enum {
     PASE_OPT_LATENCY_WORKERS = 11, /* dataflow schedule: workgroups that serve the latency queue
                                    (the chains of small vertices) before the bulk queue; 0 =
                                    chosen (default: one in 16), else clamped to [1, grid - 1] */
-    PASE_OPT_CONFIG_SET = 12    /* configuration set of the next pase_enumerate_configs: 0
+    PASE_OPT_CONFIG_SET = 12,   /* configuration set of the next pase_enumerate_configs: 0
                                    (default) power-of-two split factors, p = 2^L <= 65536; 1
                                    every tuple of positive integer factors (Sec. II's C(v)),
                                    1 <= p <= 255 */
+    PASE_OPT_ORDER = 13         /* vertex sequence: 0 (default) GenerateSeq (Fig. 3); 1 the
+                                   breadth-first order of Sec. III-A (from vertex 0, neighbours
+                                   in ascending id order), on which recurrence (4) is the
+                                   breadth-first recurrence (2): every prefix is connected, so
+                                   D(i) = D_B(i) and each table reads only its predecessor's.
+                                   Re-plans; TOO_LARGE when a dependent set exceeds
+                                   PASE_MAX_DEP or a table 2^31 entries (the blow-up that
+                                   motivates GenerateSeq) */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

@@ -169,12 +169,32 @@ extern "C" const char *pase_last_error(pase_graph_t g) { return g ? g->err.c_str
 // ------------------------------------------------------------------ planning
 namespace {
 
+// Breadth-first traversal from vertex 0, neighbours in ascending id order:
+// the sequence of the breadth-first recurrence (eq. 2).
+std::vector<int> bfs_order(pase_graph_t g) {
+    const size_t n = g->V.size();
+    std::vector<int> order;
+    order.reserve(n);
+    std::vector<char> seen(n, 0);
+    order.push_back(0);
+    seen[0] = 1;
+    for (size_t h = 0; h < order.size(); h++)
+        for (int u : g->nbr[order[h]])      // ascending, deduplicated
+            if (!seen[u]) { seen[u] = 1; order.push_back(u); }
+    return order;
+}
+
 // GenerateSeq (Fig. 3): repeatedly sequence the unsequenced vertex with the
 // smallest d-set (ties: lowest vertex id); every member of its d-set absorbs
 // it.  rule 0 keeps a vertex out of its own d-set; rule 1 applies the printed
 // update literally.  The d-set at selection (minus the vertex) is D(i)
-// (Theorem 2).  Bitsets, one per vertex.
-void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector<int>> &Dpos) {
+// (Theorem 2).  Bitsets, one per vertex.  With a fixed `order` the same
+// absorption runs along that order instead of the smallest-d-set choice: the
+// d-set of a vertex then still holds the unsequenced neighbours of the
+// sequenced component it would join, so at selection it is D(i) =
+// N(X(i)) after i for that order (for a breadth-first order, D_B(i)).
+void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector<int>> &Dpos,
+                  const std::vector<int> *order = nullptr) {
     const size_t n = g->V.size(), W = (n + 63) / 64;
     std::vector<uint64_t> d(n * W, 0);
     auto has = [&](size_t v, size_t u) { return (d[v * W + u / 64] >> (u % 64)) & 1ull; };
@@ -193,8 +213,12 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
     Dpos.assign(n, {});
     for (size_t i = 0; i < n; i++) {
         size_t best = n;
-        for (size_t u = 0; u < n; u++)
-            if (!done[u] && (best == n || size[u] < size[best])) best = u;
+        if (order) {
+            best = (size_t)(*order)[i];
+        } else {
+            for (size_t u = 0; u < n; u++)
+                if (!done[u] && (best == n || size[u] < size[best])) best = u;
+        }
         const size_t vi = best;
         done[vi] = 1;
         seq.push_back((int)vi);
@@ -371,7 +395,12 @@ static pase_status build_plan(pase_graph_t g) {
     Plan &P = g->plan;
     P = Plan();
     std::vector<std::vector<int>> Dpos;
-    generate_seq(g, P.seq, Dpos);
+    if (g->order_mode == 1) {
+        const std::vector<int> order = bfs_order(g);
+        generate_seq(g, P.seq, Dpos, &order);
+    } else {
+        generate_seq(g, P.seq, Dpos);
+    }
     P.pos.assign(n, 0);
     for (int i = 0; i < n; i++) P.pos[P.seq[i]] = i;
     P.v.assign(n, VPlan());
@@ -897,6 +926,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "latency workers <= 65535");
         g->lat_workers = (uint32_t)value;
         break;
+    case PASE_OPT_ORDER:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "order 0 or 1");
+        g->order_mode = (int)value;
+        break;
     case PASE_OPT_CONFIG_SET:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "config set 0 or 1");
         g->config_set = (uint32_t)value;
@@ -910,7 +943,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     // options that change the plan need a fresh enumeration
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
-         opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS) &&
+         opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER) &&
         g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);

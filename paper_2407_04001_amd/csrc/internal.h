@@ -295,6 +295,7 @@ struct pase_graph_s {
     uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
     uint32_t lat_workers = 0;       // dataflow latency workers, 0 = chosen
     int schedule = 0;               // pase_option PASE_OPT_SCHEDULE (SchedKind)
+    int order_mode = 0;             // pase_option PASE_OPT_ORDER: 0 GenerateSeq, 1 breadth-first
     // configurations
     bool enumerated = false;
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs

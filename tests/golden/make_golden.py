@@ -7,7 +7,7 @@ strategy, the cell count, per-vertex fingerprints of the cost and argmin
 tables (canonical order, SplitMix64-based, see ``pase.h``) and a seeded sample
 of table entries.
 
-    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only]
+    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only]
 """
 from __future__ import annotations
 
@@ -26,29 +26,37 @@ sys.path.insert(0, ROOT)
 from oracle.oracle import Oracle, build  # noqa: E402
 from workloads import workload  # noqa: E402
 
-# (workload, seed, p, every integer split): p None = the workload's own
-# power-of-two p; the every-integer instances enumerate Sec. II's full C(v)
-INSTANCES = [("w0_fc_chain", 0, None, False), ("w1_residual_cnn", 0, None, False),
-             ("w1_residual_cnn", 1, None, False), ("w1_residual_cnn", 2, None, False),
-             ("w2_inception", 0, None, False), ("w2_inception", 1, None, False),
-             ("w2_inception", 2, None, False), ("w3_lstm_grid", 0, None, False),
-             ("w4_transformer", 0, None, False),
-             ("w0_fc_chain", 0, 12, True), ("w2_inception", 0, 12, True),
-             ("w4_transformer", 0, 12, True)]
+# (workload, seed, p, every integer split, breadth-first): p None = the
+# workload's own power-of-two p; the every-integer instances enumerate
+# Sec. II's full C(v); the breadth-first ones solve recurrence (2) instead of
+# GenerateSeq + recurrence (4)
+INSTANCES = [("w0_fc_chain", 0, None, False, False), ("w1_residual_cnn", 0, None, False, False),
+             ("w1_residual_cnn", 1, None, False, False), ("w1_residual_cnn", 2, None, False, False),
+             ("w2_inception", 0, None, False, False), ("w2_inception", 1, None, False, False),
+             ("w2_inception", 2, None, False, False), ("w3_lstm_grid", 0, None, False, False),
+             ("w4_transformer", 0, None, False, False),
+             ("w0_fc_chain", 0, 12, True, False), ("w2_inception", 0, 12, True, False),
+             ("w4_transformer", 0, 12, True, False),
+             ("w1_residual_cnn", 0, 64, False, True)]
 
 
-def file_name(name: str, seed: int, p=None, all_integers: bool = False) -> str:
+def file_name(name: str, seed: int, p=None, all_integers: bool = False, bf: bool = False) -> str:
+    if bf:
+        return f"{name}_seed{seed}_p{p}_bf.json"
     return f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
 SAMPLES_PER_TABLE = 24
 
 
-def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False) -> dict:
+def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False, bf: bool = False) -> dict:
     g = workload(name, seed)
     p = p or g["p"]
     o = Oracle(g)
     K = o.configs(p, all_integers=all_integers)
     t0 = time.time()
-    o.solve(rule=0, threads=threads)
+    if bf:
+        o.solve_bf(threads=threads)
+    else:
+        o.solve(rule=0, threads=threads)
     wall = time.time() - t0
     seq = o.sequence()
     mc, strat = o.result()
@@ -65,6 +73,7 @@ def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = Fals
         tables.append({"vertex": seq[i], "dep": o.dependent_set(i), "entries": n,
                        "fp_cost": str(fpT), "fp_arg": str(fpA), "samples": samples})
     return {"workload": name, "seed": seed, "p": p, "all_integers": all_integers,
+            "order": "breadth-first" if bf else "GenerateSeq",
             "num_configs": [int(k) for k in K],
             "sequence": seq, "min_cost": str(mc), "strategy": strat, "cells": o.cells(),
             "tables": tables, "oracle_seconds": round(wall, 3)}
@@ -76,16 +85,19 @@ def main():
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 1)
     ap.add_argument("--all-integers-only", action="store_true",
                     help="only the instances with every integer split")
+    ap.add_argument("--bf-only", action="store_true", help="only the breadth-first instances")
     args = ap.parse_args()
     build(force=False)
-    for name, seed, p, all_integers in INSTANCES:
+    for name, seed, p, all_integers, bf in INSTANCES:
         if args.only and args.only != name:
             continue
         if args.all_integers_only and not all_integers:
             continue
+        if args.bf_only and not bf:
+            continue
         t = time.time()
-        out = golden(name, seed, args.threads, p, all_integers)
-        path = os.path.join(HERE, file_name(name, seed, p, all_integers))
+        out = golden(name, seed, args.threads, p, all_integers, bf)
+        path = os.path.join(HERE, file_name(name, seed, p, all_integers, bf))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))
         print(f"{name} seed {seed}: min_cost {out['min_cost']} cells {out['cells']:.3e} "

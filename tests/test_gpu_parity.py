@@ -32,13 +32,16 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _oracle(g, p=None, costs=None, rule=0, all_integers=False):
+def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False):
     from oracle.oracle import Oracle
     o = Oracle(g)
     o.configs(p or g["p"], all_integers=all_integers)
     if costs is not None:
         o.set_costs(*costs)
-    o.solve(rule=rule, threads=os.cpu_count() or 1)
+    if bf:
+        o.solve_bf(threads=os.cpu_count() or 1)
+    else:
+        o.solve(rule=rule, threads=os.cpu_count() or 1)
     return o
 
 
@@ -66,8 +69,9 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0, all_integers=False):
+         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False):
     pg = P.Graph(g, seq_rule=rule)
+    pg.set_option(P.OPT_ORDER, int(bf))
     pg.enumerate_configs(p or g["p"], all_integers=all_integers)
     pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
@@ -255,20 +259,23 @@ def test_library_owned_workspace(P):
 
 
 # ------------------------------------------------------------------ full-size workloads
-def _golden(name, seed, p=None, all_integers=False):
-    fn = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
+def _golden(name, seed, p=None, all_integers=False, bf=False):
+    if bf:
+        fn = f"{name}_seed{seed}_p{p}_bf.json"
+    else:
+        fn = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
     with open(os.path.join(GOLDEN, fn)) as f:
         return json.load(f)
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False):
-    gold = _golden(name, seed, p, all_integers)
+                  lat_workers=0, p=None, all_integers=False, bf=False):
+    gold = _golden(name, seed, p, all_integers, bf)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers} p={p} all_integers={all_integers}")
+        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers, all_integers=all_integers)
+                         lat_workers=lat_workers, all_integers=all_integers, bf=bf)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -489,3 +496,54 @@ def test_all_integer_transformer_p24_properties(P):
     for e in range(len(src)):
         tot += int(o.edge_costs(e)[strat[src[e]], strat[dst[e]]])
     assert tot == mc
+
+
+# ------------------------------------------------------------------ breadth-first recurrence (eq. 2)
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("key", [0, 1])
+def test_bf_order_random_graphs(P, seed, key):
+    """PASE_OPT_ORDER = 1 against the oracle's literal eq. (2): sequence,
+    D_B sets, every table entry, minimum and strategy; model costs, and dense
+    ties on odd seeds."""
+    g = random_graph(seed + 540, n=4 + seed % 5, p=8, max_dims=3, extra_edges=1 + seed % 3)
+    costs = None
+    if seed % 2:
+        o0 = _oracle(g)
+        K = [int(k) for k in o0.K]
+        costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    say(f"breadth-first random graph seed={seed + 540} key={key} ties={costs is not None}")
+    o = _oracle(g, costs=costs, bf=True)
+    pg, mc, strat = _run(P, g, key=key, costs=costs, bf=True)
+    assert pg.sequence() == o.sequence()
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=1024)
+
+
+def test_bf_order_kernels_and_schedules(P):
+    """The breadth-first chain of tables on the generic kernel, uint64 keys
+    and the sequential, lane and dataflow schedules: the same answer."""
+    g = random_graph(560, n=9, p=16, max_dims=3, extra_edges=3, max_size=256)
+    o = _oracle(g, bf=True)
+    for kw in ({}, {"kernel": 1}, {"key": 1}, {"schedule": 1}, {"schedule": 2}, {"schedule": 3}):
+        say(f"breadth-first seed=560 {kw}")
+        pg, mc, strat = _run(P, g, bf=True, **kw)
+        assert (mc, strat) == o.result()
+        _compare_all_entries(pg, o, g, max_entries=256)
+
+
+def test_bf_order_workloads(P):
+    """W0 and the residual CNN (three seeds) under the breadth-first order
+    against the oracle's eq. (2), every table fingerprinted; the residual CNN
+    at p = 64 (6.9e8 cells) against the stored golden."""
+    for name, seed in (("w0_fc_chain", 0), ("w1_residual_cnn", 0), ("w1_residual_cnn", 1),
+                       ("w1_residual_cnn", 2)):
+        g = workload(name, seed)
+        say(f"breadth-first {name} seed={seed}")
+        o = _oracle(g, bf=True)
+        pg, mc, strat = _run(P, g, bf=True)
+        assert pg.sequence() == o.sequence()
+        assert (mc, strat) == o.result()
+        for i, v in enumerate(o.sequence()):
+            assert pg.fingerprint(v) == o.fingerprint(i)
+    _check_golden(P, "w1_residual_cnn", 0, p=64, bf=True, keep=False)
+    _check_golden(P, "w1_residual_cnn", 0, p=64, bf=True, keep=True)

@@ -212,6 +212,48 @@ def test_workload_keys_fit_fp64(pase, name, p, all_int):
         assert (info["key_bound"] + 1) << bits <= 1 << 53, v
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_bf_order_sequence_and_dependent_sets(pase, seed):
+    """PASE_OPT_ORDER = 1: the library's sequence is the oracle's breadth-first
+    order and its dependent sets are D_B(i) (eq. 2), for both seq rules."""
+    from oracle.oracle import Oracle
+    g = random_graph(seed + 40, n=4 + seed % 9, extra_edges=seed % 6, p=4)
+    o = Oracle(g)
+    o.configs(4)
+    o.solve_bf(max_cells=1)
+    seq = o.sequence()
+    nb = pins.neighbours(len(seq), [e["src"] for e in g["edges"]], [e["dst"] for e in g["edges"]])
+    for rule in (0, 1):
+        pg = pase.Graph(g, seq_rule=rule)
+        pg.set_option(pase.OPT_ORDER, 1)
+        pg.enumerate_configs(4)
+        assert pg.sequence() == seq
+        for i, v in enumerate(seq):
+            assert pg.dependent_set(v) == o.dependent_set(i) == pins.bfs_dependent_set(nb, seq, i)
+
+
+def test_bf_order_option(pase):
+    """The order option re-plans an enumerated graph; the dense workloads are
+    refused under the breadth-first order (dependent sets of 8 and 19), and
+    switching back to GenerateSeq plans them again."""
+    P = pase
+    pg = P.Graph(workload("w1_residual_cnn"))
+    pg.enumerate_configs(8)
+    pg.set_option(P.OPT_ORDER, 1)
+    assert pg.sequence()[0] == 0
+    assert sum(pg.vertex_info(v)["cells"] for v in range(len(pg.K))) == 1_254_456
+    for name in ("w2_inception", "w4_transformer"):
+        g = workload(name)
+        pg = P.Graph(g)
+        pg.set_option(P.OPT_ORDER, 1)
+        assert _status(lambda: pg.enumerate_configs(g["p"])) == P.TOO_LARGE
+        pg.set_option(P.OPT_ORDER, 0)
+        pg.enumerate_configs(g["p"])
+        assert _status(lambda: pg.set_option(P.OPT_ORDER, 1)) == P.TOO_LARGE
+        assert _status(lambda: pg.sequence()) == P.BAD_STATE
+    assert _status(lambda: P.pase_set_option(pg.h, P.OPT_ORDER, 2)) == P.INVALID_ARGUMENT
+
+
 @pytest.mark.parametrize("seed", range(20))
 @pytest.mark.parametrize("rule", [0, 1])
 def test_sequence_and_dependent_sets(pase, seed, rule):
