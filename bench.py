@@ -56,7 +56,8 @@ def oracle_baseline(g, p, max_cells, all_integers=False, bf=False):
         if cum >= done:
             break
     return {"value": done / o.seconds(), "unit": "cell-updates/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n_done} of {len(seq)} vertices of the same GenerateSeq order "
+            "sample": f"first {n_done} of {len(seq)} vertices of the same "
+                      f"{'breadth-first' if bf else 'GenerateSeq'} order "
                       f"({done:.3e} of {o.cells():.3e} cells, {o.seconds():.1f} s, "
                       f"OpenMP over table entries)"}
 
