@@ -45,6 +45,7 @@ def _load(path: str | None = None):
     L.oracle_error.argtypes = [P]
     L.oracle_configs.argtypes = [P, I]
     L.oracle_configs_all.argtypes = [P, I]
+    L.oracle_set_transfer_model.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
     L.oracle_solve_bf.argtypes = [P, U64, I]
@@ -125,9 +126,12 @@ class Oracle:
         return rc
 
     # -- configurations and costs
-    def configs(self, p: int, all_integers: bool = False):
+    def configs(self, p: int, all_integers: bool = False, volume: bool = False):
         """C(v) for p devices: power-of-two splits (p = 2^L), or with
-        all_integers every tuple of positive integers with product <= p."""
+        all_integers every tuple of positive integers with product <= p; the
+        transfer costs follow the split-match model, or with `volume` the
+        volume-intersection model."""
+        self._check(self._L.oracle_set_transfer_model(self._h, 1 if volume else 0))
         fn = self._L.oracle_configs_all if all_integers else self._L.oracle_configs
         self._check(fn(self._h, int(p)))
         self.p = p

@@ -45,6 +45,7 @@ typedef struct {
     int *src_dim, *dst_dim;  /* ne*MAXD */
     uint64_t *elems;         /* ne */
     uint64_t r;              /* FLOP-to-byte ratio weighting communication */
+    int xmodel;              /* transfer cost: 0 split match, 1 volume intersection */
     /* configurations */
     int p;
     int *K;                  /* configs per vertex */
@@ -226,6 +227,73 @@ static int transfer_cost(oracle_t *o, int e, const uint32_t *su_, const uint32_t
     return mul_ok(o->r, words, out);
 }
 
+/* Volume-intersection transfer cost (Sec. II).  A(v,d) is the part of the
+ * edge's tensor that consumer v needs on device d, A(u,d) the part producer u
+ * holds there:
+ *   forward  = max_d |A(v,d)| - |A(v,d) n A(u,d)|
+ *   backward = max_d |A(u,d)| - |A(u,d) n A(v,d)|   (the gradient flows back)
+ *   out      = r * (ceil(forward) + ceil(backward))  in words.
+ * Device d of a configuration with P = prod s_k devices is the grid point
+ * whose mixed-radix digits (loop dim 0 slowest) spell d; devices d >= P take
+ * no part.  A tensor dim is cut into s equal parts on each side by the split s
+ * of the loop dim it maps to there (1 when unmapped, so loop dims that no
+ * tensor dim maps to replicate); a part is then a box of fractions of the
+ * tensor.  Fractions are counted exactly on a grid of L_t = s_u * s_v cells
+ * per tensor dim (cell c lies in part floor(c * s / L_t) of a side). */
+static int transfer_volume(oracle_t *o, int e, const uint32_t *su_, const uint32_t *sv_, uint64_t *out) {
+    int u = o->src[e], v = o->dst[e], R = o->rank[e];
+    uint64_t Pu = 1, Pv = 1;
+    for (int k = 0; k < o->ndims[u]; k++) Pu *= su_[k];
+    for (int k = 0; k < o->ndims[v]; k++) Pv *= sv_[k];
+    uint64_t su[MAXD], sv[MAXD];
+    unsigned __int128 cells = 1;                 /* grid cells of the whole tensor */
+    for (int t = 0; t < R; t++) {
+        int a = o->src_dim[e * MAXD + t], b = o->dst_dim[e * MAXD + t];
+        su[t] = a >= 0 ? su_[a] : 1;
+        sv[t] = b >= 0 ? sv_[b] : 1;
+        cells *= (unsigned __int128)(su[t] * sv[t]);
+    }
+    unsigned __int128 fwd = 0, bwd = 0;          /* in cells */
+    for (uint64_t d = 0; d < (Pu > Pv ? Pu : Pv); d++) {
+        int on_u = d < Pu, on_v = d < Pv;
+        uint64_t xu_loop[MAXD] = {0}, xv_loop[MAXD] = {0}, x;
+        x = d;
+        for (int k = o->ndims[u] - 1; k >= 0; k--) { xu_loop[k] = x % su_[k]; x /= su_[k]; }
+        x = d;
+        for (int k = o->ndims[v] - 1; k >= 0; k--) { xv_loop[k] = x % sv_[k]; x /= sv_[k]; }
+        unsigned __int128 need_v = 1, hold_u = 1, common = 1;
+        for (int t = 0; t < R; t++) {
+            int a = o->src_dim[e * MAXD + t], b = o->dst_dim[e * MAXD + t];
+            uint64_t xu = a >= 0 ? xu_loop[a] : 0, xv = b >= 0 ? xv_loop[b] : 0;
+            uint64_t L = su[t] * sv[t], nv_ = 0, nu_ = 0, both = 0;
+            for (uint64_t c = 0; c < L; c++) {
+                int in_v = c * sv[t] / L == xv, in_u = c * su[t] / L == xu;
+                nv_ += in_v;
+                nu_ += in_u;
+                both += in_v && in_u;
+            }
+            need_v *= nv_;
+            hold_u *= nu_;
+            common *= both;
+        }
+        unsigned __int128 f = on_v ? need_v - (on_u ? common : 0) : 0;
+        unsigned __int128 g = on_u ? hold_u - (on_v ? common : 0) : 0;
+        if (f > fwd) fwd = f;
+        if (g > bwd) bwd = g;
+    }
+    unsigned __int128 E = o->elems[e];
+    unsigned __int128 words = (E * fwd + cells - 1) / cells + (E * bwd + cells - 1) / cells;
+    if (words >> 64) return 0;
+    return mul_ok(o->r, (uint64_t)words, out);
+}
+
+/* Transfer cost model for the next configuration enumeration. */
+int oracle_set_transfer_model(oracle_t *o, int model) {
+    if (model < 0 || model > 1) return fail(o, "transfer model 0 or 1");
+    o->xmodel = model;
+    return 0;
+}
+
 /* Enumerate C(v) for every v and fill the cost tables. */
 static int configs(oracle_t *o, int p, int pow2) {
     free_tables(o);
@@ -254,16 +322,22 @@ static int configs(oracle_t *o, int p, int pow2) {
             if (!layer_cost(o, v, o->sp[v] + (size_t)c * d, &o->Lc[v][c]))
                 return fail(o, "layer cost overflows uint64");
     }
+    int bad = 0;
+    for (int e = 0; e < o->ne; e++)
+        o->Rx[e] = calloc((size_t)o->K[o->src[e]] * o->K[o->dst[e]], sizeof(uint64_t));
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+#endif
     for (int e = 0; e < o->ne; e++) {
         int u = o->src[e], v = o->dst[e];
-        o->Rx[e] = calloc((size_t)o->K[u] * o->K[v], sizeof(uint64_t));
         for (int cu = 0; cu < o->K[u]; cu++)
-            for (int cv = 0; cv < o->K[v]; cv++)
-                if (!transfer_cost(o, e, o->sp[u] + (size_t)cu * o->ndims[u],
-                                   o->sp[v] + (size_t)cv * o->ndims[v],
-                                   &o->Rx[e][(size_t)cu * o->K[v] + cv]))
-                    return fail(o, "transfer cost overflows uint64");
+            for (int cv = 0; cv < o->K[v]; cv++) {
+                const uint32_t *a = o->sp[u] + (size_t)cu * o->ndims[u], *b = o->sp[v] + (size_t)cv * o->ndims[v];
+                uint64_t *x = &o->Rx[e][(size_t)cu * o->K[v] + cv];
+                if (!(o->xmodel ? transfer_volume(o, e, a, b, x) : transfer_cost(o, e, a, b, x))) bad = 1;
+            }
     }
+    if (bad) return fail(o, "transfer cost overflows uint64");
     return 0;
 }
 

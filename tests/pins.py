@@ -238,6 +238,49 @@ def conditioned_qmax(L, R, src, dst, seq, i, Ks, limit: int = 2_000_000) -> int:
     return max(best.values())
 
 
+def volume_transfer_elements(m, src_dim, dst_dim, s_src, s_dst, r) -> int:
+    """r * t_x of the volume model by enumerating tensor elements: tensor
+    dims of sizes m (each divisible by the splits that cut it), element index
+    i of dim t lies in part i * s // m_t on a side whose loop dim (mapped by
+    src_dim / dst_dim, -1 = unmapped, s = 1) is split s ways; device d of a
+    configuration is the mixed-radix grid point spelled by d (loop dim 0
+    slowest), devices past the product take no part.  Forward = the largest
+    count of elements a consumer device needs but does not hold, backward the
+    same with the roles swapped; r * (forward + backward)."""
+    def coords(d, splits):
+        out = [0] * len(splits)
+        for k in range(len(splits) - 1, -1, -1):
+            out[k] = d % splits[k]
+            d //= splits[k]
+        return out
+
+    Pu, Pv = int(np.prod(s_src)), int(np.prod(s_dst))
+    elems = list(itertools.product(*[range(x) for x in m]))
+
+    def part(side_dims, splits, xs):
+        keep = set()
+        for el in elems:
+            ok = True
+            for t, i in enumerate(el):
+                k = side_dims[t]
+                s = splits[k] if k >= 0 else 1
+                x = xs[k] if k >= 0 else 0
+                if i * s // m[t] != x:
+                    ok = False
+                    break
+            if ok:
+                keep.add(el)
+        return keep
+
+    fwd = bwd = 0
+    for d in range(max(Pu, Pv)):
+        A_u = part(src_dim, s_src, coords(d, s_src)) if d < Pu else set()
+        A_v = part(dst_dim, s_dst, coords(d, s_dst)) if d < Pv else set()
+        fwd = max(fwd, len(A_v - A_u))
+        bwd = max(bwd, len(A_u - A_v))
+    return r * (fwd + bwd)
+
+
 def splitmix64_mix(z: int) -> int:
     """SplitMix64 output function (Steele, Lea and Flood, 2014)."""
     m = (1 << 64) - 1

@@ -515,6 +515,107 @@ def test_disconnected_graph_rejected():
 
 
 
+
+# ------------------------------------------------------------------ volume-intersection transfer cost
+def test_volume_transfer_hand_values():
+    """FC chain p = 4, edge fc0 -> fc1, tensor (b, feat) = 16 384 words, r = 8.
+    (4,1,1) -> (4,1,1): device d holds and needs batch quarter d: 0.
+    (1,1,1) -> (4,1,1): forward, devices 1..3 need a quarter the producer's
+    single device does not give them (4096); backward, device 0 of the
+    producer needs the whole gradient but holds a quarter of it on the consumer
+    side (12 288): 8 * 16 384 = 131 072.
+    (2,2,1) -> (2,1,2): device b*2+x holds feat half x (out) and needs feat half
+    x (in): 0.  (1,2,2) -> (1,1,2): the producer's device d = 2*out + in holds
+    feat half d // 2, the consumer's device d needs half d: device 1 misses a
+    half forward, devices 1..3 a half backward: 8 * (8192 + 8192) = 131 072,
+    where the split-match model charges nothing (both split feat 2 ways)."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain())
+    o.configs(4, volume=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    R = o.edge_costs(0)
+    i = sp.index
+    assert int(R[i((4, 1, 1)), i((4, 1, 1))]) == 0
+    assert int(R[i((1, 1, 1)), i((4, 1, 1))]) == 131_072
+    assert int(R[i((2, 2, 1)), i((2, 1, 2))]) == 0
+    assert int(R[i((1, 2, 2)), i((1, 1, 2))]) == 131_072
+    o2 = Oracle(fc_chain())
+    o2.configs(4)
+    assert int(o2.edge_costs(0)[i((1, 2, 2)), i((1, 1, 2))]) == 0
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_volume_transfer_against_element_enumeration(seed):
+    """Every entry of the volume model's edge matrix on a random two-vertex
+    graph equals the count over individual tensor elements (sizes divisible by
+    every split, random dim maps with unmapped dims on either side)."""
+    from oracle.oracle import Oracle
+    rng = np.random.default_rng(seed)
+    p = (2, 4, 6)[seed % 3]
+    all_int = p == 6
+    du, dv = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+    rank = 1 if all_int else int(rng.integers(1, 3))
+    size = 60 if all_int else 12          # divisible by every split factor <= p
+    src_dim = [int(x) for x in rng.permutation(du)[:rank]] + [-1] * max(0, rank - du)
+    dst_dim = [int(x) for x in rng.permutation(dv)[:rank]] + [-1] * max(0, rank - dv)
+    src_dim, dst_dim = src_dim[:rank], dst_dim[:rank]
+    if seed % 4 == 1 and rank > 1:
+        src_dim[0] = -1
+    m = [size] * rank
+    g = {"name": "vol", "p": p, "comm_weight": 3,
+         "vertices": [{"name": "u", "dims": [size] * du, "dim_names": ["x"] * du, "reduce": [],
+                       "flops_per_point": 1},
+                      {"name": "v", "dims": [size] * dv, "dim_names": ["x"] * dv, "reduce": [],
+                       "flops_per_point": 1}],
+         "edges": [{"src": 0, "dst": 1, "src_dim": src_dim, "dst_dim": dst_dim, "elems": size ** rank}]}
+    o = Oracle(g)
+    K = o.configs(p, all_integers=all_int, volume=True)
+    R = o.edge_costs(0)
+    su, sv = o.splits(0), o.splits(1)
+    for cu in range(int(K[0])):
+        for cv in range(int(K[1])):
+            want = pins.volume_transfer_elements(m, src_dim, dst_dim, [int(x) for x in su[cu]],
+                                                 [int(x) for x in sv[cv]], 3)
+            assert int(R[cu, cv]) == want, (su[cu], sv[cv])
+
+
+def test_volume_transfer_symmetric_and_bounded():
+    """t_x does not depend on the edge's direction (reversing every edge
+    transposes every matrix), vanishes on identical unsplit ends, and never
+    exceeds twice the tensor (r * 2 * elems)."""
+    from oracle.oracle import Oracle
+    g = workload("w1_residual_cnn")
+    rev = dict(g, edges=[dict(e, src=e["dst"], dst=e["src"], src_dim=e["dst_dim"], dst_dim=e["src_dim"])
+                         for e in g["edges"]])
+    a, b = Oracle(g), Oracle(rev)
+    a.configs(4, volume=True)
+    b.configs(4, volume=True)
+    for k, e in enumerate(g["edges"]):
+        Ra, Rb = a.edge_costs(k), b.edge_costs(k)
+        assert np.array_equal(Ra, Rb.T)
+        assert int(Ra[0, 0]) == 0
+        assert int(Ra.max()) <= 2 * 8 * e["elems"]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_theorem1_volume_costs(seed):
+    """The DP is unchanged by the transfer model: with volume costs the
+    minimum equals exhaustive search and every table entry the conditioned
+    exhaustive search."""
+    from oracle.oracle import Oracle
+    g = random_graph(seed + 580, n=3 + seed % 3, p=4, max_dims=2, extra_edges=seed % 3)
+    o = Oracle(g)
+    K = [int(k) for k in o.configs(4, volume=True)]
+    o.solve()
+    L, R, src, dst = _tables(o, g)
+    mc, strat = o.result()
+    assert mc == pins.brute_force(L, R, src, dst)[0] == pins.total_cost(strat, L, R, src, dst)
+    seq = o.sequence()
+    for i in range(len(seq)):
+        D, T, A = pins.conditioned_table(L, R, src, dst, seq, i, K)
+        To, Ao = o.table(i)
+        assert To.tolist() == T and Ao.tolist() == A
+
 # ------------------------------------------------------------------ breadth-first recurrence (eq. 2)
 def _bfs_order(g):
     """Breadth-first traversal from vertex 0, neighbours in ascending id
@@ -648,6 +749,10 @@ MUTANTS = {
                                "for (int k = 0; k < o->deg[w] && !adjacent; k++) adjacent = o->pos[o->nbr[w][k]] < i;"),
     "bf_earlier_edges": ("if ((a == vi && o->pos[b] > i) || (b == vi && o->pos[a] > i)) later[nlater++] = e;",
                          "if ((a == vi && o->pos[b] < i) || (b == vi && o->pos[a] < i)) later[nlater++] = e;"),
+    "volume_forward_only": ("unsigned __int128 words = (E * fwd + cells - 1) / cells + (E * bwd + cells - 1) / cells;",
+                            "unsigned __int128 words = (E * fwd + cells - 1) / cells;"),
+    "volume_dim0_fastest": ("for (int k = o->ndims[u] - 1; k >= 0; k--) { xu_loop[k] = x % su_[k]; x /= su_[k]; }",
+                            "for (int k = 0; k < o->ndims[u]; k++) { xu_loop[k] = x % su_[k]; x /= su_[k]; }"),
     "pow2_only": ("for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {",
                   "for (uint64_t s = 1; s <= budget; s = 2 * s) {"),
 }
@@ -740,8 +845,34 @@ def _pin_suite(lib):
                 return False
         return True
 
+    def volume():
+        o = Oracle(fc_chain(), lib)
+        o.configs(4, volume=True)
+        sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+        R = o.edge_costs(0)
+        if int(R[sp.index((1, 2, 2)), sp.index((1, 1, 2))]) != 131_072:
+            return False
+        g = {"name": "vol", "p": 4, "comm_weight": 3,
+             "vertices": [{"name": "u", "dims": [12, 12], "dim_names": ["x", "y"], "reduce": [],
+                           "flops_per_point": 1},
+                          {"name": "v", "dims": [12, 12], "dim_names": ["x", "y"], "reduce": [],
+                           "flops_per_point": 1}],
+             "edges": [{"src": 0, "dst": 1, "src_dim": [1, 0], "dst_dim": [0, -1], "elems": 144}]}
+        o = Oracle(g, lib)
+        K = o.configs(4, volume=True)
+        R = o.edge_costs(0)
+        su, sv = o.splits(0), o.splits(1)
+        for cu in range(int(K[0])):
+            for cv in range(int(K[1])):
+                want = pins.volume_transfer_elements([12, 12], [1, 0], [0, -1], [int(x) for x in su[cu]],
+                                                     [int(x) for x in sv[cv]], 3)
+                if int(R[cu, cv]) != want:
+                    return False
+        return True
+
     guard("w0", w0)
     guard("bf", bf)
+    guard("volume", volume)
     guard("all_integers", all_integers)
     guard("hand_costs", hand_costs)
     guard("edge_costs", edge_costs)
