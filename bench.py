@@ -37,11 +37,11 @@ def cpu_threads():
     return max(1, n)
 
 
-def oracle_baseline(g, p, max_cells, all_integers=False, bf=False):
+def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False):
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
-    o.configs(p, all_integers=all_integers)
+    o.configs(p, all_integers=all_integers, volume=volume)
     if bf:
         o.solve_bf(max_cells=max_cells, threads=threads)
     else:
@@ -95,31 +95,37 @@ def traffic_from_profile():
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
-def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False):
+def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False,
+                 volume=False):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
-    breadth-first order, i.e. recurrence (2), when `bf`); returns the report
+    breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
+    transfer costs when `volume`); returns the report
     dict (the oracle timed on the same graph: the whole search when it has at
     most `cpu_cells` cells, else a prefix of the vertex order).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import OPT_ORDER, OPT_PROFILE, Graph, PaseError
+    from paper_2407_04001_amd import OPT_ORDER, OPT_PROFILE, OPT_TRANSFER, Graph, PaseError
     from workloads import workload
 
     g = workload(name, seed)
     p = p or g["p"]
     pg = Graph(g)
     pg.set_option(OPT_ORDER, int(bf))
+    pg.set_option(OPT_TRANSFER, int(volume))
     wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
     if all_integers:
         wl += ", every integer split"
     if bf:
         wl += ", breadth-first order (eq. 2)"
-    headline = name == "w4_transformer" and p == g["p"] and not all_integers and not bf
+    if volume:
+        wl += ", volume-intersection transfer costs"
+    headline = name == "w4_transformer" and p == g["p"] and not all_integers and not bf and not volume
     metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
     config = {"workload": g["name"], "p": p,
               "config_set": "every integer split" if all_integers else "powers of two",
               "order": "breadth-first" if bf else "GenerateSeq",
+              "transfer": "volume intersection" if volume else "split match",
               "vertices": len(g["vertices"]), "edges": len(g["edges"]), "seed": seed}
     try:
         pg.enumerate_configs(p, all_integers=all_integers)
@@ -157,6 +163,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     parity = None
     if bf:
         gold_name = f"{name}_seed{seed}_p{p}_bf.json"
+    elif volume:
+        gold_name = f"{name}_seed{seed}_volume.json" if p == g["p"] and not all_integers else None
     elif all_integers:
         gold_name = f"{name}_seed{seed}_p{p}_all.json"
     else:
@@ -186,7 +194,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
                      "cells_per_step": col_cells},
     }
     if not no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf)
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf, volume)
     return out
 
 
@@ -208,6 +216,8 @@ def main():
                     help="every integer split factor (Sec. II's full C(v)) instead of powers of two")
     ap.add_argument("--order", choices=("genseq", "bf"), default="genseq",
                     help="vertex order: GenerateSeq (default) or breadth-first (recurrence 2)")
+    ap.add_argument("--transfer", choices=("match", "volume"), default="match",
+                    help="transfer cost model: split match (default) or volume intersection")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -223,7 +233,8 @@ def main():
     names = WORKLOADS if args.all_workloads else [args.workload]
     for name in names:
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
-                           args.p or None, args.all_integers, args.order == "bf")
+                           args.p or None, args.all_integers, args.order == "bf",
+                           args.transfer == "volume")
         print(json.dumps(out), flush=True)
 
 

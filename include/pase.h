@@ -126,7 +126,7 @@ typedef enum {
                                    (default) power-of-two split factors, p = 2^L <= 65536; 1
                                    every tuple of positive integer factors (Sec. II's C(v)),
                                    1 <= p <= 255 */
-    PASE_OPT_ORDER = 13         /* vertex sequence: 0 (default) GenerateSeq (Fig. 3); 1 the
+    PASE_OPT_ORDER = 13,        /* vertex sequence: 0 (default) GenerateSeq (Fig. 3); 1 the
                                    breadth-first order of Sec. III-A (from vertex 0, neighbours
                                    in ascending id order), on which recurrence (4) is the
                                    breadth-first recurrence (2): every prefix is connected, so
@@ -134,6 +134,18 @@ typedef enum {
                                    Re-plans; TOO_LARGE when a dependent set exceeds
                                    PASE_MAX_DEP or a table 2^31 entries (the blow-up that
                                    motivates GenerateSeq) */
+    PASE_OPT_TRANSFER = 14      /* transfer cost model of the next pase_enumerate_configs: 0
+                                   (default) split match -- 0 when every tensor dim is split alike
+                                   at both ends, else ceil(elems / max(P_u, P_v)); 1 the volume
+                                   intersection of Sec. II, max_d |A(v,d)| - |A(v,d) n A(u,d)|
+                                   forward plus the same backward, with device d the mixed-radix
+                                   point of each configuration's split grid (loop dim 0 slowest)
+                                   and each tensor dim cut into equal fractions by the split of
+                                   the loop dim it maps to (words rounded up per direction).
+                                   Model 1 computes every edge's K_src x K_dst matrix on the
+                                   device (workspace grows by 8 bytes per entry) and needs the
+                                   mapped loop dims of each edge side distinct
+                                   (INVALID_ARGUMENT otherwise) */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

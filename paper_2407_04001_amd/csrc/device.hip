@@ -71,6 +71,26 @@ __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, cons
     }
 }
 
+// Volume-intersection model: every entry of every edge's K_src x K_dst cost
+// matrix (one thread per entry, grid-stride), into the matrix region the prep
+// kernel then reads like caller-given matrices.
+__global__ void k_edge_volume(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t ne,
+                              const uint8_t *__restrict__ ex, uint64_t *__restrict__ out, uint64_t total,
+                              uint64_t r) {
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
+         t += (uint64_t)gridDim.x * blockDim.x) {
+        uint32_t lo = 0, hi = ne;   // last edge with mat_off <= t
+        while (hi - lo > 1) {
+            uint32_t mid = (lo + hi) / 2;
+            if (E[mid].mat_off <= t) lo = mid; else hi = mid;
+        }
+        const DevEdge de = E[lo];
+        const DevVertex u = V[de.src], v = V[de.dst];
+        const uint64_t x = t - de.mat_off, cu = x / v.K, cv = x % v.K;
+        out[t] = volume_cost(u, ex + u.ex_off + cu * u.ndims, v, ex + v.ex_off + cv * v.ndims, de, r);
+    }
+}
+
 __global__ void k_edge_costs(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t e,
                              const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
                              uint64_t *__restrict__ out, uint64_t r) {
@@ -386,10 +406,10 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             Contrib c;
             std::memset(&c, 0, sizeof c);
             bool is_src = (int)g->E[e].src == vp.vi;
-            if (g->overridden) {
+            if (g->overridden || g->volume) {
                 c.kind = kContribTable;
                 c.raw_u64 = 1;
-                c.ptr = ovedge + g->ov_edge_off[e];
+                c.ptr = ovedge + (g->overridden ? g->ov_edge_off[e] : g->mat_off[e]);
                 uint32_t Kd = g->K[g->E[e].dst];
                 if (is_src) { c.sc = Kd; c.sd[dig] = 1; }
                 else { c.sc = 1; c.sd[dig] = Kd; }
@@ -931,6 +951,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
         x.elems = g->E[e].elems;
         x.sig_off = sig_off;
+        x.mat_off = g->volume ? g->mat_off[e] : 0;
         sig_off += (uint64_t)g->K[x.src] + g->K[x.dst];
     }
     if (ne) std::memcpy(img + P.off_edge, des.data(), ne * sizeof(DevEdge));
@@ -1102,6 +1123,11 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
                            dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
         launches_n++;
+        if (g->volume && g->mat_total) {
+            hipLaunchKernelGGL(k_edge_volume, dim3(grid_for(g->mat_total, 256, 65535)), dim3(256), 0, s, dV, dE,
+                               (uint32_t)ne, dex, (uint64_t *)(ws + P.off_ovedge), g->mat_total, g->r);
+            launches_n++;
+        }
     }
     std::vector<int> fill_of(n, -1);   // fill batch of each vertex (profiling)
     uint32_t fb = 0;
@@ -1388,6 +1414,10 @@ pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
     uint64_t n = (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
     if (g->overridden) {
         HIPCHK(hipMemcpy(out, ws + P.off_ovedge + g->ov_edge_off[e] * 8, n * 8, hipMemcpyDeviceToHost));
+        return PASE_OK;
+    }
+    if (g->volume) {
+        HIPCHK(hipMemcpy(out, ws + P.off_ovedge + g->mat_off[e] * 8, n * 8, hipMemcpyDeviceToHost));
         return PASE_OK;
     }
     uint64_t *tmp = nullptr;

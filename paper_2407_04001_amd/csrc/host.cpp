@@ -670,6 +670,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     off = align_up(off + P.sig_count * 8, A);
     P.off_ovedge = off;
     if (g->overridden) off = align_up(off + g->ov_edge.size() * 8, A);
+    else if (g->volume) off = align_up(off + g->mat_total * 8, A);
     // contributions: count per vertex (layer + edges + lookups is an upper bound)
     uint64_t ncontrib = 0;
     for (const auto &vp : P.v) ncontrib += 1 + vp.edges.size() + vp.terms.size();
@@ -779,6 +780,28 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->ov_layer.clear(); g->ov_edge.clear();
     g->p = p;
     g->factors = factors;
+    g->volume = g->transfer_opt == 1;
+    g->mat_off.assign(g->E.size(), 0);
+    g->mat_total = 0;
+    if (g->volume) {
+        for (size_t e = 0; e < g->E.size(); e++) {
+            // the volume arithmetic needs distinct mapped loop dims on each side
+            const pase_edge_desc &d = g->E[e];
+            uint32_t ms = 0, md = 0;
+            for (uint32_t t = 0; t < d.rank; t++) {
+                if (d.src_dim[t] >= 0) {
+                    if ((ms >> d.src_dim[t]) & 1u)
+                        return fail(g, PASE_ERR_INVALID_ARGUMENT, "volume model: a loop dim mapped twice");
+                    ms |= 1u << d.src_dim[t];
+                }
+                if (d.dst_dim[t] >= 0) {
+                    if ((md >> d.dst_dim[t]) & 1u)
+                        return fail(g, PASE_ERR_INVALID_ARGUMENT, "volume model: a loop dim mapped twice");
+                    md |= 1u << d.dst_dim[t];
+                }
+            }
+        }
+    }
     const size_t nv = g->V.size();
     g->K.assign(nv, 0);
     g->ex.assign(nv, {});
@@ -839,8 +862,14 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     }
     g->maxR.assign(g->E.size(), 0);
     for (size_t e = 0; e < g->E.size(); e++) {
-        if (g->E[e].elems >> 62 || !mul_ok(g->r, g->E[e].elems, &g->maxR[e]))
+        // the volume model moves at most the whole tensor in each direction
+        const uint64_t words = g->E[e].elems * (g->volume ? 2 : 1);
+        if (g->E[e].elems >> 61 || !mul_ok(g->r, words, &g->maxR[e]))
             return fail(g, PASE_ERR_OVERFLOW, "transfer cost exceeds 64 bits");
+        if (g->volume) {
+            g->mat_off[e] = g->mat_total;
+            g->mat_total += (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+        }
     }
     g->enumerated = true;
     pase_status st = build_plan(g);
@@ -929,6 +958,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     case PASE_OPT_ORDER:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "order 0 or 1");
         g->order_mode = (int)value;
+        break;
+    case PASE_OPT_TRANSFER:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "transfer model 0 or 1");
+        g->transfer_opt = (uint32_t)value;
         break;
     case PASE_OPT_CONFIG_SET:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "config set 0 or 1");

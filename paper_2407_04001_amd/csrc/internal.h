@@ -44,6 +44,7 @@ struct DevEdge {
     int8_t sdim[kMaxDims], ddim[kMaxDims];
     uint64_t elems;
     uint64_t sig_off;         // element offset of its split signatures: K_src, then K_dst
+    uint64_t mat_off;         // volume transfer model: element offset of its K_src x K_dst matrix
 };
 
 // One contribution to a precomputed block element (see Prep below).
@@ -299,6 +300,10 @@ struct pase_graph_s {
     // configurations
     bool enumerated = false;
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
+    uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
+    bool volume = false;            // the enumerated transfer model is the volume intersection
+    std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix
+    uint64_t mat_total = 0;         // volume model: entries of all edge matrices
     uint32_t p = 0;
     bool factors = false;           // the enumerated set: split rows hold factors, not exponents
     std::vector<uint32_t> K;

@@ -98,6 +98,72 @@ __device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t
     return sig;
 }
 
+// r * t_x of the volume-intersection model for one (producer config, consumer
+// config) pair.  Device d of a configuration is the mixed-radix point of its
+// split grid (loop dim 0 slowest); a tensor dim is cut into equal fractions on
+// each side by the split of the loop dim it maps to (1 if unmapped).  Per
+// tensor dim the parts of u and v are measured in units of 1/(s_u * s_v):
+// v's part [x_v * s_u, (x_v + 1) * s_u), u's part [x_u * s_v, (x_u + 1) * s_v).
+// forward  = max_d |need_v(d)| - |need_v(d) n hold_u(d)|, backward the same with
+// u and v swapped; words = ceil(elems * fraction) per direction.  The grid
+// coordinates advance as odometers, one step per device.  Mapped loop dims are
+// distinct per side (host check), so Q = prod s_u * s_v <= p^2 <= 2^32.
+__device__ __forceinline__ uint64_t ceil_frac(uint64_t elems, uint64_t f, uint64_t Q) {
+    // elems * f / Q rounded up, f <= Q <= 2^32: (elems % Q) * f < Q^2 <= 2^64
+    const uint64_t q = elems / Q, rem = elems % Q;
+    return q * f + (rem * f + Q - 1) / Q;
+}
+
+__device__ __forceinline__ uint64_t volume_cost(const DevVertex &u, const uint8_t *exu, const DevVertex &v,
+                                                const uint8_t *exv, const DevEdge &de, uint64_t r) {
+    uint32_t su[kMaxDims], sv[kMaxDims], xu[kMaxDims], xv[kMaxDims];
+    uint64_t Pu = 1, Pv = 1;
+    for (uint32_t k = 0; k < u.ndims; k++) {
+        su[k] = u.factors ? exu[k] : 1u << exu[k];
+        xu[k] = 0;
+        Pu *= su[k];
+    }
+    for (uint32_t k = 0; k < v.ndims; k++) {
+        sv[k] = v.factors ? exv[k] : 1u << exv[k];
+        xv[k] = 0;
+        Pv *= sv[k];
+    }
+    uint64_t Q = 1, need_v = 1, hold_u = 1;
+    for (uint32_t t = 0; t < de.rank; t++) {
+        const uint32_t a = de.sdim[t] >= 0 ? su[de.sdim[t]] : 1, b = de.ddim[t] >= 0 ? sv[de.ddim[t]] : 1;
+        Q *= (uint64_t)a * b;
+        need_v *= a;      // |v's part| = 1/b = a units
+        hold_u *= b;
+    }
+    const uint64_t P = Pu > Pv ? Pu : Pv;
+    uint64_t fwd = 0, bwd = 0;
+    for (uint64_t d = 0; d < P; d++) {
+        const bool on_u = d < Pu, on_v = d < Pv;
+        uint64_t common = (on_u && on_v) ? 1 : 0;
+        for (uint32_t t = 0; t < de.rank && common; t++) {
+            const int ka = de.sdim[t], kb = de.ddim[t];
+            const uint64_t a = ka >= 0 ? su[ka] : 1, b = kb >= 0 ? sv[kb] : 1;
+            const uint64_t cu = ka >= 0 ? xu[ka] : 0, cv = kb >= 0 ? xv[kb] : 0;
+            const uint64_t lo = cv * a > cu * b ? cv * a : cu * b;
+            const uint64_t hi = (cv + 1) * a < (cu + 1) * b ? (cv + 1) * a : (cu + 1) * b;
+            common *= hi > lo ? hi - lo : 0;
+        }
+        const uint64_t f = on_v ? need_v - common : 0, g = on_u ? hold_u - common : 0;
+        fwd = f > fwd ? f : fwd;
+        bwd = g > bwd ? g : bwd;
+        // next device: advance both grid odometers (last loop dim fastest)
+        for (int k = (int)u.ndims - 1; k >= 0; k--) {
+            if (++xu[k] < su[k]) break;
+            xu[k] = 0;
+        }
+        for (int k = (int)v.ndims - 1; k >= 0; k--) {
+            if (++xv[k] < sv[k]) break;
+            xv[k] = 0;
+        }
+    }
+    return r * (ceil_frac(de.elems, fwd, Q) + ceil_frac(de.elems, bwd, Q));
+}
+
 // r * t_x from the two signatures and device bytes of the endpoints.
 __device__ __forceinline__ uint64_t edge_cost_sig(uint64_t sig_a, uint64_t sig_b, uint32_t la, uint32_t lb,
                                                   uint64_t elems, uint64_t r, uint32_t factors) {

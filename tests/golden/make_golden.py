@@ -7,7 +7,7 @@ strategy, the cell count, per-vertex fingerprints of the cost and argmin
 tables (canonical order, SplitMix64-based, see ``pase.h``) and a seeded sample
 of table entries.
 
-    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only]
+    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only] [--volume-only]
 """
 from __future__ import annotations
 
@@ -26,32 +26,42 @@ sys.path.insert(0, ROOT)
 from oracle.oracle import Oracle, build  # noqa: E402
 from workloads import workload  # noqa: E402
 
-# (workload, seed, p, every integer split, breadth-first): p None = the
-# workload's own power-of-two p; the every-integer instances enumerate
-# Sec. II's full C(v); the breadth-first ones solve recurrence (2) instead of
-# GenerateSeq + recurrence (4)
-INSTANCES = [("w0_fc_chain", 0, None, False, False), ("w1_residual_cnn", 0, None, False, False),
-             ("w1_residual_cnn", 1, None, False, False), ("w1_residual_cnn", 2, None, False, False),
-             ("w2_inception", 0, None, False, False), ("w2_inception", 1, None, False, False),
-             ("w2_inception", 2, None, False, False), ("w3_lstm_grid", 0, None, False, False),
-             ("w4_transformer", 0, None, False, False),
-             ("w0_fc_chain", 0, 12, True, False), ("w2_inception", 0, 12, True, False),
-             ("w4_transformer", 0, 12, True, False),
-             ("w1_residual_cnn", 0, 64, False, True)]
+# Instances: the workload and seed; p (None = the workload's own power-of-two
+# p); `all_integers` enumerates Sec. II's full C(v); `bf` solves the
+# breadth-first recurrence (2) instead of GenerateSeq + recurrence (4);
+# `volume` prices transfers with the volume-intersection model.
+def _inst(name, seed=0, p=None, all_integers=False, bf=False, volume=False):
+    return {"name": name, "seed": seed, "p": p, "all_integers": all_integers, "bf": bf, "volume": volume}
 
 
-def file_name(name: str, seed: int, p=None, all_integers: bool = False, bf: bool = False) -> str:
+INSTANCES = [_inst("w0_fc_chain"), _inst("w1_residual_cnn"), _inst("w1_residual_cnn", 1),
+             _inst("w1_residual_cnn", 2), _inst("w2_inception"), _inst("w2_inception", 1),
+             _inst("w2_inception", 2), _inst("w3_lstm_grid"), _inst("w4_transformer"),
+             _inst("w0_fc_chain", p=12, all_integers=True), _inst("w2_inception", p=12, all_integers=True),
+             _inst("w4_transformer", p=12, all_integers=True),
+             _inst("w1_residual_cnn", p=64, bf=True),
+             _inst("w1_residual_cnn", volume=True), _inst("w2_inception", volume=True),
+             _inst("w3_lstm_grid", volume=True), _inst("w4_transformer", volume=True)]
+
+
+def file_name(name: str, seed: int, p=None, all_integers: bool = False, bf: bool = False,
+              volume: bool = False) -> str:
     if bf:
         return f"{name}_seed{seed}_p{p}_bf.json"
+    if volume:
+        return f"{name}_seed{seed}_volume.json"
     return f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
+
+
 SAMPLES_PER_TABLE = 24
 
 
-def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False, bf: bool = False) -> dict:
+def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False, bf: bool = False,
+           volume: bool = False) -> dict:
     g = workload(name, seed)
     p = p or g["p"]
     o = Oracle(g)
-    K = o.configs(p, all_integers=all_integers)
+    K = o.configs(p, all_integers=all_integers, volume=volume)
     t0 = time.time()
     if bf:
         o.solve_bf(threads=threads)
@@ -74,6 +84,7 @@ def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = Fals
                        "fp_cost": str(fpT), "fp_arg": str(fpA), "samples": samples})
     return {"workload": name, "seed": seed, "p": p, "all_integers": all_integers,
             "order": "breadth-first" if bf else "GenerateSeq",
+            "transfer": "volume intersection" if volume else "split match",
             "num_configs": [int(k) for k in K],
             "sequence": seq, "min_cost": str(mc), "strategy": strat, "cells": o.cells(),
             "tables": tables, "oracle_seconds": round(wall, 3)}
@@ -86,18 +97,23 @@ def main():
     ap.add_argument("--all-integers-only", action="store_true",
                     help="only the instances with every integer split")
     ap.add_argument("--bf-only", action="store_true", help="only the breadth-first instances")
+    ap.add_argument("--volume-only", action="store_true", help="only the volume-model instances")
     args = ap.parse_args()
     build(force=False)
-    for name, seed, p, all_integers, bf in INSTANCES:
+    for inst in INSTANCES:
+        name, seed = inst["name"], inst["seed"]
         if args.only and args.only != name:
             continue
-        if args.all_integers_only and not all_integers:
+        if args.all_integers_only and not inst["all_integers"]:
             continue
-        if args.bf_only and not bf:
+        if args.bf_only and not inst["bf"]:
+            continue
+        if args.volume_only and not inst["volume"]:
             continue
         t = time.time()
-        out = golden(name, seed, args.threads, p, all_integers, bf)
-        path = os.path.join(HERE, file_name(name, seed, p, all_integers, bf))
+        out = golden(name, seed, args.threads, inst["p"], inst["all_integers"], inst["bf"], inst["volume"])
+        path = os.path.join(HERE, file_name(**{k: inst[k] for k in ("seed", "p", "all_integers", "bf", "volume")},
+                                            name=name))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))
         print(f"{name} seed {seed}: min_cost {out['min_cost']} cells {out['cells']:.3e} "

@@ -32,10 +32,10 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False):
+def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False, volume=False):
     from oracle.oracle import Oracle
     o = Oracle(g)
-    o.configs(p or g["p"], all_integers=all_integers)
+    o.configs(p or g["p"], all_integers=all_integers, volume=volume)
     if costs is not None:
         o.set_costs(*costs)
     if bf:
@@ -69,9 +69,10 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False):
+         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False):
     pg = P.Graph(g, seq_rule=rule)
     pg.set_option(P.OPT_ORDER, int(bf))
+    pg.set_option(P.OPT_TRANSFER, int(volume))
     pg.enumerate_configs(p or g["p"], all_integers=all_integers)
     pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
@@ -259,9 +260,11 @@ def test_library_owned_workspace(P):
 
 
 # ------------------------------------------------------------------ full-size workloads
-def _golden(name, seed, p=None, all_integers=False, bf=False):
+def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False):
     if bf:
         fn = f"{name}_seed{seed}_p{p}_bf.json"
+    elif volume:
+        fn = f"{name}_seed{seed}_volume.json"
     else:
         fn = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
     with open(os.path.join(GOLDEN, fn)) as f:
@@ -269,13 +272,13 @@ def _golden(name, seed, p=None, all_integers=False, bf=False):
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False, bf=False):
-    gold = _golden(name, seed, p, all_integers, bf)
+                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False):
+    gold = _golden(name, seed, p, all_integers, bf, volume)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf}")
+        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers, all_integers=all_integers, bf=bf)
+                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -547,3 +550,55 @@ def test_bf_order_workloads(P):
             assert pg.fingerprint(v) == o.fingerprint(i)
     _check_golden(P, "w1_residual_cnn", 0, p=64, bf=True, keep=False)
     _check_golden(P, "w1_residual_cnn", 0, p=64, bf=True, keep=True)
+
+
+# ------------------------------------------------------------------ volume-intersection transfer model
+@pytest.mark.parametrize("seed", range(8))
+def test_volume_model_random_graphs(P, seed):
+    """PASE_OPT_TRANSFER = 1: the device-computed edge matrices equal the
+    oracle's cell-counting ones entry for entry (mismatched dim sizes,
+    unmapped dims, both configuration sets), and so do the search and every
+    table entry."""
+    p, all_int = ((4, False), (8, False), (6, True), (16, False), (12, True), (5, True), (8, False),
+                  (2, False))[seed]
+    g = random_graph(seed + 600, n=4 + seed % 4, p=p, max_dims=3, extra_edges=1 + seed % 3, max_size=200)
+    say(f"volume model random graph seed={seed + 600} p={p} all_integers={all_int}")
+    o = _oracle(g, p=p, all_integers=all_int, volume=True)
+    pg, mc, strat = _run(P, g, p=p, all_integers=all_int, volume=True)
+    for e in range(len(g["edges"])):
+        assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=512)
+
+
+def test_volume_model_large_tensors(P):
+    """Tensors of ~2^53 words at p = 64 (Q up to 4096, so elems * f passes
+    2^64): the device's split ceil division (no 128-bit products) against the
+    oracle's 128-bit one; uint64 keys."""
+    vs = [{"name": f"v{k}", "dims": [1 << 20, 3 << 18, 7], "dim_names": ["a", "b", "c"], "reduce": [2],
+           "flops_per_point": 1} for k in range(3)]
+    big = (1 << 53) - 12345
+    es = [{"src": 0, "dst": 1, "src_dim": [0, 1], "dst_dim": [1, 0], "elems": big},
+          {"src": 1, "dst": 2, "src_dim": [1, -1], "dst_dim": [0, 2], "elems": big - 999},
+          {"src": 0, "dst": 2, "src_dim": [2], "dst_dim": [1], "elems": 3 ** 33}]
+    g = {"name": "big", "p": 64, "comm_weight": 1, "vertices": vs, "edges": es}
+    for p, all_int in ((64, False), (12, True)):
+        say(f"volume model large tensors p={p}")
+        o = _oracle(g, p=p, all_integers=all_int, volume=True)
+        pg, mc, strat = _run(P, g, p=p, all_integers=all_int, volume=True, key=1)
+        for e in range(len(es)):
+            assert np.array_equal(pg.edge_costs(e), o.edge_costs(e)), e
+        assert (mc, strat) == o.result()
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
+def test_volume_model_workloads_against_golden(P, name):
+    _check_golden(P, name, 0, volume=True)
+    _check_golden(P, name, 0, volume=True, keep=False, schedule=2)
+
+
+def test_volume_model_transformer_against_golden(P):
+    """The measured Transformer with volume transfer costs, in the benchmark's
+    configuration and with every table kept and fingerprinted."""
+    _check_golden(P, "w4_transformer", 0, volume=True, keep=False)
+    _check_golden(P, "w4_transformer", 0, volume=True, keep=True)

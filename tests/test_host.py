@@ -254,6 +254,31 @@ def test_bf_order_option(pase):
     assert _status(lambda: P.pase_set_option(pg.h, P.OPT_ORDER, 2)) == P.INVALID_ARGUMENT
 
 
+def test_transfer_model_option(pase):
+    """PASE_OPT_TRANSFER = 1 takes effect at the next enumeration, adds the
+    edge matrices (8 bytes per entry) to the workspace, and refuses an edge
+    side that maps two tensor dims to one loop dim."""
+    P = pase
+    g = workload("w2_inception")
+    pg = P.Graph(g)
+    pg.enumerate_configs(16)
+    ws0 = pg.workspace_size()
+    pg.set_option(P.OPT_TRANSFER, 1)
+    assert pg.workspace_size() == ws0
+    pg.enumerate_configs(16)
+    entries = sum(pg.K[e["src"]] * pg.K[e["dst"]] for e in g["edges"])
+    assert pg.workspace_size() >= ws0 + 8 * entries
+    assert _status(lambda: P.pase_set_option(pg.h, P.OPT_TRANSFER, 2)) == P.INVALID_ARGUMENT
+    dup = {"name": "dup", "p": 4, "comm_weight": 8,
+           "vertices": [{"name": "a", "dims": [8, 8], "dim_names": ["x", "y"], "reduce": [],
+                         "flops_per_point": 1}] * 2,
+           "edges": [{"src": 0, "dst": 1, "src_dim": [0, 0], "dst_dim": [0, 1], "elems": 64}]}
+    pg = P.Graph(dup)
+    pg.enumerate_configs(4)
+    pg.set_option(P.OPT_TRANSFER, 1)
+    assert _status(lambda: pg.enumerate_configs(4)) == P.INVALID_ARGUMENT
+
+
 @pytest.mark.parametrize("seed", range(20))
 @pytest.mark.parametrize("rule", [0, 1])
 def test_sequence_and_dependent_sets(pase, seed, rule):
