@@ -143,9 +143,9 @@ typedef enum {
                                    and each tensor dim cut into equal fractions by the split of
                                    the loop dim it maps to (words rounded up per direction).
                                    Model 1 computes every edge's K_src x K_dst matrix on the
-                                   device (workspace grows by 8 bytes per entry) and needs the
-                                   mapped loop dims of each edge side distinct
-                                   (INVALID_ARGUMENT otherwise) */
+                                   device (workspace grows by 8 bytes per entry); an edge whose
+                                   tensor maps several dims to one loop dim is refused
+                                   (INVALID_ARGUMENT) when p^(mapped dims) exceeds 2^32 */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

@@ -784,22 +784,30 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->mat_off.assign(g->E.size(), 0);
     g->mat_total = 0;
     if (g->volume) {
+        // the device's volume arithmetic needs Q = prod_t s_u(t) * s_v(t) <= 2^32:
+        // with distinct mapped loop dims per side each product is at most p,
+        // otherwise it is bounded by p to the number of mapped tensor dims
         for (size_t e = 0; e < g->E.size(); e++) {
-            // the volume arithmetic needs distinct mapped loop dims on each side
             const pase_edge_desc &d = g->E[e];
-            uint32_t ms = 0, md = 0;
+            uint32_t ms = 0, md = 0, ns = 0, nd = 0;
+            bool distinct = true;
             for (uint32_t t = 0; t < d.rank; t++) {
                 if (d.src_dim[t] >= 0) {
-                    if ((ms >> d.src_dim[t]) & 1u)
-                        return fail(g, PASE_ERR_INVALID_ARGUMENT, "volume model: a loop dim mapped twice");
+                    distinct &= !((ms >> d.src_dim[t]) & 1u);
                     ms |= 1u << d.src_dim[t];
+                    ns++;
                 }
                 if (d.dst_dim[t] >= 0) {
-                    if ((md >> d.dst_dim[t]) & 1u)
-                        return fail(g, PASE_ERR_INVALID_ARGUMENT, "volume model: a loop dim mapped twice");
+                    distinct &= !((md >> d.dst_dim[t]) & 1u);
                     md |= 1u << d.dst_dim[t];
+                    nd++;
                 }
             }
+            unsigned __int128 q = 1;
+            for (uint32_t k = 0; k < (distinct ? 2u : ns + nd); k++) q *= p;
+            if (q > ((unsigned __int128)1 << 32))
+                return fail(g, PASE_ERR_INVALID_ARGUMENT,
+                            "volume model: tensor dims mapped to one loop dim make the device fractions too fine");
         }
     }
     const size_t nv = g->V.size();

@@ -106,8 +106,9 @@ __device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t
 // v's part [x_v * s_u, (x_v + 1) * s_u), u's part [x_u * s_v, (x_u + 1) * s_v).
 // forward  = max_d |need_v(d)| - |need_v(d) n hold_u(d)|, backward the same with
 // u and v swapped; words = ceil(elems * fraction) per direction.  The grid
-// coordinates advance as odometers, one step per device.  Mapped loop dims are
-// distinct per side (host check), so Q = prod s_u * s_v <= p^2 <= 2^32.
+// coordinates advance as odometers, one step per device.  The host checks
+// Q = prod s_u * s_v <= 2^32 (p^2 when the mapped loop dims of each side are
+// distinct).
 __device__ __forceinline__ uint64_t ceil_frac(uint64_t elems, uint64_t f, uint64_t Q) {
     // elems * f / Q rounded up, f <= Q <= 2^32: (elems % Q) * f < Q^2 <= 2^64
     const uint64_t q = elems / Q, rem = elems % Q;

@@ -256,8 +256,9 @@ def test_bf_order_option(pase):
 
 def test_transfer_model_option(pase):
     """PASE_OPT_TRANSFER = 1 takes effect at the next enumeration, adds the
-    edge matrices (8 bytes per entry) to the workspace, and refuses an edge
-    side that maps two tensor dims to one loop dim."""
+    edge matrices (8 bytes per entry) to the workspace, accepts tensor dims
+    mapped to one loop dim at small p and refuses them when p^(mapped dims)
+    passes 2^32."""
     P = pase
     g = workload("w2_inception")
     pg = P.Graph(g)
@@ -276,7 +277,8 @@ def test_transfer_model_option(pase):
     pg = P.Graph(dup)
     pg.enumerate_configs(4)
     pg.set_option(P.OPT_TRANSFER, 1)
-    assert _status(lambda: pg.enumerate_configs(4)) == P.INVALID_ARGUMENT
+    pg.enumerate_configs(4)                                           # 4^4 <= 2^32
+    assert _status(lambda: pg.enumerate_configs(512)) == P.INVALID_ARGUMENT   # 512^4 > 2^32
 
 
 @pytest.mark.parametrize("seed", range(20))
