@@ -145,7 +145,9 @@ typedef enum {
                                    Model 1 computes every edge's K_src x K_dst matrix on the
                                    device (workspace grows by 8 bytes per entry); an edge whose
                                    tensor maps several dims to one loop dim is refused
-                                   (INVALID_ARGUMENT) when p^(mapped dims) exceeds 2^32 */
+                                   (INVALID_ARGUMENT) when p^(mapped dims) reaches 2^32, and
+                                   with distinct mapped loop dims p^2 must stay below 2^32 (p <
+                                   65536) */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

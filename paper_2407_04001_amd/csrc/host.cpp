@@ -784,7 +784,7 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->mat_off.assign(g->E.size(), 0);
     g->mat_total = 0;
     if (g->volume) {
-        // the device's volume arithmetic needs Q = prod_t s_u(t) * s_v(t) <= 2^32:
+        // the device's volume arithmetic needs Q = prod_t s_u(t) * s_v(t) < 2^32:
         // with distinct mapped loop dims per side each product is at most p,
         // otherwise it is bounded by p to the number of mapped tensor dims
         for (size_t e = 0; e < g->E.size(); e++) {
@@ -805,7 +805,7 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
             }
             unsigned __int128 q = 1;
             for (uint32_t k = 0; k < (distinct ? 2u : ns + nd); k++) q *= p;
-            if (q > ((unsigned __int128)1 << 32))
+            if (q >= ((unsigned __int128)1 << 32))
                 return fail(g, PASE_ERR_INVALID_ARGUMENT,
                             "volume model: tensor dims mapped to one loop dim make the device fractions too fine");
         }

@@ -105,12 +105,13 @@ __device__ __forceinline__ uint64_t split_signature(const int8_t *dims, uint32_t
 // tensor dim the parts of u and v are measured in units of 1/(s_u * s_v):
 // v's part [x_v * s_u, (x_v + 1) * s_u), u's part [x_u * s_v, (x_u + 1) * s_v).
 // forward  = max_d |need_v(d)| - |need_v(d) n hold_u(d)|, backward the same with
-// u and v swapped; words = ceil(elems * fraction) per direction.  The grid
-// coordinates advance as odometers, one step per device.  The host checks
-// Q = prod s_u * s_v <= 2^32 (p^2 when the mapped loop dims of each side are
-// distinct).
+// u and v swapped; words = ceil(elems * fraction) per direction.  The host
+// checks Q = prod s_u * s_v < 2^32, so every endpoint and volume in units fits
+// 32 bits.  Devices that only one side uses contribute that side's whole part
+// (a constant), so the walk covers the devices both use, as odometers over
+// the two grids, and stops once both maxima reach their ceilings.
 __device__ __forceinline__ uint64_t ceil_frac(uint64_t elems, uint64_t f, uint64_t Q) {
-    // elems * f / Q rounded up, f <= Q <= 2^32: (elems % Q) * f < Q^2 <= 2^64
+    // elems * f / Q rounded up, f <= Q < 2^32: (elems % Q) * f < Q^2 < 2^64
     const uint64_t q = elems / Q, rem = elems % Q;
     return q * f + (rem * f + Q - 1) / Q;
 }
@@ -118,7 +119,7 @@ __device__ __forceinline__ uint64_t ceil_frac(uint64_t elems, uint64_t f, uint64
 __device__ __forceinline__ uint64_t volume_cost(const DevVertex &u, const uint8_t *exu, const DevVertex &v,
                                                 const uint8_t *exv, const DevEdge &de, uint64_t r) {
     uint32_t su[kMaxDims], sv[kMaxDims], xu[kMaxDims], xv[kMaxDims];
-    uint64_t Pu = 1, Pv = 1;
+    uint32_t Pu = 1, Pv = 1;
     for (uint32_t k = 0; k < u.ndims; k++) {
         su[k] = u.factors ? exu[k] : 1u << exu[k];
         xu[k] = 0;
@@ -129,29 +130,31 @@ __device__ __forceinline__ uint64_t volume_cost(const DevVertex &u, const uint8_
         xv[k] = 0;
         Pv *= sv[k];
     }
-    uint64_t Q = 1, need_v = 1, hold_u = 1;
+    // per tensor dim: the split on each side (1 if unmapped); Q and the part sizes in units
+    uint32_t ta[kMaxDims], tb[kMaxDims];
+    uint32_t Q = 1, need_v = 1, hold_u = 1;
     for (uint32_t t = 0; t < de.rank; t++) {
-        const uint32_t a = de.sdim[t] >= 0 ? su[de.sdim[t]] : 1, b = de.ddim[t] >= 0 ? sv[de.ddim[t]] : 1;
-        Q *= (uint64_t)a * b;
-        need_v *= a;      // |v's part| = 1/b = a units
-        hold_u *= b;
+        ta[t] = de.sdim[t] >= 0 ? su[de.sdim[t]] : 1;
+        tb[t] = de.ddim[t] >= 0 ? sv[de.ddim[t]] : 1;
+        Q *= ta[t] * tb[t];
+        need_v *= ta[t];      // |v's part| = 1/b = a units
+        hold_u *= tb[t];
     }
-    const uint64_t P = Pu > Pv ? Pu : Pv;
-    uint64_t fwd = 0, bwd = 0;
-    for (uint64_t d = 0; d < P; d++) {
-        const bool on_u = d < Pu, on_v = d < Pv;
-        uint64_t common = (on_u && on_v) ? 1 : 0;
+    // devices only v uses need their whole part; devices only u uses hold theirs
+    uint32_t fwd = Pv > Pu ? need_v : 0, bwd = Pu > Pv ? hold_u : 0;
+    const uint32_t both = Pu < Pv ? Pu : Pv;
+    for (uint32_t d = 0; d < both && (fwd < need_v || bwd < hold_u); d++) {
+        uint32_t common = 1;
         for (uint32_t t = 0; t < de.rank && common; t++) {
             const int ka = de.sdim[t], kb = de.ddim[t];
-            const uint64_t a = ka >= 0 ? su[ka] : 1, b = kb >= 0 ? sv[kb] : 1;
-            const uint64_t cu = ka >= 0 ? xu[ka] : 0, cv = kb >= 0 ? xv[kb] : 0;
-            const uint64_t lo = cv * a > cu * b ? cv * a : cu * b;
-            const uint64_t hi = (cv + 1) * a < (cu + 1) * b ? (cv + 1) * a : (cu + 1) * b;
+            const uint32_t a = ta[t], b = tb[t];
+            const uint32_t cu = ka >= 0 ? xu[ka] : 0, cv = kb >= 0 ? xv[kb] : 0;
+            const uint32_t lo = cv * a > cu * b ? cv * a : cu * b;
+            const uint32_t hi = (cv + 1) * a < (cu + 1) * b ? (cv + 1) * a : (cu + 1) * b;
             common *= hi > lo ? hi - lo : 0;
         }
-        const uint64_t f = on_v ? need_v - common : 0, g = on_u ? hold_u - common : 0;
-        fwd = f > fwd ? f : fwd;
-        bwd = g > bwd ? g : bwd;
+        fwd = need_v - common > fwd ? need_v - common : fwd;
+        bwd = hold_u - common > bwd ? hold_u - common : bwd;
         // next device: advance both grid odometers (last loop dim fastest)
         for (int k = (int)u.ndims - 1; k >= 0; k--) {
             if (++xu[k] < su[k]) break;
