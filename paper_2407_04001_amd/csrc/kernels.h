@@ -116,55 +116,62 @@ __device__ __forceinline__ uint64_t ceil_frac(uint64_t elems, uint64_t f, uint64
     return q * f + (rem * f + Q - 1) / Q;
 }
 
+__device__ __forceinline__ uint32_t split_of(const DevVertex &x, const uint8_t *ex, int k) {
+    return x.factors ? ex[k] : 1u << ex[k];
+}
+
+// With m = min over the devices both ends use of |need_v(d) n hold_u(d)|:
+// forward = need_v - m (need_v when v uses more devices), backward = hold_u - m
+// (hold_u when u uses more).  Per tensor dim the device's coordinate on each
+// side advances every `stride` devices (the product of the splits of the loop
+// dims after the mapped one) and wraps at the split; all per-dim state is
+// indexed by unrolled constants so it stays in registers.
 __device__ __forceinline__ uint64_t volume_cost(const DevVertex &u, const uint8_t *exu, const DevVertex &v,
                                                 const uint8_t *exv, const DevEdge &de, uint64_t r) {
-    uint32_t su[kMaxDims], sv[kMaxDims], xu[kMaxDims], xv[kMaxDims];
     uint32_t Pu = 1, Pv = 1;
-    for (uint32_t k = 0; k < u.ndims; k++) {
-        su[k] = u.factors ? exu[k] : 1u << exu[k];
-        xu[k] = 0;
-        Pu *= su[k];
-    }
-    for (uint32_t k = 0; k < v.ndims; k++) {
-        sv[k] = v.factors ? exv[k] : 1u << exv[k];
-        xv[k] = 0;
-        Pv *= sv[k];
-    }
-    // per tensor dim: the split on each side (1 if unmapped); Q and the part sizes in units
-    uint32_t ta[kMaxDims], tb[kMaxDims];
+    for (uint32_t k = 0; k < u.ndims; k++) Pu *= split_of(u, exu, (int)k);
+    for (uint32_t k = 0; k < v.ndims; k++) Pv *= split_of(v, exv, (int)k);
+    uint32_t ta[kMaxDims], tb[kMaxDims], stu[kMaxDims], stv[kMaxDims];
+    uint32_t xu[kMaxDims], xv[kMaxDims], pu[kMaxDims], pv[kMaxDims];
     uint32_t Q = 1, need_v = 1, hold_u = 1;
-    for (uint32_t t = 0; t < de.rank; t++) {
-        ta[t] = de.sdim[t] >= 0 ? su[de.sdim[t]] : 1;
-        tb[t] = de.ddim[t] >= 0 ? sv[de.ddim[t]] : 1;
-        Q *= ta[t] * tb[t];
-        need_v *= ta[t];      // |v's part| = 1/b = a units
-        hold_u *= tb[t];
-    }
-    // devices only v uses need their whole part; devices only u uses hold theirs
-    uint32_t fwd = Pv > Pu ? need_v : 0, bwd = Pu > Pv ? hold_u : 0;
-    const uint32_t both = Pu < Pv ? Pu : Pv;
-    for (uint32_t d = 0; d < both && (fwd < need_v || bwd < hold_u); d++) {
-        uint32_t common = 1;
-        for (uint32_t t = 0; t < de.rank && common; t++) {
+#pragma unroll
+    for (int t = 0; t < kMaxDims; t++) {
+        ta[t] = tb[t] = stu[t] = stv[t] = 1;
+        xu[t] = xv[t] = pu[t] = pv[t] = 0;
+        if (t < (int)de.rank) {
             const int ka = de.sdim[t], kb = de.ddim[t];
-            const uint32_t a = ta[t], b = tb[t];
-            const uint32_t cu = ka >= 0 ? xu[ka] : 0, cv = kb >= 0 ? xv[kb] : 0;
-            const uint32_t lo = cv * a > cu * b ? cv * a : cu * b;
-            const uint32_t hi = (cv + 1) * a < (cu + 1) * b ? (cv + 1) * a : (cu + 1) * b;
-            common *= hi > lo ? hi - lo : 0;
-        }
-        fwd = need_v - common > fwd ? need_v - common : fwd;
-        bwd = hold_u - common > bwd ? hold_u - common : bwd;
-        // next device: advance both grid odometers (last loop dim fastest)
-        for (int k = (int)u.ndims - 1; k >= 0; k--) {
-            if (++xu[k] < su[k]) break;
-            xu[k] = 0;
-        }
-        for (int k = (int)v.ndims - 1; k >= 0; k--) {
-            if (++xv[k] < sv[k]) break;
-            xv[k] = 0;
+            if (ka >= 0) {
+                ta[t] = split_of(u, exu, ka);
+                for (int k = ka + 1; k < (int)u.ndims; k++) stu[t] *= split_of(u, exu, k);
+            }
+            if (kb >= 0) {
+                tb[t] = split_of(v, exv, kb);
+                for (int k = kb + 1; k < (int)v.ndims; k++) stv[t] *= split_of(v, exv, k);
+            }
+            Q *= ta[t] * tb[t];
+            need_v *= ta[t];      // |v's part| = 1/b = a units
+            hold_u *= tb[t];
         }
     }
+    const uint32_t both = Pu < Pv ? Pu : Pv;
+    uint32_t m = need_v < hold_u ? need_v : hold_u;
+    for (uint32_t d = 0; d < both && m; d++) {
+        uint32_t common = 1;
+#pragma unroll
+        for (int t = 0; t < kMaxDims; t++) {
+            if (t < (int)de.rank) {
+                const uint32_t a = ta[t], b = tb[t], cu = xu[t], cv = xv[t];
+                const uint32_t lo = cv * a > cu * b ? cv * a : cu * b;
+                const uint32_t hi = (cv + 1) * a < (cu + 1) * b ? (cv + 1) * a : (cu + 1) * b;
+                common *= hi > lo ? hi - lo : 0;
+                // next device
+                if (++pu[t] == stu[t]) { pu[t] = 0; if (++xu[t] == ta[t]) xu[t] = 0; }
+                if (++pv[t] == stv[t]) { pv[t] = 0; if (++xv[t] == tb[t]) xv[t] = 0; }
+            }
+        }
+        m = common < m ? common : m;
+    }
+    const uint32_t fwd = Pv > Pu ? need_v : need_v - m, bwd = Pu > Pv ? hold_u : hold_u - m;
     return r * (ceil_frac(de.elems, fwd, Q) + ceil_frac(de.elems, bwd, Q));
 }
 
