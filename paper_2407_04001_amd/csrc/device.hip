@@ -409,7 +409,7 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             if (g->overridden || g->volume) {
                 c.kind = kContribTable;
                 c.raw_u64 = 1;
-                c.ptr = ovedge + (g->overridden ? g->ov_edge_off[e] : g->mat_off[e]);
+                c.ptr = g->overridden ? ovedge + g->ov_edge_off[e] : (const uint64_t *)(ws + P.off_vmat) + g->mat_off[e];
                 uint32_t Kd = g->K[g->E[e].dst];
                 if (is_src) { c.sc = Kd; c.sd[dig] = 1; }
                 else { c.sc = 1; c.sd[dig] = Kd; }
@@ -1125,7 +1125,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         launches_n++;
         if (g->volume && g->mat_total) {
             hipLaunchKernelGGL(k_edge_volume, dim3(grid_for(g->mat_total, 256, 65535)), dim3(256), 0, s, dV, dE,
-                               (uint32_t)ne, dex, (uint64_t *)(ws + P.off_ovedge), g->mat_total, g->r);
+                               (uint32_t)ne, dex, (uint64_t *)(ws + P.off_vmat), g->mat_total, g->r);
             launches_n++;
         }
     }
@@ -1417,7 +1417,7 @@ pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
         return PASE_OK;
     }
     if (g->volume) {
-        HIPCHK(hipMemcpy(out, ws + P.off_ovedge + g->mat_off[e] * 8, n * 8, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(out, ws + P.off_vmat + g->mat_off[e] * 8, n * 8, hipMemcpyDeviceToHost));
         return PASE_OK;
     }
     uint64_t *tmp = nullptr;

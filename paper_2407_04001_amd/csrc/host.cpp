@@ -670,7 +670,6 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     off = align_up(off + P.sig_count * 8, A);
     P.off_ovedge = off;
     if (g->overridden) off = align_up(off + g->ov_edge.size() * 8, A);
-    else if (g->volume) off = align_up(off + g->mat_total * 8, A);
     // contributions: count per vertex (layer + edges + lookups is an upper bound)
     uint64_t ncontrib = 0;
     for (const auto &vp : P.v) ncontrib += 1 + vp.edges.size() + vp.terms.size();
@@ -697,6 +696,10 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     off = align_up(off + g->V.size() * 4, A);
     P.off_out = off;
     off = align_up(off + sizeof(SearchOut), A);
+    // volume transfer model: the edge matrices are computed on the device, so
+    // they sit past the uploaded constant region
+    P.off_vmat = off;
+    if (g->volume && !g->overridden) off = align_up(off + g->mat_total * 8, A);
 
     // T arena: interval packing over launch slots -- a table is written in the
     // slot of its vertex and last read in the slot of its reader
