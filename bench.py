@@ -21,9 +21,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "DP cell-updates/sec and FindBestStrategy wall time (Transformer, p=64)"
-# fp64 VALU: 256 CUs x 64 lanes x 2.4 GHz, one add or one min per lane-cycle
+# VALU: 256 CUs x 64 lanes x 2.4 GHz lane-ops/s (one fp64 add or min, or one
+# int32 op, per lane-cycle)
 FP64_OPS_PEAK_T = 256 * 64 * 2.4e9 / 1e12
-OPS_PER_CELL = 2          # one add and one min (the min-plus multiply-accumulate)
+OPS_PER_CELL = 2          # fp64 keys: one add and one min (the min-plus multiply-accumulate)
+OPS_PER_CELL_U64 = 5      # uint64 keys: add + carry, 64-bit compare, two selects (int32 lane-ops)
 
 
 def cpu_threads():
@@ -37,15 +39,35 @@ def cpu_threads():
     return max(1, n)
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False):
+    """The oracle on the host cores (OpenMP over table entries), on a prefix of
+    the vertex order of about `max_cells` cells, then single-threaded on a
+    prefix a tenth that size."""
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
     o.configs(p, all_integers=all_integers, volume=volume)
-    if bf:
-        o.solve_bf(max_cells=max_cells, threads=threads)
-    else:
-        o.solve(max_cells=max_cells, threads=threads)
+
+    def run(cells, nthreads):
+        if bf:
+            o.solve_bf(max_cells=cells, threads=nthreads)
+        else:
+            o.solve(max_cells=cells, threads=nthreads)
+        return o.cells_done() / o.seconds(), o.cells_done(), o.seconds()
+
+    one, one_cells, one_s = run(max(1, max_cells // (10 * threads)), 1)
+    run(max_cells, threads)
     done = o.cells_done()
     n_done = 0
     cum = 0
@@ -59,7 +81,9 @@ def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False)
             "sample": f"first {n_done} of {len(seq)} vertices of the same "
                       f"{'breadth-first' if bf else 'GenerateSeq'} order "
                       f"({done:.3e} of {o.cells():.3e} cells, {o.seconds():.1f} s, "
-                      f"OpenMP over table entries)"}
+                      f"OpenMP over table entries)",
+            "single_thread": {"value": one, "cells": one_cells, "seconds": round(one_s, 2)},
+            "cpu_model": cpu_model()}
 
 
 def copy_calibration(mib):
@@ -143,10 +167,12 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    walls, rows_ms, rows_launches, fill_ms = [], 0.0, 0, 0.0
+    walls, rows_ms, rows_launches, fill_ms, step_ms = [], 0.0, 0, 0.0, []
     t0 = time.perf_counter()
     for _ in range(steps):
+        ts = time.perf_counter()
         mc, strat = step()
+        step_ms.append((time.perf_counter() - ts) * 1e3)
         st = pg.stats()
         walls.append(st["wall_ms"])
         # the dominant kernel: the row kernel with a column chunk per lane (its
@@ -159,7 +185,9 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
 
     cells = st["cells"]
     col_cells = st["rows_cells"] - st["stream_cells"]
-    achieved = OPS_PER_CELL * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
+    ops = OPS_PER_CELL if st["key_type"] == 0 else OPS_PER_CELL_U64
+    achieved = ops * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
+    t_roof_ms = ops * cells / (FP64_OPS_PEAK_T * 1e12) * 1e3
     parity = None
     if bf:
         gold_name = f"{name}_seed{seed}_p{p}_bf.json"
@@ -182,11 +210,18 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
         "config": dict(config, cells=cells),
         "find_best_strategy_ms": sum(walls) / len(walls),
+        "median_ms_per_step": sorted(step_ms)[len(step_ms) // 2],
         "fill_ms_per_step": fill_ms / steps,
+        # the whole search against the ALU roofline: every cell costs `ops` VALU
+        # lane-ops (t_roof), against the fill-kernel time and the step
+        "search_roofline": {"t_roof_ms": t_roof_ms, "ops_per_cell": ops,
+                            "frac_of_fill": t_roof_ms / (fill_ms / steps) if fill_ms else None,
+                            "frac_of_step": t_roof_ms / (elapsed * 1e3 / steps)},
         "fill_cells_per_s": cells / (fill_ms / steps / 1e3) if fill_ms else None,
         "min_cost": mc, "parity_with_oracle": parity,
         "roofline": {"bound": "alu", "kernel": "k_fill_rows",
-                     "achieved": achieved, "peak": FP64_OPS_PEAK_T, "unit": "TFLOP/s",
+                     "achieved": achieved, "peak": FP64_OPS_PEAK_T,
+                     "unit": "TFLOP/s" if st["key_type"] == 0 else "T int32-op/s",
                      "frac": achieved / FP64_OPS_PEAK_T,
                      "traffic": traffic_from_profile() if headline else None,
                      "launches_per_step": rows_launches // steps,
