@@ -46,6 +46,8 @@ def _load(path: str | None = None):
     L.oracle_configs.argtypes = [P, I]
     L.oracle_configs_all.argtypes = [P, I]
     L.oracle_set_transfer_model.argtypes = [P, I]
+    L.oracle_set_weights.argtypes = [P, P, P]
+    L.oracle_set_grad_sync.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
     L.oracle_solve_bf.argtypes = [P, U64, I]
@@ -112,6 +114,13 @@ class Oracle:
                                int(graph.get("comm_weight", 8)))
         if not self._h:
             raise OracleError("oracle_new rejected the graph")
+        wmask = np.zeros(nv, dtype=np.uint32)
+        wpp = np.zeros(nv, dtype=np.uint64)
+        for i, v in enumerate(vs):
+            for k in v.get("weight_dims", []):
+                wmask[i] |= np.uint32(1 << k)
+            wpp[i] = v.get("weight_per_point", 0)
+        self._check(L.oracle_set_weights(self._h, _ptr(wmask), _ptr(wpp)))
         self.ndims = ndims
         self.p = None
 
@@ -126,12 +135,14 @@ class Oracle:
         return rc
 
     # -- configurations and costs
-    def configs(self, p: int, all_integers: bool = False, volume: bool = False):
+    def configs(self, p: int, all_integers: bool = False, volume: bool = False, grad_sync: bool = False):
         """C(v) for p devices: power-of-two splits (p = 2^L), or with
         all_integers every tuple of positive integers with product <= p; the
         transfer costs follow the split-match model, or with `volume` the
-        volume-intersection model."""
+        volume-intersection model; grad_sync adds the weight-gradient
+        all-reduce to the layer costs."""
         self._check(self._L.oracle_set_transfer_model(self._h, 1 if volume else 0))
+        self._check(self._L.oracle_set_grad_sync(self._h, 1 if grad_sync else 0))
         fn = self._L.oracle_configs_all if all_integers else self._L.oracle_configs
         self._check(fn(self._h, int(p)))
         self.p = p

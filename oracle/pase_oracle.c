@@ -46,6 +46,9 @@ typedef struct {
     uint64_t *elems;         /* ne */
     uint64_t r;              /* FLOP-to-byte ratio weighting communication */
     int xmodel;              /* transfer cost: 0 split match, 1 volume intersection */
+    int grad_sync;           /* 1: layer cost adds the weight-gradient all-reduce */
+    uint32_t *weight_mask;   /* nv: loop dims indexing the layer's weights (0: none) */
+    uint64_t *wpp;           /* nv: weight words per point of those dims */
     /* configurations */
     int p;
     int *K;                  /* configs per vertex */
@@ -94,6 +97,8 @@ oracle_t *oracle_new(int nv, const int *ndims, const uint64_t *sizes, const uint
     o->size = calloc((size_t)nv * MAXD, sizeof(uint64_t));
     o->reduce_mask = calloc(nv, sizeof(uint32_t));
     o->fpp = calloc(nv, sizeof(uint64_t));
+    o->weight_mask = calloc(nv, sizeof(uint32_t));
+    o->wpp = calloc(nv, sizeof(uint64_t));
     for (int v = 0; v < nv; v++) {
         o->ndims[v] = ndims[v];
         for (int k = 0; k < ndims[v]; k++) o->size[v * MAXD + k] = sizes[v * MAXD + k];
@@ -153,7 +158,7 @@ void oracle_free(oracle_t *o) {
     free_configs(o);
     for (int v = 0; v < o->nv; v++) free(o->nbr[v]);
     free(o->nbr); free(o->deg);
-    free(o->size); free(o->reduce_mask); free(o->fpp);
+    free(o->size); free(o->reduce_mask); free(o->fpp); free(o->weight_mask); free(o->wpp);
     free(o->src); free(o->dst); free(o->rank); free(o->src_dim); free(o->dst_dim); free(o->elems);
     free(o);
 }
@@ -184,7 +189,10 @@ static int enum_rec(int d, int k, uint64_t budget, int pow2, uint32_t *cur, uint
  *   comm    = (prod_{k in reduce} s_k - 1) * ceil(prod_{k not in reduce} n_k
  *                                                 / prod_{k not in reduce} s_k)
  *   t_l     = compute + r * comm
- * (comm is the partial-sum reduction a split contraction dim requires.) */
+ * (comm is the partial-sum reduction a split contraction dim requires.)
+ * With grad_sync, t_l also carries the data-parallel weight-gradient
+ * all-reduce (an assumed form, as the paper prints no formula; see
+ * oracle_set_grad_sync). */
 static int layer_cost(oracle_t *o, int v, const uint32_t *s, uint64_t *out) {
     uint64_t flops = o->fpp[v], P = 1, red_split = 1, keep_n = 1, keep_split = 1;
     for (int k = 0; k < o->ndims[v]; k++) {
@@ -203,8 +211,48 @@ static int layer_cost(oracle_t *o, int v, const uint32_t *s, uint64_t *out) {
     if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;
     if (!mul_ok(o->r, comm, &comm_r)) return 0;
     if (!add_ok(compute, comm_r, &total)) return 0;
+    if (o->grad_sync && o->weight_mask[v]) {
+        /* the weight tensor (wpp words per point of the weight dims) is cut by
+         * the splits of the weight dims into shards of S words; each shard is
+         * held by the R devices that differ only in the other dims, which
+         * all-reduce its gradient: a ring moves 2 (R - 1) / R * S words per
+         * device */
+        uint64_t W = o->wpp[v], Pw = 1, R = 1;
+        for (int k = 0; k < o->ndims[v]; k++) {
+            if (o->weight_mask[v] >> k & 1u) {
+                if (!mul_ok(W, o->size[v * MAXD + k], &W)) return 0;
+                Pw *= s[k];
+            } else {
+                R *= s[k];
+            }
+        }
+        uint64_t S = ceil_div(W, Pw);
+        unsigned __int128 words = ((unsigned __int128)2 * (R - 1) * S + (R - 1)) / R;
+        uint64_t grad;
+        if (words >> 64 || !mul_ok(o->r, (uint64_t)words, &grad) || !add_ok(total, grad, &total)) return 0;
+    }
     *out = total;
     return 1;
+}
+
+/* Weight tensors of the layers: mask[v] = loop dims indexing v's weights,
+ * wpp[v] = words per point of those dims.  Used by the gradient term. */
+int oracle_set_weights(oracle_t *o, const uint32_t *mask, const uint64_t *wpp) {
+    for (int v = 0; v < o->nv; v++) {
+        if (mask[v] >> o->ndims[v]) return fail(o, "weight dim out of range");
+        o->weight_mask[v] = mask[v];
+        o->wpp[v] = wpp[v];
+    }
+    return 0;
+}
+
+/* 1: the next configuration enumeration adds the weight-gradient all-reduce
+ * to every layer cost.  Data parallelism replicates weights, and Sec. I names
+ * the gradient all-reduce as its communication, but no formula is printed;
+ * this oracle takes a ring all-reduce of each weight shard among its replicas. */
+int oracle_set_grad_sync(oracle_t *o, int on) {
+    o->grad_sync = on != 0;
+    return 0;
 }
 
 /* r * t_x(u, v): zero when both endpoints split every dim of the tensor the

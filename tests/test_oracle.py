@@ -616,6 +616,70 @@ def test_theorem1_volume_costs(seed):
         To, Ao = o.table(i)
         assert To.tolist() == T and Ao.tolist() == A
 
+
+# ------------------------------------------------------------------ weight-gradient all-reduce
+def test_grad_sync_hand_values():
+    """FC (64, 256, 256), weights (out, in) = 65 536 words, r = 8, p = 4:
+    (4,1,1): 4 replicas of the whole weight, ring all-reduce 2*3/4*65536 = 98 304
+    words: 2 097 152 + 786 432 = 2 883 584.  (1,4,1): one replica, no term:
+    2 097 152.  (1,1,4): 2 490 368 (partial sums only).  (2,2,1): shards of
+    32 768 held twice: 32 768 words, 2 359 296.  (2,1,2): 2 097 152 + 65 536
+    (partial sums) + 262 144 = 2 424 832.  p = 6, (3,2,1): 3 replicas of
+    32 768-word shards, ceil(2*2/3*32768) = 43 691 words: 1 398 102 + 349 528."""
+    from oracle.oracle import Oracle
+    o = Oracle(fc_chain())
+    o.configs(4, grad_sync=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    L = o.layer_costs(0)
+    want = {(4, 1, 1): 2_883_584, (1, 4, 1): 2_097_152, (1, 1, 4): 2_490_368, (2, 2, 1): 2_359_296,
+            (2, 1, 2): 2_424_832}
+    for t, v in want.items():
+        assert int(L[sp.index(t)]) == v, t
+    o = Oracle(fc_chain(p=6))
+    o.configs(6, all_integers=True, grad_sync=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    assert int(o.layer_costs(0)[sp.index((3, 2, 1))]) == 1_747_630
+    # without the option the costs are the benchmark's model
+    o = Oracle(fc_chain())
+    o.configs(4)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    assert int(o.layer_costs(0)[sp.index((4, 1, 1))]) == 2_097_152
+
+
+def test_grad_sync_fc_chain_optimum():
+    """With the gradient term W0's optimum is no longer data parallel: every
+    layer split 4 ways over `out` (no replicas, no partial sums) costs
+    2 097 152, and each of the 3 edges re-distributes 16 384 / 4 words, x 8:
+    8 388 608 + 98 304 = 8 486 912, equal to exhaustive search."""
+    from oracle.oracle import Oracle
+    g = fc_chain()
+    o = Oracle(g)
+    o.configs(4, grad_sync=True)
+    o.solve()
+    L, R, src, dst = _tables(o, g)
+    mc, strat = o.result()
+    assert mc == 8_486_912 == pins.brute_force(L, R, src, dst)[0]
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    assert [sp[c] for c in strat] == [(1, 4, 1)] * 4
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_theorem1_grad_sync(seed):
+    """Random graphs with random weight tensors: the DP with the gradient term
+    matches exhaustive search, entry by entry."""
+    from oracle.oracle import Oracle
+    g = random_graph(seed + 620, n=3 + seed % 3, p=4, max_dims=2, extra_edges=seed % 3)
+    o = Oracle(g)
+    K = [int(k) for k in o.configs(4, grad_sync=True)]
+    o.solve()
+    L, R, src, dst = _tables(o, g)
+    assert o.result()[0] == pins.brute_force(L, R, src, dst)[0]
+    seq = o.sequence()
+    for i in range(len(seq)):
+        D, T, A = pins.conditioned_table(L, R, src, dst, seq, i, K)
+        To, Ao = o.table(i)
+        assert To.tolist() == T and Ao.tolist() == A
+
 # ------------------------------------------------------------------ breadth-first recurrence (eq. 2)
 def _bfs_order(g):
     """Breadth-first traversal from vertex 0, neighbours in ascending id
@@ -753,6 +817,8 @@ MUTANTS = {
                             "unsigned __int128 words = (E * fwd + cells - 1) / cells;"),
     "volume_dim0_fastest": ("for (int k = o->ndims[u] - 1; k >= 0; k--) { xu_loop[k] = x % su_[k]; x /= su_[k]; }",
                             "for (int k = 0; k < o->ndims[u]; k++) { xu_loop[k] = x % su_[k]; x /= su_[k]; }"),
+    "grad_replicas": ("unsigned __int128 words = ((unsigned __int128)2 * (R - 1) * S + (R - 1)) / R;",
+                      "unsigned __int128 words = ((unsigned __int128)2 * R * S + (R - 1)) / R;"),
     "pow2_only": ("for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {",
                   "for (uint64_t s = 1; s <= budget; s = 2 * s) {"),
 }
@@ -870,7 +936,15 @@ def _pin_suite(lib):
                     return False
         return True
 
+    def grad():
+        o = Oracle(fc_chain(), lib)
+        o.configs(4, grad_sync=True)
+        sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+        L = o.layer_costs(0)
+        return int(L[sp.index((4, 1, 1))]) == 2_883_584 and int(L[sp.index((2, 2, 1))]) == 2_359_296
+
     guard("w0", w0)
+    guard("grad", grad)
     guard("bf", bf)
     guard("volume", volume)
     guard("all_integers", all_integers)

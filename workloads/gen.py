@@ -11,9 +11,13 @@ Graph dict layout (shared by every consumer)::
 
     {"name": str, "p": int, "comm_weight": int,
      "vertices": [{"name", "dims": [n_0..n_{d-1}], "dim_names", "reduce": [k..],
-                   "flops_per_point": int}],
+                   "flops_per_point": int,
+                   "weight_dims": [k..], "weight_per_point": int}],   # optional
      "edges": [{"src", "dst", "src_dim": [..], "dst_dim": [..], "elems": int}]}
 
+``weight_dims`` (optional) name the loop dims that index the layer's weight
+tensor, which holds ``weight_per_point`` words per point of those dims (a
+k x k convolution: 9 per (co, ci) pair); layers without weights omit both.
 ``src_dim[k]`` / ``dst_dim[k]`` give, for tensor dim k, the loop dim of the
 source / destination vertex that indexes it (-1: that endpoint does not split
 this tensor dim).  Vertex ids are list positions; they are the tie-break of the
@@ -36,12 +40,16 @@ class _Builder:
         self.g = {"name": name, "p": int(p), "comm_weight": int(comm_weight),
                   "vertices": [], "edges": []}
 
-    def vertex(self, name, dims, dim_names, reduce, flops_per_point):
+    def vertex(self, name, dims, dim_names, reduce, flops_per_point, weights=None):
+        """weights: (loop dims indexing the weight tensor, words per point)."""
         assert len(dims) == len(dim_names)
-        self.g["vertices"].append({
-            "name": name, "dims": [int(x) for x in dims],
-            "dim_names": list(dim_names), "reduce": sorted(int(k) for k in reduce),
-            "flops_per_point": int(flops_per_point)})
+        vx = {"name": name, "dims": [int(x) for x in dims],
+              "dim_names": list(dim_names), "reduce": sorted(int(k) for k in reduce),
+              "flops_per_point": int(flops_per_point)}
+        if weights is not None:
+            vx["weight_dims"] = sorted(int(k) for k in weights[0])
+            vx["weight_per_point"] = int(weights[1])
+        self.g["vertices"].append(vx)
         return len(self.g["vertices"]) - 1
 
     def edge(self, src, dst, src_dim, dst_dim, elems=None):
@@ -70,7 +78,7 @@ def fc_chain(p: int = 4, layers: int = 4, batch: int = 64, width: int = 256):
     the next.
     """
     b = _Builder(f"fc_chain{layers}_b{batch}_w{width}_p{p}", p)
-    ids = [b.vertex(f"fc{k}", (batch, width, width), ("b", "out", "in"), (2,), 2)
+    ids = [b.vertex(f"fc{k}", (batch, width, width), ("b", "out", "in"), (2,), 2, ((1, 2), 1))
            for k in range(layers)]
     for u, v in zip(ids, ids[1:]):
         b.edge(u, v, (0, 1), (0, 2))
@@ -97,7 +105,7 @@ def residual_cnn(seed: int = 0, p: int = 8, layers: int = 16, batch: int = 128):
     ci = ci0
     for k in range(layers):
         hw = 64 if k < layers // 2 else 32
-        ids.append(b.vertex(f"conv{k}", (batch, cos[k], ci, hw, hw), _CONV_DIMS, (2,), 18))
+        ids.append(b.vertex(f"conv{k}", (batch, cos[k], ci, hw, hw), _CONV_DIMS, (2,), 18, ((1, 2), 9)))
         ci = cos[k]
     # activation (b, c, h, w): producer dims (b, co, h, w) -> consumer (b, ci, h, w)
     for k in range(layers - 1):
@@ -122,7 +130,7 @@ def inception(seed: int = 0, p: int = 16, modules: int = 12, batch: int = 128):
     """
     rng = np.random.default_rng(seed)
     b = _Builder(f"inception{modules}_seed{seed}_p{p}", p)
-    stem = b.vertex("stem", (batch, 192, 3, 35, 35), _CONV_DIMS, (2,), 18)
+    stem = b.vertex("stem", (batch, 192, 3, 35, 35), _CONV_DIMS, (2,), 18, ((1, 2), 9))
     x, x_is_concat, cin = stem, False, 192
     third = modules // 3
     for m in range(modules):
@@ -135,7 +143,7 @@ def inception(seed: int = 0, p: int = 16, modules: int = 12, batch: int = 128):
                 ksz = int(rng.choice((1, 3, 5)))
                 co = int(rng.choice(_CHANNELS_W2))
                 v = b.vertex(f"m{m}_b{br}_c{dl}_k{ksz}", (batch, co, prev_c, hw, hw),
-                             _CONV_DIMS, (2,), 2 * ksz * ksz)
+                             _CONV_DIMS, (2,), 2 * ksz * ksz, ((1, 2), ksz * ksz))
                 src = (0, 1, 2, 3) if prev_is_concat else (0, 1, 3, 4)
                 b.edge(prev, v, src, (0, 2, 3, 4))
                 prev, prev_c, prev_is_concat = v, co, False
@@ -145,7 +153,7 @@ def inception(seed: int = 0, p: int = 16, modules: int = 12, batch: int = 128):
         for e in ends:
             b.edge(e, cat, (0, 1, 3, 4), (0, 1, 2, 3))
         x, x_is_concat, cin = cat, True, cout_total
-    fc = b.vertex("fc", (batch, 1000, cin), ("b", "out", "in"), (2,), 2)
+    fc = b.vertex("fc", (batch, 1000, cin), ("b", "out", "in"), (2,), 2, ((1, 2), 1))
     # pooled features: batch and channels map onto the FC, spatial dims do not
     hw_last = b.g["vertices"][x]["dims"][2]
     b.edge(x, fc, (0, 1, 2, 3), (0, 2, -1, -1), elems=batch * cin * hw_last * hw_last)
@@ -167,7 +175,7 @@ def lstm_grid(p: int = 32, layers: int = 2, steps: int = 20, batch: int = 64,
     for l in range(layers):
         for t in range(steps):
             cell[l, t] = b.vertex(f"cell_l{l}_t{t}", (batch, 4 * hidden, 2 * hidden),
-                                  ("b", "gate", "in"), (2,), 2)
+                                  ("b", "gate", "in"), (2,), 2, ((1, 2), 1))
     hid_elems = batch * hidden
     for l in range(layers):
         for t in range(steps):
@@ -175,7 +183,7 @@ def lstm_grid(p: int = 32, layers: int = 2, steps: int = 20, batch: int = 64,
                 b.edge(cell[l, t], cell[l, t + 1], (0, 1), (0, 2), elems=hid_elems)
             if l + 1 < layers:
                 b.edge(cell[l, t], cell[l + 1, t], (0, 1), (0, 2), elems=hid_elems)
-    proj = b.vertex("proj", (batch * steps, vocab, hidden), ("bs", "vocab", "in"), (2,), 2)
+    proj = b.vertex("proj", (batch * steps, vocab, hidden), ("bs", "vocab", "in"), (2,), 2, ((1, 2), 1))
     for t in range(steps):
         b.edge(cell[layers - 1, t], proj, (0, 1), (0, 2), elems=hid_elems)
     return b.done()
@@ -200,14 +208,14 @@ def transformer(p: int = 64, enc_layers: int = 6, dec_layers: int = 6, d_model: 
     BSD = ("b", "s", "d")
     ATT = ("b", "s", "h", "o", "i")
 
-    def ln(name):
-        return b.vertex(name, (B, S, D), BSD, (), 8)
+    def ln(name):   # residual add + layernorm; gain and bias per model dim
+        return b.vertex(name, (B, S, D), BSD, (), 8, ((2,), 2))
 
     def self_attention(x, pre):
-        qkv = b.vertex(pre + "qkv", (B, S, H, 3 * dk, D), ATT, (4,), 2)
+        qkv = b.vertex(pre + "qkv", (B, S, H, 3 * dk, D), ATT, (4,), 2, ((2, 3, 4), 1))
         score = b.vertex(pre + "score", (B, S, H, S, dk), ATT, (4,), 2)
         ctx = b.vertex(pre + "ctx", (B, S, H, dk, S), ATT, (4,), 2)
-        oproj = b.vertex(pre + "oproj", (B, S, H, D, dk), ATT, (2, 4), 2)
+        oproj = b.vertex(pre + "oproj", (B, S, H, D, dk), ATT, (2, 4), 2, ((2, 3, 4), 1))
         ln1 = ln(pre + "ln1")
         b.edge(x, qkv, (0, 1, 2), (0, 1, 4))           # (b,s,d) -> qkv (b,s,i)
         b.edge(qkv, score, (0, 1, 2, 3), (0, 1, 2, 4))  # Q (b,s,h,dk) -> score (b,s,h,i)
@@ -219,8 +227,8 @@ def transformer(p: int = 64, enc_layers: int = 6, dec_layers: int = 6, d_model: 
         return ln1
 
     def ffn_block(x, pre, out_name):
-        f1 = b.vertex(pre + "ffn1", (B, S, F, D), ("b", "s", "o", "i"), (3,), 2)
-        f2 = b.vertex(pre + "ffn2", (B, S, D, F), ("b", "s", "o", "i"), (3,), 2)
+        f1 = b.vertex(pre + "ffn1", (B, S, F, D), ("b", "s", "o", "i"), (3,), 2, ((2, 3), 1))
+        f2 = b.vertex(pre + "ffn2", (B, S, D, F), ("b", "s", "o", "i"), (3,), 2, ((2, 3), 1))
         out = ln(pre + out_name)
         b.edge(x, f1, (0, 1, 2), (0, 1, 3))
         b.edge(f1, f2, (0, 1, 2), (0, 1, 3))
@@ -228,22 +236,22 @@ def transformer(p: int = 64, enc_layers: int = 6, dec_layers: int = 6, d_model: 
         b.edge(x, out, (0, 1, 2), (0, 1, 2))            # residual
         return out
 
-    src = b.vertex("src_emb", (B, S, D, V), ("b", "s", "d", "v"), (3,), 2)
+    src = b.vertex("src_emb", (B, S, D, V), ("b", "s", "d", "v"), (3,), 2, ((2, 3), 1))
     x = src
     for l in range(enc_layers):
         pre = f"enc{l}_"
         x = ffn_block(self_attention(x, pre), pre, "ln2")
     enc_out = x
 
-    y = b.vertex("tgt_emb", (B, S, D, V), ("b", "s", "d", "v"), (3,), 2)
+    y = b.vertex("tgt_emb", (B, S, D, V), ("b", "s", "d", "v"), (3,), 2, ((2, 3), 1))
     for l in range(dec_layers):
         pre = f"dec{l}_"
         ln1 = self_attention(y, pre)
-        xq = b.vertex(pre + "xq", (B, S, H, dk, D), ATT, (4,), 2)
-        xkv = b.vertex(pre + "xkv", (B, S, H, 2 * dk, D), ATT, (4,), 2)
+        xq = b.vertex(pre + "xq", (B, S, H, dk, D), ATT, (4,), 2, ((2, 3, 4), 1))
+        xkv = b.vertex(pre + "xkv", (B, S, H, 2 * dk, D), ATT, (4,), 2, ((2, 3, 4), 1))
         xscore = b.vertex(pre + "xscore", (B, S, H, S, dk), ATT, (4,), 2)
         xctx = b.vertex(pre + "xctx", (B, S, H, dk, S), ATT, (4,), 2)
-        xoproj = b.vertex(pre + "xoproj", (B, S, H, D, dk), ATT, (2, 4), 2)
+        xoproj = b.vertex(pre + "xoproj", (B, S, H, D, dk), ATT, (2, 4), 2, ((2, 3, 4), 1))
         ln2 = ln(pre + "ln2")
         b.edge(ln1, xq, (0, 1, 2), (0, 1, 4))
         b.edge(enc_out, xkv, (0, 1, 2), (0, 1, 4))
@@ -256,7 +264,7 @@ def transformer(p: int = 64, enc_layers: int = 6, dec_layers: int = 6, d_model: 
         b.edge(ln1, ln2, (0, 1, 2), (0, 1, 2))           # residual
         y = ffn_block(ln2, pre, "ln3")
 
-    proj = b.vertex("proj", (B, S, V, D), ("b", "s", "v", "d"), (3,), 2)
+    proj = b.vertex("proj", (B, S, V, D), ("b", "s", "v", "d"), (3,), 2, ((2, 3), 1))
     soft = b.vertex("softmax", (B, S, V), ("b", "s", "v"), (), 5)
     b.edge(y, proj, (0, 1, 2), (0, 1, 3))
     b.edge(proj, soft, (0, 1, 2), (0, 1, 2))
@@ -315,7 +323,21 @@ def random_graph(seed: int, n: int, p: int = 4, max_dims: int = 3, extra_edges: 
             continue
         rand_edge(u, v)
         added += 1
+    _random_weights(b, seed)
     return b.done()
+
+
+def _random_weights(b, seed):
+    """Give about two thirds of the vertices a weight tensor over a random
+    non-empty subset of their loop dims (1..4 words per point).  Drawn from a
+    stream of its own, so the rest of the graph does not depend on it."""
+    rng = np.random.default_rng([seed, 0x3E1])
+    for vx in b.g["vertices"]:
+        d = len(vx["dims"])
+        if rng.random() < 0.67:
+            dims = [k for k in range(d) if rng.random() < 0.6] or [int(rng.integers(0, d))]
+            vx["weight_dims"] = dims
+            vx["weight_per_point"] = int(rng.integers(1, 5))
 
 
 def random_costs(seed: int, layer_sizes, edge_shapes, hi: int = 4):
@@ -345,4 +367,5 @@ def chain_graph(seed: int, n: int, p: int = 4, max_dims: int = 3, max_size: int 
         rank = int(rng.integers(1, max(du, dw) + 1))
         b.edge(u, w, [int(rng.integers(-1, du)) for _ in range(rank)],
                [int(rng.integers(-1, dw)) for _ in range(rank)], elems=int(rng.integers(1, 5000)))
+    _random_weights(b, seed)
     return b.done()
