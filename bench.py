@@ -50,14 +50,14 @@ def cpu_model():
     return "unknown"
 
 
-def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False):
+def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False, grad=False):
     """The oracle on the host cores (OpenMP over table entries), on a prefix of
     the vertex order of about `max_cells` cells, then single-threaded on a
     prefix a tenth that size."""
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
-    o.configs(p, all_integers=all_integers, volume=volume)
+    o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad)
 
     def run(cells, nthreads):
         if bf:
@@ -120,16 +120,17 @@ WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "
 
 
 def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False,
-                 volume=False):
+                 volume=False, grad=False):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
-    transfer costs when `volume`); returns the report
+    transfer costs when `volume`; with the weight-gradient term when `grad`);
+    returns the report
     dict (the oracle timed on the same graph: the whole search when it has at
     most `cpu_cells` cells, else a prefix of the vertex order).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import OPT_ORDER, OPT_PROFILE, OPT_TRANSFER, Graph, PaseError
+    from paper_2407_04001_amd import OPT_GRAD_SYNC, OPT_ORDER, OPT_PROFILE, OPT_TRANSFER, Graph, PaseError
     from workloads import workload
 
     g = workload(name, seed)
@@ -137,6 +138,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     pg = Graph(g)
     pg.set_option(OPT_ORDER, int(bf))
     pg.set_option(OPT_TRANSFER, int(volume))
+    pg.set_option(OPT_GRAD_SYNC, int(grad))
     wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
     if all_integers:
         wl += ", every integer split"
@@ -144,12 +146,16 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         wl += ", breadth-first order (eq. 2)"
     if volume:
         wl += ", volume-intersection transfer costs"
-    headline = name == "w4_transformer" and p == g["p"] and not all_integers and not bf and not volume
+    if grad:
+        wl += ", weight-gradient all-reduce"
+    headline = (name == "w4_transformer" and p == g["p"] and not all_integers and not bf and not volume
+                and not grad)
     metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
     config = {"workload": g["name"], "p": p,
               "config_set": "every integer split" if all_integers else "powers of two",
               "order": "breadth-first" if bf else "GenerateSeq",
               "transfer": "volume intersection" if volume else "split match",
+              "grad_sync": grad,
               "vertices": len(g["vertices"]), "edges": len(g["edges"]), "seed": seed}
     try:
         pg.enumerate_configs(p, all_integers=all_integers)
@@ -189,19 +195,25 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     achieved = ops * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
     t_roof_ms = ops * cells / (FP64_OPS_PEAK_T * 1e12) * 1e3
     parity = None
-    if bf:
-        gold_name = f"{name}_seed{seed}_p{p}_bf.json"
-    elif volume:
-        gold_name = f"{name}_seed{seed}_volume.json" if p == g["p"] and not all_integers else None
-    elif all_integers:
-        gold_name = f"{name}_seed{seed}_p{p}_all.json"
-    else:
-        gold_name = f"{name}_seed{seed}.json" if p == g["p"] else None
+    # the oracle's stored answer for exactly this variant, if one was written
+    gold_name = None
+    if sum((bf, volume, grad, all_integers)) <= 1:
+        if bf:
+            gold_name = f"{name}_seed{seed}_p{p}_bf.json"
+        elif volume:
+            gold_name = f"{name}_seed{seed}_volume.json"
+        elif grad:
+            gold_name = f"{name}_seed{seed}_grad.json"
+        elif all_integers:
+            gold_name = f"{name}_seed{seed}_p{p}_all.json"
+        else:
+            gold_name = f"{name}_seed{seed}.json"
     gold_path = os.path.join(ROOT, "tests", "golden", gold_name) if gold_name else None
     if gold_path and os.path.exists(gold_path):
         with open(gold_path) as f:
             gold = json.load(f)
-        parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
+        if gold.get("p", g["p"]) == p:
+            parity = (mc == int(gold["min_cost"]) and strat == gold["strategy"])
     out = {
         "metric": metric, "value": cells * steps / elapsed, "unit": "cell-updates/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup,
@@ -229,7 +241,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
                      "cells_per_step": col_cells},
     }
     if not no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf, volume)
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf, volume, grad)
     return out
 
 
@@ -253,6 +265,8 @@ def main():
                     help="vertex order: GenerateSeq (default) or breadth-first (recurrence 2)")
     ap.add_argument("--transfer", choices=("match", "volume"), default="match",
                     help="transfer cost model: split match (default) or volume intersection")
+    ap.add_argument("--grad-sync", action="store_true",
+                    help="add the weight-gradient all-reduce to the layer costs")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -269,7 +283,7 @@ def main():
     for name in names:
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
-                           args.transfer == "volume")
+                           args.transfer == "volume", args.grad_sync)
         print(json.dumps(out), flush=True)
 
 

@@ -59,12 +59,18 @@ typedef enum {
 /* One vertex = one layer and its iteration space (Sec. II).  size[k] is the
  * extent of loop dim k.  reduce_mask bit k marks loop dim k as contracted
  * (splitting it requires a partial-sum reduction).  flops_per_point is the
- * work of one iteration point (2 for a GEMM, 2*kh*kw for a convolution). */
+ * work of one iteration point (2 for a GEMM, 2*kh*kw for a convolution).
+ * weight_mask bit k marks loop dim k as an index of the layer's weight tensor,
+ * which holds weight_per_point words per point of those dims (kh*kw for a
+ * convolution's (co, ci)); 0 = no weights.  Read only with
+ * PASE_OPT_GRAD_SYNC. */
 typedef struct {
     uint32_t ndims;
     uint64_t size[PASE_MAX_DIMS];
     uint32_t reduce_mask;
     uint64_t flops_per_point;
+    uint32_t weight_mask;
+    uint64_t weight_per_point;
 } pase_vertex_desc;
 
 /* One edge = a tensor flowing from src to dst (Sec. II).  Tensor dim k is
@@ -134,7 +140,7 @@ typedef enum {
                                    Re-plans; TOO_LARGE when a dependent set exceeds
                                    PASE_MAX_DEP or a table 2^31 entries (the blow-up that
                                    motivates GenerateSeq) */
-    PASE_OPT_TRANSFER = 14      /* transfer cost model of the next pase_enumerate_configs: 0
+    PASE_OPT_TRANSFER = 14,     /* transfer cost model of the next pase_enumerate_configs: 0
                                    (default) split match -- 0 when every tensor dim is split alike
                                    at both ends, else ceil(elems / max(P_u, P_v)); 1 the volume
                                    intersection of Sec. II, max_d |A(v,d)| - |A(v,d) n A(u,d)|
@@ -148,6 +154,15 @@ typedef enum {
                                    (INVALID_ARGUMENT) when p^(mapped dims) reaches 2^32, and
                                    with distinct mapped loop dims p^2 must stay below 2^32 (p <
                                    65536) */
+    PASE_OPT_GRAD_SYNC = 15     /* 1: the next pase_enumerate_configs adds the data-parallel
+                                   weight-gradient all-reduce to every layer cost (an assumed
+                                   form; the paper names the communication but prints no
+                                   formula): the weight tensor (weight_per_point x the sizes of
+                                   the weight_mask dims) is cut into shards by the splits of
+                                   those dims, each shard is replicated on the R devices that
+                                   differ in the other dims, and a ring all-reduce moves
+                                   ceil(2 (R - 1) S / R) words of an S-word shard per device,
+                                   weighted by r.  0 (default): the benchmark's cost model */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

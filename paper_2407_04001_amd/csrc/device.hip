@@ -932,6 +932,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         x.ndims = g->V[v].ndims;
         x.reduce_mask = g->V[v].reduce_mask;
         x.factors = g->factors ? 1 : 0;
+        x.weight_n = g->weight_n[v];
+        x.weight_mask = g->V[v].weight_mask;
         off += g->ex[v].size();
         loff += g->K[v];
     }

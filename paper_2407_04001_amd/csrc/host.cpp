@@ -34,8 +34,8 @@ static uint32_t bits_for(uint32_t K) {
 // every edge joining v_i and a later vertex, plus the table lookup of every
 // connected subset -- is at most maxL(v_i) + sum maxR + sum Tmax_j.  The table
 // entry T_i(phi) = min_c Q_i(phi, c) is at most Q_i(phi, c0) for any single c0:
-// with model costs c0 is the unsplit configuration (cost F) or the one that
-// splits a non-contracted dim p ways (cost ceil(F / p), no partial sums); with
+// with model costs c0 is the cheapest of the unsplit configuration (cost F)
+// and the ones that split a single dim p ways (costs evaluated exactly); with
 // caller-given costs it is the cheapest layer configuration.  These bounds
 // follow the recurrence instead of summing every cost of the graph, so deep
 // graphs keep exact fp64 keys.  false: a bound exceeds 64 bits.
@@ -56,12 +56,18 @@ bool cost_bounds(pase_graph_t g, std::vector<uint64_t> *qmax, std::vector<uint64
                 lo = std::min(lo, g->ov_layer[g->ov_layer_off[v] + c]);
             }
         } else {
+            // the exact cost of single configurations: unsplit (F: no partial
+            // sums, no replicas), and each dim k split p ways; every term of
+            // these is bounded by the parts of maxL, so nothing overflows
             const pase_vertex_desc &d = g->V[v];
-            const uint64_t F = g->flops[v];
-            const bool keep_dim = (d.reduce_mask & ((1u << d.ndims) - 1)) != ((1u << d.ndims) - 1);
-            // all dims contracted: keep_n = 1 and r * (p - 1) <= maxL - F
-            const uint64_t one = (F + g->p - 1) / g->p + (keep_dim ? 0 : g->r * (uint64_t)(g->p - 1));
-            lo = std::min(F, one);
+            const uint64_t F = g->flops[v], W = g->weight_n[v], p = g->p;
+            lo = F;
+            for (uint32_t k = 0; k < d.ndims; k++) {
+                uint64_t c = (F + p - 1) / p;
+                if ((d.reduce_mask >> k) & 1u) c += g->r * (p - 1) * g->keep_n[v];
+                if (W && !((d.weight_mask >> k) & 1u)) c += g->r * (2 * W - 2 * W / p);
+                lo = std::min(lo, c);
+            }
         }
         uint64_t rest = 0;
         for (int e : vp.edges) {
@@ -113,6 +119,7 @@ extern "C" pase_status pase_graph_create(const pase_vertex_desc *v, uint32_t nv,
         for (uint32_t k = 0; k < v[i].ndims; k++)
             if (v[i].size[k] == 0) return PASE_ERR_INVALID_ARGUMENT;
         if (v[i].reduce_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
+        if (v[i].weight_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
     }
     for (uint32_t k = 0; k < ne; k++) {
         const pase_edge_desc &d = e[k];
@@ -816,6 +823,7 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     const size_t nv = g->V.size();
     g->K.assign(nv, 0);
     g->ex.assign(nv, {});
+    g->weight_n.assign(nv, 0);
     g->flops.assign(nv, 0);
     g->keep_n.assign(nv, 0);
     g->maxL.assign(nv, 0);
@@ -865,10 +873,19 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
         if (fl >> 62 || keep >> 62) return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 2^62");
         g->flops[v] = fl;
         g->keep_n[v] = keep;
-        // t_l <= flops + r * (p - 1) * keep
+        // t_l <= flops + r * (p - 1) * keep (+ r * 2 * weight words with the gradient term)
         uint64_t comm, m;
         if (!mul_ok(g->r, (uint64_t)(p - 1), &comm) || !mul_ok(comm, keep, &comm) || !add_ok(fl, comm, &m))
             return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 64 bits");
+        if (g->grad_opt && g->V[v].weight_mask && g->V[v].weight_per_point) {
+            uint64_t w = g->V[v].weight_per_point, gr;
+            for (uint32_t k = 0; k < d; k++)
+                if (((g->V[v].weight_mask >> k) & 1u) && !mul_ok(w, g->V[v].size[k], &w))
+                    return fail(g, PASE_ERR_OVERFLOW, "weight tensor exceeds 64 bits");
+            if (w >> 60 || !mul_ok(g->r, 2 * w, &gr) || !add_ok(m, gr, &m))
+                return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 64 bits");
+            g->weight_n[v] = w;
+        }
         g->maxL[v] = m;
     }
     g->maxR.assign(g->E.size(), 0);
@@ -969,6 +986,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     case PASE_OPT_ORDER:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "order 0 or 1");
         g->order_mode = (int)value;
+        break;
+    case PASE_OPT_GRAD_SYNC:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "grad sync 0 or 1");
+        g->grad_opt = (uint32_t)value;
         break;
     case PASE_OPT_TRANSFER:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "transfer model 0 or 1");

@@ -36,6 +36,8 @@ struct DevVertex {            // configuration data of one vertex (uploaded once
     uint32_t factors;         // 0: split rows hold log2 of power-of-two factors and the
                               // per-configuration device byte its exponent sum; 1: both
                               // hold the factors / device count themselves (p <= 255)
+    uint64_t weight_n;        // gradient term: words of the weight tensor (0: no term)
+    uint32_t weight_mask, pad;
 };
 
 struct DevEdge {
@@ -301,6 +303,8 @@ struct pase_graph_s {
     bool enumerated = false;
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
     uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
+    uint32_t grad_opt = 0;          // pase_option PASE_OPT_GRAD_SYNC, read by pase_enumerate_configs
+    std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix
     uint64_t mat_total = 0;         // volume model: entries of all edge matrices

@@ -58,24 +58,40 @@ constexpr int kBufferWord3 = 0x00020000;
 // nothing overflows.
 __device__ __forceinline__ uint64_t ceil_div_u64(uint64_t a, uint32_t b) { return (a + (b - 1)) / b; }
 
+// Optional weight-gradient term: the weight tensor (weight_n words) is cut
+// into shards of S = ceil(weight_n / P_w) words by the splits of its dims and
+// each shard lives on the R = P / P_w devices that differ in the other dims;
+// a ring all-reduce moves ceil(2 (R - 1) S / R) = 2S - floor(2S / R) words.
 __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
     if (dv.factors) {
-        uint32_t P = 1, red = 1;
+        uint32_t P = 1, red = 1, Pw = 1;
         for (uint32_t k = 0; k < dv.ndims; k++) {
             P *= ex[k];
             if ((dv.reduce_mask >> k) & 1u) red *= ex[k];
+            if ((dv.weight_mask >> k) & 1u) Pw *= ex[k];
         }
-        return ceil_div_u64(dv.flops, P) + r * ((uint64_t)(red - 1) * ceil_div_u64(dv.keep_n, P / red));
+        uint64_t cost = ceil_div_u64(dv.flops, P) + r * ((uint64_t)(red - 1) * ceil_div_u64(dv.keep_n, P / red));
+        if (dv.weight_n) {
+            const uint64_t S2 = 2 * ceil_div_u64(dv.weight_n, Pw);
+            cost += r * (S2 - S2 / (P / Pw));
+        }
+        return cost;
     }
-    uint32_t E = 0, ered = 0;
+    uint32_t E = 0, ered = 0, ew = 0;
     for (uint32_t k = 0; k < dv.ndims; k++) {
         E += ex[k];
         if ((dv.reduce_mask >> k) & 1u) ered += ex[k];
+        if ((dv.weight_mask >> k) & 1u) ew += ex[k];
     }
     uint64_t compute = (dv.flops + ((1ull << E) - 1)) >> E;
     uint32_t ek = E - ered;
     uint64_t part = (dv.keep_n + ((1ull << ek) - 1)) >> ek;
-    return compute + r * (((1ull << ered) - 1) * part);
+    uint64_t cost = compute + r * (((1ull << ered) - 1) * part);
+    if (dv.weight_n) {
+        const uint64_t S2 = 2 * ((dv.weight_n + ((1ull << ew) - 1)) >> ew);
+        cost += r * (S2 - (S2 >> (E - ew)));
+    }
+    return cost;
 }
 
 // Device byte of one configuration: the exponent sum log2(P) of power-of-two

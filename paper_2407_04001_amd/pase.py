@@ -21,12 +21,12 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STAT
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
 (OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
  OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS, OPT_LATENCY_WORKERS,
- OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER) = range(1, 15)
+ OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER, OPT_GRAD_SYNC) = range(1, 16)
 
 
 class VertexDesc(C.Structure):
     _fields_ = [("ndims", C.c_uint32), ("size", C.c_uint64 * MAX_DIMS), ("reduce_mask", C.c_uint32),
-                ("flops_per_point", C.c_uint64)]
+                ("flops_per_point", C.c_uint64), ("weight_mask", C.c_uint32), ("weight_per_point", C.c_uint64)]
 
 
 class EdgeDesc(C.Structure):
@@ -144,6 +144,8 @@ def pase_graph_create(vertices, edges, comm_weight: int = 8, seq_rule: int = 0):
             V[i].size[k] = int(n)
         V[i].reduce_mask = sum(1 << int(k) for k in v["reduce"])
         V[i].flops_per_point = int(v["flops_per_point"])
+        V[i].weight_mask = sum(1 << int(k) for k in v.get("weight_dims", []))
+        V[i].weight_per_point = int(v.get("weight_per_point", 0))
     E = (EdgeDesc * max(ne, 1))()
     for i, e in enumerate(edges):
         E[i].src, E[i].dst, E[i].rank = int(e["src"]), int(e["dst"]), len(e["src_dim"])

@@ -7,7 +7,7 @@ strategy, the cell count, per-vertex fingerprints of the cost and argmin
 tables (canonical order, SplitMix64-based, see ``pase.h``) and a seeded sample
 of table entries.
 
-    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only] [--volume-only]
+    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only] [--volume-only] [--grad-only]
 """
 from __future__ import annotations
 
@@ -29,9 +29,11 @@ from workloads import workload  # noqa: E402
 # Instances: the workload and seed; p (None = the workload's own power-of-two
 # p); `all_integers` enumerates Sec. II's full C(v); `bf` solves the
 # breadth-first recurrence (2) instead of GenerateSeq + recurrence (4);
-# `volume` prices transfers with the volume-intersection model.
-def _inst(name, seed=0, p=None, all_integers=False, bf=False, volume=False):
-    return {"name": name, "seed": seed, "p": p, "all_integers": all_integers, "bf": bf, "volume": volume}
+# `volume` prices transfers with the volume-intersection model; `grad` adds the
+# weight-gradient all-reduce to the layer costs.
+def _inst(name, seed=0, p=None, all_integers=False, bf=False, volume=False, grad=False):
+    return {"name": name, "seed": seed, "p": p, "all_integers": all_integers, "bf": bf, "volume": volume,
+            "grad": grad}
 
 
 INSTANCES = [_inst("w0_fc_chain"), _inst("w1_residual_cnn"), _inst("w1_residual_cnn", 1),
@@ -41,15 +43,19 @@ INSTANCES = [_inst("w0_fc_chain"), _inst("w1_residual_cnn"), _inst("w1_residual_
              _inst("w4_transformer", p=12, all_integers=True),
              _inst("w1_residual_cnn", p=64, bf=True),
              _inst("w1_residual_cnn", volume=True), _inst("w2_inception", volume=True),
-             _inst("w3_lstm_grid", volume=True), _inst("w4_transformer", volume=True)]
+             _inst("w3_lstm_grid", volume=True), _inst("w4_transformer", volume=True),
+             _inst("w1_residual_cnn", grad=True), _inst("w2_inception", grad=True),
+             _inst("w3_lstm_grid", grad=True), _inst("w4_transformer", grad=True)]
 
 
 def file_name(name: str, seed: int, p=None, all_integers: bool = False, bf: bool = False,
-              volume: bool = False) -> str:
+              volume: bool = False, grad: bool = False) -> str:
     if bf:
         return f"{name}_seed{seed}_p{p}_bf.json"
     if volume:
         return f"{name}_seed{seed}_volume.json"
+    if grad:
+        return f"{name}_seed{seed}_grad.json"
     return f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
 
 
@@ -57,11 +63,11 @@ SAMPLES_PER_TABLE = 24
 
 
 def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False, bf: bool = False,
-           volume: bool = False) -> dict:
+           volume: bool = False, grad: bool = False) -> dict:
     g = workload(name, seed)
     p = p or g["p"]
     o = Oracle(g)
-    K = o.configs(p, all_integers=all_integers, volume=volume)
+    K = o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad)
     t0 = time.time()
     if bf:
         o.solve_bf(threads=threads)
@@ -85,6 +91,7 @@ def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = Fals
     return {"workload": name, "seed": seed, "p": p, "all_integers": all_integers,
             "order": "breadth-first" if bf else "GenerateSeq",
             "transfer": "volume intersection" if volume else "split match",
+            "grad_sync": grad,
             "num_configs": [int(k) for k in K],
             "sequence": seq, "min_cost": str(mc), "strategy": strat, "cells": o.cells(),
             "tables": tables, "oracle_seconds": round(wall, 3)}
@@ -98,6 +105,7 @@ def main():
                     help="only the instances with every integer split")
     ap.add_argument("--bf-only", action="store_true", help="only the breadth-first instances")
     ap.add_argument("--volume-only", action="store_true", help="only the volume-model instances")
+    ap.add_argument("--grad-only", action="store_true", help="only the gradient-term instances")
     args = ap.parse_args()
     build(force=False)
     for inst in INSTANCES:
@@ -110,10 +118,13 @@ def main():
             continue
         if args.volume_only and not inst["volume"]:
             continue
+        if args.grad_only and not inst["grad"]:
+            continue
         t = time.time()
-        out = golden(name, seed, args.threads, inst["p"], inst["all_integers"], inst["bf"], inst["volume"])
-        path = os.path.join(HERE, file_name(**{k: inst[k] for k in ("seed", "p", "all_integers", "bf", "volume")},
-                                            name=name))
+        out = golden(name, seed, args.threads, inst["p"], inst["all_integers"], inst["bf"], inst["volume"],
+                     inst["grad"])
+        keys = ("seed", "p", "all_integers", "bf", "volume", "grad")
+        path = os.path.join(HERE, file_name(name=name, **{k: inst[k] for k in keys}))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))
         print(f"{name} seed {seed}: min_cost {out['min_cost']} cells {out['cells']:.3e} "

@@ -32,10 +32,10 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False, volume=False):
+def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False, volume=False, grad=False):
     from oracle.oracle import Oracle
     o = Oracle(g)
-    o.configs(p or g["p"], all_integers=all_integers, volume=volume)
+    o.configs(p or g["p"], all_integers=all_integers, volume=volume, grad_sync=grad)
     if costs is not None:
         o.set_costs(*costs)
     if bf:
@@ -69,10 +69,11 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False):
+         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False, grad=False):
     pg = P.Graph(g, seq_rule=rule)
     pg.set_option(P.OPT_ORDER, int(bf))
     pg.set_option(P.OPT_TRANSFER, int(volume))
+    pg.set_option(P.OPT_GRAD_SYNC, int(grad))
     pg.enumerate_configs(p or g["p"], all_integers=all_integers)
     pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
@@ -260,11 +261,13 @@ def test_library_owned_workspace(P):
 
 
 # ------------------------------------------------------------------ full-size workloads
-def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False):
+def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad=False):
     if bf:
         fn = f"{name}_seed{seed}_p{p}_bf.json"
     elif volume:
         fn = f"{name}_seed{seed}_volume.json"
+    elif grad:
+        fn = f"{name}_seed{seed}_grad.json"
     else:
         fn = f"{name}_seed{seed}_p{p}_all.json" if all_integers else f"{name}_seed{seed}.json"
     with open(os.path.join(GOLDEN, fn)) as f:
@@ -272,13 +275,13 @@ def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False):
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False):
-    gold = _golden(name, seed, p, all_integers, bf, volume)
+                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False):
+    gold = _golden(name, seed, p, all_integers, bf, volume, grad)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume}")
+        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume)
+                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume, grad=grad)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -602,3 +605,39 @@ def test_volume_model_transformer_against_golden(P):
     configuration and with every table kept and fingerprinted."""
     _check_golden(P, "w4_transformer", 0, volume=True, keep=False)
     _check_golden(P, "w4_transformer", 0, volume=True, keep=True)
+
+
+# ------------------------------------------------------------------ weight-gradient all-reduce
+@pytest.mark.parametrize("seed", range(8))
+def test_grad_sync_random_graphs(P, seed):
+    """PASE_OPT_GRAD_SYNC = 1 on random graphs with random weight tensors: the
+    device layer costs equal the oracle's, and so do the search and every
+    table entry (both configuration sets, with and without volume costs)."""
+    p, all_int, volume = ((4, False, False), (8, False, False), (6, True, False), (16, False, True),
+                          (12, True, True), (32, False, False), (5, True, False), (2, False, True))[seed]
+    g = random_graph(seed + 640, n=4 + seed % 4, p=p, max_dims=3, extra_edges=1 + seed % 3, max_size=300)
+    say(f"gradient term random graph seed={seed + 640} p={p} all_integers={all_int} volume={volume}")
+    o = _oracle(g, p=p, all_integers=all_int, volume=volume, grad=True)
+    pg, mc, strat = _run(P, g, p=p, all_integers=all_int, volume=volume, grad=True)
+    for v in range(len(g["vertices"])):
+        assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=512)
+
+
+def test_grad_sync_fc_chain(P):
+    """W0 with the gradient term: 8 486 912, every layer split 4 ways over out."""
+    g = workload("w0_fc_chain")
+    pg, mc, strat = _run(P, g, grad=True)
+    assert mc == 8_486_912
+    assert [pg.config_splits(v, c) for v, c in enumerate(strat)] == [[1, 4, 1]] * 4
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
+def test_grad_sync_workloads_against_golden(P, name):
+    _check_golden(P, name, 0, grad=True)
+
+
+def test_grad_sync_transformer_against_golden(P):
+    _check_golden(P, "w4_transformer", 0, grad=True, keep=False)
+    _check_golden(P, "w4_transformer", 0, grad=True, keep=True)

@@ -164,24 +164,28 @@ def test_config_set_option(pase):
     assert _status(lambda: P.pase_set_option(pg.h, P.OPT_CONFIG_SET, 2)) == P.INVALID_ARGUMENT
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(16))
 def test_key_bounds_hold(pase, seed):
     """The per-position bounds that size the keys hold on the oracle's tables:
     key_bound >= the largest value minimised over at that position (exhaustive
     search) and table_bound >= every table entry; model costs with both
-    configuration sets, and caller-given costs."""
+    configuration sets, with the gradient term, with volume transfer costs,
+    and caller-given costs."""
     from oracle.oracle import Oracle
     all_int = seed % 3 == 1
     p = (4, 6, 8)[seed % 3]
+    grad, volume = seed % 4 == 3, seed % 5 == 4
     g = random_graph(seed + 900, n=3 + seed % 4, p=p, max_dims=2, extra_edges=seed % 3, max_size=200)
     o = Oracle(g)
-    K = [int(k) for k in o.configs(p, all_integers=all_int)]
+    K = [int(k) for k in o.configs(p, all_integers=all_int, grad_sync=grad, volume=volume)]
     costs = None
     if seed % 3 == 2:
         costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=1000)
         o.set_costs(*costs)
     o.solve()
     pg = pase.Graph(g)
+    pg.set_option(pase.OPT_GRAD_SYNC, int(grad))
+    pg.set_option(pase.OPT_TRANSFER, int(volume))
     pg.enumerate_configs(p, all_integers=all_int)
     if costs is not None:
         pg.override_costs(*costs)
@@ -252,6 +256,24 @@ def test_bf_order_option(pase):
         assert _status(lambda: pg.set_option(P.OPT_ORDER, 1)) == P.TOO_LARGE
         assert _status(lambda: pg.sequence()) == P.BAD_STATE
     assert _status(lambda: P.pase_set_option(pg.h, P.OPT_ORDER, 2)) == P.INVALID_ARGUMENT
+
+
+def test_grad_sync_option(pase):
+    """PASE_OPT_GRAD_SYNC takes 0 or 1; a weight mask past ndims is refused at
+    graph creation; the option raises the layer-cost bound by 2 r W (W0: the
+    weight tensors are 65 536 words, so the key bound grows)."""
+    P = pase
+    pg = P.Graph(fc_chain())
+    pg.enumerate_configs(4)
+    b0 = pg.vertex_info(3)["key_bound"]
+    pg.set_option(P.OPT_GRAD_SYNC, 1)
+    pg.enumerate_configs(4)
+    assert pg.vertex_info(3)["key_bound"] > b0
+    assert _status(lambda: P.pase_set_option(pg.h, P.OPT_GRAD_SYNC, 2)) == P.INVALID_ARGUMENT
+    bad = fc_chain()
+    bad["vertices"][0]["weight_dims"] = [3]
+    with pytest.raises(P.PaseError):
+        P.Graph(bad)
 
 
 def test_transfer_model_option(pase):
