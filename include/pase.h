@@ -154,7 +154,7 @@ typedef enum {
                                    (INVALID_ARGUMENT) when p^(mapped dims) reaches 2^32, and
                                    with distinct mapped loop dims p^2 must stay below 2^32 (p <
                                    65536) */
-    PASE_OPT_GRAD_SYNC = 15     /* 1: the next pase_enumerate_configs adds the data-parallel
+    PASE_OPT_GRAD_SYNC = 15,    /* 1: the next pase_enumerate_configs adds the data-parallel
                                    weight-gradient all-reduce to every layer cost (an assumed
                                    form; the paper names the communication but prints no
                                    formula): the weight tensor (weight_per_point x the sizes of
@@ -163,6 +163,12 @@ typedef enum {
                                    differ in the other dims, and a ring all-reduce moves
                                    ceil(2 (R - 1) S / R) words of an S-word shard per device,
                                    weighted by r.  0 (default): the benchmark's cost model */
+    PASE_OPT_DIRECT_CELLS = 16  /* vertices with at most this many cells (K_v x table entries)
+                                   use the direct fill: every term of recurrence (4) summed per
+                                   cell from its source arrays in one launch, no prep blocks --
+                                   for the long chains of small dependent vertices, where launch
+                                   count dominates.  Default 2^25; 0 = never.  Not used by the
+                                   dataflow schedule or with PASE_OPT_KERNEL = 1 */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */
@@ -291,7 +297,7 @@ pase_status pase_stats(pase_graph_t g, pase_run_stats *out);
  * PASE_OPT_PROFILE=1, its fill time. */
 typedef struct {
     uint32_t position;   /* index in the GenerateSeq order */
-    uint32_t kernel;     /* 0 = generic fill, 1 = row/column-chunk fill */
+    uint32_t kernel;     /* 0 = generic fill, 1 = row/column-chunk fill, 2 = direct fill */
     uint32_t num_configs, dep_count;
     uint64_t entries;    /* |table| = product of K over D(v) */
     uint64_t cells;      /* K_v * entries */

@@ -144,6 +144,19 @@ __global__ __launch_bounds__(256) void k_fill_generic(const GenericArgs *__restr
     generic_item<KeyT, NT>(descs[be[kb].pos], blockIdx.x - be[kb].first);
 }
 
+// Direct fill of the small vertices of one level (batched like the others).
+template <typename KeyT>
+__global__ __launch_bounds__(256) void k_fill_direct(const DirectArgs *__restrict__ descs,
+                                                    const BatchEntry *__restrict__ be, uint32_t nbe,
+                                                    const DevVertex *__restrict__ V, const DevEdge *__restrict__ E,
+                                                    const uint64_t *__restrict__ L, const uint8_t *__restrict__ lsum,
+                                                    const uint64_t *__restrict__ sig, const Contrib *__restrict__ cb,
+                                                    uint64_t r) {
+    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
+    set_priority(be[kb]);
+    direct_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r);
+}
+
 // ------------------------------------------------------------------ back-substitution
 // From the last position down: the configuration of v_i is A_i at the
 // already-chosen configurations of D(i) (every member of D(i) is later in the
@@ -348,9 +361,11 @@ template <typename KeyT>
 struct Launch {
     PrepArgs prep;
     bool rows = false;
+    bool direct = false;
     RowsArgs ra;
     GenericArgs ga;
     ReduceArgs red;
+    DirectArgs da;
 };
 
 static uint32_t plan_digit(const VPlan &vp, int vertex) {
@@ -465,7 +480,31 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             L.prep.total += bk.elems;
             return (int)L.prep.nblocks++;
         };
-        if (vp.kernel == kRows) {
+        if (vp.kernel == kDirect) {
+            // every term over all plan digits; no blocks
+            DirectArgs &da = L.da;
+            std::memset(&da, 0, sizeof da);
+            da.c_begin = (uint32_t)contrib.size();
+            layer_contrib();
+            for (int e : vp.edges) edge_contrib(e, plan_digit(vp, other_of(e)));
+            for (const auto &t : vp.terms) table_contrib(t);
+            da.c_end = (uint32_t)contrib.size();
+            da.vi = (uint32_t)vp.vi;
+            da.K = vp.K;
+            da.bits = vp.bits;
+            da.out_shift = vp.out_shift;
+            da.m = (uint32_t)vp.layout.size();
+            for (size_t k = 0; k < vp.layout.size(); k++) da.rad[k] = g->K[vp.layout[k]];
+            // lanes per entry: enough threads to fill the GPU, at most one wave, at most K
+            da.group_log2 = 0;
+            while (da.group_log2 < 6 && (vp.N << da.group_log2) < 65536 && (2u << da.group_log2) <= vp.K)
+                da.group_log2++;
+            da.N = vp.N;
+            da.T = ws + P.off_T + vp.T_off;
+            da.A = (uint16_t *)(ws + P.off_A + vp.A_off);
+            da.nblk = (uint32_t)std::min<uint64_t>(((vp.N << da.group_log2) + 255) / 256, 65535);
+            L.direct = true;
+        } else if (vp.kernel == kRows) {
             // column block B over (O..., c, z): everything not touching a row digit
             std::vector<int> OZ = vp.O;
             OZ.push_back(vp.z);
@@ -828,7 +867,7 @@ static pase_status flow_simulate(pase_graph_t g, const FlowPlan &fp, uint32_t wo
 // A batched launch: vertices (sequence positions) sharing one kernel variant
 // within one launch slot, with their first workgroups.
 struct Batch {
-    enum Kind { kPrep, kRows, kGeneric, kReduce } kind;
+    enum Kind { kPrep, kRows, kGeneric, kReduce, kDirect } kind;
     int lane;              // two-lane schedule: the stream it runs on
     int group;             // launch group (a slot, or a (level, lane) pair) it belongs to
     uint32_t variant;      // rows: (TZ * 4 + TM) * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime)
@@ -988,11 +1027,13 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     RowsArgs *hr = (RowsArgs *)(hp + n);
     GenericArgs *hg = (GenericArgs *)(hr + n);
     ReduceArgs *hd = (ReduceArgs *)(hg + n);
+    DirectArgs *hx = (DirectArgs *)(hd + n);
     for (int i = 0; i < n; i++) {
         hp[i] = launches[i].prep;
         hr[i] = launches[i].ra;
         hg[i] = launches[i].ga;
         hd[i] = launches[i].red;
+        hx[i] = launches[i].da;
     }
     BatchEntry *hbe = (BatchEntry *)(img + P.off_batch);
     std::vector<Batch> batches;
@@ -1028,9 +1069,12 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         const auto &mem = groups[sl];
         cur_lane = group_lane[sl];
         cur_group = (int)sl;
-        add_batch(Batch::kPrep, 0, mem, [](const Launch<KeyT> &L) { return L.prep.nwg; });
+        std::vector<int> prepped, direct;
+        for (int i : mem) (launches[i].direct ? direct : prepped).push_back(i);
+        add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
+        add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
         std::vector<std::pair<uint32_t, int>> rows, gens, reds;
-        for (int i : mem) {
+        for (int i : prepped) {
             const Launch<KeyT> &L = launches[i];
             if (L.rows) {
                 uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
@@ -1107,12 +1151,14 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     const RowsArgs *dr = (const RowsArgs *)(dp + n);
     const GenericArgs *dg = (const GenericArgs *)(dr + n);
     const ReduceArgs *dd = (const ReduceArgs *)(dg + n);
+    const DirectArgs *dx = (const DirectArgs *)(dd + n);
     const BatchEntry *dbe = (const BatchEntry *)(ws + P.off_batch);
     uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
     SearchOut *dout = (SearchOut *)(ws + P.off_out);
 
     uint32_t nfill = use_flow ? 1 : 0;
-    for (const Batch &b : batches) nfill += b.kind == Batch::kRows || b.kind == Batch::kGeneric;
+    for (const Batch &b : batches)
+        nfill += b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
     if (g->profile && d->ev.size() < 2 * (size_t)nfill) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
             hipEvent_t e;
@@ -1225,14 +1271,19 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             break;
         case Batch::kRows:
         case Batch::kGeneric:
+        case Batch::kDirect:
         {
             // with profiling, the launch itself records its start and end
             // (events attached to the dispatch, no extra packets in the stream)
             hipEvent_t e0 = g->profile ? d->ev[2 * fb] : nullptr, e1 = g->profile ? d->ev[2 * fb + 1] : nullptr;
             if (b.kind == Batch::kRows) {
                 if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
-            } else {
+            } else if (b.kind == Batch::kGeneric) {
                 launch_generic<KeyT>(dg, e, b, bs, e0, e1);
+            } else {
+                hipExtLaunchKernelGGL((k_fill_direct<KeyT>), dim3(b.blocks), dim3(256), 0, bs, e0, e1, 0, dx, e,
+                                      b.nentries, dV, dE, (const uint64_t *)dL, (const uint8_t *)dls,
+                                      (const uint64_t *)dsig, dC, g->r);
             }
         }
             for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
@@ -1291,7 +1342,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         std::vector<float> ms(fb, 0.f);
         uint32_t k = 0;
         for (const Batch &b : batches) {
-            if (b.kind != Batch::kRows && b.kind != Batch::kGeneric) continue;
+            if (b.kind != Batch::kRows && b.kind != Batch::kGeneric && b.kind != Batch::kDirect) continue;
             HIPCHK(hipEventElapsedTime(&ms[k], d->ev[2 * k], d->ev[2 * k + 1]));
             g->stats.fill_ms += ms[k];
             if (b.kind == Batch::kRows) {

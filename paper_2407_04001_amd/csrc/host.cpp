@@ -489,8 +489,39 @@ static pase_status build_plan(pase_graph_t g) {
     }
 
     // ---- kernel choice and T_i layout
+    // threads of the generic and direct fills walk the table in layout order:
+    // follow the memory order of the largest lookup that spans several digits
+    // so that its reads coalesce
+    auto gather_layout = [&](const VPlan &vp) {
+        int big = -1;
+        for (size_t t = 0; t < vp.terms.size(); t++)
+            if (vp.terms[t].dig.size() >= 2 && (big < 0 || P.v[vp.terms[t].j].N > P.v[vp.terms[big].j].N))
+                big = (int)t;
+        if (big < 0) return vp.D;
+        const VPlan &pj = P.v[vp.terms[big].j];
+        std::vector<int> order;
+        for (int u : pj.layout)
+            if (u != vp.vi) order.push_back(u);   // slowest first in T_j
+        for (int u : vp.D)
+            if (std::find(order.begin(), order.end(), u) == order.end()) order.insert(order.begin(), u);
+        return order;
+    };
     for (int i = 0; i < n; i++) {
         VPlan &vp = P.v[i];
+        // small vertices: the direct fill (one launch, no prep blocks), whose
+        // time is a launch plus the gather of every term of every cell
+        if (g->direct_cells && g->kernel_mode == 0 && g->schedule != kSchedFlow &&
+            vp.N * vp.K <= g->direct_cells) {
+            vp.kernel = kDirect;
+            vp.est_us = 4.0 + (double)vp.N * vp.K * (1.0 + vp.edges.size() + vp.terms.size()) / 4e5;
+            vp.layout = gather_layout(vp);
+            vp.nsplit = 1;
+            vp.cper = vp.K;
+            vp.stride.assign(vp.layout.size(), 1);
+            for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
+                vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
+            continue;
+        }
         RowsChoice best;
         // candidates: every digit of D(i) as the column digit z, and -- only
         // when none of those fits -- no column at all (z = -1: every digit is
@@ -595,22 +626,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.kernel = kGeneric;
             // gather-bound: ~1e11 cell updates/s, plus a launch's worth of latency
             vp.est_us = 5.0 + (double)vp.N * vp.K / 1e5;
-            vp.layout = vp.D;
-            // threads walk the table in layout order: follow the memory order of the
-            // largest lookup that spans several digits so that its reads coalesce
-            int big = -1;
-            for (size_t t = 0; t < vp.terms.size(); t++)
-                if (vp.terms[t].dig.size() >= 2 && (big < 0 || P.v[vp.terms[t].j].N > P.v[vp.terms[big].j].N))
-                    big = (int)t;
-            if (big >= 0) {
-                const VPlan &pj = P.v[vp.terms[big].j];
-                std::vector<int> order;
-                for (int u : pj.layout)
-                    if (u != vp.vi) order.push_back(u);   // slowest first in T_j
-                for (int u : vp.D)
-                    if (std::find(order.begin(), order.end(), u) == order.end()) order.insert(order.begin(), u);
-                vp.layout = order;
-            }
+            vp.layout = gather_layout(vp);
             vp.nsplit = 1;
             vp.cper = vp.K;
         }
@@ -686,7 +702,8 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     P.off_bt = off;
     off = align_up(off + n * sizeof(BacktrackDesc), A);
     P.off_desc = off;
-    off = align_up(off + n * (sizeof(PrepArgs) + sizeof(RowsArgs) + sizeof(GenericArgs) + sizeof(ReduceArgs)), A);
+    off = align_up(off + n * (sizeof(PrepArgs) + sizeof(RowsArgs) + sizeof(GenericArgs) + sizeof(ReduceArgs) +
+                              sizeof(DirectArgs)), A);
     P.off_batch = off;
     off = align_up(off + 3 * (uint64_t)n * sizeof(BatchEntry), A);
     // dataflow tables: control block, done counters, segments (prep, fill,
@@ -753,10 +770,10 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
             e += align_up(vp.MO * vp.K * vp.ldz, 32);
             for (int u : vp.R) e += align_up((uint64_t)vp.K * g->K[u], 32);
             if (vp.nsplit > 1) pb = align_up((uint64_t)vp.nsplit * vp.N * 8, A);
-        } else {
+        } else if (vp.kernel == kGeneric) {
             e += align_up(vp.K, 32);
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
-        }
+        }   // the direct fill needs no prep blocks and no split scratch
         vp.block_elems = e;
         // (the dataflow schedule keeps every vertex's scratch: one slot for all)
         const int sl = flow ? 0 : vp.slot;
@@ -987,6 +1004,9 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "order 0 or 1");
         g->order_mode = (int)value;
         break;
+    case PASE_OPT_DIRECT_CELLS:
+        g->direct_cells = value;
+        break;
     case PASE_OPT_GRAD_SYNC:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "grad sync 0 or 1");
         g->grad_opt = (uint32_t)value;
@@ -1008,7 +1028,8 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     // options that change the plan need a fresh enumeration
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
-         opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER) &&
+         opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER ||
+         opt == PASE_OPT_DIRECT_CELLS) &&
         g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);
@@ -1131,7 +1152,7 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     pase_vertex_info x;
     std::memset(&x, 0, sizeof x);
     x.position = (uint32_t)g->plan.pos[v];
-    x.kernel = vp.kernel == kRows ? 1 : 0;
+    x.kernel = (uint32_t)vp.kernel;
     x.num_configs = vp.K;
     x.dep_count = (uint32_t)vp.D.size();
     x.entries = vp.N;

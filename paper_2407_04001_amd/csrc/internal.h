@@ -147,6 +147,22 @@ struct GenericArgs {
     uint32_t out_shift, nblk;  // nblk: workgroups of this vertex
 };
 
+// Direct fill of a small vertex: every term of recurrence (4) -- layer cost,
+// transfer costs, table lookups -- is summed per (entry, c) from its source
+// arrays (contributions [c_begin, c_end) over the plan digits), with no prep
+// blocks; one launch per level instead of prep + fill (+ split reduction).
+struct DirectArgs {
+    uint32_t vi, K, bits, out_shift;
+    uint32_t m;               // plan digits (= T_i layout), slowest first
+    uint32_t group_log2;      // lanes per entry = 2^group_log2 (c is strided over them)
+    uint32_t c_begin, c_end;  // contributions
+    uint32_t rad[kMaxDep];
+    uint32_t nblk, pad;       // nblk: workgroups of this vertex
+    uint64_t N;
+    void *T;
+    uint16_t *A;
+};
+
 struct ReduceArgs {
     const void *partial;
     void *T;
@@ -227,7 +243,7 @@ struct TermRef {
     std::vector<int> dig;     // D(j) - {v_i}: vertex ids
 };
 
-enum KernelKind { kGeneric = 0, kRows = 1 };
+enum KernelKind { kGeneric = 0, kRows = 1, kDirect = 2 };
 
 struct VPlan {
     int vi = -1;
@@ -304,6 +320,7 @@ struct pase_graph_s {
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
     uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
     uint32_t grad_opt = 0;          // pase_option PASE_OPT_GRAD_SYNC, read by pase_enumerate_configs
+    uint64_t direct_cells = 1ull << 25;  // pase_option PASE_OPT_DIRECT_CELLS
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix

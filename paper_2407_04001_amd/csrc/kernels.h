@@ -219,6 +219,41 @@ __device__ __forceinline__ void set_priority(const BatchEntry &e) {
     if (e.prio) __builtin_amdgcn_s_setprio(3);
 }
 
+// The key of configuration c of vertex `me` under plan digits dv, summed over
+// contributions [c0, c1): plain costs (layer, transfer) are summed in `sum`
+// and shifted into key space at the end; DP tables are stored in this
+// vertex's key space already; the layer term carries c into the low bits.
+template <typename KeyT>
+__device__ __forceinline__ uint64_t contrib_key(const Contrib *__restrict__ cb, uint32_t c0, uint32_t c1,
+                                                const DevVertex &me, uint32_t c, const uint32_t (&dv)[kMaxDep],
+                                                uint32_t bits, const DevVertex *__restrict__ V,
+                                                const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
+                                                const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
+                                                uint64_t r) {
+    using Val = typename KeyOps<KeyT>::Val;
+    uint64_t sum = 0, keysum = 0, low = 0;
+    for (uint32_t k = c0; k < c1; k++) {
+        const Contrib ct = cb[k];
+        if (ct.kind == kContribLayer) {
+            sum += L[me.L_off + c];
+            low = c;
+        } else if (ct.kind == kContribEdge) {
+            const DevEdge de = E[ct.edge];
+            const uint32_t xo = dv[ct.dig];
+            const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
+            const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
+            const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
+            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r, de.factors);
+        } else {
+            uint64_t idx = (uint64_t)c * ct.sc;
+            for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
+            if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
+            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
+        }
+    }
+    return (sum << bits) + keysum + low;
+}
+
 // One workgroup handles kPrepThreads consecutive (c, column) elements of one
 // outer index of one block, so the block, its contributions and the outer
 // digits are uniform across the workgroup (scalar loads); lanes differ only in
@@ -228,7 +263,6 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
                                           const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
                                           const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
                                           const Contrib *__restrict__ cb, uint64_t r) {
-    using Val = typename KeyOps<KeyT>::Val;
     KeyT *__restrict__ blocks = (KeyT *)a.blocks;
     uint32_t b = 0;
     while (b + 1 < a.nblocks && wg >= a.blk[b + 1].wg_begin) b++;
@@ -251,29 +285,8 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
     }
     if (bk.post >= 0) dv[bk.post] = q;
     const DevVertex me = V[a.vi];
-    // plain costs (layer, transfer) are summed in `sum` and shifted into key
-    // space at the end; DP tables are stored in this vertex's key space already
-    uint64_t sum = 0, keysum = 0, low = 0;
-    for (uint32_t k = bk.c_begin; k < bk.c_end; k++) {
-        const Contrib ct = cb[k];
-        if (ct.kind == kContribLayer) {
-            sum += L[me.L_off + c];
-            low = c;
-        } else if (ct.kind == kContribEdge) {
-            const DevEdge de = E[ct.edge];
-            const uint32_t xo = dv[ct.dig];
-            const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
-            const uint64_t sme = sig[de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K) + c];
-            const uint64_t sot = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
-            sum += edge_cost_sig(sme, sot, lsum[me.L_off + c], lsum[ov.L_off + xo], de.elems, r, de.factors);
-        } else {
-            uint64_t idx = (uint64_t)c * ct.sc;
-            for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
-            if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
-            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
-        }
-    }
-    *out = KeyOps<KeyT>::from_u64((sum << a.bits) + keysum + low);
+    *out = KeyOps<KeyT>::from_u64(contrib_key<KeyT>(cb, bk.c_begin, bk.c_end, me, c, dv, a.bits, V, E, L, lsum,
+                                                     sig, r));
 }
 
 // Waits for every outstanding scalar-memory and LDS read (s_waitcnt
@@ -590,6 +603,43 @@ __device__ __forceinline__ void generic_item(const GenericArgs &a, uint32_t lb) 
             best0 = Ops::min(best0, k0);
         }
         KeyT best = Ops::min(best0, best1);
+        for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
+        if (live && lane == 0) {
+            Val v;
+            uint32_t cc;
+            Ops::split(best, a.bits, a.out_shift, v, cc);
+            ((Val *)a.T)[phi] = v;
+            a.A[phi] = (uint16_t)cc;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ direct fill (small vertices)
+// Like the generic fill, 2^group_log2 lanes share one table entry and stride
+// over c; each (entry, c) key is summed from the contributions directly.
+template <typename KeyT>
+__device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, const DevVertex *__restrict__ V,
+                                            const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
+                                            const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
+                                            const Contrib *__restrict__ cb, uint64_t r) {
+    using Ops = KeyOps<KeyT>;
+    using Val = typename Ops::Val;
+    const uint32_t G = 1u << a.group_log2;
+    const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
+    const DevVertex me = V[a.vi];
+    for (uint64_t tid = lb * (uint64_t)blockDim.x + threadIdx.x; tid < ((nthreads + 255) / 256) * 256;
+         tid += (uint64_t)a.nblk * blockDim.x) {
+        const bool live = tid < nthreads;
+        const uint64_t phi = live ? tid >> a.group_log2 : a.N - 1;
+        const uint32_t lane = (uint32_t)(tid & (G - 1));
+        uint32_t dv[kMaxDep];
+        uint64_t x = phi;
+        for (int k = kMaxDep - 1; k >= 0; k--)
+            if (k < (int)a.m) { dv[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else dv[k] = 0;
+        KeyT best = Ops::sentinel();
+        for (uint32_t c = lane; c < a.K; c += G)
+            best = Ops::min(best, Ops::from_u64(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V, E,
+                                                                  L, lsum, sig, r)));
         for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
         if (live && lane == 0) {
             Val v;

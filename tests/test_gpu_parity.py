@@ -69,8 +69,13 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False, grad=False):
+         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False, grad=False,
+         direct=0):
+    """direct: PASE_OPT_DIRECT_CELLS (0 = off, so the tests aimed at the row and
+    generic kernels keep them; None = the library's default)."""
     pg = P.Graph(g, seq_rule=rule)
+    if direct is not None:
+        pg.set_option(P.OPT_DIRECT_CELLS, direct)
     pg.set_option(P.OPT_ORDER, int(bf))
     pg.set_option(P.OPT_TRANSFER, int(volume))
     pg.set_option(P.OPT_GRAD_SYNC, int(grad))
@@ -275,13 +280,15 @@ def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False):
+                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None):
     gold = _golden(name, seed, p, all_integers, bf, volume, grad)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad}")
+        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad} "
+        f"direct={direct}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume, grad=grad)
+                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume, grad=grad,
+                         direct=direct)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -313,7 +320,9 @@ def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, sched
                                        ("w2_inception", 0), ("w2_inception", 1),
                                        ("w2_inception", 2), ("w3_lstm_grid", 0)])
 def test_workloads_against_golden(P, name, seed):
+    """Default plan (small vertices on the direct fill), then without it."""
     _check_golden(P, name, seed)
+    _check_golden(P, name, seed, direct=0)
 
 
 @pytest.mark.parametrize("name", ["w2_inception", "w3_lstm_grid"])
@@ -390,9 +399,10 @@ def test_graph_replays_match_direct_launches(P, name):
 def test_transformer_p64_against_golden(P):
     """The measured workload at full size, in the configuration the benchmark
     times (default kernels and memory plan), then with every table kept and
-    fingerprinted."""
+    fingerprinted, and without the direct fill."""
     _check_golden(P, "w4_transformer", 0, keep=False)
     _check_golden(P, "w4_transformer", 0, keep=True)
+    _check_golden(P, "w4_transformer", 0, keep=True, samples=False, direct=0)
 
 
 def test_cost_tables_against_oracle(P):
@@ -641,3 +651,57 @@ def test_grad_sync_workloads_against_golden(P, name):
 def test_grad_sync_transformer_against_golden(P):
     _check_golden(P, "w4_transformer", 0, grad=True, keep=False)
     _check_golden(P, "w4_transformer", 0, grad=True, keep=True)
+
+
+# ------------------------------------------------------------------ direct fill
+ALL_DIRECT = 1 << 62
+
+
+@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("key", [0, 1])
+def test_direct_fill_random_graphs(P, seed, key):
+    """Every vertex on the direct fill (each term summed per cell from its
+    source arrays): every table entry equals the oracle's, with model costs,
+    dense ties (odd seeds), volume transfer costs and the gradient term."""
+    g = random_graph(seed + 660, n=4 + seed % 6, p=8, max_dims=3, extra_edges=1 + seed % 4)
+    volume, grad = seed % 3 == 2, seed % 4 == 3
+    costs = None
+    if seed % 2:
+        o0 = _oracle(g)
+        K = [int(k) for k in o0.K]
+        costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    say(f"direct fill random graph seed={seed + 660} key={key} ties={costs is not None} volume={volume} grad={grad}")
+    o = _oracle(g, costs=costs, volume=volume, grad=grad)
+    pg, mc, strat = _run(P, g, key=key, costs=costs, volume=volume, grad=grad, direct=ALL_DIRECT)
+    assert all(pg.vertex_info(v)["kernel"] == 2 for v in range(len(g["vertices"])))
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=1024)
+
+
+def test_direct_fill_schedules_and_orders(P):
+    """The direct fill under the sequential and lane schedules, the
+    breadth-first order and every-integer configurations; the dataflow
+    schedule does not use it."""
+    g = random_graph(680, n=9, p=16, max_dims=3, extra_edges=4, max_size=256)
+    o = _oracle(g)
+    for sched in (0, 1, 2):
+        say(f"direct fill seed=680 schedule={sched}")
+        pg, mc, strat = _run(P, g, schedule=sched, direct=ALL_DIRECT)
+        assert (mc, strat) == o.result()
+        _compare_all_entries(pg, o, g, max_entries=256)
+    pg, mc, strat = _run(P, g, schedule=3, direct=ALL_DIRECT)
+    assert (mc, strat) == o.result()
+    assert all(pg.vertex_info(v)["kernel"] != 2 for v in range(len(g["vertices"])))
+    ob = _oracle(g, bf=True)
+    pg, mc, strat = _run(P, g, bf=True, direct=ALL_DIRECT)
+    assert (mc, strat) == ob.result()
+    _compare_all_entries(pg, ob, g, max_entries=256)
+    oa = _oracle(g, p=12, all_integers=True)
+    pg, mc, strat = _run(P, g, p=12, all_integers=True, direct=ALL_DIRECT)
+    assert (mc, strat) == oa.result()
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
+def test_direct_fill_whole_workloads(P, name):
+    """Every vertex of a workload on the direct fill, against the golden."""
+    _check_golden(P, name, 0, direct=ALL_DIRECT)
