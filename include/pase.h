@@ -167,8 +167,10 @@ typedef enum {
                                    use the direct fill: every term of recurrence (4) summed per
                                    cell from its source arrays in one launch, no prep blocks --
                                    for the long chains of small dependent vertices, where launch
-                                   count dominates.  Default 2^25; 0 = never.  Not used by the
-                                   dataflow schedule or with PASE_OPT_KERNEL = 1 */
+                                   count dominates.  A level uses it only when all its vertices
+                                   qualify (so that it saves launches; any vertex under the
+                                   sequential schedule).  Default 2^20; 0 = never.  Not used by
+                                   the dataflow schedule or with PASE_OPT_KERNEL = 1 */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

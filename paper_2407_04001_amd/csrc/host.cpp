@@ -506,12 +506,19 @@ static pase_status build_plan(pase_graph_t g) {
             if (std::find(order.begin(), order.end(), u) == order.end()) order.insert(order.begin(), u);
         return order;
     };
+    // the direct fill pays where it removes launches: for a whole level (the
+    // vertices of one launch group), or any vertex when each has its own slot
+    int maxlev = 0;
+    for (int i = 0; i < n; i++) maxlev = std::max(maxlev, P.v[i].level);
+    std::vector<char> level_small((size_t)maxlev + 1, 1);
+    for (int i = 0; i < n; i++)
+        if (P.v[i].N * P.v[i].K > g->direct_cells) level_small[P.v[i].level] = 0;
     for (int i = 0; i < n; i++) {
         VPlan &vp = P.v[i];
         // small vertices: the direct fill (one launch, no prep blocks), whose
         // time is a launch plus the gather of every term of every cell
         if (g->direct_cells && g->kernel_mode == 0 && g->schedule != kSchedFlow &&
-            vp.N * vp.K <= g->direct_cells) {
+            vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
             vp.kernel = kDirect;
             vp.est_us = 4.0 + (double)vp.N * vp.K * (1.0 + vp.edges.size() + vp.terms.size()) / 4e5;
             vp.layout = gather_layout(vp);

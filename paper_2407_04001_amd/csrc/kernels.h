@@ -616,7 +616,14 @@ __device__ __forceinline__ void generic_item(const GenericArgs &a, uint32_t lb) 
 
 // ------------------------------------------------------------------ direct fill (small vertices)
 // Like the generic fill, 2^group_log2 lanes share one table entry and stride
-// over c; each (entry, c) key is summed from the contributions directly.
+// over c.  Each lane first resolves every contribution for its entry once --
+// an array read at base + c * stride (layer costs, caller or volume edge
+// matrices, producer tables) or a split-signature edge term with the other
+// endpoint's signature and device byte fixed -- so the loop over c only loads
+// data.  Vertices with more contributions than fit the register set take the
+// per-cell path of the prep kernel.
+constexpr int kDirectTerms = 8;
+
 template <typename KeyT>
 __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, const DevVertex *__restrict__ V,
                                             const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
@@ -627,6 +634,8 @@ __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, co
     const uint32_t G = 1u << a.group_log2;
     const uint64_t nthreads = (uint64_t)a.N << a.group_log2;
     const DevVertex me = V[a.vi];
+    const uint32_t nt = a.c_end - a.c_begin;
+    const bool fast = nt <= (uint32_t)kDirectTerms;
     for (uint64_t tid = lb * (uint64_t)blockDim.x + threadIdx.x; tid < ((nthreads + 255) / 256) * 256;
          tid += (uint64_t)a.nblk * blockDim.x) {
         const bool live = tid < nthreads;
@@ -637,9 +646,67 @@ __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, co
         for (int k = kMaxDep - 1; k >= 0; k--)
             if (k < (int)a.m) { dv[k] = (uint32_t)(x % a.rad[k]); x /= a.rad[k]; } else dv[k] = 0;
         KeyT best = Ops::sentinel();
-        for (uint32_t c = lane; c < a.K; c += G)
-            best = Ops::min(best, Ops::from_u64(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V, E,
-                                                                  L, lsum, sig, r)));
+        if (fast) {
+            // kind: 0 plain u64 array, 1 key-space table, 2 signature edge
+            const char *base[kDirectTerms];
+            uint32_t stride[kDirectTerms], kind[kDirectTerms], lot[kDirectTerms], fac[kDirectTerms];
+            const uint8_t *lme[kDirectTerms];
+            uint64_t sot[kDirectTerms], elems[kDirectTerms];
+#pragma unroll
+            for (int t = 0; t < kDirectTerms; t++) {
+                base[t] = nullptr;
+                lme[t] = nullptr;
+                stride[t] = kind[t] = lot[t] = fac[t] = 0;
+                sot[t] = elems[t] = 0;
+                if (t < (int)nt) {
+                    const Contrib ct = cb[a.c_begin + t];
+                    if (ct.kind == kContribLayer) {
+                        base[t] = (const char *)(L + me.L_off);
+                        stride[t] = 8;
+                    } else if (ct.kind == kContribEdge) {
+                        const DevEdge de = E[ct.edge];
+                        const uint32_t xo = dv[ct.dig];
+                        const DevVertex ov = V[ct.vi_is_src ? de.dst : de.src];
+                        kind[t] = 2;
+                        base[t] = (const char *)(sig + de.sig_off + (ct.vi_is_src ? 0 : V[de.src].K));
+                        stride[t] = 8;
+                        sot[t] = sig[de.sig_off + (ct.vi_is_src ? me.K : 0) + xo];
+                        lme[t] = lsum + me.L_off;
+                        lot[t] = lsum[ov.L_off + xo];
+                        elems[t] = de.elems;
+                        fac[t] = de.factors;
+                    } else {
+                        uint64_t idx = 0;
+                        for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
+                        kind[t] = ct.raw_u64 ? 0 : 1;
+                        stride[t] = ct.sc * 8;
+                        base[t] = (const char *)ct.ptr + idx * 8;
+                    }
+                }
+            }
+            for (uint32_t c = lane; c < a.K; c += G) {
+                uint64_t sum = 0, keysum = 0;
+#pragma unroll
+                for (int t = 0; t < kDirectTerms; t++) {
+                    if (t < (int)nt) {
+                        if (kind[t] == 2) {
+                            const uint64_t sme = *(const uint64_t *)(base[t] + (uint64_t)c * stride[t]);
+                            sum += edge_cost_sig(sme, sot[t], lme[t][c], lot[t], elems[t], r, fac[t]);
+                        } else {
+                            const uint64_t v = *(const uint64_t *)(base[t] + (uint64_t)c * stride[t]);
+                            if (kind[t] == 0) sum += v;
+                            else keysum += Ops::val_to_u64(__builtin_bit_cast(Val, v));
+                        }
+                    }
+                }
+                // the layer term is always present: c fills the low bits
+                best = Ops::min(best, Ops::from_u64((sum << a.bits) + keysum + c));
+            }
+        } else {
+            for (uint32_t c = lane; c < a.K; c += G)
+                best = Ops::min(best, Ops::from_u64(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V,
+                                                                      E, L, lsum, sig, r)));
+        }
         for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
         if (live && lane == 0) {
             Val v;
