@@ -169,7 +169,7 @@ typedef enum {
                                    for the long chains of small dependent vertices, where launch
                                    count dominates.  A level uses it only when all its vertices
                                    qualify (so that it saves launches; any vertex under the
-                                   sequential schedule).  Default 2^20; 0 = never.  Not used by
+                                   sequential schedule).  Default 2^18; 0 = never.  Not used by
                                    the dataflow schedule or with PASE_OPT_KERNEL = 1 */
 } pase_option;
 

@@ -320,7 +320,7 @@ struct pase_graph_s {
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
     uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
     uint32_t grad_opt = 0;          // pase_option PASE_OPT_GRAD_SYNC, read by pase_enumerate_configs
-    uint64_t direct_cells = 1ull << 20;  // pase_option PASE_OPT_DIRECT_CELLS
+    uint64_t direct_cells = 1ull << 18;  // pase_option PASE_OPT_DIRECT_CELLS
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix
