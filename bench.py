@@ -163,7 +163,10 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         return {"metric": metric, "value": None, "unit": "cell-updates/s", "n_gpus": 1, "steps": 0,
                 "warmup": 0, "higher_is_better": True, "data": "synthetic", "config": config,
                 "refused": str(e)}
-    pg.set_option(OPT_PROFILE, 1)
+    # HIP events on the dominant kernel's launches only (the row kernel with a
+    # column chunk per lane), so the timed steps carry as few events as the
+    # roofline needs
+    pg.set_option(OPT_PROFILE, 2)
     stream = torch.cuda.current_stream()
 
     def step():
@@ -173,7 +176,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    walls, rows_ms, rows_launches, fill_ms, step_ms = [], 0.0, 0, 0.0, []
+    walls, rows_ms, rows_launches, step_ms = [], 0.0, 0, []
     t0 = time.perf_counter()
     for _ in range(steps):
         ts = time.perf_counter()
@@ -181,11 +184,10 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         step_ms.append((time.perf_counter() - ts) * 1e3)
         st = pg.stats()
         walls.append(st["wall_ms"])
-        # the dominant kernel: the row kernel with a column chunk per lane (its
-        # column-less, memory-streaming form is reported apart)
-        rows_ms += st["rows_fill_ms"] - st["stream_fill_ms"]
-        fill_ms += st["fill_ms"]
-        rows_launches += st["rows_launches"] - st["stream_launches"]
+        # the dominant kernel: the row kernel with a column chunk per lane (the
+        # only launches timed; its column-less form is not)
+        rows_ms += st["rows_fill_ms"]
+        rows_launches += st["rows_launches"]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
@@ -223,13 +225,10 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         "config": dict(config, cells=cells),
         "find_best_strategy_ms": sum(walls) / len(walls),
         "median_ms_per_step": sorted(step_ms)[len(step_ms) // 2],
-        "fill_ms_per_step": fill_ms / steps,
         # the whole search against the ALU roofline: every cell costs `ops` VALU
         # lane-ops (t_roof), against the fill-kernel time and the step
         "search_roofline": {"t_roof_ms": t_roof_ms, "ops_per_cell": ops,
-                            "frac_of_fill": t_roof_ms / (fill_ms / steps) if fill_ms else None,
                             "frac_of_step": t_roof_ms / (elapsed * 1e3 / steps)},
-        "fill_cells_per_s": cells / (fill_ms / steps / 1e3) if fill_ms else None,
         "min_cost": mc, "parity_with_oracle": parity,
         "roofline": {"bound": "alu", "kernel": "k_fill_rows",
                      "achieved": achieved, "peak": FP64_OPS_PEAK_T,

@@ -102,7 +102,9 @@ typedef enum {
     PASE_OPT_MEMORY_BUDGET = 2, /* bytes of device memory a search may use (default 64 GiB) */
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
     PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
-    PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats) */
+    PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats);
+                                   2: only the row kernel's launches with a column chunk per lane
+                                   (the dominant kernel; fewer events, so less overhead) */
     PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
                                    do not read each other) share their kernel launches, one
                                    stream, table memory packed by lifetimes.  1: one vertex at a
@@ -185,7 +187,8 @@ typedef struct {
     uint64_t rows_cells;       /* cells filled by that kernel */
     double host_plan_ms;       /* pase_enumerate_configs: ordering + plans (host) */
     double wall_ms;            /* pase_find_best_strategy, host wall clock */
-    double fill_ms;            /* PASE_OPT_PROFILE: sum of fill-kernel event times */
+    double fill_ms;            /* PASE_OPT_PROFILE: sum of the timed fill launches' event times
+                                  (profile 2: the column-form row-kernel launches only) */
     double rows_fill_ms;       /* PASE_OPT_PROFILE: same, row/column-chunk kernel only */
     uint32_t rows_launches;    /* PASE_OPT_PROFILE: launches of that kernel */
     uint32_t slots;            /* launch slots: dependency levels, or vertices when sequential */

@@ -957,13 +957,18 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     // ---- constant region image (one host-to-device copy)
     char *img = (char *)d->pinned;
     std::memset(img, 0, P.off_cfg);
-    uint64_t off = 0;
+    // one row set per dimension count, shared by the vertices with that count
+    uint64_t row_off[kMaxDims + 1] = {0}, off = 0;
+    for (size_t d = 0; d < g->ex_rows.size() && d <= (size_t)kMaxDims; d++) {
+        row_off[d] = off;
+        if (!g->ex_rows[d].empty()) std::memcpy(img + P.off_ex + off, g->ex_rows[d].data(), g->ex_rows[d].size());
+        off += g->ex_rows[d].size();
+    }
     std::vector<DevVertex> dvs(nv);
     uint64_t loff = 0;
     for (size_t v = 0; v < nv; v++) {
-        std::memcpy(img + P.off_ex + off, g->ex[v].data(), g->ex[v].size());
         DevVertex &x = dvs[v];
-        x.ex_off = off;
+        x.ex_off = row_off[g->V[v].ndims];
         x.L_off = loff;
         x.flops = g->flops[v];
         x.keep_n = g->keep_n[v];
@@ -973,7 +978,6 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         x.factors = g->factors ? 1 : 0;
         x.weight_n = g->weight_n[v];
         x.weight_mask = g->V[v].weight_mask;
-        off += g->ex[v].size();
         loff += g->K[v];
     }
     std::memcpy(img + P.off_vert, dvs.data(), nv * sizeof(DevVertex));
@@ -1156,9 +1160,14 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     uint32_t *dcfg = (uint32_t *)(ws + P.off_cfg);
     SearchOut *dout = (SearchOut *)(ws + P.off_out);
 
+    // fill launches timed with events: every one (profile 1), or only those of
+    // the row kernel with a column chunk per lane (profile 2)
+    auto timed = [&](const Batch &b) {
+        if (g->profile == 1) return b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
+        return g->profile == 2 && b.kind == Batch::kRows && b.variant / 32 != 1;
+    };
     uint32_t nfill = use_flow ? 1 : 0;
-    for (const Batch &b : batches)
-        nfill += b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
+    for (const Batch &b : batches) nfill += timed(b);
     if (g->profile && d->ev.size() < 2 * (size_t)nfill) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
             hipEvent_t e;
@@ -1275,7 +1284,10 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         {
             // with profiling, the launch itself records its start and end
             // (events attached to the dispatch, no extra packets in the stream)
-            hipEvent_t e0 = g->profile ? d->ev[2 * fb] : nullptr, e1 = g->profile ? d->ev[2 * fb + 1] : nullptr;
+            const bool tb = timed(b);
+            if (tb)
+                for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
+            hipEvent_t e0 = tb ? d->ev[2 * fb] : nullptr, e1 = tb ? d->ev[2 * fb + 1] : nullptr;
             if (b.kind == Batch::kRows) {
                 if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
             } else if (b.kind == Batch::kGeneric) {
@@ -1285,9 +1297,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
                                       b.nentries, dV, dE, (const uint64_t *)dL, (const uint8_t *)dls,
                                       (const uint64_t *)dsig, dC, g->r);
             }
+            if (tb) fb++;
         }
-            for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
-            fb++;
             break;
         case Batch::kReduce:
             hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, bs, dd, e, b.nentries);
@@ -1342,7 +1353,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         std::vector<float> ms(fb, 0.f);
         uint32_t k = 0;
         for (const Batch &b : batches) {
-            if (b.kind != Batch::kRows && b.kind != Batch::kGeneric && b.kind != Batch::kDirect) continue;
+            if (!timed(b)) continue;
             HIPCHK(hipEventElapsedTime(&ms[k], d->ev[2 * k], d->ev[2 * k + 1]));
             g->stats.fill_ms += ms[k];
             if (b.kind == Batch::kRows) {

@@ -682,7 +682,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     const uint64_t A = 256;
     uint64_t off = 0;
     P.off_ex = off;
-    for (size_t v = 0; v < g->V.size(); v++) off += (uint64_t)g->K[v] * g->V[v].ndims;
+    for (const auto &rows : g->ex_rows) off += rows.size();   // one row set per dimension count
     off = align_up(off, A);
     P.off_vert = off;
     off = align_up(off + g->V.size() * sizeof(DevVertex), A);
@@ -743,22 +743,24 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     std::vector<int> order(n);
     std::iota(order.begin(), order.end(), 0);
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return iv[a].size > iv[b].size; });
+    // placed tables in ascending offset order: the first gap that fits among
+    // those whose lifetimes overlap is found in one pass
     std::vector<int> placed;
+    placed.reserve(n);
     uint64_t tbytes = 0;
     for (int k : order) {
-        std::vector<std::pair<uint64_t, uint64_t>> busy;
-        for (int q : placed)
-            if (iv[q].s <= iv[k].e && iv[k].s <= iv[q].e)
-                busy.push_back({P.v[iv[q].i].T_off, P.v[iv[q].i].T_off + iv[q].size});
-        std::sort(busy.begin(), busy.end());
         uint64_t cand = 0;
-        for (const auto &b : busy) {
-            if (cand + iv[k].size <= b.first) break;
-            cand = std::max(cand, b.second);
+        for (int q : placed) {
+            if (!(iv[q].s <= iv[k].e && iv[k].s <= iv[q].e)) continue;
+            const uint64_t b0 = P.v[iv[q].i].T_off;
+            if (cand + iv[k].size <= b0) break;
+            cand = std::max(cand, b0 + iv[q].size);
         }
         P.v[iv[k].i].T_off = cand;
         tbytes = std::max(tbytes, cand + iv[k].size);
-        placed.push_back(k);
+        auto at = std::upper_bound(placed.begin(), placed.end(), cand,
+                                   [&](uint64_t x, int q) { return x < P.v[iv[q].i].T_off; });
+        placed.insert(at, k);
     }
     P.T_bytes = tbytes;
     P.off_T = off;
@@ -846,13 +848,14 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     }
     const size_t nv = g->V.size();
     g->K.assign(nv, 0);
-    g->ex.assign(nv, {});
+    g->ex.assign(nv, nullptr);
     g->weight_n.assign(nv, 0);
     g->flops.assign(nv, 0);
     g->keep_n.assign(nv, 0);
     g->maxL.assign(nv, 0);
     // the configurations of a vertex depend only on its dimension count
-    std::vector<std::vector<uint8_t>> by_dims(kMaxDims + 1);
+    std::vector<std::vector<uint8_t>> &by_dims = g->ex_rows;
+    by_dims.assign(kMaxDims + 1, {});
     for (size_t v = 0; v < nv; v++) {
         const uint32_t d = g->V[v].ndims;
         std::vector<uint8_t> &rows = by_dims[d];
@@ -886,7 +889,7 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
         uint64_t K = rows.size() / d;
         if (K > 65535) return fail(g, PASE_ERR_TOO_LARGE, "more than 65535 configurations");
         g->K[v] = (uint32_t)K;
-        g->ex[v] = rows;
+        g->ex[v] = &rows;
         uint64_t fl = g->V[v].flops_per_point, keep = 1;
         for (uint32_t k = 0; k < d; k++) {
             if (!mul_ok(fl, g->V[v].size[k], &fl))
@@ -946,7 +949,7 @@ extern "C" pase_status pase_config_splits(pase_graph_t g, uint32_t v, uint32_t i
     if (v >= g->V.size() || idx >= g->K[v]) return fail(g, PASE_ERR_INVALID_ARGUMENT, "bad id");
     const uint32_t d = g->V[v].ndims;
     for (uint32_t k = 0; k < d; k++) {
-        const uint32_t x = g->ex[v][(size_t)idx * d + k];
+        const uint32_t x = (*g->ex[v])[(size_t)idx * d + k];
         splits[k] = g->factors ? x : 1u << x;
     }
     return PASE_OK;
@@ -984,7 +987,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "key type 0 or 1");
         g->key_mode = (int)value;
         break;
-    case PASE_OPT_PROFILE: g->profile = value != 0; break;
+    case PASE_OPT_PROFILE:
+        if (value > 2) return fail(g, PASE_ERR_INVALID_ARGUMENT, "profile 0, 1 or 2");
+        g->profile = (int)value;
+        break;
     case PASE_OPT_SCHEDULE:
         if (value > 3) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 2 or 3");
         g->schedule = (int)value;

@@ -308,7 +308,9 @@ struct pase_graph_s {
     std::vector<std::vector<int>> nbr;     // undirected, deduplicated, ascending
     std::string err;
     // options
-    bool keep_tables = false, profile = false;
+    bool keep_tables = false;
+    int profile = 0;                // pase_option PASE_OPT_PROFILE: 0 off, 1 every fill launch, 2 the
+                                    // column-form row-kernel launches only
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
     uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
@@ -328,8 +330,11 @@ struct pase_graph_s {
     uint32_t p = 0;
     bool factors = false;           // the enumerated set: split rows hold factors, not exponents
     std::vector<uint32_t> K;
-    std::vector<std::vector<uint8_t>> ex;  // [v][c*ndims + k]: log2 of the split factor, or the
-                                           // factor itself when `factors`
+    // the configurations of a vertex depend only on its dimension count: one
+    // row set per count, ex_rows[d][c*d + k] = log2 of the split factor, or the
+    // factor itself when `factors`
+    std::vector<std::vector<uint8_t>> ex_rows;
+    std::vector<const std::vector<uint8_t> *> ex;  // [v] -> ex_rows[ndims of v]
     std::vector<uint64_t> flops, keep_n;
     std::vector<uint64_t> maxL;            // upper bound of the layer cost per vertex
     std::vector<uint64_t> maxR;            // upper bound of the transfer cost per edge
