@@ -116,11 +116,12 @@ def traffic_from_profile():
     return prof.get("bytes_per_launch")
 
 
+SCHEDULES = {0: "level", 1: "sequential", 2: "lanes", 3: "dataflow", 4: "bulk lane"}
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
 def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False,
-                 volume=False, grad=False):
+                 volume=False, grad=False, schedule=None):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
@@ -130,7 +131,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     most `cpu_cells` cells, else a prefix of the vertex order).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import OPT_GRAD_SYNC, OPT_ORDER, OPT_PROFILE, OPT_TRANSFER, Graph, PaseError
+    from paper_2407_04001_amd import OPT_GRAD_SYNC, OPT_ORDER, OPT_PROFILE, OPT_SCHEDULE, OPT_TRANSFER, Graph, PaseError
     from workloads import workload
 
     g = workload(name, seed)
@@ -139,6 +140,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
     pg.set_option(OPT_ORDER, int(bf))
     pg.set_option(OPT_TRANSFER, int(volume))
     pg.set_option(OPT_GRAD_SYNC, int(grad))
+    if schedule is not None:
+        pg.set_option(OPT_SCHEDULE, schedule)
     wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
     if all_integers:
         wl += ", every integer split"
@@ -222,7 +225,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         "ms_per_step": elapsed * 1e3 / steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
-        "config": dict(config, cells=cells),
+        "config": dict(config, cells=cells, schedule=SCHEDULES.get(st["schedule"], st["schedule"])),
         "find_best_strategy_ms": sum(walls) / len(walls),
         "median_ms_per_step": sorted(step_ms)[len(step_ms) // 2],
         # the whole search against the ALU roofline: every cell costs `ops` VALU
@@ -266,6 +269,8 @@ def main():
                     help="transfer cost model: split match (default) or volume intersection")
     ap.add_argument("--grad-sync", action="store_true",
                     help="add the weight-gradient all-reduce to the layer costs")
+    ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 2, 3, 4),
+                    help="launch schedule (PASE_OPT_SCHEDULE; default: the library's)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -282,7 +287,7 @@ def main():
     for name in names:
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
-                           args.transfer == "volume", args.grad_sync)
+                           args.transfer == "volume", args.grad_sync, args.schedule)
         print(json.dumps(out), flush=True)
 
 

@@ -117,7 +117,13 @@ typedef enum {
                                    are complete (device-side dependency counters, two ticket
                                    queues).  2 and 3 keep every table resident and fall back to 0
                                    over the memory budget; 3 also when a vertex needs a fill
-                                   variant the persistent kernel does not carry. */
+                                   variant the persistent kernel does not carry.  4: bulk lane --
+                                   every row-kernel vertex whose planned fill takes at least
+                                   PASE_OPT_BULK_US runs on a stream of its own, all other
+                                   vertices level by level on a second stream at the highest wave
+                                   priority, events only where a table is read across the two;
+                                   so a latency-bound chain never waits for a large vertex it
+                                   does not read (every table resident, 0 over the budget). */
     PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
                                    vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
                                    that kernel runs (a tuning and test knob) */
@@ -165,7 +171,7 @@ typedef enum {
                                    differ in the other dims, and a ring all-reduce moves
                                    ceil(2 (R - 1) S / R) words of an S-word shard per device,
                                    weighted by r.  0 (default): the benchmark's cost model */
-    PASE_OPT_DIRECT_CELLS = 16  /* vertices with at most this many cells (K_v x table entries)
+    PASE_OPT_DIRECT_CELLS = 16, /* vertices with at most this many cells (K_v x table entries)
                                    use the direct fill: every term of recurrence (4) summed per
                                    cell from its source arrays in one launch, no prep blocks --
                                    for the long chains of small dependent vertices, where launch
@@ -173,6 +179,8 @@ typedef enum {
                                    qualify (so that it saves launches; any vertex under the
                                    sequential schedule).  Default 2^18; 0 = never.  Not used by
                                    the dataflow schedule or with PASE_OPT_KERNEL = 1 */
+    PASE_OPT_BULK_US = 17       /* schedule 4: planned fill time (microseconds) from which a
+                                   row-kernel vertex runs on the bulk stream (default 100) */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

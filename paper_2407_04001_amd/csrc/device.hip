@@ -948,7 +948,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     // carries for every row fill; otherwise the level schedule runs (the
     // resident layout serves it as well)
     bool use_flow = P.resident && g->schedule == kSchedFlow;
-    const bool use_lanes = P.resident && g->schedule == kSchedLanes;
+    const bool use_lanes = P.resident && (g->schedule == kSchedLanes || g->schedule == kSchedBulk);
     for (int i = 0; i < n && use_flow; i++)
         if (launches[i].rows)
             use_flow = flow_rows_ok(!std::is_same<KeyT, double>::value, P.v[i].TZ, P.v[i].TM,
@@ -1340,7 +1340,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
     if (!use_flow) g->stats.flow_grid = g->stats.flow_lat_workers = 0, g->stats.flow_items = 0;
-    g->stats.schedule = use_flow ? 3u : use_lanes ? 2u : (P.by_level ? 0u : 1u);
+    g->stats.schedule = use_flow ? 3u : use_lanes ? (uint32_t)g->schedule : (P.by_level ? 0u : 1u);
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;
     if (g->profile && use_flow) {

@@ -397,6 +397,22 @@ static void assign_lanes(Plan &P) {
     for (int i = 0; i < n; i++) P.v[i].lane = lane[chain[i]];
 }
 
+// Bulk lane schedule.  Row-kernel vertices planned to take at least bulk_us
+// (the large fills, which keep the whole GPU busy on their own) run on lane 2,
+// and so does every vertex that reads a table of lane 2 (it has to wait for
+// that fill anyway); every other vertex -- one whose producers are all small
+// -- runs on lane 1, level by level, at the highest wave priority.  A level
+// group of lane 1 then never waits for a large fill, so a chain of small
+// dependent vertices runs beside the large fills instead of after them.
+// Producers precede their reader in the sequence, so one pass suffices.
+static void assign_bulk_lanes(Plan &P, double bulk_us) {
+    for (auto &vp : P.v) {
+        bool bulk = vp.kernel == kRows && vp.est_us >= bulk_us;
+        for (const auto &t : vp.terms) bulk |= P.v[t.j].lane == 2;
+        vp.lane = bulk ? 2 : 1;
+    }
+}
+
 static pase_status build_plan(pase_graph_t g) {
     const int n = (int)g->V.size();
     Plan &P = g->plan;
@@ -642,6 +658,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
     }
     assign_lanes(P);
+    if (g->schedule == kSchedBulk) assign_bulk_lanes(P, (double)g->bulk_us);
     return PASE_OK;
 }
 
@@ -659,7 +676,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode);
 // budget, or for the level schedule, tables share memory by lifetimes over
 // levels; when even that does not fit, one vertex at a time.
 static pase_status layout_memory(pase_graph_t g) {
-    if ((g->schedule == kSchedLanes || g->schedule == kSchedFlow) &&
+    if ((g->schedule == kSchedLanes || g->schedule == kSchedFlow || g->schedule == kSchedBulk) &&
         layout_memory_mode(g, kLayoutResident) == PASE_OK)
         return PASE_OK;
     if (g->schedule != kSchedSeq && layout_memory_mode(g, kLayoutLevel) == PASE_OK) return PASE_OK;
@@ -992,7 +1009,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->profile = (int)value;
         break;
     case PASE_OPT_SCHEDULE:
-        if (value > 3) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 2 or 3");
+        if (value > 4) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 2, 3 or 4");
         g->schedule = (int)value;
         break;
     case PASE_OPT_TILE_COLS:
@@ -1020,6 +1037,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     case PASE_OPT_DIRECT_CELLS:
         g->direct_cells = value;
         break;
+    case PASE_OPT_BULK_US:
+        if (value > 1000000000ull) return fail(g, PASE_ERR_INVALID_ARGUMENT, "bulk threshold <= 1e9 us");
+        g->bulk_us = (uint32_t)value;
+        break;
     case PASE_OPT_GRAD_SYNC:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "grad sync 0 or 1");
         g->grad_opt = (uint32_t)value;
@@ -1042,7 +1063,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
          opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER ||
-         opt == PASE_OPT_DIRECT_CELLS) &&
+         opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US) &&
         g->enumerated) {
         g->searched = false;
         pase_status st = build_plan(g);

@@ -218,7 +218,7 @@ struct SegDep {
 constexpr int kLatQ = 0, kBulkQ = 1;
 
 // PASE_OPT_SCHEDULE values
-enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedLanes = 2, kSchedFlow = 3 };
+enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedLanes = 2, kSchedFlow = 3, kSchedBulk = 4 };
 
 // Row-fill variants (columns per lane TZ, rows per lane TM, row terms NA) the
 // dataflow kernel carries: those that need at most ~96 VGPRs, so that the one
@@ -273,7 +273,8 @@ struct VPlan {
     // schedule
     int level = 0;                  // dependency level: 1 + max level of the tables it reads
     int slot = 0;                   // launch slot: its level (level schedule) or its position
-    int lane = 0;                   // lane schedule: 0 = the caller's stream, 1 = the latency chain's, 2 = other
+    int lane = 0;                   // lane schedules: 0 = the caller's stream, 1 = the latency chain's, 2 = other
+                                    // (bulk schedule: 1 = every small vertex, 2 = the large fills)
 };
 
 struct Plan {
@@ -323,6 +324,7 @@ struct pase_graph_s {
     uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
     uint32_t grad_opt = 0;          // pase_option PASE_OPT_GRAD_SYNC, read by pase_enumerate_configs
     uint64_t direct_cells = 1ull << 18;  // pase_option PASE_OPT_DIRECT_CELLS
+    uint32_t bulk_us = 100;         // pase_option PASE_OPT_BULK_US
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix

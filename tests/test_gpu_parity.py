@@ -70,7 +70,7 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
          parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False, grad=False,
-         direct=0):
+         direct=0, bulk_us=None):
     """direct: PASE_OPT_DIRECT_CELLS (0 = off, so the tests aimed at the row and
     generic kernels keep them; None = the library's default)."""
     pg = P.Graph(g, seq_rule=rule)
@@ -89,6 +89,8 @@ def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=
     pg.set_option(P.OPT_TILE_ROWS, tile[1])
     pg.set_option(P.OPT_TILE_PARTS, parts)
     pg.set_option(P.OPT_C_SPLITS, splits)
+    if bulk_us is not None:
+        pg.set_option(P.OPT_BULK_US, bulk_us)
     if costs is not None:
         pg.override_costs(*costs)
     mc, strat = pg.find_best_strategy()
@@ -133,6 +135,20 @@ def test_random_graphs_model_costs(P, seed):
         assert np.array_equal(pg.layer_costs(v), o.layer_costs(v))
     for e in range(len(g["edges"])):
         assert np.array_equal(pg.edge_costs(e), o.edge_costs(e))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_graphs_bulk_lane_schedule(P, seed):
+    """Bulk lane schedule on small random graphs, every row-kernel vertex on
+    the bulk stream (threshold 0): every table entry against the oracle."""
+    g = random_graph(seed + 300, n=5 + seed % 5, p=16, max_dims=3, extra_edges=seed % 5,
+                     max_size=512)
+    say(f"random graph bulk lane seed={seed + 300}")
+    o = _oracle(g)
+    pg, mc, strat = _run(P, g, schedule=4, bulk_us=0)
+    assert pg.stats()["schedule"] == 4
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g)
 
 
 # every form of the row kernel: columns x rows per lane, fp64 and uint64 keys
@@ -280,7 +296,8 @@ def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None):
+                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None,
+                  bulk_us=None):
     gold = _golden(name, seed, p, all_integers, bf, volume, grad)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
@@ -288,7 +305,7 @@ def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, sched
         f"direct={direct}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
                          lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume, grad=grad,
-                         direct=direct)
+                         direct=direct, bulk_us=bulk_us)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -345,6 +362,31 @@ def test_lane_schedule_against_golden(P, name):
     _check_golden(P, name, 0, keep=True, samples=False, schedule=2)
 
 
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
+def test_bulk_lane_schedule_against_golden(P, name):
+    """Large fills on a stream of their own, every other vertex level by
+    level on a second one: the same answer as the level schedule, with the
+    default threshold and with every row-kernel vertex on the bulk stream."""
+    _check_golden(P, name, 0, keep=False, schedule=4)
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=4)
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=4, bulk_us=0)
+
+
+def test_bulk_lane_assignment(P):
+    """The Transformer's large fills and every vertex reading their tables run
+    on the bulk stream; no vertex of the other stream reads a bulk table."""
+    g = workload("w4_transformer")
+    pg, _, _ = _run(P, g, keep=False, schedule=4)
+    assert pg.stats()["schedule"] == 4
+    info = {v: pg.vertex_info(v) for v in range(len(g["vertices"]))}
+    bulk = {v for v, x in info.items() if x["lane"] == 2}
+    assert bulk and len(bulk) < len(info)
+    assert all(x["lane"] in (1, 2) for x in info.values())
+    for v, x in info.items():
+        if x["kernel"] == 1 and x["cells"] >= 8e9:
+            assert v in bulk, v
+
+
 @pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
 @pytest.mark.parametrize("lat_workers", [0, 1, 65535])
 def test_dataflow_schedule_against_golden(P, name, lat_workers):
@@ -360,9 +402,10 @@ def test_workloads_run_the_requested_schedule(P):
     caller's stream."""
     for name in ("w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"):
         g = workload(name)
-        for sched in (0, 1, 2, 3):
+        for sched in (0, 1, 2, 3, 4):
             pg, _, _ = _run(P, g, keep=False, schedule=sched)
             assert pg.stats()["schedule"] == sched, (name, sched)
+    pg, _, _ = _run(P, g, keep=False, schedule=2)
     lanes = [pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))]
     assert 0 < sum(1 for x in lanes if x) < len(lanes)
 

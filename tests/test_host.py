@@ -347,3 +347,27 @@ def test_options_validate(pase):
     assert g.sequence() == [0, 1, 2, 3]
     costs = [np.zeros(10, np.uint64)] * 4
     assert _status(lambda: P.pase_override_costs(g.h, costs, [np.zeros((10, 10), np.uint64)] * 3)) == 0
+
+
+def test_bulk_lane_plan(pase):
+    """Schedule 4 on the Transformer graph: the large fills (>= 8e9 cells) and
+    every vertex at a level after them that reads only large fills' chain run
+    on the bulk stream (lane 2), all others on lane 1; a threshold above every
+    planned time leaves the bulk stream empty; the threshold validates."""
+    g = transformer()
+    pg = pase.Graph(g)
+    pg.set_option(pase.OPT_SCHEDULE, 4)
+    pg.enumerate_configs(g["p"])
+    info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
+    lanes = [x["lane"] for x in info]
+    assert set(lanes) == {1, 2}
+    for x in info:
+        if x["kernel"] == 1 and x["cells"] >= 8e9:
+            assert x["lane"] == 2
+    # the Transformer's encoder (the sequence's first vertices) never reads a large fill
+    seq = pg.sequence()
+    assert all(lanes[v] == 1 for v in seq[:20])
+    pg.set_option(pase.OPT_BULK_US, 10 ** 9)
+    assert {pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))} == {1}
+    assert _status(lambda: pg.set_option(pase.OPT_BULK_US, 10 ** 9 + 1)) == pase.INVALID_ARGUMENT
+    assert _status(lambda: pg.set_option(pase.OPT_SCHEDULE, 5)) == pase.INVALID_ARGUMENT
