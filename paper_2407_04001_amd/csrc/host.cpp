@@ -260,8 +260,12 @@ struct RowsChoice {
 // the latency bound of a single wave: per value of c at least one memory round
 // trip for the operands prefetched one c ahead (~450 cycles; column-less tiles
 // keep 8 values of c in flight, ~360 cycles per c), or its own VALU work at
-// about one op per 8 cycles; column-less tiles also stream their row terms at
-// ~5 TB/s.  A c split adds a reduction launch (~10 us with its gap) and the
+// about one op per 8 cycles.  Column-less tiles also stream their large
+// lookups (stream_bytes: the multi-digit tables they read, each entry once;
+// the one-digit row blocks stay in cache) at ~3.3 TB/s; when that stream binds,
+// the estimates of several part counts tie, and the most parts win: more
+// waves keep more loads in flight (measured on the Transformer's streaming
+// fills: 287 us with one part, 244 us with two or four).  A c split adds a reduction launch (~10 us with its gap) and the
 // partial keys' traffic; the column block is built at ~115 G elements/s.
 struct TileTime {
     double us;
@@ -269,7 +273,7 @@ struct TileTime {
 };
 
 TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t na, uint32_t tz, uint32_t tm,
-                   uint32_t force_parts, uint32_t force_splits) {
+                   uint32_t force_parts, uint32_t force_splits, double stream_bytes) {
     const double clk = 2400.0;   // cycles per us
     const uint64_t nch = (Kz + tz - 1) / tz;
     const uint64_t tiles = MO * ((MR + 64 * tm - 1) / (64 * tm)) * nch;
@@ -307,14 +311,16 @@ TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t n
             } else {
                 wave_cyc = 4.0 * cw * (2.0 * tm + tm * (na > 0 ? na - 1.0 : 0.0) + 1.0);
                 lat_cyc = 360.0 * cw;
-                bw_us = (double)N * K * na * 8 / 5e6;
+                bw_us = stream_bytes / 3.3e6;
             }
             // the busiest SIMD: the average share plus, on average, half a wave
             const double W = (double)tiles * P * Sx;
             const double t_tp = (W / 1024.0 + 0.5) * wave_cyc / clk;
             double us = std::max(std::max(t_tp, lat_cyc / clk), bw_us) + prep_us;
             if (Sx > 1) us += 10.0 + (double)N * Sx * 16 / 5e6;
-            if (us < best.us) best = {us, P, Sx};
+            // parts ascend: a column-less tie goes to the later, larger count
+            const bool tie_more_parts = tz < 8 && Sx == 1 && best.nsplit == 1 && us <= best.us * (1.0 + 1e-9);
+            if (us < best.us || tie_more_parts) best = {us, P, Sx};
         }
     }
     return best;
@@ -323,28 +329,29 @@ TileTime tile_time(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t n
 // Vertices of one graph often share a shape (the layers of a stack): the tile
 // model is evaluated once per distinct argument tuple.
 TileTime tile_time_cached(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uint32_t na, uint32_t tz, uint32_t tm,
-                          uint32_t force_parts, uint32_t force_splits) {
+                          uint32_t force_parts, uint32_t force_splits, double stream_bytes) {
     struct Key {
         uint64_t MO, MR;
         uint32_t Kz, K, na, tz, tm, parts, splits;
+        double sb;
         bool operator==(const Key &o) const {
             return MO == o.MO && MR == o.MR && Kz == o.Kz && K == o.K && na == o.na && tz == o.tz && tm == o.tm &&
-                   parts == o.parts && splits == o.splits;
+                   parts == o.parts && splits == o.splits && sb == o.sb;
         }
     };
     struct Hash {
         size_t operator()(const Key &k) const {
-            uint64_t h = k.MO * 0x9E3779B97F4A7C15ull ^ (k.MR + 0x632BE59BD9B4E019ull);
+            uint64_t h = k.MO * 0x9E3779B97F4A7C15ull ^ (k.MR + 0x632BE59BD9B4E019ull) ^ (uint64_t)k.sb;
             for (uint32_t x : {k.Kz, k.K, k.na, k.tz, k.tm, k.parts, k.splits}) h = (h ^ x) * 0x100000001B3ull;
             return (size_t)h;
         }
     };
     thread_local std::unordered_map<Key, TileTime, Hash> memo;
-    const Key key{MO, MR, Kz, K, na, tz, tm, force_parts, force_splits};
+    const Key key{MO, MR, Kz, K, na, tz, tm, force_parts, force_splits, stream_bytes};
     auto it = memo.find(key);
     if (it != memo.end()) return it->second;
     if (memo.size() > 65536) memo.clear();
-    const TileTime t = tile_time(MO, MR, Kz, K, na, tz, tm, force_parts, force_splits);
+    const TileTime t = tile_time(MO, MR, Kz, K, na, tz, tm, force_parts, force_splits, stream_bytes);
     memo.emplace(key, t);
     return t;
 }
@@ -582,12 +589,14 @@ static pase_status build_plan(pase_graph_t g) {
                     na += used;
                 }
                 bool small = true;   // row terms are read with 32-bit buffer offsets
+                double stream_bytes = 0;
                 for (const auto &t : vp.terms) {
                     if (t.dig.size() < 2) continue;
                     bool touches = false;
                     for (int u : t.dig) touches |= std::binary_search(rc.R.begin(), rc.R.end(), u);
                     na += touches;
                     if (touches && P.v[t.j].N * 8 >= (1ull << 31)) small = false;
+                    if (touches) stream_bytes += 8.0 * (double)std::min<uint64_t>(P.v[t.j].N, vp.N * vp.K);
                 }
                 if (na > (uint32_t)kMaxATerms || !small) continue;
                 rc.na = na;
@@ -607,7 +616,7 @@ static pase_status build_plan(pase_graph_t g) {
                             !flow_rows_ok(false, tz, tm, std::min<uint32_t>(na, 4)))
                             continue;
                         const TileTime tt = tile_time_cached(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts,
-                                                             g->c_splits);
+                                                             g->c_splits, stream_bytes);
                         if (!rc.ok || tt.us < rc.cost) {
                             rc.ok = true;
                             rc.cost = tt.us;
