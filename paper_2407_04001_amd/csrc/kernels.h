@@ -399,10 +399,12 @@ __device__ __forceinline__ void rows_item(const RowsArgs &a, uint32_t b, MergeBu
     // row terms and column chunks of the next U values are requested while
     // the cells of the current ones are computed from the other set, so load
     // latency overlaps VALU work.  Narrow tiles have little work per c and
-    // keep U = 4 values in flight per set.  Loads past c1 repeat column
-    // c1 - 1 (in bounds, unused) so that every load is unconditional and the
-    // register sets never need copying.
-    constexpr int U = TZ <= 2 ? 4 : 1;
+    // keep U = 4 values in flight per set; 8-column tiles keep 2 (two sets of
+    // 2 x 8 keys still fit in SGPRs) -- they serve the small, latency-bound
+    // vertices, whose waves otherwise wait out a round trip per c.  Loads past
+    // c1 repeat column c1 - 1 (in bounds, unused) so that every load is
+    // unconditional and the register sets never need copying.
+    constexpr int U = TZ <= 2 ? 4 : TZ <= 8 ? 2 : 1;
     using SKey = const __attribute__((address_space(4))) KeyT;
     uint64_t xe[U][TM][NTA], xo[U][TM][NTA];
     KeyT ce[U][TZ], co[U][TZ];
