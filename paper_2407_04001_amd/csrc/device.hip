@@ -474,7 +474,13 @@ static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<K
             bk.c_begin = cb;
             bk.c_end = (uint32_t)contrib.size();
             bk.rows = (uint32_t)el;
-            bk.chunks = (uint32_t)(((uint64_t)vp.K * ld + kPrepThreads - 1) / kPrepThreads);
+            // a workgroup covers `span` runs of kPrepThreads elements, so that
+            // the chain of scalar loads of the block's descriptors and
+            // contributions is paid once per span; large blocks keep at
+            // least ~4096 workgroups
+            const uint64_t runs = ((uint64_t)vp.K * ld + kPrepThreads - 1) / kPrepThreads;
+            bk.span = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(8, runs * el / 4096));
+            bk.chunks = (uint32_t)((runs + bk.span - 1) / bk.span);
             bk.wg_begin = L.prep.nwg;
             L.prep.nwg += bk.rows * bk.chunks;
             L.prep.total += bk.elems;

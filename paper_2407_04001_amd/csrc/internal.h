@@ -78,8 +78,9 @@ struct Block {
     uint32_t ld;              // row pitch (>= postrad, padded columns hold 0)
     uint32_t c_begin, c_end;  // contribution range
     uint32_t rows;            // prod(pre radices)
-    uint32_t chunks;          // workgroups per row: ceil(K * ld / kPrepThreads)
+    uint32_t chunks;          // workgroups per row: ceil(K * ld / (kPrepThreads * span))
     uint32_t wg_begin;        // first workgroup of this block
+    uint32_t span;            // kPrepThreads-element spans per workgroup
 };
 
 constexpr uint32_t kPrepThreads = 256;

@@ -254,10 +254,10 @@ __device__ __forceinline__ uint64_t contrib_key(const Contrib *__restrict__ cb, 
     return (sum << bits) + keysum + low;
 }
 
-// One workgroup handles kPrepThreads consecutive (c, column) elements of one
-// outer index of one block, so the block, its contributions and the outer
-// digits are uniform across the workgroup (scalar loads); lanes differ only in
-// (c, column).
+// One workgroup handles `span` runs of kPrepThreads consecutive (c, column)
+// elements of one outer index of one block, so the block, its contributions
+// and the outer digits are uniform across the workgroup (scalar loads, which
+// later runs find in the scalar cache); lanes differ only in (c, column).
 template <typename KeyT>
 __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const DevVertex *__restrict__ V,
                                           const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
@@ -271,11 +271,6 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
     const uint32_t rel = wg - bk.wg_begin;
     const uint32_t row = rel / bk.chunks, chunk = rel % bk.chunks;
     const uint32_t per_row = a.K * bk.ld;
-    const uint32_t e = chunk * kPrepThreads + threadIdx.x;
-    if (e >= per_row) return;
-    const uint32_t c = e / bk.ld, q = e % bk.ld;
-    KeyT *out = blocks + bk.out_off + (uint64_t)row * per_row + e;
-    if (bk.post >= 0 && q >= bk.postrad) { *out = (KeyT)0; return; }
     uint32_t dv[kMaxDep];
     for (int k = 0; k < kMaxDep; k++) dv[k] = 0;
     uint32_t x = row;
@@ -283,10 +278,20 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
         dv[bk.pre[k]] = x % bk.prerad[k];
         x /= bk.prerad[k];
     }
-    if (bk.post >= 0) dv[bk.post] = q;
     const DevVertex me = V[a.vi];
-    *out = KeyOps<KeyT>::from_u64(contrib_key<KeyT>(cb, bk.c_begin, bk.c_end, me, c, dv, a.bits, V, E, L, lsum,
-                                                     sig, r));
+    for (uint32_t s = 0; s < bk.span; s++) {
+        const uint32_t e = (chunk * bk.span + s) * kPrepThreads + threadIdx.x;
+        if (e >= per_row) return;
+        const uint32_t c = e / bk.ld, q = e % bk.ld;
+        KeyT *out = blocks + bk.out_off + (uint64_t)row * per_row + e;
+        if (bk.post >= 0 && q >= bk.postrad) {
+            *out = (KeyT)0;
+            continue;
+        }
+        if (bk.post >= 0) dv[bk.post] = q;
+        *out = KeyOps<KeyT>::from_u64(contrib_key<KeyT>(cb, bk.c_begin, bk.c_end, me, c, dv, a.bits, V, E, L,
+                                                         lsum, sig, r));
+    }
 }
 
 // Waits for every outstanding scalar-memory and LDS read (s_waitcnt
