@@ -20,6 +20,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <map>
 #include <type_traits>
 #include <cstring>
 #include <numeric>
@@ -1084,10 +1085,34 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
         add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
         std::vector<std::pair<uint32_t, int>> rows, gens, reds;
+        // fp64 keys: the row-term count is a kernel template parameter; a
+        // small vertex with fewer row terms than the largest vertex of its tile
+        // shape in this group gets zero terms appended (each lane adds the
+        // zero key once per c) and joins that vertex's launch
+        std::map<uint32_t, int> shape_dom;   // TZ * 4 + TM -> largest vertex of the group
+        for (int i : prepped)
+            if (launches[i].rows && std::is_same<KeyT, double>::value) {
+                auto it = shape_dom.find(P.v[i].TZ * 4 + P.v[i].TM);
+                if (it == shape_dom.end()) shape_dom[P.v[i].TZ * 4 + P.v[i].TM] = i;
+                else if (P.v[i].est_us > P.v[it->second].est_us) it->second = i;
+            }
         for (int i : prepped) {
             const Launch<KeyT> &L = launches[i];
             if (L.rows) {
                 uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
+                if (std::is_same<KeyT, double>::value && !use_flow) {
+                    const int d = shape_dom[P.v[i].TZ * 4 + P.v[i].TM];
+                    const uint32_t nd = std::min<uint32_t>(launches[d].ra.na, 4);
+                    if (d != i && na < nd && P.v[i].est_us <= 0.5 * P.v[d].est_us) {
+                        RowsArgs &ra = hr[i];
+                        for (uint32_t t = na; t < nd; t++) {
+                            std::memset(&ra.a[t], 0, sizeof ra.a[t]);
+                            ra.a[t].ptr = ws + P.off_zero;
+                            ra.a[t].bytes = 8;
+                        }
+                        na = nd;
+                    }
+                }
                 rows.push_back({(P.v[i].TZ * 4 + P.v[i].TM) * 8 + na, i});
                 if (P.v[i].nsplit > 1) reds.push_back({0, i});
             } else {

@@ -536,11 +536,15 @@ static pase_status build_plan(pase_graph_t g) {
     std::vector<char> level_small((size_t)maxlev + 1, 1);
     for (int i = 0; i < n; i++)
         if (P.v[i].N * P.v[i].K > g->direct_cells) level_small[P.v[i].level] = 0;
-    for (int i = 0; i < n; i++) {
+    // plan_one(i, ftz, ftm): kernel, tile and layout of position i; ftz/ftm
+    // (0 = free) force the row kernel's columns and rows per lane for this
+    // vertex and rule out the column-less form
+    auto plan_one = [&](int i, uint32_t ftz, uint32_t ftm) {
         VPlan &vp = P.v[i];
+        const uint32_t tile_cols = ftz ? ftz : g->tile_cols, tile_rows = ftm ? ftm : g->tile_rows;
         // small vertices: the direct fill (one launch, no prep blocks), whose
         // time is a launch plus the gather of every term of every cell
-        if (g->direct_cells && g->kernel_mode == 0 && g->schedule != kSchedFlow &&
+        if (!ftz && g->direct_cells && g->kernel_mode == 0 && g->schedule != kSchedFlow &&
             vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
             vp.kernel = kDirect;
             vp.est_us = 4.0 + (double)vp.N * vp.K * (1.0 + vp.edges.size() + vp.terms.size()) / 4e5;
@@ -550,7 +554,7 @@ static pase_status build_plan(pase_graph_t g) {
             vp.stride.assign(vp.layout.size(), 1);
             for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
                 vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
-            continue;
+            return;
         }
         RowsChoice best;
         // candidates: every digit of D(i) as the column digit z, and -- only
@@ -559,7 +563,7 @@ static pase_status build_plan(pase_graph_t g) {
         // lookup that covers all of D(i) this reads T_j once, coalesced)
         std::vector<int> zs;
         if (g->kernel_mode == 0 && vp.D.size() >= 2) zs = vp.D;
-        if (g->kernel_mode == 0 && !vp.D.empty()) zs.push_back(-1);
+        if (g->kernel_mode == 0 && !vp.D.empty() && !ftz) zs.push_back(-1);
         for (int z : zs) {
             if (z < 0 && best.ok) break;
             {
@@ -604,15 +608,15 @@ static pase_status build_plan(pase_graph_t g) {
                 static const uint32_t kNoColumn[] = {1};
                 for (uint32_t tz : z >= 0 ? std::vector<uint32_t>(std::begin(kTZ), std::end(kTZ))
                                           : std::vector<uint32_t>(std::begin(kNoColumn), std::end(kNoColumn))) {
-                    if (z >= 0 && g->tile_cols && tz != g->tile_cols) continue;
+                    if (z >= 0 && tile_cols && tz != tile_cols) continue;
                     uint64_t nch = (Kz + tz - 1) / tz;
                     if (rc.MO * vp.K * nch * tz > kMaxTableEntries) continue;
                     for (uint32_t tm = 1; tm <= 2; tm++) {
-                        if (g->tile_rows && tm != g->tile_rows) continue;
+                        if (tile_rows && tm != tile_rows) continue;
                         // more than 32 accumulators per lane cost waves (VGPRs)
-                        if (!g->tile_rows && !g->tile_cols && tz * tm > 32) continue;
+                        if (!tile_rows && !tile_cols && tz * tm > 32) continue;
                         // the dataflow kernel carries the variants of modest register need
-                        if (g->schedule == kSchedFlow && !g->tile_rows && !g->tile_cols &&
+                        if (g->schedule == kSchedFlow && !tile_rows && !tile_cols &&
                             !flow_rows_ok(false, tz, tm, std::min<uint32_t>(na, 4)))
                             continue;
                         const TileTime tt = tile_time_cached(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts,
@@ -651,9 +655,6 @@ static pase_status build_plan(pase_graph_t g) {
             const uint64_t ns = best.nsplit;
             vp.cper = (uint32_t)((vp.K + ns - 1) / ns);
             vp.nsplit = (vp.K + vp.cper - 1) / vp.cper;
-            P.rows_vertices++;
-            P.rows_cells += vp.N * vp.K;
-            if (vp.z < 0) P.stream_cells += vp.N * vp.K;
         } else {
             vp.kernel = kGeneric;
             // gather-bound: ~1e11 cell updates/s, plus a launch's worth of latency
@@ -665,6 +666,40 @@ static pase_status build_plan(pase_graph_t g) {
         vp.stride.assign(vp.layout.size(), 1);
         for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
             vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
+    };
+    for (int i = 0; i < n; i++) plan_one(i, 0, 0);
+    // One launch per level and kernel variant: a small column-form row vertex
+    // of a level is re-planned with the tile shape of the level's largest one
+    // when its fill then stays under half of that vertex's, so that the two
+    // share a launch (the small one's workgroups come first and finish inside
+    // the large one's) instead of adding a latency-bound launch of its own.
+    // Level schedule only: the lanes split a level over streams.
+    if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && g->kernel_mode == 0) {
+        std::vector<int> dom((size_t)maxlev + 1, -1);
+        for (int i = 0; i < n; i++) {
+            const VPlan &vp = P.v[i];
+            if (vp.kernel != kRows || vp.z < 0) continue;
+            int &d = dom[vp.level];
+            if (d < 0 || vp.est_us > P.v[d].est_us) d = i;
+        }
+        for (int i = 0; i < n; i++) {
+            const int d = dom[P.v[i].level];
+            if (d < 0 || d == i || P.v[i].kernel != kRows || P.v[i].z < 0) continue;
+            const VPlan &dv = P.v[d];
+            if (P.v[i].TZ == dv.TZ && P.v[i].TM == dv.TM) continue;
+            const VPlan saved = P.v[i];
+            plan_one(i, dv.TZ, dv.TM);
+            const VPlan &nv = P.v[i];
+            const bool ok = nv.kernel == kRows && nv.z >= 0 && nv.TZ == dv.TZ && nv.TM == dv.TM &&
+                            nv.na <= dv.na && nv.est_us <= 0.5 * dv.est_us;
+            if (!ok) P.v[i] = saved;
+        }
+    }
+    for (const auto &vp : P.v) {
+        if (vp.kernel != kRows) continue;
+        P.rows_vertices++;
+        P.rows_cells += vp.N * vp.K;
+        if (vp.z < 0) P.stream_cells += vp.N * vp.K;
     }
     assign_lanes(P);
     if (g->schedule == kSchedBulk) assign_bulk_lanes(P, (double)g->bulk_us);
@@ -749,6 +784,10 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
         P.flow_bytes = sizeof(FlowCtl) + align_up(4ull * n, 16) + 3ull * n * sizeof(Seg) + ndeps * sizeof(SegDep);
         off = align_up(off + P.flow_bytes, A);
     }
+    // one zero key: the row term that pads a row-kernel vertex up to the
+    // row-term count of the launch it shares (uploaded zeroed with the rest)
+    P.off_zero = off;
+    off = align_up(off + 8, A);
     P.off_cfg = off;
     off = align_up(off + g->V.size() * 4, A);
     P.off_out = off;

@@ -286,7 +286,7 @@ struct Plan {
     // workspace layout, byte offsets from the workspace base
     uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_lsum = 0, off_sig = 0,
              off_ovedge = 0, off_contrib = 0,
-             off_bt = 0, off_cfg = 0, off_out = 0, off_vmat = 0, off_T = 0, off_A = 0, off_block = 0,
+             off_bt = 0, off_zero = 0, off_cfg = 0, off_out = 0, off_vmat = 0, off_T = 0, off_A = 0, off_block = 0,
              off_partial = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
     uint64_t sig_count = 0;         // split signatures of all edge endpoints

@@ -371,3 +371,30 @@ def test_bulk_lane_plan(pase):
     assert {pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))} == {1}
     assert _status(lambda: pg.set_option(pase.OPT_BULK_US, 10 ** 9 + 1)) == pase.INVALID_ARGUMENT
     assert _status(lambda: pg.set_option(pase.OPT_SCHEDULE, 5)) == pase.INVALID_ARGUMENT
+
+
+def test_level_launch_unification(pase):
+    """Level schedule: a level's small column-form row vertices take the tile
+    shape of its largest one (so they share its launch) when their fill stays
+    small; the sequential schedule plans every vertex on its own."""
+    g = transformer()
+    shapes = {}
+    for sched in (0, 1):
+        pg = pase.Graph(g)
+        pg.set_option(pase.OPT_SCHEDULE, sched)
+        pg.enumerate_configs(g["p"])
+        info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
+        rows = [x for x in info if x["kernel"] == 1 and x["column"] >= 0]
+        shapes[sched] = rows
+        if sched == 0:
+            by_level = {}
+            for x in rows:
+                by_level.setdefault(x["level"], []).append(x)
+            # level 0 holds the four largest fills and the small leaves of the
+            # encoder and decoder layers: one tile shape for all of them
+            lvl0 = by_level[0]
+            big = max(lvl0, key=lambda x: x["cells"])
+            assert {(x["tile_cols"], x["tile_rows"]) for x in lvl0} == {(big["tile_cols"], big["tile_rows"])}
+    distinct0 = {(x["tile_cols"], x["tile_rows"]) for x in shapes[0] if x["level"] == 0}
+    distinct1 = {(x["tile_cols"], x["tile_rows"]) for x in shapes[1] if x["level"] == 0}
+    assert len(distinct0) < len(distinct1)
