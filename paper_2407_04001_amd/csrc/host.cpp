@@ -204,7 +204,6 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
                   const std::vector<int> *order = nullptr) {
     const size_t n = g->V.size(), W = (n + 63) / 64;
     std::vector<uint64_t> d(n * W, 0);
-    auto has = [&](size_t v, size_t u) { return (d[v * W + u / 64] >> (u % 64)) & 1ull; };
     for (size_t v = 0; v < n; v++)
         for (int u : g->nbr[v]) d[v * W + u / 64] |= 1ull << (u % 64);
     // |u.d| is kept per vertex and recounted only when u.d changes
@@ -215,7 +214,11 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
     };
     std::vector<int> size(n);
     for (size_t u = 0; u < n; u++) size[u] = count(u);
-    std::vector<char> done(n, 0);
+    // vertices not sequenced yet, in no particular order: the pick is the
+    // smallest (|u.d|, vertex id), so the scan order does not matter
+    std::vector<int> left(n), where(n);
+    std::iota(left.begin(), left.end(), 0);
+    std::iota(where.begin(), where.end(), 0);
     seq.clear();
     Dpos.assign(n, {});
     for (size_t i = 0; i < n; i++) {
@@ -223,14 +226,22 @@ void generate_seq(pase_graph_t g, std::vector<int> &seq, std::vector<std::vector
         if (order) {
             best = (size_t)(*order)[i];
         } else {
-            for (size_t u = 0; u < n; u++)
-                if (!done[u] && (best == n || size[u] < size[best])) best = u;
+            for (int u : left)
+                if (best == n || size[u] < size[best] || (size[u] == size[best] && (size_t)u < best)) best = (size_t)u;
         }
         const size_t vi = best;
-        done[vi] = 1;
+        // remove vi from the unsequenced set (swap with the last)
+        const int at = where[vi], tail = left.back();
+        left[at] = tail;
+        where[tail] = at;
+        left.pop_back();
         seq.push_back((int)vi);
-        for (size_t u = 0; u < n; u++)
-            if (u != vi && has(vi, u)) Dpos[i].push_back((int)u);
+        // D(i) = vi.d (ascending vertex id): the set bits of its row
+        for (size_t w = 0; w < W; w++)
+            for (uint64_t bits = d[vi * W + w]; bits; bits &= bits - 1) {
+                const size_t u = w * 64 + (size_t)__builtin_ctzll(bits);
+                if (u != vi) Dpos[i].push_back((int)u);
+            }
         for (int v : Dpos[i]) {
             for (size_t w = 0; w < W; w++) d[(size_t)v * W + w] |= d[vi * W + w];
             d[(size_t)v * W + vi / 64] &= ~(1ull << (vi % 64));
@@ -265,8 +276,9 @@ struct RowsChoice {
 // the one-digit row blocks stay in cache) at ~3.3 TB/s; when that stream binds,
 // the estimates of several part counts tie, and the most parts win: more
 // waves keep more loads in flight (measured on the Transformer's streaming
-// fills: 287 us with one part, 244 us with two or four).  A c split adds a reduction launch (~10 us with its gap) and the
-// partial keys' traffic; the column block is built at ~115 G elements/s.
+// fills: 287 us with one part, 244 us with two or four).  A c split adds a
+// reduction launch (~10 us with its gap) and the partial keys' traffic; the
+// column block is built at ~115 G elements/s.
 struct TileTime {
     double us;
     uint32_t parts, nsplit;
