@@ -748,3 +748,43 @@ def test_direct_fill_schedules_and_orders(P):
 def test_direct_fill_whole_workloads(P, name):
     """Every vertex of a workload on the direct fill, against the golden."""
     _check_golden(P, name, 0, direct=ALL_DIRECT)
+
+
+@pytest.mark.parametrize("block", range(4))
+def test_random_graph_sweep_schedules(P, block):
+    """Seeded sweep over random graphs (4-13 vertices, 2-5 loop dims, p from 4
+    to 64, sizes up to 4096): the level schedule (shared level launches), the
+    bulk lane with every row vertex on the bulk stream, the sequential
+    schedule and the level schedule without the direct fill all give the
+    oracle's minimum, strategy and every table (fingerprints).  A graph whose
+    worst-case key exceeds 64 bits is refused with OVERFLOW (key bound) and
+    skipped."""
+    checked = 0
+    for seed in range(block * 20, block * 20 + 20):
+        rng = np.random.default_rng(seed)
+        n = int(rng.integers(4, 14))
+        p = int(rng.choice([4, 8, 16, 32, 64]))
+        g = random_graph(seed + 5000, n=n, p=p, max_dims=int(rng.integers(2, 6)),
+                         extra_edges=int(rng.integers(0, 6)), max_size=int(rng.choice([8, 64, 512, 4096])))
+        say(f"random sweep seed={seed + 5000} n={n} p={p}")
+        o = _oracle(g)
+        fps = [o.fingerprint(i) for i in range(len(o.sequence()))]
+        for sched, bulk, direct in ((0, None, None), (4, 0, None), (1, None, 0), (0, None, 0)):
+            pg = P.Graph(g)
+            pg.set_option(P.OPT_SCHEDULE, sched)
+            if bulk is not None:
+                pg.set_option(P.OPT_BULK_US, bulk)
+            if direct is not None:
+                pg.set_option(P.OPT_DIRECT_CELLS, direct)
+            pg.set_option(P.OPT_KEEP_TABLES, 1)
+            pg.enumerate_configs(p)
+            try:
+                mc, strat = pg.find_best_strategy()
+            except P.PaseError as e:
+                assert e.status == P.OVERFLOW, e
+                continue
+            assert (mc, strat) == o.result(), (seed, sched)
+            for i, v in enumerate(o.sequence()):
+                assert pg.fingerprint(v) == fps[i], (seed, sched, v)
+            checked += 1
+    assert checked >= 60
