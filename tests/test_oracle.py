@@ -821,6 +821,15 @@ MUTANTS = {
                       "unsigned __int128 words = ((unsigned __int128)2 * R * S + (R - 1)) / R;"),
     "pow2_only": ("for (uint64_t s = 1; s <= budget; s = pow2 ? 2 * s : s + 1) {",
                   "for (uint64_t s = 1; s <= budget; s = 2 * s) {"),
+    "edge_min_devices": ("uint64_t words = ceil_div(o->elems[e], Pu > Pv ? Pu : Pv);",
+                         "uint64_t words = ceil_div(o->elems[e], Pu < Pv ? Pu : Pv);"),
+    "compute_over_kept_split": ("uint64_t compute = ceil_div(flops, P);",
+                                "uint64_t compute = ceil_div(flops, keep_split);"),
+    "comm_over_all_devices": ("if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;",
+                              "if (!mul_ok(red_split - 1, ceil_div(keep_n, P), &comm)) return 0;"),
+    "seq_keeps_self": ("if (rule == 0) d[(size_t)v * n + v] = 0;", "if (rule == 2) d[(size_t)v * n + v] = 0;"),
+    "grad_replicas_from_weight_dims": ("                Pw *= s[k];\n            } else {\n                R *= s[k];",
+                                       "                R *= s[k];\n            } else {\n                Pw *= s[k];"),
 }
 
 
@@ -856,7 +865,8 @@ def _pin_suite(lib):
         ex = [tuple(int(x) for x in r) for r in o.exponents(0)]
         R = o.edge_costs(0)
         return (int(R[ex.index((2, 0, 0)), ex.index((0, 0, 2))]) == 8 * 4096
-                and int(R[ex.index((1, 1, 0)), ex.index((1, 0, 1))]) == 0)
+                and int(R[ex.index((1, 1, 0)), ex.index((1, 0, 1))]) == 0
+                and int(R[ex.index((0, 0, 0)), ex.index((1, 0, 0))]) == 8 * 8192)   # max(P_u, P_v) = 2
 
     def tables():
         for seed in range(6):
