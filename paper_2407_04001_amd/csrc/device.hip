@@ -963,7 +963,18 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
 
     // ---- constant region image (one host-to-device copy)
     char *img = (char *)d->pinned;
-    std::memset(img, 0, P.off_cfg);
+    // the layer costs, their device bytes and the split signatures
+    // [off_L, off_ovedge) are written by k_cost_tables on the device: unless
+    // the caller overrode the costs, that range is not cleared here, and it is
+    // left out of the upload once it is large enough to pay for a second copy
+    // call (what the one copy then carries there is overwritten on the device)
+    const bool upload_costs = g->overridden || P.off_ovedge - P.off_L < (256u << 10);
+    if (g->overridden) {
+        std::memset(img, 0, P.off_cfg);
+    } else {
+        std::memset(img, 0, P.off_L);
+        std::memset(img + P.off_ovedge, 0, P.off_cfg - P.off_ovedge);
+    }
     // one row set per dimension count, shared by the vertices with that count
     uint64_t row_off[kMaxDims + 1] = {0}, off = 0;
     for (size_t d = 0; d < g->ex_rows.size() && d <= (size_t)kMaxDims; d++) {
@@ -1076,20 +1087,27 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
         batches.push_back(b);
     };
+    // per-group scratch, reused across groups (cleared, capacity kept)
+    std::vector<int> prepped, direct, grp;
+    std::vector<std::pair<uint32_t, int>> rows, gens, reds;
+    std::map<uint32_t, int> shape_dom;   // TZ * 4 + TM -> largest vertex of the group
     for (size_t sl = 0; sl < groups.size(); sl++) {
         const auto &mem = groups[sl];
         cur_lane = group_lane[sl];
         cur_group = (int)sl;
-        std::vector<int> prepped, direct;
+        prepped.clear();
+        direct.clear();
         for (int i : mem) (launches[i].direct ? direct : prepped).push_back(i);
         add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
         add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
-        std::vector<std::pair<uint32_t, int>> rows, gens, reds;
+        rows.clear();
+        gens.clear();
+        reds.clear();
         // fp64 keys: the row-term count is a kernel template parameter; a
         // small vertex with fewer row terms than the largest vertex of its tile
         // shape in this group gets zero terms appended (each lane adds the
         // zero key once per c) and joins that vertex's launch
-        std::map<uint32_t, int> shape_dom;   // TZ * 4 + TM -> largest vertex of the group
+        shape_dom.clear();
         for (int i : prepped)
             if (launches[i].rows && std::is_same<KeyT, double>::value) {
                 auto it = shape_dom.find(P.v[i].TZ * 4 + P.v[i].TM);
@@ -1124,22 +1142,22 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         std::stable_sort(gens.begin(), gens.end(),
                          [](const std::pair<uint32_t, int> &a, const std::pair<uint32_t, int> &b) { return a.first < b.first; });
         for (size_t k = 0; k < rows.size();) {
-            std::vector<int> grp;
+            grp.clear();
             size_t k2 = k;
             for (; k2 < rows.size() && rows[k2].first == rows[k].first; k2++) grp.push_back(rows[k2].second);
             add_batch(Batch::kRows, rows[k].first, grp, [](const Launch<KeyT> &L) { return L.ra.nblocks_launched; });
             k = k2;
         }
         for (size_t k = 0; k < gens.size();) {
-            std::vector<int> grp;
+            grp.clear();
             size_t k2 = k;
             for (; k2 < gens.size() && gens[k2].first == gens[k].first; k2++) grp.push_back(gens[k2].second);
             add_batch(Batch::kGeneric, gens[k].first, grp, [](const Launch<KeyT> &L) { return L.ga.nblk; });
             k = k2;
         }
-        std::vector<int> rgrp;
-        for (auto &x : reds) rgrp.push_back(x.second);
-        add_batch(Batch::kReduce, 0, rgrp, [](const Launch<KeyT> &L) { return L.red.nblk; });
+        grp.clear();
+        for (auto &x : reds) grp.push_back(x.second);
+        add_batch(Batch::kReduce, 0, grp, [](const Launch<KeyT> &L) { return L.red.nblk; });
     }
     if (nbe > 3 * (uint64_t)n) return fail(g, PASE_ERR_INTERNAL, "batch table overflow");
     for (const Batch &b : batches)
@@ -1173,7 +1191,13 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         fa.done = (uint32_t *)(ws + P.off_flow + sizeof(FlowCtl));
     }
 
-    HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
+    if (upload_costs) {
+        HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
+    } else {
+        HIPCHK(hipMemcpyAsync(ws, img, P.off_L, hipMemcpyHostToDevice, s));
+        HIPCHK(hipMemcpyAsync(ws + P.off_ovedge, img + P.off_ovedge, P.off_cfg - P.off_ovedge,
+                              hipMemcpyHostToDevice, s));
+    }
 
     const DevVertex *dV = (const DevVertex *)(ws + P.off_vert);
     const DevEdge *dE = (const DevEdge *)(ws + P.off_edge);
