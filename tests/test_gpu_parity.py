@@ -271,6 +271,31 @@ def test_repeat_and_reenumerate(P):
     assert results[2] == _oracle(g, p=4).result()
 
 
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception"])
+def test_model_costs_after_override(P, name):
+    # model costs -> caller-given costs (the model's doubled) -> model costs
+    # again on one graph and workspace.  The model's cost tables are computed
+    # on the device; the two workloads put them below (W1, 27 KiB) and above
+    # (W2, 353 KiB) the size from which the search leaves them out of its
+    # host-to-device upload.  Doubling every cost keeps every argmin, so the
+    # strategy is unchanged and the minimum doubles.
+    g = workload(name)
+    say(f"model / override / model costs: {name}")
+    pg = P.Graph(g)
+    pg.enumerate_configs(g["p"])
+    mc0, s0 = pg.find_best_strategy()
+    layer = [pg.layer_costs(v) for v in range(len(g["vertices"]))]
+    edge = [pg.edge_costs(e) for e in range(len(g["edges"]))]
+    pg.override_costs([2 * np.asarray(a, np.uint64) for a in layer], [2 * np.asarray(a, np.uint64) for a in edge])
+    mc1, s1 = pg.find_best_strategy()
+    assert mc1 == 2 * mc0 and s1 == s0
+    assert np.array_equal(pg.layer_costs(0), 2 * np.asarray(layer[0], np.uint64))
+    pg.enumerate_configs(g["p"])
+    assert pg.find_best_strategy() == (mc0, s0)
+    for v in range(len(g["vertices"])):
+        assert np.array_equal(pg.layer_costs(v), layer[v])
+
+
 def test_library_owned_workspace(P):
     g = workload("w1_residual_cnn", 1)
     say("library-owned workspace")
