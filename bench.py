@@ -9,7 +9,8 @@ Prints one JSON line: DP cell-updates/s of whole steps (`value`), the step
 wall time, the roofline of the dominant kernel (the row/column-chunk fill,
 fp64 add + min per cell, timed with HIP events on the search stream), the
 parity of the result with the CPU oracle's stored answer, and the oracle's
-own speed on a bounded prefix of the same vertex sequence.
+own time for the same search on the host cores (and single-threaded on a
+prefix of the vertex sequence).
 """
 import argparse
 import json
@@ -50,10 +51,11 @@ def cpu_model():
     return "unknown"
 
 
-def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False, grad=False):
-    """The oracle on the host cores (OpenMP over table entries), on a prefix of
-    the vertex order of about `max_cells` cells, then single-threaded on a
-    prefix a tenth that size."""
+def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False, volume=False, grad=False):
+    """The oracle on the host cores (OpenMP over table entries): the whole
+    search when it has at most `max_cells` cells (else the prefix of the vertex
+    order that reaches that many), then single-threaded on a prefix of about
+    `single_cells` cells."""
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
@@ -66,8 +68,9 @@ def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False,
             o.solve(max_cells=cells, threads=nthreads)
         return o.cells_done() / o.seconds(), o.cells_done(), o.seconds()
 
-    one, one_cells, one_s = run(max(1, max_cells // (10 * threads)), 1)
-    run(max_cells, threads)
+    one, one_cells, one_s = run(max(1, int(single_cells)), 1)
+    total = o.cells()
+    run(0 if total <= max_cells else int(max_cells), threads)
     done = o.cells_done()
     n_done = 0
     cum = 0
@@ -77,11 +80,14 @@ def oracle_baseline(g, p, max_cells, all_integers=False, bf=False, volume=False,
         n_done += 1
         if cum >= done:
             break
+    order = "breadth-first" if bf else "GenerateSeq"
+    whole = done == total
+    sample = (f"the whole search: all {len(seq)} vertices of the {order} order" if whole else
+              f"first {n_done} of {len(seq)} vertices of the same {order} order")
     return {"value": done / o.seconds(), "unit": "cell-updates/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n_done} of {len(seq)} vertices of the same "
-                      f"{'breadth-first' if bf else 'GenerateSeq'} order "
-                      f"({done:.3e} of {o.cells():.3e} cells, {o.seconds():.1f} s, "
+            "sample": f"{sample} ({done:.3e} of {total:.3e} cells, {o.seconds():.1f} s, "
                       f"OpenMP over table entries)",
+            "whole_search": whole, "seconds": round(o.seconds(), 2),
             "single_thread": {"value": one, "cells": one_cells, "seconds": round(one_s, 2)},
             "cpu_model": cpu_model()}
 
@@ -116,19 +122,20 @@ def traffic_from_profile():
     return prof.get("bytes_per_launch")
 
 
-SCHEDULES = {0: "level", 1: "sequential", 2: "lanes", 3: "dataflow", 4: "bulk lane"}
+SCHEDULES = {0: "level", 1: "sequential", 4: "bulk lane"}
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
-def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integers=False, bf=False,
-                 volume=False, grad=False, schedule=None):
+def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu, p=None, all_integers=False,
+                 bf=False, volume=False, grad=False, schedule=None):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
     transfer costs when `volume`; with the weight-gradient term when `grad`);
     returns the report
     dict (the oracle timed on the same graph: the whole search when it has at
-    most `cpu_cells` cells, else a prefix of the vertex order).  A search the
+    most `cpu_cells` cells, else a prefix of the vertex order; single-threaded
+    on a prefix of about `cpu_single_cells` cells).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
     from paper_2407_04001_amd import OPT_GRAD_SYNC, OPT_ORDER, OPT_PROFILE, OPT_SCHEDULE, OPT_TRANSFER, Graph, PaseError
@@ -180,6 +187,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         step()
     torch.cuda.synchronize()
     walls, rows_ms, rows_launches, step_ms = [], 0.0, 0, []
+    phase_keys = ("seq_ms", "plan_ms", "setup_ms", "cost_tables_ms", "fill_span_ms", "backtrack_ms")
+    phases = dict.fromkeys(phase_keys, 0.0)
     t0 = time.perf_counter()
     for _ in range(steps):
         ts = time.perf_counter()
@@ -187,6 +196,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         step_ms.append((time.perf_counter() - ts) * 1e3)
         st = pg.stats()
         walls.append(st["wall_ms"])
+        for k in phase_keys:
+            phases[k] += st[k] / steps
         # the dominant kernel: the row kernel with a column chunk per lane (the
         # only launches timed; its column-less form is not)
         rows_ms += st["rows_fill_ms"]
@@ -227,6 +238,9 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
         "config": dict(config, cells=cells, schedule=SCHEDULES.get(st["schedule"], st["schedule"])),
         "find_best_strategy_ms": sum(walls) / len(walls),
+        # mean per step: host GenerateSeq / plans (enumerate), host launch
+        # setup, and the device phases timed with events on the search stream
+        "phases_ms": {k[:-3]: round(v, 4) for k, v in phases.items()},
         "median_ms_per_step": sorted(step_ms)[len(step_ms) // 2],
         # the whole search against the ALU roofline: every cell costs `ops` VALU
         # lane-ops (t_roof), against the fill-kernel time and the step
@@ -235,7 +249,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
         "min_cost": mc, "parity_with_oracle": parity,
         "roofline": {"bound": "alu", "kernel": "k_fill_rows",
                      "achieved": achieved, "peak": FP64_OPS_PEAK_T,
-                     "unit": "TFLOP/s" if st["key_type"] == 0 else "T int32-op/s",
+                     "unit": "T fp64-op/s" if st["key_type"] == 0 else "T int32-op/s",
                      "frac": achieved / FP64_OPS_PEAK_T,
                      "traffic": traffic_from_profile() if headline else None,
                      "launches_per_step": rows_launches // steps,
@@ -243,7 +257,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, no_cpu, p=None, all_integ
                      "cells_per_step": col_cells},
     }
     if not no_cpu:
-        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), all_integers, bf, volume, grad)
+        out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), int(cpu_single_cells), all_integers, bf,
+                                              volume, grad)
     return out
 
 
@@ -254,7 +269,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="w4_transformer")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-cells", type=float, default=3e10, help="oracle sample size (cells)")
+    ap.add_argument("--cpu-cells", type=float, default=1e11,
+                    help="oracle on all host cores: the whole search up to this many cells, else a prefix")
+    ap.add_argument("--cpu-single-cells", type=float, default=3e9,
+                    help="single-threaded oracle sample (cells, a prefix of the vertex order)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (HBM counter calibration)")
@@ -269,7 +287,7 @@ def main():
                     help="transfer cost model: split match (default) or volume intersection")
     ap.add_argument("--grad-sync", action="store_true",
                     help="add the weight-gradient all-reduce to the layer costs")
-    ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 2, 3, 4),
+    ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 4),
                     help="launch schedule (PASE_OPT_SCHEDULE; default: the library's)")
     args = ap.parse_args()
     if args.copy_calibration:
@@ -285,7 +303,8 @@ def main():
     torch.cuda.set_device(0)
     names = WORKLOADS if args.all_workloads else [args.workload]
     for name in names:
-        out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.no_cpu,
+        out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.cpu_single_cells,
+                           args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
                            args.transfer == "volume", args.grad_sync, args.schedule)
         print(json.dumps(out), flush=True)

@@ -108,22 +108,15 @@ typedef enum {
     PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
                                    do not read each other) share their kernel launches, one
                                    stream, table memory packed by lifetimes.  1: one vertex at a
-                                   time in sequence order (same packing).  2: lanes -- the
-                                   tables' reader tree cut into chains that run on three streams
-                                   (the latency-bound chain at the highest wave priority), level
-                                   batches within each, events where a table is read across
-                                   lanes.  3: dataflow -- one persistent launch runs every prep,
-                                   fill and reduction workgroup as soon as the tables it reads
-                                   are complete (device-side dependency counters, two ticket
-                                   queues).  2 and 3 keep every table resident and fall back to 0
-                                   over the memory budget; 3 also when a vertex needs a fill
-                                   variant the persistent kernel does not carry.  4: bulk lane --
-                                   every row-kernel vertex whose planned fill takes at least
-                                   PASE_OPT_BULK_US runs on a stream of its own, all other
-                                   vertices level by level on a second stream at the highest wave
-                                   priority, events only where a table is read across the two;
-                                   so a latency-bound chain never waits for a large vertex it
-                                   does not read (every table resident, 0 over the budget). */
+                                   time in sequence order (same packing).  4: bulk lane -- every
+                                   row-kernel vertex whose planned fill takes at least
+                                   PASE_OPT_BULK_US runs, with every vertex reading its table, on
+                                   a stream of its own; all other vertices level by level on the
+                                   caller's stream at the highest wave priority; events only where
+                                   a table is read across the two; so a latency-bound chain never
+                                   waits for a large vertex it does not read (every table
+                                   resident; falls back to 0 over the memory budget).  Other
+                                   values: INVALID_ARGUMENT */
     PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
                                    vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
                                    that kernel runs (a tuning and test knob) */
@@ -133,9 +126,6 @@ typedef enum {
     PASE_OPT_C_SPLITS = 10,     /* same kernel: workgroups sharing one tile's c range (partial
                                    keys reduced by a second launch), 0 = chosen (default), else
                                    min(value, K_v) for every vertex */
-    PASE_OPT_LATENCY_WORKERS = 11, /* dataflow schedule: workgroups that serve the latency queue
-                                   (the chains of small vertices) before the bulk queue; 0 =
-                                   chosen (default: one in 16), else clamped to [1, grid - 1] */
     PASE_OPT_CONFIG_SET = 12,   /* configuration set of the next pase_enumerate_configs: 0
                                    (default) power-of-two split factors, p = 2^L <= 65536; 1
                                    every tuple of positive integer factors (Sec. II's C(v)),
@@ -177,8 +167,8 @@ typedef enum {
                                    for the long chains of small dependent vertices, where launch
                                    count dominates.  A level uses it only when all its vertices
                                    qualify (so that it saves launches; any vertex under the
-                                   sequential schedule).  Default 2^18; 0 = never.  Not used by
-                                   the dataflow schedule or with PASE_OPT_KERNEL = 1 */
+                                   sequential schedule).  Default 2^18; 0 = never.  Not used with
+                                   PASE_OPT_KERNEL = 1 */
     PASE_OPT_BULK_US = 17       /* schedule 4: planned fill time (microseconds) from which a
                                    row-kernel vertex runs on the bulk stream (default 100) */
 } pase_option;
@@ -193,7 +183,7 @@ typedef struct {
     uint32_t launches;         /* kernels launched by the search */
     uint32_t rows_vertices;    /* vertices filled by the row/column-chunk kernel */
     uint64_t rows_cells;       /* cells filled by that kernel */
-    double host_plan_ms;       /* pase_enumerate_configs: ordering + plans (host) */
+    double host_plan_ms;       /* pase_enumerate_configs (host): seq_ms + plan_ms */
     double wall_ms;            /* pase_find_best_strategy, host wall clock */
     double fill_ms;            /* PASE_OPT_PROFILE: sum of the timed fill launches' event times
                                   (profile 2: the column-form row-kernel launches only) */
@@ -205,11 +195,18 @@ typedef struct {
     double stream_fill_ms;     /* PASE_OPT_PROFILE: event time of those launches, a part of
                                   rows_fill_ms */
     uint32_t stream_launches;  /* PASE_OPT_PROFILE: their launches, a part of rows_launches */
-    uint32_t schedule;         /* schedule the search ran with (PASE_OPT_SCHEDULE values); with 3
-                                  rows_fill_ms is the duration of the one dataflow launch */
-    uint32_t flow_grid;        /* dataflow: workgroups of the launch */
-    uint32_t flow_lat_workers; /* dataflow: of them, latency workers */
-    uint64_t flow_items;       /* dataflow: work items (prep, fill and reduction workgroups) */
+    uint32_t schedule;         /* schedule the search ran with (PASE_OPT_SCHEDULE values) */
+    uint32_t pad0;
+    /* phases of the last enumeration and search, milliseconds */
+    double seq_ms;             /* pase_enumerate_configs, host: GenerateSeq and the sets D(i), X(i), S(i) */
+    double plan_ms;            /* pase_enumerate_configs, host: kernel plans and the device memory layout */
+    double setup_ms;           /* pase_find_best_strategy, host: key bound, launch descriptors and the
+                                  constant-region image, up to the upload */
+    double cost_tables_ms;     /* PASE_OPT_PROFILE, device: upload and cost-table kernels */
+    double fill_span_ms;       /* PASE_OPT_PROFILE, device: from the end of the cost tables to the end
+                                  of the last fill or split reduction (every prep, fill and reduction
+                                  launch and the gaps between them) */
+    double backtrack_ms;       /* PASE_OPT_PROFILE, device: back-substitution */
 } pase_run_stats;
 
 /* Copy a computation graph G=(V,E) (Sec. II) into a new handle.
@@ -321,25 +318,14 @@ typedef struct {
     uint32_t parts;      /* row kernel: waves sharing one tile's c range (1, 2 or 4) */
     double fill_ms;      /* PASE_OPT_PROFILE: event time of this vertex's fill kernel */
     uint32_t level;      /* dependency level: 1 + the largest level of the tables it reads */
-    uint32_t lane;       /* lane schedule: the stream it runs on: 0 = the caller's, 1 = the latency-bound
-                            chain's (highest wave priority), 2 = the other chains' */
+    uint32_t lane;       /* bulk lane schedule: the stream it runs on: 0 = the caller's (small vertices,
+                            highest wave priority), 1 = the bulk stream (large fills and their readers) */
     uint64_t key_bound;  /* upper bound of every summed cost before the min over c (keys stay
                             below (key_bound + 1) * 2^ceil(log2 K_v)); ~0 if it exceeds 64 bits */
     uint64_t table_bound; /* upper bound of every entry of its DP table; ~0 likewise */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);
-
-/* Test hook (host only, no device work): build the dataflow schedule of the
- * current plan (PASE_OPT_SCHEDULE 0, after pase_enumerate_configs) and run a
- * randomized simulation of its worker protocol with `workers` workgroups, the
- * first `lat_workers` of them serving the latency queue first.  *items: the
- * number of work items.  Errors: INVALID_ARGUMENT (workers < 2, lat_workers
- * not in [1, workers)), BAD_STATE (no plan, or the plan fell back to another
- * schedule), INTERNAL (the simulated workers deadlock, an item would start
- * before its dependencies are met, or items are left undone). */
-pase_status pase_flow_check(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
-                            uint64_t *items);
 
 #ifdef __cplusplus
 }

@@ -20,7 +20,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
 
 
 def sources():
-    return [os.path.join(CSRC, f) for f in ("host.cpp", "device.hip", "flow.hip")]
+    return [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "device.hip")]
 
 
 def build(verbose: bool = False, out: str = LIB, extra=()) -> str:

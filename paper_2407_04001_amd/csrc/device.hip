@@ -28,6 +28,7 @@
 
 #include "internal.h"
 #include "kernels.h"
+#include "launch.h"
 
 using namespace pase;
 
@@ -164,7 +165,7 @@ __global__ __launch_bounds__(256) void k_fill_direct(const DirectArgs *__restric
 // sequence).  Single thread; n dependent reads.
 template <typename KeyT>
 __global__ void k_backtrack(const BacktrackDesc *__restrict__ bt, uint32_t n, const void *Tlast,
-                            uint32_t *__restrict__ cfg, SearchOut *out, const uint32_t *flow_error) {
+                            uint32_t *__restrict__ cfg, SearchOut *out) {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
     uint32_t status = 0;
     for (int i = (int)n - 1; i >= 0; i--) {
@@ -177,7 +178,7 @@ __global__ void k_backtrack(const BacktrackDesc *__restrict__ bt, uint32_t n, co
         cfg[d.vi] = c;
     }
     out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
-    out->status = status | (flow_error ? *flow_error : 0u);
+    out->status = status;
 }
 
 // Back-substitution by backward levels: one thread per position; the
@@ -189,8 +190,7 @@ __global__ __launch_bounds__(kMaxBacktrackThreads) void k_backtrack_levels(const
                                                                           uint32_t n, uint32_t nlev,
                                                                           const void *Tlast,
                                                                           uint32_t *__restrict__ cfg,
-                                                                          SearchOut *out,
-                                                                          const uint32_t *flow_error) {
+                                                                          SearchOut *out) {
     __shared__ uint32_t scfg[kMaxBacktrackThreads];
     __shared__ uint32_t sbad;
     const uint32_t t = threadIdx.x;
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kMaxBacktrackThreads) void k_backtrack_levels(const
     if (mine) cfg[t] = scfg[t];
     if (t == 0) {
         out->min_cost = KeyOps<KeyT>::val_to_u64(((const typename KeyOps<KeyT>::Val *)Tlast)[0]);
-        out->status = sbad | (flow_error ? *flow_error : 0u);
+        out->status = sbad;
     }
 }
 
@@ -269,8 +269,6 @@ __global__ void k_fingerprint(FingerArgs a) {
 // ------------------------------------------------------------------ runtime
 namespace pase {
 
-constexpr int kLanes = 3;   // streams of the lane schedule
-
 struct DeviceState {
     void *ws = nullptr;
     uint64_t ws_bytes = 0;
@@ -279,12 +277,11 @@ struct DeviceState {
     uint64_t lent_bytes = 0;
     void *pinned = nullptr;
     uint64_t pinned_bytes = 0;
-    std::vector<hipEvent_t> ev;        // profiling: two per fill launch (timed)
+    std::vector<hipEvent_t> ev;        // profiling: two per timed fill launch
+    hipEvent_t phase_ev[4] = {};       // profiling: search phases (cost tables | fill | back-substitution)
     hipStream_t last_stream = nullptr;
-    int flow_grid[2] = {0, 0};         // resident workgroups of the dataflow kernel, per key type
-    int wall_khz = 0;                  // device wall clock (wall_clock64) rate
-    hipStream_t side[kLanes - 1] = {}; // lane schedule: the streams of lanes 1.. (default priority)
-    std::vector<hipEvent_t> lane_ev;   // lane schedule: joins (no timing)
+    hipStream_t side = nullptr;        // bulk lane schedule: the bulk stream (default priority)
+    std::vector<hipEvent_t> lane_ev;   // bulk lane schedule: joins (no timing)
 };
 
 #define HIPCHK(x)                                                                              \
@@ -301,8 +298,9 @@ void device_release(pase_graph_t g) {
     if (d->pinned) (void)hipHostFree(d->pinned);
     for (auto e : d->ev) (void)hipEventDestroy(e);
     for (auto e : d->lane_ev) (void)hipEventDestroy(e);
-    for (auto st : d->side)
-        if (st) (void)hipStreamDestroy(st);
+    for (auto e : d->phase_ev)
+        if (e) (void)hipEventDestroy(e);
+    if (d->side) (void)hipStreamDestroy(d->side);
     delete d;
     g->dev = nullptr;
 }
@@ -356,532 +354,6 @@ static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) 
     uint64_t b = (n + block - 1) / block;
     return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, cap));
 }
-
-// One vertex's launch description, resolved against the workspace base.
-template <typename KeyT>
-struct Launch {
-    PrepArgs prep;
-    bool rows = false;
-    bool direct = false;
-    RowsArgs ra;
-    GenericArgs ga;
-    ReduceArgs red;
-    DirectArgs da;
-};
-
-static uint32_t plan_digit(const VPlan &vp, int vertex) {
-    for (size_t k = 0; k < vp.layout.size(); k++)
-        if (vp.layout[k] == vertex) return (uint32_t)k;
-    return ~0u;
-}
-
-// Strides with which consumer position i reads table T_j: (stride of v_i, per plan digit).
-static void lookup_strides(const Plan &P, int i, int j, uint32_t &sc, uint32_t sd[kMaxDep]) {
-    const VPlan &vi = P.v[i], &vj = P.v[j];
-    sc = 0;
-    for (int k = 0; k < kMaxDep; k++) sd[k] = 0;
-    for (size_t k = 0; k < vj.layout.size(); k++) {
-        int u = vj.layout[k];
-        if (u == vi.vi) sc = (uint32_t)vj.stride[k];
-        else sd[plan_digit(vi, u)] = (uint32_t)vj.stride[k];
-    }
-}
-
-// Largest element index a strided read can reach: (K-1)*sc + sum (radix-1)*stride.
-static uint64_t max_index(uint32_t K, uint32_t sc, const uint32_t *sd, const uint32_t *rad, int m) {
-    uint64_t x = (uint64_t)(K - 1) * sc;
-    for (int k = 0; k < m; k++) x += (uint64_t)(rad[k] - 1) * sd[k];
-    return x;
-}
-
-template <typename KeyT>
-static pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &out,
-                                   std::vector<Contrib> &contrib) {
-    const Plan &P = g->plan;
-    const int n = (int)P.v.size();
-    out.assign(n, Launch<KeyT>());
-    contrib.clear();
-    const uint64_t *ovedge = (const uint64_t *)(ws + P.off_ovedge);
-    for (int i = 0; i < n; i++) {
-        const VPlan &vp = P.v[i];
-        Launch<KeyT> &L = out[i];
-        KeyT *blocks = (KeyT *)(ws + P.off_block + vp.block_off);
-        std::memset(&L.prep, 0, sizeof L.prep);
-        L.prep.blocks = blocks;
-        L.prep.vi = (uint32_t)vp.vi;
-        L.prep.K = vp.K;
-        L.prep.bits = vp.bits;
-        uint32_t rad[kMaxDep];
-        for (size_t k = 0; k < vp.layout.size(); k++) rad[k] = g->K[vp.layout[k]];
-        const int m = (int)vp.layout.size();
-        bool bounds_ok = true;
-        auto other_of = [&](int e) {
-            return (int)g->E[e].src == vp.vi ? (int)g->E[e].dst : (int)g->E[e].src;
-        };
-        auto edge_contrib = [&](int e, uint32_t dig) {
-            Contrib c;
-            std::memset(&c, 0, sizeof c);
-            bool is_src = (int)g->E[e].src == vp.vi;
-            if (g->overridden || g->volume) {
-                c.kind = kContribTable;
-                c.raw_u64 = 1;
-                c.ptr = g->overridden ? ovedge + g->ov_edge_off[e] : (const uint64_t *)(ws + P.off_vmat) + g->mat_off[e];
-                uint32_t Kd = g->K[g->E[e].dst];
-                if (is_src) { c.sc = Kd; c.sd[dig] = 1; }
-                else { c.sc = 1; c.sd[dig] = Kd; }
-                if (max_index(vp.K, c.sc, c.sd, rad, m) >= (uint64_t)g->K[g->E[e].src] * Kd)
-                    bounds_ok = false;
-            } else {
-                c.kind = kContribEdge;
-                c.edge = (uint32_t)e;
-                c.dig = dig;
-                c.vi_is_src = is_src;
-            }
-            contrib.push_back(c);
-        };
-        auto table_contrib = [&](const TermRef &t) {
-            Contrib c;
-            std::memset(&c, 0, sizeof c);
-            c.kind = kContribTable;
-            c.ptr = ws + P.off_T + P.v[t.j].T_off;
-            lookup_strides(P, i, t.j, c.sc, c.sd);
-            // the prep block only feeds digits of the lookup, so every index stays inside T_j
-            if (max_index(vp.K, c.sc, c.sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
-            contrib.push_back(c);
-        };
-        auto layer_contrib = [&]() {
-            Contrib c;
-            std::memset(&c, 0, sizeof c);
-            c.kind = kContribLayer;
-            contrib.push_back(c);
-        };
-        uint64_t boff = 0;
-        auto add_block = [&](const std::vector<int> &pre, int post, uint32_t ld, uint32_t cb) -> int {
-            Block &bk = L.prep.blk[L.prep.nblocks];
-            std::memset(&bk, 0, sizeof bk);
-            bk.npre = (uint32_t)pre.size();
-            uint64_t el = 1;
-            for (size_t k = 0; k < pre.size(); k++) {
-                bk.pre[k] = plan_digit(vp, pre[k]);
-                bk.prerad[k] = g->K[pre[k]];
-                el *= g->K[pre[k]];
-            }
-            bk.post = post >= 0 ? (int32_t)plan_digit(vp, post) : -1;
-            bk.postrad = post >= 0 ? g->K[post] : 1;
-            bk.ld = ld;
-            bk.elems = el * vp.K * ld;
-            bk.out_off = boff;
-            boff += (bk.elems + 31) / 32 * 32;
-            bk.c_begin = cb;
-            bk.c_end = (uint32_t)contrib.size();
-            bk.rows = (uint32_t)el;
-            // a workgroup covers `span` runs of kPrepThreads elements, so that
-            // the chain of scalar loads of the block's descriptors and
-            // contributions is paid once per span; large blocks keep at
-            // least ~4096 workgroups
-            const uint64_t runs = ((uint64_t)vp.K * ld + kPrepThreads - 1) / kPrepThreads;
-            bk.span = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(8, runs * el / 4096));
-            bk.chunks = (uint32_t)((runs + bk.span - 1) / bk.span);
-            bk.wg_begin = L.prep.nwg;
-            L.prep.nwg += bk.rows * bk.chunks;
-            L.prep.total += bk.elems;
-            return (int)L.prep.nblocks++;
-        };
-        if (vp.kernel == kDirect) {
-            // every term over all plan digits; no blocks
-            DirectArgs &da = L.da;
-            std::memset(&da, 0, sizeof da);
-            da.c_begin = (uint32_t)contrib.size();
-            layer_contrib();
-            for (int e : vp.edges) edge_contrib(e, plan_digit(vp, other_of(e)));
-            for (const auto &t : vp.terms) table_contrib(t);
-            da.c_end = (uint32_t)contrib.size();
-            da.vi = (uint32_t)vp.vi;
-            da.K = vp.K;
-            da.bits = vp.bits;
-            da.out_shift = vp.out_shift;
-            da.m = (uint32_t)vp.layout.size();
-            for (size_t k = 0; k < vp.layout.size(); k++) da.rad[k] = g->K[vp.layout[k]];
-            // lanes per entry: enough threads to fill the GPU, at most one wave, at most K
-            da.group_log2 = 0;
-            while (da.group_log2 < 6 && (vp.N << da.group_log2) < 65536 && (2u << da.group_log2) <= vp.K)
-                da.group_log2++;
-            da.N = vp.N;
-            da.T = ws + P.off_T + vp.T_off;
-            da.A = (uint16_t *)(ws + P.off_A + vp.A_off);
-            da.nblk = (uint32_t)std::min<uint64_t>(((vp.N << da.group_log2) + 255) / 256, 65535);
-            L.direct = true;
-        } else if (vp.kernel == kRows) {
-            // column block B over (O..., c, z): everything not touching a row digit
-            std::vector<int> OZ = vp.O;
-            OZ.push_back(vp.z);
-            auto in_oz = [&](int u) { return std::find(OZ.begin(), OZ.end(), u) != OZ.end(); };
-            uint32_t cb = (uint32_t)contrib.size();
-            layer_contrib();
-            for (int e : vp.edges)
-                if (in_oz(other_of(e))) edge_contrib(e, plan_digit(vp, other_of(e)));
-            for (const auto &t : vp.terms) {
-                bool all = true;
-                for (int u : t.dig) all &= in_oz(u);
-                if (all) table_contrib(t);
-            }
-            add_block(vp.O, vp.z, vp.ldz, cb);
-            RowsArgs &ra = L.ra;
-            std::memset(&ra, 0, sizeof ra);
-            ra.B = blocks + L.prep.blk[0].out_off;
-            // one-digit row blocks E_w, w in R
-            for (size_t rk = 0; rk < vp.R.size(); rk++) {
-                int w = vp.R[rk];
-                cb = (uint32_t)contrib.size();
-                for (int e : vp.edges)
-                    if (other_of(e) == w) edge_contrib(e, plan_digit(vp, w));
-                for (const auto &t : vp.terms)
-                    if (t.dig.size() == 1 && t.dig[0] == w) table_contrib(t);
-                if (contrib.size() == cb) continue;
-                int b = add_block({}, w, g->K[w], cb);
-                ATerm &at = ra.a[ra.na++];
-                at.ptr = blocks + L.prep.blk[b].out_off;
-                at.sc = g->K[w];
-                at.bytes = (uint32_t)(L.prep.blk[b].elems * sizeof(KeyT));
-                at.sdR[rk] = 1;
-            }
-            // lookups touching a row digit with two or more digits: read in the kernel
-            for (const auto &t : vp.terms) {
-                if (t.dig.size() < 2) continue;
-                bool touches = false;
-                for (int u : t.dig) touches |= std::count(vp.R.begin(), vp.R.end(), u) > 0;
-                if (!touches) continue;
-                if (ra.na >= (uint32_t)kMaxATerms) return fail(g, PASE_ERR_INTERNAL, "row terms");
-                ATerm &at = ra.a[ra.na++];
-                uint32_t sc, sd[kMaxDep];
-                lookup_strides(P, i, t.j, sc, sd);
-                if (max_index(vp.K, sc, sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
-                at.ptr = ws + P.off_T + P.v[t.j].T_off;
-                at.sc = sc;
-                at.bytes = (uint32_t)(P.v[t.j].N * 8);
-                // plan digits: z (if there is a column digit), then O, then R
-                const size_t zoff = vp.z >= 0 ? 1 : 0;
-                for (size_t k = 0; k < vp.O.size(); k++) at.sdO[k] = sd[zoff + k];
-                for (size_t k = 0; k < vp.R.size(); k++) at.sdR[k] = sd[zoff + vp.O.size() + k];
-            }
-            ra.ldz = vp.ldz;
-            ra.Kz = vp.z >= 0 ? g->K[vp.z] : 1;
-            ra.K = vp.K;
-            ra.bits = vp.bits;
-            ra.MO = (uint32_t)vp.MO;
-            ra.MR = (uint32_t)vp.MR;
-            ra.tiles_per_o = (uint32_t)((vp.MR + 64 * vp.TM - 1) / (64 * vp.TM));
-            ra.nchunks = vp.nchunks;
-            ra.nsplit = vp.nsplit;
-            ra.cper = vp.cper;
-            ra.nO = (uint32_t)vp.O.size();
-            ra.nR = (uint32_t)vp.R.size();
-            for (size_t k = 0; k < vp.O.size(); k++) ra.radO[k] = g->K[vp.O[k]];
-            for (size_t k = 0; k < vp.R.size(); k++) ra.radR[k] = g->K[vp.R[k]];
-            ra.T = ws + P.off_T + vp.T_off;
-            ra.A = (uint16_t *)(ws + P.off_A + vp.A_off);
-            ra.partial = ws + P.off_partial + vp.partial_off;
-            ra.N = vp.N;
-            ra.out_shift = vp.out_shift;
-            // a workgroup takes 4 / parts tiles
-            ra.parts = vp.parts;
-            ra.total_tiles = (uint64_t)vp.nsplit * vp.nchunks * vp.MO * ra.tiles_per_o;
-            uint64_t nbk = (ra.total_tiles + 4 / vp.parts - 1) / (4 / vp.parts);
-            nbk = (nbk + 7) / 8 * 8;
-            if (nbk > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "grid too large");
-            ra.nblocks_launched = (uint32_t)nbk;
-            L.rows = true;
-            if (vp.nsplit > 1) {
-                L.red.nblk = grid_for(vp.N);
-                L.red.partial = ra.partial;
-                L.red.T = ra.T;
-                L.red.A = ra.A;
-                L.red.N = vp.N;
-                L.red.nsplit = vp.nsplit;
-                L.red.bits = vp.bits;
-                L.red.out_shift = vp.out_shift;
-            }
-        } else {
-            GenericArgs &ga = L.ga;
-            std::memset(&ga, 0, sizeof ga);
-            uint32_t cb = (uint32_t)contrib.size();
-            layer_contrib();
-            for (const auto &t : vp.terms)
-                if (t.dig.empty()) table_contrib(t);
-            int b0 = add_block({}, -1, 1, cb);
-            GTerm &g0 = ga.t[ga.nt++];
-            g0.ptr = blocks + L.prep.blk[b0].out_off;
-            g0.sc = 1;
-            for (int w : vp.D) {
-                cb = (uint32_t)contrib.size();
-                for (int e : vp.edges)
-                    if (other_of(e) == w) edge_contrib(e, plan_digit(vp, w));
-                for (const auto &t : vp.terms)
-                    if (t.dig.size() == 1 && t.dig[0] == w) table_contrib(t);
-                if (contrib.size() == cb) continue;
-                int b = add_block({}, w, g->K[w], cb);
-                GTerm &gt = ga.t[ga.nt++];
-                gt.ptr = blocks + L.prep.blk[b].out_off;
-                gt.sc = g->K[w];
-                gt.sd[plan_digit(vp, w)] = 1;
-            }
-            for (const auto &t : vp.terms) {
-                if (t.dig.size() < 2) continue;
-                if (ga.nt >= (uint32_t)kMaxGTerms)
-                    return fail(g, PASE_ERR_TOO_LARGE, "too many table lookups for one vertex");
-                GTerm &gt = ga.t[ga.nt++];
-                gt.ptr = ws + P.off_T + P.v[t.j].T_off;
-                lookup_strides(P, i, t.j, gt.sc, gt.sd);
-                if (max_index(vp.K, gt.sc, gt.sd, rad, m) >= P.v[t.j].N) bounds_ok = false;
-            }
-            ga.m = (uint32_t)vp.layout.size();
-            ga.K = vp.K;
-            ga.bits = vp.bits;
-            // lanes per entry: enough threads to fill the GPU, at most one wave, at most K
-            ga.group_log2 = 0;
-            while (ga.group_log2 < 6 && (vp.N << ga.group_log2) < 65536 && (2u << ga.group_log2) <= vp.K)
-                ga.group_log2++;
-            for (size_t k = 0; k < vp.layout.size(); k++) ga.rad[k] = g->K[vp.layout[k]];
-            ga.T = ws + P.off_T + vp.T_off;
-            ga.A = (uint16_t *)(ws + P.off_A + vp.A_off);
-            ga.N = vp.N;
-            ga.out_shift = vp.out_shift;
-            ga.nblk = (uint32_t)std::min<uint64_t>(((vp.N << ga.group_log2) + 255) / 256, 65535);
-        }
-        if (boff > vp.block_elems) return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
-        if (!bounds_ok) return fail(g, PASE_ERR_INTERNAL, "a table lookup would leave its table");
-        if (vp.nsplit > 1 && vp.partial_off + (uint64_t)vp.nsplit * vp.N * sizeof(KeyT) > P.partial_bytes)
-            return fail(g, PASE_ERR_INTERNAL, "split scratch overflow");
-        if (vp.block_off + boff * sizeof(KeyT) > P.block_bytes)
-            return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
-    }
-    if (contrib.size() > P.contrib_count) return fail(g, PASE_ERR_INTERNAL, "contribution overflow");
-    return PASE_OK;
-}
-
-// ------------------------------------------------------------------ dataflow segments
-// Vertices whose planned fill takes at least this long (us, whole GPU) go to
-// the bulk queue; the rest -- the long chains of small dependent vertices --
-// to the latency queue.
-constexpr double kBulkUs = 25.0;
-
-struct FlowPlan {
-    std::vector<Seg> seg[2];
-    std::vector<SegDep> deps;
-    uint32_t nitems[2] = {0, 0};
-};
-
-// Segments (prep, fill, split reduction of every position) in one global
-// order: by the start time of their vertex in a simulation of the schedule
-// (latency vertices start when their producers end; bulk vertices also wait
-// for the previous bulk vertex), then position, then phase.  Every vertex
-// starts strictly after its producers end, so the order is topological.
-template <typename KeyT>
-static pase_status build_flow(pase_graph_t g, const std::vector<Launch<KeyT>> &launches, FlowPlan &fp) {
-    const Plan &P = g->plan;
-    const int n = (int)P.v.size();
-    std::vector<uint32_t> np(n), nf(n), nr(n);
-    std::vector<char> bulk(n);
-    for (int i = 0; i < n; i++) {
-        const Launch<KeyT> &L = launches[i];
-        np[i] = L.prep.nwg;
-        nf[i] = L.rows ? L.ra.nblocks_launched : L.ga.nblk;
-        nr[i] = (L.rows && P.v[i].nsplit > 1) ? L.red.nblk : 0;
-        bulk[i] = P.v[i].est_us >= kBulkUs;
-        if (np[i] == 0 || nf[i] == 0) return fail(g, PASE_ERR_INTERNAL, "empty segment");
-    }
-    const double delta = 2.0;
-    std::vector<int> order(n);
-    std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return P.v[a].level < P.v[b].level; });
-    std::vector<double> esi(n, 0.0), efi(n, 0.0);
-    for (int i : order) {
-        for (const auto &t : P.v[i].terms) esi[i] = std::max(esi[i], efi[t.j]);
-        efi[i] = esi[i] + P.v[i].est_us + delta;
-    }
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return esi[a] < esi[b]; });
-    std::vector<double> start(n, 0.0), fin(n, 0.0);
-    double bulk_free = 0;
-    for (int i : order) {
-        double r = 0;
-        for (const auto &t : P.v[i].terms) r = std::max(r, fin[t.j]);
-        start[i] = bulk[i] ? std::max(r, bulk_free) : r;
-        fin[i] = start[i] + P.v[i].est_us + delta;
-        if (bulk[i]) bulk_free = start[i] + P.v[i].est_us;
-    }
-    struct Item { double key; int pos, phase; };
-    std::vector<Item> items;
-    for (int i = 0; i < n; i++) {
-        items.push_back({start[i], i, 0});
-        items.push_back({start[i], i, 1});
-        if (nr[i]) items.push_back({start[i], i, 2});
-    }
-    std::sort(items.begin(), items.end(), [](const Item &a, const Item &b) {
-        if (a.key != b.key) return a.key < b.key;
-        if (a.pos != b.pos) return a.pos < b.pos;
-        return a.phase < b.phase;
-    });
-    // check the order before anything runs: a vertex's segments come after
-    // all segments of every producer it reads, and in phase order
-    std::vector<int> last_idx(n, -1), first_idx(n, -1);
-    for (size_t k = 0; k < items.size(); k++) {
-        const int i = items[k].pos;
-        if (first_idx[i] < 0) first_idx[i] = (int)k;
-        if (last_idx[i] >= 0 && items[last_idx[i]].phase >= items[k].phase)
-            return fail(g, PASE_ERR_INTERNAL, "dataflow order: phases out of order");
-        last_idx[i] = (int)k;
-    }
-    for (int i = 0; i < n; i++)
-        for (const auto &t : P.v[i].terms)
-            if (last_idx[t.j] >= first_idx[i]) return fail(g, PASE_ERR_INTERNAL, "dataflow order not topological");
-    fp = FlowPlan();
-    for (const Item &it : items) {
-        const int i = it.pos;
-        const int q = bulk[i] ? kBulkQ : kLatQ;
-        Seg sg;
-        std::memset(&sg, 0, sizeof sg);
-        sg.first = fp.nitems[q];
-        sg.pos = (uint32_t)i;
-        sg.dep_begin = (uint32_t)fp.deps.size();
-        if (it.phase == 0) {
-            sg.kind = kSegPrep;
-            sg.count = np[i];
-            for (const auto &t : P.v[i].terms) fp.deps.push_back({(uint32_t)t.j, np[t.j] + nf[t.j] + nr[t.j]});
-        } else if (it.phase == 1) {
-            const Launch<KeyT> &L = launches[i];
-            if (L.rows) {
-                sg.kind = kSegRows;
-                const uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
-                sg.variant = (P.v[i].TZ * 4 + P.v[i].TM) * 8 + na;
-            } else {
-                sg.kind = kSegGeneric;
-                sg.variant = L.ga.nt <= 6 ? L.ga.nt : 0;
-            }
-            sg.count = nf[i];
-            fp.deps.push_back({(uint32_t)i, np[i]});
-        } else {
-            sg.kind = kSegReduce;
-            sg.count = nr[i];
-            fp.deps.push_back({(uint32_t)i, np[i] + nf[i]});
-        }
-        sg.dep_end = (uint32_t)fp.deps.size();
-        if ((uint64_t)fp.nitems[q] + sg.count > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "dataflow items");
-        fp.nitems[q] += sg.count;
-        fp.seg[q].push_back(sg);
-    }
-    return PASE_OK;
-}
-
-// Randomized simulation of the k_flow worker protocol on the host: `workers`
-// workgroups, the first `lat_workers` of them latency workers, take tickets
-// exactly as the kernel does, wait until the dependencies of their item are
-// met, run it for a random time and count it as done.  Fails if the workers
-// can no longer make progress (deadlock), if an item would start before its
-// dependencies are met, or if a counter does not end at its vertex's item
-// count.
-static pase_status flow_simulate(pase_graph_t g, const FlowPlan &fp, uint32_t workers, uint32_t lat_workers,
-                                 uint64_t seed) {
-    const int n = (int)g->plan.v.size();
-    std::vector<uint32_t> done(n, 0), total(n, 0);
-    for (int q = 0; q < 2; q++)
-        for (const Seg &sg : fp.seg[q]) total[sg.pos] += sg.count;
-    auto seg_of = [&](int q, uint32_t t) -> const Seg & {
-        size_t lo = 0, hi = fp.seg[q].size();
-        while (hi - lo > 1) {
-            const size_t mid = (lo + hi) / 2;
-            if (fp.seg[q][mid].first <= t) lo = mid; else hi = mid;
-        }
-        return fp.seg[q][lo];
-    };
-    auto met = [&](const Seg &sg) {
-        for (uint32_t k = sg.dep_begin; k < sg.dep_end; k++)
-            if (done[fp.deps[k].counter] < fp.deps[k].target) return false;
-        return true;
-    };
-    for (const SegDep &d : fp.deps)
-        if (d.counter >= (uint32_t)n || d.target > total[d.counter])
-            return fail(g, PASE_ERR_INTERNAL, "dataflow dependency can never be met");
-    enum { kIdle, kWaiting, kRunning, kExited };
-    struct W { bool lat; int state; int q; uint32_t t; double until; };
-    std::vector<W> w(workers);
-    for (uint32_t k = 0; k < workers; k++) w[k] = {k < lat_workers, kIdle, -1, 0, 0.0};
-    uint64_t head[2] = {0, 0};
-    uint64_t rs = seed * 0x9E3779B97F4A7C15ull + 1;
-    auto rnd = [&]() {   // xorshift64*
-        rs ^= rs >> 12; rs ^= rs << 25; rs ^= rs >> 27;
-        return rs * 0x2545F4914F6CDD1Dull;
-    };
-    std::vector<uint32_t> idx(workers);
-    std::iota(idx.begin(), idx.end(), 0u);
-    double now = 0;
-    for (;;) {
-        for (uint32_t k = workers; k > 1; k--) std::swap(idx[k - 1], idx[rnd() % k]);
-        for (uint32_t k : idx) {
-            W &x = w[k];
-            if (x.state != kIdle) continue;
-            int q = -1;
-            uint64_t t = 0;
-            if (x.lat) {
-                t = head[kLatQ]++;
-                if (t < fp.nitems[kLatQ]) q = kLatQ; else x.lat = false;
-            }
-            if (q < 0 && head[kLatQ] < fp.nitems[kLatQ] && met(seg_of(kLatQ, (uint32_t)head[kLatQ]))) {
-                t = head[kLatQ]++;
-                q = kLatQ;
-            }
-            if (q < 0) {
-                t = head[kBulkQ]++;
-                if (t < fp.nitems[kBulkQ]) {
-                    q = kBulkQ;
-                } else {
-                    t = head[kLatQ]++;
-                    if (t < fp.nitems[kLatQ]) q = kLatQ;
-                }
-            }
-            if (q < 0) { x.state = kExited; continue; }
-            x.q = q;
-            x.t = (uint32_t)t;
-            x.state = kWaiting;
-        }
-        bool any_running = false, any_waiting = false;
-        for (W &x : w) {
-            if (x.state == kWaiting && met(seg_of(x.q, x.t))) {
-                x.state = kRunning;
-                x.until = now + 1.0 + (double)(rnd() % 1000) / 100.0;
-            }
-            any_running |= x.state == kRunning;
-            any_waiting |= x.state == kWaiting;
-        }
-        if (!any_running) {
-            if (any_waiting) return fail(g, PASE_ERR_INTERNAL, "dataflow schedule deadlocks");
-            break;
-        }
-        double next = 1e300;
-        for (const W &x : w)
-            if (x.state == kRunning) next = std::min(next, x.until);
-        now = next;
-        for (W &x : w)
-            if (x.state == kRunning && x.until <= now) {
-                done[seg_of(x.q, x.t).pos]++;
-                x.state = kIdle;
-            }
-    }
-    for (int i = 0; i < n; i++)
-        if (done[i] != total[i]) return fail(g, PASE_ERR_INTERNAL, "dataflow items left undone");
-    return PASE_OK;
-}
-
-// A batched launch: vertices (sequence positions) sharing one kernel variant
-// within one launch slot, with their first workgroups.
-struct Batch {
-    enum Kind { kPrep, kRows, kGeneric, kReduce, kDirect } kind;
-    int lane;              // two-lane schedule: the stream it runs on
-    int group;             // launch group (a slot, or a (level, lane) pair) it belongs to
-    uint32_t variant;      // rows: (TZ * 4 + TM) * 8 + NA (NA 7 = runtime count); generic: NT (0 = runtime)
-    uint32_t entry0;       // first BatchEntry of this batch
-    uint32_t nentries;
-    uint32_t blocks;       // workgroups of the launch
-};
 
 template <typename KeyT, int TZ, int TM>
 static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s, hipEvent_t e0,
@@ -946,252 +418,16 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     Plan &P = g->plan;
     const int n = (int)P.v.size();
     const size_t nv = g->V.size(), ne = g->E.size();
+    const auto t_setup = std::chrono::steady_clock::now();
 
-    std::vector<Launch<KeyT>> launches;
-    std::vector<Contrib> contrib;
-    pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
-    if (st != PASE_OK) return st;
-    // the dataflow launch needs the resident layout and a kernel variant it
-    // carries for every row fill; otherwise the level schedule runs (the
-    // resident layout serves it as well)
-    bool use_flow = P.resident && g->schedule == kSchedFlow;
-    const bool use_lanes = P.resident && (g->schedule == kSchedLanes || g->schedule == kSchedBulk);
-    for (int i = 0; i < n && use_flow; i++)
-        if (launches[i].rows)
-            use_flow = flow_rows_ok(!std::is_same<KeyT, double>::value, P.v[i].TZ, P.v[i].TM,
-                                    std::min<uint32_t>(launches[i].ra.na, std::is_same<KeyT, double>::value ? 4 : 7));
-
-    // ---- constant region image (one host-to-device copy)
+    // ---- constant region image and batched launches (host), one upload
     char *img = (char *)d->pinned;
-    // the layer costs, their device bytes and the split signatures
-    // [off_L, off_ovedge) are written by k_cost_tables on the device: unless
-    // the caller overrode the costs, that range is not cleared here, and it is
-    // left out of the upload once it is large enough to pay for a second copy
-    // call (what the one copy then carries there is overwritten on the device)
-    const bool upload_costs = g->overridden || P.off_ovedge - P.off_L < (256u << 10);
-    if (g->overridden) {
-        std::memset(img, 0, P.off_cfg);
-    } else {
-        std::memset(img, 0, P.off_L);
-        std::memset(img + P.off_ovedge, 0, P.off_cfg - P.off_ovedge);
-    }
-    // one row set per dimension count, shared by the vertices with that count
-    uint64_t row_off[kMaxDims + 1] = {0}, off = 0;
-    for (size_t d = 0; d < g->ex_rows.size() && d <= (size_t)kMaxDims; d++) {
-        row_off[d] = off;
-        if (!g->ex_rows[d].empty()) std::memcpy(img + P.off_ex + off, g->ex_rows[d].data(), g->ex_rows[d].size());
-        off += g->ex_rows[d].size();
-    }
-    std::vector<DevVertex> dvs(nv);
-    uint64_t loff = 0;
-    for (size_t v = 0; v < nv; v++) {
-        DevVertex &x = dvs[v];
-        x.ex_off = row_off[g->V[v].ndims];
-        x.L_off = loff;
-        x.flops = g->flops[v];
-        x.keep_n = g->keep_n[v];
-        x.K = g->K[v];
-        x.ndims = g->V[v].ndims;
-        x.reduce_mask = g->V[v].reduce_mask;
-        x.factors = g->factors ? 1 : 0;
-        x.weight_n = g->weight_n[v];
-        x.weight_mask = g->V[v].weight_mask;
-        loff += g->K[v];
-    }
-    std::memcpy(img + P.off_vert, dvs.data(), nv * sizeof(DevVertex));
-    std::vector<DevEdge> des(ne);
-    uint64_t sig_off = 0;
-    for (size_t e = 0; e < ne; e++) {
-        DevEdge &x = des[e];
-        std::memset(&x, 0, sizeof x);
-        x.src = g->E[e].src;
-        x.dst = g->E[e].dst;
-        x.rank = g->E[e].rank;
-        x.factors = g->factors ? 1 : 0;
-        for (uint32_t k = 0; k < kMaxDims; k++) {
-            x.sdim[k] = (int8_t)(k < x.rank ? g->E[e].src_dim[k] : -1);
-            x.ddim[k] = (int8_t)(k < x.rank ? g->E[e].dst_dim[k] : -1);
-        }
-        x.elems = g->E[e].elems;
-        x.sig_off = sig_off;
-        x.mat_off = g->volume ? g->mat_off[e] : 0;
-        sig_off += (uint64_t)g->K[x.src] + g->K[x.dst];
-    }
-    if (ne) std::memcpy(img + P.off_edge, des.data(), ne * sizeof(DevEdge));
-    if (g->overridden) {
-        std::memcpy(img + P.off_L, g->ov_layer.data(), g->ov_layer.size() * 8);
-        if (!g->ov_edge.empty()) std::memcpy(img + P.off_ovedge, g->ov_edge.data(), g->ov_edge.size() * 8);
-    }
-    std::memcpy(img + P.off_contrib, contrib.data(), contrib.size() * sizeof(Contrib));
-    std::vector<BacktrackDesc> bt(n);
-    uint32_t nlev = 0;
-    for (int i = n - 1; i >= 0; i--) {
-        const VPlan &vp = P.v[i];
-        BacktrackDesc &b = bt[i];
-        std::memset(&b, 0, sizeof b);
-        b.A = (const uint16_t *)(ws + P.off_A + vp.A_off);
-        b.vi = (uint32_t)vp.vi;
-        b.K = vp.K;
-        b.m = (uint32_t)vp.layout.size();
-        for (size_t k = 0; k < vp.layout.size(); k++) {
-            b.dig[k] = (uint32_t)vp.layout[k];
-            b.stride[k] = vp.stride[k];
-        }
-        // the configuration of v_i needs those of D(i), all later in the order
-        for (int u : vp.D) b.level = std::max(b.level, bt[P.pos[u]].level + 1);
-        nlev = std::max(nlev, b.level + 1);
-    }
-    std::memcpy(img + P.off_bt, bt.data(), n * sizeof(BacktrackDesc));
-
-    // ---- batches: per launch slot, one prep launch, one fill launch per kernel
-    // variant and one split-reduction launch
-    PrepArgs *hp = (PrepArgs *)(img + P.off_desc);
-    RowsArgs *hr = (RowsArgs *)(hp + n);
-    GenericArgs *hg = (GenericArgs *)(hr + n);
-    ReduceArgs *hd = (ReduceArgs *)(hg + n);
-    DirectArgs *hx = (DirectArgs *)(hd + n);
-    for (int i = 0; i < n; i++) {
-        hp[i] = launches[i].prep;
-        hr[i] = launches[i].ra;
-        hg[i] = launches[i].ga;
-        hd[i] = launches[i].red;
-        hx[i] = launches[i].da;
-    }
-    BatchEntry *hbe = (BatchEntry *)(img + P.off_batch);
-    std::vector<Batch> batches;
-    uint32_t nbe = 0;
-    // launch groups in enqueue order: the slots (levels, or positions); with
-    // lanes, each level's vertices of lane 0, then lane 1, then lane 2
-    std::vector<std::vector<int>> groups;
-    std::vector<int> group_lane;
-    const int nl = use_lanes ? kLanes : 1;
-    if (!use_flow) {
-        groups.assign((size_t)P.nslots * nl, {});
-        group_lane.assign(groups.size(), 0);
-        for (int i = 0; i < n; i++) groups[(size_t)P.v[i].slot * nl + (use_lanes ? P.v[i].lane : 0)].push_back(i);
-        for (size_t k = 0; k < groups.size(); k++) group_lane[k] = (int)(k % nl);
-    }
-    int cur_lane = 0, cur_group = 0;
-    auto add_batch = [&](Batch::Kind kind, uint32_t variant, const std::vector<int> &members,
-                         uint32_t (*nblk)(const Launch<KeyT> &)) {
-        if (members.empty()) return;
-        Batch b{kind, cur_lane, cur_group, variant, nbe, 0, 0};
-        for (int i : members) {
-            hbe[nbe].pos = (uint32_t)i;
-            hbe[nbe].first = b.blocks;
-            hbe[nbe].prio = use_lanes && P.v[i].lane == 1 ? 1u : 0u;
-            hbe[nbe].pad = 0;
-            b.blocks += nblk(launches[i]);
-            nbe++;
-            b.nentries++;
-        }
-        batches.push_back(b);
-    };
-    // per-group scratch, reused across groups (cleared, capacity kept)
-    std::vector<int> prepped, direct, grp;
-    std::vector<std::pair<uint32_t, int>> rows, gens, reds;
-    std::map<uint32_t, int> shape_dom;   // TZ * 4 + TM -> largest vertex of the group
-    for (size_t sl = 0; sl < groups.size(); sl++) {
-        const auto &mem = groups[sl];
-        cur_lane = group_lane[sl];
-        cur_group = (int)sl;
-        prepped.clear();
-        direct.clear();
-        for (int i : mem) (launches[i].direct ? direct : prepped).push_back(i);
-        add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
-        add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
-        rows.clear();
-        gens.clear();
-        reds.clear();
-        // fp64 keys: the row-term count is a kernel template parameter; a
-        // small vertex with fewer row terms than the largest vertex of its tile
-        // shape in this group gets zero terms appended (each lane adds the
-        // zero key once per c) and joins that vertex's launch
-        shape_dom.clear();
-        for (int i : prepped)
-            if (launches[i].rows && std::is_same<KeyT, double>::value) {
-                auto it = shape_dom.find(P.v[i].TZ * 4 + P.v[i].TM);
-                if (it == shape_dom.end()) shape_dom[P.v[i].TZ * 4 + P.v[i].TM] = i;
-                else if (P.v[i].est_us > P.v[it->second].est_us) it->second = i;
-            }
-        for (int i : prepped) {
-            const Launch<KeyT> &L = launches[i];
-            if (L.rows) {
-                uint32_t na = std::is_same<KeyT, double>::value ? std::min<uint32_t>(L.ra.na, 4) : 7;
-                if (std::is_same<KeyT, double>::value && !use_flow) {
-                    const int d = shape_dom[P.v[i].TZ * 4 + P.v[i].TM];
-                    const uint32_t nd = std::min<uint32_t>(launches[d].ra.na, 4);
-                    if (d != i && na < nd && P.v[i].est_us <= 0.5 * P.v[d].est_us) {
-                        RowsArgs &ra = hr[i];
-                        for (uint32_t t = na; t < nd; t++) {
-                            std::memset(&ra.a[t], 0, sizeof ra.a[t]);
-                            ra.a[t].ptr = ws + P.off_zero;
-                            ra.a[t].bytes = 8;
-                        }
-                        na = nd;
-                    }
-                }
-                rows.push_back({(P.v[i].TZ * 4 + P.v[i].TM) * 8 + na, i});
-                if (P.v[i].nsplit > 1) reds.push_back({0, i});
-            } else {
-                gens.push_back({L.ga.nt <= 6 ? L.ga.nt : 0, i});
-            }
-        }
-        std::stable_sort(rows.begin(), rows.end(),
-                         [](const std::pair<uint32_t, int> &a, const std::pair<uint32_t, int> &b) { return a.first < b.first; });
-        std::stable_sort(gens.begin(), gens.end(),
-                         [](const std::pair<uint32_t, int> &a, const std::pair<uint32_t, int> &b) { return a.first < b.first; });
-        for (size_t k = 0; k < rows.size();) {
-            grp.clear();
-            size_t k2 = k;
-            for (; k2 < rows.size() && rows[k2].first == rows[k].first; k2++) grp.push_back(rows[k2].second);
-            add_batch(Batch::kRows, rows[k].first, grp, [](const Launch<KeyT> &L) { return L.ra.nblocks_launched; });
-            k = k2;
-        }
-        for (size_t k = 0; k < gens.size();) {
-            grp.clear();
-            size_t k2 = k;
-            for (; k2 < gens.size() && gens[k2].first == gens[k].first; k2++) grp.push_back(gens[k2].second);
-            add_batch(Batch::kGeneric, gens[k].first, grp, [](const Launch<KeyT> &L) { return L.ga.nblk; });
-            k = k2;
-        }
-        grp.clear();
-        for (auto &x : reds) grp.push_back(x.second);
-        add_batch(Batch::kReduce, 0, grp, [](const Launch<KeyT> &L) { return L.red.nblk; });
-    }
-    if (nbe > 3 * (uint64_t)n) return fail(g, PASE_ERR_INTERNAL, "batch table overflow");
-    for (const Batch &b : batches)
-        if (b.blocks == 0 || b.blocks > 0x7fffffffu) return fail(g, PASE_ERR_TOO_LARGE, "launch grid size");
-
-    // ---- dataflow tables: control block and done counters (zeroed), then the
-    // segments of both queues and their dependencies
-    FlowPlan fp;
-    FlowArgs fa;
-    std::memset(&fa, 0, sizeof fa);
-    if (use_flow) {
-        st = build_flow<KeyT>(g, launches, fp);
-        if (st != PASE_OK) return st;
-        const uint64_t ctl_bytes = sizeof(FlowCtl) + (4ull * n + 15) / 16 * 16;
-        const uint64_t need = ctl_bytes + (fp.seg[0].size() + fp.seg[1].size()) * sizeof(Seg) +
-                              fp.deps.size() * sizeof(SegDep);
-        if (need > P.flow_bytes) return fail(g, PASE_ERR_INTERNAL, "dataflow table overflow");
-        char *fimg = img + P.off_flow;
-        std::memset(fimg, 0, ctl_bytes);
-        uint64_t o = ctl_bytes;
-        for (int q = 0; q < 2; q++) {
-            if (!fp.seg[q].empty()) std::memcpy(fimg + o, fp.seg[q].data(), fp.seg[q].size() * sizeof(Seg));
-            fa.seg[q] = (const Seg *)(ws + P.off_flow + o);
-            fa.nseg[q] = (uint32_t)fp.seg[q].size();
-            fa.nitems[q] = fp.nitems[q];
-            o += fp.seg[q].size() * sizeof(Seg);
-        }
-        if (!fp.deps.empty()) std::memcpy(fimg + o, fp.deps.data(), fp.deps.size() * sizeof(SegDep));
-        fa.deps = (const SegDep *)(ws + P.off_flow + o);
-        fa.ctl = (FlowCtl *)(ws + P.off_flow);
-        fa.done = (uint32_t *)(ws + P.off_flow + sizeof(FlowCtl));
-    }
-
-    if (upload_costs) {
+    SearchImage si;
+    pase_status st = build_image<KeyT>(g, ws, img, si);
+    if (st != PASE_OK) return st;
+    g->stats.setup_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_setup).count();
+    const std::vector<Batch> &batches = si.batches;
+    if (si.upload_costs) {
         HIPCHK(hipMemcpyAsync(ws, img, P.off_cfg, hipMemcpyHostToDevice, s));
     } else {
         HIPCHK(hipMemcpyAsync(ws, img, P.off_L, hipMemcpyHostToDevice, s));
@@ -1221,23 +457,26 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         if (g->profile == 1) return b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
         return g->profile == 2 && b.kind == Batch::kRows && b.variant / 32 != 1;
     };
-    uint32_t nfill = use_flow ? 1 : 0;
+    uint32_t nfill = 0;
     for (const Batch &b : batches) nfill += timed(b);
     // the timing events only time the launches they are attached to (read
     // after the search's final synchronization), so they skip the
     // system-scope cache write-back and invalidation a default event performs
     // around the dispatch -- a few microseconds per timed launch otherwise
-    if (g->profile && d->ev.size() < 2 * (size_t)nfill) {
+    if (g->profile) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
             hipEvent_t e;
             HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
             d->ev.push_back(e);
         }
+        for (auto &e : d->phase_ev)
+            if (!e) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+        HIPCHK(hipEventRecord(d->phase_ev[0], s));
     }
     uint32_t launches_n = 0;
     if (!g->overridden) {
-        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(loff + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
-                           dE, (uint32_t)ne, dex, dL, dls, dsig, loff, P.sig_count, g->r);
+        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(si.nL + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
+                           dE, (uint32_t)ne, dex, dL, dls, dsig, si.nL, P.sig_count, g->r);
         launches_n++;
         if (g->volume && g->mat_total) {
             hipLaunchKernelGGL(k_edge_volume, dim3(grid_for(g->mat_total, 256, 65535)), dim3(256), 0, s, dV, dE,
@@ -1245,61 +484,24 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             launches_n++;
         }
     }
-    std::vector<int> fill_of(n, -1);   // fill batch of each vertex (profiling)
+    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[1], s));
+    std::vector<int> fill_of(n, -1);   // timed fill batch of each vertex (profiling)
     uint32_t fb = 0;
-    if (use_flow) {
-        // every resident workgroup is a worker; at least one per queue
-        int &grid = d->flow_grid[std::is_same<KeyT, double>::value ? 0 : 1];
-        if (grid == 0) {
-            int dev = 0, cus = 0, per_cu = 0;
-            HIPCHK(hipGetDevice(&dev));
-            HIPCHK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-            HIPCHK(hipDeviceGetAttribute(&d->wall_khz, hipDeviceAttributeWallClockRate, dev));
-            HIPCHK(flow_occupancy<KeyT>(&per_cu));
-            grid = std::max(2, cus * std::max(1, per_cu));
-        }
-        const uint64_t items = (uint64_t)fp.nitems[0] + fp.nitems[1];
-        const uint32_t G = (uint32_t)std::max<uint64_t>(2, std::min<uint64_t>((uint64_t)grid, items));
-        const uint32_t lw = g->lat_workers ? g->lat_workers : G / 16;
-        fa.lat_workers = std::max(1u, std::min(G - 1, lw));
-        fa.prep = dp;
-        fa.rows = dr;
-        fa.gen = dg;
-        fa.red = dd;
-        fa.V = dV;
-        fa.E = dE;
-        fa.L = dL;
-        fa.lsum = dls;
-        fa.sig = dsig;
-        fa.cb = dC;
-        fa.r = g->r;
-        // a dependency wait gives up after 10 s plus 100x the planned search time
-        double est = 0;
-        for (int i = 0; i < n; i++) est += P.v[i].est_us;
-        const double hz = 1e3 * (d->wall_khz > 0 ? d->wall_khz : 100000);
-        fa.timeout_ticks = (uint64_t)(hz * (10.0 + 100.0 * est * 1e-6));
-        hipEvent_t e0 = g->profile ? d->ev[0] : nullptr, e1 = g->profile ? d->ev[1] : nullptr;
-        HIPCHK(flow_launch<KeyT>(fa, G, s, e0, e1));
-        g->stats.flow_grid = G;
-        g->stats.flow_lat_workers = fa.lat_workers;
-        g->stats.flow_items = items;
-        for (int i = 0; i < n; i++) fill_of[i] = 0;
-        fb = 1;
-        launches_n++;
-    }
-    // lanes: every lane starts after the upload and the cost tables; a group
-    // (level, lane) waits, per other lane, for the latest level of that lane
-    // whose tables it reads (always a lower level: the event is recorded
-    // already); the caller's stream joins every lane at the end
-    hipStream_t lane_stream[kLanes] = {s, s, s};
-    // event of (lane l, level L): lane_ev[1 + L * kLanes + l]; lane_ev[0]: start
+    // bulk lane schedule: the bulk stream starts after the upload and the cost
+    // tables; a group (slot, lane) waits, for the other lane, for the latest
+    // slot of that lane whose tables it reads (always an earlier slot: its
+    // event is recorded already); the caller's stream joins the bulk stream at
+    // the end
+    const int nl = si.lanes ? kLanes : 1;
+    hipStream_t lane_stream[kLanes] = {s, s};
+    // event of (lane l, slot L): lane_ev[1 + L * kLanes + l]; lane_ev[0]: start
     auto lev = [&](int l, int L) { return d->lane_ev[1 + (size_t)L * kLanes + l]; };
-    std::vector<std::vector<int>> waited(kLanes, std::vector<int>(kLanes, -1));
-    if (use_lanes) {
-        for (int l = 1; l < kLanes; l++) {
-            if (!d->side[l - 1]) HIPCHK(hipStreamCreateWithFlags(&d->side[l - 1], hipStreamNonBlocking));
-            lane_stream[l] = d->side[l - 1];
-        }
+    int waited[kLanes][kLanes];
+    for (auto &row : waited)
+        for (int &w : row) w = -1;
+    if (si.lanes) {
+        if (!d->side) HIPCHK(hipStreamCreateWithFlags(&d->side, hipStreamNonBlocking));
+        lane_stream[1] = d->side;
         const size_t nev = 1 + (size_t)(P.nslots + 1) * kLanes;
         while (d->lane_ev.size() < nev) {
             hipEvent_t e;
@@ -1307,24 +509,25 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             d->lane_ev.push_back(e);
         }
         HIPCHK(hipEventRecord(d->lane_ev[0], s));
-        for (int l = 1; l < kLanes; l++) HIPCHK(hipStreamWaitEvent(lane_stream[l], d->lane_ev[0], 0));
+        HIPCHK(hipStreamWaitEvent(lane_stream[1], d->lane_ev[0], 0));
     }
     int prev_group = -1;
     for (const Batch &b : batches) {
         const BatchEntry *e = dbe + b.entry0;
         hipStream_t bs = s;
-        if (use_lanes) {
+        if (si.lanes) {
             if (b.group != prev_group) {
                 if (prev_group >= 0)
-                    HIPCHK(hipEventRecord(lev(group_lane[prev_group], prev_group / nl), lane_stream[group_lane[prev_group]]));
-                std::vector<int> need(kLanes, -1);
-                for (int i : groups[b.group])
+                    HIPCHK(hipEventRecord(lev(si.group_lane[prev_group], prev_group / nl),
+                                          lane_stream[si.group_lane[prev_group]]));
+                int need[kLanes] = {-1, -1};
+                for (int i : si.groups[b.group])
                     for (const auto &t : P.v[i].terms)
                         if (P.v[t.j].lane != b.lane) need[P.v[t.j].lane] = std::max(need[P.v[t.j].lane], P.v[t.j].slot);
                 for (int l = 0; l < kLanes; l++)
                     if (need[l] > waited[b.lane][l]) {
-                        if (need[l] >= b.group / nl)   // a table is read at a later level only
-                            return fail(g, PASE_ERR_INTERNAL, "lane wait on a level not enqueued yet");
+                        if (need[l] >= b.group / nl)   // a table is read at a later slot only
+                            return fail(g, PASE_ERR_INTERNAL, "lane wait on a slot not enqueued yet");
                         HIPCHK(hipStreamWaitEvent(lane_stream[b.lane], lev(l, need[l]), 0));
                         waited[b.lane][l] = need[l];
                     }
@@ -1345,7 +548,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             // (events attached to the dispatch, no extra packets in the stream)
             const bool tb = timed(b);
             if (tb)
-                for (uint32_t k = 0; k < b.nentries; k++) fill_of[hbe[b.entry0 + k].pos] = (int)fb;
+                for (uint32_t k = 0; k < b.nentries; k++) fill_of[((const BatchEntry *)(img + P.off_batch))[b.entry0 + k].pos] = (int)fb;
             hipEvent_t e0 = tb ? d->ev[2 * fb] : nullptr, e1 = tb ? d->ev[2 * fb + 1] : nullptr;
             if (b.kind == Batch::kRows) {
                 if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
@@ -1365,22 +568,21 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         }
         launches_n++;
     }
-    if (use_lanes) {
-        // join: the caller's stream waits for the last work of every other lane
-        for (int l = 1; l < kLanes; l++) {
-            HIPCHK(hipEventRecord(lev(l, P.nslots), lane_stream[l]));
-            HIPCHK(hipStreamWaitEvent(s, lev(l, P.nslots), 0));
-        }
+    if (si.lanes) {
+        // join: the caller's stream waits for the last work of the bulk stream
+        HIPCHK(hipEventRecord(lev(1, P.nslots), lane_stream[1]));
+        HIPCHK(hipStreamWaitEvent(s, lev(1, P.nslots), 0));
     }
-    const uint32_t *flow_err = use_flow ? &fa.ctl->error : nullptr;
+    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[2], s));
     if ((uint32_t)n <= kMaxBacktrackThreads)
         hipLaunchKernelGGL((k_backtrack_levels<KeyT>), dim3(1), dim3((n + 63) / 64 * 64), 0, s,
-                           (const BacktrackDesc *)(ws + P.off_bt), (uint32_t)n, nlev,
-                           (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout, flow_err);
+                           (const BacktrackDesc *)(ws + P.off_bt), (uint32_t)n, si.nlev,
+                           (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
     else
         hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
-                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout, flow_err);
+                           (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
     launches_n++;
+    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[3], s));
     HIPCHK(hipGetLastError());
     // the staging buffer is reused for the results: the stream runs the
     // upload before these copies
@@ -1390,25 +592,22 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     HIPCHK(hipStreamSynchronize(s));
     SearchOut so;
     std::memcpy(&so, host_out, sizeof so);
-    if (so.status & 1u) return fail(g, PASE_ERR_INTERNAL, "a dependency wait of the dataflow launch timed out");
-    if (so.status & 2u) return fail(g, PASE_ERR_INTERNAL, "the dataflow launch met an item it cannot run");
     if (so.status) return fail(g, PASE_ERR_INTERNAL, "back-substitution read an argmin out of range");
     *min_cost = so.min_cost;
     std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
-    if (!use_flow) g->stats.flow_grid = g->stats.flow_lat_workers = 0, g->stats.flow_items = 0;
-    g->stats.schedule = use_flow ? 3u : use_lanes ? (uint32_t)g->schedule : (P.by_level ? 0u : 1u);
+    g->stats.schedule = si.lanes ? (uint32_t)kSchedBulk : (P.by_level ? (uint32_t)kSchedLevel : (uint32_t)kSchedSeq);
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
+    g->stats.cost_tables_ms = g->stats.fill_span_ms = g->stats.backtrack_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;
-    if (g->profile && use_flow) {
-        float ms = 0.f;
-        HIPCHK(hipEventElapsedTime(&ms, d->ev[0], d->ev[1]));
-        g->stats.fill_ms = g->stats.rows_fill_ms = ms;
-        g->stats.rows_launches = 1;
-        for (int i = 0; i < n; i++) P.v[i].fill_ms = 0.0;
-    } else if (g->profile) {
+    if (g->profile) {
+        float ph[3] = {0.f, 0.f, 0.f};
+        for (int k = 0; k < 3; k++) HIPCHK(hipEventElapsedTime(&ph[k], d->phase_ev[k], d->phase_ev[k + 1]));
+        g->stats.cost_tables_ms = ph[0];
+        g->stats.fill_span_ms = ph[1];
+        g->stats.backtrack_ms = ph[2];
         std::vector<float> ms(fb, 0.f);
         uint32_t k = 0;
         for (const Batch &b : batches) {
@@ -1555,34 +754,3 @@ pase_status device_edge_costs(pase_graph_t g, uint32_t e, uint64_t *out) {
 }
 
 }  // namespace pase
-
-template <typename KeyT>
-static pase_status flow_check_t(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
-                                uint64_t *items) {
-    // descriptors hold device addresses only: any base will do, nothing is read through it
-    char *fake_ws = (char *)(uintptr_t)(1ull << 40);
-    std::vector<Launch<KeyT>> launches;
-    std::vector<Contrib> contrib;
-    pase_status st = build_launches<KeyT>(g, fake_ws, launches, contrib);
-    if (st != PASE_OK) return st;
-    FlowPlan fp;
-    st = build_flow<KeyT>(g, launches, fp);
-    if (st != PASE_OK) return st;
-    *items = (uint64_t)fp.nitems[0] + fp.nitems[1];
-    return flow_simulate(g, fp, workers, lat_workers, seed);
-}
-
-extern "C" pase_status pase_flow_check(pase_graph_t g, uint32_t workers, uint32_t lat_workers, uint64_t seed,
-                                       uint64_t *items) {
-    if (!g || !items || workers < 2 || lat_workers < 1 || lat_workers >= workers)
-        return g ? fail(g, PASE_ERR_INVALID_ARGUMENT, "need items, workers >= 2, 1 <= lat_workers < workers")
-                 : PASE_ERR_INVALID_ARGUMENT;
-    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "call pase_enumerate_configs first");
-    if (!g->plan.resident || g->schedule != kSchedFlow)
-        return fail(g, PASE_ERR_BAD_STATE, "the plan does not use the dataflow schedule");
-    pase_status st;
-    const uint32_t kt = choose_key_type(g, &st);
-    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
-    return kt == 0 ? flow_check_t<double>(g, workers, lat_workers, seed, items)
-                   : flow_check_t<uint64_t>(g, workers, lat_workers, seed, items);
-}

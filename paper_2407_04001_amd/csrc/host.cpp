@@ -4,6 +4,7 @@
 // layout.  No HIP calls here: everything is pure host computation so it can be
 // exercised without a GPU.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstring>
 #include <numeric>
@@ -370,69 +371,29 @@ TileTime tile_time_cached(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uin
 
 }  // namespace
 
-// Lane schedule.  The tables form an in-tree: every table but the last has
-// exactly one reader, a later position.  The tree is cut into chains: each
-// vertex continues the chain of its reader when it is the reader's longest
-// producer path (planned fill time plus a launch latency per vertex), and
-// heads a chain of its own otherwise.  The chain through the root runs on
-// lane 0 (the caller's stream); the longest other chain -- in a Transformer
-// graph, the encoder: a long run of small dependent vertices -- on lane 1,
-// whose waves issue at the highest priority; every other chain with
-// substantial work on lane 2; a chain with little work follows the lane of
-// the vertex that reads it.  Lanes are streams: the latency-bound chain then
-// no longer queues behind large vertices it does not depend on.
-static void assign_lanes(Plan &P) {
-    const int n = (int)P.v.size();
-    constexpr double kLaunchUs = 10.0, kLongUs = 200.0, kWorkUs = 50.0;
-    std::vector<double> top(n, 0.0);   // largest time of a producer path ending at i
-    for (int i = 0; i < n; i++) {
-        double m = 0;
-        for (const auto &t : P.v[i].terms) m = std::max(m, top[t.j]);
-        top[i] = m + P.v[i].est_us + kLaunchUs;
-    }
-    std::vector<int> chain(n, -1), head;
-    std::vector<double> work;
-    for (int x = n - 1; x >= 0; x--) {
-        if (chain[x] < 0) {
-            chain[x] = (int)head.size();
-            head.push_back(x);
-            work.push_back(0.0);
-        }
-        work[chain[x]] += P.v[x].est_us;
-        int best = -1;
-        for (const auto &t : P.v[x].terms)
-            if (best < 0 || top[t.j] > top[best]) best = t.j;
-        if (best >= 0) chain[best] = chain[x];
-    }
-    // chains are numbered by decreasing head position, so the chain of a
-    // head's reader always has its lane already
-    const int nc = (int)head.size();
-    std::vector<int> lane(nc, 0);
-    int second = -1;
-    for (int c = 1; c < nc; c++)
-        if (top[head[c]] >= kLongUs && (second < 0 || top[head[c]] > top[head[second]])) second = c;
-    for (int c = 1; c < nc; c++)
-        lane[c] = c == second ? 1 : work[c] >= kWorkUs ? 2 : lane[chain[P.v[head[c]].consumer]];
-    for (int i = 0; i < n; i++) P.v[i].lane = lane[chain[i]];
-}
-
 // Bulk lane schedule.  Row-kernel vertices planned to take at least bulk_us
-// (the large fills, which keep the whole GPU busy on their own) run on lane 2,
-// and so does every vertex that reads a table of lane 2 (it has to wait for
-// that fill anyway); every other vertex -- one whose producers are all small
-// -- runs on lane 1, level by level, at the highest wave priority.  A level
-// group of lane 1 then never waits for a large fill, so a chain of small
-// dependent vertices runs beside the large fills instead of after them.
-// Producers precede their reader in the sequence, so one pass suffices.
+// (the large fills, which keep the whole GPU busy on their own) run on lane 1
+// (a stream of its own), and so does every vertex that reads a table of lane 1
+// (it has to wait for that fill anyway); every other vertex -- one whose
+// producers are all small -- runs on lane 0 (the caller's stream), level by
+// level, at the highest wave priority.  A level group of lane 0 then never
+// waits for a large fill, so a chain of small dependent vertices runs beside
+// the large fills instead of after them.  Producers precede their reader in
+// the sequence, so one pass suffices.
 static void assign_bulk_lanes(Plan &P, double bulk_us) {
     for (auto &vp : P.v) {
         bool bulk = vp.kernel == kRows && vp.est_us >= bulk_us;
-        for (const auto &t : vp.terms) bulk |= P.v[t.j].lane == 2;
-        vp.lane = bulk ? 2 : 1;
+        for (const auto &t : vp.terms) bulk |= P.v[t.j].lane == 1;
+        vp.lane = bulk ? 1 : 0;
     }
 }
 
+static double ms_since(std::chrono::steady_clock::time_point t0) {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+}
+
 static pase_status build_plan(pase_graph_t g) {
+    const auto t0 = std::chrono::steady_clock::now();
     const int n = (int)g->V.size();
     Plan &P = g->plan;
     P = Plan();
@@ -517,6 +478,8 @@ static pase_status build_plan(pase_graph_t g) {
         if (P.v[i].consumer < 0) return fail(g, PASE_ERR_INTERNAL, "table never read");
         P.v[i].out_shift = P.v[P.v[i].consumer].bits;
     }
+    g->stats.seq_ms = ms_since(t0);
+    const auto t1 = std::chrono::steady_clock::now();
     // dependency level: vertices of one level read no table of each other
     for (int i = 0; i < n; i++) {
         P.v[i].level = 0;
@@ -556,8 +519,7 @@ static pase_status build_plan(pase_graph_t g) {
         const uint32_t tile_cols = ftz ? ftz : g->tile_cols, tile_rows = ftm ? ftm : g->tile_rows;
         // small vertices: the direct fill (one launch, no prep blocks), whose
         // time is a launch plus the gather of every term of every cell
-        if (!ftz && g->direct_cells && g->kernel_mode == 0 && g->schedule != kSchedFlow &&
-            vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
+        if (!ftz && g->direct_cells && g->kernel_mode == 0 && vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
             vp.kernel = kDirect;
             vp.est_us = 4.0 + (double)vp.N * vp.K * (1.0 + vp.edges.size() + vp.terms.size()) / 4e5;
             vp.layout = gather_layout(vp);
@@ -627,10 +589,6 @@ static pase_status build_plan(pase_graph_t g) {
                         if (tile_rows && tm != tile_rows) continue;
                         // more than 32 accumulators per lane cost waves (VGPRs)
                         if (!tile_rows && !tile_cols && tz * tm > 32) continue;
-                        // the dataflow kernel carries the variants of modest register need
-                        if (g->schedule == kSchedFlow && !tile_rows && !tile_cols &&
-                            !flow_rows_ok(false, tz, tm, std::min<uint32_t>(na, 4)))
-                            continue;
                         const TileTime tt = tile_time_cached(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts,
                                                              g->c_splits, stream_bytes);
                         if (!rc.ok || tt.us < rc.cost) {
@@ -685,7 +643,7 @@ static pase_status build_plan(pase_graph_t g) {
     // when its fill then stays under half of that vertex's, so that the two
     // share a launch (the small one's workgroups come first and finish inside
     // the large one's) instead of adding a latency-bound launch of its own.
-    // Level schedule only: the lanes split a level over streams.
+    // Level schedule only: the bulk lane splits a level over two streams.
     if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && g->kernel_mode == 0) {
         std::vector<int> dom((size_t)maxlev + 1, -1);
         for (int i = 0; i < n; i++) {
@@ -713,8 +671,9 @@ static pase_status build_plan(pase_graph_t g) {
         P.rows_cells += vp.N * vp.K;
         if (vp.z < 0) P.stream_cells += vp.N * vp.K;
     }
-    assign_lanes(P);
+    for (auto &vp : P.v) vp.lane = 0;
     if (g->schedule == kSchedBulk) assign_bulk_lanes(P, (double)g->bulk_us);
+    g->stats.plan_ms = ms_since(t1);
     return PASE_OK;
 }
 
@@ -727,25 +686,28 @@ static pase_status build_plan(pase_graph_t g) {
 enum LayoutMode { kLayoutResident = 0, kLayoutSeq = 1, kLayoutLevel = 2 };
 static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode);
 
-// The two-lane and dataflow schedules run vertices concurrently and need
+// The bulk lane schedule runs vertices of two streams concurrently and needs
 // every table and scratch buffer resident at once; when that exceeds the
 // budget, or for the level schedule, tables share memory by lifetimes over
 // levels; when even that does not fit, one vertex at a time.
 static pase_status layout_memory(pase_graph_t g) {
-    if ((g->schedule == kSchedLanes || g->schedule == kSchedFlow || g->schedule == kSchedBulk) &&
-        layout_memory_mode(g, kLayoutResident) == PASE_OK)
-        return PASE_OK;
-    if (g->schedule != kSchedSeq && layout_memory_mode(g, kLayoutLevel) == PASE_OK) return PASE_OK;
-    return layout_memory_mode(g, kLayoutSeq);
+    const auto t0 = std::chrono::steady_clock::now();
+    pase_status st = PASE_ERR_TOO_LARGE;
+    if (g->schedule == kSchedBulk) st = layout_memory_mode(g, kLayoutResident);
+    if (st != PASE_OK && g->schedule != kSchedSeq) st = layout_memory_mode(g, kLayoutLevel);
+    if (st != PASE_OK) st = layout_memory_mode(g, kLayoutSeq);
+    g->stats.plan_ms += ms_since(t0);
+    g->stats.host_plan_ms = g->stats.seq_ms + g->stats.plan_ms;
+    return st;
 }
 
 static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     Plan &P = g->plan;
     // resident: vertices may run in any order the dependencies allow, so
     // every vertex has scratch of its own and no table memory is reused
-    const bool flow = mode == kLayoutResident, by_level = mode != kLayoutSeq;
+    const bool resident = mode == kLayoutResident, by_level = mode != kLayoutSeq;
     P.by_level = by_level;
-    P.resident = flow;
+    P.resident = resident;
     P.nslots = 0;
     for (auto &vp : P.v) {
         vp.slot = by_level ? vp.level : (int)(&vp - &P.v[0]);
@@ -786,16 +748,6 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
                               sizeof(DirectArgs)), A);
     P.off_batch = off;
     off = align_up(off + 3 * (uint64_t)n * sizeof(BatchEntry), A);
-    // dataflow tables: control block, done counters, segments (prep, fill,
-    // reduce per vertex, two queues) and their dependencies
-    P.off_flow = off;
-    P.flow_bytes = 0;
-    if (flow) {
-        uint64_t ndeps = 0;
-        for (const auto &vp : P.v) ndeps += vp.terms.size() + 2;
-        P.flow_bytes = sizeof(FlowCtl) + align_up(4ull * n, 16) + 3ull * n * sizeof(Seg) + ndeps * sizeof(SegDep);
-        off = align_up(off + P.flow_bytes, A);
-    }
     // one zero key: the row term that pads a row-kernel vertex up to the
     // row-term count of the launch it shares (uploaded zeroed with the rest)
     P.off_zero = off;
@@ -814,7 +766,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     struct Iv { int i, s, e; uint64_t size; };
     std::vector<Iv> iv;
     for (int i = 0; i < n; i++) {
-        int end = (flow || g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
+        int end = (resident || g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
         iv.push_back({i, P.v[i].slot, end, align_up(P.v[i].N * 8, A)});
     }
     std::vector<int> order(n);
@@ -861,8 +813,8 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
         }   // the direct fill needs no prep blocks and no split scratch
         vp.block_elems = e;
-        // (the dataflow schedule keeps every vertex's scratch: one slot for all)
-        const int sl = flow ? 0 : vp.slot;
+        // (the resident layout keeps every vertex's scratch: one slot for all)
+        const int sl = resident ? 0 : vp.slot;
         vp.block_off = bsum[sl];
         vp.partial_off = psum[sl];
         bsum[sl] += align_up(e * 8, A);
@@ -1069,7 +1021,8 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->profile = (int)value;
         break;
     case PASE_OPT_SCHEDULE:
-        if (value > 4) return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 2, 3 or 4");
+        if (value != kSchedLevel && value != kSchedSeq && value != kSchedBulk)
+            return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1 or 4");
         g->schedule = (int)value;
         break;
     case PASE_OPT_TILE_COLS:
@@ -1085,10 +1038,6 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value != 0 && value != 1 && value != 2 && value != 4)
             return fail(g, PASE_ERR_INVALID_ARGUMENT, "tile parts 0, 1, 2 or 4");
         g->tile_parts = (uint32_t)value;
-        break;
-    case PASE_OPT_LATENCY_WORKERS:
-        if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "latency workers <= 65535");
-        g->lat_workers = (uint32_t)value;
         break;
     case PASE_OPT_ORDER:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "order 0 or 1");

@@ -99,7 +99,7 @@ struct PrepArgs {
 struct BatchEntry {
     uint32_t pos;
     uint32_t first;
-    uint32_t prio;            // 1: the latency lane's work -- its waves issue before others
+    uint32_t prio;            // 1: the bulk lane schedule's small vertices -- their waves issue first
     uint32_t pad;
 };
 
@@ -185,58 +185,12 @@ constexpr uint32_t kMaxBacktrackThreads = 1024;   // one thread per position
 
 struct SearchOut {            // written by the back-substitution kernel
     uint64_t min_cost;
-    uint32_t status;          // 0 = ok; bits: 1, 2 = dataflow error word, 4 = an argmin out of range
+    uint32_t status;          // 0 = ok; 4 = an argmin out of range
     uint32_t pad;
 };
-
-// ------------------------------------------------------------------ dataflow schedule
-// One persistent launch runs every prep, fill and split-reduction workgroup of
-// a search ("items").  Items are grouped in segments (one segment = the
-// workgroups one of those launches would have had) and handed out by two
-// ticket queues: the latency queue (vertices on the dependency chains, small)
-// and the bulk queue (large vertices).  Both queues hand out their items in
-// one global order that is a topological order of the item dependencies, so
-// the smallest unfinished item can always run.  Position i counts its
-// finished items in done[i]; a segment waits until the counters it depends
-// on reach their targets.
-enum SegKind : uint32_t { kSegPrep = 0, kSegRows = 1, kSegGeneric = 2, kSegReduce = 3 };
-
-struct Seg {
-    uint32_t first;           // first ticket of the segment in its queue
-    uint32_t count;           // items
-    uint32_t kind;            // SegKind
-    uint32_t variant;         // rows: (TZ * 4 + TM) * 8 + NA; generic: NT (0 = runtime count)
-    uint32_t pos;             // sequence position (descriptor index and done counter)
-    uint32_t dep_begin, dep_end;   // range in the dependency array
-    uint32_t pad;
-};
-
-struct SegDep {
-    uint32_t counter;         // position whose done counter is waited for
-    uint32_t target;          // value it must reach
-};
-
-constexpr int kLatQ = 0, kBulkQ = 1;
 
 // PASE_OPT_SCHEDULE values
-enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedLanes = 2, kSchedFlow = 3, kSchedBulk = 4 };
-
-// Row-fill variants (columns per lane TZ, rows per lane TM, row terms NA) the
-// dataflow kernel carries: those that need at most ~96 VGPRs, so that the one
-// kernel keeps the occupancy (5 waves per SIMD) of the per-vertex launches of
-// the hot variants.  A plan using another variant runs the level schedule.
-constexpr bool flow_rows_ok(bool u64_keys, uint32_t TZ, uint32_t TM, uint32_t NA) {
-    if (u64_keys) return TM == 1 ? (TZ >= 8 && TZ <= 24) : TZ == 8;
-    if (TM == 1) return true;
-    if (TZ == 1) return NA <= 2;
-    return TZ <= 12 || (TZ <= 16 && NA <= 2);
-}
-
-struct FlowCtl {              // zeroed by the per-search upload
-    uint32_t head[2];         // next ticket of each queue
-    uint32_t error;           // 1: a dependency wait gave up (the result is invalid)
-    uint32_t pad;
-};
+enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedBulk = 4 };
 
 // ------------------------------------------------------------------ host plan
 struct TermRef {
@@ -274,8 +228,8 @@ struct VPlan {
     // schedule
     int level = 0;                  // dependency level: 1 + max level of the tables it reads
     int slot = 0;                   // launch slot: its level (level schedule) or its position
-    int lane = 0;                   // lane schedules: 0 = the caller's stream, 1 = the latency chain's, 2 = other
-                                    // (bulk schedule: 1 = every small vertex, 2 = the large fills)
+    int lane = 0;                   // bulk lane schedule: 0 = the caller's stream (small vertices, level
+                                    // by level), 1 = the bulk stream (the large fills and their readers)
 };
 
 struct Plan {
@@ -293,8 +247,6 @@ struct Plan {
     int nslots = 0;                 // launch slots (levels, or positions when sequential)
     bool by_level = false;          // the vertices of one dependency level share launches
     bool resident = false;          // every table and scratch buffer resident at once (no reuse)
-    uint64_t off_flow = 0;          // dataflow tables: control block, done counters, segments, deps
-    uint64_t flow_bytes = 0;
     uint64_t off_desc = 0, off_batch = 0;   // per-vertex launch descriptors, batch tables
 };
 
@@ -316,7 +268,6 @@ struct pase_graph_s {
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
     uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
-    uint32_t lat_workers = 0;       // dataflow latency workers, 0 = chosen
     int schedule = 0;               // pase_option PASE_OPT_SCHEDULE (SchedKind)
     int order_mode = 0;             // pase_option PASE_OPT_ORDER: 0 GenerateSeq, 1 breadth-first
     // configurations

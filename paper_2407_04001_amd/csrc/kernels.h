@@ -1,6 +1,5 @@
-// Device code shared by the kernels of libpase (gfx950): key arithmetic, the
-// device cost model, and the work of one workgroup of each kernel ("items"),
-// which the per-vertex launches and the one-launch dataflow schedule both run.
+// Device code of the kernels of libpase (gfx950): key arithmetic, the device
+// cost model, and the work of one workgroup of each kernel ("items").
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -212,9 +211,9 @@ __device__ __forceinline__ uint32_t batch_find(const BatchEntry *__restrict__ be
     return __builtin_amdgcn_readfirstlane(lo);
 }
 
-// Work of the latency lane (the chain of small dependent vertices of the lane
-// schedule) runs its waves at the highest issue priority: on a SIMD shared
-// with the long fills of another stream they then issue first.
+// The small vertices of the bulk lane schedule (the chains of dependent
+// vertices) run their waves at the highest issue priority: on a SIMD shared
+// with the long fills of the bulk stream they then issue first.
 __device__ __forceinline__ void set_priority(const BatchEntry &e) {
     if (e.prio) __builtin_amdgcn_s_setprio(3);
 }
@@ -724,72 +723,5 @@ __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, co
         }
     }
 }
-
-// ------------------------------------------------------------------ dataflow launch
-// One persistent launch runs the prep, fill and split-reduction workgroups of
-// every vertex (the "items" of the segments built on the host).  Thread 0 of
-// a workgroup takes a ticket, the workgroup waits until the item's
-// dependencies (done counters of earlier positions) are met, runs the item
-// exactly as the corresponding kernel's workgroup would, publishes its stores
-// at device scope and counts the item as done.
-//
-// Taking a ticket: a latency worker (workgroup index < lat_workers) takes the
-// next latency-queue item; any other workgroup takes the latency queue's head
-// item when its dependencies are already met (so idle throughput can serve a
-// wide latency-bound vertex), else the next bulk item.  A drained queue sends
-// its workers to the other one; the launch ends when both are drained.
-// Both queues hand out items in one global topological order and each has a
-// worker of its own, so the smallest unfinished item can always run.  A wait
-// that exceeds timeout_ticks (100 MHz real-time clock) sets the error word and
-// every later wait returns at once: the launch still drains, and the host
-// reports the search as failed.
-struct FlowArgs {
-    const Seg *seg[2];
-    uint32_t nseg[2];
-    uint32_t nitems[2];
-    const SegDep *deps;
-    FlowCtl *ctl;
-    uint32_t *done;
-    const PrepArgs *prep;
-    const RowsArgs *rows;
-    const GenericArgs *gen;
-    const ReduceArgs *red;
-    const DevVertex *V;
-    const DevEdge *E;
-    const uint64_t *L;
-    const uint8_t *lsum;
-    const uint64_t *sig;
-    const Contrib *cb;
-    uint64_t r;
-    uint64_t timeout_ticks;
-    uint32_t lat_workers;
-};
-
-__device__ __forceinline__ uint32_t load_counter(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint32_t seg_find(const Seg *seg, uint32_t nseg, uint32_t t) {
-    uint32_t lo = 0, hi = nseg;
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (seg[mid].first <= t) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
-__device__ __forceinline__ bool deps_met(const FlowArgs &f, const Seg &sg) {
-    for (uint32_t k = sg.dep_begin; k < sg.dep_end; k++)
-        if (load_counter(&f.done[f.deps[k].counter]) < f.deps[k].target) return false;
-    return true;
-}
-
-
-// Dataflow launch of the search (flow.hip): resident workgroups per compute
-// unit, and the launch itself.
-template <typename KeyT>
-hipError_t flow_occupancy(int *per_cu);
-template <typename KeyT>
-hipError_t flow_launch(const FlowArgs &f, uint32_t grid, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 }  // namespace pase

@@ -20,8 +20,9 @@ OK, INVALID_ARGUMENT, NOT_CONNECTED, BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMO
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STATE", 4: "OVERFLOW",
                 5: "TOO_LARGE", 6: "OUT_OF_MEMORY", 7: "HIP", 8: "INTERNAL"}
 (OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
- OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS, OPT_LATENCY_WORKERS,
- OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER, OPT_GRAD_SYNC, OPT_DIRECT_CELLS, OPT_BULK_US) = range(1, 18)
+ OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS) = range(1, 11)
+(OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER, OPT_GRAD_SYNC, OPT_DIRECT_CELLS, OPT_BULK_US) = range(12, 18)
+SCHEDULE_LEVEL, SCHEDULE_SEQUENTIAL, SCHEDULE_BULK = 0, 1, 4
 
 
 class VertexDesc(C.Structure):
@@ -46,7 +47,8 @@ class RunStats(C.Structure):
                 ("wall_ms", C.c_double), ("fill_ms", C.c_double), ("rows_fill_ms", C.c_double),
                 ("rows_launches", C.c_uint32), ("slots", C.c_uint32), ("stream_cells", C.c_uint64),
                 ("stream_fill_ms", C.c_double), ("stream_launches", C.c_uint32), ("schedule", C.c_uint32),
-                ("flow_grid", C.c_uint32), ("flow_lat_workers", C.c_uint32), ("flow_items", C.c_uint64)]
+                ("pad0", C.c_uint32), ("seq_ms", C.c_double), ("plan_ms", C.c_double), ("setup_ms", C.c_double),
+                ("cost_tables_ms", C.c_double), ("fill_span_ms", C.c_double), ("backtrack_ms", C.c_double)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -69,16 +71,18 @@ EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_e
            "pase_num_configs", "pase_config_splits", "pase_get_sequence", "pase_get_dependent_set",
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
-           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get", "pase_flow_check"]
+           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get"]
 
 _lib = None
 
 
-def load(path: str = LIB_PATH):
-    """Load libpase.so; raises if the HIP library has not been built."""
+def load(path: str | None = None):
+    """Load libpase.so (``LIB_PATH`` unless a path is given); raises if the
+    HIP library has not been built."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(f"libpase.so not found at {path}: build it with "
                           "`python -c 'import __graft_entry__ as g; g.build()'`")
@@ -105,7 +109,6 @@ def load(path: str = LIB_PATH):
         "pase_edge_costs": (st, [P, U32, P]),
         "pase_stats": (st, [P, P]),
         "pase_vertex_info_get": (st, [P, U32, P]),
-        "pase_flow_check": (st, [P, U32, U32, U64, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -259,12 +262,6 @@ def pase_vertex_info_get(h, v: int) -> dict:
     return x.as_dict()
 
 
-def pase_flow_check(h, workers: int, lat_workers: int, seed: int = 0) -> int:
-    items = C.c_uint64()
-    _check(h, load().pase_flow_check(h, int(workers), int(lat_workers), int(seed), C.byref(items)))
-    return items.value
-
-
 # ------------------------------------------------------------------ convenience wrapper
 class Graph:
     """A computation graph handle.  ``graph`` is a dict in the layout of
@@ -362,6 +359,3 @@ class Graph:
 
     def vertex_info(self, v: int) -> dict:
         return pase_vertex_info_get(self.h, v)
-
-    def flow_check(self, workers: int, lat_workers: int, seed: int = 0) -> int:
-        return pase_flow_check(self.h, workers, lat_workers, seed)

@@ -69,7 +69,7 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
-         parts=0, splits=0, lat_workers=0, all_integers=False, bf=False, volume=False, grad=False,
+         parts=0, splits=0, all_integers=False, bf=False, volume=False, grad=False,
          direct=0, bulk_us=None):
     """direct: PASE_OPT_DIRECT_CELLS (0 = off, so the tests aimed at the row and
     generic kernels keep them; None = the library's default)."""
@@ -80,7 +80,6 @@ def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=
     pg.set_option(P.OPT_TRANSFER, int(volume))
     pg.set_option(P.OPT_GRAD_SYNC, int(grad))
     pg.enumerate_configs(p or g["p"], all_integers=all_integers)
-    pg.set_option(P.OPT_LATENCY_WORKERS, lat_workers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
     pg.set_option(P.OPT_KEY_TYPE, key)
@@ -321,15 +320,14 @@ def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad
 
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
-                  lat_workers=0, p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None,
+                  p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None,
                   bulk_us=None):
     gold = _golden(name, seed, p, all_integers, bf, volume, grad)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
-        f"lat_workers={lat_workers} p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad} "
-        f"direct={direct}")
+        f"p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad} direct={direct}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
-                         lat_workers=lat_workers, all_integers=all_integers, bf=bf, volume=volume, grad=grad,
+                         all_integers=all_integers, bf=bf, volume=volume, grad=grad,
                          direct=direct, bulk_us=bulk_us)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
@@ -380,14 +378,6 @@ def test_sequential_schedule_against_golden(P, name):
 
 
 @pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
-def test_lane_schedule_against_golden(P, name):
-    """Chains of the tables' reader tree on three streams, every table
-    resident: the same answer as the level schedule."""
-    _check_golden(P, name, 0, keep=False, schedule=2)
-    _check_golden(P, name, 0, keep=True, samples=False, schedule=2)
-
-
-@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
 def test_bulk_lane_schedule_against_golden(P, name):
     """Large fills on a stream of their own, every other vertex level by
     level on a second one: the same answer as the level schedule, with the
@@ -404,33 +394,22 @@ def test_bulk_lane_assignment(P):
     pg, _, _ = _run(P, g, keep=False, schedule=4)
     assert pg.stats()["schedule"] == 4
     info = {v: pg.vertex_info(v) for v in range(len(g["vertices"]))}
-    bulk = {v for v, x in info.items() if x["lane"] == 2}
+    bulk = {v for v, x in info.items() if x["lane"] == 1}
     assert bulk and len(bulk) < len(info)
-    assert all(x["lane"] in (1, 2) for x in info.values())
+    assert all(x["lane"] in (0, 1) for x in info.values())
     for v, x in info.items():
         if x["kernel"] == 1 and x["cells"] >= 8e9:
             assert v in bulk, v
 
 
-@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
-@pytest.mark.parametrize("lat_workers", [0, 1, 65535])
-def test_dataflow_schedule_against_golden(P, name, lat_workers):
-    """The one-launch dataflow schedule with the default worker split, with
-    one latency worker, and with every workgroup but one serving the latency
-    queue first."""
-    _check_golden(P, name, 0, keep=True, samples=False, schedule=3, lat_workers=lat_workers)
-
-
 def test_workloads_run_the_requested_schedule(P):
-    """The workloads fit the resident layout: the lane and dataflow schedules
-    run as requested, and the lanes put chains of the Transformer off the
-    caller's stream."""
+    """The workloads fit the resident layout: every schedule runs as requested,
+    and the bulk lane puts the Transformer's large fills on the bulk stream."""
     for name in ("w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"):
         g = workload(name)
-        for sched in (0, 1, 2, 3, 4):
+        for sched in (0, 1, 4):
             pg, _, _ = _run(P, g, keep=False, schedule=sched)
             assert pg.stats()["schedule"] == sched, (name, sched)
-    pg, _, _ = _run(P, g, keep=False, schedule=2)
     lanes = [pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))]
     assert 0 < sum(1 for x in lanes if x) < len(lanes)
 
@@ -543,12 +522,12 @@ def test_all_integer_edge_cases(P):
 def test_all_integer_workloads_against_golden(P, name):
     """Full-size workloads at p = 12 with every integer split, against the
     oracle's stored results: default plan, generic kernel, uint64 keys, and
-    the sequential, lane and dataflow schedules."""
+    the sequential and bulk lane schedules."""
     _check_golden(P, name, 0, p=12, all_integers=True)
     if name == "w2_inception":
         _check_golden(P, name, 0, p=12, all_integers=True, kernel=1)
         _check_golden(P, name, 0, p=12, all_integers=True, key=1)
-        for sched in (1, 2, 3):
+        for sched in (1, 4):
             _check_golden(P, name, 0, p=12, all_integers=True, keep=False, schedule=sched)
 
 
@@ -605,10 +584,10 @@ def test_bf_order_random_graphs(P, seed, key):
 
 def test_bf_order_kernels_and_schedules(P):
     """The breadth-first chain of tables on the generic kernel, uint64 keys
-    and the sequential, lane and dataflow schedules: the same answer."""
+    and the sequential and bulk lane schedules: the same answer."""
     g = random_graph(560, n=9, p=16, max_dims=3, extra_edges=3, max_size=256)
     o = _oracle(g, bf=True)
-    for kw in ({}, {"kernel": 1}, {"key": 1}, {"schedule": 1}, {"schedule": 2}, {"schedule": 3}):
+    for kw in ({}, {"kernel": 1}, {"key": 1}, {"schedule": 1}, {"schedule": 4, "bulk_us": 0}):
         say(f"breadth-first seed=560 {kw}")
         pg, mc, strat = _run(P, g, bf=True, **kw)
         assert (mc, strat) == o.result()
@@ -675,7 +654,7 @@ def test_volume_model_large_tensors(P):
 @pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid"])
 def test_volume_model_workloads_against_golden(P, name):
     _check_golden(P, name, 0, volume=True)
-    _check_golden(P, name, 0, volume=True, keep=False, schedule=2)
+    _check_golden(P, name, 0, volume=True, keep=False, schedule=4)
 
 
 def test_volume_model_transformer_against_golden(P):
@@ -747,17 +726,17 @@ def test_direct_fill_random_graphs(P, seed, key):
 
 
 def test_direct_fill_schedules_and_orders(P):
-    """The direct fill under the sequential and lane schedules, the
-    breadth-first order and every-integer configurations; the dataflow
-    schedule does not use it."""
+    """The direct fill under the level, sequential and bulk lane schedules,
+    the breadth-first order and every-integer configurations; the generic-only
+    kernel mode does not use it."""
     g = random_graph(680, n=9, p=16, max_dims=3, extra_edges=4, max_size=256)
     o = _oracle(g)
-    for sched in (0, 1, 2):
+    for sched in (0, 1, 4):
         say(f"direct fill seed=680 schedule={sched}")
         pg, mc, strat = _run(P, g, schedule=sched, direct=ALL_DIRECT)
         assert (mc, strat) == o.result()
         _compare_all_entries(pg, o, g, max_entries=256)
-    pg, mc, strat = _run(P, g, schedule=3, direct=ALL_DIRECT)
+    pg, mc, strat = _run(P, g, kernel=1, direct=ALL_DIRECT)
     assert (mc, strat) == o.result()
     assert all(pg.vertex_info(v)["kernel"] != 2 for v in range(len(g["vertices"])))
     ob = _oracle(g, bf=True)

@@ -352,25 +352,27 @@ def test_options_validate(pase):
 def test_bulk_lane_plan(pase):
     """Schedule 4 on the Transformer graph: the large fills (>= 8e9 cells) and
     every vertex at a level after them that reads only large fills' chain run
-    on the bulk stream (lane 2), all others on lane 1; a threshold above every
-    planned time leaves the bulk stream empty; the threshold validates."""
+    on the bulk stream (lane 1), all others on the caller's stream (lane 0); a
+    threshold above every planned time leaves the bulk stream empty; the
+    threshold and the schedule values validate."""
     g = transformer()
     pg = pase.Graph(g)
     pg.set_option(pase.OPT_SCHEDULE, 4)
     pg.enumerate_configs(g["p"])
     info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
     lanes = [x["lane"] for x in info]
-    assert set(lanes) == {1, 2}
+    assert set(lanes) == {0, 1}
     for x in info:
         if x["kernel"] == 1 and x["cells"] >= 8e9:
-            assert x["lane"] == 2
+            assert x["lane"] == 1
     # the Transformer's encoder (the sequence's first vertices) never reads a large fill
     seq = pg.sequence()
-    assert all(lanes[v] == 1 for v in seq[:20])
+    assert all(lanes[v] == 0 for v in seq[:20])
     pg.set_option(pase.OPT_BULK_US, 10 ** 9)
-    assert {pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))} == {1}
+    assert {pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))} == {0}
     assert _status(lambda: pg.set_option(pase.OPT_BULK_US, 10 ** 9 + 1)) == pase.INVALID_ARGUMENT
-    assert _status(lambda: pg.set_option(pase.OPT_SCHEDULE, 5)) == pase.INVALID_ARGUMENT
+    for bad in (2, 3, 5):
+        assert _status(lambda: pg.set_option(pase.OPT_SCHEDULE, bad)) == pase.INVALID_ARGUMENT
 
 
 def test_level_launch_unification(pase):
