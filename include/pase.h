@@ -280,6 +280,27 @@ pase_status pase_set_workspace(pase_graph_t g, void *device_ptr, uint64_t bytes)
 pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_cost,
                                     uint32_t *config_idx);
 
+/* Allocation-free variant of pase_find_best_strategy, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It allocates nothing -- no hipMalloc,
+ * hipFree, pinned host memory, stream or event: every device buffer of the
+ * search (constant region, DP and argmin tables, prep blocks, split scratch)
+ * lives in one static device array of PASE_NOALLOC_WORKSPACE_BYTES that each
+ * GPU the library runs on holds until the process ends, and the constant
+ * region is staged through a static host buffer of the same size.  Same
+ * arguments, results and errors as pase_find_best_strategy, plus TOO_LARGE
+ * when pase_workspace_size() exceeds PASE_NOALLOC_WORKSPACE_BYTES (checked on
+ * the host before any device work).  Profiling (PASE_OPT_PROFILE) is ignored
+ * and a bulk lane plan (PASE_OPT_SCHEDULE 4) runs level by level on `stream`.
+ * The array keeps the last call's contents and every call on one GPU shares
+ * it: calls in one process are serialized by a lock, calls from different
+ * processes that overlap on one GPU race, and the next allocation-free search
+ * on that GPU (any handle) overwrites the tables that pase_table_entry /
+ * pase_table_fingerprint read after this one. */
+#define PASE_NOALLOC_WORKSPACE_BYTES (64ull << 20)
+pase_status pase_find_best_strategy_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost,
+                                            uint32_t *config_idx);
+
 /* Read entry T_v[dep_cfg] of the DP table of vertex v and its argmin after a
  * search with PASE_OPT_KEEP_TABLES=1.  dep_cfg: host array of |D(v)|
  * configuration indices, one per member of D(v) in ascending vertex id. */

@@ -21,6 +21,8 @@
 #include <algorithm>
 #include <chrono>
 #include <map>
+#include <mutex>
+#include <string>
 #include <type_traits>
 #include <cstring>
 #include <numeric>
@@ -280,6 +282,7 @@ struct DeviceState {
     std::vector<hipEvent_t> ev;        // profiling: two per timed fill launch
     hipEvent_t phase_ev[4] = {};       // profiling: search phases (cost tables | fill | back-substitution)
     hipStream_t last_stream = nullptr;
+    char *last_ws = nullptr;           // workspace of the last search (its tables are read there)
     hipStream_t side = nullptr;        // bulk lane schedule: the bulk stream (default priority)
     std::vector<hipEvent_t> lane_ev;   // bulk lane schedule: joins (no timing)
 };
@@ -412,8 +415,12 @@ static void launch_generic(const GenericArgs *descs, const BatchEntry *be, const
 }
 
 
+// One search on stream s with the workspace at device address ws and the
+// host staging buffer img (at least plan.off_cfg bytes).  noalloc: create no
+// stream or event (profiling off, one stream).
 template <typename KeyT>
-static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t *min_cost, uint32_t *cfg) {
+static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img, bool noalloc, uint64_t *min_cost,
+                              uint32_t *cfg) {
     DeviceState *d = g->dev;
     Plan &P = g->plan;
     const int n = (int)P.v.size();
@@ -421,9 +428,8 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     const auto t_setup = std::chrono::steady_clock::now();
 
     // ---- constant region image and batched launches (host), one upload
-    char *img = (char *)d->pinned;
     SearchImage si;
-    pase_status st = build_image<KeyT>(g, ws, img, si);
+    pase_status st = build_image<KeyT>(g, ws, img, si, !noalloc);
     if (st != PASE_OK) return st;
     g->stats.setup_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_setup).count();
     const std::vector<Batch> &batches = si.batches;
@@ -453,9 +459,10 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
 
     // fill launches timed with events: every one (profile 1), or only those of
     // the row kernel with a column chunk per lane (profile 2)
+    const int profile = noalloc ? 0 : g->profile;
     auto timed = [&](const Batch &b) {
-        if (g->profile == 1) return b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
-        return g->profile == 2 && b.kind == Batch::kRows && b.variant / 32 != 1;
+        if (profile == 1) return b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect;
+        return profile == 2 && b.kind == Batch::kRows && b.variant / 32 != 1;
     };
     uint32_t nfill = 0;
     for (const Batch &b : batches) nfill += timed(b);
@@ -463,7 +470,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     // after the search's final synchronization), so they skip the
     // system-scope cache write-back and invalidation a default event performs
     // around the dispatch -- a few microseconds per timed launch otherwise
-    if (g->profile) {
+    if (profile) {
         for (size_t k = d->ev.size(); k < 2 * (size_t)nfill; k++) {
             hipEvent_t e;
             HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
@@ -484,7 +491,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
             launches_n++;
         }
     }
-    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[1], s));
+    if (profile) HIPCHK(hipEventRecord(d->phase_ev[1], s));
     std::vector<int> fill_of(n, -1);   // timed fill batch of each vertex (profiling)
     uint32_t fb = 0;
     // bulk lane schedule: the bulk stream starts after the upload and the cost
@@ -573,7 +580,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         HIPCHK(hipEventRecord(lev(1, P.nslots), lane_stream[1]));
         HIPCHK(hipStreamWaitEvent(s, lev(1, P.nslots), 0));
     }
-    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[2], s));
+    if (profile) HIPCHK(hipEventRecord(d->phase_ev[2], s));
     if ((uint32_t)n <= kMaxBacktrackThreads)
         hipLaunchKernelGGL((k_backtrack_levels<KeyT>), dim3(1), dim3((n + 63) / 64 * 64), 0, s,
                            (const BacktrackDesc *)(ws + P.off_bt), (uint32_t)n, si.nlev,
@@ -582,7 +589,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
         hipLaunchKernelGGL((k_backtrack<KeyT>), dim3(1), dim3(64), 0, s, (const BacktrackDesc *)(ws + P.off_bt),
                            (uint32_t)n, (const void *)(ws + P.off_T + P.v[n - 1].T_off), dcfg, dout);
     launches_n++;
-    if (g->profile) HIPCHK(hipEventRecord(d->phase_ev[3], s));
+    if (profile) HIPCHK(hipEventRecord(d->phase_ev[3], s));
     HIPCHK(hipGetLastError());
     // the staging buffer is reused for the results: the stream runs the
     // upload before these copies
@@ -602,7 +609,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
     g->stats.cost_tables_ms = g->stats.fill_span_ms = g->stats.backtrack_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;
-    if (g->profile) {
+    if (profile) {
         float ph[3] = {0.f, 0.f, 0.f};
         for (int k = 0; k < 3; k++) HIPCHK(hipEventElapsedTime(&ph[k], d->phase_ev[k], d->phase_ev[k + 1]));
         g->stats.cost_tables_ms = ph[0];
@@ -629,25 +636,22 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, uint64_t 
     return PASE_OK;
 }
 
-pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
-    auto t0 = std::chrono::steady_clock::now();
-    pase_status st;
-    uint32_t kt = choose_key_type(g, &st);
-    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
-    char *ws = nullptr;
-    st = ensure_memory(g, &ws);
-    if (st != PASE_OK) return st;
-    hipStream_t s = (hipStream_t)stream;
+// The search itself, once the workspace (device) and staging buffer (host)
+// are known; records the statistics and the workspace the tables live in.
+static pase_status search_in(pase_graph_t g, hipStream_t s, char *ws, char *img, bool noalloc, uint32_t kt,
+                             std::chrono::steady_clock::time_point t0, uint64_t *min_cost, uint32_t *cfg) {
     g->searched = false;
     uint64_t mc = 0;
     std::vector<uint32_t> out(g->V.size());
-    st = kt == 0 ? run_search<double>(g, s, ws, &mc, out.data()) : run_search<uint64_t>(g, s, ws, &mc, out.data());
+    pase_status st = kt == 0 ? run_search<double>(g, s, ws, img, noalloc, &mc, out.data())
+                             : run_search<uint64_t>(g, s, ws, img, noalloc, &mc, out.data());
     if (st != PASE_OK) return st;
     *min_cost = mc;
     std::memcpy(cfg, out.data(), out.size() * 4);
     g->key_type = kt;
     g->searched = true;
     g->dev->last_stream = s;
+    g->dev->last_ws = ws;
     const Plan &P = g->plan;
     g->stats.cells = P.cells;
     g->stats.table_entries = P.entries;
@@ -661,10 +665,58 @@ pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint
     return PASE_OK;
 }
 
-static char *workspace(pase_graph_t g) {
-    DeviceState *d = g->dev;
-    return d->lent ? (char *)d->lent : (char *)d->ws;
+pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
+    const auto t0 = std::chrono::steady_clock::now();
+    pase_status st;
+    const uint32_t kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    char *ws = nullptr;
+    st = ensure_memory(g, &ws);
+    if (st != PASE_OK) return st;
+    return search_in(g, (hipStream_t)stream, ws, (char *)g->dev->pinned, false, kt, t0, min_cost, cfg);
 }
+
+// ------------------------------------------------------------------ allocation-free search
+// The workspace of pase_find_best_strategy_noalloc: one static array that
+// every GPU the library runs on holds for the life of the process, each at
+// its own address.  In host code `scratch` only names the symbol: its device
+// address on the current GPU comes from hipGetSymbolAddress, once per device,
+// and only that address is ever handed to a kernel or a copy.
+constexpr uint64_t kScratchBytes = PASE_NOALLOC_WORKSPACE_BYTES;
+constexpr int kScratchDevices = 64;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;                        // one allocation-free search at a time per process
+char *g_scratch_ptr[kScratchDevices] = {};      // device address of `scratch` per device
+alignas(256) char g_scratch_img[kScratchBytes]; // host staging of the constant region
+}  // namespace
+
+pase_status device_search_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
+    const auto t0 = std::chrono::steady_clock::now();
+    pase_status st;
+    const uint32_t kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    if (g->plan.total > kScratchBytes)
+        return fail(g, PASE_ERR_TOO_LARGE,
+                    "the search needs " + std::to_string(g->plan.total) + " bytes of device memory, more than the " +
+                        std::to_string(kScratchBytes) + " of the allocation-free workspace");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    int dev = 0;
+    HIPCHK(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kScratchDevices) return fail(g, PASE_ERR_INVALID_ARGUMENT, "device index out of range");
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p || (uintptr_t)p % 256) return fail(g, PASE_ERR_INTERNAL, "static workspace address");
+        g_scratch_ptr[dev] = (char *)p;
+    }
+    state(g);
+    return search_in(g, (hipStream_t)stream, g_scratch_ptr[dev], g_scratch_img, true, kt, t0, min_cost, cfg);
+}
+
+// The workspace the last search ran in (library-owned, lent or static).
+static char *workspace(pase_graph_t g) { return g->dev->last_ws; }
 
 pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *cost, uint32_t *arg) {
     const Plan &P = g->plan;

@@ -1124,6 +1124,13 @@ extern "C" pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uin
     return device_search(g, stream, min_cost, config_idx);
 }
 
+extern "C" pase_status pase_find_best_strategy_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost,
+                                                       uint32_t *config_idx) {
+    if (!g || !min_cost || !config_idx) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    return device_search_noalloc(g, stream, min_cost, config_idx);
+}
+
 static pase_status find_entry(pase_graph_t g, uint32_t v, const uint32_t *dep_cfg, int *pos,
                               uint64_t *idx) {
     if (!g->searched) return fail(g, PASE_ERR_BAD_STATE, "no search has run");

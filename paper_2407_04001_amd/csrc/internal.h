@@ -313,6 +313,7 @@ uint32_t choose_key_type(pase_graph_t g, pase_status *st);
 // device.hip
 void device_release(pase_graph_t g);
 pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);
+pase_status device_search_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);
 pase_status device_set_workspace(pase_graph_t g, void *ptr, uint64_t bytes);
 pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *cost,
                                uint32_t *arg);

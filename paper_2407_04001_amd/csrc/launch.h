@@ -56,8 +56,9 @@ pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &
 // The constant-region image [0, plan.off_cfg) of one search into `img` (host
 // memory of at least plan.off_cfg bytes) and its batches, for a workspace at
 // device address `ws`.  Every write into `img` is checked against the plan's
-// region bounds before it is made.
+// region bounds before it is made.  allow_lanes = false runs a bulk lane plan
+// level by level on one stream (its resident layout serves that order too).
 template <typename KeyT>
-pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si);
+pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_lanes = true);
 
 }  // namespace pase

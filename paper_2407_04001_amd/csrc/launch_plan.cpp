@@ -315,7 +315,7 @@ template pase_status build_launches<uint64_t>(pase_graph_t, char *, std::vector<
 
 // ------------------------------------------------------------------ constant image and batches
 template <typename KeyT>
-pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si) {
+pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_lanes) {
     const Plan &P = g->plan;
     const int n = (int)P.v.size();
     const size_t nv = g->V.size(), ne = g->E.size();
@@ -324,7 +324,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si) {
     pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
     if (st != PASE_OK) return st;
     si = SearchImage();
-    si.lanes = P.resident && g->schedule == kSchedBulk;
+    si.lanes = allow_lanes && P.resident && g->schedule == kSchedBulk;
     // every piece of the image is checked against the end of its region first
     auto region = [&](uint64_t off, uint64_t bytes, uint64_t end, const char *what) {
         return off + bytes <= end && end <= P.off_cfg ? PASE_OK
@@ -554,7 +554,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si) {
     return PASE_OK;
 }
 
-template pase_status build_image<double>(pase_graph_t, char *, char *, SearchImage &);
-template pase_status build_image<uint64_t>(pase_graph_t, char *, char *, SearchImage &);
+template pase_status build_image<double>(pase_graph_t, char *, char *, SearchImage &, bool);
+template pase_status build_image<uint64_t>(pase_graph_t, char *, char *, SearchImage &, bool);
 
 }  // namespace pase

@@ -71,7 +71,8 @@ EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_e
            "pase_num_configs", "pase_config_splits", "pase_get_sequence", "pase_get_dependent_set",
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
-           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get"]
+           "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get",
+           "pase_find_best_strategy_noalloc"]
 
 _lib = None
 
@@ -103,6 +104,7 @@ def load(path: str | None = None):
         "pase_workspace_size": (st, [P, P]),
         "pase_set_workspace": (st, [P, P, U64]),
         "pase_find_best_strategy": (st, [P, P, P, P]),
+        "pase_find_best_strategy_noalloc": (st, [P, P, P, P]),
         "pase_table_entry": (st, [P, U32, P, P, P]),
         "pase_table_fingerprint": (st, [P, U32, P, P]),
         "pase_layer_costs": (st, [P, U32, P]),
@@ -223,6 +225,17 @@ def pase_find_best_strategy(h, nv: int, stream: int = 0):
     _check(h, load().pase_find_best_strategy(h, C.c_void_p(stream) if stream else None, C.byref(mc),
                                              _ptr(cfg)))
     return mc.value, cfg.tolist()
+
+
+def pase_find_best_strategy_noalloc(h, nv: int, stream: int = 0):
+    mc = C.c_uint64()
+    cfg = np.zeros(nv, np.uint32)
+    _check(h, load().pase_find_best_strategy_noalloc(h, C.c_void_p(stream) if stream else None, C.byref(mc),
+                                                     _ptr(cfg)))
+    return mc.value, cfg.tolist()
+
+
+NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 
 def pase_table_entry(h, v: int, dep_cfg):
