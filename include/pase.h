@@ -45,8 +45,10 @@ typedef enum {
     PASE_ERR_NOT_CONNECTED = 2,    /* the graph is not weakly connected (Sec. II) */
     PASE_ERR_BAD_STATE = 3,        /* call order violated (e.g. search before enumeration,
                                       table query without PASE_OPT_KEEP_TABLES) */
-    PASE_ERR_OVERFLOW = 4,         /* a cost, or the worst-case total cost shifted by the
-                                      argmin bits, does not fit in 64 bits */
+    PASE_ERR_OVERFLOW = 4,         /* a cost, or a bound of the costs summed by the
+                                      recurrence (a key without its argmin bits), does not fit
+                                      in 64 bits; raised by pase_enumerate_configs and
+                                      pase_override_costs */
     PASE_ERR_TOO_LARGE = 5,        /* a DP table, |D(i)|, the number of table lookups or
                                       the device memory need exceeds a limit; detected on the
                                       host before any device work */
@@ -101,7 +103,12 @@ typedef enum {
                                    pase_table_entry / pase_table_fingerprint can read it */
     PASE_OPT_MEMORY_BUDGET = 2, /* bytes of device memory a search may use (default 64 GiB) */
     PASE_OPT_KERNEL = 3,        /* 0 = choose per vertex (default), 1 = generic kernel only */
-    PASE_OPT_KEY_TYPE = 4,      /* 0 = choose from the cost bound (default), 1 = force uint64 keys */
+    PASE_OPT_KEY_TYPE = 4,      /* keys of the fill, cost * 2^ceil(log2 K_v) + c (min and argmin in
+                                   one comparison): 0 = choose from the recurrence's cost bounds
+                                   (default): fp64 when every key stays within 2^53 (exact integer
+                                   arithmetic), else uint64 when within 2^64, else 128-bit keys
+                                   (every vertex on prep + the generic kernel); 1 = uint64 unless
+                                   the keys need 128 bits; 2 = force 128-bit keys.  Re-plans */
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats);
                                    2: only the row kernel's launches with a column chunk per lane
                                    (the dominant kernel; fewer events, so less overhead) */
@@ -231,8 +238,9 @@ const char *pase_last_error(pase_graph_t g);
  * dependent sets D(i), connected sets X(i) and connected subsets S(i)
  * (Sec. III-B) and the device memory plan.  Host only; resets any earlier
  * search state and cost override.
- * Errors: INVALID_ARGUMENT (p), OVERFLOW (a layer cost exceeds 64 bits),
- * TOO_LARGE (|D(i)| > PASE_MAX_DEP, a table over 2^31 entries, K_v > 65535). */
+ * Errors: INVALID_ARGUMENT (p), OVERFLOW (a layer or transfer cost, or a
+ * bound of a sum of them along the recurrence, exceeds 64 bits), TOO_LARGE
+ * (|D(i)| > PASE_MAX_DEP, a table over 2^31 entries, K_v > 65535). */
 pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p);
 
 /* K_v = |C(v)|.  Needs pase_enumerate_configs. */
@@ -256,7 +264,9 @@ pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t value);
  * pase_enumerate_configs).  layer: host array, the K_v layer costs of every
  * vertex concatenated in vertex order.  edge: host array, for every edge the
  * row-major K_src x K_dst matrix of r*t_x, concatenated in edge order (may be
- * NULL when ne = 0).  Cleared by the next pase_enumerate_configs. */
+ * NULL when ne = 0).  Re-plans the key type (R10).  Cleared by the next
+ * pase_enumerate_configs.  Errors: OVERFLOW (a bound of the costs summed by
+ * the recurrence exceeds 64 bits; the earlier costs stay in force). */
 pase_status pase_override_costs(pase_graph_t g, const uint64_t *layer, const uint64_t *edge);
 
 /* Device bytes pase_find_best_strategy needs (after pase_enumerate_configs). */
@@ -276,7 +286,7 @@ pase_status pase_set_workspace(pase_graph_t g, void *device_ptr, uint64_t bytes)
  * config_idx: host array of nv, receives the chosen configuration index per
  * vertex id.  Among equal-cost configurations a table entry keeps the lowest
  * index (the strict "<" of Fig. 4 with ascending indices).
- * Errors: BAD_STATE, OVERFLOW, TOO_LARGE, OUT_OF_MEMORY, HIP, INTERNAL. */
+ * Errors: BAD_STATE, TOO_LARGE, OUT_OF_MEMORY, HIP, INTERNAL. */
 pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_cost,
                                     uint32_t *config_idx);
 
@@ -344,6 +354,8 @@ typedef struct {
     uint64_t key_bound;  /* upper bound of every summed cost before the min over c (keys stay
                             below (key_bound + 1) * 2^ceil(log2 K_v)); ~0 if it exceeds 64 bits */
     uint64_t table_bound; /* upper bound of every entry of its DP table; ~0 likewise */
+    uint32_t key_type;    /* key type of the plan (the same for every vertex): 0 fp64, 1 uint64, 2 128-bit */
+    uint32_t pad;
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

@@ -248,7 +248,7 @@ __global__ void k_fingerprint(FingerArgs a) {
             x /= a.rad[k];
         }
         uint64_t h = splitmix64_mix(canon);
-        st += splitmix64_mix(h ^ (KeyOps<KeyT>::val_to_u64(((const Val *)a.T)[t]) >> a.out_shift));
+        st += splitmix64_mix(h ^ KeyOps<KeyT>::unshift(((const Val *)a.T)[t], a.out_shift));
         sa += splitmix64_mix(h ^ (uint64_t)a.A[t]);
     }
     __shared__ uint64_t red[2][256];
@@ -426,6 +426,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
     const int n = (int)P.v.size();
     const size_t nv = g->V.size(), ne = g->E.size();
     const auto t_setup = std::chrono::steady_clock::now();
+    constexpr bool kWide = std::is_same<KeyT, u128>::value;   // 128-bit keys: prep + generic fills only
 
     // ---- constant region image and batched launches (host), one upload
     SearchImage si;
@@ -557,10 +558,12 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
             if (tb)
                 for (uint32_t k = 0; k < b.nentries; k++) fill_of[((const BatchEntry *)(img + P.off_batch))[b.entry0 + k].pos] = (int)fb;
             hipEvent_t e0 = tb ? d->ev[2 * fb] : nullptr, e1 = tb ? d->ev[2 * fb + 1] : nullptr;
-            if (b.kind == Batch::kRows) {
-                if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
-            } else if (b.kind == Batch::kGeneric) {
+            if (b.kind == Batch::kGeneric) {
                 launch_generic<KeyT>(dg, e, b, bs, e0, e1);
+            } else if constexpr (kWide) {
+                return fail(g, PASE_ERR_INTERNAL, "a 128-bit key plan holds a row or direct fill");
+            } else if (b.kind == Batch::kRows) {
+                if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
             } else {
                 hipExtLaunchKernelGGL((k_fill_direct<KeyT>), dim3(b.blocks), dim3(256), 0, bs, e0, e1, 0, dx, e,
                                       b.nentries, dV, dE, (const uint64_t *)dL, (const uint8_t *)dls,
@@ -570,7 +573,11 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         }
             break;
         case Batch::kReduce:
-            hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, bs, dd, e, b.nentries);
+            if constexpr (kWide) {
+                return fail(g, PASE_ERR_INTERNAL, "a 128-bit key plan holds a split reduction");
+            } else {
+                hipLaunchKernelGGL((k_reduce_splits<KeyT>), dim3(b.blocks), dim3(256), 0, bs, dd, e, b.nentries);
+            }
             break;
         }
         launches_n++;
@@ -643,8 +650,9 @@ static pase_status search_in(pase_graph_t g, hipStream_t s, char *ws, char *img,
     g->searched = false;
     uint64_t mc = 0;
     std::vector<uint32_t> out(g->V.size());
-    pase_status st = kt == 0 ? run_search<double>(g, s, ws, img, noalloc, &mc, out.data())
-                             : run_search<uint64_t>(g, s, ws, img, noalloc, &mc, out.data());
+    pase_status st = kt == 0   ? run_search<double>(g, s, ws, img, noalloc, &mc, out.data())
+                     : kt == 1 ? run_search<uint64_t>(g, s, ws, img, noalloc, &mc, out.data())
+                               : run_search<u128>(g, s, ws, img, noalloc, &mc, out.data());
     if (st != PASE_OK) return st;
     *min_cost = mc;
     std::memcpy(cfg, out.data(), out.size() * 4);
@@ -665,11 +673,21 @@ static pase_status search_in(pase_graph_t g, hipStream_t s, char *ws, char *img,
     return PASE_OK;
 }
 
+// The key type of the plan (R10), decided when the plan was made.
+static pase_status plan_keys(pase_graph_t g, uint32_t *kt) {
+    pase_status st;
+    *kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "a cost bound of the recurrence exceeds 64 bits");
+    if (*kt != g->plan_key_type || (*kt == 2) != g->plan_wide)
+        return fail(g, PASE_ERR_INTERNAL, "key type differs from the plan's");
+    return PASE_OK;
+}
+
 pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
     const auto t0 = std::chrono::steady_clock::now();
-    pase_status st;
-    const uint32_t kt = choose_key_type(g, &st);
-    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    uint32_t kt = 0;
+    pase_status st = plan_keys(g, &kt);
+    if (st != PASE_OK) return st;
     char *ws = nullptr;
     st = ensure_memory(g, &ws);
     if (st != PASE_OK) return st;
@@ -694,9 +712,9 @@ alignas(256) char g_scratch_img[kScratchBytes]; // host staging of the constant 
 
 pase_status device_search_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg) {
     const auto t0 = std::chrono::steady_clock::now();
-    pase_status st;
-    const uint32_t kt = choose_key_type(g, &st);
-    if (st != PASE_OK) return fail(g, st, "worst-case key exceeds 64 bits");
+    uint32_t kt = 0;
+    const pase_status st = plan_keys(g, &kt);
+    if (st != PASE_OK) return st;
     if (g->plan.total > kScratchBytes)
         return fail(g, PASE_ERR_TOO_LARGE,
                     "the search needs " + std::to_string(g->plan.total) + " bytes of device memory, more than the " +
@@ -722,17 +740,24 @@ pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *
     const Plan &P = g->plan;
     char *ws = workspace(g);
     const VPlan &vp = P.v[pos];
-    uint64_t raw = 0;
+    const uint64_t kb = key_bytes(g);
+    unsigned char raw[16] = {0};
     uint16_t a = 0;
-    HIPCHK(hipMemcpy(&raw, ws + P.off_T + vp.T_off + idx * 8, 8, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(raw, ws + P.off_T + vp.T_off + idx * kb, kb, hipMemcpyDeviceToHost));
     HIPCHK(hipMemcpy(&a, ws + P.off_A + vp.A_off + idx * 2, 2, hipMemcpyDeviceToHost));
     // tables are stored in their reader's key space (x 2^out_shift)
     if (g->key_type == 0) {
         double dv;
-        std::memcpy(&dv, &raw, 8);
+        std::memcpy(&dv, raw, 8);
         *cost = ((uint64_t)dv) >> vp.out_shift;
+    } else if (g->key_type == 1) {
+        uint64_t x;
+        std::memcpy(&x, raw, 8);
+        *cost = x >> vp.out_shift;
     } else {
-        *cost = raw >> vp.out_shift;
+        unsigned __int128 x;
+        std::memcpy(&x, raw, 16);
+        *cost = (uint64_t)(x >> vp.out_shift);
     }
     *arg = a;
     return PASE_OK;
@@ -763,7 +788,8 @@ pase_status device_fingerprint(pase_graph_t g, int pos, uint64_t *fpT, uint64_t 
     fa.out = dout;
     uint32_t grid = grid_for(vp.N, 256, 1024);
     if (g->key_type == 0) hipLaunchKernelGGL(k_fingerprint<double>, dim3(grid), dim3(256), 0, 0, fa);
-    else hipLaunchKernelGGL(k_fingerprint<uint64_t>, dim3(grid), dim3(256), 0, 0, fa);
+    else if (g->key_type == 1) hipLaunchKernelGGL(k_fingerprint<uint64_t>, dim3(grid), dim3(256), 0, 0, fa);
+    else hipLaunchKernelGGL(k_fingerprint<u128>, dim3(grid), dim3(256), 0, 0, fa);
     unsigned long long h[2];
     hipError_t e = hipMemcpy(h, dout, 16, hipMemcpyDeviceToHost);
     (void)hipFree(dout);

@@ -89,8 +89,12 @@ bool cost_bounds(pase_graph_t g, std::vector<uint64_t> *qmax, std::vector<uint64
 
 // Key type: fp64 when every key (cost * 2^bits + c) of every position stays
 // within 2^53 so that double arithmetic on them is exact integer arithmetic;
-// otherwise uint64 when it stays within 2^64; otherwise overflow.  A stored
-// table entry T_j (in its reader's key space) is at most the reader's bound.
+// otherwise uint64 when it stays within 2^64; otherwise 128-bit keys, which
+// hold cost * 2^bits + c exactly as long as every cost sum fits 64 bits (the
+// costs and tables the C ABI reports are uint64); when a cost bound itself
+// passes 64 bits, overflow.  A stored table entry T_j (in its reader's key
+// space) is at most the reader's bound.  key_mode 1 / 2 force uint64 (when
+// the keys fit) / 128-bit keys.
 uint32_t choose_key_type(pase_graph_t g, pase_status *st) {
     *st = PASE_OK;
     std::vector<uint64_t> qmax, tmax;
@@ -101,11 +105,13 @@ uint32_t choose_key_type(pase_graph_t g, pase_status *st) {
         const unsigned __int128 t = ((unsigned __int128)qmax[i] + 1) << g->plan.v[i].bits;
         top = std::max(top, t);
     }
+    if (g->key_mode == 2) return 2;
     if (g->key_mode == 0 && top <= ((unsigned __int128)1 << 53)) return 0;
     if (top <= ((unsigned __int128)1 << 64)) return 1;
-    *st = PASE_ERR_OVERFLOW;
-    return 0;
+    return 2;
 }
+
+uint32_t key_bytes(pase_graph_t g) { return g->plan_wide ? 16u : 8u; }
 
 }  // namespace pase
 
@@ -514,12 +520,14 @@ static pase_status build_plan(pase_graph_t g) {
     // plan_one(i, ftz, ftm): kernel, tile and layout of position i; ftz/ftm
     // (0 = free) force the row kernel's columns and rows per lane for this
     // vertex and rule out the column-less form
+    // 128-bit keys: every vertex on prep + the generic kernel
+    const int kernel_mode = g->plan_wide ? 1 : g->kernel_mode;
     auto plan_one = [&](int i, uint32_t ftz, uint32_t ftm) {
         VPlan &vp = P.v[i];
         const uint32_t tile_cols = ftz ? ftz : g->tile_cols, tile_rows = ftm ? ftm : g->tile_rows;
         // small vertices: the direct fill (one launch, no prep blocks), whose
         // time is a launch plus the gather of every term of every cell
-        if (!ftz && g->direct_cells && g->kernel_mode == 0 && vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
+        if (!ftz && g->direct_cells && kernel_mode == 0 && vp.N * vp.K <= g->direct_cells && (g->schedule == kSchedSeq || level_small[vp.level])) {
             vp.kernel = kDirect;
             vp.est_us = 4.0 + (double)vp.N * vp.K * (1.0 + vp.edges.size() + vp.terms.size()) / 4e5;
             vp.layout = gather_layout(vp);
@@ -536,8 +544,8 @@ static pase_status build_plan(pase_graph_t g) {
         // a row digit, each lane streams its own entry's terms over c; for a
         // lookup that covers all of D(i) this reads T_j once, coalesced)
         std::vector<int> zs;
-        if (g->kernel_mode == 0 && vp.D.size() >= 2) zs = vp.D;
-        if (g->kernel_mode == 0 && !vp.D.empty() && !ftz) zs.push_back(-1);
+        if (kernel_mode == 0 && vp.D.size() >= 2) zs = vp.D;
+        if (kernel_mode == 0 && !vp.D.empty() && !ftz) zs.push_back(-1);
         for (int z : zs) {
             if (z < 0 && best.ok) break;
             {
@@ -644,7 +652,7 @@ static pase_status build_plan(pase_graph_t g) {
     // share a launch (the small one's workgroups come first and finish inside
     // the large one's) instead of adding a latency-bound launch of its own.
     // Level schedule only: the bulk lane splits a level over two streams.
-    if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && g->kernel_mode == 0) {
+    if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && kernel_mode == 0) {
         std::vector<int> dom((size_t)maxlev + 1, -1);
         for (int i = 0; i < n; i++) {
             const VPlan &vp = P.v[i];
@@ -706,6 +714,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     // resident: vertices may run in any order the dependencies allow, so
     // every vertex has scratch of its own and no table memory is reused
     const bool resident = mode == kLayoutResident, by_level = mode != kLayoutSeq;
+    const uint64_t kb = key_bytes(g);   // bytes per table value and block key
     P.by_level = by_level;
     P.resident = resident;
     P.nslots = 0;
@@ -767,7 +776,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     std::vector<Iv> iv;
     for (int i = 0; i < n; i++) {
         int end = (resident || g->keep_tables || i == n - 1) ? P.nslots : P.v[P.v[i].consumer].slot;
-        iv.push_back({i, P.v[i].slot, end, align_up(P.v[i].N * 8, A)});
+        iv.push_back({i, P.v[i].slot, end, align_up(P.v[i].N * kb, A)});
     }
     std::vector<int> order(n);
     std::iota(order.begin(), order.end(), 0);
@@ -807,7 +816,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
         if (vp.kernel == kRows) {
             e += align_up(vp.MO * vp.K * vp.ldz, 32);
             for (int u : vp.R) e += align_up((uint64_t)vp.K * g->K[u], 32);
-            if (vp.nsplit > 1) pb = align_up((uint64_t)vp.nsplit * vp.N * 8, A);
+            if (vp.nsplit > 1) pb = align_up((uint64_t)vp.nsplit * vp.N * kb, A);
         } else if (vp.kernel == kGeneric) {
             e += align_up(vp.K, 32);
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
@@ -817,7 +826,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
         const int sl = resident ? 0 : vp.slot;
         vp.block_off = bsum[sl];
         vp.partial_off = psum[sl];
-        bsum[sl] += align_up(e * 8, A);
+        bsum[sl] += align_up(e * kb, A);
         psum[sl] += pb;
         bmax = std::max(bmax, bsum[sl]);
         pmax = std::max(pmax, psum[sl]);
@@ -832,6 +841,24 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     if (P.total > g->mem_budget)
         return fail(g, PASE_ERR_TOO_LARGE, "device memory need exceeds the memory budget");
     return PASE_OK;
+}
+
+// Plan (or, with replan, re-plan from the vertex order on) the search: the
+// key type that the plans and the current costs need (R10), then the memory
+// layout.  A change to or from 128-bit keys re-plans every vertex (such plans
+// run on the generic kernel).  OVERFLOW when a cost bound of the recurrence
+// passes 64 bits.
+static pase_status plan_search(pase_graph_t g, bool replan) {
+    pase_status st;
+    if (replan && (st = build_plan(g)) != PASE_OK) return st;
+    const uint32_t kt = choose_key_type(g, &st);
+    if (st != PASE_OK) return fail(g, st, "a cost bound of the recurrence exceeds 64 bits");
+    if ((kt == 2) != g->plan_wide) {
+        g->plan_wide = kt == 2;
+        if ((st = build_plan(g)) != PASE_OK) return st;
+    }
+    g->plan_key_type = kt;
+    return layout_memory(g);
 }
 
 extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
@@ -956,9 +983,8 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
         }
     }
     g->enumerated = true;
-    pase_status st = build_plan(g);
-    if (st != PASE_OK) { g->enumerated = false; return st; }
-    st = layout_memory(g);
+    g->plan_wide = false;
+    const pase_status st = plan_search(g, true);
     if (st != PASE_OK) { g->enumerated = false; return st; }
     g->planned = true;
     return PASE_OK;
@@ -1013,7 +1039,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->kernel_mode = (int)value;
         break;
     case PASE_OPT_KEY_TYPE:
-        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "key type 0 or 1");
+        if (value > 2) return fail(g, PASE_ERR_INVALID_ARGUMENT, "key type 0, 1 or 2");
         g->key_mode = (int)value;
         break;
     case PASE_OPT_PROFILE:
@@ -1072,11 +1098,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
          opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER ||
-         opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US) &&
+         opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US || opt == PASE_OPT_KEY_TYPE) &&
         g->enumerated) {
         g->searched = false;
-        pase_status st = build_plan(g);
-        if (st == PASE_OK) st = layout_memory(g);
+        const pase_status st = plan_search(g, true);
         g->planned = st == PASE_OK;
         if (st != PASE_OK) return st;
     }
@@ -1087,6 +1112,9 @@ extern "C" pase_status pase_override_costs(pase_graph_t g, const uint64_t *layer
     if (!g || !layer || (!edge && !g->E.empty())) return PASE_ERR_INVALID_ARGUMENT;
     if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
     const size_t nv = g->V.size(), ne = g->E.size();
+    std::vector<uint64_t> old_layer = g->ov_layer, old_layer_off = g->ov_layer_off, old_edge = g->ov_edge,
+                          old_edge_off = g->ov_edge_off;
+    const bool was = g->overridden;
     g->ov_layer_off.assign(nv, 0);
     uint64_t tot = 0;
     for (size_t v = 0; v < nv; v++) { g->ov_layer_off[v] = tot; tot += g->K[v]; }
@@ -1100,7 +1128,21 @@ extern "C" pase_status pase_override_costs(pase_graph_t g, const uint64_t *layer
     g->ov_edge.assign(edge ? edge : layer, edge ? edge + tot : layer);
     g->overridden = true;
     g->searched = false;
-    return layout_memory(g);
+    const pase_status st = plan_search(g, false);
+    if (st != PASE_OK) {
+        // back to the plan of the costs before this call (which was valid)
+        const std::string msg = g->err;
+        g->overridden = false;
+        g->ov_layer.swap(old_layer);
+        g->ov_layer_off.swap(old_layer_off);
+        g->ov_edge.swap(old_edge);
+        g->ov_edge_off.swap(old_edge_off);
+        g->overridden = was;
+        g->planned = plan_search(g, false) == PASE_OK;
+        g->err = msg;
+        return st;
+    }
+    return PASE_OK;
 }
 
 extern "C" pase_status pase_workspace_size(pase_graph_t g, uint64_t *bytes) {
@@ -1226,6 +1268,7 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     } else {
         x.key_bound = x.table_bound = ~0ull;
     }
+    x.key_type = g->plan_key_type;
     *out = x;
     return PASE_OK;
 }

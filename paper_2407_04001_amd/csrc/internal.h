@@ -298,6 +298,10 @@ struct pase_graph_s {
     // plan
     pase::Plan plan;
     bool planned = false;
+    // keys of the plan (R10): 0 fp64, 1 uint64, 2 128-bit (packed keys past 2^64 while every
+    // cost sum fits 64 bits; such a plan runs every vertex on prep + the generic kernel)
+    uint32_t plan_key_type = 0;
+    bool plan_wide = false;         // the plan was built for 128-bit keys
     // last search
     bool searched = false;
     uint32_t key_type = 0;
@@ -310,6 +314,7 @@ namespace pase {
 // host.cpp
 pase_status fail(pase_graph_t g, pase_status st, const std::string &msg);
 uint32_t choose_key_type(pase_graph_t g, pase_status *st);
+uint32_t key_bytes(pase_graph_t g);   // bytes of a table value / block key of the plan (8 or 16)
 // device.hip
 void device_release(pase_graph_t g);
 pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);

@@ -14,11 +14,18 @@ namespace pase {
 // ------------------------------------------------------------------ key arithmetic
 template <typename KeyT> struct KeyOps;
 
+// Val: the type of a stored table value (cost x 2^out_shift, in its reader's
+// key space); Acc: an exact integer wide enough for one key, in which prep
+// sums its contributions before the key is formed.
 template <> struct KeyOps<double> {
     using Val = double;   // table value type
+    using Acc = uint64_t;
     static constexpr double sentinel() { return 1152921504606846976.0; }  // 2^60 > any key
     __device__ static double from_u64(uint64_t x) { return (double)x; }
+    __device__ static double from_acc(uint64_t x) { return (double)x; }
     __device__ static uint64_t val_to_u64(double x) { return (uint64_t)x; }
+    __device__ static uint64_t val_to_acc(double x) { return (uint64_t)x; }
+    __device__ static uint64_t unshift(double x, uint32_t s) { return (uint64_t)x >> s; }
     __device__ static double add(double a, double b) { return a + b; }
     __device__ static double min(double a, double b) { return __builtin_fmin(a, b); }
     // key = cost * 2^bits + c  ->  (cost * 2^out_shift, c)
@@ -32,14 +39,37 @@ template <> struct KeyOps<double> {
 
 template <> struct KeyOps<uint64_t> {
     using Val = uint64_t;
+    using Acc = uint64_t;
     static constexpr uint64_t sentinel() { return ~0ull; }
     __device__ static uint64_t from_u64(uint64_t x) { return x; }
+    __device__ static uint64_t from_acc(uint64_t x) { return x; }
     __device__ static uint64_t val_to_u64(uint64_t x) { return x; }
+    __device__ static uint64_t val_to_acc(uint64_t x) { return x; }
+    __device__ static uint64_t unshift(uint64_t x, uint32_t s) { return x >> s; }
     __device__ static uint64_t add(uint64_t a, uint64_t b) { return a + b; }
     __device__ static uint64_t min(uint64_t a, uint64_t b) { return a < b ? a : b; }
     __device__ static void split(uint64_t key, uint32_t bits, uint32_t out_shift, uint64_t &val, uint32_t &c) {
         val = (key >> bits) << out_shift;
         c = (uint32_t)(key & ((1ull << bits) - 1));
+    }
+};
+
+// 128-bit keys: cost * 2^bits + c for costs up to 2^64 (bits <= 16), so the
+// packed key never overflows; table values are stored in 16 bytes.
+using u128 = unsigned __int128;
+template <> struct KeyOps<u128> {
+    using Val = u128;
+    using Acc = u128;
+    static constexpr u128 sentinel() { return ~(u128)0; }
+    __device__ static u128 from_acc(u128 x) { return x; }
+    __device__ static uint64_t val_to_u64(u128 x) { return (uint64_t)x; }
+    __device__ static u128 val_to_acc(u128 x) { return x; }
+    __device__ static uint64_t unshift(u128 x, uint32_t s) { return (uint64_t)(x >> s); }
+    __device__ static u128 add(u128 a, u128 b) { return a + b; }
+    __device__ static u128 min(u128 a, u128 b) { return a < b ? a : b; }
+    __device__ static void split(u128 key, uint32_t bits, uint32_t out_shift, u128 &val, uint32_t &c) {
+        val = (key >> bits) << out_shift;
+        c = (uint32_t)key & ((1u << bits) - 1u);
     }
 };
 
@@ -223,14 +253,16 @@ __device__ __forceinline__ void set_priority(const BatchEntry &e) {
 // and shifted into key space at the end; DP tables are stored in this
 // vertex's key space already; the layer term carries c into the low bits.
 template <typename KeyT>
-__device__ __forceinline__ uint64_t contrib_key(const Contrib *__restrict__ cb, uint32_t c0, uint32_t c1,
+__device__ __forceinline__ typename KeyOps<KeyT>::Acc contrib_key(const Contrib *__restrict__ cb, uint32_t c0, uint32_t c1,
                                                 const DevVertex &me, uint32_t c, const uint32_t (&dv)[kMaxDep],
                                                 uint32_t bits, const DevVertex *__restrict__ V,
                                                 const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
                                                 const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
                                                 uint64_t r) {
     using Val = typename KeyOps<KeyT>::Val;
-    uint64_t sum = 0, keysum = 0, low = 0;
+    using Acc = typename KeyOps<KeyT>::Acc;
+    uint64_t sum = 0, low = 0;
+    Acc keysum = 0;
     for (uint32_t k = c0; k < c1; k++) {
         const Contrib ct = cb[k];
         if (ct.kind == kContribLayer) {
@@ -247,10 +279,10 @@ __device__ __forceinline__ uint64_t contrib_key(const Contrib *__restrict__ cb, 
             uint64_t idx = (uint64_t)c * ct.sc;
             for (int k2 = 0; k2 < kMaxDep; k2++) idx += (uint64_t)dv[k2] * ct.sd[k2];
             if (ct.raw_u64) sum += ((const uint64_t *)ct.ptr)[idx];
-            else keysum += KeyOps<KeyT>::val_to_u64(((const Val *)ct.ptr)[idx]);
+            else keysum += KeyOps<KeyT>::val_to_acc(((const Val *)ct.ptr)[idx]);
         }
     }
-    return (sum << bits) + keysum + low;
+    return ((Acc)sum << bits) + keysum + low;
 }
 
 // One workgroup handles `span` runs of kPrepThreads consecutive (c, column)
@@ -288,7 +320,7 @@ __device__ __forceinline__ void prep_item(const PrepArgs &a, uint32_t wg, const 
             continue;
         }
         if (bk.post >= 0) dv[bk.post] = q;
-        *out = KeyOps<KeyT>::from_u64(contrib_key<KeyT>(cb, bk.c_begin, bk.c_end, me, c, dv, a.bits, V, E, L,
+        *out = KeyOps<KeyT>::from_acc(contrib_key<KeyT>(cb, bk.c_begin, bk.c_end, me, c, dv, a.bits, V, E, L,
                                                          lsum, sig, r));
     }
 }
@@ -553,10 +585,12 @@ __device__ __forceinline__ void reduce_item(const ReduceArgs &a, uint32_t lb) {
 // optimal c -- does not depend on the evaluation order.
 template <typename KeyT>
 __device__ __forceinline__ KeyT shfl_xor_key(KeyT v, int mask) {
-    uint64_t u = __builtin_bit_cast(uint64_t, v);
-    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)u, mask, 64);
-    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), mask, 64);
-    return __builtin_bit_cast(KeyT, ((uint64_t)hi << 32) | lo);
+    constexpr int W = sizeof(KeyT) / 4;   // 32-bit words of a key
+    struct Words { uint32_t w[W]; };
+    Words x = __builtin_bit_cast(Words, v);
+#pragma unroll
+    for (int k = 0; k < W; k++) x.w[k] = (uint32_t)__shfl_xor((int)x.w[k], mask, 64);
+    return __builtin_bit_cast(KeyT, x);
 }
 
 template <typename KeyT, int NT>
@@ -710,7 +744,7 @@ __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, co
             }
         } else {
             for (uint32_t c = lane; c < a.K; c += G)
-                best = Ops::min(best, Ops::from_u64(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V,
+                best = Ops::min(best, Ops::from_acc(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V,
                                                                       E, L, lsum, sig, r)));
         }
         for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));

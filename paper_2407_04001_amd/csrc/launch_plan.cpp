@@ -312,6 +312,9 @@ template pase_status build_launches<double>(pase_graph_t, char *, std::vector<La
                                             std::vector<Contrib> &);
 template pase_status build_launches<uint64_t>(pase_graph_t, char *, std::vector<Launch<uint64_t>> &,
                                               std::vector<Contrib> &);
+template pase_status build_launches<unsigned __int128>(pase_graph_t, char *,
+                                                       std::vector<Launch<unsigned __int128>> &,
+                                                       std::vector<Contrib> &);
 
 // ------------------------------------------------------------------ constant image and batches
 template <typename KeyT>
@@ -556,5 +559,6 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
 
 template pase_status build_image<double>(pase_graph_t, char *, char *, SearchImage &, bool);
 template pase_status build_image<uint64_t>(pase_graph_t, char *, char *, SearchImage &, bool);
+template pase_status build_image<unsigned __int128>(pase_graph_t, char *, char *, SearchImage &, bool);
 
 }  // namespace pase

@@ -754,16 +754,79 @@ def test_direct_fill_whole_workloads(P, name):
     _check_golden(P, name, 0, direct=ALL_DIRECT)
 
 
+# ------------------------------------------------------------------ key types at their edges (R10)
+@pytest.mark.parametrize("seed", range(3))
+def test_key_type_edges(P, seed):
+    """Caller-given costs near a magnitude M (dense ties), placed so that the
+    largest key bound sits just under 2^53 (fp64 keys), just over it (uint64),
+    just under 2^64 (uint64), just over it (128-bit keys), and at the largest M
+    whose cost bounds still fit 64 bits (128-bit keys, table values past
+    2^63): every table entry against the oracle with the same costs.  The
+    largest table value shifted by its position's argmin bits -- a key the
+    fill formed -- lies within 1% of the edge, so the fp64 arithmetic runs
+    next to 2^53 and the uint64 keys next to 2^64."""
+    import keyedge
+    g = random_graph(seed + 1200, n=5 + seed % 3, p=8, max_dims=3, extra_edges=2 + seed % 3)
+    pg0 = P.Graph(g)
+    pg0.enumerate_configs(8)
+    K = pg0.K
+    shapes = [(K[e["src"]], K[e["dst"]]) for e in g["edges"]]
+    m53 = keyedge.largest_m(P, pg0, seed, K, shapes, lambda kt: kt == 0)
+    m64 = keyedge.largest_m(P, pg0, seed, K, shapes, lambda kt: kt in (0, 1), lo=m53)
+    mov = keyedge.largest_m(P, pg0, seed, K, shapes, lambda kt: kt >= 0, lo=m64)
+    for M, kt, edge in ((m53, 0, 2 ** 53), (m53 + 1, 1, 2 ** 53), (m64, 1, 2 ** 64), (m64 + 1, 2, 2 ** 64),
+                        (mov, 2, None)):
+        say(f"key edge seed={seed + 1200} M={M} key_type={kt}")
+        costs = keyedge.near_costs(seed, K, shapes, M)
+        o = _oracle(g, costs=costs)
+        for direct in (None, 0):
+            pg, mc, strat = _run(P, g, costs=costs, direct=direct)
+            assert pg.stats()["key_type"] == kt
+            assert (mc, strat) == o.result()
+            _compare_all_entries(pg, o, g)
+        top = max(int(max(o.table(i)[0])) << max(0, (int(K[v]) - 1).bit_length())
+                  for i, v in enumerate(o.sequence()))
+        if edge is not None:
+            assert 0.99 * edge < top <= edge * 1.01, (M, kt, top)
+        else:
+            assert max(int(max(o.table(i)[0])) for i in range(len(K))) > 2 ** 63
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_forced_wide_keys_random_costs(P, seed):
+    """128-bit keys forced (PASE_OPT_KEY_TYPE 2) on random graphs with dense
+    ties: prep + generic fill in 16-byte keys, every entry against the oracle."""
+    g = random_graph(seed + 1300, n=4 + seed % 6, p=8, max_dims=3, extra_edges=1 + seed % 4)
+    say(f"forced 128-bit keys seed={seed + 1300}")
+    o0 = _oracle(g)
+    K = [int(k) for k in o0.K]
+    costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=4)
+    o = _oracle(g, costs=costs)
+    pg, mc, strat = _run(P, g, key=2, costs=costs, direct=None)
+    assert pg.stats()["key_type"] == 2
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g)
+    pg, mc, strat = _run(P, g, key=2)
+    assert pg.stats()["key_type"] == 2
+    assert (mc, strat) == o0.result()
+    _compare_all_entries(pg, o0, g)
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception"])
+def test_forced_wide_keys_against_golden(P, name):
+    _check_golden(P, name, 0, key=2)
+
+
 @pytest.mark.parametrize("block", range(4))
 def test_random_graph_sweep_schedules(P, block):
     """Seeded sweep over random graphs (4-13 vertices, 2-5 loop dims, p from 4
     to 64, sizes up to 4096): the level schedule (shared level launches), the
     bulk lane with every row vertex on the bulk stream, the sequential
     schedule and the level schedule without the direct fill all give the
-    oracle's minimum, strategy and every table (fingerprints).  A graph whose
-    worst-case key exceeds 64 bits is refused with OVERFLOW (key bound) and
-    skipped."""
+    oracle's minimum, strategy and every table (fingerprints).  No graph is
+    refused: those whose packed keys pass 64 bits run on 128-bit keys."""
     checked = 0
+    wide = 0
     for seed in range(block * 20, block * 20 + 20):
         rng = np.random.default_rng(seed)
         n = int(rng.integers(4, 14))
@@ -782,13 +845,11 @@ def test_random_graph_sweep_schedules(P, block):
                 pg.set_option(P.OPT_DIRECT_CELLS, direct)
             pg.set_option(P.OPT_KEEP_TABLES, 1)
             pg.enumerate_configs(p)
-            try:
-                mc, strat = pg.find_best_strategy()
-            except P.PaseError as e:
-                assert e.status == P.OVERFLOW, e
-                continue
+            mc, strat = pg.find_best_strategy()
             assert (mc, strat) == o.result(), (seed, sched)
             for i, v in enumerate(o.sequence()):
                 assert pg.fingerprint(v) == fps[i], (seed, sched, v)
             checked += 1
-    assert checked >= 60
+            wide += pg.stats()["key_type"] == 2
+    assert checked == 80
+    say(f"   {wide} runs on 128-bit keys")

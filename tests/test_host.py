@@ -340,7 +340,7 @@ def test_options_validate(pase):
     g = P.Graph(fc_chain())
     g.enumerate_configs(4)
     assert _status(lambda: g.set_option(P.OPT_KERNEL, 2)) == P.INVALID_ARGUMENT
-    assert _status(lambda: g.set_option(P.OPT_KEY_TYPE, 7)) == P.INVALID_ARGUMENT
+    assert _status(lambda: g.set_option(P.OPT_KEY_TYPE, 3)) == P.INVALID_ARGUMENT
     assert _status(lambda: g.set_option(99, 1)) == P.INVALID_ARGUMENT
     g.set_option(P.OPT_KEEP_TABLES, 1)
     g.set_option(P.OPT_KERNEL, 1)
@@ -400,3 +400,44 @@ def test_level_launch_unification(pase):
     distinct0 = {(x["tile_cols"], x["tile_rows"]) for x in shapes[0] if x["level"] == 0}
     distinct1 = {(x["tile_cols"], x["tile_rows"]) for x in shapes[1] if x["level"] == 0}
     assert len(distinct0) < len(distinct1)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_key_type_windows(pase, seed):
+    """Reading R10 on caller-given costs near a magnitude M: fp64 keys exactly
+    while the largest key bound (key_bound + 1) * 2^bits stays within 2^53,
+    uint64 keys within 2^64, 128-bit keys beyond while every cost bound fits
+    64 bits, and OVERFLOW from pase_override_costs once one does not -- with
+    the earlier costs' plan still in force.  128-bit plans run every vertex on
+    the generic kernel; key type 2 forces them."""
+    import keyedge
+    g = random_graph(seed + 1200, n=5 + seed % 3, p=8, max_dims=3, extra_edges=2 + seed % 3)
+    pg = pase.Graph(g)
+    pg.enumerate_configs(8)
+    K = pg.K
+    shapes = [(K[e["src"]], K[e["dst"]]) for e in g["edges"]]
+    m53 = keyedge.largest_m(pase, pg, seed, K, shapes, lambda kt: kt == 0)
+    keyedge.plan_key_type(pase, pg, seed, K, shapes, m53)
+    assert keyedge.key_top(pg, K) <= 1 << 53
+    assert keyedge.plan_key_type(pase, pg, seed, K, shapes, m53 + 1) == 1
+    assert keyedge.key_top(pg, K) > 1 << 53
+    m64 = keyedge.largest_m(pase, pg, seed, K, shapes, lambda kt: kt in (0, 1), lo=m53)
+    keyedge.plan_key_type(pase, pg, seed, K, shapes, m64)
+    assert keyedge.key_top(pg, K) <= 1 << 64
+    assert keyedge.plan_key_type(pase, pg, seed, K, shapes, m64 + 1) == 2
+    assert all(pg.vertex_info(v)["kernel"] == 0 for v in range(len(K)))
+    mov = keyedge.largest_m(pase, pg, seed, K, shapes, lambda kt: kt >= 0, lo=m64)
+    assert keyedge.plan_key_type(pase, pg, seed, K, shapes, mov) == 2
+    assert all(pg.vertex_info(v)["key_bound"] < (1 << 64) - 1 for v in range(len(K)))
+    # one past: OVERFLOW, and the plan of the costs at mov stays
+    assert keyedge.plan_key_type(pase, pg, seed, K, shapes, mov + 1) == -1
+    assert pg.vertex_info(0)["key_type"] == 2
+    assert pg.workspace_size() > 0
+    # back to small costs: fp64 keys and the row / direct kernels again
+    assert keyedge.plan_key_type(pase, pg, seed, K, shapes, 1000) == 0
+    # forced 128-bit keys re-plan on the generic kernel
+    pg.set_option(pase.OPT_KEY_TYPE, 2)
+    assert pg.vertex_info(0)["key_type"] == 2
+    assert all(pg.vertex_info(v)["kernel"] == 0 for v in range(len(K)))
+    pg.set_option(pase.OPT_KEY_TYPE, 0)
+    assert pg.vertex_info(0)["key_type"] == 0
