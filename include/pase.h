@@ -360,6 +360,15 @@ typedef struct {
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);
 
+/* Diagnostics (host only, no device work): build the kernel descriptors,
+ * batched launches and constant-region image that pase_find_best_strategy
+ * would upload for the current plan and costs, against a stand-in workspace
+ * address, into a host buffer of exactly the constant region's size, and
+ * check that every vertex is filled by exactly one launch.  *image_bytes
+ * receives that size.  Errors: BAD_STATE (no plan), INTERNAL (a region or
+ * table bound of the plan would be exceeded), TOO_LARGE (a launch grid). */
+pase_status pase_plan_check(pase_graph_t g, uint64_t *image_bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -48,6 +48,26 @@ def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
     return out
 
 
+# Host-only build of the planner (host.cpp, launch_plan.cpp) with a stub
+# device runtime, under AddressSanitizer and UBSan, for the CPU test suite.
+# The GPU library is never built this way: this is g++ on host sources only.
+SAN_LIB = os.path.join(ROOT, "_build", "libpase_host_san.so")
+SAN_FLAGS = ["-O1", "-g", "-std=c++17", "-fPIC", "-shared", "-fno-omit-frame-pointer",
+             "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-Wall", "-Wno-unused-function"]
+
+
+def build_host_sanitized(out: str = SAN_LIB, verbose: bool = False) -> str:
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    srcs = [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "device_stub.cpp")]
+    cmd = [os.environ.get("CXX", "g++"), *SAN_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           *srcs, "-o", out + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     build(verbose="-v" in sys.argv)
     print(LIB)

@@ -275,8 +275,6 @@ struct DeviceState {
     void *ws = nullptr;
     uint64_t ws_bytes = 0;
     bool owned = false;
-    void *lent = nullptr;
-    uint64_t lent_bytes = 0;
     void *pinned = nullptr;
     uint64_t pinned_bytes = 0;
     std::vector<hipEvent_t> ev;        // profiling: two per timed fill launch
@@ -313,21 +311,11 @@ static DeviceState *state(pase_graph_t g) {
     return g->dev;
 }
 
-pase_status device_set_workspace(pase_graph_t g, void *ptr, uint64_t bytes) {
-    DeviceState *d = state(g);
-    d->lent = ptr;
-    d->lent_bytes = ptr ? bytes : 0;
-    g->searched = false;
-    return PASE_OK;
-}
-
 static pase_status ensure_memory(pase_graph_t g, char **ws) {
     DeviceState *d = state(g);
     const uint64_t need = g->plan.total;
-    if (d->lent) {
-        if (d->lent_bytes < need)
-            return fail(g, PASE_ERR_OUT_OF_MEMORY, "lent workspace smaller than pase_workspace_size");
-        *ws = (char *)d->lent;
+    if (g->lent_ws) {
+        *ws = (char *)g->lent_ws;   // its size was checked before any device work
     } else {
         if (!d->owned || d->ws_bytes < need) {
             if (d->owned && d->ws) HIPCHK(hipFree(d->ws));

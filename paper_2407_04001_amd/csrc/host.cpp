@@ -1156,14 +1156,25 @@ extern "C" pase_status pase_set_workspace(pase_graph_t g, void *device_ptr, uint
     if (!g) return PASE_ERR_INVALID_ARGUMENT;
     if (device_ptr && ((uintptr_t)device_ptr % 256))
         return fail(g, PASE_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
-    return device_set_workspace(g, device_ptr, bytes);
+    g->lent_ws = device_ptr;
+    g->lent_bytes = device_ptr ? bytes : 0;
+    g->searched = false;
+    return PASE_OK;
 }
 
 extern "C" pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_cost,
                                                uint32_t *config_idx) {
     if (!g || !min_cost || !config_idx) return PASE_ERR_INVALID_ARGUMENT;
     if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    if (g->lent_ws && g->lent_bytes < g->plan.total)
+        return fail(g, PASE_ERR_OUT_OF_MEMORY, "lent workspace smaller than pase_workspace_size");
     return device_search(g, stream, min_cost, config_idx);
+}
+
+extern "C" pase_status pase_plan_check(pase_graph_t g, uint64_t *image_bytes) {
+    if (!g || !image_bytes) return PASE_ERR_INVALID_ARGUMENT;
+    if (!g->planned) return fail(g, PASE_ERR_BAD_STATE, "configurations not enumerated");
+    return plan_check(g, image_bytes);
 }
 
 extern "C" pase_status pase_find_best_strategy_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost,

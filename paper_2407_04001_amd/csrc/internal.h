@@ -306,6 +306,9 @@ struct pase_graph_s {
     bool searched = false;
     uint32_t key_type = 0;
     pase_run_stats stats{};
+    // a workspace lent by the caller (pase_set_workspace), else library-owned memory
+    void *lent_ws = nullptr;
+    uint64_t lent_bytes = 0;
     // device runtime
     pase::DeviceState *dev = nullptr;
 };
@@ -315,11 +318,14 @@ namespace pase {
 pase_status fail(pase_graph_t g, pase_status st, const std::string &msg);
 uint32_t choose_key_type(pase_graph_t g, pase_status *st);
 uint32_t key_bytes(pase_graph_t g);   // bytes of a table value / block key of the plan (8 or 16)
+// launch_plan.cpp: the launch descriptors and constant image of the plan's key
+// type, built against a stand-in workspace base into a host buffer of exactly
+// the constant region's size (no device work)
+pase_status plan_check(pase_graph_t g, uint64_t *image_bytes);
 // device.hip
 void device_release(pase_graph_t g);
 pase_status device_search(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);
 pase_status device_search_noalloc(pase_graph_t g, void *stream, uint64_t *min_cost, uint32_t *cfg);
-pase_status device_set_workspace(pase_graph_t g, void *ptr, uint64_t bytes);
 pase_status device_table_entry(pase_graph_t g, int pos, uint64_t idx, uint64_t *cost,
                                uint32_t *arg);
 pase_status device_fingerprint(pase_graph_t g, int pos, uint64_t *fpT, uint64_t *fpA);

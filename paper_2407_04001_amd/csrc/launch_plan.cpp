@@ -561,4 +561,32 @@ template pase_status build_image<double>(pase_graph_t, char *, char *, SearchIma
 template pase_status build_image<uint64_t>(pase_graph_t, char *, char *, SearchImage &, bool);
 template pase_status build_image<unsigned __int128>(pase_graph_t, char *, char *, SearchImage &, bool);
 
+pase_status plan_check(pase_graph_t g, uint64_t *image_bytes) {
+    // descriptors only hold device addresses: any base will do, nothing is
+    // read through it; the image buffer is exactly the constant region, so a
+    // write past it is a heap overflow (and a sanitizer build reports it)
+    char *fake_ws = (char *)(uintptr_t)(1ull << 40);
+    const uint64_t bytes = g->plan.off_cfg;
+    std::vector<char> img(bytes);
+    SearchImage si;
+    pase_status st = g->plan_key_type == 0   ? build_image<double>(g, fake_ws, img.data(), si)
+                     : g->plan_key_type == 1 ? build_image<uint64_t>(g, fake_ws, img.data(), si)
+                                             : build_image<unsigned __int128>(g, fake_ws, img.data(), si);
+    if (st != PASE_OK) return st;
+    // every vertex appears in exactly one fill batch (direct, row or generic)
+    std::vector<int> fills(g->plan.v.size(), 0);
+    const BatchEntry *be = (const BatchEntry *)(img.data() + g->plan.off_batch);
+    for (const Batch &b : si.batches)
+        if (b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect)
+            for (uint32_t k = 0; k < b.nentries; k++) {
+                const uint32_t pos = be[b.entry0 + k].pos;
+                if (pos >= fills.size()) return fail(g, PASE_ERR_INTERNAL, "batch entry out of range");
+                fills[pos]++;
+            }
+    for (int f : fills)
+        if (f != 1) return fail(g, PASE_ERR_INTERNAL, "a vertex is not filled exactly once");
+    *image_bytes = bytes;
+    return PASE_OK;
+}
+
 }  // namespace pase

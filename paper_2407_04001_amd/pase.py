@@ -73,7 +73,7 @@ EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_e
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
            "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get",
-           "pase_find_best_strategy_noalloc"]
+           "pase_find_best_strategy_noalloc", "pase_plan_check"]
 
 _lib = None
 
@@ -106,6 +106,7 @@ def load(path: str | None = None):
         "pase_set_workspace": (st, [P, P, U64]),
         "pase_find_best_strategy": (st, [P, P, P, P]),
         "pase_find_best_strategy_noalloc": (st, [P, P, P, P]),
+        "pase_plan_check": (st, [P, P]),
         "pase_table_entry": (st, [P, U32, P, P, P]),
         "pase_table_fingerprint": (st, [P, U32, P, P]),
         "pase_layer_costs": (st, [P, U32, P]),
@@ -276,6 +277,12 @@ def pase_vertex_info_get(h, v: int) -> dict:
     return x.as_dict()
 
 
+def pase_plan_check(h) -> int:
+    b = C.c_uint64()
+    _check(h, load().pase_plan_check(h, C.byref(b)))
+    return b.value
+
+
 # ------------------------------------------------------------------ convenience wrapper
 class Graph:
     """A computation graph handle.  ``graph`` is a dict in the layout of
@@ -373,3 +380,6 @@ class Graph:
 
     def vertex_info(self, v: int) -> dict:
         return pase_vertex_info_get(self.h, v)
+
+    def plan_check(self) -> int:
+        return pase_plan_check(self.h)

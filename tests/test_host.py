@@ -441,3 +441,52 @@ def test_key_type_windows(pase, seed):
     assert all(pg.vertex_info(v)["kernel"] == 0 for v in range(len(K)))
     pg.set_option(pase.OPT_KEY_TYPE, 0)
     assert pg.vertex_info(0)["key_type"] == 0
+
+
+PLAN_WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
+
+
+@pytest.mark.parametrize("name", PLAN_WORKLOADS)
+def test_plan_check_workloads(pase, name):
+    """The launch descriptors, batches and constant-region image of every
+    workload, for each schedule and key type, with and without the direct
+    fill and the kept tables: every region write in bounds and every vertex
+    filled by one launch (checked on the host, no device work)."""
+    g = workload(name)
+    pg = pase.Graph(g)
+    pg.enumerate_configs(g["p"])
+    for sched in (0, 1, 4):
+        for key in (0, 1, 2):
+            for direct, keep in ((None, 0), (0, 1)):
+                if name == "w4_transformer" and (key == 2 or direct == 0):
+                    continue   # the generic-only plan of 7e10 cells: covered by the smaller graphs
+                pg.set_option(pase.OPT_SCHEDULE, sched)
+                pg.set_option(pase.OPT_KEY_TYPE, key)
+                if direct is not None:
+                    pg.set_option(pase.OPT_DIRECT_CELLS, direct)
+                pg.set_option(pase.OPT_KEEP_TABLES, keep)
+                assert pg.plan_check() > 0
+                assert pg.vertex_info(0)["key_type"] == (key if key else pg.vertex_info(0)["key_type"])
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_plan_check_random_graphs(pase, seed):
+    """Seeded random graphs (2-5 loop dims, sizes up to 4096, p up to 64) and
+    caller-given costs: the launch image of every schedule and key type."""
+    rng = np.random.default_rng(seed + 40)
+    for k in range(6):
+        n = int(rng.integers(3, 12))
+        p = int(rng.choice([4, 8, 16, 32, 64]))
+        g = random_graph(seed * 100 + k + 7000, n=n, p=p, max_dims=int(rng.integers(2, 6)),
+                         extra_edges=int(rng.integers(0, 6)), max_size=int(rng.choice([8, 64, 512, 4096])))
+        pg = pase.Graph(g)
+        pg.enumerate_configs(p)
+        for sched in (0, 1, 4):
+            pg.set_option(pase.OPT_SCHEDULE, sched)
+            for key in (0, 2):
+                pg.set_option(pase.OPT_KEY_TYPE, key)
+                assert pg.plan_check() > 0
+        K = pg.K
+        costs = random_costs(seed + k, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=1 << 20)
+        pg.override_costs(*costs)
+        assert pg.plan_check() > 0
