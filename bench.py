@@ -54,8 +54,9 @@ def cpu_model():
 def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False, volume=False, grad=False):
     """The oracle on the host cores (OpenMP over table entries): the whole
     search when it has at most `max_cells` cells (else the prefix of the vertex
-    order that reaches that many), then single-threaded on a prefix of about
-    `single_cells` cells."""
+    order that reaches that many), and single-threaded on the longest prefix
+    of the vertex order with at most `single_cells` cells (at least one
+    vertex)."""
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
@@ -68,7 +69,15 @@ def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False,
             o.solve(max_cells=cells, threads=nthreads)
         return o.cells_done() / o.seconds(), o.cells_done(), o.seconds()
 
-    one, one_cells, one_s = run(max(1, int(single_cells)), 1)
+    # the sequence and table sizes (the first vertex only), then the prefix
+    run(1, 1)
+    cum, budget = 0, 0
+    for i, v in enumerate(o.sequence()):
+        cum += o.table_size(i) * int(o.K[v])
+        if i > 0 and cum > single_cells:
+            break
+        budget = cum
+    one, one_cells, one_s = run(max(1, budget), 1)
     total = o.cells()
     run(0 if total <= max_cells else int(max_cells), threads)
     done = o.cells_done()
@@ -88,7 +97,9 @@ def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False,
             "sample": f"{sample} ({done:.3e} of {total:.3e} cells, {o.seconds():.1f} s, "
                       f"OpenMP over table entries)",
             "whole_search": whole, "seconds": round(o.seconds(), 2),
-            "single_thread": {"value": one, "cells": one_cells, "seconds": round(one_s, 2)},
+            "single_thread": {"value": one, "cells": one_cells, "seconds": round(one_s, 2),
+                              "sample": f"the longest prefix of the {order} order with at most "
+                                        f"{single_cells:.1e} cells"},
             "cpu_model": cpu_model()}
 
 
