@@ -138,7 +138,7 @@ WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "
 
 
 def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu, p=None, all_integers=False,
-                 bf=False, volume=False, grad=False, schedule=None):
+                 bf=False, volume=False, grad=False, schedule=None, no_roofline=False):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
@@ -184,21 +184,20 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
         return {"metric": metric, "value": None, "unit": "cell-updates/s", "n_gpus": 1, "steps": 0,
                 "warmup": 0, "higher_is_better": True, "data": "synthetic", "config": config,
                 "refused": str(e)}
-    # HIP events on the dominant kernel's launches only (the row kernel with a
-    # column chunk per lane), so the timed steps carry as few events as the
-    # roofline needs
-    pg.set_option(OPT_PROFILE, 2)
     stream = torch.cuda.current_stream()
 
     def step():
         pg.enumerate_configs(p)
         return pg.find_best_strategy(stream)
 
+    # timed steps: no timing events at all (each event attached to a launch or
+    # recorded between launches costs the stream ~4.4 us of serialization)
+    pg.set_option(OPT_PROFILE, 0)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    walls, rows_ms, rows_launches, step_ms = [], 0.0, 0, []
-    phase_keys = ("seq_ms", "plan_ms", "setup_ms", "cost_tables_ms", "fill_span_ms", "backtrack_ms")
+    walls, step_ms = [], []
+    phase_keys = ("seq_ms", "plan_ms", "setup_ms")
     phases = dict.fromkeys(phase_keys, 0.0)
     t0 = time.perf_counter()
     for _ in range(steps):
@@ -209,17 +208,40 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
         walls.append(st["wall_ms"])
         for k in phase_keys:
             phases[k] += st[k] / steps
-        # the dominant kernel: the row kernel with a column chunk per lane (the
-        # only launches timed; its column-less form is not)
-        rows_ms += st["rows_fill_ms"]
-        rows_launches += st["rows_launches"]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+
+    # profiled steps, right after the timed ones: the same searches with HIP
+    # events (on the search stream) attached to every launch of the dominant
+    # kernel -- the row kernel with a column chunk per lane -- and recorded at
+    # the phase boundaries; they give the roofline and the device phases
+    rows_ms, rows_launches, prof_ms = 0.0, 0, []
+    if no_roofline:
+        prof_steps = 0
+    else:
+        prof_steps = steps
+        pg.set_option(OPT_PROFILE, 2)
+        step()
+        torch.cuda.synchronize()
+    dev_keys = ("cost_tables_ms", "fill_span_ms", "backtrack_ms")
+    dev_phases = dict.fromkeys(dev_keys, 0.0)
+    for _ in range(prof_steps):
+        ts = time.perf_counter()
+        pmc, pstrat = step()
+        prof_ms.append((time.perf_counter() - ts) * 1e3)
+        assert (pmc, pstrat) == (mc, strat)
+        pst = pg.stats()
+        rows_ms += pst["rows_fill_ms"]
+        rows_launches += pst["rows_launches"]
+        for k in dev_keys:
+            dev_phases[k] += pst[k] / prof_steps
+    torch.cuda.synchronize()
+    phases.update(dev_phases)
 
     cells = st["cells"]
     col_cells = st["rows_cells"] - st["stream_cells"]
     ops = OPS_PER_CELL if st["key_type"] == 0 else OPS_PER_CELL_U64
-    achieved = ops * col_cells * steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
+    achieved = ops * col_cells * prof_steps / (rows_ms / 1e3) / 1e12 if rows_ms else 0.0
     t_roof_ms = ops * cells / (FP64_OPS_PEAK_T * 1e12) * 1e3
     parity = None
     # the oracle's stored answer for exactly this variant, if one was written
@@ -249,9 +271,11 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
         "dtype": "f64" if st["key_type"] == 0 else "u64", "data": "synthetic",
         "config": dict(config, cells=cells, schedule=SCHEDULES.get(st["schedule"], st["schedule"])),
         "find_best_strategy_ms": sum(walls) / len(walls),
-        # mean per step: host GenerateSeq / plans (enumerate), host launch
-        # setup, and the device phases timed with events on the search stream
+        # mean per step: host GenerateSeq / plans (enumerate) and launch setup
+        # of the timed steps; device phases of the profiled steps (events on
+        # the search stream)
         "phases_ms": {k[:-3]: round(v, 4) for k, v in phases.items()},
+        "profiled_ms_per_step": sorted(prof_ms)[len(prof_ms) // 2] if prof_ms else None,
         "median_ms_per_step": sorted(step_ms)[len(step_ms) // 2],
         # the whole search against the ALU roofline: every cell costs `ops` VALU
         # lane-ops (t_roof), against the fill-kernel time and the step
@@ -265,7 +289,9 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
                      "traffic": traffic_from_profile() if headline else None,
                      "launches_per_step": rows_launches // steps,
                      "avg_launch_us": rows_ms * 1e3 / max(rows_launches, 1),
-                     "cells_per_step": col_cells},
+                     "cells_per_step": col_cells,
+                     "timed_in": f"{steps} profiled steps after the timed ones (HIP events on the search "
+                                 "stream around every launch of the kernel)"},
     }
     if not no_cpu:
         out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), int(cpu_single_cells), all_integers, bf,
@@ -298,6 +324,8 @@ def main():
                     help="transfer cost model: split match (default) or volume intersection")
     ap.add_argument("--grad-sync", action="store_true",
                     help="add the weight-gradient all-reduce to the layer costs")
+    ap.add_argument("--no-roofline", action="store_true",
+                    help="skip the profiled steps (no HIP events at all; for traces of the timed steps)")
     ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 4),
                     help="launch schedule (PASE_OPT_SCHEDULE; default: the library's)")
     args = ap.parse_args()
@@ -317,7 +345,7 @@ def main():
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.cpu_single_cells,
                            args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
-                           args.transfer == "volume", args.grad_sync, args.schedule)
+                           args.transfer == "volume", args.grad_sync, args.schedule, args.no_roofline)
         print(json.dumps(out), flush=True)
 
 
