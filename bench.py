@@ -51,7 +51,8 @@ def cpu_model():
     return "unknown"
 
 
-def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False, volume=False, grad=False):
+def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False, volume=False, grad=False,
+                    halo=False):
     """The oracle on the host cores (OpenMP over table entries): the whole
     search when it has at most `max_cells` cells (else the prefix of the vertex
     order that reaches that many), and single-threaded on the longest prefix
@@ -60,7 +61,7 @@ def oracle_baseline(g, p, max_cells, single_cells, all_integers=False, bf=False,
     from oracle.oracle import Oracle
     threads = cpu_threads()
     o = Oracle(g)
-    o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad)
+    o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad, halo=halo)
 
     def run(cells, nthreads):
         if bf:
@@ -138,7 +139,7 @@ WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "
 
 
 def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu, p=None, all_integers=False,
-                 bf=False, volume=False, grad=False, schedule=None, no_roofline=False):
+                 bf=False, volume=False, grad=False, schedule=None, no_roofline=False, halo=False):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
@@ -149,7 +150,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
     on a prefix of about `cpu_single_cells` cells).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import OPT_GRAD_SYNC, OPT_ORDER, OPT_PROFILE, OPT_SCHEDULE, OPT_TRANSFER, Graph, PaseError
+    from paper_2407_04001_amd import (OPT_GRAD_SYNC, OPT_HALO, OPT_ORDER, OPT_PROFILE, OPT_SCHEDULE, OPT_TRANSFER,
+                                      Graph, PaseError)
     from workloads import workload
 
     g = workload(name, seed)
@@ -158,6 +160,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
     pg.set_option(OPT_ORDER, int(bf))
     pg.set_option(OPT_TRANSFER, int(volume))
     pg.set_option(OPT_GRAD_SYNC, int(grad))
+    pg.set_option(OPT_HALO, int(halo))
     if schedule is not None:
         pg.set_option(OPT_SCHEDULE, schedule)
     wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
@@ -169,14 +172,16 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
         wl += ", volume-intersection transfer costs"
     if grad:
         wl += ", weight-gradient all-reduce"
+    if halo:
+        wl += ", halo exchange"
     headline = (name == "w4_transformer" and p == g["p"] and not all_integers and not bf and not volume
-                and not grad)
+                and not grad and not halo)
     metric = METRIC if headline else f"DP cell-updates/sec and FindBestStrategy wall time ({wl})"
     config = {"workload": g["name"], "p": p,
               "config_set": "every integer split" if all_integers else "powers of two",
               "order": "breadth-first" if bf else "GenerateSeq",
               "transfer": "volume intersection" if volume else "split match",
-              "grad_sync": grad,
+              "grad_sync": grad, "halo": halo,
               "vertices": len(g["vertices"]), "edges": len(g["edges"]), "seed": seed}
     try:
         pg.enumerate_configs(p, all_integers=all_integers)
@@ -246,7 +251,9 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
     parity = None
     # the oracle's stored answer for exactly this variant, if one was written
     gold_name = None
-    if sum((bf, volume, grad, all_integers)) <= 1:
+    if halo and not (bf or volume or all_integers):
+        gold_name = f"{name}_seed{seed}_{'grad_' if grad else ''}halo.json"
+    elif sum((bf, volume, grad, all_integers)) <= 1:
         if bf:
             gold_name = f"{name}_seed{seed}_p{p}_bf.json"
         elif volume:
@@ -295,7 +302,7 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
     }
     if not no_cpu:
         out["cpu_baseline"] = oracle_baseline(g, p, int(cpu_cells), int(cpu_single_cells), all_integers, bf,
-                                              volume, grad)
+                                              volume, grad, halo)
     return out
 
 
@@ -324,6 +331,7 @@ def main():
                     help="transfer cost model: split match (default) or volume intersection")
     ap.add_argument("--grad-sync", action="store_true",
                     help="add the weight-gradient all-reduce to the layer costs")
+    ap.add_argument("--halo", action="store_true", help="add the halo exchange of convolutions to the layer costs")
     ap.add_argument("--no-roofline", action="store_true",
                     help="skip the profiled steps (no HIP events at all; for traces of the timed steps)")
     ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 4),
@@ -345,7 +353,7 @@ def main():
         out = run_workload(name, args.seed, args.steps, args.warmup, args.cpu_cells, args.cpu_single_cells,
                            args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
-                           args.transfer == "volume", args.grad_sync, args.schedule, args.no_roofline)
+                           args.transfer == "volume", args.grad_sync, args.schedule, args.no_roofline, args.halo)
         print(json.dumps(out), flush=True)
 
 

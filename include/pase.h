@@ -65,7 +65,11 @@ typedef enum {
  * weight_mask bit k marks loop dim k as an index of the layer's weight tensor,
  * which holds weight_per_point words per point of those dims (kh*kw for a
  * convolution's (co, ci)); 0 = no weights.  Read only with
- * PASE_OPT_GRAD_SYNC. */
+ * PASE_OPT_GRAD_SYNC.  Convolution geometry, read only with PASE_OPT_HALO:
+ * input_mask bit k marks loop dim k as an index of the layer's input tensor
+ * ((b, ci, h, w) of a convolution over (b, co, ci, h, w)); halo[k] is the
+ * halo width along loop dim k (floor(kernel extent / 2) on a spatial dim, 0
+ * elsewhere); a nonzero halo[k] needs bit k of input_mask. */
 typedef struct {
     uint32_t ndims;
     uint64_t size[PASE_MAX_DIMS];
@@ -73,6 +77,8 @@ typedef struct {
     uint64_t flops_per_point;
     uint32_t weight_mask;
     uint64_t weight_per_point;
+    uint32_t input_mask;
+    uint32_t halo[PASE_MAX_DIMS];
 } pase_vertex_desc;
 
 /* One edge = a tensor flowing from src to dst (Sec. II).  Tensor dim k is
@@ -176,8 +182,18 @@ typedef enum {
                                    qualify (so that it saves launches; any vertex under the
                                    sequential schedule).  Default 2^18; 0 = never.  Not used with
                                    PASE_OPT_KERNEL = 1 */
-    PASE_OPT_BULK_US = 17       /* schedule 4: planned fill time (microseconds) from which a
+    PASE_OPT_BULK_US = 17,      /* schedule 4: planned fill time (microseconds) from which a
                                    row-kernel vertex runs on the bulk stream (default 100) */
+    PASE_OPT_HALO = 19          /* 1: the next pase_enumerate_configs adds the halo exchange of
+                                   convolutions to every layer cost (an assumed form; the paper
+                                   counts halo communication in t_l but prints no formula): for
+                                   every loop dim k with halo[k] > 0 that the configuration
+                                   splits, each part receives halo[k] boundary rows of the input
+                                   from each of its two neighbours along k, a row being the
+                                   part's share of the input tensor over its other dims:
+                                   2 * halo[k] * ceil(prod_{j in input, j != k} n_j /
+                                   prod_{j in input, j != k} s_j) words, weighted by r.
+                                   0 (default): the benchmark's cost model */
 } pase_option;
 
 /* Search statistics of the last pase_find_best_strategy call. */

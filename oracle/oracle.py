@@ -48,6 +48,8 @@ def _load(path: str | None = None):
     L.oracle_set_transfer_model.argtypes = [P, I]
     L.oracle_set_weights.argtypes = [P, P, P]
     L.oracle_set_grad_sync.argtypes = [P, I]
+    L.oracle_set_halo.argtypes = [P, P, P]
+    L.oracle_set_halo_model.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
     L.oracle_solve_bf.argtypes = [P, U64, I]
@@ -121,6 +123,14 @@ class Oracle:
                 wmask[i] |= np.uint32(1 << k)
             wpp[i] = v.get("weight_per_point", 0)
         self._check(L.oracle_set_weights(self._h, _ptr(wmask), _ptr(wpp)))
+        halo = np.zeros((nv, MAXD), dtype=np.uint32)
+        imask = np.zeros(nv, dtype=np.uint32)
+        for i, v in enumerate(vs):
+            for k, w in enumerate(v.get("halo", [])):
+                halo[i, k] = w
+            for k in v.get("input_dims", []):
+                imask[i] |= np.uint32(1 << k)
+        self._check(L.oracle_set_halo(self._h, _ptr(halo), _ptr(imask)))
         self.ndims = ndims
         self.p = None
 
@@ -135,14 +145,17 @@ class Oracle:
         return rc
 
     # -- configurations and costs
-    def configs(self, p: int, all_integers: bool = False, volume: bool = False, grad_sync: bool = False):
+    def configs(self, p: int, all_integers: bool = False, volume: bool = False, grad_sync: bool = False,
+                halo: bool = False):
         """C(v) for p devices: power-of-two splits (p = 2^L), or with
         all_integers every tuple of positive integers with product <= p; the
         transfer costs follow the split-match model, or with `volume` the
         volume-intersection model; grad_sync adds the weight-gradient
-        all-reduce to the layer costs."""
+        all-reduce to the layer costs, halo the halo exchange of
+        convolutions."""
         self._check(self._L.oracle_set_transfer_model(self._h, 1 if volume else 0))
         self._check(self._L.oracle_set_grad_sync(self._h, 1 if grad_sync else 0))
+        self._check(self._L.oracle_set_halo_model(self._h, 1 if halo else 0))
         fn = self._L.oracle_configs_all if all_integers else self._L.oracle_configs
         self._check(fn(self._h, int(p)))
         self.p = p

@@ -49,6 +49,9 @@ typedef struct {
     int grad_sync;           /* 1: layer cost adds the weight-gradient all-reduce */
     uint32_t *weight_mask;   /* nv: loop dims indexing the layer's weights (0: none) */
     uint64_t *wpp;           /* nv: weight words per point of those dims */
+    int halo_model;          /* 1: layer cost adds the halo exchange of convolutions */
+    uint32_t *halo;          /* nv*MAXD: halo width of each loop dim (0: none) */
+    uint32_t *in_mask;       /* nv: loop dims indexing the layer's input tensor */
     /* configurations */
     int p;
     int *K;                  /* configs per vertex */
@@ -99,6 +102,8 @@ oracle_t *oracle_new(int nv, const int *ndims, const uint64_t *sizes, const uint
     o->fpp = calloc(nv, sizeof(uint64_t));
     o->weight_mask = calloc(nv, sizeof(uint32_t));
     o->wpp = calloc(nv, sizeof(uint64_t));
+    o->halo = calloc((size_t)nv * MAXD, sizeof(uint32_t));
+    o->in_mask = calloc(nv, sizeof(uint32_t));
     for (int v = 0; v < nv; v++) {
         o->ndims[v] = ndims[v];
         for (int k = 0; k < ndims[v]; k++) o->size[v * MAXD + k] = sizes[v * MAXD + k];
@@ -159,6 +164,7 @@ void oracle_free(oracle_t *o) {
     for (int v = 0; v < o->nv; v++) free(o->nbr[v]);
     free(o->nbr); free(o->deg);
     free(o->size); free(o->reduce_mask); free(o->fpp); free(o->weight_mask); free(o->wpp);
+    free(o->halo); free(o->in_mask);
     free(o->src); free(o->dst); free(o->rank); free(o->src_dim); free(o->dst_dim); free(o->elems);
     free(o);
 }
@@ -192,7 +198,8 @@ static int enum_rec(int d, int k, uint64_t budget, int pow2, uint32_t *cur, uint
  * (comm is the partial-sum reduction a split contraction dim requires.)
  * With grad_sync, t_l also carries the data-parallel weight-gradient
  * all-reduce (an assumed form, as the paper prints no formula; see
- * oracle_set_grad_sync). */
+ * oracle_set_grad_sync); with the halo model, the halo exchange of a
+ * convolution (oracle_set_halo_model). */
 static int layer_cost(oracle_t *o, int v, const uint32_t *s, uint64_t *out) {
     uint64_t flops = o->fpp[v], P = 1, red_split = 1, keep_n = 1, keep_split = 1;
     for (int k = 0; k < o->ndims[v]; k++) {
@@ -231,8 +238,52 @@ static int layer_cost(oracle_t *o, int v, const uint32_t *s, uint64_t *out) {
         uint64_t grad;
         if (words >> 64 || !mul_ok(o->r, (uint64_t)words, &grad) || !add_ok(total, grad, &total)) return 0;
     }
+    if (o->halo_model) {
+        /* a part along loop dim k (halo width w, the kernel's half extent
+         * along an input spatial dim) needs w boundary rows of the input from
+         * each of its two neighbours once dim k is split; a row spans the
+         * part's share of the input tensor over its other dims */
+        for (int k = 0; k < o->ndims[v]; k++) {
+            uint64_t w = o->halo[v * MAXD + k];
+            if (w == 0 || s[k] == 1) continue;
+            uint64_t rest = 1, rest_split = 1, words, cost;
+            for (int j = 0; j < o->ndims[v]; j++) {
+                if (j == k || !(o->in_mask[v] >> j & 1u)) continue;
+                if (!mul_ok(rest, o->size[v * MAXD + j], &rest)) return 0;
+                rest_split *= s[j];
+            }
+            if (!mul_ok(2 * w, ceil_div(rest, rest_split), &words)) return 0;
+            if (!mul_ok(o->r, words, &cost) || !add_ok(total, cost, &total)) return 0;
+        }
+    }
     *out = total;
     return 1;
+}
+
+/* Convolution geometry of the layers: halo[v*MAXD+k] = halo width of loop dim
+ * k of v (0: none), in_mask[v] = loop dims indexing v's input tensor.  Used by
+ * the halo term. */
+int oracle_set_halo(oracle_t *o, const uint32_t *halo, const uint32_t *in_mask) {
+    for (int v = 0; v < o->nv; v++) {
+        if (in_mask[v] >> o->ndims[v]) return fail(o, "input dim out of range");
+        for (int k = 0; k < MAXD; k++) {
+            uint32_t w = halo[v * MAXD + k];
+            if (w && (k >= o->ndims[v] || !(in_mask[v] >> k & 1u))) return fail(o, "halo on a non-input dim");
+            o->halo[v * MAXD + k] = w;
+        }
+        o->in_mask[v] = in_mask[v];
+    }
+    return 0;
+}
+
+/* 1: the next configuration enumeration adds the halo exchange of
+ * convolutions to every layer cost.  The paper lists halo communication among
+ * the intra-layer communication of t_l without printing a formula; this
+ * oracle takes the exchange of w rows with both neighbours along each split
+ * halo dim, in words per device. */
+int oracle_set_halo_model(oracle_t *o, int on) {
+    o->halo_model = on != 0;
+    return 0;
 }
 
 /* Weight tensors of the layers: mask[v] = loop dims indexing v's weights,

@@ -67,6 +67,8 @@ bool cost_bounds(pase_graph_t g, std::vector<uint64_t> *qmax, std::vector<uint64
                 uint64_t c = (F + p - 1) / p;
                 if ((d.reduce_mask >> k) & 1u) c += g->r * (p - 1) * g->keep_n[v];
                 if (W && !((d.weight_mask >> k) & 1u)) c += g->r * (2 * W - 2 * W / p);
+                // the halo of the split dim itself: the other input dims are unsplit
+                if (g->halo && d.halo[k]) c += g->r * 2 * (uint64_t)d.halo[k] * g->halo_n[v][k];
                 lo = std::min(lo, c);
             }
         }
@@ -127,6 +129,10 @@ extern "C" pase_status pase_graph_create(const pase_vertex_desc *v, uint32_t nv,
             if (v[i].size[k] == 0) return PASE_ERR_INVALID_ARGUMENT;
         if (v[i].reduce_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
         if (v[i].weight_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
+        if (v[i].input_mask >> v[i].ndims) return PASE_ERR_INVALID_ARGUMENT;
+        for (uint32_t k = 0; k < kMaxDims; k++)
+            if (v[i].halo[k] && (k >= v[i].ndims || !((v[i].input_mask >> k) & 1u) || v[i].halo[k] > (1u << 16)))
+                return PASE_ERR_INVALID_ARGUMENT;
     }
     for (uint32_t k = 0; k < ne; k++) {
         const pase_edge_desc &d = e[k];
@@ -906,6 +912,8 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->K.assign(nv, 0);
     g->ex.assign(nv, nullptr);
     g->weight_n.assign(nv, 0);
+    g->halo = g->halo_opt == 1;
+    g->halo_n.assign(nv, {});
     g->flops.assign(nv, 0);
     g->keep_n.assign(nv, 0);
     g->maxL.assign(nv, 0);
@@ -968,6 +976,22 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
             if (w >> 60 || !mul_ok(g->r, 2 * w, &gr) || !add_ok(m, gr, &m))
                 return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 64 bits");
             g->weight_n[v] = w;
+        }
+        g->halo_n[v].fill(0);
+        if (g->halo) {
+            // halo term: per halo dim k, I_k = prod of the other input dims'
+            // sizes; t_l grows by at most r * 2 * halo[k] * I_k per dim
+            const pase_vertex_desc &vd = g->V[v];
+            for (uint32_t k = 0; k < d; k++) {
+                if (!vd.halo[k]) continue;
+                uint64_t I = 1, hw;
+                for (uint32_t j = 0; j < d; j++)
+                    if (j != k && ((vd.input_mask >> j) & 1u) && !mul_ok(I, vd.size[j], &I))
+                        return fail(g, PASE_ERR_OVERFLOW, "input tensor exceeds 64 bits");
+                if (I >> 62 || !mul_ok(2ull * vd.halo[k], I, &hw) || !mul_ok(g->r, hw, &hw) || !add_ok(m, hw, &m))
+                    return fail(g, PASE_ERR_OVERFLOW, "layer cost exceeds 64 bits");
+                g->halo_n[v][k] = I;
+            }
         }
         g->maxL[v] = m;
     }
@@ -1075,6 +1099,10 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
     case PASE_OPT_BULK_US:
         if (value > 1000000000ull) return fail(g, PASE_ERR_INVALID_ARGUMENT, "bulk threshold <= 1e9 us");
         g->bulk_us = (uint32_t)value;
+        break;
+    case PASE_OPT_HALO:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "halo 0 or 1");
+        g->halo_opt = (uint32_t)value;
         break;
     case PASE_OPT_GRAD_SYNC:
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "grad sync 0 or 1");

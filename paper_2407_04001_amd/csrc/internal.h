@@ -10,6 +10,7 @@
 // dependent set in the table's own memory order.
 #pragma once
 
+#include <array>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -37,7 +38,11 @@ struct DevVertex {            // configuration data of one vertex (uploaded once
                               // per-configuration device byte its exponent sum; 1: both
                               // hold the factors / device count themselves (p <= 255)
     uint64_t weight_n;        // gradient term: words of the weight tensor (0: no term)
-    uint32_t weight_mask, pad;
+    uint32_t weight_mask;
+    uint32_t halo_mask;       // halo term: loop dims with a halo (0: no term)
+    uint32_t input_mask;      // halo term: loop dims indexing the input tensor
+    uint32_t halo_w[kMaxDims];   // halo width per loop dim
+    uint64_t halo_n[kMaxDims];   // halo term: prod of the input dims' sizes other than this one
 };
 
 struct DevEdge {
@@ -275,6 +280,10 @@ struct pase_graph_s {
     uint32_t config_set = 0;        // pase_option PASE_OPT_CONFIG_SET, read by pase_enumerate_configs
     uint32_t transfer_opt = 0;      // pase_option PASE_OPT_TRANSFER, read by pase_enumerate_configs
     uint32_t grad_opt = 0;          // pase_option PASE_OPT_GRAD_SYNC, read by pase_enumerate_configs
+    uint32_t halo_opt = 0;          // pase_option PASE_OPT_HALO, read by pase_enumerate_configs
+    bool halo = false;              // the enumerated layer costs carry the halo term
+    std::vector<std::array<uint64_t, pase::kMaxDims>> halo_n;   // halo term: per vertex and loop dim, the
+                                    // product of the input dims' sizes other than that dim
     uint64_t direct_cells = 1ull << 18;  // pase_option PASE_OPT_DIRECT_CELLS
     uint32_t bulk_us = 100;         // pase_option PASE_OPT_BULK_US
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)

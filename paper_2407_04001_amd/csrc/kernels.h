@@ -91,7 +91,26 @@ __device__ __forceinline__ uint64_t ceil_div_u64(uint64_t a, uint32_t b) { retur
 // into shards of S = ceil(weight_n / P_w) words by the splits of its dims and
 // each shard lives on the R = P / P_w devices that differ in the other dims;
 // a ring all-reduce moves ceil(2 (R - 1) S / R) = 2S - floor(2S / R) words.
+// Optional halo term: for every split loop dim k with a halo of width w, each
+// part receives w boundary rows of the input from both neighbours along k; a
+// row is the part's share of the input over its other dims:
+// 2 w ceil(halo_n[k] / (product of the other input dims' splits)) words.
+__device__ __forceinline__ uint64_t halo_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
+    uint64_t words = 0;
+    for (uint32_t k = 0; k < dv.ndims; k++) {
+        if (!((dv.halo_mask >> k) & 1u) || ex[k] == (dv.factors ? 1 : 0)) continue;
+        uint32_t S = dv.factors ? 1 : 0;
+        for (uint32_t j = 0; j < dv.ndims; j++)
+            if (j != k && ((dv.input_mask >> j) & 1u)) S = dv.factors ? S * ex[j] : S + ex[j];
+        const uint64_t part = dv.factors ? ceil_div_u64(dv.halo_n[k], S)
+                                         : (dv.halo_n[k] + ((1ull << S) - 1)) >> S;
+        words += 2ull * dv.halo_w[k] * part;
+    }
+    return r * words;
+}
+
 __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_t *ex, uint64_t r) {
+    const uint64_t halo = dv.halo_mask ? halo_cost(dv, ex, r) : 0;
     if (dv.factors) {
         uint32_t P = 1, red = 1, Pw = 1;
         for (uint32_t k = 0; k < dv.ndims; k++) {
@@ -104,7 +123,7 @@ __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_
             const uint64_t S2 = 2 * ceil_div_u64(dv.weight_n, Pw);
             cost += r * (S2 - S2 / (P / Pw));
         }
-        return cost;
+        return cost + halo;
     }
     uint32_t E = 0, ered = 0, ew = 0;
     for (uint32_t k = 0; k < dv.ndims; k++) {
@@ -120,7 +139,7 @@ __device__ __forceinline__ uint64_t layer_cost(const DevVertex &dv, const uint8_
         const uint64_t S2 = 2 * ((dv.weight_n + ((1ull << ew) - 1)) >> ew);
         cost += r * (S2 - (S2 >> (E - ew)));
     }
-    return cost;
+    return cost + halo;
 }
 
 // Device byte of one configuration: the exponent sum log2(P) of power-of-two

@@ -371,6 +371,14 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         x.factors = g->factors ? 1 : 0;
         x.weight_n = g->weight_n[v];
         x.weight_mask = g->V[v].weight_mask;
+        if (g->halo) {
+            x.input_mask = g->V[v].input_mask;
+            for (uint32_t k = 0; k < kMaxDims; k++) {
+                x.halo_w[k] = g->V[v].halo[k];
+                x.halo_n[k] = g->halo_n[v][k];
+                if (x.halo_w[k]) x.halo_mask |= 1u << k;
+            }
+        }
         loff += g->K[v];
     }
     si.nL = loff;

@@ -22,12 +22,14 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STAT
 (OPT_KEEP_TABLES, OPT_MEMORY_BUDGET, OPT_KERNEL, OPT_KEY_TYPE, OPT_PROFILE, OPT_SCHEDULE,
  OPT_TILE_COLS, OPT_TILE_ROWS, OPT_TILE_PARTS, OPT_C_SPLITS) = range(1, 11)
 (OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER, OPT_GRAD_SYNC, OPT_DIRECT_CELLS, OPT_BULK_US) = range(12, 18)
+OPT_HALO = 19
 SCHEDULE_LEVEL, SCHEDULE_SEQUENTIAL, SCHEDULE_BULK = 0, 1, 4
 
 
 class VertexDesc(C.Structure):
     _fields_ = [("ndims", C.c_uint32), ("size", C.c_uint64 * MAX_DIMS), ("reduce_mask", C.c_uint32),
-                ("flops_per_point", C.c_uint64), ("weight_mask", C.c_uint32), ("weight_per_point", C.c_uint64)]
+                ("flops_per_point", C.c_uint64), ("weight_mask", C.c_uint32), ("weight_per_point", C.c_uint64),
+                ("input_mask", C.c_uint32), ("halo", C.c_uint32 * MAX_DIMS)]
 
 
 class EdgeDesc(C.Structure):
@@ -153,6 +155,9 @@ def pase_graph_create(vertices, edges, comm_weight: int = 8, seq_rule: int = 0):
         V[i].flops_per_point = int(v["flops_per_point"])
         V[i].weight_mask = sum(1 << int(k) for k in v.get("weight_dims", []))
         V[i].weight_per_point = int(v.get("weight_per_point", 0))
+        V[i].input_mask = sum(1 << int(k) for k in v.get("input_dims", []))
+        for k, w in enumerate(v.get("halo", [])):
+            V[i].halo[k] = int(w)
     E = (EdgeDesc * max(ne, 1))()
     for i, e in enumerate(edges):
         E[i].src, E[i].dst, E[i].rank = int(e["src"]), int(e["dst"]), len(e["src_dim"])

@@ -7,7 +7,7 @@ strategy, the cell count, per-vertex fingerprints of the cost and argmin
 tables (canonical order, SplitMix64-based, see ``pase.h``) and a seeded sample
 of table entries.
 
-    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only] [--volume-only] [--grad-only]
+    python tests/golden/make_golden.py [--only NAME] [--threads N] [--all-integers-only] [--bf-only] [--volume-only] [--grad-only] [--halo-only]
 """
 from __future__ import annotations
 
@@ -30,10 +30,11 @@ from workloads import workload  # noqa: E402
 # p); `all_integers` enumerates Sec. II's full C(v); `bf` solves the
 # breadth-first recurrence (2) instead of GenerateSeq + recurrence (4);
 # `volume` prices transfers with the volume-intersection model; `grad` adds the
-# weight-gradient all-reduce to the layer costs.
-def _inst(name, seed=0, p=None, all_integers=False, bf=False, volume=False, grad=False):
+# weight-gradient all-reduce to the layer costs; `halo` the halo exchange of
+# convolutions.
+def _inst(name, seed=0, p=None, all_integers=False, bf=False, volume=False, grad=False, halo=False):
     return {"name": name, "seed": seed, "p": p, "all_integers": all_integers, "bf": bf, "volume": volume,
-            "grad": grad}
+            "grad": grad, "halo": halo}
 
 
 INSTANCES = [_inst("w0_fc_chain"), _inst("w1_residual_cnn"), _inst("w1_residual_cnn", 1),
@@ -45,11 +46,15 @@ INSTANCES = [_inst("w0_fc_chain"), _inst("w1_residual_cnn"), _inst("w1_residual_
              _inst("w1_residual_cnn", volume=True), _inst("w2_inception", volume=True),
              _inst("w3_lstm_grid", volume=True), _inst("w4_transformer", volume=True),
              _inst("w1_residual_cnn", grad=True), _inst("w2_inception", grad=True),
-             _inst("w3_lstm_grid", grad=True), _inst("w4_transformer", grad=True)]
+             _inst("w3_lstm_grid", grad=True), _inst("w4_transformer", grad=True),
+             _inst("w1_residual_cnn", halo=True), _inst("w2_inception", halo=True),
+             _inst("w1_residual_cnn", grad=True, halo=True), _inst("w2_inception", grad=True, halo=True)]
 
 
 def file_name(name: str, seed: int, p=None, all_integers: bool = False, bf: bool = False,
-              volume: bool = False, grad: bool = False) -> str:
+              volume: bool = False, grad: bool = False, halo: bool = False) -> str:
+    if halo:
+        return f"{name}_seed{seed}_{'grad_' if grad else ''}halo.json"
     if bf:
         return f"{name}_seed{seed}_p{p}_bf.json"
     if volume:
@@ -63,11 +68,11 @@ SAMPLES_PER_TABLE = 24
 
 
 def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = False, bf: bool = False,
-           volume: bool = False, grad: bool = False) -> dict:
+           volume: bool = False, grad: bool = False, halo: bool = False) -> dict:
     g = workload(name, seed)
     p = p or g["p"]
     o = Oracle(g)
-    K = o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad)
+    K = o.configs(p, all_integers=all_integers, volume=volume, grad_sync=grad, halo=halo)
     t0 = time.time()
     if bf:
         o.solve_bf(threads=threads)
@@ -91,7 +96,7 @@ def golden(name: str, seed: int, threads: int, p=None, all_integers: bool = Fals
     return {"workload": name, "seed": seed, "p": p, "all_integers": all_integers,
             "order": "breadth-first" if bf else "GenerateSeq",
             "transfer": "volume intersection" if volume else "split match",
-            "grad_sync": grad,
+            "grad_sync": grad, "halo": halo,
             "num_configs": [int(k) for k in K],
             "sequence": seq, "min_cost": str(mc), "strategy": strat, "cells": o.cells(),
             "tables": tables, "oracle_seconds": round(wall, 3)}
@@ -106,6 +111,7 @@ def main():
     ap.add_argument("--bf-only", action="store_true", help="only the breadth-first instances")
     ap.add_argument("--volume-only", action="store_true", help="only the volume-model instances")
     ap.add_argument("--grad-only", action="store_true", help="only the gradient-term instances")
+    ap.add_argument("--halo-only", action="store_true", help="only the halo-term instances")
     args = ap.parse_args()
     build(force=False)
     for inst in INSTANCES:
@@ -118,12 +124,14 @@ def main():
             continue
         if args.volume_only and not inst["volume"]:
             continue
-        if args.grad_only and not inst["grad"]:
+        if args.grad_only and (not inst["grad"] or inst["halo"]):
+            continue
+        if args.halo_only and not inst["halo"]:
             continue
         t = time.time()
         out = golden(name, seed, args.threads, inst["p"], inst["all_integers"], inst["bf"], inst["volume"],
-                     inst["grad"])
-        keys = ("seed", "p", "all_integers", "bf", "volume", "grad")
+                     inst["grad"], inst["halo"])
+        keys = ("seed", "p", "all_integers", "bf", "volume", "grad", "halo")
         path = os.path.join(HERE, file_name(name=name, **{k: inst[k] for k in keys}))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))

@@ -32,10 +32,10 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False, volume=False, grad=False):
+def _oracle(g, p=None, costs=None, rule=0, all_integers=False, bf=False, volume=False, grad=False, halo=False):
     from oracle.oracle import Oracle
     o = Oracle(g)
-    o.configs(p or g["p"], all_integers=all_integers, volume=volume, grad_sync=grad)
+    o.configs(p or g["p"], all_integers=all_integers, volume=volume, grad_sync=grad, halo=halo)
     if costs is not None:
         o.set_costs(*costs)
     if bf:
@@ -70,7 +70,7 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
          parts=0, splits=0, all_integers=False, bf=False, volume=False, grad=False,
-         direct=0, bulk_us=None):
+         direct=0, bulk_us=None, halo=False):
     """direct: PASE_OPT_DIRECT_CELLS (0 = off, so the tests aimed at the row and
     generic kernels keep them; None = the library's default)."""
     pg = P.Graph(g, seq_rule=rule)
@@ -79,6 +79,7 @@ def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=
     pg.set_option(P.OPT_ORDER, int(bf))
     pg.set_option(P.OPT_TRANSFER, int(volume))
     pg.set_option(P.OPT_GRAD_SYNC, int(grad))
+    pg.set_option(P.OPT_HALO, int(halo))
     pg.enumerate_configs(p or g["p"], all_integers=all_integers)
     pg.set_option(P.OPT_KEEP_TABLES, int(keep))
     pg.set_option(P.OPT_KERNEL, kernel)
@@ -306,8 +307,10 @@ def test_library_owned_workspace(P):
 
 
 # ------------------------------------------------------------------ full-size workloads
-def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad=False):
-    if bf:
+def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad=False, halo=False):
+    if halo:
+        fn = f"{name}_seed{seed}_{'grad_' if grad else ''}halo.json"
+    elif bf:
         fn = f"{name}_seed{seed}_p{p}_bf.json"
     elif volume:
         fn = f"{name}_seed{seed}_volume.json"
@@ -321,14 +324,14 @@ def _golden(name, seed, p=None, all_integers=False, bf=False, volume=False, grad
 
 def _check_golden(P, name, seed, kernel=0, key=0, keep=True, samples=True, schedule=0, tile=(0, 0),
                   p=None, all_integers=False, bf=False, volume=False, grad=False, direct=None,
-                  bulk_us=None):
-    gold = _golden(name, seed, p, all_integers, bf, volume, grad)
+                  bulk_us=None, halo=False):
+    gold = _golden(name, seed, p, all_integers, bf, volume, grad, halo)
     g = workload(name, seed)
     say(f"{name} seed={seed} kernel={kernel} key={key} keep={keep} schedule={schedule} tile={tile} "
         f"p={p} all_integers={all_integers} bf={bf} volume={volume} grad={grad} direct={direct}")
     pg, mc, strat = _run(P, g, p=p, keep=keep, kernel=kernel, key=key, schedule=schedule, tile=tile,
                          all_integers=all_integers, bf=bf, volume=volume, grad=grad,
-                         direct=direct, bulk_us=bulk_us)
+                         direct=direct, bulk_us=bulk_us, halo=halo)
     st = pg.stats()
     say(f"   cells {st['cells']:.3e}  wall {st['wall_ms']:.1f} ms  key_type {st['key_type']} "
         f"rows_vertices {st['rows_vertices']} slots {st['slots']} launches {st['launches']} "
@@ -680,6 +683,41 @@ def test_grad_sync_random_graphs(P, seed):
         assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
     assert (mc, strat) == o.result()
     _compare_all_entries(pg, o, g, max_entries=512)
+
+
+# ------------------------------------------------------------------ halo exchange of convolutions
+def _halo_graph(seed, **kw):
+    """The first random graph from seed on with at least two haloed layers."""
+    while True:
+        g = random_graph(seed, **kw)
+        if sum(1 for v in g["vertices"] if any(v.get("halo", []))) >= 2:
+            return g
+        seed += 1000
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_halo_random_graphs(P, seed):
+    """PASE_OPT_HALO = 1 on random graphs with random convolution geometry:
+    the device layer costs equal the oracle's, and so do the search and every
+    table entry (both configuration sets, with the gradient term on some)."""
+    p, all_int, grad = ((4, False, False), (8, False, True), (6, True, False), (16, False, False),
+                        (12, True, True), (32, False, False), (5, True, False), (64, False, True))[seed]
+    g = _halo_graph(seed + 1500, n=4 + seed % 4, p=p, max_dims=5, extra_edges=1 + seed % 3, max_size=300)
+    say(f"halo term random graph p={p} all_integers={all_int} grad={grad}")
+    o = _oracle(g, p=p, all_integers=all_int, grad=grad, halo=True)
+    for direct in (None, 0):
+        pg, mc, strat = _run(P, g, p=p, all_integers=all_int, grad=grad, halo=True, direct=direct)
+        for v in range(len(g["vertices"])):
+            assert np.array_equal(pg.layer_costs(v), o.layer_costs(v)), v
+        assert (mc, strat) == o.result()
+        _compare_all_entries(pg, o, g, max_entries=512)
+
+
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception"])
+@pytest.mark.parametrize("grad", [False, True])
+def test_halo_workloads_against_golden(P, name, grad):
+    _check_golden(P, name, 0, halo=True, grad=grad)
+    _check_golden(P, name, 0, halo=True, grad=grad, keep=False, direct=0)
 
 
 def test_grad_sync_fc_chain(P):

@@ -169,15 +169,15 @@ def test_key_bounds_hold(pase, seed):
     """The per-position bounds that size the keys hold on the oracle's tables:
     key_bound >= the largest value minimised over at that position (exhaustive
     search) and table_bound >= every table entry; model costs with both
-    configuration sets, with the gradient term, with volume transfer costs,
-    and caller-given costs."""
+    configuration sets, with the gradient term, the halo term, volume transfer
+    costs, and caller-given costs."""
     from oracle.oracle import Oracle
     all_int = seed % 3 == 1
     p = (4, 6, 8)[seed % 3]
-    grad, volume = seed % 4 == 3, seed % 5 == 4
+    grad, volume, halo = seed % 4 == 3, seed % 5 == 4, seed % 2 == 1
     g = random_graph(seed + 900, n=3 + seed % 4, p=p, max_dims=2, extra_edges=seed % 3, max_size=200)
     o = Oracle(g)
-    K = [int(k) for k in o.configs(p, all_integers=all_int, grad_sync=grad, volume=volume)]
+    K = [int(k) for k in o.configs(p, all_integers=all_int, grad_sync=grad, volume=volume, halo=halo)]
     costs = None
     if seed % 3 == 2:
         costs = random_costs(seed, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=1000)
@@ -186,6 +186,7 @@ def test_key_bounds_hold(pase, seed):
     pg = pase.Graph(g)
     pg.set_option(pase.OPT_GRAD_SYNC, int(grad))
     pg.set_option(pase.OPT_TRANSFER, int(volume))
+    pg.set_option(pase.OPT_HALO, int(halo))
     pg.enumerate_configs(p, all_integers=all_int)
     if costs is not None:
         pg.override_costs(*costs)
@@ -490,3 +491,26 @@ def test_plan_check_random_graphs(pase, seed):
         costs = random_costs(seed + k, K, [(K[e["src"]], K[e["dst"]]) for e in g["edges"]], hi=1 << 20)
         pg.override_costs(*costs)
         assert pg.plan_check() > 0
+
+
+def test_halo_option_and_geometry(pase):
+    """PASE_OPT_HALO validates; a halo on a dim that is not an input dim, or an
+    input dim out of range, is refused at creation; the option changes the
+    key bounds (the layer costs) only for graphs with a halo."""
+    P = pase
+    g = fc_chain()
+    pg = P.Graph(g)
+    assert _status(lambda: pg.set_option(P.OPT_HALO, 2)) == P.INVALID_ARGUMENT
+    bad = dict(g["vertices"][0], halo=[0, 1, 0], input_dims=[0, 2])
+    assert _status(lambda: P.pase_graph_create([bad] + g["vertices"][1:], g["edges"])) == P.INVALID_ARGUMENT
+    bad = dict(g["vertices"][0], halo=[0, 0, 0], input_dims=[3])
+    assert _status(lambda: P.pase_graph_create([bad] + g["vertices"][1:], g["edges"])) == P.INVALID_ARGUMENT
+    for name, changes in (("w0_fc_chain", False), ("w1_residual_cnn", True)):
+        w = workload(name)
+        bounds = []
+        for halo in (0, 1):
+            pg = P.Graph(w)
+            pg.set_option(P.OPT_HALO, halo)
+            pg.enumerate_configs(w["p"])
+            bounds.append([pg.vertex_info(v)["key_bound"] for v in range(len(w["vertices"]))])
+        assert (bounds[0] != bounds[1]) == changes, name

@@ -788,6 +788,90 @@ def test_bf_dependent_sets_blow_up_on_dense_graphs():
     o.solve_bf()
     assert o.result() == (8_388_608, [9, 9, 9, 9]) and o.cells() == 310
 
+# ------------------------------------------------------------------ halo exchange of convolutions
+def _conv_graph(h, w, k, p):
+    return {"name": "conv", "p": p, "comm_weight": 8,
+            "vertices": [{"name": "c", "dims": [2, 4, 3, h, w], "dim_names": ["b", "co", "ci", "h", "w"],
+                          "reduce": [2], "flops_per_point": 2 * k * k,
+                          "halo": [0, 0, 0, k // 2, k // 2], "input_dims": [0, 2, 3, 4]}], "edges": []}
+
+
+def test_halo_hand_values():
+    """A 3x3 convolution (b 2, co 4, ci 3, h 8, w 6), r = 8, p = 4, FLOPs
+    18 * 1152 = 20 736.  (1,1,1,2,1): 10 368 + 8 * 2 * 1 * (b ci w = 36) = 10 944.
+    (1,1,1,2,2): 5 184 + 8 * (2 * ceil(36 / 2) + 2 * ceil(48 / 2)) = 5 856.
+    (2,1,1,2,1): 5 184 + 8 * 2 * ceil(36 / 2) = 5 472.  (1,1,4,1,1): no halo,
+    5 184 + 8 * 3 * 384 = 14 400.  Ragged, every integer split, p = 6, h 7,
+    w 5, (1,1,1,3,2): ceil(15 120 / 6) = 2 520 + 8 * (2 * ceil(30 / 2) +
+    2 * ceil(42 / 3)) = 2 984; with a 5x5 kernel (halo 2, 18 * 25 / 9 the
+    FLOPs): 7 000 + 8 * (4 * 15 + 4 * 14) = 7 928."""
+    from oracle.oracle import Oracle
+    o = Oracle(_conv_graph(8, 6, 3, 4))
+    o.configs(4, halo=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    L = o.layer_costs(0)
+    want = {(1, 1, 1, 2, 1): 10_944, (1, 1, 1, 2, 2): 5_856, (2, 1, 1, 2, 1): 5_472, (1, 1, 4, 1, 1): 14_400,
+            (1, 1, 1, 1, 1): 20_736}
+    for t, v in want.items():
+        assert int(L[sp.index(t)]) == v, t
+    o.configs(4)   # the option off: the benchmark's model
+    assert int(o.layer_costs(0)[sp.index((1, 1, 1, 2, 1))]) == 10_368
+    o = Oracle(_conv_graph(7, 5, 3, 6))
+    o.configs(6, all_integers=True, halo=True)
+    sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+    assert int(o.layer_costs(0)[sp.index((1, 1, 1, 3, 2))]) == 2_984
+    o = Oracle(_conv_graph(7, 5, 5, 6))
+    o.configs(6, all_integers=True, halo=True)
+    assert int(o.layer_costs(0)[sp.index((1, 1, 1, 3, 2))]) == 7_928
+
+
+def test_halo_invariants():
+    """The halo term vanishes for configurations that split no halo dim and
+    for 1x1 kernels; it is symmetric in h and w on a square input; it never
+    grows when a non-halo input dim is split further."""
+    from oracle.oracle import Oracle
+    for k in (1, 3, 5):
+        g = _conv_graph(8, 8, k, 16)
+        a, b = Oracle(g), Oracle(g)
+        a.configs(16, halo=True)
+        b.configs(16)
+        sp = [tuple(int(x) for x in r) for r in a.splits(0)]
+        La, Lb = a.layer_costs(0), b.layer_costs(0)
+        for c, t in enumerate(sp):
+            if k == 1 or (t[3] == 1 and t[4] == 1):
+                assert La[c] == Lb[c], t
+            else:
+                assert La[c] > Lb[c], t
+            mirror = (t[0], t[1], t[2], t[4], t[3])
+            assert La[c] - Lb[c] == La[sp.index(mirror)] - Lb[sp.index(mirror)], t
+            if t[0] * 2 * t[1] * t[2] * t[3] * t[4] <= 16:
+                more_b = (2 * t[0],) + t[1:]
+                d = sp.index(more_b)
+                assert La[d] - Lb[d] <= La[c] - Lb[c], t
+
+
+def _halo_graph(seed):
+    """The first random graph from seed on whose layers carry a halo."""
+    while True:
+        g = random_graph(seed, n=3 + seed % 3, p=4, max_dims=3, extra_edges=seed % 3)
+        if sum(1 for v in g["vertices"] if any(v.get("halo", []))) >= 2:
+            return g
+        seed += 1000
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_theorem1_halo(seed):
+    """Random graphs with convolution geometry: the DP minimum under the halo
+    term equals exhaustive search over every strategy."""
+    g = _halo_graph(seed + 1400)
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    o.configs(4, halo=True)
+    o.solve()
+    L, R, src, dst = _tables(o, g)
+    assert o.result()[0] == pins.brute_force(L, R, src, dst)[0]
+
+
 # ------------------------------------------------------------------ planted mistakes
 MUTANTS = {
     "tie_break_last": ("if (cost < mincost) { mincost = cost; arg = c; }",
@@ -828,6 +912,11 @@ MUTANTS = {
     "comm_over_all_devices": ("if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;",
                               "if (!mul_ok(red_split - 1, ceil_div(keep_n, P), &comm)) return 0;"),
     "seq_keeps_self": ("if (rule == 0) d[(size_t)v * n + v] = 0;", "if (rule == 2) d[(size_t)v * n + v] = 0;"),
+    "halo_one_neighbour": ("if (!mul_ok(2 * w, ceil_div(rest, rest_split), &words)) return 0;",
+                           "if (!mul_ok(w, ceil_div(rest, rest_split), &words)) return 0;"),
+    "halo_own_split": ("if (j == k || !(o->in_mask[v] >> j & 1u)) continue;",
+                       "if (!(o->in_mask[v] >> j & 1u)) continue;"),
+    "halo_when_unsplit": ("if (w == 0 || s[k] == 1) continue;", "if (w == 0) continue;"),
     "grad_replicas_from_weight_dims": ("                Pw *= s[k];\n            } else {\n                R *= s[k];",
                                        "                R *= s[k];\n            } else {\n                Pw *= s[k];"),
 }
@@ -953,8 +1042,17 @@ def _pin_suite(lib):
         L = o.layer_costs(0)
         return int(L[sp.index((4, 1, 1))]) == 2_883_584 and int(L[sp.index((2, 2, 1))]) == 2_359_296
 
+    def halo():
+        o = Oracle(_conv_graph(8, 6, 3, 4), lib)
+        o.configs(4, halo=True)
+        sp = [tuple(int(x) for x in r) for r in o.splits(0)]
+        L = o.layer_costs(0)
+        return (int(L[sp.index((1, 1, 1, 2, 1))]) == 10_944 and int(L[sp.index((1, 1, 1, 2, 2))]) == 5_856
+                and int(L[sp.index((1, 1, 1, 1, 1))]) == 20_736)
+
     guard("w0", w0)
     guard("grad", grad)
+    guard("halo", halo)
     guard("bf", bf)
     guard("volume", volume)
     guard("all_integers", all_integers)

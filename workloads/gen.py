@@ -18,6 +18,10 @@ Graph dict layout (shared by every consumer)::
 ``weight_dims`` (optional) name the loop dims that index the layer's weight
 tensor, which holds ``weight_per_point`` words per point of those dims (a
 k x k convolution: 9 per (co, ci) pair); layers without weights omit both.
+``halo`` (optional, convolutions) gives per loop dim the half extent of the
+kernel along it (1 for a 3x3 kernel's h and w, 0 elsewhere) and
+``input_dims`` the loop dims that index the layer's input tensor
+((b, ci, h, w) of a convolution).
 ``src_dim[k]`` / ``dst_dim[k]`` give, for tensor dim k, the loop dim of the
 source / destination vertex that indexes it (-1: that endpoint does not split
 this tensor dim).  Vertex ids are list positions; they are the tie-break of the
@@ -40,8 +44,9 @@ class _Builder:
         self.g = {"name": name, "p": int(p), "comm_weight": int(comm_weight),
                   "vertices": [], "edges": []}
 
-    def vertex(self, name, dims, dim_names, reduce, flops_per_point, weights=None):
-        """weights: (loop dims indexing the weight tensor, words per point)."""
+    def vertex(self, name, dims, dim_names, reduce, flops_per_point, weights=None, conv=None):
+        """weights: (loop dims indexing the weight tensor, words per point);
+        conv: (halo width per loop dim, loop dims indexing the input tensor)."""
         assert len(dims) == len(dim_names)
         vx = {"name": name, "dims": [int(x) for x in dims],
               "dim_names": list(dim_names), "reduce": sorted(int(k) for k in reduce),
@@ -49,6 +54,9 @@ class _Builder:
         if weights is not None:
             vx["weight_dims"] = sorted(int(k) for k in weights[0])
             vx["weight_per_point"] = int(weights[1])
+        if conv is not None:
+            vx["halo"] = [int(w) for w in conv[0]]
+            vx["input_dims"] = sorted(int(k) for k in conv[1])
         self.g["vertices"].append(vx)
         return len(self.g["vertices"]) - 1
 
@@ -87,6 +95,11 @@ def fc_chain(p: int = 4, layers: int = 4, batch: int = 64, width: int = 256):
 
 # ---------------------------------------------------------------- W1
 _CONV_DIMS = ("b", "co", "ci", "h", "w")
+
+
+def _conv(k):
+    """Halo widths and input dims of a k x k convolution over _CONV_DIMS."""
+    return (0, 0, 0, k // 2, k // 2), (0, 2, 3, 4)
 _CHANNELS_W1 = (64, 128, 256, 512)
 
 
@@ -105,7 +118,8 @@ def residual_cnn(seed: int = 0, p: int = 8, layers: int = 16, batch: int = 128):
     ci = ci0
     for k in range(layers):
         hw = 64 if k < layers // 2 else 32
-        ids.append(b.vertex(f"conv{k}", (batch, cos[k], ci, hw, hw), _CONV_DIMS, (2,), 18, ((1, 2), 9)))
+        ids.append(b.vertex(f"conv{k}", (batch, cos[k], ci, hw, hw), _CONV_DIMS, (2,), 18, ((1, 2), 9),
+                            _conv(3)))
         ci = cos[k]
     # activation (b, c, h, w): producer dims (b, co, h, w) -> consumer (b, ci, h, w)
     for k in range(layers - 1):
@@ -130,7 +144,7 @@ def inception(seed: int = 0, p: int = 16, modules: int = 12, batch: int = 128):
     """
     rng = np.random.default_rng(seed)
     b = _Builder(f"inception{modules}_seed{seed}_p{p}", p)
-    stem = b.vertex("stem", (batch, 192, 3, 35, 35), _CONV_DIMS, (2,), 18, ((1, 2), 9))
+    stem = b.vertex("stem", (batch, 192, 3, 35, 35), _CONV_DIMS, (2,), 18, ((1, 2), 9), _conv(3))
     x, x_is_concat, cin = stem, False, 192
     third = modules // 3
     for m in range(modules):
@@ -143,7 +157,7 @@ def inception(seed: int = 0, p: int = 16, modules: int = 12, batch: int = 128):
                 ksz = int(rng.choice((1, 3, 5)))
                 co = int(rng.choice(_CHANNELS_W2))
                 v = b.vertex(f"m{m}_b{br}_c{dl}_k{ksz}", (batch, co, prev_c, hw, hw),
-                             _CONV_DIMS, (2,), 2 * ksz * ksz, ((1, 2), ksz * ksz))
+                             _CONV_DIMS, (2,), 2 * ksz * ksz, ((1, 2), ksz * ksz), _conv(ksz))
                 src = (0, 1, 2, 3) if prev_is_concat else (0, 1, 3, 4)
                 b.edge(prev, v, src, (0, 2, 3, 4))
                 prev, prev_c, prev_is_concat = v, co, False
@@ -324,6 +338,7 @@ def random_graph(seed: int, n: int, p: int = 4, max_dims: int = 3, extra_edges: 
         rand_edge(u, v)
         added += 1
     _random_weights(b, seed)
+    _random_halos(b, seed)
     return b.done()
 
 
@@ -338,6 +353,21 @@ def _random_weights(b, seed):
             dims = [k for k in range(d) if rng.random() < 0.6] or [int(rng.integers(0, d))]
             vx["weight_dims"] = dims
             vx["weight_per_point"] = int(rng.integers(1, 5))
+
+
+def _random_halos(b, seed):
+    """Give about half of the vertices a convolution geometry: a random
+    non-empty set of input dims, and on some of them a halo width in 1..2.
+    Drawn from a stream of its own, so the rest of the graph does not depend
+    on it."""
+    rng = np.random.default_rng([seed, 0x4A1])
+    for vx in b.g["vertices"]:
+        d = len(vx["dims"])
+        if rng.random() < 0.5:
+            ins = [k for k in range(d) if rng.random() < 0.7] or [int(rng.integers(0, d))]
+            halo = [int(rng.integers(1, 3)) if (k in ins and rng.random() < 0.5) else 0 for k in range(d)]
+            vx["halo"] = halo
+            vx["input_dims"] = ins
 
 
 def random_costs(seed: int, layer_sizes, edge_shapes, hi: int = 4):
@@ -368,4 +398,5 @@ def chain_graph(seed: int, n: int, p: int = 4, max_dims: int = 3, max_size: int 
         b.edge(u, w, [int(rng.integers(-1, du)) for _ in range(rank)],
                [int(rng.integers(-1, dw)) for _ in range(rank)], elems=int(rng.integers(1, 5000)))
     _random_weights(b, seed)
+    _random_halos(b, seed)
     return b.done()
