@@ -230,6 +230,7 @@ typedef struct {
                                   of the last fill or split reduction (every prep, fill and reduction
                                   launch and the gaps between them) */
     double backtrack_ms;       /* PASE_OPT_PROFILE, device: back-substitution */
+    double assign_ms;          /* pase_assign_devices, host: the last device assignment */
 } pase_run_stats;
 
 /* Copy a computation graph G=(V,E) (Sec. II) into a new handle.
@@ -375,6 +376,35 @@ typedef struct {
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);
+
+/* Device assignment of a strategy (Sec. II, the paragraph on assigning
+ * devices after the search): the cost model numbers the parts of each
+ * configuration by their grid point; this places them on the p modeled
+ * devices greedily so that tensors stay where they are.  Vertices in
+ * ascending id order; vertex 0 puts part g on device g; every later vertex v
+ * places all its parts on distinct devices, pair (part q, device d) by pair,
+ * largest locality first, ties to the lower part and then the lower device,
+ * where the locality of (q, d) is the number of tensor elements, over all
+ * edges joining v to an already placed (lower-id) vertex u, that part q and
+ * u's part on d both cover.  Part geometry: loop dim k of a configuration is
+ * cut into s_k equal fractions, part g is the mixed-radix grid point of g
+ * (loop dim 0 slowest), a tensor dim covers the fraction of the loop dim it
+ * maps to (all of it when unmapped); shared elements of two parts are
+ * floor(elems * shared fraction).  Host only, after pase_enumerate_configs.
+ * config_idx: host array of nv configuration indices (a strategy, e.g. from
+ * pase_find_best_strategy).  devices: host array of nv * p, receives the part
+ * of vertex v on device d at [v * p + d], -1 where v has no part.
+ * edge_locality (host array of ne, or NULL): the elements of each edge's
+ * tensor the two ends hold on the same device, summed over devices.
+ * edge_xfer (host array of ne, or NULL): r * t_x of each edge under this
+ * assignment -- the volume model of PASE_OPT_TRANSFER = 1 with these devices
+ * in place of the grid numbering (equal to it when both ends keep the grid
+ * numbering).  Errors: INVALID_ARGUMENT (null array, index out of range),
+ * BAD_STATE (no enumeration), TOO_LARGE (p > 1024, or an edge cut into 2^64
+ * cells or more), OVERFLOW (the tensor elements of one vertex's edges, or a
+ * transfer cost, exceed 64 bits). */
+pase_status pase_assign_devices(pase_graph_t g, const uint32_t *config_idx, int32_t *devices,
+                                uint64_t *edge_locality, uint64_t *edge_xfer);
 
 /* Diagnostics (host only, no device work): build the kernel descriptors,
  * batched launches and constant-region image that pase_find_best_strategy

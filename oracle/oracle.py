@@ -49,6 +49,7 @@ def _load(path: str | None = None):
     L.oracle_set_weights.argtypes = [P, P, P]
     L.oracle_set_grad_sync.argtypes = [P, I]
     L.oracle_set_halo.argtypes = [P, P, P]
+    L.oracle_assign_devices.argtypes = [P, P, P, P, P]
     L.oracle_set_halo_model.argtypes = [P, I]
     L.oracle_set_costs.argtypes = [P, P, P]
     L.oracle_solve.argtypes = [P, I, P, U64, I]
@@ -247,6 +248,18 @@ class Oracle:
         st = np.zeros(self.nv, np.int32)
         self._check(self._L.oracle_result(self._h, _ptr(mc), _ptr(st)))
         return int(mc[0]), st.tolist()
+
+    def assign_devices(self, strategy):
+        """Greedy device assignment of `strategy` (configuration per vertex id):
+        (dev [nv, p] -- the part of each vertex on each device, -1 for none --,
+        locality [ne] in elements, r * t_x [ne] under the assignment)."""
+        cfg = np.ascontiguousarray(np.asarray(strategy, dtype=np.int32))
+        dev = np.zeros((self.nv, int(self.p)), dtype=np.int32)
+        loc = np.zeros(max(len(self.src), 1), dtype=np.uint64)
+        xfer = np.zeros(max(len(self.src), 1), dtype=np.uint64)
+        self._check(self._L.oracle_assign_devices(self._h, _ptr(cfg), _ptr(dev), _ptr(loc), _ptr(xfer)))
+        ne = len(self.src)
+        return dev, loc[:ne], xfer[:ne]
 
     def fingerprint(self, i: int):
         a = np.zeros(1, np.uint64)

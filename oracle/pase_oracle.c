@@ -18,6 +18,10 @@
  *     with the node function of eq. (3), the connected set X(i) and connected
  *     subsets S(i) of Sec. III-B, the strict "<" update over configurations in
  *     ascending index order, and back-substitution from the last vertex;
+ *   - device assignment after the search: the greedy locality-maximising
+ *     placement of Sec. II's device-assignment paragraph (oracle_assign_devices),
+ *     repeated argmax over every (part, device) pair, shared elements counted
+ *     cell by cell;
  *   - every addition is overflow-checked in uint64.
  *
  * Tables are stored in canonical order: the dependent set D(i) sorted by
@@ -861,6 +865,162 @@ int oracle_solve_bf(oracle_t *o, uint64_t max_cells, int nthreads) {
     if (o->overflow) return fail(o, "cost overflows uint64");
     if (stopped == 2) return 2;
     back_substitute(o);
+    return 0;
+}
+
+/* --------------------------------------------------------- device assignment */
+
+/* Part g of a configuration with splits s (d loop dims): its grid point, the
+ * mixed-radix digits of g with loop dim 0 slowest. */
+static void part_digits(const uint32_t *s, int d, uint64_t g, uint64_t *x) {
+    for (int k = d - 1; k >= 0; k--) { x[k] = g % s[k]; g /= s[k]; }
+}
+
+/* Elements of edge e's tensor that part gu of the source's configuration su
+ * and part gw of the destination's configuration sw both cover, rounded down.
+ * Per tensor dim the part of a side is the fraction interval [x/s, (x+1)/s)
+ * of the loop dim it maps to there (the whole dim when unmapped); the
+ * intersection is counted cell by cell on a grid of s_u * s_w cells per dim. */
+static uint64_t part_overlap(oracle_t *o, int e, const uint32_t *su, uint64_t gu, const uint32_t *sw, uint64_t gw) {
+    int u = o->src[e], w = o->dst[e];
+    uint64_t xu[MAXD], xw[MAXD];
+    part_digits(su, o->ndims[u], gu, xu);
+    part_digits(sw, o->ndims[w], gw, xw);
+    unsigned __int128 common = 1, cells = 1;
+    for (int t = 0; t < o->rank[e]; t++) {
+        int a = o->src_dim[e * MAXD + t], b = o->dst_dim[e * MAXD + t];
+        uint64_t au = a >= 0 ? su[a] : 1, aw = b >= 0 ? sw[b] : 1;
+        uint64_t pu = a >= 0 ? xu[a] : 0, pw = b >= 0 ? xw[b] : 0;
+        uint64_t L = au * aw, both = 0;
+        for (uint64_t c = 0; c < L; c++) both += (c * au / L == pu) && (c * aw / L == pw);
+        common *= both;
+        cells *= L;
+    }
+    return (uint64_t)(((unsigned __int128)o->elems[e] * common) / cells);
+}
+
+/* Elements of edge e's tensor on the source's part gu (side 0) or the
+ * destination's part gw (side 1): elems / (product of that side's splits of
+ * the mapped dims), counted in the same cells. */
+static unsigned __int128 part_cells(oracle_t *o, int e, const uint32_t *su, const uint32_t *sw, int side,
+                                    unsigned __int128 *cells) {
+    unsigned __int128 mine = 1, all = 1;
+    for (int t = 0; t < o->rank[e]; t++) {
+        int a = o->src_dim[e * MAXD + t], b = o->dst_dim[e * MAXD + t];
+        uint64_t au = a >= 0 ? su[a] : 1, aw = b >= 0 ? sw[b] : 1;
+        all *= au * aw;
+        mine *= side == 0 ? aw : au;   /* a part of u covers aw of the au * aw cells */
+    }
+    *cells = all;
+    return mine;
+}
+
+/* The greedy device assignment of strategy cfg after the search (Sec. II):
+ * vertices in ascending id order; the first gets part g on device g; every
+ * later one assigns its parts to distinct devices, largest locality first --
+ * the locality of (part g, device d) is the elements of the tensors of all
+ * edges joining it to an already placed vertex that g and that vertex's part
+ * on d both cover -- ties to the lowest part, then the lowest device.
+ * dev[v * p + d]: the part of v on device d, -1 for none.  locality[e]: the
+ * elements of e's tensor that the two ends hold on the same device, summed
+ * over devices.  xfer[e]: r * t_x of e under the assignment, the volume model
+ * (forward max_d |need| - |common| plus the same backward, words rounded up
+ * per direction) with these devices instead of the grid numbering. */
+int oracle_assign_devices(oracle_t *o, const int *cfg, int *dev, uint64_t *locality, uint64_t *xfer) {
+    if (!o->K) return fail(o, "configs not enumerated");
+    int n = o->nv, p = o->p;
+    if (p > 1024) return fail(o, "assignment needs p <= 1024");
+    uint64_t *P = calloc(n, sizeof(uint64_t));
+    const uint32_t **s = calloc(n, sizeof(uint32_t *));
+    for (int v = 0; v < n; v++) {
+        if (cfg[v] < 0 || cfg[v] >= o->K[v]) { free(P); free(s); return fail(o, "config out of range"); }
+        s[v] = o->sp[v] + (size_t)cfg[v] * o->ndims[v];
+        P[v] = 1;
+        for (int k = 0; k < o->ndims[v]; k++) P[v] *= s[v][k];
+    }
+    /* a locality sums the tensors of a vertex's edges: each sum must fit 64 bits */
+    uint64_t *esum = calloc(n, sizeof(uint64_t));
+    for (int e = 0; e < o->ne; e++)
+        if (!add_ok(esum[o->src[e]], o->elems[e], &esum[o->src[e]]) ||
+            !add_ok(esum[o->dst[e]], o->elems[e], &esum[o->dst[e]])) {
+            free(P); free(s); free(esum);
+            return fail(o, "tensor elements of a vertex's edges overflow uint64");
+        }
+    free(esum);
+    for (int i = 0; i < n * p; i++) dev[i] = -1;
+    uint64_t *W = calloc((size_t)p * p, sizeof(uint64_t));
+    char *gdone = calloc(p, 1), *dused = calloc(p, 1);
+    for (int v = 0; v < n; v++) {
+        if (v == 0) {
+            for (uint64_t g = 0; g < P[v]; g++) dev[v * p + g] = (int)g;
+            continue;
+        }
+        memset(W, 0, (size_t)p * p * sizeof(uint64_t));
+        for (int e = 0; e < o->ne; e++) {
+            int u = o->src[e], w = o->dst[e];
+            int other = u == v ? w : (w == v ? u : -1);
+            if (other < 0 || other > v) continue;   /* placed neighbours only */
+            for (uint64_t g = 0; g < P[v]; g++)
+                for (int d = 0; d < p; d++) {
+                    int h = dev[other * p + d];
+                    if (h < 0) continue;
+                    W[g * p + d] += u == v ? part_overlap(o, e, s[v], g, s[other], (uint64_t)h)
+                                           : part_overlap(o, e, s[other], (uint64_t)h, s[v], g);
+                }
+        }
+        memset(gdone, 0, p);
+        memset(dused, 0, p);
+        for (uint64_t step = 0; step < P[v]; step++) {
+            int bg = -1, bd = -1;
+            uint64_t best = 0;
+            for (uint64_t g = 0; g < P[v]; g++) {
+                if (gdone[g]) continue;
+                for (int d = 0; d < p; d++) {
+                    if (dused[d]) continue;
+                    if (bg < 0 || W[g * p + d] > best) { bg = (int)g; bd = d; best = W[g * p + d]; }
+                }
+            }
+            gdone[bg] = 1;
+            dused[bd] = 1;
+            dev[v * p + bd] = bg;
+        }
+    }
+    for (int e = 0; e < o->ne; e++) {
+        int u = o->src[e], w = o->dst[e];
+        uint64_t loc = 0;
+        unsigned __int128 cells, fwd = 0, bwd = 0;
+        unsigned __int128 hold = part_cells(o, e, s[u], s[w], 0, &cells), need = part_cells(o, e, s[u], s[w], 1, &cells);
+        for (int d = 0; d < p; d++) {
+            int hu = dev[u * p + d], hw = dev[w * p + d];
+            unsigned __int128 common_cells = 0;
+            if (hu >= 0 && hw >= 0) {
+                /* the shared cells of the two parts, counted again exactly */
+                uint64_t xu[MAXD], xw[MAXD];
+                part_digits(s[u], o->ndims[u], (uint64_t)hu, xu);
+                part_digits(s[w], o->ndims[w], (uint64_t)hw, xw);
+                common_cells = 1;
+                for (int t = 0; t < o->rank[e]; t++) {
+                    int a = o->src_dim[e * MAXD + t], b = o->dst_dim[e * MAXD + t];
+                    uint64_t au = a >= 0 ? s[u][a] : 1, aw = b >= 0 ? s[w][b] : 1;
+                    uint64_t pu = a >= 0 ? xu[a] : 0, pw = b >= 0 ? xw[b] : 0, L = au * aw, both = 0;
+                    for (uint64_t c = 0; c < L; c++) both += (c * au / L == pu) && (c * aw / L == pw);
+                    common_cells *= both;
+                }
+                loc += part_overlap(o, e, s[u], (uint64_t)hu, s[w], (uint64_t)hw);
+            }
+            unsigned __int128 f = hw >= 0 ? need - common_cells : 0, b = hu >= 0 ? hold - common_cells : 0;
+            if (f > fwd) fwd = f;
+            if (b > bwd) bwd = b;
+        }
+        locality[e] = loc;
+        unsigned __int128 E = o->elems[e];
+        unsigned __int128 moved = (E * fwd + cells - 1) / cells + (E * bwd + cells - 1) / cells;
+        if (moved >> 64 || !mul_ok(o->r, (uint64_t)moved, &xfer[e])) {
+            free(P); free(s); free(W); free(gdone); free(dused);
+            return fail(o, "transfer cost overflows uint64");
+        }
+    }
+    free(P); free(s); free(W); free(gdone); free(dused);
     return 0;
 }
 

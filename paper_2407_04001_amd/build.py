@@ -20,7 +20,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
 
 
 def sources():
-    return [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "device.hip")]
+    return [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "assign.cpp", "device.hip")]
 
 
 def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
@@ -48,7 +48,7 @@ def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
     return out
 
 
-# Host-only build of the planner (host.cpp, launch_plan.cpp) with a stub
+# Host-only build of the planner (host.cpp, launch_plan.cpp, assign.cpp) with a stub
 # device runtime, under AddressSanitizer and UBSan, for the CPU test suite.
 # The GPU library is never built this way: this is g++ on host sources only.
 SAN_LIB = os.path.join(ROOT, "_build", "libpase_host_san.so")
@@ -58,7 +58,7 @@ SAN_FLAGS = ["-O1", "-g", "-std=c++17", "-fPIC", "-shared", "-fno-omit-frame-poi
 
 def build_host_sanitized(out: str = SAN_LIB, verbose: bool = False) -> str:
     os.makedirs(os.path.dirname(out), exist_ok=True)
-    srcs = [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "device_stub.cpp")]
+    srcs = [os.path.join(CSRC, f) for f in ("host.cpp", "launch_plan.cpp", "assign.cpp", "device_stub.cpp")]
     cmd = [os.environ.get("CXX", "g++"), *SAN_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            *srcs, "-o", out + ".tmp"]
     if verbose:

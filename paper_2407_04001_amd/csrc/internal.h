@@ -26,6 +26,7 @@ constexpr int kMaxGTerms = 24;     // terms of the generic kernel
 constexpr int kMaxContrib = 64;    // contributions to one precomputed block
 constexpr int kMaxBlocks = kMaxDep + 1;
 constexpr uint64_t kMaxTableEntries = (1ull << 31) - 1;
+constexpr uint32_t kAssignMaxDevices = 1024;   // p bound of the device assignment
 
 // ------------------------------------------------------------------ device descriptors
 struct DevVertex {            // configuration data of one vertex (uploaded once per search)

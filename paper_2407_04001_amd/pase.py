@@ -50,7 +50,8 @@ class RunStats(C.Structure):
                 ("rows_launches", C.c_uint32), ("slots", C.c_uint32), ("stream_cells", C.c_uint64),
                 ("stream_fill_ms", C.c_double), ("stream_launches", C.c_uint32), ("schedule", C.c_uint32),
                 ("pad0", C.c_uint32), ("seq_ms", C.c_double), ("plan_ms", C.c_double), ("setup_ms", C.c_double),
-                ("cost_tables_ms", C.c_double), ("fill_span_ms", C.c_double), ("backtrack_ms", C.c_double)]
+                ("cost_tables_ms", C.c_double), ("fill_span_ms", C.c_double), ("backtrack_ms", C.c_double),
+                ("assign_ms", C.c_double)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -75,7 +76,7 @@ EXPORTS = ["pase_graph_create", "pase_graph_destroy", "pase_last_error", "pase_e
            "pase_set_option", "pase_override_costs", "pase_workspace_size", "pase_set_workspace",
            "pase_find_best_strategy", "pase_table_entry", "pase_table_fingerprint",
            "pase_layer_costs", "pase_edge_costs", "pase_stats", "pase_vertex_info_get",
-           "pase_find_best_strategy_noalloc", "pase_plan_check"]
+           "pase_find_best_strategy_noalloc", "pase_plan_check", "pase_assign_devices"]
 
 _lib = None
 
@@ -109,6 +110,7 @@ def load(path: str | None = None):
         "pase_find_best_strategy": (st, [P, P, P, P]),
         "pase_find_best_strategy_noalloc": (st, [P, P, P, P]),
         "pase_plan_check": (st, [P, P]),
+        "pase_assign_devices": (st, [P, P, P, P, P]),
         "pase_table_entry": (st, [P, U32, P, P, P]),
         "pase_table_fingerprint": (st, [P, U32, P, P]),
         "pase_layer_costs": (st, [P, U32, P]),
@@ -288,6 +290,17 @@ def pase_plan_check(h) -> int:
     return b.value
 
 
+def pase_assign_devices(h, config_idx, nv: int, ne: int, p: int):
+    cfg = np.ascontiguousarray(np.asarray(config_idx, np.uint32))
+    if cfg.shape != (nv,):
+        raise ValueError(f"strategy of {cfg.size} configurations for {nv} vertices")
+    dev = np.zeros((nv, p), np.int32)
+    loc = np.zeros(max(ne, 1), np.uint64)
+    xfer = np.zeros(max(ne, 1), np.uint64)
+    _check(h, load().pase_assign_devices(h, _ptr(cfg), _ptr(dev), _ptr(loc), _ptr(xfer)))
+    return dev, loc[:ne], xfer[:ne]
+
+
 # ------------------------------------------------------------------ convenience wrapper
 class Graph:
     """A computation graph handle.  ``graph`` is a dict in the layout of
@@ -322,6 +335,7 @@ class Graph:
         if all_integers is not None:
             pase_set_option(self.h, OPT_CONFIG_SET, 1 if all_integers else 0)
         pase_enumerate_configs(self.h, p)
+        self.p = int(p)
         self._K = None
 
     @property
@@ -388,3 +402,8 @@ class Graph:
 
     def plan_check(self) -> int:
         return pase_plan_check(self.h)
+
+    def assign_devices(self, strategy):
+        """Greedy device assignment of a strategy: (devices [nv, p] = part on
+        each device or -1, edge locality [ne], edge r * t_x [ne])."""
+        return pase_assign_devices(self.h, strategy, self.nv, self.ne, self.p)

@@ -281,6 +281,40 @@ def volume_transfer_elements(m, src_dim, dst_dim, s_src, s_dst, r) -> int:
     return r * (fwd + bwd)
 
 
+def assigned_transfer_elements(m, src_dim, dst_dim, s_src, s_dst, part_src, part_dst, r):
+    """Locality and r * t_x of one edge under explicit device maps, by
+    enumerating tensor elements (dims of sizes m, each divisible by the splits
+    that cut it): part_src[d] / part_dst[d] is the part (mixed-radix grid
+    point, loop dim 0 slowest) each end holds on device d, -1 for none.
+    Locality = sum over devices of the elements both ends hold there; forward
+    = the largest count a consumer device needs but does not hold, backward
+    the same with the roles swapped."""
+    def coords(g, splits):
+        out = [0] * len(splits)
+        for k in range(len(splits) - 1, -1, -1):
+            out[k] = g % splits[k]
+            g //= splits[k]
+        return out
+
+    elems = list(itertools.product(*[range(x) for x in m]))
+
+    def part(side_dims, splits, g):
+        if g < 0:
+            return set()
+        xs = coords(g, splits)
+        return {el for el in elems
+                if all(i * (splits[side_dims[t]] if side_dims[t] >= 0 else 1) // m[t]
+                       == (xs[side_dims[t]] if side_dims[t] >= 0 else 0) for t, i in enumerate(el))}
+
+    loc = fwd = bwd = 0
+    for d in range(len(part_src)):
+        A_u, A_v = part(src_dim, s_src, part_src[d]), part(dst_dim, s_dst, part_dst[d])
+        loc += len(A_u & A_v)
+        fwd = max(fwd, len(A_v - A_u))
+        bwd = max(bwd, len(A_u - A_v))
+    return loc, r * (fwd + bwd)
+
+
 def splitmix64_mix(z: int) -> int:
     """SplitMix64 output function (Steele, Lea and Flood, 2014)."""
     m = (1 << 64) - 1

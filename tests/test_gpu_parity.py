@@ -667,6 +667,48 @@ def test_volume_model_transformer_against_golden(P):
     _check_golden(P, "w4_transformer", 0, volume=True, keep=True)
 
 
+# ------------------------------------------------------------------ device assignment of the found strategy
+@pytest.mark.parametrize("name,seed", [("random", 0), ("random", 1), ("random", 2), ("w1_residual_cnn", 0),
+                                       ("w2_inception", 0), ("w4_transformer", 0)])
+def test_assign_devices_after_search(P, name, seed):
+    """The strategy the GPU search returns, placed on devices by
+    pase_assign_devices: devices, localities and transfers equal the oracle's
+    assignment of the oracle's own optimum (the same strategy); where both
+    ends of an edge keep the grid numbering, the transfer equals the device's
+    volume-model matrix entry."""
+    if name == "random":
+        p = (4, 8, 16)[seed]
+        g = random_graph(seed + 720, n=5 + seed, p=p, max_dims=3, extra_edges=2, max_size=200)
+        volume = True
+    else:
+        g = workload(name, seed)
+        p, volume = g["p"], name != "w4_transformer"
+    say(f"device assignment after search {name} seed={seed} p={p} volume={volume}")
+    if name == "random":
+        o = _oracle(g, p=p, volume=True)
+        want = o.result()
+    else:
+        gold = _golden(name, seed, volume=volume)
+        want = (int(gold["min_cost"]), gold["strategy"])
+        from oracle.oracle import Oracle
+        o = Oracle(g)
+        o.configs(p)
+    pg, mc, strat = _run(P, g, p=p, keep=False, volume=volume)
+    assert (mc, strat) == want
+    dev, loc, xfer = pg.assign_devices(strat)
+    odev, oloc, oxfer = o.assign_devices(want[1])
+    assert np.array_equal(dev, odev) and np.array_equal(loc, oloc) and np.array_equal(xfer, oxfer)
+    assert pg.stats()["assign_ms"] > 0
+    if volume:
+        def grid(w):
+            n = int((dev[w] >= 0).sum())
+            return dev[w].tolist() == list(range(n)) + [-1] * (p - n)
+        for e, ed in enumerate(g["edges"]):
+            u, v = ed["src"], ed["dst"]
+            if grid(u) and grid(v):
+                assert int(xfer[e]) == int(pg.edge_costs(e)[strat[u], strat[v]]), e
+
+
 # ------------------------------------------------------------------ weight-gradient all-reduce
 @pytest.mark.parametrize("seed", range(8))
 def test_grad_sync_random_graphs(P, seed):

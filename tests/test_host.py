@@ -514,3 +514,68 @@ def test_halo_option_and_geometry(pase):
             pg.enumerate_configs(w["p"])
             bounds.append([pg.vertex_info(v)["key_bound"] for v in range(len(w["vertices"]))])
         assert (bounds[0] != bounds[1]) == changes, name
+
+
+def _oracle_for(g, p, all_int=False):
+    from oracle.oracle import Oracle
+    o = Oracle(g)
+    o.configs(p, all_integers=all_int)   # the assignment needs the configurations only
+    return o
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_assign_devices_match_oracle(pase, seed):
+    """Device assignment of random strategies on random graphs (several tensor
+    dims on one loop dim, unsplit dims, parallel edges; p = 4, 8, 16 with
+    power-of-two splits, p = 6 with every integer split): devices, edge
+    localities and transfers equal the oracle's, entry by entry."""
+    P = pase
+    rng = np.random.default_rng(seed + 500)
+    all_int = seed % 4 == 3
+    p = 6 if all_int else [4, 8, 16][seed % 3]
+    g = random_graph(seed + 40, int(rng.integers(2, 9)), p=p, extra_edges=int(rng.integers(0, 4)))
+    o = _oracle_for(g, p, all_int)
+    pg = P.Graph(g)
+    pg.enumerate_configs(p, all_integers=all_int)
+    assert pg.K == [int(k) for k in o.K]
+    for trial in range(4):
+        strat = [int(rng.integers(0, k)) for k in pg.K]
+        dev, loc, xfer = pg.assign_devices(strat)
+        odev, oloc, oxfer = o.assign_devices(strat)
+        assert np.array_equal(dev, odev), (trial, strat)
+        assert np.array_equal(loc, oloc) and np.array_equal(xfer, oxfer), (trial, strat)
+
+
+@pytest.mark.parametrize("name", ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w4_transformer"])
+def test_assign_devices_workload_strategies(pase, name):
+    """The assignment of each workload's optimal strategy (the stored expected
+    strategy) equals the oracle's; an edge's locality never exceeds its tensor,
+    and on the FC chain (every vertex data parallel) the assignment is the
+    identity with zero transfer."""
+    import json
+    P = pase
+    g = workload(name)
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", f"{name}_seed0.json")))
+    strat = gold["strategy"]
+    o = _oracle_for(g, g["p"])
+    pg = P.Graph(g)
+    pg.enumerate_configs(g["p"])
+    dev, loc, xfer = pg.assign_devices(strat)
+    odev, oloc, oxfer = o.assign_devices(strat)
+    assert np.array_equal(dev, odev) and np.array_equal(loc, oloc) and np.array_equal(xfer, oxfer)
+    assert all(int(loc[e]) <= ed["elems"] for e, ed in enumerate(g["edges"]))
+    if name == "w0_fc_chain":
+        assert (dev == np.arange(g["p"])).all() and not xfer.any()
+
+
+def test_assign_devices_errors(pase):
+    """Call order, bad strategies and the p bound of the assignment."""
+    P = pase
+    g = fc_chain()
+    pg = P.Graph(g)
+    assert _status(lambda: P.pase_assign_devices(pg.h, [0] * pg.nv, pg.nv, pg.ne, 4)) == P.BAD_STATE
+    pg.enumerate_configs(4)
+    assert _status(lambda: pg.assign_devices([pg.K[0]] + [0] * (pg.nv - 1))) == P.INVALID_ARGUMENT
+    assert P.load().pase_assign_devices(pg.h, None, None, None, None) == P.INVALID_ARGUMENT
+    pg.enumerate_configs(2048)
+    assert _status(lambda: pg.assign_devices([0] * pg.nv)) == P.TOO_LARGE

@@ -872,6 +872,99 @@ def test_theorem1_halo(seed):
     assert o.result()[0] == pins.brute_force(L, R, src, dst)[0]
 
 
+# ------------------------------------------------------------------ greedy device assignment
+def _pair_graph(m, src_dim, dst_dim, du, dv, p=4, r=2):
+    """Two vertices joined by one edge carrying a tensor of dims m."""
+    return {"name": "pair", "p": p, "comm_weight": r,
+            "vertices": [{"name": "u", "dims": [max(m)] * du, "dim_names": [f"a{k}" for k in range(du)],
+                          "reduce": [], "flops_per_point": 1},
+                         {"name": "v", "dims": [max(m)] * dv, "dim_names": [f"b{k}" for k in range(dv)],
+                          "reduce": [], "flops_per_point": 1}],
+            "edges": [{"src": 0, "dst": 1, "src_dim": list(src_dim), "dst_dim": list(dst_dim),
+                       "elems": int(np.prod(m))}]}
+
+
+def test_assign_transposed_splits():
+    """u splits (x, y) 2 x 2, v receives the tensor transposed (tensor dim 0
+    on its loop dim 1) and splits it 2 x 2 too: the grid numbering puts
+    mismatched parts on devices 1 and 2 (the volume model charges 2 * 2 * 4 =
+    16), the greedy assignment swaps them -- full locality, no transfer."""
+    from oracle.oracle import Oracle
+    g = _pair_graph([4, 4], [0, 1], [1, 0], 2, 2)
+    o = Oracle(g)
+    o.configs(4, volume=True)
+    sp = [[tuple(int(x) for x in r) for r in o.splits(v)] for v in range(2)]
+    cu, cv = sp[0].index((2, 2)), sp[1].index((2, 2))
+    assert int(o.edge_costs(0)[cu, cv]) == 16
+    dev, loc, xfer = o.assign_devices([cu, cv])
+    assert dev[0].tolist() == [0, 1, 2, 3]
+    assert dev[1].tolist() == [0, 2, 1, 3]
+    assert loc.tolist() == [16] and xfer.tolist() == [0]
+    assert pins.assigned_transfer_elements([4, 4], [0, 1], [1, 0], [2, 2], [2, 2], dev[0].tolist(),
+                                           dev[1].tolist(), 2) == (16, 0)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_assign_against_enumeration(seed):
+    """Random two-vertex edges (tensor dims of 4 or 8 elements, random maps,
+    p = 4, every strategy): the oracle's locality and transfer under its
+    assignment equal element enumeration with the same device maps; each
+    vertex's parts sit on distinct devices; the first keeps the grid
+    numbering (and then the transfer equals the volume model's when the
+    second does too); the greedy reaches at least half the best locality over
+    every injective map of the second vertex's parts (the greedy matching
+    bound), and the best itself when that best is the whole tensor."""
+    from oracle.oracle import Oracle
+    rng = np.random.default_rng(seed + 77)
+    rank = int(rng.integers(1, 3))
+    m = [int(rng.choice([4, 8])) for _ in range(rank)]
+    du, dv = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+    sd = [int(rng.integers(-1, du)) for _ in range(rank)]
+    dd = [int(rng.integers(-1, dv)) for _ in range(rank)]
+    g = _pair_graph(m, sd, dd, du, dv)
+    o = Oracle(g)
+    K = o.configs(4, volume=True)
+    sp = [[[int(x) for x in r] for r in o.splits(v)] for v in range(2)]
+    R = o.edge_costs(0)
+    for cu in range(int(K[0])):
+        for cv in range(int(K[1])):
+            dev, loc, xfer = o.assign_devices([cu, cv])
+            pu, pv = int(np.prod(sp[0][cu])), int(np.prod(sp[1][cv]))
+            assert dev[0].tolist() == list(range(pu)) + [-1] * (4 - pu)
+            assert sorted(x for x in dev[1].tolist() if x >= 0) == list(range(pv))
+            want = pins.assigned_transfer_elements(m, sd, dd, sp[0][cu], sp[1][cv], dev[0].tolist(),
+                                                   dev[1].tolist(), 2)
+            assert (int(loc[0]), int(xfer[0])) == want, (cu, cv)
+            if dev[1].tolist() == list(range(pv)) + [-1] * (4 - pv):
+                assert int(xfer[0]) == int(R[cu, cv])
+            best = 0
+            for devs in itertools.permutations(range(4), pv):
+                part_v = [-1] * 4
+                for h, d in enumerate(devs):
+                    part_v[d] = h
+                best = max(best, pins.assigned_transfer_elements(m, sd, dd, sp[0][cu], sp[1][cv],
+                                                                 dev[0].tolist(), part_v, 2)[0])
+            assert 2 * int(loc[0]) >= best, (cu, cv)
+            if best == int(np.prod(m)) and pu == pv:
+                assert int(loc[0]) == best, (cu, cv)
+
+
+def test_assign_workloads_are_consistent():
+    """On W0 and a residual CNN strategy the assignment is a set of injective
+    maps, and the locality of each edge never exceeds its tensor."""
+    from oracle.oracle import Oracle
+    for g in (fc_chain(), workload("w1_residual_cnn")):
+        o = Oracle(g)
+        o.configs(g["p"], volume=True)
+        o.solve()
+        dev, loc, xfer = o.assign_devices(o.result()[1])
+        for v in range(len(g["vertices"])):
+            parts = [x for x in dev[v].tolist() if x >= 0]
+            assert len(parts) == len(set(parts))
+        for e, ed in enumerate(g["edges"]):
+            assert int(loc[e]) <= ed["elems"]
+
+
 # ------------------------------------------------------------------ planted mistakes
 MUTANTS = {
     "tie_break_last": ("if (cost < mincost) { mincost = cost; arg = c; }",
@@ -912,6 +1005,14 @@ MUTANTS = {
     "comm_over_all_devices": ("if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;",
                               "if (!mul_ok(red_split - 1, ceil_div(keep_n, P), &comm)) return 0;"),
     "seq_keeps_self": ("if (rule == 0) d[(size_t)v * n + v] = 0;", "if (rule == 2) d[(size_t)v * n + v] = 0;"),
+    "assign_smallest": ("if (bg < 0 || W[g * p + d] > best) { bg = (int)g; bd = d; best = W[g * p + d]; }",
+                        "if (bg < 0 || W[g * p + d] < best) { bg = (int)g; bd = d; best = W[g * p + d]; }"),
+    "assign_later_neighbours": ("if (other < 0 || other > v) continue;   /* placed neighbours only */",
+                                "if (other < 0 || other < v) continue;   /* placed neighbours only */"),
+    "assign_ties_last": ("if (bg < 0 || W[g * p + d] > best) { bg = (int)g; bd = d; best = W[g * p + d]; }",
+                         "if (bg < 0 || W[g * p + d] >= best) { bg = (int)g; bd = d; best = W[g * p + d]; }"),
+    "assign_forward_only": ("unsigned __int128 moved = (E * fwd + cells - 1) / cells + (E * bwd + cells - 1) / cells;",
+                            "unsigned __int128 moved = (E * fwd + cells - 1) / cells;"),
     "halo_one_neighbour": ("if (!mul_ok(2 * w, ceil_div(rest, rest_split), &words)) return 0;",
                            "if (!mul_ok(w, ceil_div(rest, rest_split), &words)) return 0;"),
     "halo_own_split": ("if (j == k || !(o->in_mask[v] >> j & 1u)) continue;",
@@ -1050,9 +1151,31 @@ def _pin_suite(lib):
         return (int(L[sp.index((1, 1, 1, 2, 1))]) == 10_944 and int(L[sp.index((1, 1, 1, 2, 2))]) == 5_856
                 and int(L[sp.index((1, 1, 1, 1, 1))]) == 20_736)
 
+    def assign():
+        g = _pair_graph([4, 4], [0, 1], [1, 0], 2, 2)
+        o = Oracle(g, lib)
+        o.configs(4, volume=True)
+        sp = [[tuple(int(x) for x in r) for r in o.splits(v)] for v in range(2)]
+        dev, loc, xfer = o.assign_devices([sp[0].index((2, 2)), sp[1].index((2, 2))])
+        if dev[1].tolist() != [0, 2, 1, 3] or loc.tolist() != [16] or xfer.tolist() != [0]:
+            return False
+        # a 2-part consumer next to a 4-part producer: ties between the parts'
+        # equal localities go to the lowest device
+        g = _pair_graph([4, 4], [0, 1], [0, -1], 2, 1)
+        o = Oracle(g, lib)
+        o.configs(4, volume=True)
+        sp = [[tuple(int(x) for x in r) for r in o.splits(v)] for v in range(2)]
+        dev, loc, xfer = o.assign_devices([sp[0].index((2, 2)), sp[1].index((2,))])
+        if dev[1].tolist() != [0, -1, 1, -1] or loc.tolist() != [8]:
+            return False
+        # both directions of the transfer against element enumeration
+        return (int(loc[0]), int(xfer[0])) == pins.assigned_transfer_elements(
+            [4, 4], [0, 1], [0, -1], [2, 2], [2], dev[0].tolist(), dev[1].tolist(), 2)
+
     guard("w0", w0)
     guard("grad", grad)
     guard("halo", halo)
+    guard("assign", assign)
     guard("bf", bf)
     guard("volume", volume)
     guard("all_integers", all_integers)
