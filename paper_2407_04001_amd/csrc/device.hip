@@ -76,22 +76,120 @@ __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, cons
 }
 
 // Volume-intersection model: every entry of every edge's K_src x K_dst cost
-// matrix (one thread per entry, grid-stride), into the matrix region the prep
-// kernel then reads like caller-given matrices.
-__global__ void k_edge_volume(const DevVertex *__restrict__ V, const DevEdge *__restrict__ E, uint32_t ne,
-                              const uint8_t *__restrict__ ex, uint64_t *__restrict__ out, uint64_t total,
-                              uint64_t r) {
-    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < total;
-         t += (uint64_t)gridDim.x * blockDim.x) {
-        uint32_t lo = 0, hi = ne;   // last edge with mat_off <= t
+// matrix, into the matrix region the prep kernel then reads like caller-given
+// matrices, for every-integer splits (the device walk of volume_cost).  One
+// wave per matrix row (grid-stride over the rows of all edges):
+// the edge and the producer configuration are uniform, found once per row by
+// a scalar search; the lanes take the consumer configurations and write the
+// row contiguously.
+constexpr int kVolumeThreads = 64;
+__global__ __launch_bounds__(kVolumeThreads) void k_edge_volume(const DevVertex *__restrict__ V,
+                                                                const DevEdge *__restrict__ E, uint32_t ne,
+                                                                const uint8_t *__restrict__ ex,
+                                                                uint64_t *__restrict__ out, uint64_t rows,
+                                                                uint64_t r) {
+    for (uint64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+        uint32_t lo = 0, hi = ne;   // last edge with row0 <= row
         while (hi - lo > 1) {
-            uint32_t mid = (lo + hi) / 2;
-            if (E[mid].mat_off <= t) lo = mid; else hi = mid;
+            const uint32_t mid = (lo + hi) / 2;
+            if (E[mid].row0 <= row) lo = mid; else hi = mid;
         }
+        lo = __builtin_amdgcn_readfirstlane(lo);
         const DevEdge de = E[lo];
         const DevVertex u = V[de.src], v = V[de.dst];
-        const uint64_t x = t - de.mat_off, cu = x / v.K, cv = x % v.K;
-        out[t] = volume_cost(u, ex + u.ex_off + cu * u.ndims, v, ex + v.ex_off + cv * v.ndims, de, r);
+        const uint64_t cu = row - de.row0;
+        const uint8_t *exu = ex + u.ex_off + cu * u.ndims;
+        uint64_t *o = out + de.mat_off + cu * v.K;
+        for (uint32_t cv = threadIdx.x; cv < v.K; cv += kVolumeThreads)
+            o[cv] = volume_cost(u, exu, v, ex + v.ex_off + (uint64_t)cv * v.ndims, de, r);
+    }
+}
+
+// The same for power-of-two splits, which have a closed form.  Every
+// coordinate is then a bit field of the device index: tensor dim t's coordinate on u's side is bits
+// [o_u, o_u + l_u) of d (o_u = log2 of the splits of the loop dims after the
+// mapped one, l_u = log2 of its split), on v's side [o_v, o_v + l_v).  The
+// per-dim overlap is min(2^l_u, 2^l_v) when the parts nest -- the top
+// w = min(l_u, l_v) bits of both fields agree -- and 0 otherwise, so
+// |need n hold| over the devices both ends use (d < 2^n, n = the smaller
+// exponent sum; higher bits are zero) is either the product of those minima
+// or 0.  The minimum over d is the product iff, for every tensor dim, the
+// nested fields coincide for every d: w = 0, the fields start at the same bit
+// (o_u + l_u - w = o_v + l_v - w), or both start at bit n or above.  (A
+// minimum over d of a conjunction is the conjunction of the minima.)
+//
+// The producer side of every tensor dim -- its bit field's width and offset --
+// is uniform per row and computed once; each lane reads its consumer row's
+// exponents into registers.
+__global__ __launch_bounds__(kVolumeThreads) void k_edge_volume_pow2(const DevVertex *__restrict__ V,
+                                                                     const DevEdge *__restrict__ E, uint32_t ne,
+                                                                     const uint8_t *__restrict__ ex,
+                                                                     uint64_t *__restrict__ out, uint64_t rows,
+                                                                     uint64_t r) {
+    for (uint64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+        uint32_t lo = 0, hi = ne;   // last edge with row0 <= row
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) / 2;
+            if (E[mid].row0 <= row) lo = mid; else hi = mid;
+        }
+        lo = __builtin_amdgcn_readfirstlane(lo);
+        const DevEdge &de = E[lo];
+        const uint32_t rank = de.rank, du = V[de.src].ndims, dv = V[de.dst].ndims, Kv = V[de.dst].K;
+        const uint64_t cu = row - de.row0;
+        const uint8_t *exu = ex + V[de.src].ex_off + cu * du;
+        // producer side, uniform: exponent sum, and per tensor dim the width and
+        // offset of its bit field
+        uint32_t nu = 0, lu[kMaxDims], ou[kMaxDims];
+#pragma unroll
+        for (int k = 0; k < kMaxDims; k++)
+            if (k < (int)du) nu += exu[k];
+#pragma unroll
+        for (int t = 0; t < kMaxDims; t++) {
+            lu[t] = ou[t] = 0;
+            const int ka = t < (int)rank ? de.sdim[t] : -1;
+            if (ka >= 0) {
+                lu[t] = exu[ka];
+#pragma unroll
+                for (int k = 0; k < kMaxDims; k++)
+                    if (k > ka && k < (int)du) ou[t] += exu[k];
+            }
+        }
+        const uint64_t elems = de.elems;
+        const uint8_t *exv0 = ex + V[de.dst].ex_off;
+        uint64_t *o = out + de.mat_off + cu * Kv;
+        for (uint32_t cv = threadIdx.x; cv < Kv; cv += kVolumeThreads) {
+            const uint8_t *exv = exv0 + (uint64_t)cv * dv;
+            uint32_t e[kMaxDims], suffix[kMaxDims + 1];
+#pragma unroll
+            for (int k = 0; k < kMaxDims; k++) e[k] = k < (int)dv ? exv[k] : 0;
+            suffix[kMaxDims] = 0;   // suffix[k] = sum of the exponents of loop dims k..
+#pragma unroll
+            for (int k = kMaxDims - 1; k >= 0; k--) suffix[k] = suffix[k + 1] + e[k];
+            const uint32_t nv = suffix[0], n = nu < nv ? nu : nv;
+            uint32_t lq = 0, lneed = 0, lhold = 0, lc = 0;
+            bool nested = true;
+#pragma unroll
+            for (int t = 0; t < kMaxDims; t++) {
+                if (t < (int)rank) {
+                    const int kb = de.ddim[t];
+                    uint32_t lv = 0, ov = 0;
+                    // select by an unrolled scan so that e[] and suffix[] stay in registers
+#pragma unroll
+                    for (int k = 0; k < kMaxDims; k++)
+                        if (k == kb) { lv = e[k]; ov = suffix[k + 1]; }
+                    const uint32_t w = lu[t] < lv ? lu[t] : lv, fu = ou[t] + lu[t] - w, fv = ov + lv - w;
+                    nested &= w == 0 || fu == fv || (fu >= n && fv >= n);
+                    lq += lu[t] + lv;
+                    lneed += lu[t];
+                    lhold += lv;
+                    lc += w;
+                }
+            }
+            const uint32_t need_v = 1u << lneed, hold_u = 1u << lhold, m = nested ? 1u << lc : 0;
+            const uint32_t fwd = nv > nu ? need_v : need_v - m, bwd = nu > nv ? hold_u : hold_u - m;
+            const uint64_t hi_ = elems >> lq, lo_ = elems & ((1ull << lq) - 1), round = (1ull << lq) - 1;
+            o[cv] = r * (hi_ * fwd + ((lo_ * fwd + round) >> lq) + hi_ * bwd + ((lo_ * bwd + round) >> lq));
+        }
     }
 }
 
@@ -475,8 +573,9 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
                            dE, (uint32_t)ne, dex, dL, dls, dsig, si.nL, P.sig_count, g->r);
         launches_n++;
         if (g->volume && g->mat_total) {
-            hipLaunchKernelGGL(k_edge_volume, dim3(grid_for(g->mat_total, 256, 65535)), dim3(256), 0, s, dV, dE,
-                               (uint32_t)ne, dex, (uint64_t *)(ws + P.off_vmat), g->mat_total, g->r);
+            hipLaunchKernelGGL(g->factors ? k_edge_volume : k_edge_volume_pow2, dim3(grid_for(g->mat_rows, 1, 65535)),
+                               dim3(kVolumeThreads), 0, s, dV, dE, (uint32_t)ne, dex, (uint64_t *)(ws + P.off_vmat),
+                               g->mat_rows, g->r);
             launches_n++;
         }
     }

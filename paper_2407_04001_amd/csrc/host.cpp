@@ -881,6 +881,8 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
     g->volume = g->transfer_opt == 1;
     g->mat_off.assign(g->E.size(), 0);
     g->mat_total = 0;
+    g->mat_row0.assign(g->E.size(), 0);
+    g->mat_rows = 0;
     if (g->volume) {
         // the device's volume arithmetic needs Q = prod_t s_u(t) * s_v(t) < 2^32:
         // with distinct mapped loop dims per side each product is at most p,
@@ -1004,6 +1006,8 @@ extern "C" pase_status pase_enumerate_configs(pase_graph_t g, uint32_t p) {
         if (g->volume) {
             g->mat_off[e] = g->mat_total;
             g->mat_total += (uint64_t)g->K[g->E[e].src] * g->K[g->E[e].dst];
+            g->mat_row0[e] = g->mat_rows;
+            g->mat_rows += g->K[g->E[e].src];
         }
     }
     g->enumerated = true;

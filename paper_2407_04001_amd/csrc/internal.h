@@ -53,6 +53,7 @@ struct DevEdge {
     uint64_t elems;
     uint64_t sig_off;         // element offset of its split signatures: K_src, then K_dst
     uint64_t mat_off;         // volume transfer model: element offset of its K_src x K_dst matrix
+    uint64_t row0;            // volume transfer model: its first matrix row among all edges' rows
 };
 
 // One contribution to a precomputed block element (see Prep below).
@@ -291,6 +292,8 @@ struct pase_graph_s {
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix
     uint64_t mat_total = 0;         // volume model: entries of all edge matrices
+    std::vector<uint64_t> mat_row0; // volume model: first matrix row of each edge (rows = K_src)
+    uint64_t mat_rows = 0;          // volume model: rows of all edge matrices
     uint32_t p = 0;
     bool factors = false;           // the enumerated set: split rows hold factors, not exponents
     std::vector<uint32_t> K;

@@ -190,6 +190,8 @@ __device__ __forceinline__ uint32_t split_of(const DevVertex &x, const uint8_t *
 // side advances every `stride` devices (the product of the splits of the loop
 // dims after the mapped one) and wraps at the split; all per-dim state is
 // indexed by unrolled constants so it stays in registers.
+//
+// Power-of-two splits take the closed form of k_edge_volume_pow2 instead.
 __device__ __forceinline__ uint64_t volume_cost(const DevVertex &u, const uint8_t *exu, const DevVertex &v,
                                                 const uint8_t *exv, const DevEdge &de, uint64_t r) {
     uint32_t Pu = 1, Pv = 1;

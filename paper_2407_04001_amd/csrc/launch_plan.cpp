@@ -400,6 +400,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         x.elems = g->E[e].elems;
         x.sig_off = sig_off;
         x.mat_off = g->volume ? g->mat_off[e] : 0;
+        x.row0 = g->volume ? g->mat_row0[e] : 0;
         sig_off += (uint64_t)g->K[x.src] + g->K[x.dst];
     }
     if (ne) {
