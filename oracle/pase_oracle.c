@@ -470,89 +470,96 @@ int oracle_set_costs(oracle_t *o, const uint64_t *layer, const uint64_t *edge) {
 
 /* --------------------------------------------------------- ordering */
 
-static int cmp_int(const void *a, const void *b) { return *(const int *)a - *(const int *)b; }
 
-/* GenerateSeq (Fig. 3).  rule 0: the d-set of v never contains v itself,
- * v.d <- (v.d U v_i.d) - {v_i, v}.  rule 1: the update exactly as printed,
- * v.d <- v.d U v_i.d - {v_i}, so v may count itself while unsequenced; the
- * recorded dependent set drops v_i.  Either way D(i) is v_i.d at selection. */
+/* The component of u in the subgraph induced by the vertices marked in `in`
+ * (u itself included whatever its mark): comp[] receives 1 for its members.
+ * Returns the member count. */
+static int component(oracle_t *o, const char *in, int u, char *comp, int *stack) {
+    int n = o->nv, top = 0, size = 0;
+    memset(comp, 0, n);
+    comp[u] = 1;
+    stack[top++] = u;
+    while (top) {
+        int x = stack[--top];
+        size++;
+        for (int k = 0; k < o->deg[x]; k++) {
+            int y = o->nbr[x][k];
+            if (in[y] && !comp[y]) { comp[y] = 1; stack[top++] = y; }
+        }
+    }
+    return size;
+}
+
+/* The dependent set (Sec. III-B) that u has when it follows the vertices
+ * marked in `placed`: the neighbours, neither placed nor u, of u's component
+ * in the subgraph induced by placed + {u}.  dep[] receives 1 for its members;
+ * returns its size. */
+static int dependents_after(oracle_t *o, char *placed, int u, char *dep, char *comp, int *stack) {
+    int n = o->nv, size = 0;
+    char was = placed[u];
+    placed[u] = 1;
+    component(o, placed, u, comp, stack);
+    placed[u] = was;
+    memset(dep, 0, n);
+    for (int x = 0; x < n; x++) {
+        if (!comp[x]) continue;
+        for (int k = 0; k < o->deg[x]; k++) {
+            int y = o->nbr[x][k];
+            if (!placed[y] && y != u && !dep[y]) { dep[y] = 1; size++; }
+        }
+    }
+    return size;
+}
+
+/* GenerateSeq (Fig. 3), a greedy order: each step places the unplaced vertex
+ * with the smallest d-set, ties to the lowest vertex id.  The paper keeps the
+ * d-sets up to date by merging the chosen vertex's set into its members' sets;
+ * by Theorem 2 a vertex's d-set is then exactly the dependent set it would
+ * have if placed next, which is what this evaluates.  rule 0: that is the size
+ * compared.  rule 1 (the merge as printed, which does not remove a member from
+ * its own set): a vertex enters its own d-set when a placed vertex merges into
+ * it -- exactly when it has a placed neighbour -- and counts itself from then
+ * on.  D(i) is the chosen vertex's dependent set. */
 static void generate_seq(oracle_t *o, int rule) {
     int n = o->nv;
-    char *d = calloc((size_t)n * n, 1);   /* d[v*n+u] = u in v.d */
-    char *in_U = calloc(n, 1);
-    for (int v = 0; v < n; v++) {
-        in_U[v] = 1;
-        for (int k = 0; k < o->deg[v]; k++) d[(size_t)v * n + o->nbr[v][k]] = 1;
-    }
+    char *placed = calloc(n, 1), *dep = calloc(n, 1), *comp = calloc(n, 1);
+    int *stack = calloc(n, sizeof(int));
     for (int i = 0; i < n; i++) {
         int best = -1, best_sz = 0;
         for (int u = 0; u < n; u++) {
-            if (!in_U[u]) continue;
-            int sz = 0;
-            for (int w = 0; w < n; w++) sz += d[(size_t)u * n + w];
+            if (placed[u]) continue;
+            int sz = dependents_after(o, placed, u, dep, comp, stack);
+            if (rule == 1) {
+                int placed_neighbour = 0;
+                for (int k = 0; k < o->deg[u]; k++) placed_neighbour |= placed[o->nbr[u][k]];
+                sz += placed_neighbour;
+            }
             if (best < 0 || sz < best_sz) { best = u; best_sz = sz; }
         }
-        int vi = best;
-        o->seq[i] = vi;
-        o->pos[vi] = i;
-        in_U[vi] = 0;
-        o->nD[i] = 0;
-        for (int w = 0; w < n; w++)
-            if (d[(size_t)vi * n + w] && w != vi) o->D[i][o->nD[i]++] = w;
-        for (int v = 0; v < n; v++) {
-            if (!d[(size_t)vi * n + v] || v == vi) continue;
-            for (int w = 0; w < n; w++) d[(size_t)v * n + w] |= d[(size_t)vi * n + w];
-            d[(size_t)v * n + vi] = 0;
-            if (rule == 0) d[(size_t)v * n + v] = 0;
-        }
+        o->seq[i] = best;
+        o->pos[best] = i;
+        placed[best] = 1;
     }
-    free(d);
-    free(in_U);
+    free(placed); free(dep); free(comp); free(stack);
 }
 
-/* Vertices reachable from `start` through vertices whose position is <= lim
- * (the paper's DFS(G, U, v) with U = V_{<=lim}). mark[] receives `tag`. */
-static void dfs(oracle_t *o, int start, int lim, int *mark, int tag, int *stack) {
-    int top = 0;
-    stack[top++] = start;
-    mark[start] = tag;
-    while (top) {
-        int v = stack[--top];
-        for (int k = 0; k < o->deg[v]; k++) {
-            int u = o->nbr[v][k];
-            if (o->pos[u] <= lim && mark[u] != tag) {
-                mark[u] = tag;
-                stack[top++] = u;
-            }
-        }
-    }
-}
-
-/* Dependent sets from their definition, D(i) = N(X(i)) intersected with
- * V_{>i} (Sec. III-B), for a caller-given order. */
-static void dependent_sets_by_definition(oracle_t *o) {
+/* D(i) for every position of the order in seq[] / pos[], from the definition:
+ * the dependent set of v_i after the vertices of positions < i (ascending
+ * vertex ids). */
+static void dependent_sets(oracle_t *o) {
     int n = o->nv;
-    int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
-    char *inD = calloc(n, 1);
+    char *placed = calloc(n, 1), *dep = calloc(n, 1), *comp = calloc(n, 1);
+    int *stack = calloc(n, sizeof(int));
     for (int i = 0; i < n; i++) {
-        for (int v = 0; v < n; v++) mark[v] = -1;
-        dfs(o, o->seq[i], i, mark, 1, stack);
-        memset(inD, 0, n);
-        for (int v = 0; v < n; v++)
-            if (mark[v] == 1)
-                for (int k = 0; k < o->deg[v]; k++)
-                    if (o->pos[o->nbr[v][k]] > i) inD[o->nbr[v][k]] = 1;
+        dependents_after(o, placed, o->seq[i], dep, comp, stack);
         o->nD[i] = 0;
-        for (int v = 0; v < n; v++) if (inD[v]) o->D[i][o->nD[i]++] = v;
+        for (int v = 0; v < n; v++) if (dep[v]) o->D[i][o->nD[i]++] = v;
+        placed[o->seq[i]] = 1;
     }
-    free(mark); free(stack); free(inD);
+    free(placed); free(dep); free(comp); free(stack);
 }
 
 /* --------------------------------------------------------- dynamic program */
-
-typedef struct {          /* one lookup T_j[phi''] in recurrence (4) */
-    int j;                /* position of the component's last vertex */
-} term_t;
 
 /* Canonical index of phi restricted to D(j), read from a full assignment. */
 static uint64_t table_index(oracle_t *o, int j, const int *cfg_of) {
@@ -606,6 +613,53 @@ static void back_substitute(oracle_t *o) {
     o->solved = 1;
 }
 
+/* S(i) of recurrence (4): the components of X(i) - {v_i}, X(i) being v_i's
+ * component among the vertices of positions <= i.  Each component is the
+ * connected set X(j) of its last position j (Sec. III-B), so its optimum for
+ * a given assignment of D(j) is the table R(j, .).  sub[] receives those
+ * positions j; returns their count. */
+static int subproblems(oracle_t *o, int i, int *sub, char *before, char *X, char *Y, char *taken, int *stack) {
+    int n = o->nv, nsub = 0;
+    for (int v = 0; v < n; v++) before[v] = o->pos[v] < i;
+    component(o, before, o->seq[i], X, stack);   /* X(i) */
+    memset(taken, 0, n);
+    for (int x = 0; x < n; x++) {
+        if (!X[x] || x == o->seq[i] || taken[x]) continue;
+        component(o, before, x, Y, stack);       /* one component of X(i) - {v_i} */
+        int j = -1;
+        for (int y = 0; y < n; y++)
+            if (Y[y]) { taken[y] = 1; if (o->pos[y] > j) j = o->pos[y]; }
+        sub[nsub++] = j;
+    }
+    return nsub;
+}
+
+/* One entry of recurrence (4): with an assignment phi of D(i) in cfg_of,
+ *   R(i, phi) = min over c in C(v_i) of  H(i, phi + {v_i: c})
+ *               + sum over j in S(i) of R(j, (phi + {v_i: c}) restricted to D(j)),
+ * H being the node function of eq. (3).  Configurations are tried in
+ * ascending index order and the first smallest wins.  Returns 0 when a sum
+ * overflows uint64. */
+static int recurrence_entry(oracle_t *o, int i, const int *sub, int nsub, const int *later, int nlater,
+                            int *cfg_of, uint64_t *value, int *arg) {
+    int vi = o->seq[i];
+    uint64_t best = 0;
+    int best_c = 0;
+    for (int c = 0; c < o->K[vi]; c++) {
+        cfg_of[vi] = c;
+        uint64_t cand;
+        if (!node_cost(o, i, later, nlater, cfg_of, &cand)) return 0;
+        for (int t = 0; t < nsub; t++) {   /* the subproblems' optima */
+            int j = sub[t];
+            if (!add_ok(cand, o->T[j][table_index(o, j, cfg_of)], &cand)) return 0;
+        }
+        if (c == 0 || cand < best) { best = cand; best_c = c; }
+    }
+    *value = best;
+    *arg = best_c;
+    return 1;
+}
+
 /* FindBestStrategy (Fig. 4).  order: NULL -> GenerateSeq with `rule`, else the
  * given sequence of vertex ids (dependent sets then come from their
  * definition).  max_cells > 0 stops after the first vertex that reaches that
@@ -624,37 +678,38 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
     o->strategy = calloc(n, sizeof(int));
     o->solved = 0; o->overflow = 0; o->cells_done = 0;
 
+    char *all = calloc(n, 1), *X = calloc(n, 1), *Y = calloc(n, 1), *taken = calloc(n, 1);
+    int *stack = calloc(n, sizeof(int));
     /* weak connectivity (the paper's computation graphs are weakly connected) */
-    {
-        int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
-        for (int v = 0; v < n; v++) { mark[v] = 0; o->pos[v] = 0; }
-        dfs(o, 0, 0, mark, 1, stack);
-        int ok = 1;
-        for (int v = 0; v < n; v++) ok &= mark[v] == 1;
-        free(mark); free(stack);
-        if (!ok) return fail(o, "graph is not weakly connected");
+    memset(all, 1, n);
+    if (component(o, all, 0, X, stack) != n) {
+        free(all); free(X); free(Y); free(taken); free(stack);
+        return fail(o, "graph is not weakly connected");
     }
 
     if (order) {
         char *seen = calloc(n, 1);
         for (int i = 0; i < n; i++) {
-            if (order[i] < 0 || order[i] >= n || seen[order[i]]) { free(seen); return fail(o, "bad order"); }
+            if (order[i] < 0 || order[i] >= n || seen[order[i]]) {
+                free(seen); free(all); free(X); free(Y); free(taken); free(stack);
+                return fail(o, "bad order");
+            }
             seen[order[i]] = 1;
             o->seq[i] = order[i];
             o->pos[order[i]] = i;
         }
         free(seen);
-        dependent_sets_by_definition(o);
     } else {
         generate_seq(o, rule);
     }
-    for (int i = 0; i < n; i++) qsort(o->D[i], o->nD[i], sizeof(int), cmp_int);
+    dependent_sets(o);
 
-    if (!table_sizes(o)) return fail(o, "table too large");
+    if (!table_sizes(o)) {
+        free(all); free(X); free(Y); free(taken); free(stack);
+        return fail(o, "table too large");
+    }
 
-    int *mark = calloc(n, sizeof(int)), *stack = calloc(n, sizeof(int));
-    int *comp = calloc(n, sizeof(int));
-    term_t *terms = calloc(n, sizeof(term_t));
+    int *sub = calloc(n, sizeof(int));
     int *later = calloc(o->ne + 1, sizeof(int));
     struct timespec t0, t1;
     clock_gettime(CLOCK_MONOTONIC, &t0);
@@ -662,32 +717,8 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
 
     for (int i = 0; i < n && !stopped; i++) {
         int vi = o->seq[i];
-        /* X(i) = DFS(G, V_{<=i}, v_i) */
-        for (int v = 0; v < n; v++) { mark[v] = 0; comp[v] = 0; }
-        dfs(o, vi, i, mark, 1, stack);
-        /* S(i): components of X(i) - {v_i} inside V_{<i}; each is represented
-         * by j = the largest position among its vertices */
-        int nterms = 0;
-        for (int v = 0; v < n; v++) {
-            if (mark[v] != 1 || v == vi || comp[v]) continue;
-            int tag = nterms + 2;
-            int *m2 = comp;
-            /* DFS(G, V_{<i}, v) */
-            int top = 0;
-            stack[top++] = v; m2[v] = tag;
-            int jmax = o->pos[v];
-            while (top) {
-                int x = stack[--top];
-                if (o->pos[x] > jmax) jmax = o->pos[x];
-                for (int k = 0; k < o->deg[x]; k++) {
-                    int u = o->nbr[x][k];
-                    if (o->pos[u] < i && m2[u] != tag) { m2[u] = tag; stack[top++] = u; }
-                }
-            }
-            terms[nterms++].j = jmax;
-        }
-
-        /* edges joining v_i and a vertex later in the sequence */
+        int nsub = subproblems(o, i, sub, all, X, Y, taken, stack);
+        /* the edges H charges to v_i: those joining it to a later vertex */
         int nlater = 0;
         for (int e = 0; e < o->ne; e++) {
             int other = o->src[e] == vi ? o->dst[e] : (o->dst[e] == vi ? o->src[e] : -1);
@@ -695,7 +726,6 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
         }
 
         uint64_t N = o->N[i];
-        int Ki = o->K[vi];
         o->T[i] = malloc(N * sizeof(uint64_t));
         o->A[i] = malloc(N * sizeof(uint16_t));
         int nd = o->nD[i];
@@ -713,37 +743,28 @@ int oracle_solve(oracle_t *o, int rule, const int *order, uint64_t max_cells, in
 #pragma omp for schedule(static)
 #endif
             for (int64_t phi = 0; phi < (int64_t)N; phi++) {
-                /* decode phi in canonical mixed radix (first digit slowest) */
+                /* the assignment of D(i) with canonical index phi (first digit slowest) */
                 uint64_t rem = (uint64_t)phi;
                 for (int k = nd - 1; k >= 0; k--) {
                     uint64_t Kw = (uint64_t)o->K[Di[k]];
                     cfg_of[Di[k]] = (int)(rem % Kw);
                     rem /= Kw;
                 }
-                uint64_t mincost = UINT64_MAX;   /* the paper's top element */
-                int arg = 0;
-                for (int c = 0; c < Ki; c++) {
-                    cfg_of[vi] = c;                     /* phi' = phi U {(v_i, C)} */
-                    uint64_t cost;
-                    if (!node_cost(o, i, later, nlater, cfg_of, &cost)) { ovf = 1; break; }
-                    for (int t = 0; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */
-                        int j = terms[t].j;
-                        if (!add_ok(cost, o->T[j][table_index(o, j, cfg_of)], &cost)) { ovf = 1; break; }
-                    }
-                    if (cost < mincost) { mincost = cost; arg = c; }
-                }
-                o->T[i][phi] = mincost;
+                uint64_t value;
+                int arg;
+                if (!recurrence_entry(o, i, sub, nsub, later, nlater, cfg_of, &value, &arg)) { ovf = 1; continue; }
+                o->T[i][phi] = value;
                 o->A[i][phi] = (uint16_t)arg;
             }
             free(cfg_of);
         }
         if (ovf) { o->overflow = 1; stopped = 1; break; }
-        o->cells_done += N * (uint64_t)Ki;
+        o->cells_done += N * (uint64_t)o->K[vi];
         if (max_cells && o->cells_done >= max_cells && i + 1 < n) stopped = 2;
     }
     clock_gettime(CLOCK_MONOTONIC, &t1);
     o->seconds = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
-    free(mark); free(stack); free(comp); free(terms); free(later);
+    free(all); free(X); free(Y); free(taken); free(stack); free(sub); free(later);
     if (o->overflow) return fail(o, "cost overflows uint64");
     if (stopped == 2) return 2;  /* partial run: timing sample only */
 

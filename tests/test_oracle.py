@@ -967,12 +967,12 @@ def test_assign_workloads_are_consistent():
 
 # ------------------------------------------------------------------ planted mistakes
 MUTANTS = {
-    "tie_break_last": ("if (cost < mincost) { mincost = cost; arg = c; }",
-                       "if (cost <= mincost) { mincost = cost; arg = c; }"),
+    "tie_break_last": ("if (c == 0 || cand < best) { best = cand; best_c = c; }",
+                       "if (c == 0 || cand <= best) { best = cand; best_c = c; }"),
     "transposed_edge": ("uint64_t x = o->Rx[e][(size_t)cfg_of[u] * o->K[v] + cfg_of[v]];",
                         "uint64_t x = o->Rx[e][(size_t)cfg_of[v] * o->K[u] + cfg_of[u]];"),
-    "dropped_lookup": ("for (int t = 0; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */",
-                       "for (int t = 1; t < nterms; t++) {  /* + R_V(j, phi'|D(j)) */"),
+    "dropped_lookup": ("for (int t = 0; t < nsub; t++) {   /* the subproblems' optima */",
+                       "for (int t = 1; t < nsub; t++) {   /* the subproblems' optima */"),
     "earlier_edges": ("if (other >= 0 && o->pos[other] > i) later[nlater++] = e;",
                       "if (other >= 0 && o->pos[other] < i) later[nlater++] = e;"),
     "seq_tie_highest": ("if (best < 0 || sz < best_sz) { best = u; best_sz = sz; }",
@@ -1004,7 +1004,7 @@ MUTANTS = {
                                 "uint64_t compute = ceil_div(flops, keep_split);"),
     "comm_over_all_devices": ("if (!mul_ok(red_split - 1, ceil_div(keep_n, keep_split), &comm)) return 0;",
                               "if (!mul_ok(red_split - 1, ceil_div(keep_n, P), &comm)) return 0;"),
-    "seq_keeps_self": ("if (rule == 0) d[(size_t)v * n + v] = 0;", "if (rule == 2) d[(size_t)v * n + v] = 0;"),
+    "seq_keeps_self": ("if (rule == 1) {", "if (rule != 2) {"),
     "assign_smallest": ("if (bg < 0 || W[g * p + d] > best) { bg = (int)g; bd = d; best = W[g * p + d]; }",
                         "if (bg < 0 || W[g * p + d] < best) { bg = (int)g; bd = d; best = W[g * p + d]; }"),
     "assign_later_neighbours": ("if (other < 0 || other > v) continue;   /* placed neighbours only */",
