@@ -184,6 +184,15 @@ typedef enum {
                                    PASE_OPT_KERNEL = 1 */
     PASE_OPT_BULK_US = 17,      /* schedule 4: planned fill time (microseconds) from which a
                                    row-kernel vertex runs on the bulk stream (default 100) */
+    PASE_OPT_FUSED_MIN = 20,    /* 1 (default): a row-kernel vertex without a column digit whose one
+                                   lookup is the whole table of its predecessor in the recurrence
+                                   (that table's column digit being this vertex, the same row
+                                   digits, no outer digits, no c split) has its minimum over c
+                                   formed in that predecessor's fill epilogue, combined across
+                                   workgroups with 64-bit atomic minima of the packed keys (the
+                                   strict "<" tie-break is unchanged: keys are distinct per c),
+                                   so the predecessor's table is never written to HBM and read
+                                   back; 0: every vertex fills on its own.  Re-plans */
     PASE_OPT_HALO = 19          /* 1: the next pase_enumerate_configs adds the halo exchange of
                                    convolutions to every layer cost (an assumed form; the paper
                                    counts halo communication in t_l but prints no formula): for
@@ -372,7 +381,8 @@ typedef struct {
                             below (key_bound + 1) * 2^ceil(log2 K_v)); ~0 if it exceeds 64 bits */
     uint64_t table_bound; /* upper bound of every entry of its DP table; ~0 likewise */
     uint32_t key_type;    /* key type of the plan (the same for every vertex): 0 fp64, 1 uint64, 2 128-bit */
-    uint32_t pad;
+    uint32_t fused;       /* PASE_OPT_FUSED_MIN: 1 = its fill also forms the minimum of its table's reader,
+                             2 = that reader (its fill is then a one-split reduction of those keys), 0 = neither */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

@@ -37,14 +37,18 @@ using namespace pase;
 // Cost tables of the search: layer cost and device byte (device count or its
 // log2) of every (vertex, configuration), and the split signatures of every
 // (edge endpoint, configuration); r * t_x(e, cu, cv) is then read off two
-// signatures and two device bytes (edge_cost_sig).
+// signatures and two device bytes (edge_cost_sig).  The same launch sets the
+// nF keys of the fused minima to the sentinel `fill` (with caller-given costs
+// it runs for that alone, nL = nS = 0).
 __global__ void k_cost_tables(const DevVertex *__restrict__ V, uint32_t nv, const DevEdge *__restrict__ E,
                               uint32_t ne, const uint8_t *__restrict__ ex, uint64_t *__restrict__ L,
                               uint8_t *__restrict__ lsum, uint64_t *__restrict__ sig, uint64_t nL,
-                              uint64_t nS, uint64_t r) {
-    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < nL + nS;
+                              uint64_t nS, uint64_t r, uint64_t *__restrict__ fkeys, uint64_t nF, uint64_t fill) {
+    for (uint64_t t = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; t < nL + nS + nF;
          t += (uint64_t)gridDim.x * blockDim.x) {
-        if (t < nL) {
+        if (t >= nL + nS) {
+            fkeys[t - nL - nS] = fill;
+        } else if (t < nL) {
             uint32_t lo = 0, hi = nv;   // last vertex with L_off <= t
             while (hi - lo > 1) {
                 uint32_t mid = (lo + hi) / 2;
@@ -568,9 +572,24 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         HIPCHK(hipEventRecord(d->phase_ev[0], s));
     }
     uint32_t launches_n = 0;
+    // keys of the fused minima start at the sentinel (the bit pattern of the
+    // key type's sentinel: keys are non-negative, so 64-bit patterns order like them)
+    uint64_t nF = 0, fsent = 0;
+    if constexpr (!kWide) {
+        nF = P.fused_bytes / 8;
+        const KeyT sk = KeyOps<KeyT>::sentinel();
+        std::memcpy(&fsent, &sk, 8);
+    }
+    uint64_t *dfk = (uint64_t *)(ws + P.off_fused);
+    if (g->overridden && nF) {
+        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(nF)), dim3(256), 0, s, dV, (uint32_t)nv, dE, (uint32_t)ne, dex,
+                           dL, dls, dsig, (uint64_t)0, (uint64_t)0, g->r, dfk, nF, fsent);
+        launches_n++;
+    }
     if (!g->overridden) {
-        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(si.nL + P.sig_count)), dim3(256), 0, s, dV, (uint32_t)nv,
-                           dE, (uint32_t)ne, dex, dL, dls, dsig, si.nL, P.sig_count, g->r);
+        hipLaunchKernelGGL(k_cost_tables, dim3(grid_for(si.nL + P.sig_count + nF)), dim3(256), 0, s, dV,
+                           (uint32_t)nv, dE, (uint32_t)ne, dex, dL, dls, dsig, si.nL, P.sig_count, g->r, dfk, nF,
+                           fsent);
         launches_n++;
         if (g->volume && g->mat_total) {
             hipLaunchKernelGGL(g->factors ? k_edge_volume : k_edge_volume_pow2, dim3(grid_for(g->mat_rows, 1, 65535)),
@@ -686,16 +705,20 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
     if (profile) HIPCHK(hipEventRecord(d->phase_ev[3], s));
     HIPCHK(hipGetLastError());
     // the staging buffer is reused for the results: the stream runs the
-    // upload before these copies
+    // upload before this copy.  The strategy and the search output are
+    // adjacent in the workspace ([off_cfg, off_out + sizeof(SearchOut))), so
+    // one copy brings both back
     char *host_out = img;
-    HIPCHK(hipMemcpyAsync(host_out, dout, sizeof(SearchOut), hipMemcpyDeviceToHost, s));
-    HIPCHK(hipMemcpyAsync(host_out + sizeof(SearchOut), dcfg, nv * 4, hipMemcpyDeviceToHost, s));
+    const uint64_t out_bytes = P.off_out - P.off_cfg + sizeof(SearchOut);
+    // (the staging buffer holds at least max(off_cfg, 4096) bytes)
+    if (out_bytes > std::max<uint64_t>(P.off_cfg, 4096)) return fail(g, PASE_ERR_INTERNAL, "result staging size");
+    HIPCHK(hipMemcpyAsync(host_out, dcfg, out_bytes, hipMemcpyDeviceToHost, s));
     HIPCHK(hipStreamSynchronize(s));
     SearchOut so;
-    std::memcpy(&so, host_out, sizeof so);
+    std::memcpy(&so, host_out + (P.off_out - P.off_cfg), sizeof so);
     if (so.status) return fail(g, PASE_ERR_INTERNAL, "back-substitution read an argmin out of range");
     *min_cost = so.min_cost;
-    std::memcpy(cfg, host_out + sizeof(SearchOut), nv * 4);
+    std::memcpy(cfg, host_out, nv * 4);
 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;

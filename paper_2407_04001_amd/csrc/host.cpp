@@ -383,6 +383,33 @@ TileTime tile_time_cached(uint64_t MO, uint64_t MR, uint32_t Kz, uint32_t K, uin
 
 }  // namespace
 
+// Fused minima.  A row-kernel vertex i2 without a column digit whose only
+// lookup is the table of i1 -- a row-kernel vertex whose column digit is v_i2,
+// with no outer digits, the same row digits and neither of them split over c
+// -- streams all of T_i1 once to take, per row, a minimum over c = z.  i1's fill
+// forms those keys itself in its epilogue instead (T_i1 has no other reader),
+// so T_i1 is neither written to nor read back from HBM, and i2 keeps a
+// one-split reduction of the combined keys.  i2's prep blocks hold static
+// costs only (its one lookup is read in the kernel), so they are built in
+// i1's prep launch, before i1's fill.  Both run on one lane.
+static void fuse_minima(pase_graph_t g, Plan &P) {
+    (void)g;
+    const int n = (int)P.v.size();
+    for (int i2 = 0; i2 < n; i2++) {
+        VPlan &b = P.v[i2];
+        if (b.kernel != kRows || b.z >= 0 || b.nsplit != 1 || b.terms.size() != 1 || b.terms[0].dig.size() < 2)
+            continue;
+        const int i1 = b.terms[0].j;
+        VPlan &a = P.v[i1];
+        if (a.kernel != kRows || a.z != b.vi || !a.O.empty() || a.R != b.R || a.nsplit != 1 || a.consumer != i2 ||
+            a.lane != b.lane || a.fuse_into >= 0 || a.fused_from >= 0)
+            continue;
+        a.fuse_into = i2;
+        b.fused_from = i1;
+        P.fused++;
+    }
+}
+
 // Bulk lane schedule.  Row-kernel vertices planned to take at least bulk_us
 // (the large fills, which keep the whole GPU busy on their own) run on lane 1
 // (a stream of its own), and so does every vertex that reads a table of lane 1
@@ -687,6 +714,7 @@ static pase_status build_plan(pase_graph_t g) {
     }
     for (auto &vp : P.v) vp.lane = 0;
     if (g->schedule == kSchedBulk) assign_bulk_lanes(P, (double)g->bulk_us);
+    if (g->fuse_min && kernel_mode == 0) fuse_minima(g, P);
     g->stats.plan_ms = ms_since(t1);
     return PASE_OK;
 }
@@ -828,8 +856,9 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
             for (int u : vp.D) e += align_up((uint64_t)vp.K * g->K[u], 32);
         }   // the direct fill needs no prep blocks and no split scratch
         vp.block_elems = e;
-        // (the resident layout keeps every vertex's scratch: one slot for all)
-        const int sl = resident ? 0 : vp.slot;
+        // (the resident layout keeps every vertex's scratch: one slot for all;
+        // a fused minimum's blocks are built and read in its producer's slot)
+        const int sl = resident ? 0 : vp.fused_from >= 0 ? P.v[vp.fused_from].slot : vp.slot;
         vp.block_off = bsum[sl];
         vp.partial_off = psum[sl];
         bsum[sl] += align_up(e * kb, A);
@@ -843,6 +872,16 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     P.partial_bytes = pmax;
     P.off_partial = off;
     off = align_up(off + P.partial_bytes, A);
+    // keys of the fused minima: written in the producer's slot, read in the
+    // reader's, so not shared with any other scratch
+    P.fused_bytes = 0;
+    for (auto &vp : P.v)
+        if (vp.fused_from >= 0) {
+            vp.fkeys_off = P.fused_bytes;
+            P.fused_bytes += align_up(vp.N * kb, A);
+        }
+    P.off_fused = off;
+    off = align_up(off + P.fused_bytes, A);
     P.total = off;
     if (P.total > g->mem_budget)
         return fail(g, PASE_ERR_TOO_LARGE, "device memory need exceeds the memory budget");
@@ -1124,13 +1163,18 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 65535) return fail(g, PASE_ERR_INVALID_ARGUMENT, "c splits 0..65535");
         g->c_splits = (uint32_t)value;
         break;
+    case PASE_OPT_FUSED_MIN:
+        if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "fused minimum 0 or 1");
+        g->fuse_min = value != 0;
+        break;
     default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
     }
     // options that change the plan need a fresh enumeration
     if ((opt == PASE_OPT_KEEP_TABLES || opt == PASE_OPT_KERNEL || opt == PASE_OPT_MEMORY_BUDGET ||
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
          opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER ||
-         opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US || opt == PASE_OPT_KEY_TYPE) &&
+         opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US || opt == PASE_OPT_KEY_TYPE ||
+         opt == PASE_OPT_FUSED_MIN) &&
         g->enumerated) {
         g->searched = false;
         const pase_status st = plan_search(g, true);
@@ -1312,6 +1356,7 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
         x.key_bound = x.table_bound = ~0ull;
     }
     x.key_type = g->plan_key_type;
+    x.fused = vp.fuse_into >= 0 ? 1u : vp.fused_from >= 0 ? 2u : 0u;
     *out = x;
     return PASE_OK;
 }

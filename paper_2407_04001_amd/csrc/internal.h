@@ -135,6 +135,18 @@ struct RowsArgs {
     uint32_t nblocks_launched;
     uint32_t parts;           // waves sharing one tile's c range: 1, 2 or 4
     uint32_t out_shift;       // bits of the table's reader: values are stored x 2^out_shift
+    // Fused minimum of the reader (fz_keys non-null): the table's only reader
+    // v_j is this vertex's column digit and takes, per row r, the minimum over
+    // its configuration c = z of T[z][r] plus its other row terms at (r, z)
+    // plus its column block at z.  The epilogue forms those keys of v_j for
+    // the tile's columns and min-combines them into fz_keys[r] atomically (64-bit
+    // keys, non-negative, so their bit patterns order like the keys); a
+    // one-split reduction then turns the keys into v_j's table.  T may then
+    // be null: nothing else reads it.
+    void *fz_keys;
+    const void *fz_B;         // the reader's column block, element z * fz_ldz
+    uint32_t fz_ldz, fz_na;   // its row pitch; the reader's row terms other than T
+    ATerm fz_a[kMaxATerms];   // those row terms (ptr, sc, sdR over the same row digits)
 };
 
 struct GTerm {                // term of the generic kernel (key space)
@@ -225,6 +237,11 @@ struct VPlan {
     uint32_t TZ = 0, TM = 1, ldz = 0, nchunks = 0, nsplit = 1, cper = 0, parts = 1;
     uint64_t MO = 1, MR = 1;
     uint32_t na = 0;                // row kernel: per-lane row terms
+    // fused minimum (row kernel): this vertex's table feeds only the minimum
+    // of its column digit's vertex, which its fill forms in the epilogue
+    int fuse_into = -1;             // position of that reader, -1 = none
+    int fused_from = -1;            // the reader: position of the producer, -1 = none
+    uint64_t fkeys_off = 0;         // the reader: bytes into the fused-key region
     double fill_ms = 0;             // last profiled fill time
     double est_us = 0;              // planned fill time (tile model), for the schedule
     // memory
@@ -248,8 +265,10 @@ struct Plan {
     uint64_t off_ex = 0, off_vert = 0, off_edge = 0, off_L = 0, off_lsum = 0, off_sig = 0,
              off_ovedge = 0, off_contrib = 0,
              off_bt = 0, off_zero = 0, off_cfg = 0, off_out = 0, off_vmat = 0, off_T = 0, off_A = 0, off_block = 0,
-             off_partial = 0, total = 0;
+             off_partial = 0, off_fused = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
+    uint64_t fused_bytes = 0;       // keys of the fused minima (initialised by k_cost_tables)
+    uint32_t fused = 0;             // fused producer/reader pairs
     uint64_t sig_count = 0;         // split signatures of all edge endpoints
     int nslots = 0;                 // launch slots (levels, or positions when sequential)
     bool by_level = false;          // the vertices of one dependency level share launches
@@ -288,6 +307,7 @@ struct pase_graph_s {
                                     // product of the input dims' sizes other than that dim
     uint64_t direct_cells = 1ull << 18;  // pase_option PASE_OPT_DIRECT_CELLS
     uint32_t bulk_us = 100;         // pase_option PASE_OPT_BULK_US
+    bool fuse_min = true;           // pase_option PASE_OPT_FUSED_MIN
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix

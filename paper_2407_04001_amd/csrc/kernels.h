@@ -560,10 +560,29 @@ __device__ __forceinline__ void rows_item(const RowsArgs &a, uint32_t b, MergeBu
 
     const uint64_t plane = (uint64_t)a.MO * a.MR;
     const uint32_t zbase = chunk * TZ;
+    // fused minimum of the reader v_j (c_j = z): per row, its keys over this
+    // tile's columns -- the stored value of T[z][r] (already in v_j's key
+    // space) plus v_j's other row terms at (r, z) and its column block at z
+    // -- reduced in the lane, then min-combined across tiles atomically
+    constexpr bool kFuse = sizeof(KeyT) == 8;
+    const bool fuse = kFuse && a.fz_keys != nullptr;
 #pragma unroll
     for (int m = 0; m < TM; m++) {
         if (!valid[m]) continue;
         const uint64_t base_idx = (uint64_t)o * a.MR + r[m];
+        uint32_t fzoff[kMaxATerms];
+        KeyT best = Ops::sentinel();
+        if (fuse) {
+            uint32_t x = r[m], dR[kMaxDep];
+            for (int k = kMaxDep - 1; k >= 0; k--)
+                if (k < (int)a.nR) { dR[k] = x % a.radR[k]; x /= a.radR[k]; } else dR[k] = 0;
+            for (int q = 0; q < kMaxATerms; q++) {
+                uint32_t off = 0;
+                if (q < (int)a.fz_na)
+                    for (int k = 0; k < kMaxDep; k++) off += dR[k] * a.fz_a[q].sdR[k];
+                fzoff[q] = off;
+            }
+        }
 #pragma unroll
         for (int t = 0; t < TZ; t++) {
             const uint32_t z = zbase + t;
@@ -575,10 +594,25 @@ __device__ __forceinline__ void rows_item(const RowsArgs &a, uint32_t b, MergeBu
                     Val v;
                     uint32_t cc;
                     Ops::split(acc[m][t], a.bits, a.out_shift, v, cc);
-                    ((Val *)a.T)[idx] = v;
+                    if (a.T) ((Val *)a.T)[idx] = v;
                     a.A[idx] = (uint16_t)cc;
+                    if constexpr (kFuse) {
+                        if (fuse) {
+                            KeyT k = __builtin_bit_cast(KeyT, v);
+                            for (int q = 0; q < kMaxATerms; q++)
+                                if (q < (int)a.fz_na)
+                                    k = Ops::add(k, ((const KeyT *)a.fz_a[q].ptr)[fzoff[q] + z * a.fz_a[q].sc]);
+                            k = Ops::add(k, ((const KeyT *)a.fz_B)[(uint64_t)z * a.fz_ldz]);
+                            best = Ops::min(best, k);
+                        }
+                    }
                 }
             }
+        }
+        if constexpr (kFuse) {
+            if (fuse)
+                atomicMin((unsigned long long *)a.fz_keys + r[m],
+                          (unsigned long long)__builtin_bit_cast(uint64_t, best));
         }
     }
 }

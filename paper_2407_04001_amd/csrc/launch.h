@@ -18,6 +18,7 @@ struct Launch {
     PrepArgs prep;
     bool rows = false;
     bool direct = false;
+    bool fused = false;    // a fused minimum: its fill is the one-split reduction `red`
     RowsArgs ra;
     GenericArgs ga;
     ReduceArgs red;

@@ -239,15 +239,23 @@ pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &
             if (nbk > 0x7fffffffull) return fail(g, PASE_ERR_TOO_LARGE, "grid too large");
             ra.nblocks_launched = (uint32_t)nbk;
             L.rows = true;
-            if (vp.nsplit > 1) {
+            if (vp.nsplit > 1 || vp.fused_from >= 0) {
                 L.red.nblk = grid_for(vp.N);
-                L.red.partial = ra.partial;
+                L.red.partial = vp.fused_from >= 0 ? (void *)(ws + P.off_fused + vp.fkeys_off) : ra.partial;
                 L.red.T = ra.T;
                 L.red.A = ra.A;
                 L.red.N = vp.N;
                 L.red.nsplit = vp.nsplit;
                 L.red.bits = vp.bits;
                 L.red.out_shift = vp.out_shift;
+            }
+            if (vp.fused_from >= 0) {
+                // the producer's epilogue forms this vertex's keys; its own fill
+                // is the reduction of those keys (its row descriptor stays for
+                // the producer to copy the row terms from)
+                L.rows = false;
+                L.fused = true;
+                if (vp.nsplit != 1) return fail(g, PASE_ERR_INTERNAL, "fused minimum split over c");
             }
         } else {
             GenericArgs &ga = L.ga;
@@ -304,6 +312,43 @@ pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &
             return fail(g, PASE_ERR_INTERNAL, "block scratch overflow");
     }
     if (contrib.size() > P.contrib_count) return fail(g, PASE_ERR_INTERNAL, "contribution overflow");
+    // fused minima: the producer's epilogue gets the reader's row terms other
+    // than the producer's own table, and its column block
+    for (int i1 = 0; i1 < n; i1++) {
+        const int i2 = P.v[i1].fuse_into;
+        if (i2 < 0) continue;
+        if constexpr (sizeof(KeyT) != 8) {
+            return fail(g, PASE_ERR_INTERNAL, "fused minimum with 128-bit keys");
+        } else {
+            const VPlan &a = P.v[i1], &b = P.v[i2];
+            RowsArgs &r1 = out[i1].ra;
+            const RowsArgs &r2 = out[i2].ra;
+            if (!out[i1].rows || !out[i2].fused || a.MO != 1 || a.R != b.R || b.fused_from != i1)
+                return fail(g, PASE_ERR_INTERNAL, "fused minimum plan");
+            const void *Tp = ws + P.off_T + a.T_off;
+            int own = 0;
+            r1.fz_na = 0;
+            for (uint32_t t = 0; t < r2.na; t++) {
+                if (r2.a[t].ptr == Tp) {
+                    // the reader's lookup of T_i1 must address it as the producer
+                    // writes it: [z][r], z stride MR, row strides those of T_i1
+                    bool same = r2.a[t].sc == a.MR;
+                    for (size_t k = 0; k < a.R.size(); k++) same &= r2.a[t].sdR[k] == a.stride[1 + k];
+                    if (!same) return fail(g, PASE_ERR_INTERNAL, "fused minimum lookup layout");
+                    own++;
+                    continue;
+                }
+                r1.fz_a[r1.fz_na++] = r2.a[t];
+            }
+            if (own != 1) return fail(g, PASE_ERR_INTERNAL, "fused minimum lookup");
+            r1.fz_keys = ws + P.off_fused + b.fkeys_off;
+            r1.fz_B = r2.B;
+            r1.fz_ldz = r2.ldz;
+            if (r1.Kz != b.K || r2.MR != a.MR) return fail(g, PASE_ERR_INTERNAL, "fused minimum shape");
+            // nothing else reads T_i1 unless the tables are kept for queries
+            if (!g->keep_tables) r1.T = nullptr;
+        }
+    }
     return PASE_OK;
 }
 
@@ -497,7 +542,13 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         cur_group = (int)sl;
         prepped.clear();
         direct.clear();
-        for (int i : mem) (launches[i].direct ? direct : prepped).push_back(i);
+        // a fused minimum's blocks are built with its producer's, before the
+        // producer's fill reads them; its own fill is a reduction (below)
+        for (int i : mem) {
+            if (launches[i].direct) direct.push_back(i);
+            else if (!launches[i].fused) prepped.push_back(i);
+            if (P.v[i].fuse_into >= 0) prepped.push_back(P.v[i].fuse_into);
+        }
         add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
         add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
         rows.clear();
@@ -509,13 +560,14 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         // zero key once per c) and joins that vertex's launch
         shape_dom.clear();
         for (int i : prepped)
-            if (launches[i].rows && kF64) {
+            if (launches[i].rows && !launches[i].fused && kF64) {
                 auto it = shape_dom.find(P.v[i].TZ * 4 + P.v[i].TM);
                 if (it == shape_dom.end()) shape_dom[P.v[i].TZ * 4 + P.v[i].TM] = i;
                 else if (P.v[i].est_us > P.v[it->second].est_us) it->second = i;
             }
         for (int i : prepped) {
             const Launch<KeyT> &L = launches[i];
+            if (L.fused) continue;
             if (L.rows) {
                 uint32_t na = kF64 ? std::min<uint32_t>(L.ra.na, 4) : 7;
                 if (kF64) {
@@ -556,6 +608,8 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
             add_batch(Batch::kGeneric, gens[k].first, grp, [](const Launch<KeyT> &L) { return L.ga.nblk; });
             k = k2;
         }
+        for (int i : mem)
+            if (launches[i].fused) reds.push_back({0, i});
         grp.clear();
         for (auto &x : reds) grp.push_back(x.second);
         add_batch(Batch::kReduce, 0, grp, [](const Launch<KeyT> &L) { return L.red.nblk; });
@@ -585,13 +639,29 @@ pase_status plan_check(pase_graph_t g, uint64_t *image_bytes) {
     // every vertex appears in exactly one fill batch (direct, row or generic)
     std::vector<int> fills(g->plan.v.size(), 0);
     const BatchEntry *be = (const BatchEntry *)(img.data() + g->plan.off_batch);
-    for (const Batch &b : si.batches)
-        if (b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect)
-            for (uint32_t k = 0; k < b.nentries; k++) {
-                const uint32_t pos = be[b.entry0 + k].pos;
-                if (pos >= fills.size()) return fail(g, PASE_ERR_INTERNAL, "batch entry out of range");
+    std::vector<int> prep_batch(g->plan.v.size(), -1), fill_batch(g->plan.v.size(), -1);
+    for (size_t bi = 0; bi < si.batches.size(); bi++) {
+        const Batch &b = si.batches[bi];
+        for (uint32_t k = 0; k < b.nentries; k++) {
+            const uint32_t pos = be[b.entry0 + k].pos;
+            if (pos >= fills.size()) return fail(g, PASE_ERR_INTERNAL, "batch entry out of range");
+            const bool fused = g->plan.v[pos].fused_from >= 0;
+            if (b.kind == Batch::kRows || b.kind == Batch::kGeneric || b.kind == Batch::kDirect ||
+                (b.kind == Batch::kReduce && fused)) {
                 fills[pos]++;
+                fill_batch[pos] = (int)bi;
             }
+            if (b.kind == Batch::kPrep) prep_batch[pos] = (int)bi;
+        }
+    }
+    // a fused minimum: its blocks are built before its producer's fill, and its
+    // reduction comes after that fill
+    for (size_t i = 0; i < g->plan.v.size(); i++) {
+        const int j = g->plan.v[i].fused_from;
+        if (j < 0) continue;
+        if (prep_batch[i] < 0 || fill_batch[j] < 0 || prep_batch[i] > fill_batch[j] || fill_batch[i] < fill_batch[j])
+            return fail(g, PASE_ERR_INTERNAL, "fused minimum out of order");
+    }
     for (int f : fills)
         if (f != 1) return fail(g, PASE_ERR_INTERNAL, "a vertex is not filled exactly once");
     *image_bytes = bytes;

@@ -70,7 +70,7 @@ def _compare_all_entries(pg, o, g, max_entries=2048):
 
 def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=0, tile=(0, 0),
          parts=0, splits=0, all_integers=False, bf=False, volume=False, grad=False,
-         direct=0, bulk_us=None, halo=False):
+         direct=0, bulk_us=None, halo=False, fuse=None):
     """direct: PASE_OPT_DIRECT_CELLS (0 = off, so the tests aimed at the row and
     generic kernels keep them; None = the library's default)."""
     pg = P.Graph(g, seq_rule=rule)
@@ -91,6 +91,8 @@ def _run(P, g, p=None, keep=True, kernel=0, key=0, costs=None, rule=0, schedule=
     pg.set_option(P.OPT_C_SPLITS, splits)
     if bulk_us is not None:
         pg.set_option(P.OPT_BULK_US, bulk_us)
+    if fuse is not None:
+        pg.set_option(P.OPT_FUSED_MIN, int(fuse))
     if costs is not None:
         pg.override_costs(*costs)
     mc, strat = pg.find_best_strategy()
@@ -665,6 +667,52 @@ def test_volume_model_transformer_against_golden(P):
     configuration and with every table kept and fingerprinted."""
     _check_golden(P, "w4_transformer", 0, volume=True, keep=False)
     _check_golden(P, "w4_transformer", 0, volume=True, keep=True)
+
+
+# ------------------------------------------------------------------ fused minimum (PASE_OPT_FUSED_MIN)
+def _fused_graph():
+    """A Transformer with one encoder and two decoder layers at p = 16 (4.1e8
+    cells): its last cross-attention key/value projection takes a minimum
+    over the whole table of its predecessor, which the plan fuses."""
+    from workloads import transformer
+    return transformer(p=16, enc_layers=1, dec_layers=2)
+
+
+@pytest.mark.parametrize("schedule,key", [(0, 0), (1, 0), (4, 0), (0, 1)])
+def test_fused_minimum_every_entry(P, schedule, key):
+    """The fused producer/reader pair against the oracle entry by entry (every
+    table, with tables kept so the producer also writes its own), under each
+    schedule and both 64-bit key types; and the same search with fusion off."""
+    g = _fused_graph()
+    say(f"fused minimum schedule={schedule} key={key}")
+    o = _oracle(g)
+    pg, mc, strat = _run(P, g, schedule=schedule, key=key, direct=None, bulk_us=5)
+    fused = [v for v in range(pg.nv) if pg.vertex_info(v)["fused"]]
+    assert len(fused) == 2, fused
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=4096)
+    pg2, mc2, strat2 = _run(P, g, schedule=schedule, key=key, direct=None, bulk_us=5, fuse=False)
+    assert not any(pg2.vertex_info(v)["fused"] for v in range(pg2.nv))
+    assert (mc2, strat2) == (mc, strat)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_fused_minimum_random_costs(P, seed):
+    """Caller-given costs in [0, 4) on the fused graph (dense ties: the atomic
+    minimum must still keep the lowest configuration), tables kept and not."""
+    g = _fused_graph()
+    say(f"fused minimum random costs seed={seed}")
+    o0 = _oracle(g)
+    K = [int(k) for k in o0.K]
+    shapes = [(K[e["src"]], K[e["dst"]]) for e in g["edges"]]
+    costs = random_costs(seed + 900, K, shapes, hi=4)
+    o = _oracle(g, costs=costs)
+    pg, mc, strat = _run(P, g, costs=costs, direct=None)
+    assert any(pg.vertex_info(v)["fused"] == 2 for v in range(pg.nv))
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=4096)
+    pg2, mc2, strat2 = _run(P, g, costs=costs, keep=False, direct=None)
+    assert (mc2, strat2) == o.result()
 
 
 # ------------------------------------------------------------------ device assignment of the found strategy

@@ -579,3 +579,33 @@ def test_assign_devices_errors(pase):
     assert P.load().pase_assign_devices(pg.h, None, None, None, None) == P.INVALID_ARGUMENT
     pg.enumerate_configs(2048)
     assert _status(lambda: pg.assign_devices([0] * pg.nv)) == P.TOO_LARGE
+
+
+def test_fused_minimum_plan(pase):
+    """PASE_OPT_FUSED_MIN: on the measured Transformer the plan fuses the
+    minimum of the last cross-attention key/value projection into its
+    predecessor's fill (producer flagged 1, reader 2, adjacent in the order,
+    the producer's column digit being the reader); the option validates,
+    turns it off and on, and the launch plan checks in every schedule."""
+    P = pase
+    g = workload("w4_transformer")
+    pg = P.Graph(g)
+    assert _status(lambda: pg.set_option(P.OPT_FUSED_MIN, 2)) == P.INVALID_ARGUMENT
+    pg.enumerate_configs(g["p"])
+    info = {v: pg.vertex_info(v) for v in range(pg.nv)}
+    prod = [v for v in info if info[v]["fused"] == 1]
+    read = [v for v in info if info[v]["fused"] == 2]
+    assert len(prod) == 1 and len(read) == 1
+    a, b = info[prod[0]], info[read[0]]
+    assert b["position"] == a["position"] + 1 and a["column"] == read[0] and b["column"] == -1
+    assert a["splits"] == 1 and b["splits"] == 1 and a["outer"] == 1 and a["rows"] == b["rows"]
+    for sched in (0, 1, 4):
+        for keep in (0, 1):
+            pg.set_option(P.OPT_SCHEDULE, sched)
+            pg.set_option(P.OPT_KEEP_TABLES, keep)
+            assert pg.plan_check() > 0
+    pg.set_option(P.OPT_FUSED_MIN, 0)
+    assert not any(pg.vertex_info(v)["fused"] for v in range(pg.nv))
+    assert pg.plan_check() > 0
+    pg.set_option(P.OPT_FUSED_MIN, 1)
+    assert sum(pg.vertex_info(v)["fused"] for v in range(pg.nv)) == 3
