@@ -193,6 +193,14 @@ typedef enum {
                                    strict "<" tie-break is unchanged: keys are distinct per c),
                                    so the predecessor's table is never written to HBM and read
                                    back; 0: every vertex fills on its own.  Re-plans */
+    PASE_OPT_HOIST_ELEMS = 21,  /* one-stream level layout (the level schedule, or the bulk lane
+                                   schedule over its memory budget): a vertex whose prep blocks
+                                   hold at least this many elements (default 2^20) and read only
+                                   tables filled two or more slots before its own has its prep
+                                   built on a second stream right after the last of them, while
+                                   the slots in between run; its blocks get memory of their own.
+                                   0: never.  The allocation-free entry point builds every prep
+                                   in its own slot.  Re-plans */
     PASE_OPT_HALO = 19          /* 1: the next pase_enumerate_configs adds the halo exchange of
                                    convolutions to every layer cost (an assumed form; the paper
                                    counts halo communication in t_l but prints no formula): for
@@ -383,6 +391,10 @@ typedef struct {
     uint32_t key_type;    /* key type of the plan (the same for every vertex): 0 fp64, 1 uint64, 2 128-bit */
     uint32_t fused;       /* PASE_OPT_FUSED_MIN: 1 = its fill also forms the minimum of its table's reader,
                              2 = that reader (its fill is then a one-split reduction of those keys), 0 = neither */
+    int32_t prep_after;   /* level layout: its prep blocks read only tables of slots up to this one (-1:
+                             none) and are built on a side stream right after it, beside the launches of
+                             the slots in between; -2 = built in its own slot */
+    uint32_t pad;
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

@@ -383,8 +383,10 @@ struct DeviceState {
     hipEvent_t phase_ev[4] = {};       // profiling: search phases (cost tables | fill | back-substitution)
     hipStream_t last_stream = nullptr;
     char *last_ws = nullptr;           // workspace of the last search (its tables are read there)
-    hipStream_t side = nullptr;        // bulk lane schedule: the bulk stream (default priority)
+    hipStream_t side = nullptr;        // bulk lane schedule: the bulk stream; level layout: hoisted
+                                       // preps (default priority)
     std::vector<hipEvent_t> lane_ev;   // bulk lane schedule: joins (no timing)
+    std::vector<hipEvent_t> hoist_ev;  // hoisted preps: per side batch, its start and its end (no timing)
 };
 
 #define HIPCHK(x)                                                                              \
@@ -401,6 +403,7 @@ void device_release(pase_graph_t g) {
     if (d->pinned) (void)hipHostFree(d->pinned);
     for (auto e : d->ev) (void)hipEventDestroy(e);
     for (auto e : d->lane_ev) (void)hipEventDestroy(e);
+    for (auto e : d->hoist_ev) (void)hipEventDestroy(e);
     for (auto e : d->phase_ev)
         if (e) (void)hipEventDestroy(e);
     if (d->side) (void)hipStreamDestroy(d->side);
@@ -625,10 +628,46 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         HIPCHK(hipEventRecord(d->lane_ev[0], s));
         HIPCHK(hipStreamWaitEvent(lane_stream[1], d->lane_ev[0], 0));
     }
+    // hoisted preps: a side batch starts after everything enqueued on s before
+    // it (the fills of the tables it reads) and its vertex's group waits for it
+    std::vector<int> side_of(batches.size(), -1);
+    if (si.hoist) {
+        if (!d->side) HIPCHK(hipStreamCreateWithFlags(&d->side, hipStreamNonBlocking));
+        size_t nside = 0;
+        for (const Batch &b : batches) nside += b.side;
+        while (d->hoist_ev.size() < 2 * nside) {
+            hipEvent_t e;
+            HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+            d->hoist_ev.push_back(e);
+        }
+    }
+    int nside_done = 0, waits_group = -1;
     int prev_group = -1;
-    for (const Batch &b : batches) {
+    for (size_t bi = 0; bi < batches.size(); bi++) {
+        const Batch &b = batches[bi];
         const BatchEntry *e = dbe + b.entry0;
         hipStream_t bs = s;
+        if (si.hoist) {
+            if (b.side) {
+                hipEvent_t e0 = d->hoist_ev[2 * nside_done], e1 = d->hoist_ev[2 * nside_done + 1];
+                HIPCHK(hipEventRecord(e0, s));
+                HIPCHK(hipStreamWaitEvent(d->side, e0, 0));
+                hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, d->side, dp, e, b.nentries,
+                                   dV, dE, (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r);
+                HIPCHK(hipEventRecord(e1, d->side));
+                side_of[bi] = nside_done++;
+                launches_n++;
+                continue;
+            }
+            if (b.group != waits_group) {
+                for (int sb : si.group_waits[(size_t)b.group]) {
+                    if (sb < 0 || (size_t)sb >= bi || side_of[sb] < 0)
+                        return fail(g, PASE_ERR_INTERNAL, "wait on a hoisted prep not enqueued yet");
+                    HIPCHK(hipStreamWaitEvent(s, d->hoist_ev[2 * side_of[sb] + 1], 0));
+                }
+                waits_group = b.group;
+            }
+        }
         if (si.lanes) {
             if (b.group != prev_group) {
                 if (prev_group >= 0)

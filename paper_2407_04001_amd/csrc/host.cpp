@@ -410,6 +410,44 @@ static void fuse_minima(pase_graph_t g, Plan &P) {
     }
 }
 
+// Hoisted preps (level layout: one stream, slots = levels).  A vertex's prep builds its key-space blocks
+// from static costs and from the tables of the lookups that enter blocks (the
+// column block's and the one-digit row blocks'; multi-digit lookups on row
+// digits are read by the fill itself).  When the last of those tables is
+// filled two or more slots before the vertex's own, and the blocks are large
+// (PASE_OPT_HOIST_ELEMS, by default 2^20 elements: ~10 us or more of HBM
+// writes), the prep runs on a side
+// stream right after that slot -- beside the chains of small launches that
+// follow, which leave most of the GPU idle -- instead of in the vertex's slot.
+static void hoist_preps(pase_graph_t g, Plan &P) {
+    for (auto &vp : P.v) {
+        if ((vp.kernel != kRows && vp.kernel != kGeneric) || vp.fused_from >= 0 || vp.fuse_into >= 0) continue;
+        uint64_t elems = 0;
+        int ready = -1;
+        if (vp.kernel == kRows) {
+            elems = vp.MO * vp.K * vp.ldz;
+            for (int u : vp.R) elems += (uint64_t)vp.K * g->K[u];
+            std::vector<int> OZ = vp.O;
+            if (vp.z >= 0) OZ.push_back(vp.z);
+            for (const auto &t : vp.terms) {
+                bool all = true;
+                for (int u : t.dig) all &= std::find(OZ.begin(), OZ.end(), u) != OZ.end();
+                const bool row1 = t.dig.size() == 1 && std::count(vp.R.begin(), vp.R.end(), t.dig[0]);
+                if (all || row1) ready = std::max(ready, P.v[t.j].slot);
+            }
+        } else {
+            elems = vp.K;
+            for (int u : vp.D) elems += (uint64_t)vp.K * g->K[u];
+            for (const auto &t : vp.terms)
+                if (t.dig.size() <= 1) ready = std::max(ready, P.v[t.j].slot);
+        }
+        if (g->hoist_elems && elems >= g->hoist_elems && ready + 2 <= vp.slot) {
+            vp.prep_after = ready;
+            P.hoisted++;
+        }
+    }
+}
+
 // Bulk lane schedule.  Row-kernel vertices planned to take at least bulk_us
 // (the large fills, which keep the whole GPU busy on their own) run on lane 1
 // (a stream of its own), and so does every vertex that reads a table of lane 1
@@ -755,7 +793,10 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     for (auto &vp : P.v) {
         vp.slot = by_level ? vp.level : (int)(&vp - &P.v[0]);
         P.nslots = std::max(P.nslots, vp.slot + 1);
+        vp.prep_after = -2;
     }
+    P.hoisted = 0;
+    if (mode == kLayoutLevel) hoist_preps(g, P);
     const int n = (int)P.v.size();
     const uint64_t A = 256;
     uint64_t off = 0;
@@ -845,6 +886,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
     // block and split scratch: vertices of one slot get disjoint pieces; slots reuse it
     std::vector<uint64_t> bsum(P.nslots, 0), psum(P.nslots, 0);
     uint64_t bmax = 0, pmax = 0;
+    std::vector<VPlan *> hoisted;
     for (auto &vp : P.v) {
         uint64_t e = 0, pb = 0;
         if (vp.kernel == kRows) {
@@ -859,12 +901,21 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
         // (the resident layout keeps every vertex's scratch: one slot for all;
         // a fused minimum's blocks are built and read in its producer's slot)
         const int sl = resident ? 0 : vp.fused_from >= 0 ? P.v[vp.fused_from].slot : vp.slot;
-        vp.block_off = bsum[sl];
         vp.partial_off = psum[sl];
-        bsum[sl] += align_up(e * kb, A);
         psum[sl] += pb;
-        bmax = std::max(bmax, bsum[sl]);
         pmax = std::max(pmax, psum[sl]);
+        if (vp.prep_after >= -1) {   // hoisted: blocks live from an earlier slot on
+            hoisted.push_back(&vp);
+            continue;
+        }
+        vp.block_off = bsum[sl];
+        bsum[sl] += align_up(e * kb, A);
+        bmax = std::max(bmax, bsum[sl]);
+    }
+    // hoisted blocks: after every slot's scratch, one piece each
+    for (VPlan *vp : hoisted) {
+        vp->block_off = bmax;
+        bmax += align_up(vp->block_elems * kb, A);
     }
     P.block_bytes = bmax;
     P.off_block = off;
@@ -1167,6 +1218,9 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         if (value > 1) return fail(g, PASE_ERR_INVALID_ARGUMENT, "fused minimum 0 or 1");
         g->fuse_min = value != 0;
         break;
+    case PASE_OPT_HOIST_ELEMS:
+        g->hoist_elems = value;
+        break;
     default: return fail(g, PASE_ERR_INVALID_ARGUMENT, "unknown option");
     }
     // options that change the plan need a fresh enumeration
@@ -1174,7 +1228,7 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
          opt == PASE_OPT_SCHEDULE || opt == PASE_OPT_TILE_COLS || opt == PASE_OPT_TILE_ROWS ||
          opt == PASE_OPT_TILE_PARTS || opt == PASE_OPT_C_SPLITS || opt == PASE_OPT_ORDER ||
          opt == PASE_OPT_DIRECT_CELLS || opt == PASE_OPT_BULK_US || opt == PASE_OPT_KEY_TYPE ||
-         opt == PASE_OPT_FUSED_MIN) &&
+         opt == PASE_OPT_FUSED_MIN || opt == PASE_OPT_HOIST_ELEMS) &&
         g->enumerated) {
         g->searched = false;
         const pase_status st = plan_search(g, true);
@@ -1357,6 +1411,7 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     }
     x.key_type = g->plan_key_type;
     x.fused = vp.fuse_into >= 0 ? 1u : vp.fused_from >= 0 ? 2u : 0u;
+    x.prep_after = vp.prep_after;
     *out = x;
     return PASE_OK;
 }

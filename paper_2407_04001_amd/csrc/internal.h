@@ -242,6 +242,10 @@ struct VPlan {
     int fuse_into = -1;             // position of that reader, -1 = none
     int fused_from = -1;            // the reader: position of the producer, -1 = none
     uint64_t fkeys_off = 0;         // the reader: bytes into the fused-key region
+    // hoisted prep (level schedule): the blocks read only tables filled by
+    // slot prep_after or earlier, so they are built on a side stream right
+    // after that slot, beside the slots in between; -2 = not hoisted
+    int prep_after = -2;
     double fill_ms = 0;             // last profiled fill time
     double est_us = 0;              // planned fill time (tile model), for the schedule
     // memory
@@ -268,6 +272,7 @@ struct Plan {
              off_partial = 0, off_fused = 0, total = 0;
     uint64_t T_bytes = 0, A_bytes = 0, block_bytes = 0, partial_bytes = 0, contrib_count = 0;
     uint64_t fused_bytes = 0;       // keys of the fused minima (initialised by k_cost_tables)
+    uint32_t hoisted = 0;           // vertices whose prep runs on the side stream
     uint32_t fused = 0;             // fused producer/reader pairs
     uint64_t sig_count = 0;         // split signatures of all edge endpoints
     int nslots = 0;                 // launch slots (levels, or positions when sequential)
@@ -308,6 +313,7 @@ struct pase_graph_s {
     uint64_t direct_cells = 1ull << 18;  // pase_option PASE_OPT_DIRECT_CELLS
     uint32_t bulk_us = 100;         // pase_option PASE_OPT_BULK_US
     bool fuse_min = true;           // pase_option PASE_OPT_FUSED_MIN
+    uint64_t hoist_elems = 1ull << 20;   // pase_option PASE_OPT_HOIST_ELEMS (0 = never)
     std::vector<uint64_t> weight_n; // gradient term of the enumeration: weight words per vertex (0 = none)
     bool volume = false;            // the enumerated transfer model is the volume intersection
     std::vector<uint64_t> mat_off;  // volume model: element offset of each edge's cost matrix

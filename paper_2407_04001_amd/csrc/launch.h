@@ -35,6 +35,7 @@ struct Batch {
     uint32_t entry0;       // first BatchEntry of this batch
     uint32_t nentries;
     uint32_t blocks;       // workgroups of the launch
+    bool side = false;     // a hoisted prep launch: on the side stream, after the work enqueued before it
 };
 
 constexpr int kLanes = 2;   // streams of the bulk lane schedule
@@ -44,6 +45,8 @@ struct SearchImage {
     std::vector<std::vector<int>> groups;  // positions of each launch group
     std::vector<int> group_lane;           // lane of each launch group
     bool lanes = false;                    // the bulk lane schedule runs (two streams)
+    bool hoist = false;                    // hoisted preps run on a side stream (level layout)
+    std::vector<std::vector<int>> group_waits;   // per launch group: the side batches it waits for
     bool upload_costs = true;              // the device cost tables' range is part of the upload
     uint32_t nlev = 0;                     // backward levels of the back-substitution
     uint64_t nL = 0;                       // layer costs of all vertices (sum of K)
@@ -57,9 +60,11 @@ pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &
 // The constant-region image [0, plan.off_cfg) of one search into `img` (host
 // memory of at least plan.off_cfg bytes) and its batches, for a workspace at
 // device address `ws`.  Every write into `img` is checked against the plan's
-// region bounds before it is made.  allow_lanes = false runs a bulk lane plan
-// level by level on one stream (its resident layout serves that order too).
+// region bounds before it is made.  allow_streams = false runs everything on
+// one stream: a bulk lane plan level by level (its resident layout serves that
+// order too), hoisted preps in their own slot (their blocks have memory of
+// their own either way).
 template <typename KeyT>
-pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_lanes = true);
+pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_streams = true);
 
 }  // namespace pase

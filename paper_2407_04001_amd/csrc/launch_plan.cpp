@@ -363,7 +363,7 @@ template pase_status build_launches<unsigned __int128>(pase_graph_t, char *,
 
 // ------------------------------------------------------------------ constant image and batches
 template <typename KeyT>
-pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_lanes) {
+pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bool allow_streams) {
     const Plan &P = g->plan;
     const int n = (int)P.v.size();
     const size_t nv = g->V.size(), ne = g->E.size();
@@ -372,7 +372,8 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
     pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
     if (st != PASE_OK) return st;
     si = SearchImage();
-    si.lanes = allow_lanes && P.resident && g->schedule == kSchedBulk;
+    si.lanes = allow_streams && P.resident && g->schedule == kSchedBulk;
+    si.hoist = allow_streams && !si.lanes && P.hoisted > 0;
     // every piece of the image is checked against the end of its region first
     auto region = [&](uint64_t off, uint64_t bytes, uint64_t end, const char *what) {
         return off + bytes <= end && end <= P.off_cfg ? PASE_OK
@@ -518,7 +519,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
     auto add_batch = [&](Batch::Kind kind, uint32_t variant, const std::vector<int> &members,
                          uint32_t (*nblk)(const Launch<KeyT> &)) {
         if (members.empty()) return;
-        Batch b{kind, cur_lane, cur_group, variant, nbe, 0, 0};
+        Batch b{kind, cur_lane, cur_group, variant, nbe, 0, 0, false};
         for (int i : members) {
             if (nbe >= be_cap) { be_overflow = true; return; }
             hbe[nbe].pos = (uint32_t)i;
@@ -536,6 +537,22 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
     std::vector<std::pair<uint32_t, int>> rows, gens, reds;
     std::map<uint32_t, int> shape_dom;   // TZ * 4 + TM -> largest vertex of the group
     constexpr bool kF64 = std::is_same<KeyT, double>::value;
+    // hoisted preps: a side batch after the group of the slot whose tables
+    // they read last (before group 0 when they read none); each vertex's group
+    // waits for its side batch
+    std::vector<std::vector<int>> hoist_after(si.groups.size() + 1);   // [slot + 1] -> positions
+    si.group_waits.assign(si.groups.size(), {});
+    if (si.hoist)
+        for (int i = 0; i < n; i++)
+            if (P.v[i].prep_after >= -1) hoist_after[(size_t)(P.v[i].prep_after + 1)].push_back(i);
+    auto add_side = [&](size_t k) {
+        if (hoist_after[k].empty()) return;
+        const int bi = (int)si.batches.size();
+        add_batch(Batch::kPrep, 0, hoist_after[k], [](const Launch<KeyT> &L) { return L.prep.nwg; });
+        if ((int)si.batches.size() == bi + 1) si.batches.back().side = true;
+        for (int i : hoist_after[k]) si.group_waits[(size_t)P.v[i].slot].push_back(bi);
+    };
+    add_side(0);
     for (size_t sl = 0; sl < si.groups.size(); sl++) {
         const auto &mem = si.groups[sl];
         cur_lane = si.group_lane[sl];
@@ -544,13 +561,15 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         direct.clear();
         // a fused minimum's blocks are built with its producer's, before the
         // producer's fill reads them; its own fill is a reduction (below)
+        std::vector<int> fills;   // members with a prep here or hoisted: rows / generic fills
         for (int i : mem) {
             if (launches[i].direct) direct.push_back(i);
-            else if (!launches[i].fused) prepped.push_back(i);
+            else if (!launches[i].fused) (si.hoist && P.v[i].prep_after >= -1 ? fills : prepped).push_back(i);
             if (P.v[i].fuse_into >= 0) prepped.push_back(P.v[i].fuse_into);
         }
         add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
         add_batch(Batch::kPrep, 0, prepped, [](const Launch<KeyT> &L) { return L.prep.nwg; });
+        prepped.insert(prepped.end(), fills.begin(), fills.end());
         rows.clear();
         gens.clear();
         reds.clear();
@@ -614,6 +633,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         for (auto &x : reds) grp.push_back(x.second);
         add_batch(Batch::kReduce, 0, grp, [](const Launch<KeyT> &L) { return L.red.nblk; });
         if (be_overflow) return fail(g, PASE_ERR_INTERNAL, "batch table overflow");
+        add_side(sl + 1);
     }
     for (const Batch &b : si.batches)
         if (b.blocks == 0 || b.blocks > 0x7fffffffu) return fail(g, PASE_ERR_TOO_LARGE, "launch grid size");
@@ -652,6 +672,27 @@ pase_status plan_check(pase_graph_t g, uint64_t *image_bytes) {
                 fill_batch[pos] = (int)bi;
             }
             if (b.kind == Batch::kPrep) prep_batch[pos] = (int)bi;
+        }
+    }
+    // every vertex with blocks has them built before its fill; a hoisted
+    // prep's side batch comes after the fills of the slot it waits for and is
+    // waited for by the vertex's group
+    for (size_t i = 0; i < g->plan.v.size(); i++) {
+        const VPlan &vp = g->plan.v[i];
+        if (vp.kernel == kDirect || vp.fused_from >= 0) continue;
+        if (prep_batch[i] < 0 || prep_batch[i] > fill_batch[i])
+            return fail(g, PASE_ERR_INTERNAL, "a prep does not precede its fill");
+        if (si.hoist && vp.prep_after >= -1) {
+            const Batch &b = si.batches[prep_batch[i]];
+            const auto &w = si.group_waits[(size_t)vp.slot];
+            if (!b.side || std::find(w.begin(), w.end(), prep_batch[i]) == w.end())
+                return fail(g, PASE_ERR_INTERNAL, "a hoisted prep is not waited for");
+            for (size_t k = 0; k < (size_t)prep_batch[i]; k++)
+                if (si.batches[k].group > vp.prep_after && !si.batches[k].side)
+                    return fail(g, PASE_ERR_INTERNAL, "a hoisted prep runs after a later slot");
+            for (size_t k = prep_batch[i] + 1; k < si.batches.size(); k++)
+                if (si.batches[k].group <= vp.prep_after && !si.batches[k].side)
+                    return fail(g, PASE_ERR_INTERNAL, "a hoisted prep runs before the tables it reads");
         }
     }
     // a fused minimum: its blocks are built before its producer's fill, and its

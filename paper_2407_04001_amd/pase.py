@@ -24,6 +24,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STAT
 (OPT_CONFIG_SET, OPT_ORDER, OPT_TRANSFER, OPT_GRAD_SYNC, OPT_DIRECT_CELLS, OPT_BULK_US) = range(12, 18)
 OPT_HALO = 19
 OPT_FUSED_MIN = 20
+OPT_HOIST_ELEMS = 21
 SCHEDULE_LEVEL, SCHEDULE_SEQUENTIAL, SCHEDULE_BULK = 0, 1, 4
 
 
@@ -66,7 +67,7 @@ class VertexInfo(C.Structure):
                 ("row_terms", C.c_uint32), ("lookups", C.c_uint32), ("parts", C.c_uint32),
                 ("fill_ms", C.c_double), ("level", C.c_uint32), ("lane", C.c_uint32),
                 ("key_bound", C.c_uint64), ("table_bound", C.c_uint64), ("key_type", C.c_uint32),
-                ("fused", C.c_uint32)]
+                ("fused", C.c_uint32), ("prep_after", C.c_int32), ("pad", C.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

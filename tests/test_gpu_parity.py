@@ -696,6 +696,29 @@ def test_fused_minimum_every_entry(P, schedule, key):
     assert (mc2, strat2) == (mc, strat)
 
 
+@pytest.mark.parametrize("key", [0, 1])
+def test_hoisted_preps_every_entry(P, key):
+    """Every eligible prep hoisted to the side stream (PASE_OPT_HOIST_ELEMS =
+    1) on the fused graph: every table against the oracle, and the same
+    result with hoisting off."""
+    g = _fused_graph()
+    say(f"hoisted preps key={key}")
+    o = _oracle(g)
+    pg = P.Graph(g)
+    pg.set_option(P.OPT_HOIST_ELEMS, 1)
+    pg.set_option(P.OPT_KEY_TYPE, key)
+    pg.enumerate_configs(16)
+    pg.set_option(P.OPT_KEEP_TABLES, 1)
+    hoisted = [v for v in range(pg.nv) if pg.vertex_info(v)["prep_after"] >= -1]
+    assert hoisted
+    mc, strat = pg.find_best_strategy()
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=4096)
+    pg.set_option(P.OPT_HOIST_ELEMS, 0)
+    assert not any(pg.vertex_info(v)["prep_after"] >= -1 for v in range(pg.nv))
+    assert pg.find_best_strategy() == (mc, strat)
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_fused_minimum_random_costs(P, seed):
     """Caller-given costs in [0, 4) on the fused graph (dense ties: the atomic

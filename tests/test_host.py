@@ -609,3 +609,28 @@ def test_fused_minimum_plan(pase):
     assert pg.plan_check() > 0
     pg.set_option(P.OPT_FUSED_MIN, 1)
     assert sum(pg.vertex_info(v)["fused"] for v in range(pg.nv)) == 3
+
+
+def test_hoisted_prep_plan(pase):
+    """PASE_OPT_HOIST_ELEMS: on the measured Transformer the one large prep
+    whose blocks read only an early table (the fourth decoder layer's
+    cross-attention key/value projection, level 43, reading level-1 tables)
+    is hoisted to run after slot 1; 0 hoists nothing; the sequential schedule
+    never hoists; the launch plan checks either way."""
+    P = pase
+    g = workload("w4_transformer")
+    pg = P.Graph(g)
+    pg.enumerate_configs(g["p"])
+    h = {v: pg.vertex_info(v) for v in range(pg.nv) if pg.vertex_info(v)["prep_after"] >= -1}
+    assert len(h) == 1
+    (v, info), = h.items()
+    assert g["vertices"][v]["name"] == "dec4_xkv" and info["prep_after"] == 1 and info["level"] == 43
+    assert pg.plan_check() > 0
+    pg.set_option(P.OPT_HOIST_ELEMS, 0)
+    assert all(pg.vertex_info(v)["prep_after"] == -2 for v in range(pg.nv))
+    pg.set_option(P.OPT_HOIST_ELEMS, 1)
+    assert sum(pg.vertex_info(v)["prep_after"] >= -1 for v in range(pg.nv)) >= 1
+    assert pg.plan_check() > 0
+    pg.set_option(P.OPT_SCHEDULE, 1)
+    assert all(pg.vertex_info(v)["prep_after"] == -2 for v in range(pg.nv))
+    assert pg.plan_check() > 0

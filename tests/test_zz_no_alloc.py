@@ -45,16 +45,19 @@ def _tables(P, pg, g):
     return out
 
 
-def _both(P, g, p, schedule=0, direct=None):
+def _both(P, g, p, schedule=0, direct=None, options=()):
     """The same graph through both entry points (two handles); returns
     (result, tables, handle) of each.  direct: PASE_OPT_DIRECT_CELLS (0 keeps
-    small vertices on the prep + row / generic kernels and their scratch)."""
+    small vertices on the prep + row / generic kernels and their scratch);
+    options: further (option, value) pairs."""
     res = []
     for noalloc in (False, True):
         pg = P.Graph(g)
         pg.set_option(P.OPT_SCHEDULE, schedule)
         if direct is not None:
             pg.set_option(P.OPT_DIRECT_CELLS, direct)
+        for opt, val in options:
+            pg.set_option(opt, val)
         pg.enumerate_configs(p)
         pg.set_option(P.OPT_KEEP_TABLES, 1)
         assert pg.workspace_size() <= P.NOALLOC_WORKSPACE_BYTES
@@ -107,3 +110,18 @@ def test_noalloc_refuses_a_search_larger_than_the_array(P):
     # the handle stays usable through the ordinary entry point
     mc, _ = pg.find_best_strategy()
     assert mc == 146_670_616_576
+
+
+def test_noalloc_fused_minimum_and_hoisted_preps(P):
+    """A Transformer (one encoder, two decoder layers, p = 16) with a fused
+    minimum and, with every eligible prep hoisted, side-stream preps in the
+    allocating search -- which the allocation-free one builds in their own
+    slots: both agree on every table."""
+    from workloads import transformer
+    g = transformer(p=16, enc_layers=1, dec_layers=2)
+    say("noalloc vs allocating: fused minimum, hoisted preps")
+    (r0, t0, pg0), (r1, t1, _) = _both(P, g, 16, options=((P.OPT_HOIST_ELEMS, 1),))
+    assert any(pg0.vertex_info(v)["fused"] for v in range(pg0.nv))
+    assert any(pg0.vertex_info(v)["prep_after"] >= -1 for v in range(pg0.nv))
+    assert r1 == r0
+    assert t1 == t0
