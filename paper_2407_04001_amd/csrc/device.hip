@@ -258,9 +258,10 @@ __global__ __launch_bounds__(256) void k_fill_direct(const DirectArgs *__restric
                                                     const uint64_t *__restrict__ L, const uint8_t *__restrict__ lsum,
                                                     const uint64_t *__restrict__ sig, const Contrib *__restrict__ cb,
                                                     uint64_t r) {
+    __shared__ KeyT xch[4];   // per-wave minima of a group of several waves
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
     set_priority(be[kb]);
-    direct_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r);
+    direct_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r, xch);
 }
 
 // ------------------------------------------------------------------ back-substitution

@@ -174,7 +174,7 @@ struct GenericArgs {
 struct DirectArgs {
     uint32_t vi, K, bits, out_shift;
     uint32_t m;               // plan digits (= T_i layout), slowest first
-    uint32_t group_log2;      // lanes per entry = 2^group_log2 (c is strided over them)
+    uint32_t group_log2;      // lanes per entry = 2^group_log2 <= 256 (c is strided over them)
     uint32_t c_begin, c_end;  // contributions
     uint32_t rad[kMaxDep];
     uint32_t nblk, pad;       // nblk: workgroups of this vertex

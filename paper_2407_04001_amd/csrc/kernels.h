@@ -723,7 +723,7 @@ template <typename KeyT>
 __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, const DevVertex *__restrict__ V,
                                             const DevEdge *__restrict__ E, const uint64_t *__restrict__ L,
                                             const uint8_t *__restrict__ lsum, const uint64_t *__restrict__ sig,
-                                            const Contrib *__restrict__ cb, uint64_t r) {
+                                            const Contrib *__restrict__ cb, uint64_t r, KeyT (&xch)[4]) {
     using Ops = KeyOps<KeyT>;
     using Val = typename Ops::Val;
     const uint32_t G = 1u << a.group_log2;
@@ -802,7 +802,17 @@ __device__ __forceinline__ void direct_item(const DirectArgs &a, uint32_t lb, co
                 best = Ops::min(best, Ops::from_acc(contrib_key<KeyT>(cb, a.c_begin, a.c_end, me, c, dv, a.bits, V,
                                                                       E, L, lsum, sig, r)));
         }
-        for (uint32_t m = G >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
+        for (uint32_t m = (G < 64 ? G : 64) >> 1; m > 0; m >>= 1) best = Ops::min(best, shfl_xor_key(best, (int)m));
+        if (G > 64) {
+            // a group of 2 or 4 waves: their minima meet in LDS (every thread
+            // of the workgroup runs the same iterations, so the barriers match)
+            const uint32_t wave = threadIdx.x >> 6;
+            if ((threadIdx.x & 63) == 0) xch[wave] = best;
+            __syncthreads();
+            if (lane == 0)
+                for (uint32_t w = 1; w < G / 64; w++) best = Ops::min(best, xch[wave + w]);
+            __syncthreads();
+        }
         if (live && lane == 0) {
             Val v;
             uint32_t cc;

@@ -150,9 +150,10 @@ pase_status build_launches(pase_graph_t g, char *ws, std::vector<Launch<KeyT>> &
             da.out_shift = vp.out_shift;
             da.m = (uint32_t)vp.layout.size();
             for (size_t k = 0; k < vp.layout.size(); k++) da.rad[k] = g->K[vp.layout[k]];
-            // lanes per entry: enough threads to fill the GPU, at most one wave, at most K
+            // lanes per entry: enough threads to fill the GPU, at most a
+            // workgroup (four waves, combined in LDS), at most K
             da.group_log2 = 0;
-            while (da.group_log2 < 6 && (vp.N << da.group_log2) < 65536 && (2u << da.group_log2) <= vp.K)
+            while (da.group_log2 < 8 && (vp.N << da.group_log2) < 65536 && (2u << da.group_log2) <= vp.K)
                 da.group_log2++;
             da.N = vp.N;
             da.T = ws + P.off_T + vp.T_off;
