@@ -34,6 +34,8 @@
 
 using namespace pase;
 
+constexpr uint32_t kSidePrepBlocks = 256;   // grid of a hoisted prep: one workgroup per CU
+
 // Cost tables of the search: layer cost and device byte (device count or its
 // log2) of every (vertex, configuration), and the split signatures of every
 // (edge endpoint, configuration); r * t_x(e, cu, cv) is then read off two
@@ -219,10 +221,15 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restric
                                                      const uint64_t *__restrict__ L,
                                                      const uint8_t *__restrict__ lsum,
                                                      const uint64_t *__restrict__ sig,
-                                                     const Contrib *__restrict__ cb, uint64_t r) {
-    const uint32_t kb = batch_find(be, nbe, blockIdx.x);
-    set_priority(be[kb]);
-    prep_item<KeyT>(descs[be[kb].pos], blockIdx.x - be[kb].first, V, E, L, lsum, sig, cb, r);
+                                                     const Contrib *__restrict__ cb, uint64_t r, uint32_t nvb) {
+    // nvb work items (the batch's workgroups), grid-stride: a hoisted prep on
+    // the side stream runs on a small grid, so that it leaves most CUs to the
+    // launches beside it
+    for (uint32_t vb = blockIdx.x; vb < nvb; vb += gridDim.x) {
+        const uint32_t kb = batch_find(be, nbe, vb);
+        set_priority(be[kb]);
+        prep_item<KeyT>(descs[be[kb].pos], vb - be[kb].first, V, E, L, lsum, sig, cb, r);
+    }
 }
 
 template <typename KeyT, int TZ, int TM, int NA>
@@ -653,8 +660,9 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
                 hipEvent_t e0 = d->hoist_ev[2 * nside_done], e1 = d->hoist_ev[2 * nside_done + 1];
                 HIPCHK(hipEventRecord(e0, s));
                 HIPCHK(hipStreamWaitEvent(d->side, e0, 0));
-                hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, d->side, dp, e, b.nentries,
-                                   dV, dE, (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r);
+                hipLaunchKernelGGL((k_prep<KeyT>), dim3(std::min<uint32_t>(b.blocks, kSidePrepBlocks)), dim3(kPrepThreads),
+                                   0, d->side, dp, e, b.nentries, dV, dE, (const uint64_t *)dL, (const uint8_t *)dls,
+                                   (const uint64_t *)dsig, dC, g->r, b.blocks);
                 HIPCHK(hipEventRecord(e1, d->side));
                 side_of[bi] = nside_done++;
                 launches_n++;
@@ -692,7 +700,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         switch (b.kind) {
         case Batch::kPrep:
             hipLaunchKernelGGL((k_prep<KeyT>), dim3(b.blocks), dim3(kPrepThreads), 0, bs, dp, e, b.nentries, dV, dE,
-                               (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r);
+                               (const uint64_t *)dL, (const uint8_t *)dls, (const uint64_t *)dsig, dC, g->r, b.blocks);
             break;
         case Batch::kRows:
         case Batch::kGeneric:

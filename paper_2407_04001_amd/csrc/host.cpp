@@ -416,9 +416,11 @@ static void fuse_minima(pase_graph_t g, Plan &P) {
 // digits are read by the fill itself).  When the last of those tables is
 // filled two or more slots before the vertex's own, and the blocks are large
 // (PASE_OPT_HOIST_ELEMS, by default 2^20 elements: ~10 us or more of HBM
-// writes), the prep runs on a side
-// stream right after that slot -- beside the chains of small launches that
-// follow, which leave most of the GPU idle -- instead of in the vertex's slot.
+// writes), the prep runs on a side stream instead of in the vertex's slot,
+// started right after that slot, on a grid of one workgroup per CU: it then
+// takes several times longer but leaves most of the GPU to the launches of
+// the slots in between (a full-size prep grid beside them slows them down
+// more than it saves).
 static void hoist_preps(pase_graph_t g, Plan &P) {
     for (auto &vp : P.v) {
         if ((vp.kernel != kRows && vp.kernel != kGeneric) || vp.fused_from >= 0 || vp.fuse_into >= 0) continue;
@@ -588,12 +590,13 @@ static pase_status build_plan(pase_graph_t g) {
     std::vector<char> level_small((size_t)maxlev + 1, 1);
     for (int i = 0; i < n; i++)
         if (P.v[i].N * P.v[i].K > g->direct_cells) level_small[P.v[i].level] = 0;
-    // plan_one(i, ftz, ftm): kernel, tile and layout of position i; ftz/ftm
-    // (0 = free) force the row kernel's columns and rows per lane for this
-    // vertex and rule out the column-less form
+    // plan_one(i, ftz, ftm, no_split): kernel, tile and layout of position i;
+    // ftz/ftm (0 = free) force the row kernel's columns and rows per lane for
+    // this vertex and rule out the column-less form; no_split rules out a c
+    // split
     // 128-bit keys: every vertex on prep + the generic kernel
     const int kernel_mode = g->plan_wide ? 1 : g->kernel_mode;
-    auto plan_one = [&](int i, uint32_t ftz, uint32_t ftm) {
+    auto plan_one = [&](int i, uint32_t ftz, uint32_t ftm, bool no_split) {
         VPlan &vp = P.v[i];
         const uint32_t tile_cols = ftz ? ftz : g->tile_cols, tile_rows = ftm ? ftm : g->tile_rows;
         // small vertices: the direct fill (one launch, no prep blocks), whose
@@ -669,7 +672,7 @@ static pase_status build_plan(pase_graph_t g) {
                         // more than 32 accumulators per lane cost waves (VGPRs)
                         if (!tile_rows && !tile_cols && tz * tm > 32) continue;
                         const TileTime tt = tile_time_cached(rc.MO, rc.MR, Kz, vp.K, na, tz, tm, g->tile_parts,
-                                                             g->c_splits, stream_bytes);
+                                                             no_split ? 1u : g->c_splits, stream_bytes);
                         if (!rc.ok || tt.us < rc.cost) {
                             rc.ok = true;
                             rc.cost = tt.us;
@@ -716,12 +719,15 @@ static pase_status build_plan(pase_graph_t g) {
         for (int k = (int)vp.layout.size() - 2; k >= 0; k--)
             vp.stride[k] = vp.stride[k + 1] * g->K[vp.layout[k + 1]];
     };
-    for (int i = 0; i < n; i++) plan_one(i, 0, 0);
+    for (int i = 0; i < n; i++) plan_one(i, 0, 0, false);
     // One launch per level and kernel variant: a small column-form row vertex
     // of a level is re-planned with the tile shape of the level's largest one
     // when its fill then stays under half of that vertex's, so that the two
     // share a launch (the small one's workgroups come first and finish inside
     // the large one's) instead of adding a latency-bound launch of its own.
+    // When the largest one is not split over c, the small one is not either:
+    // its latency is hidden in the shared launch anyway, and a split would
+    // only add the level's reduction launch.
     // Level schedule only: the bulk lane splits a level over two streams.
     if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && kernel_mode == 0) {
         std::vector<int> dom((size_t)maxlev + 1, -1);
@@ -735,9 +741,10 @@ static pase_status build_plan(pase_graph_t g) {
             const int d = dom[P.v[i].level];
             if (d < 0 || d == i || P.v[i].kernel != kRows || P.v[i].z < 0) continue;
             const VPlan &dv = P.v[d];
-            if (P.v[i].TZ == dv.TZ && P.v[i].TM == dv.TM) continue;
+            const bool unsplit = dv.nsplit == 1 && !g->c_splits;
+            if (P.v[i].TZ == dv.TZ && P.v[i].TM == dv.TM && (!unsplit || P.v[i].nsplit == 1)) continue;
             const VPlan saved = P.v[i];
-            plan_one(i, dv.TZ, dv.TM);
+            plan_one(i, dv.TZ, dv.TM, unsplit);
             const VPlan &nv = P.v[i];
             const bool ok = nv.kernel == kRows && nv.z >= 0 && nv.TZ == dv.TZ && nv.TM == dv.TM &&
                             nv.na <= dv.na && nv.est_us <= 0.5 * dv.est_us;

@@ -615,7 +615,8 @@ def test_hoisted_prep_plan(pase):
     """PASE_OPT_HOIST_ELEMS: on the measured Transformer the one large prep
     whose blocks read only an early table (the fourth decoder layer's
     cross-attention key/value projection, level 43, reading level-1 tables)
-    is hoisted to run after slot 1; 0 hoists nothing; the sequential schedule
+    is hoisted to start after a slot in [1, 41] (the one before the longest
+    planned fill of that window); 0 hoists nothing; the sequential schedule
     never hoists; the launch plan checks either way."""
     P = pase
     g = workload("w4_transformer")
@@ -624,7 +625,7 @@ def test_hoisted_prep_plan(pase):
     h = {v: pg.vertex_info(v) for v in range(pg.nv) if pg.vertex_info(v)["prep_after"] >= -1}
     assert len(h) == 1
     (v, info), = h.items()
-    assert g["vertices"][v]["name"] == "dec4_xkv" and info["prep_after"] == 1 and info["level"] == 43
+    assert g["vertices"][v]["name"] == "dec4_xkv" and 1 <= info["prep_after"] <= 41 and info["level"] == 43
     assert pg.plan_check() > 0
     pg.set_option(P.OPT_HOIST_ELEMS, 0)
     assert all(pg.vertex_info(v)["prep_after"] == -2 for v in range(pg.nv))
