@@ -210,12 +210,13 @@ def report(trace_dir, fetch_dir, write_dir, cfetch_dir, cwrite_dir, valu_dir, wo
     return "\n".join(L) + "\n", rec
 
 
-KERNEL_SOURCES = ("device.hip", "kernels.h", "internal.h", "flow.hip")
+KERNEL_SOURCES = ("device.hip", "kernels.h", "internal.h", "launch_plan.cpp", "host.cpp")
 
 
 def kernel_source_digest(root: str) -> str:
-    """sha256 over the device-code sources, in a fixed order: a counter
-    record is valid for the kernels only while this digest matches."""
+    """sha256 over the device code and the host code that plans its launches,
+    in a fixed order: a counter record is valid for the kernels only while this
+    digest matches."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
         with open(os.path.join(root, "paper_2407_04001_amd", "csrc", name), "rb") as f:
