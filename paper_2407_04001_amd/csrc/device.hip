@@ -234,10 +234,18 @@ __global__ __launch_bounds__(kPrepThreads) void k_prep(const PrepArgs *__restric
 
 template <typename KeyT, int TZ, int TM, int NA>
 __global__ __launch_bounds__(256) void k_fill_rows(const RowsArgs *__restrict__ descs,
+                                                  const GenericArgs *__restrict__ gdescs,
                                                   const BatchEntry *__restrict__ be, uint32_t nbe) {
     __shared__ MergeBuf<KeyT> xch;
     const uint32_t kb = batch_find(be, nbe, blockIdx.x);
     set_priority(be[kb]);
+    // a small two-term generic fill of the same level rides along in this
+    // launch instead of a launch of its own (its workgroups use no LDS and no
+    // barrier, and need fewer registers than the row fill)
+    if (be[kb].kind == kEntryGeneric2) {
+        generic_item<KeyT, 2>(gdescs[be[kb].pos], blockIdx.x - be[kb].first);
+        return;
+    }
     rows_item<KeyT, TZ, TM, NA>(descs[be[kb].pos], blockIdx.x - be[kb].first, xch);
 }
 
@@ -460,42 +468,43 @@ static uint32_t grid_for(uint64_t n, uint32_t block = 256, uint32_t cap = 8192) 
 }
 
 template <typename KeyT, int TZ, int TM>
-static void launch_rows_tz(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s, hipEvent_t e0,
-                           hipEvent_t e1) {
+static void launch_rows_tz(const RowsArgs *descs, const GenericArgs *gdescs, const BatchEntry *be, const Batch &b,
+                           hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     dim3 grid(b.blocks), block(256);
     const uint32_t na = b.variant % 8;
     if constexpr (std::is_same<KeyT, double>::value) {
         switch (na) {
-        case 0: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 0>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
-        case 1: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
-        case 2: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 2>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
-        case 3: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 3>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
-        default: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 4>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries); break;
+        case 0: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 0>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be, b.nentries); break;
+        case 1: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 1>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be, b.nentries); break;
+        case 2: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 2>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be, b.nentries); break;
+        case 3: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 3>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be, b.nentries); break;
+        default: hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, 4>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be, b.nentries); break;
         }
     } else {
-        hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, -1>), grid, block, 0, s, e0, e1, 0, descs, be, b.nentries);
+        hipExtLaunchKernelGGL((k_fill_rows<KeyT, TZ, TM, -1>), grid, block, 0, s, e0, e1, 0, descs, gdescs, be,
+                              b.nentries);
     }
 }
 
 // variant = (TZ * 4 + TM) * 8 + NA
 template <typename KeyT>
-static bool launch_rows(const RowsArgs *descs, const BatchEntry *be, const Batch &b, hipStream_t s, hipEvent_t e0,
-                        hipEvent_t e1) {
+static bool launch_rows(const RowsArgs *descs, const GenericArgs *gdescs, const BatchEntry *be, const Batch &b,
+                        hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     switch (b.variant / 8) {
-    case 1 * 4 + 1: launch_rows_tz<KeyT, 1, 1>(descs, be, b, s, e0, e1); return true;
-    case 1 * 4 + 2: launch_rows_tz<KeyT, 1, 2>(descs, be, b, s, e0, e1); return true;
-    case 8 * 4 + 1: launch_rows_tz<KeyT, 8, 1>(descs, be, b, s, e0, e1); return true;
-    case 8 * 4 + 2: launch_rows_tz<KeyT, 8, 2>(descs, be, b, s, e0, e1); return true;
-    case 12 * 4 + 1: launch_rows_tz<KeyT, 12, 1>(descs, be, b, s, e0, e1); return true;
-    case 12 * 4 + 2: launch_rows_tz<KeyT, 12, 2>(descs, be, b, s, e0, e1); return true;
-    case 14 * 4 + 1: launch_rows_tz<KeyT, 14, 1>(descs, be, b, s, e0, e1); return true;
-    case 14 * 4 + 2: launch_rows_tz<KeyT, 14, 2>(descs, be, b, s, e0, e1); return true;
-    case 16 * 4 + 1: launch_rows_tz<KeyT, 16, 1>(descs, be, b, s, e0, e1); return true;
-    case 16 * 4 + 2: launch_rows_tz<KeyT, 16, 2>(descs, be, b, s, e0, e1); return true;
-    case 24 * 4 + 1: launch_rows_tz<KeyT, 24, 1>(descs, be, b, s, e0, e1); return true;
-    case 24 * 4 + 2: launch_rows_tz<KeyT, 24, 2>(descs, be, b, s, e0, e1); return true;
-    case 28 * 4 + 1: launch_rows_tz<KeyT, 28, 1>(descs, be, b, s, e0, e1); return true;
-    case 28 * 4 + 2: launch_rows_tz<KeyT, 28, 2>(descs, be, b, s, e0, e1); return true;
+    case 1 * 4 + 1: launch_rows_tz<KeyT, 1, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 1 * 4 + 2: launch_rows_tz<KeyT, 1, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 8 * 4 + 1: launch_rows_tz<KeyT, 8, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 8 * 4 + 2: launch_rows_tz<KeyT, 8, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 12 * 4 + 1: launch_rows_tz<KeyT, 12, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 12 * 4 + 2: launch_rows_tz<KeyT, 12, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 14 * 4 + 1: launch_rows_tz<KeyT, 14, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 14 * 4 + 2: launch_rows_tz<KeyT, 14, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 16 * 4 + 1: launch_rows_tz<KeyT, 16, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 16 * 4 + 2: launch_rows_tz<KeyT, 16, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 24 * 4 + 1: launch_rows_tz<KeyT, 24, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 24 * 4 + 2: launch_rows_tz<KeyT, 24, 2>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 28 * 4 + 1: launch_rows_tz<KeyT, 28, 1>(descs, gdescs, be, b, s, e0, e1); return true;
+    case 28 * 4 + 2: launch_rows_tz<KeyT, 28, 2>(descs, gdescs, be, b, s, e0, e1); return true;
     default: return false;
     }
 }
@@ -717,7 +726,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
             } else if constexpr (kWide) {
                 return fail(g, PASE_ERR_INTERNAL, "a 128-bit key plan holds a row or direct fill");
             } else if (b.kind == Batch::kRows) {
-                if (!launch_rows<KeyT>(dr, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
+                if (!launch_rows<KeyT>(dr, dg, e, b, bs, e0, e1)) return fail(g, PASE_ERR_INTERNAL, "no kernel for TZ");
             } else {
                 hipExtLaunchKernelGGL((k_fill_direct<KeyT>), dim3(b.blocks), dim3(256), 0, bs, e0, e1, 0, dx, e,
                                       b.nentries, dV, dE, (const uint64_t *)dL, (const uint8_t *)dls,

@@ -107,8 +107,9 @@ struct BatchEntry {
     uint32_t pos;
     uint32_t first;
     uint32_t prio;            // 1: the bulk lane schedule's small vertices -- their waves issue first
-    uint32_t pad;
+    uint32_t kind;            // row-kernel launches: 0 a row fill, 1 a two-term generic fill riding along
 };
+constexpr uint32_t kEntryGeneric2 = 1;
 
 struct ATerm {                // per-lane row term of the row kernel (key space)
     const void *ptr;

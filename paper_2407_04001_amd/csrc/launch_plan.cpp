@@ -526,7 +526,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
             hbe[nbe].pos = (uint32_t)i;
             hbe[nbe].first = b.blocks;
             hbe[nbe].prio = si.lanes && P.v[i].lane == 0 ? 1u : 0u;
-            hbe[nbe].pad = 0;
+            hbe[nbe].kind = 0;
             b.blocks += nblk(launches[i]);
             nbe++;
             b.nentries++;
@@ -614,11 +614,47 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         };
         std::stable_sort(rows.begin(), rows.end(), by_variant);
         std::stable_sort(gens.begin(), gens.end(), by_variant);
+        // two-term generic fills of the group ride along in its largest row
+        // launch (64-bit keys) instead of a generic launch of their own
+        std::vector<int> ride;
+        uint32_t ride_variant = ~0u;
+        if constexpr (sizeof(KeyT) == 8) {
+            uint64_t best = 0;
+            for (size_t k = 0; k < rows.size();) {
+                size_t k2 = k;
+                uint64_t blocks = 0;
+                for (; k2 < rows.size() && rows[k2].first == rows[k].first; k2++)
+                    blocks += launches[rows[k2].second].ra.nblocks_launched;
+                if (ride_variant == ~0u || blocks > best) { best = blocks; ride_variant = rows[k].first; }
+                k = k2;
+            }
+            if (ride_variant != ~0u) {
+                std::vector<std::pair<uint32_t, int>> keep;
+                for (const auto &x : gens) {
+                    if (launches[x.second].ga.nt == 2) ride.push_back(x.second);
+                    else keep.push_back(x);
+                }
+                gens.swap(keep);
+            }
+        }
         for (size_t k = 0; k < rows.size();) {
             grp.clear();
             size_t k2 = k;
             for (; k2 < rows.size() && rows[k2].first == rows[k].first; k2++) grp.push_back(rows[k2].second);
             add_batch(Batch::kRows, rows[k].first, grp, [](const Launch<KeyT> &L) { return L.ra.nblocks_launched; });
+            if (rows[k].first == ride_variant && !si.batches.empty()) {
+                Batch &b = si.batches.back();
+                for (int i : ride) {
+                    if (nbe >= be_cap) { be_overflow = true; break; }
+                    hbe[nbe].pos = (uint32_t)i;
+                    hbe[nbe].first = b.blocks;
+                    hbe[nbe].prio = si.lanes && P.v[i].lane == 0 ? 1u : 0u;
+                    hbe[nbe].kind = kEntryGeneric2;
+                    b.blocks += launches[i].ga.nblk;
+                    nbe++;
+                    b.nentries++;
+                }
+            }
             k = k2;
         }
         for (size_t k = 0; k < gens.size();) {
