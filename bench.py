@@ -134,13 +134,13 @@ def traffic_from_profile():
     return prof.get("bytes_per_launch")
 
 
-SCHEDULES = {0: "level", 1: "sequential", 4: "bulk lane"}
+SCHEDULES = {0: "level", 1: "sequential", 4: "bulk lane", 5: "split chains"}
 WORKLOADS = ["w0_fc_chain", "w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"]
 
 
 def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu, p=None, all_integers=False,
                  bf=False, volume=False, grad=False, schedule=None, no_roofline=False, halo=False, fused_min=None,
-                 hoist_elems=None):
+                 hoist_elems=None, bulk_us=None):
     """Time `steps` whole searches of one workload (at its own power-of-two p,
     or at `p` with every integer split when `all_integers`; over the
     breadth-first order, i.e. recurrence (2), when `bf`; with volume-intersection
@@ -151,8 +151,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
     on a prefix of about `cpu_single_cells` cells).  A search the
     library refuses as too large gives a line with value null and the reason."""
     import torch
-    from paper_2407_04001_amd import (OPT_FUSED_MIN, OPT_GRAD_SYNC, OPT_HALO, OPT_HOIST_ELEMS, OPT_ORDER, OPT_PROFILE,
-                                      OPT_SCHEDULE, OPT_TRANSFER, Graph, PaseError)
+    from paper_2407_04001_amd import (OPT_BULK_US, OPT_FUSED_MIN, OPT_GRAD_SYNC, OPT_HALO, OPT_HOIST_ELEMS, OPT_ORDER,
+                                      OPT_PROFILE, OPT_SCHEDULE, OPT_TRANSFER, Graph, PaseError)
     from workloads import workload
 
     g = workload(name, seed)
@@ -168,6 +168,8 @@ def run_workload(name, seed, steps, warmup, cpu_cells, cpu_single_cells, no_cpu,
         pg.set_option(OPT_FUSED_MIN, fused_min)
     if hoist_elems is not None:
         pg.set_option(OPT_HOIST_ELEMS, hoist_elems)
+    if bulk_us is not None:
+        pg.set_option(OPT_BULK_US, bulk_us)
     wl = g["name"] if p == g["p"] else f"{g['name']} at p={p}"
     if all_integers:
         wl += ", every integer split"
@@ -339,10 +341,12 @@ def main():
     ap.add_argument("--halo", action="store_true", help="add the halo exchange of convolutions to the layer costs")
     ap.add_argument("--no-roofline", action="store_true",
                     help="skip the profiled steps (no HIP events at all; for traces of the timed steps)")
-    ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 4),
+    ap.add_argument("--schedule", type=int, default=None, choices=(0, 1, 4, 5),
                     help="launch schedule (PASE_OPT_SCHEDULE; default: the library's)")
     ap.add_argument("--fused-min", type=int, default=None, choices=(0, 1),
                     help="fused minima (PASE_OPT_FUSED_MIN; default: the library's, on)")
+    ap.add_argument("--bulk-us", type=int, default=None,
+                    help="bulk lane threshold in planned microseconds (PASE_OPT_BULK_US; default: the library's)")
     ap.add_argument("--hoist-elems", type=int, default=None,
                     help="prep hoisting threshold (PASE_OPT_HOIST_ELEMS; 0 = off; default: the library's)")
     args = ap.parse_args()
@@ -363,7 +367,7 @@ def main():
                            args.no_cpu,
                            args.p or None, args.all_integers, args.order == "bf",
                            args.transfer == "volume", args.grad_sync, args.schedule, args.no_roofline, args.halo,
-                           args.fused_min, args.hoist_elems)
+                           args.fused_min, args.hoist_elems, args.bulk_us)
         print(json.dumps(out), flush=True)
 
 

@@ -118,18 +118,22 @@ typedef enum {
     PASE_OPT_PROFILE = 5,       /* 1: time every fill launch with HIP events (pase_stats);
                                    2: only the row kernel's launches with a column chunk per lane
                                    (the dominant kernel; fewer events, so less overhead) */
-    PASE_OPT_SCHEDULE = 6,      /* 0 (default): vertices of one dependency level (whose tables
-                                   do not read each other) share their kernel launches, one
-                                   stream, table memory packed by lifetimes.  1: one vertex at a
-                                   time in sequence order (same packing).  4: bulk lane -- every
-                                   row-kernel vertex whose planned fill takes at least
-                                   PASE_OPT_BULK_US runs, with every vertex reading its table, on
-                                   a stream of its own; all other vertices level by level on the
-                                   caller's stream at the highest wave priority; events only where
-                                   a table is read across the two; so a latency-bound chain never
-                                   waits for a large vertex it does not read (every table
-                                   resident; falls back to 0 over the memory budget).  Other
-                                   values: INVALID_ARGUMENT */
+    PASE_OPT_SCHEDULE = 6,      /* 5 (default): split chains -- the leaves (dependency level 0)
+                                   share their kernel launches on a stream of their own; after
+                                   them every row-kernel vertex whose planned fill takes at least
+                                   PASE_OPT_BULK_US, with every vertex reading its table, runs on
+                                   that stream level by level, and all other vertices level by
+                                   level on the caller's stream at the highest wave priority;
+                                   events only where a table is read across the two, so the chain
+                                   of small vertices and the chain of large fills never wait for
+                                   each other level by level.  0: vertices of one dependency level
+                                   (whose tables do not read each other) share their kernel
+                                   launches, one stream, table memory packed by lifetimes.  1: one
+                                   vertex at a time in sequence order (same packing).  4: bulk
+                                   lane -- as 5, without the batched leaves (the large fills and
+                                   their readers from level 0 on one stream).  4 and 5 keep every
+                                   table resident and fall back to 0 over the memory budget.
+                                   Other values: INVALID_ARGUMENT */
     PASE_OPT_TILE_COLS = 7,     /* row/column-chunk kernel: columns per lane, 0 = chosen per
                                    vertex (default), else 8, 12, 14, 16, 24 or 28 for every vertex
                                    that kernel runs (a tuning and test knob) */
@@ -182,7 +186,7 @@ typedef enum {
                                    qualify (so that it saves launches; any vertex under the
                                    sequential schedule).  Default 2^18; 0 = never.  Not used with
                                    PASE_OPT_KERNEL = 1 */
-    PASE_OPT_BULK_US = 17,      /* schedule 4: planned fill time (microseconds) from which a
+    PASE_OPT_BULK_US = 17,      /* schedules 4 and 5: planned fill time (microseconds) from which a
                                    row-kernel vertex runs on the bulk stream (default 100) */
     PASE_OPT_FUSED_MIN = 20,    /* 1 (default): a row-kernel vertex without a column digit whose one
                                    lookup is the whole table of its predecessor in the recurrence

@@ -7,4 +7,4 @@ from .pase import (EXPORTS, LIB_PATH, OPT_BULK_US, OPT_C_SPLITS, OPT_CONFIG_SET,
                    OPT_DIRECT_CELLS, OPT_FUSED_MIN, OPT_GRAD_SYNC, OPT_HALO, OPT_KEEP_TABLES, OPT_KERNEL,
                    OPT_HOIST_ELEMS, OPT_KEY_TYPE, OPT_MEMORY_BUDGET, OPT_ORDER, OPT_PROFILE, OPT_SCHEDULE, OPT_TILE_COLS,
                    OPT_TILE_PARTS, OPT_TILE_ROWS, OPT_TRANSFER, SCHEDULE_BULK, SCHEDULE_LEVEL,
-                   SCHEDULE_SEQUENTIAL, Graph, PaseError, load)
+                   SCHEDULE_SEQUENTIAL, SCHEDULE_SPLIT, Graph, PaseError, load)

@@ -399,8 +399,8 @@ struct DeviceState {
     hipEvent_t phase_ev[4] = {};       // profiling: search phases (cost tables | fill | back-substitution)
     hipStream_t last_stream = nullptr;
     char *last_ws = nullptr;           // workspace of the last search (its tables are read there)
-    hipStream_t side = nullptr;        // bulk lane schedule: the bulk stream; level layout: hoisted
-                                       // preps (default priority)
+    hipStream_t side = nullptr;        // lanes: lane 1's stream; level layout: hoisted preps
+                                       // (default priority, as every stream here)
     std::vector<hipEvent_t> lane_ev;   // bulk lane schedule: joins (no timing)
     std::vector<hipEvent_t> hoist_ev;  // hoisted preps: per side batch, its start and its end (no timing)
 };
@@ -627,12 +627,14 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
     // event is recorded already); the caller's stream joins the bulk stream at
     // the end
     const int nl = si.lanes ? kLanes : 1;
-    hipStream_t lane_stream[kLanes] = {s, s};
+    hipStream_t lane_stream[kLanes];
+    for (auto &ls : lane_stream) ls = s;
     // event of (lane l, slot L): lane_ev[1 + L * kLanes + l]; lane_ev[0]: start
     auto lev = [&](int l, int L) { return d->lane_ev[1 + (size_t)L * kLanes + l]; };
     int waited[kLanes][kLanes];
     for (auto &row : waited)
         for (int &w : row) w = -1;
+    std::vector<char> lane_ev_used;
     if (si.lanes) {
         if (!d->side) HIPCHK(hipStreamCreateWithFlags(&d->side, hipStreamNonBlocking));
         lane_stream[1] = d->side;
@@ -643,7 +645,18 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
             d->lane_ev.push_back(e);
         }
         HIPCHK(hipEventRecord(d->lane_ev[0], s));
-        HIPCHK(hipStreamWaitEvent(lane_stream[1], d->lane_ev[0], 0));
+        for (int l = 1; l < kLanes; l++)
+            if (lane_stream[l] != s) HIPCHK(hipStreamWaitEvent(lane_stream[l], d->lane_ev[0], 0));
+        // a group's event is recorded only when a group of the other lane
+        // waits on it: a record is a packet of its own in the lane's queue,
+        // which the next kernel of that lane waits behind
+        lane_ev_used.assign(nev, 0);
+        for (size_t gi = 0; gi < si.groups.size(); gi++) {
+            const int ln = si.group_lane[gi];
+            for (int i : si.groups[gi])
+                for (const auto &t : P.v[i].terms)
+                    if (P.v[t.j].lane != ln) lane_ev_used[1 + (size_t)P.v[t.j].slot * kLanes + P.v[t.j].lane] = 1;
+        }
     }
     // hoisted preps: a side batch starts after everything enqueued on s before
     // it (the fills of the tables it reads) and its vertex's group waits for it
@@ -688,10 +701,12 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         }
         if (si.lanes) {
             if (b.group != prev_group) {
-                if (prev_group >= 0)
+                if (prev_group >= 0 &&
+                    lane_ev_used[1 + (size_t)(prev_group / nl) * kLanes + si.group_lane[prev_group]])
                     HIPCHK(hipEventRecord(lev(si.group_lane[prev_group], prev_group / nl),
                                           lane_stream[si.group_lane[prev_group]]));
-                int need[kLanes] = {-1, -1};
+                int need[kLanes];
+                for (int &x : need) x = -1;
                 for (int i : si.groups[b.group])
                     for (const auto &t : P.v[i].terms)
                         if (P.v[t.j].lane != b.lane) need[P.v[t.j].lane] = std::max(need[P.v[t.j].lane], P.v[t.j].slot);
@@ -746,9 +761,12 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
         launches_n++;
     }
     if (si.lanes) {
-        // join: the caller's stream waits for the last work of the bulk stream
-        HIPCHK(hipEventRecord(lev(1, P.nslots), lane_stream[1]));
-        HIPCHK(hipStreamWaitEvent(s, lev(1, P.nslots), 0));
+        // join: the caller's stream waits for the last work of the other lanes
+        for (int l = 1; l < kLanes; l++)
+            if (lane_stream[l] != s) {
+                HIPCHK(hipEventRecord(lev(l, P.nslots), lane_stream[l]));
+                HIPCHK(hipStreamWaitEvent(s, lev(l, P.nslots), 0));
+            }
     }
     if (profile) HIPCHK(hipEventRecord(d->phase_ev[2], s));
     if ((uint32_t)n <= kMaxBacktrackThreads)
@@ -779,7 +797,7 @@ static pase_status run_search(pase_graph_t g, hipStream_t s, char *ws, char *img
 
     g->stats.launches = launches_n;
     g->stats.slots = (uint32_t)P.nslots;
-    g->stats.schedule = si.lanes ? (uint32_t)kSchedBulk : (P.by_level ? (uint32_t)kSchedLevel : (uint32_t)kSchedSeq);
+    g->stats.schedule = si.lanes ? (uint32_t)g->schedule : (P.by_level ? (uint32_t)kSchedLevel : (uint32_t)kSchedSeq);
     g->stats.fill_ms = g->stats.rows_fill_ms = g->stats.stream_fill_ms = 0;
     g->stats.cost_tables_ms = g->stats.fill_span_ms = g->stats.backtrack_ms = 0;
     g->stats.rows_launches = g->stats.stream_launches = 0;

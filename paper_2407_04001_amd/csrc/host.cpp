@@ -421,11 +421,16 @@ static void fuse_minima(pase_graph_t g, Plan &P) {
 // takes several times longer but leaves most of the GPU to the launches of
 // the slots in between (a full-size prep grid beside them slows them down
 // more than it saves).
-static void hoist_preps(pase_graph_t g, Plan &P) {
+static void hoist_preps(pase_graph_t g, Plan &P, bool lanes) {
     for (auto &vp : P.v) {
         if ((vp.kernel != kRows && vp.kernel != kGeneric) || vp.fused_from >= 0 || vp.fuse_into >= 0) continue;
         uint64_t elems = 0;
         int ready = -1;
+        int lane = -1;            // lane of the tables the blocks read (-2: more than one)
+        auto note = [&](int j) {
+            ready = std::max(ready, P.v[j].slot);
+            lane = lane == -1 || lane == P.v[j].lane ? P.v[j].lane : -2;
+        };
         if (vp.kernel == kRows) {
             elems = vp.MO * vp.K * vp.ldz;
             for (int u : vp.R) elems += (uint64_t)vp.K * g->K[u];
@@ -435,16 +440,26 @@ static void hoist_preps(pase_graph_t g, Plan &P) {
                 bool all = true;
                 for (int u : t.dig) all &= std::find(OZ.begin(), OZ.end(), u) != OZ.end();
                 const bool row1 = t.dig.size() == 1 && std::count(vp.R.begin(), vp.R.end(), t.dig[0]);
-                if (all || row1) ready = std::max(ready, P.v[t.j].slot);
+                if (all || row1) note(t.j);
             }
         } else {
             elems = vp.K;
             for (int u : vp.D) elems += (uint64_t)vp.K * g->K[u];
             for (const auto &t : vp.terms)
-                if (t.dig.size() <= 1) ready = std::max(ready, P.v[t.j].slot);
+                if (t.dig.size() <= 1) note(t.j);
+        }
+        // with lanes, the prep runs at the end of the group (slot `ready`, at
+        // least 0) of the lane whose tables it reads (the vertex's own when it
+        // reads none): stream order puts it after those fills, and the
+        // vertex's group waits for that lane up to that slot anyway -- or
+        // shares its stream -- so the prep precedes the fill
+        if (lanes) {
+            if (lane == -2) continue;
+            ready = std::max(ready, 0);
         }
         if (g->hoist_elems && elems >= g->hoist_elems && ready + 2 <= vp.slot) {
             vp.prep_after = ready;
+            vp.prep_lane = lanes && lane >= 0 ? lane : vp.lane;
             P.hoisted++;
         }
     }
@@ -464,6 +479,23 @@ static void assign_bulk_lanes(Plan &P, double bulk_us) {
         bool bulk = vp.kernel == kRows && vp.est_us >= bulk_us;
         for (const auto &t : vp.terms) bulk |= P.v[t.j].lane == 1;
         vp.lane = bulk ? 1 : 0;
+    }
+}
+
+// Split chains schedule.  The first kSplitBatchedLevels levels -- the leaves,
+// where the largest fills and most small vertices are -- run level by level
+// on lane 1, batched as in the level schedule.  After them, a row-kernel
+// vertex planned at bulk_us or more, and every vertex reading a table such a
+// vertex (or one of its readers) fills after the batched levels, runs on lane
+// 1 too; the remaining small vertices run on lane 0.  A lane-0 group waits
+// once for the batched levels whose tables it reads and then runs beside lane
+// 1, so a chain of small vertices and a chain of larger fills no longer wait
+// for each other level by level.
+static void assign_split_lanes(Plan &P, double bulk_us) {
+    for (auto &vp : P.v) {
+        bool one = vp.level < kSplitBatchedLevels || (vp.kernel == kRows && vp.est_us >= bulk_us);
+        for (const auto &t : vp.terms) one |= P.v[t.j].lane == 1 && P.v[t.j].level >= kSplitBatchedLevels;
+        vp.lane = one ? 1 : 0;
     }
 }
 
@@ -729,7 +761,8 @@ static pase_status build_plan(pase_graph_t g) {
     // its latency is hidden in the shared launch anyway, and a split would
     // only add the level's reduction launch.
     // Level schedule only: the bulk lane splits a level over two streams.
-    if (g->schedule == kSchedLevel && !g->tile_cols && !g->tile_rows && kernel_mode == 0) {
+    if ((g->schedule == kSchedLevel || g->schedule == kSchedSplit) && !g->tile_cols && !g->tile_rows &&
+        kernel_mode == 0) {
         std::vector<int> dom((size_t)maxlev + 1, -1);
         for (int i = 0; i < n; i++) {
             const VPlan &vp = P.v[i];
@@ -740,6 +773,8 @@ static pase_status build_plan(pase_graph_t g) {
         for (int i = 0; i < n; i++) {
             const int d = dom[P.v[i].level];
             if (d < 0 || d == i || P.v[i].kernel != kRows || P.v[i].z < 0) continue;
+            // (split chains: only the batched levels share launches level-wide)
+            if (g->schedule == kSchedSplit && P.v[i].level >= kSplitBatchedLevels) continue;
             const VPlan &dv = P.v[d];
             const bool unsplit = dv.nsplit == 1 && !g->c_splits;
             if (P.v[i].TZ == dv.TZ && P.v[i].TM == dv.TM && (!unsplit || P.v[i].nsplit == 1)) continue;
@@ -759,6 +794,7 @@ static pase_status build_plan(pase_graph_t g) {
     }
     for (auto &vp : P.v) vp.lane = 0;
     if (g->schedule == kSchedBulk) assign_bulk_lanes(P, (double)g->bulk_us);
+    if (g->schedule == kSchedSplit) assign_split_lanes(P, (double)g->bulk_us);
     if (g->fuse_min && kernel_mode == 0) fuse_minima(g, P);
     g->stats.plan_ms = ms_since(t1);
     return PASE_OK;
@@ -780,7 +816,7 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode);
 static pase_status layout_memory(pase_graph_t g) {
     const auto t0 = std::chrono::steady_clock::now();
     pase_status st = PASE_ERR_TOO_LARGE;
-    if (g->schedule == kSchedBulk) st = layout_memory_mode(g, kLayoutResident);
+    if (g->schedule == kSchedBulk || g->schedule == kSchedSplit) st = layout_memory_mode(g, kLayoutResident);
     if (st != PASE_OK && g->schedule != kSchedSeq) st = layout_memory_mode(g, kLayoutLevel);
     if (st != PASE_OK) st = layout_memory_mode(g, kLayoutSeq);
     g->stats.plan_ms += ms_since(t0);
@@ -803,7 +839,8 @@ static pase_status layout_memory_mode(pase_graph_t g, LayoutMode mode) {
         vp.prep_after = -2;
     }
     P.hoisted = 0;
-    if (mode == kLayoutLevel) hoist_preps(g, P);
+    if (mode == kLayoutLevel) hoist_preps(g, P, false);
+    if (resident && (g->schedule == kSchedBulk || g->schedule == kSchedSplit)) hoist_preps(g, P, true);
     const int n = (int)P.v.size();
     const uint64_t A = 256;
     uint64_t off = 0;
@@ -1172,8 +1209,8 @@ extern "C" pase_status pase_set_option(pase_graph_t g, pase_option opt, uint64_t
         g->profile = (int)value;
         break;
     case PASE_OPT_SCHEDULE:
-        if (value != kSchedLevel && value != kSchedSeq && value != kSchedBulk)
-            return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1 or 4");
+        if (value != kSchedLevel && value != kSchedSeq && value != kSchedBulk && value != kSchedSplit)
+            return fail(g, PASE_ERR_INVALID_ARGUMENT, "schedule 0, 1, 4 or 5");
         g->schedule = (int)value;
         break;
     case PASE_OPT_TILE_COLS:

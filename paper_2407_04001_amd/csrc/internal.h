@@ -210,7 +210,8 @@ struct SearchOut {            // written by the back-substitution kernel
 };
 
 // PASE_OPT_SCHEDULE values
-enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedBulk = 4 };
+enum SchedKind { kSchedLevel = 0, kSchedSeq = 1, kSchedBulk = 4, kSchedSplit = 5 };
+constexpr int kSplitBatchedLevels = 1;   // split chains: levels that stay batched on one lane
 
 // ------------------------------------------------------------------ host plan
 struct TermRef {
@@ -243,10 +244,12 @@ struct VPlan {
     int fuse_into = -1;             // position of that reader, -1 = none
     int fused_from = -1;            // the reader: position of the producer, -1 = none
     uint64_t fkeys_off = 0;         // the reader: bytes into the fused-key region
-    // hoisted prep (level schedule): the blocks read only tables filled by
-    // slot prep_after or earlier, so they are built on a side stream right
-    // after that slot, beside the slots in between; -2 = not hoisted
+    // hoisted prep: the blocks read only tables filled by slot prep_after or
+    // earlier, so they are built right after that slot, beside the slots in
+    // between -- on a side stream (level layout), or at the end of that
+    // slot's group of lane prep_lane (lanes); -2 = not hoisted
     int prep_after = -2;
+    int prep_lane = 0;
     double fill_ms = 0;             // last profiled fill time
     double est_us = 0;              // planned fill time (tile model), for the schedule
     // memory
@@ -300,7 +303,7 @@ struct pase_graph_s {
     uint64_t mem_budget = 64ull << 30;
     int kernel_mode = 0, key_mode = 0;
     uint32_t tile_cols = 0, tile_rows = 0, tile_parts = 0, c_splits = 0;   // 0 = chosen by the plan
-    int schedule = 0;               // pase_option PASE_OPT_SCHEDULE (SchedKind)
+    int schedule = pase::kSchedSplit;   // pase_option PASE_OPT_SCHEDULE (SchedKind)
     int order_mode = 0;             // pase_option PASE_OPT_ORDER: 0 GenerateSeq, 1 breadth-first
     // configurations
     bool enumerated = false;

@@ -38,14 +38,15 @@ struct Batch {
     bool side = false;     // a hoisted prep launch: on the side stream, after the work enqueued before it
 };
 
-constexpr int kLanes = 2;   // streams of the bulk lane schedule
+constexpr int kLanes = 2;   // streams of the bulk lane and split chains schedules
 
 struct SearchImage {
     std::vector<Batch> batches;            // in enqueue order
     std::vector<std::vector<int>> groups;  // positions of each launch group
     std::vector<int> group_lane;           // lane of each launch group
-    bool lanes = false;                    // the bulk lane schedule runs (two streams)
+    bool lanes = false;                    // a lane schedule runs (one stream per lane in use)
     bool hoist = false;                    // hoisted preps run on a side stream (level layout)
+    bool lane_hoist = false;               // hoisted preps run early on their vertex's lane (lanes)
     std::vector<std::vector<int>> group_waits;   // per launch group: the side batches it waits for
     bool upload_costs = true;              // the device cost tables' range is part of the upload
     uint32_t nlev = 0;                     // backward levels of the back-substitution

@@ -373,8 +373,9 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
     pase_status st = build_launches<KeyT>(g, ws, launches, contrib);
     if (st != PASE_OK) return st;
     si = SearchImage();
-    si.lanes = allow_streams && P.resident && g->schedule == kSchedBulk;
+    si.lanes = allow_streams && P.resident && (g->schedule == kSchedBulk || g->schedule == kSchedSplit);
     si.hoist = allow_streams && !si.lanes && P.hoisted > 0;
+    si.lane_hoist = si.lanes && P.hoisted > 0;
     // every piece of the image is checked against the end of its region first
     auto region = [&](uint64_t off, uint64_t bytes, uint64_t end, const char *what) {
         return off + bytes <= end && end <= P.off_cfg ? PASE_OK
@@ -546,6 +547,14 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
     if (si.hoist)
         for (int i = 0; i < n; i++)
             if (P.v[i].prep_after >= -1) hoist_after[(size_t)(P.v[i].prep_after + 1)].push_back(i);
+    // with lanes: a hoisted prep is a prep batch of its own at the end of the
+    // group (prep_after, lane of the tables it reads)
+    std::vector<std::vector<int>> lane_hoist_at(si.groups.size());   // group -> positions
+    if (si.lane_hoist)
+        for (int i = 0; i < n; i++)
+            if (P.v[i].prep_after >= 0)
+                lane_hoist_at[(size_t)P.v[i].prep_after * nl + P.v[i].prep_lane].push_back(i);
+    const bool hoisting = si.hoist || si.lane_hoist;
     auto add_side = [&](size_t k) {
         if (hoist_after[k].empty()) return;
         const int bi = (int)si.batches.size();
@@ -565,7 +574,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         std::vector<int> fills;   // members with a prep here or hoisted: rows / generic fills
         for (int i : mem) {
             if (launches[i].direct) direct.push_back(i);
-            else if (!launches[i].fused) (si.hoist && P.v[i].prep_after >= -1 ? fills : prepped).push_back(i);
+            else if (!launches[i].fused) (hoisting && P.v[i].prep_after >= -1 ? fills : prepped).push_back(i);
             if (P.v[i].fuse_into >= 0) prepped.push_back(P.v[i].fuse_into);
         }
         add_batch(Batch::kDirect, 0, direct, [](const Launch<KeyT> &L) { return L.da.nblk; });
@@ -669,6 +678,7 @@ pase_status build_image(pase_graph_t g, char *ws, char *img, SearchImage &si, bo
         grp.clear();
         for (auto &x : reds) grp.push_back(x.second);
         add_batch(Batch::kReduce, 0, grp, [](const Launch<KeyT> &L) { return L.red.nblk; });
+        add_batch(Batch::kPrep, 0, lane_hoist_at[sl], [](const Launch<KeyT> &L) { return L.prep.nwg; });
         if (be_overflow) return fail(g, PASE_ERR_INTERNAL, "batch table overflow");
         add_side(sl + 1);
     }
@@ -730,6 +740,24 @@ pase_status plan_check(pase_graph_t g, uint64_t *image_bytes) {
             for (size_t k = prep_batch[i] + 1; k < si.batches.size(); k++)
                 if (si.batches[k].group <= vp.prep_after && !si.batches[k].side)
                     return fail(g, PASE_ERR_INTERNAL, "a hoisted prep runs before the tables it reads");
+        }
+        // with lanes: at the end of group (prep_after, prep_lane), after the
+        // fills of that lane's tables up to that slot (the ones its blocks
+        // read among them); on another lane than the vertex's, the vertex
+        // reads a table of the prep's lane at that slot or later, so its group
+        // waits for that lane past the prep
+        if (si.lane_hoist && vp.prep_after >= 0) {
+            const Batch &b = si.batches[prep_batch[i]];
+            if (b.lane != vp.prep_lane || b.group != vp.prep_after * kLanes + vp.prep_lane)
+                return fail(g, PASE_ERR_INTERNAL, "a hoisted prep is not on its lane");
+            bool waited = vp.prep_lane == vp.lane;
+            for (const auto &t : vp.terms) {
+                const VPlan &pj = g->plan.v[t.j];
+                if (pj.slot <= vp.prep_after && pj.lane == vp.prep_lane && fill_batch[t.j] > prep_batch[i])
+                    return fail(g, PASE_ERR_INTERNAL, "a hoisted prep runs before the tables it reads");
+                waited |= pj.lane == vp.prep_lane && pj.slot >= vp.prep_after;
+            }
+            if (!waited) return fail(g, PASE_ERR_INTERNAL, "a hoisted prep on another lane is not waited for");
         }
     }
     // a fused minimum: its blocks are built before its producer's fill, and its

@@ -25,7 +25,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "NOT_CONNECTED", 3: "BAD_STAT
 OPT_HALO = 19
 OPT_FUSED_MIN = 20
 OPT_HOIST_ELEMS = 21
-SCHEDULE_LEVEL, SCHEDULE_SEQUENTIAL, SCHEDULE_BULK = 0, 1, 4
+SCHEDULE_LEVEL, SCHEDULE_SEQUENTIAL, SCHEDULE_BULK, SCHEDULE_SPLIT = 0, 1, 4, 5
 
 
 class VertexDesc(C.Structure):

@@ -392,6 +392,17 @@ def test_bulk_lane_schedule_against_golden(P, name):
     _check_golden(P, name, 0, keep=True, samples=False, schedule=4, bulk_us=0)
 
 
+@pytest.mark.parametrize("name", ["w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"])
+def test_split_chains_schedule_against_golden(P, name):
+    """Level 0 batched, then the small vertices' chain on one stream and the
+    large fills with their readers on another: the same answer as the level
+    schedule, with the default threshold and with every row-kernel vertex
+    large (then only the generic and direct fills form the chain)."""
+    _check_golden(P, name, 0, keep=False, schedule=5)
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=5)
+    _check_golden(P, name, 0, keep=True, samples=False, schedule=5, bulk_us=0)
+
+
 def test_bulk_lane_assignment(P):
     """The Transformer's large fills and every vertex reading their tables run
     on the bulk stream; no vertex of the other stream reads a bulk table."""
@@ -412,7 +423,7 @@ def test_workloads_run_the_requested_schedule(P):
     and the bulk lane puts the Transformer's large fills on the bulk stream."""
     for name in ("w1_residual_cnn", "w2_inception", "w3_lstm_grid", "w4_transformer"):
         g = workload(name)
-        for sched in (0, 1, 4):
+        for sched in (0, 1, 4, 5):
             pg, _, _ = _run(P, g, keep=False, schedule=sched)
             assert pg.stats()["schedule"] == sched, (name, sched)
     lanes = [pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))]
@@ -532,7 +543,7 @@ def test_all_integer_workloads_against_golden(P, name):
     if name == "w2_inception":
         _check_golden(P, name, 0, p=12, all_integers=True, kernel=1)
         _check_golden(P, name, 0, p=12, all_integers=True, key=1)
-        for sched in (1, 4):
+        for sched in (1, 4, 5):
             _check_golden(P, name, 0, p=12, all_integers=True, keep=False, schedule=sched)
 
 
@@ -592,7 +603,8 @@ def test_bf_order_kernels_and_schedules(P):
     and the sequential and bulk lane schedules: the same answer."""
     g = random_graph(560, n=9, p=16, max_dims=3, extra_edges=3, max_size=256)
     o = _oracle(g, bf=True)
-    for kw in ({}, {"kernel": 1}, {"key": 1}, {"schedule": 1}, {"schedule": 4, "bulk_us": 0}):
+    for kw in ({}, {"kernel": 1}, {"key": 1}, {"schedule": 1}, {"schedule": 4, "bulk_us": 0}, {"schedule": 5},
+               {"schedule": 5, "bulk_us": 0}):
         say(f"breadth-first seed=560 {kw}")
         pg, mc, strat = _run(P, g, bf=True, **kw)
         assert (mc, strat) == o.result()
@@ -678,7 +690,7 @@ def _fused_graph():
     return transformer(p=16, enc_layers=1, dec_layers=2)
 
 
-@pytest.mark.parametrize("schedule,key", [(0, 0), (1, 0), (4, 0), (0, 1)])
+@pytest.mark.parametrize("schedule,key", [(0, 0), (1, 0), (4, 0), (5, 0), (0, 1), (5, 1)])
 def test_fused_minimum_every_entry(P, schedule, key):
     """The fused producer/reader pair against the oracle entry by entry (every
     table, with tables kept so the producer also writes its own), under each
@@ -882,7 +894,7 @@ def test_direct_fill_schedules_and_orders(P):
     kernel mode does not use it."""
     g = random_graph(680, n=9, p=16, max_dims=3, extra_edges=4, max_size=256)
     o = _oracle(g)
-    for sched in (0, 1, 4):
+    for sched in (0, 1, 4, 5):
         say(f"direct fill seed=680 schedule={sched}")
         pg, mc, strat = _run(P, g, schedule=sched, direct=ALL_DIRECT)
         assert (mc, strat) == o.result()
@@ -972,9 +984,10 @@ def test_forced_wide_keys_against_golden(P, name):
 def test_random_graph_sweep_schedules(P, block):
     """Seeded sweep over random graphs (4-13 vertices, 2-5 loop dims, p from 4
     to 64, sizes up to 4096): the level schedule (shared level launches), the
-    bulk lane with every row vertex on the bulk stream, the sequential
-    schedule and the level schedule without the direct fill all give the
-    oracle's minimum, strategy and every table (fingerprints).  No graph is
+    bulk lane with every row vertex on the bulk stream, the split chains
+    schedule, the sequential schedule and the level schedule without the
+    direct fill all give the oracle's minimum, strategy and every table
+    (fingerprints).  No graph is
     refused: those whose packed keys pass 64 bits run on 128-bit keys."""
     checked = 0
     wide = 0
@@ -987,7 +1000,7 @@ def test_random_graph_sweep_schedules(P, block):
         say(f"random sweep seed={seed + 5000} n={n} p={p}")
         o = _oracle(g)
         fps = [o.fingerprint(i) for i in range(len(o.sequence()))]
-        for sched, bulk, direct in ((0, None, None), (4, 0, None), (1, None, 0), (0, None, 0)):
+        for sched, bulk, direct in ((0, None, None), (4, 0, None), (5, 0, None), (1, None, 0), (0, None, 0)):
             pg = P.Graph(g)
             pg.set_option(P.OPT_SCHEDULE, sched)
             if bulk is not None:
@@ -1002,5 +1015,5 @@ def test_random_graph_sweep_schedules(P, block):
                 assert pg.fingerprint(v) == fps[i], (seed, sched, v)
             checked += 1
             wide += pg.stats()["key_type"] == 2
-    assert checked == 80
+    assert checked == 100
     say(f"   {wide} runs on 128-bit keys")

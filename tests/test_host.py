@@ -372,8 +372,40 @@ def test_bulk_lane_plan(pase):
     pg.set_option(pase.OPT_BULK_US, 10 ** 9)
     assert {pg.vertex_info(v)["lane"] for v in range(len(g["vertices"]))} == {0}
     assert _status(lambda: pg.set_option(pase.OPT_BULK_US, 10 ** 9 + 1)) == pase.INVALID_ARGUMENT
-    for bad in (2, 3, 5):
+    for bad in (2, 3, 6):
         assert _status(lambda: pg.set_option(pase.OPT_SCHEDULE, bad)) == pase.INVALID_ARGUMENT
+
+
+def test_split_chains_plan(pase):
+    """Schedule 5 (the default) on the Transformer graph: level 0 is batched
+    on lane 1; after it the large fills (>= 8e9 cells) and their readers run
+    on lane 1, the encoder's chain of small vertices on lane 0; level 0's
+    small row vertices share the tile shape of its largest fill; a hoisted
+    prep (the cross-attention block that reads only a level-1 table) is built
+    right after that level on the lane of the table it reads; a threshold
+    above every planned time leaves only level 0 on lane 1."""
+    g = transformer()
+    pg = pase.Graph(g)
+    pg.enumerate_configs(g["p"])
+    assert pg.plan_check() > 0
+    info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
+    lanes = [x["lane"] for x in info]
+    assert set(lanes) == {0, 1}
+    for x in info:
+        if x["level"] == 0 or (x["kernel"] == 1 and x["cells"] >= 8e9):
+            assert x["lane"] == 1
+    seq = pg.sequence()
+    chain = [v for v in seq[:50] if info[v]["level"] >= 1]
+    assert len(chain) >= 30 and all(lanes[v] == 0 for v in chain)
+    rows0 = [x for x in info if x["level"] == 0 and x["kernel"] == 1 and x["column"] >= 0]
+    big = max(rows0, key=lambda x: x["cells"])
+    assert {(x["tile_cols"], x["tile_rows"]) for x in rows0} == {(big["tile_cols"], big["tile_rows"])}
+    hoisted = [x for x in info if x["prep_after"] >= -1]
+    assert len(hoisted) == 1 and hoisted[0]["prep_after"] == 1 and hoisted[0]["level"] > 10
+    pg.set_option(pase.OPT_BULK_US, 10 ** 9)
+    assert pg.plan_check() > 0
+    assert {v for v in range(len(g["vertices"])) if pg.vertex_info(v)["lane"] == 1} == \
+        {v for v in range(len(g["vertices"])) if pg.vertex_info(v)["level"] == 0}
 
 
 def test_level_launch_unification(pase):
@@ -456,7 +488,7 @@ def test_plan_check_workloads(pase, name):
     g = workload(name)
     pg = pase.Graph(g)
     pg.enumerate_configs(g["p"])
-    for sched in (0, 1, 4):
+    for sched in (0, 1, 4, 5):
         for key in (0, 1, 2):
             for direct, keep in ((None, 0), (0, 1)):
                 if name == "w4_transformer" and (key == 2 or direct == 0):
@@ -482,7 +514,7 @@ def test_plan_check_random_graphs(pase, seed):
                          extra_edges=int(rng.integers(0, 6)), max_size=int(rng.choice([8, 64, 512, 4096])))
         pg = pase.Graph(g)
         pg.enumerate_configs(p)
-        for sched in (0, 1, 4):
+        for sched in (0, 1, 4, 5):
             pg.set_option(pase.OPT_SCHEDULE, sched)
             for key in (0, 2):
                 pg.set_option(pase.OPT_KEY_TYPE, key)
@@ -599,7 +631,7 @@ def test_fused_minimum_plan(pase):
     a, b = info[prod[0]], info[read[0]]
     assert b["position"] == a["position"] + 1 and a["column"] == read[0] and b["column"] == -1
     assert a["splits"] == 1 and b["splits"] == 1 and a["outer"] == 1 and a["rows"] == b["rows"]
-    for sched in (0, 1, 4):
+    for sched in (0, 1, 4, 5):
         for keep in (0, 1):
             pg.set_option(P.OPT_SCHEDULE, sched)
             pg.set_option(P.OPT_KEEP_TABLES, keep)
