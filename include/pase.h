@@ -339,7 +339,7 @@ pase_status pase_find_best_strategy(pase_graph_t g, void *stream, uint64_t *min_
  * arguments, results and errors as pase_find_best_strategy, plus TOO_LARGE
  * when pase_workspace_size() exceeds PASE_NOALLOC_WORKSPACE_BYTES (checked on
  * the host before any device work).  Profiling (PASE_OPT_PROFILE) is ignored
- * and a bulk lane plan (PASE_OPT_SCHEDULE 4) runs level by level on `stream`.
+ * and a two-stream plan (PASE_OPT_SCHEDULE 4 or 5) runs level by level on `stream`.
  * The array keeps the last call's contents and every call on one GPU shares
  * it: calls in one process are serialized by a lock, calls from different
  * processes that overlap on one GPU race, and the next allocation-free search
