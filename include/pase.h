@@ -395,10 +395,12 @@ typedef struct {
     uint32_t key_type;    /* key type of the plan (the same for every vertex): 0 fp64, 1 uint64, 2 128-bit */
     uint32_t fused;       /* PASE_OPT_FUSED_MIN: 1 = its fill also forms the minimum of its table's reader,
                              2 = that reader (its fill is then a one-split reduction of those keys), 0 = neither */
-    int32_t prep_after;   /* level layout: its prep blocks read only tables of slots up to this one (-1:
-                             none) and are built on a side stream right after it, beside the launches of
-                             the slots in between; -2 = built in its own slot */
-    uint32_t pad;
+    int32_t prep_after;   /* its prep blocks read only tables of slots up to this one (-1: none) and are
+                             built right after it, beside the launches of the slots in between -- on a
+                             side stream (level layout) or at the end of that slot's launches on lane
+                             prep_lane (schedules 4 and 5); -2 = built in its own slot */
+    uint32_t prep_lane;   /* schedules 4 and 5, prep_after >= 0: the lane its prep runs on (that of the
+                             tables it reads) */
 } pase_vertex_info;
 
 pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_vertex_info *out);

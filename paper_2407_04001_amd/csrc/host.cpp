@@ -1456,6 +1456,7 @@ extern "C" pase_status pase_vertex_info_get(pase_graph_t g, uint32_t v, pase_ver
     x.key_type = g->plan_key_type;
     x.fused = vp.fuse_into >= 0 ? 1u : vp.fused_from >= 0 ? 2u : 0u;
     x.prep_after = vp.prep_after;
+    x.prep_lane = (uint32_t)vp.prep_lane;
     *out = x;
     return PASE_OK;
 }

@@ -67,7 +67,7 @@ class VertexInfo(C.Structure):
                 ("row_terms", C.c_uint32), ("lookups", C.c_uint32), ("parts", C.c_uint32),
                 ("fill_ms", C.c_double), ("level", C.c_uint32), ("lane", C.c_uint32),
                 ("key_bound", C.c_uint64), ("table_bound", C.c_uint64), ("key_type", C.c_uint32),
-                ("fused", C.c_uint32), ("prep_after", C.c_int32), ("pad", C.c_uint32)]
+                ("fused", C.c_uint32), ("prep_after", C.c_int32), ("prep_lane", C.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

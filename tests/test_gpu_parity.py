@@ -403,6 +403,30 @@ def test_split_chains_schedule_against_golden(P, name):
     _check_golden(P, name, 0, keep=True, samples=False, schedule=5, bulk_us=0)
 
 
+@pytest.mark.parametrize("case", [(2021, 14, 32, 3, 5, 512, 5, 0), (2021, 14, 32, 3, 5, 512, 4, 0),
+                                  (2060, 9, 32, 4, 4, 64, 5, 10)])
+def test_hoisted_prep_on_the_other_lane(P, case):
+    """A hoisted prep that runs on the lane of the tables it reads, not on its
+    vertex's (each direction over the cases): the minimum, the strategy and
+    every table entry match the oracle."""
+    seed, n, p, dims, extra, size, sched, bulk = case
+    g = random_graph(seed, n=n, p=p, max_dims=dims, extra_edges=extra, max_size=size)
+    say(f"cross-lane hoisted prep seed={seed} schedule={sched} bulk_us={bulk}")
+    o = _oracle(g)
+    pg = P.Graph(g)
+    pg.set_option(P.OPT_SCHEDULE, sched)
+    pg.set_option(P.OPT_BULK_US, bulk)
+    pg.set_option(P.OPT_HOIST_ELEMS, 1)
+    pg.set_option(P.OPT_KEEP_TABLES, 1)
+    pg.enumerate_configs(p)
+    info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
+    assert any(x["prep_after"] >= 0 and x["prep_lane"] != x["lane"] for x in info)
+    mc, strat = pg.find_best_strategy()
+    assert pg.stats()["schedule"] == sched
+    assert (mc, strat) == o.result()
+    _compare_all_entries(pg, o, g, max_entries=2048)
+
+
 def test_bulk_lane_assignment(P):
     """The Transformer's large fills and every vertex reading their tables run
     on the bulk stream; no vertex of the other stream reads a bulk table."""

@@ -408,6 +408,40 @@ def test_split_chains_plan(pase):
         {v for v in range(len(g["vertices"])) if pg.vertex_info(v)["level"] == 0}
 
 
+# random graphs whose lane plans hoist a prep onto the other lane than its
+# vertex's: (seed, n, p, max_dims, extra_edges, max_size, schedule, bulk_us)
+CROSS_LANE_PREPS = [(2021, 14, 32, 3, 5, 512, 5, 0), (2021, 14, 32, 3, 5, 512, 4, 0),
+                    (2060, 9, 32, 4, 4, 64, 5, 10)]
+
+
+def cross_lane_graph(pase, case):
+    seed, n, p, dims, extra, size, sched, bulk = case
+    g = random_graph(seed, n=n, p=p, max_dims=dims, extra_edges=extra, max_size=size)
+    pg = pase.Graph(g)
+    pg.set_option(pase.OPT_SCHEDULE, sched)
+    pg.set_option(pase.OPT_BULK_US, bulk)
+    pg.set_option(pase.OPT_HOIST_ELEMS, 1)
+    pg.enumerate_configs(p)
+    return g, pg
+
+
+@pytest.mark.parametrize("case", CROSS_LANE_PREPS)
+def test_hoisted_prep_on_the_other_lane_plan(pase, case):
+    """With lanes, a hoisted prep runs on the lane of the tables its blocks
+    read, after their slot: these plans hold such a prep on the other lane than
+    its vertex's (both directions over the cases), and the launch plan check
+    accepts them (the prep after those fills, the vertex's group waiting for
+    that lane at that slot or later)."""
+    g, pg = cross_lane_graph(pase, case)
+    info = [pg.vertex_info(v) for v in range(len(g["vertices"]))]
+    other = [x for x in info if x["prep_after"] >= 0 and x["prep_lane"] != x["lane"]]
+    assert other
+    for x in other:
+        assert x["prep_after"] + 2 <= x["level"]
+    assert pg.plan_check() > 0
+    pg.close()
+
+
 def test_level_launch_unification(pase):
     """Level schedule: a level's small column-form row vertices take the tile
     shape of its largest one (so they share its launch) when their fill stays
